@@ -1,0 +1,228 @@
+"""Rollout-ResQ linear layer (oracle; test infrastructure only).
+
+Follows paper Sec. 3 (Eq. 1), Sec. 4.3 (Eq. 2, Eq. 3, Eq. 4 and the sparsity functions S),
+the FP4 training policy of Sec. 1 / Sec. 4.1 (forward and backward at 4 bits) and the cost
+model of Sec. 5.4.  Notation: X is m x d (tokens x input features), W is n x d, Y = X W^T.
+
+Readings of points the paper leaves open (also listed in the design notes):
+
+  R1  the residual Delta X = X - Q(X) is formed in float32 (exact for bf16 inputs whose
+      quantized value is within range).
+  R2  S acts on the quantized residual Q(Delta X) and the residual GEMM multiplies by Q(W)
+      (Eq. 4), not by W.
+  S1  S_50% is the paper's structured channel-wise sparsity; an element-wise (unstructured)
+      50% variant is provided as well.
+  S2  a channel is a column of the m x d activation (an input feature); its L2 norm runs over
+      all m rows of the call (the residual is taken at tensor level, Sec. 4.3).
+  S3  a 32 x 64 block covers 32 rows (tokens) by 64 columns (features); a last row-block with
+      fewer than 32 rows is a smaller block.
+  S4  ranking uses the sum of squares (same order as the L2 norm); ties go to the lowest
+      index; floor(count / 2) items are kept.
+  S5  sums of squares are float64 in a fixed order (stated at each function), so near-ties
+      are decided the same way on every implementation that keeps that order.
+  T1  backward: dY, W and X are quantized along the contraction axis of each backward GEMM
+      (dX = Q_n(dY) Q_n(W), dW = Q_m(dY)^T Q_m(X)), no residual (ResQ is rollout-only).
+  Y1  Y, dX and dW are float32: the exact float64 result rounded once.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import formats as F
+
+SPARSITY = ("none", "identity", "2:4", "channel50", "block32x64_50", "unstructured50")
+
+
+# ----------------------------------------------------------------------------------------
+# Eq. 2: the activation residual
+# ----------------------------------------------------------------------------------------
+def residual(x: np.ndarray, xhat: np.ndarray) -> np.ndarray:
+    """Delta X = X - Q(X) in float32 (Eq. 2, reading R1)."""
+    return np.asarray(x, np.float32) - np.asarray(xhat).astype(np.float32)
+
+
+# ----------------------------------------------------------------------------------------
+# Sec. 4.3: sparsity functions applied to Q(Delta X)
+# ----------------------------------------------------------------------------------------
+def keep_2_4(rhat: np.ndarray) -> np.ndarray:
+    """S_{2:4}: in every group of 4 consecutive elements along d, keep the 2 largest |value|.
+
+    An element's rank in its group is the number of elements that beat it: larger magnitude,
+    or equal magnitude and a lower index.  Ranks 0 and 1 are kept.
+    """
+    m, d = rhat.shape
+    a = np.abs(rhat).reshape(m, d // 4, 4)
+    rank = np.zeros(a.shape, dtype=np.int64)
+    for i in range(4):
+        for j in range(4):
+            if j == i:
+                continue
+            beats = (a[..., j] > a[..., i]) | ((a[..., j] == a[..., i]) & (j < i))
+            rank[..., i] += beats
+    return (rank < 2).reshape(m, d)
+
+
+def channel_keys(rhat: np.ndarray) -> np.ndarray:
+    """Sum of squares of every column, accumulated in float64 over rows i = 0, 1, ..., m-1."""
+    acc = np.zeros(rhat.shape[1], dtype=np.float64)
+    for i in range(rhat.shape[0]):
+        acc = acc + rhat[i].astype(np.float64) ** 2
+    return acc
+
+
+def _top_half(keys: np.ndarray) -> np.ndarray:
+    """Boolean mask of the floor(len/2) largest keys; ties go to the lower index."""
+    idx = np.arange(keys.size)
+    order = np.lexsort((idx, -keys))  # primary: key descending, secondary: index ascending
+    keep = np.zeros(keys.size, dtype=bool)
+    keep[order[: keys.size // 2]] = True
+    return keep
+
+
+def keep_channel50(rhat: np.ndarray):
+    """S_50% (structured, channel-wise): keep the top half of the d channels by L2 norm."""
+    ch = _top_half(channel_keys(rhat))
+    return np.broadcast_to(ch[None, :], rhat.shape).copy(), ch
+
+
+def block_keys(rhat: np.ndarray, fmt: str) -> np.ndarray:
+    """Sum of squares of every 32 x 64 block, shape (ceil(m/32), d/64).
+
+    Order: rows of the block in increasing order; within a row, the block's format scale
+    blocks in increasing column order (one for HiF4, two 32-wide halves for MXFP4), each
+    added as its own sum.  All elements of one scale block share one power-of-two factor and
+    have at most 6 significant bits, so that inner sum is exact in any order.
+    """
+    m, d = rhat.shape
+    sb = F.block_size(fmt)
+    sq = rhat.astype(np.float64) ** 2
+    inner = sq.reshape(m, d // sb, sb).sum(axis=-1)  # exact per scale block
+    per64 = inner.reshape(m, d // 64, 64 // sb)
+    nI = (m + 31) // 32
+    keys = np.zeros((nI, d // 64), dtype=np.float64)
+    for bi in range(nI):
+        acc = np.zeros(d // 64, dtype=np.float64)
+        for i in range(32 * bi, min(m, 32 * bi + 32)):
+            for q in range(64 // sb):
+                acc = acc + per64[i, :, q]
+        keys[bi] = acc
+    return keys
+
+
+def keep_block50(rhat: np.ndarray, fmt: str):
+    """S^{32x64}_50%: keep the top half of the 32 x 64 blocks by L2 norm (row-major index)."""
+    keys = block_keys(rhat, fmt)
+    blk = _top_half(keys.ravel()).reshape(keys.shape)
+    elem = np.repeat(np.repeat(blk, 32, axis=0)[: rhat.shape[0]], 64, axis=1)
+    return elem, blk
+
+
+def keep_unstructured50(rhat: np.ndarray) -> np.ndarray:
+    """Element-wise 50%: keep the floor(m*d/2) largest |value| of the tensor (row-major index)."""
+    return _top_half(np.abs(rhat).ravel()).reshape(rhat.shape)
+
+
+def sparsify(kind: str, fmt: str, rcodes: np.ndarray, rhat: np.ndarray):
+    """Apply S to Q(Delta X).
+
+    Returns ``(codes, keep, groups)``: the residual codes with pruned elements set to the +0
+    code, the element keep mask, and the kept channels (d,) or blocks (ceil(m/32), d/64) for
+    the channel and block kinds (None otherwise).
+    """
+    groups = None
+    if kind == "identity":
+        keep = np.ones(rhat.shape, dtype=bool)
+    elif kind == "2:4":
+        keep = keep_2_4(rhat)
+    elif kind == "channel50":
+        keep, groups = keep_channel50(rhat)
+    elif kind == "block32x64_50":
+        keep, groups = keep_block50(rhat, fmt)
+    elif kind == "unstructured50":
+        keep = keep_unstructured50(rhat)
+    else:
+        raise ValueError(kind)
+    return np.where(keep, rcodes, 0).astype(np.uint8), keep, groups
+
+
+def pack_bits(mask: np.ndarray) -> np.ndarray:
+    """Bit b of byte i along the last axis is element 8i + b."""
+    return np.packbits(np.asarray(mask, dtype=bool), axis=-1, bitorder="little")
+
+
+# ----------------------------------------------------------------------------------------
+# forward: Eq. 1 (S = none), Eq. 3 (S = identity), Eq. 4 (S = one of the sparsifiers)
+# ----------------------------------------------------------------------------------------
+def resq_quantize_residual(fmt: str, sparsity: str, x: np.ndarray) -> dict:
+    """Q(X), Delta X, Q(Delta X) and S(Q(Delta X)) for activations x (m x d, float32)."""
+    qx_codes, qx_scales = F.quantize(fmt, x)
+    xhat = F.dequantize(fmt, qx_codes, qx_scales)
+    out = {"qx_codes": qx_codes, "qx_scales": qx_scales, "xhat": xhat}
+    if sparsity == "none":
+        return out
+    r = residual(x, xhat)
+    qr_codes, qr_scales = F.quantize(fmt, r)
+    rhat = F.dequantize(fmt, qr_codes, qr_scales)
+    sr_codes, keep, groups = sparsify(sparsity, fmt, qr_codes, rhat)
+    out.update(r=r, qr_codes_dense=qr_codes, qr_scales=qr_scales, qr_codes=sr_codes,
+               keep=keep, groups=groups, srhat=np.where(keep, rhat, 0.0))
+    return out
+
+
+def resq_forward(fmt: str, sparsity: str, x: np.ndarray, w: np.ndarray) -> dict:
+    """Y = Q(X) Q(W)^T + S(Q(Delta X)) Q(W)^T, float64 products rounded to float32 once."""
+    out = resq_quantize_residual(fmt, sparsity, x)
+    qw_codes, qw_scales = F.quantize(fmt, w)
+    what = F.dequantize(fmt, qw_codes, qw_scales)
+    y = out["xhat"] @ what.T
+    if sparsity != "none":
+        y = y + out["srhat"] @ what.T
+    out.update(qw_codes=qw_codes, qw_scales=qw_scales, what=what, y=y.astype(np.float32),
+               y64=y)
+    return out
+
+
+# ----------------------------------------------------------------------------------------
+# FP4 training-policy backward (reading T1)
+# ----------------------------------------------------------------------------------------
+def resq_backward(fmt: str, dy: np.ndarray, x: np.ndarray, w: np.ndarray) -> dict:
+    """dX = Q_n(dY) Q_n(W) and dW = Q_m(dY)^T Q_m(X), each quantized along its contraction.
+
+    dy is m x n, x is m x d, w is n x d.  Q_a(T) means T quantized in blocks along axis a.
+    """
+    dyn = F.dequantize(fmt, *F.quantize(fmt, dy))            # blocks along n
+    wn_t = F.dequantize(fmt, *F.quantize(fmt, w.T))          # d x n, blocks along n
+    dym_t = F.dequantize(fmt, *F.quantize(fmt, dy.T))        # n x m, blocks along m
+    xm_t = F.dequantize(fmt, *F.quantize(fmt, x.T))          # d x m, blocks along m
+    dx = dyn @ wn_t.T
+    dw = dym_t @ xm_t.T
+    return {"dx": dx.astype(np.float32), "dw": dw.astype(np.float32), "dx64": dx, "dw64": dw}
+
+
+# ----------------------------------------------------------------------------------------
+# Sec. 5.4: overhead cost model (FLOPs)
+# ----------------------------------------------------------------------------------------
+def flops_dense(m: int, d: int, n: int) -> int:
+    """A dense GEMM Y = X W^T costs 2mdn FLOPs."""
+    return 2 * m * d * n
+
+
+def flops_resq(m: int, d: int, n: int, sparsity: str) -> int:
+    """Algorithmic FLOPs of a ResQ linear: the FP4 main GEMM plus the kept residual part.
+
+    S_2:4, S_50% (channel or element-wise) and the 50% block pattern keep half of the residual
+    (mdn); the identity keeps all of it (2mdn); no residual adds nothing.
+    """
+    main = flops_dense(m, d, n)
+    extra = {"none": 0, "identity": 2 * m * d * n}.get(sparsity, m * d * n)
+    return main + extra
+
+
+def effective_cost(m: int, d: int, n: int, sparsity: str, fp4_speedup: float = 4.0) -> float:
+    """Sec. 5.4 cost in FP16-equivalent FLOPs, FP4 GEMMs taken as fp4_speedup times cheaper."""
+    return flops_resq(m, d, n, sparsity) / fp4_speedup
+
+
+def speedup_vs_fp16(sparsity: str, fp4_speedup: float = 4.0) -> float:
+    m = d = n = 1
+    return flops_dense(m, d, n) / effective_cost(m, d, n, sparsity, fp4_speedup)

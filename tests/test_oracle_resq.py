@@ -1,0 +1,277 @@
+"""Pins for the oracle's residual, sparsity functions, GEMMs and cost model (CPU only)."""
+import math
+import os
+
+import numpy as np
+import pytest
+
+from oracle import formats as F
+from oracle import resq as Q
+from synth import activations, bf16_bits_to_f32, f32_to_bf16_bits, rng_tree, weights
+import _intref as R
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _bf16(a):
+    return bf16_bits_to_f32(f32_to_bf16_bits(np.asarray(a, np.float32)))
+
+
+def _outlier_x(m, d, seed=0, frac=0.01, scale=50.0):
+    return bf16_bits_to_f32(activations(rng_tree(seed, 1)[0], m, d, frac, scale))
+
+
+# ----------------------------------------------------------------------------------------
+# Eq. 2: residual
+# ----------------------------------------------------------------------------------------
+@pytest.mark.parametrize("fmt", F.FORMATS)
+def test_residual_is_exact(fmt):
+    """Q(X) + Delta X == X bit-exactly in float32, for outlier data and extreme values."""
+    x = _outlier_x(64, 512)
+    x[0, :64] = bf16_bits_to_f32(np.arange(1, 65, dtype=np.uint16))  # bf16 subnormals
+    x[1, :64] = np.float32(3.0e9)  # large, inside the HiF4 scale range
+    x[2, :] = 0.0
+    x[3, ::2] = -0.0
+    codes, sc = F.quantize(fmt, x)
+    xh = F.dequantize(fmt, codes, sc)
+    r = Q.residual(x, xh)
+    assert r.dtype == np.float32
+    assert np.array_equal(xh.astype(np.float32) + r, x)
+    assert np.array_equal(xh + r.astype(np.float64), x.astype(np.float64))
+
+
+@pytest.mark.parametrize("fmt", F.FORMATS)
+def test_representable_x_has_zero_residual(fmt):
+    rng = np.random.default_rng(4)
+    codes = rng.integers(0, 16, (8, 128)).astype(np.uint8)
+    if fmt == "mxfp4":
+        sc = rng.integers(100, 140, (8, 4)).astype(np.uint8)
+        codes.reshape(8, 4, 32)[:, :, 0] = 7  # make the block max 6 * 2**e (scale is stable)
+    else:
+        _, sc = F.hif4_quantize(rng.standard_normal((8, 128)).astype(np.float32))
+    x = F.dequantize(fmt, codes, sc).astype(np.float32)
+    out = Q.resq_quantize_residual(fmt, "identity", x)
+    assert np.array_equal(out["xhat"], x.astype(np.float64))
+    assert (out["r"] == 0).all() and ((out["qr_codes"] & 7) == 0).all()
+    w = _bf16(rng.standard_normal((5, 128)) * 0.02)
+    y_resq = Q.resq_forward(fmt, "2:4", x, w)["y64"]
+    y_eq1 = Q.resq_forward(fmt, "none", x, w)["y64"]
+    assert np.array_equal(y_resq, y_eq1)
+
+
+# ----------------------------------------------------------------------------------------
+# Sec. 4.3: sparsity functions
+# ----------------------------------------------------------------------------------------
+def _tie_heavy(rng, m, d):
+    """Values with many exact ties (small integers, random signs)."""
+    return (rng.integers(0, 4, (m, d)) * rng.choice([-1.0, 1.0], (m, d))).astype(np.float64)
+
+
+def test_keep_2_4_brute_force_and_invariants():
+    rng = np.random.default_rng(0)
+    v = _tie_heavy(rng, 37, 64)
+    keep = Q.keep_2_4(v)
+    assert (keep.reshape(37, 16, 4).sum(-1) == 2).all()
+    for i in range(v.shape[0]):
+        for g in range(16):
+            grp = [(-abs(v[i, 4 * g + t]), t) for t in range(4)]
+            want = {t for _, t in sorted(grp)[:2]}
+            got = {t for t in range(4) if keep[i, 4 * g + t]}
+            assert got == want
+
+
+def _brute_top_half(keys):
+    order = sorted(range(len(keys)), key=lambda i: (-keys[i], i))
+    return set(order[: len(keys) // 2])
+
+
+def test_channel50_brute_force_and_invariants():
+    rng = np.random.default_rng(1)
+    for m, d in [(5, 8), (33, 64), (7, 130)]:
+        v = _tie_heavy(rng, m, d)
+        keep, ch = Q.keep_channel50(v)
+        assert ch.sum() == d // 2
+        keys = [math.fsum(float(t) ** 2 for t in v[:, j]) for j in range(d)]
+        assert set(np.nonzero(ch)[0]) == _brute_top_half(keys)
+        assert (keep == ch[None, :]).all()
+
+
+def test_channel_keys_are_exact_sums_on_ranged_data():
+    x = _outlier_x(96, 256, seed=3)
+    out = Q.resq_quantize_residual("hif4", "identity", x)
+    rh = F.dequantize("hif4", out["qr_codes_dense"], out["qr_scales"])
+    keys = Q.channel_keys(rh)
+    for j in range(0, 256, 17):
+        assert keys[j] == math.fsum(float(t) ** 2 for t in rh[:, j])
+
+
+@pytest.mark.parametrize("fmt", F.FORMATS)
+def test_block50_brute_force_and_invariants(fmt):
+    rng = np.random.default_rng(2)
+    for m, d in [(32, 128), (70, 192), (5, 64)]:
+        v = _tie_heavy(rng, m, d)
+        keep, blk = Q.keep_block50(v, fmt)
+        nI, nJ = (m + 31) // 32, d // 64
+        assert blk.shape == (nI, nJ) and blk.sum() == (nI * nJ) // 2
+        keys = []
+        for I in range(nI):
+            for J in range(nJ):
+                keys.append(math.fsum(float(t) ** 2 for t in v[32 * I:32 * I + 32, 64 * J:64 * J + 64].ravel()))
+        assert set(np.nonzero(blk.ravel())[0]) == _brute_top_half(keys)
+        for I in range(nI):
+            for J in range(nJ):
+                assert (keep[32 * I:32 * I + 32, 64 * J:64 * J + 64] == blk[I, J]).all()
+
+
+def test_unstructured50_brute_force_and_invariants():
+    rng = np.random.default_rng(3)
+    for m, d in [(3, 8), (9, 64), (5, 12)]:
+        v = _tie_heavy(rng, m, d)
+        keep = Q.keep_unstructured50(v)
+        assert keep.sum() == (m * d) // 2
+        flat = [abs(t) for t in v.ravel()]
+        assert set(np.nonzero(keep.ravel())[0]) == _brute_top_half(flat)
+
+
+@pytest.mark.parametrize("fmt", F.FORMATS)
+@pytest.mark.parametrize("sp", ["2:4", "channel50", "block32x64_50", "unstructured50"])
+def test_sparsify_zeroes_pruned_codes_and_keeps_scales(fmt, sp):
+    x = _outlier_x(64, 256, seed=5)
+    out = Q.resq_quantize_residual(fmt, sp, x)
+    dense, kept, keep = out["qr_codes_dense"], out["qr_codes"], out["keep"]
+    assert (kept[~keep] == 0).all()
+    assert np.array_equal(kept[keep], dense[keep])
+    assert abs(keep.mean() - 0.5) < 0.02
+
+
+# ----------------------------------------------------------------------------------------
+# Eq. 1 / Eq. 3 / Eq. 4 and the backward GEMMs: brute force with independently quantized
+# operands (integer reference quantizers, explicit loops over blocks along the right axis)
+# ----------------------------------------------------------------------------------------
+def _ref_quant_rows(fmt, x):
+    """Dequantized values of x quantized along its rows, using the integer references."""
+    b = F.block_size(fmt)
+    ref = R.mx_block_ref if fmt == "mxfp4" else R.hif4_block_ref
+    out = np.zeros(x.shape, dtype=np.float64)
+    bits = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    for i in range(x.shape[0]):
+        for j0 in range(0, x.shape[1], b):
+            codes, sc = ref([int(u) for u in bits[i, j0:j0 + b]])
+            c = np.array(codes, dtype=np.uint8)[None, :]
+            s = np.array([[sc]], dtype=np.uint8 if fmt == "mxfp4" else np.uint32)
+            out[i, j0:j0 + b] = F.dequantize(fmt, c, s)[0]
+    return out
+
+
+def _dot(a, b):
+    return math.fsum(float(p) * float(q) for p, q in zip(a, b))
+
+
+@pytest.mark.parametrize("fmt", F.FORMATS)
+def test_forward_brute_force(fmt):
+    m, d, n = 5, 128, 3
+    x = _outlier_x(m, d, seed=6, frac=0.05)
+    w = bf16_bits_to_f32(weights(rng_tree(7, 1)[0], n, d))
+    xq = _ref_quant_rows(fmt, x)
+    wq = _ref_quant_rows(fmt, w)
+    r = (x.astype(np.float64) - xq).astype(np.float32)
+    rq = _ref_quant_rows(fmt, r)
+    keep = Q.keep_2_4(rq)
+    srq = np.where(keep, rq, 0.0)
+    for sp, extra in [("none", None), ("identity", rq), ("2:4", srq)]:
+        y = Q.resq_forward(fmt, sp, x, w)["y64"]
+        for i in range(m):
+            for j in range(n):
+                want = _dot(xq[i], wq[j]) + (0.0 if extra is None else _dot(extra[i], wq[j]))
+                assert y[i, j] == pytest.approx(want, rel=1e-13, abs=1e-300)
+
+
+@pytest.mark.parametrize("fmt", F.FORMATS)
+def test_identity_equals_sum_of_operands(fmt):
+    x = _outlier_x(33, 256, seed=8)
+    w = bf16_bits_to_f32(weights(rng_tree(9, 1)[0], 17, 256))
+    o = Q.resq_forward(fmt, "identity", x, w)
+    rh = F.dequantize(fmt, o["qr_codes_dense"], o["qr_scales"])
+    np.testing.assert_allclose(o["y64"], (o["xhat"] + rh) @ o["what"].T, rtol=1e-13, atol=1e-300)
+
+
+@pytest.mark.parametrize("fmt", F.FORMATS)
+def test_backward_brute_force(fmt):
+    b = F.block_size(fmt)
+    m, n, d = 2 * b, b, 3
+    rng = rng_tree(10, 3)
+    x = bf16_bits_to_f32(activations(rng[0], m, d, 0.0, 1.0))
+    w = bf16_bits_to_f32(weights(rng[1], n, d))
+    dy = _bf16(rng[2].standard_normal((m, n)) * 1e-3)
+    out = Q.resq_backward(fmt, dy, x, w)
+    dyn = _ref_quant_rows(fmt, dy)              # blocks along n
+    wn = _ref_quant_rows(fmt, w.T).T            # blocks along n (columns of W)
+    dym = _ref_quant_rows(fmt, dy.T).T          # blocks along m (columns of dY)
+    xm = _ref_quant_rows(fmt, x.T).T            # blocks along m (columns of X)
+    for i in range(m):
+        for j in range(d):
+            assert out["dx64"][i, j] == pytest.approx(_dot(dyn[i], wn[:, j]), rel=1e-13, abs=1e-300)
+    for k in range(n):
+        for j in range(d):
+            assert out["dw64"][k, j] == pytest.approx(_dot(dym[:, k], xm[:, j]), rel=1e-13, abs=1e-300)
+    assert out["dx"].dtype == np.float32 and out["dw"].dtype == np.float32
+
+
+# ----------------------------------------------------------------------------------------
+# the paper's qualitative claims, on synthetic outlier data (statistical, not parity)
+# ----------------------------------------------------------------------------------------
+@pytest.mark.parametrize("fmt", F.FORMATS)
+def test_resq_reduces_activation_error(fmt):
+    """Sec. 4.3: the residual recovers precision lost to activation quantization."""
+    x = _outlier_x(64, 1024, seed=11)
+    w = bf16_bits_to_f32(weights(rng_tree(12, 1)[0], 64, 1024))
+    base = Q.resq_forward(fmt, "none", x, w)
+    ref = x.astype(np.float64) @ base["what"].T  # isolates the activation-side error
+    err = {sp: np.linalg.norm(Q.resq_forward(fmt, sp, x, w)["y64"] - ref)
+           for sp in ["none", "identity", "2:4", "channel50", "block32x64_50", "unstructured50"]}
+    for sp in ["identity", "2:4", "channel50", "block32x64_50", "unstructured50"]:
+        assert err[sp] < err["none"], (sp, err)
+    assert err["identity"] <= min(err[s] for s in ["2:4", "channel50", "block32x64_50"])
+
+
+@pytest.mark.parametrize("fmt", F.FORMATS)
+def test_residual_more_robust_to_2_4_than_activation(fmt):
+    """Fig. 4: S_2:4 costs Q(Delta X) less error than it costs Q(X)."""
+    x = _outlier_x(128, 1024, seed=13)
+    o = Q.resq_quantize_residual(fmt, "identity", x)
+    rh = F.dequantize(fmt, o["qr_codes_dense"], o["qr_scales"])
+    xh = o["xhat"]
+    mse_r = np.mean((rh - np.where(Q.keep_2_4(rh), rh, 0)) ** 2)
+    mse_x = np.mean((xh - np.where(Q.keep_2_4(xh), xh, 0)) ** 2)
+    assert mse_r < mse_x
+
+
+@pytest.mark.parametrize("fmt", F.FORMATS)
+def test_outliers_cause_zero_collapse(fmt):
+    """Fig. 2 / Sec. 4.2: outlier channels raise the fraction of zero codes after Q."""
+    clean = _outlier_x(64, 2048, seed=14, frac=0.0)
+    dirty = _outlier_x(64, 2048, seed=14, frac=0.01, scale=100.0)
+    z = lambda x: np.mean((F.quantize(fmt, x)[0] & 7) == 0)
+    assert z(dirty) > z(clean) + 0.05
+
+
+# ----------------------------------------------------------------------------------------
+# Sec. 5.4: overhead cost model
+# ----------------------------------------------------------------------------------------
+def test_overhead_model_matches_golden():
+    g = {}
+    with open(os.path.join(GOLDEN, "overhead_sec5_4.txt")) as f:
+        for line in f:
+            line = line.split("#")[0].strip()
+            if line:
+                k, v = line.split()
+                g[k] = float(v)
+    m, d, n = 3, 5, 7
+    mdn = m * d * n
+    assert Q.flops_dense(m, d, n) == g["dense_fp16_flops"] * mdn
+    assert Q.flops_resq(m, d, n, "2:4") - Q.flops_dense(m, d, n) == g["resq_2_4_sparse_residual_flops"] * mdn
+    assert Q.effective_cost(m, d, n, "identity", g["fp4_throughput_advantage"]) == g["effective_resq_dense_total"] * mdn
+    assert Q.effective_cost(m, d, n, "2:4", g["fp4_throughput_advantage"]) == g["effective_resq_2_4_total"] * mdn
+    assert Q.effective_cost(m, d, n, "none") == g["effective_dense_fp4_gemm"] * mdn
+    assert Q.speedup_vs_fp16("identity") == g["speedup_resq_dense_vs_fp16"]
+    assert Q.speedup_vs_fp16("2:4") == pytest.approx(g["speedup_resq_2_4_vs_fp16"], abs=1e-4)
