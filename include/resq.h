@@ -1,0 +1,169 @@
+/*
+ * resq.h - C ABI of the Rollout-ResQ FP4 linear layer for AMD Instinct MI355X (gfx950).
+ *
+ * The layer is the rollout projection of "HiFloat4 Format for End-To-End Reinforcement
+ * Learning Post-Training of Large Language Models" (Sec. 4.3, Eq. 4):
+ *
+ *     Y = Q(X) Q(W)^T + S(Q(dX)) Q(W)^T,   dX = X - Q(X)   (Eq. 2)
+ *
+ * with X (m x d, bf16 activations), W (n x d, bf16 weights), Q a block-scaled FP4
+ * quantizer (MXFP4 or HiF4, Sec. 3) and S a sparsity function (Sec. 4.3).  S = none gives
+ * the plain FP4 linear of Eq. 1, S = identity gives ResQ-Dense (Eq. 3).  The training
+ * policy's FP4 backward GEMMs (Sec. 1, Sec. 4.1: forward and backward at 4 bits) are
+ * provided by resq_linear_bwd.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Pointers named x, X, W, dY, Y, dX, dW, codes, scales, masks and workspace are DEVICE
+ *   pointers on the current HIP device; the caller owns every buffer.  The library
+ *   allocates no device memory in these calls: scratch comes from `workspace`
+ *   (size from resq_workspace_size), which must be 256-byte aligned.
+ * - `stream` is a hipStream_t passed as void* (NULL = the default stream).  Every call only
+ *   enqueues work on that stream and returns; results are ready when the stream is.
+ * - bf16 tensors are passed as uint16_t bit patterns; float outputs are IEEE float32.
+ * - Matrices are row-major; `ld*` is the row stride in elements (>= the row length).
+ * - Return value: RESQ_OK (0) or a negative resq_status.  Argument and shape errors are
+ *   detected on the host before anything is enqueued; resq_last_error() then describes the
+ *   problem (thread-local, valid until the next call on the same thread).  RESQ_ERR_HIP
+ *   reports a failed launch (hipGetLastError after enqueueing).
+ * - Inputs must be finite (no NaN / Inf); bf16 subnormals and signed zeros are handled.
+ *
+ * Quantized tensor layout ("K-major"): a tensor quantized in blocks along its contraction
+ * axis K is stored as `outer` rows of K elements:
+ *   codes : uint8 [outer][K/2]   two 4-bit codes per byte, element 2i in the low nibble;
+ *                                a code is sign << 3 | magnitude.
+ *   scales: MXFP4 -> uint8  [outer][K/32]  E8M0 code (exponent + 127) of each 32-block;
+ *           HiF4  -> uint32 [outer][K/64]  bits 0-7: E6M2 level-1 scale code; bit 8+g:
+ *                                level-2 bit of 8-element group g; bit 16+h: level-3 bit of
+ *                                4-element group h (a set bit halves the scale above it).
+ * MXFP4 element magnitudes: {0, .5, 1, 1.5, 2, 3, 4, 6} (E2M1); value = mag * 2^(E8M0-127).
+ * HiF4 element magnitudes : k/4, k = 0..7 (S1P2); value = k/4 * s1 * 2^-(b2+b3) with
+ *   s1 = 2^(c>>2 - 31) * (1 + (c&3)/4).  The paper fixes HiF4's three-level structure
+ *   (Sec. 3) but not its group sizes, E6M2 bias or scale-selection rule; the library
+ *   implements one stated reading (8- and 4-element groups, bias 31, smallest non-clipping
+ *   scale at each level, round to nearest with ties to the even code).
+ *
+ * Bit masks: bit b of byte i is element 8i + b along a row.
+ */
+#ifndef RESQ_H
+#define RESQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { RESQ_MXFP4 = 0, RESQ_HIF4 = 1 } resq_format;
+
+/* Sparsity function S applied to the quantized residual Q(dX) (Sec. 4.3). */
+typedef enum {
+  RESQ_S_NONE = 0,          /* no residual term: plain FP4 linear, Eq. 1 */
+  RESQ_S_IDENTITY = 1,      /* ResQ-Dense, Eq. 3 */
+  RESQ_S_2_4 = 2,           /* S_2:4: keep the 2 largest |values| of every 4 along d */
+  RESQ_S_CHANNEL50 = 3,     /* S_50%: keep the floor(d/2) channels (columns) of largest L2 norm */
+  RESQ_S_BLOCK32X64_50 = 4, /* S^{32x64}_50%: keep half of the 32-row x 64-column blocks */
+  RESQ_S_UNSTRUCT50 = 5     /* keep the floor(m*d/2) largest |values| of the tensor */
+} resq_sparsity;
+
+typedef enum {
+  RESQ_OK = 0,
+  RESQ_ERR_ARG = -1,         /* NULL pointer, bad enum, negative size, ld too small */
+  RESQ_ERR_SHAPE = -2,       /* a blocked axis is not a multiple of the block size */
+  RESQ_ERR_UNSUPPORTED = -3, /* valid but not implemented combination */
+  RESQ_ERR_HIP = -4,         /* HIP launch or runtime failure */
+  RESQ_ERR_WORKSPACE = -5    /* workspace missing, too small or misaligned */
+} resq_status;
+
+typedef enum { RESQ_IN_BF16 = 0, RESQ_IN_F32 = 1 } resq_dtype;
+
+typedef enum {
+  RESQ_OP_RESIDUAL_SPARSIFY = 0,
+  RESQ_OP_LINEAR_FWD = 1,
+  RESQ_OP_LINEAR_BWD = 2
+} resq_op;
+
+/*
+ * resq_quantize - Q: block-scaled FP4 quantization of one matrix (Sec. 3).
+ *
+ * x      : rows x cols, bf16 (in_dtype = RESQ_IN_BF16) or float32 (RESQ_IN_F32), row stride
+ *          ld elements.
+ * axis   : 1 -> blocks run along cols (each row is quantized on its own); output layout
+ *               [rows][cols] K-major with K = cols.  Requires cols % B == 0.
+ *          0 -> blocks run along rows (each column is quantized on its own), as the
+ *               backward GEMMs need ("transposed block scaling"); output layout
+ *               [cols][rows] K-major with K = rows, i.e. the transpose.  Requires
+ *               rows % B == 0.
+ *          B = 32 (MXFP4) or 64 (HiF4).
+ * codes  : output, uint8 [outer][K/2]; scales: output, see the layout above.
+ * Rounding is to nearest, ties to the even code, saturating; the scale choice is the
+ * format's (MXFP4: floor(log2 max|x|) - 2 clamped to [-127, 127]; HiF4: see above).
+ */
+int resq_quantize(int format, const void* x, int in_dtype, int64_t rows, int64_t cols,
+                  int64_t ld, int axis, uint8_t* codes, void* scales, void* stream);
+
+/*
+ * resq_residual_sparsify - Q(X), dX = X - Q(X) (Eq. 2, formed in float32), Q(dX) with fresh
+ * block scales, and S(Q(dX)) (Sec. 4.3), the activation side of Eq. 4.
+ *
+ * X         : m x d bf16, row stride ldx; d must be a multiple of 64 for HiF4, 32 for
+ *             MXFP4, and of 4 for S_2:4.
+ * qx_codes, qx_scales : output Q(X), layout [m][d] K-major.
+ * qr_codes, qr_scales : output S(Q(dX)): pruned elements hold the +0 code, scales are those
+ *             of Q(dX).  May be NULL when sparsity == RESQ_S_NONE.
+ * keep_mask : output, uint8 [m][d/8], 1 = element kept by S (NULL to skip).
+ * group_mask: output, kept channels (uint8 [d/8]) for RESQ_S_CHANNEL50, kept blocks
+ *             (uint8 [ceil(ceil(m/32) * (d/64) / 8)], blocks row-major) for
+ *             RESQ_S_BLOCK32X64_50; ignored otherwise (NULL allowed).
+ * Ranking (channel, block, unstructured): by sum of squares of the dequantized Q(dX) values
+ * (|value| for unstructured) in float64, ties to the lowest index; a channel's sum runs over
+ * rows 0..m-1 in order; a block's over its rows in order, each row adding its per-scale-block
+ * partial sums (exact) in column order.
+ */
+int resq_residual_sparsify(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
+                           int64_t ldx, uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes,
+                           void* qr_scales, uint8_t* keep_mask, uint8_t* group_mask,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * resq_linear_fwd - the rollout projection, Eq. 4 (Eq. 1 / Eq. 3 for S = none / identity):
+ *     Y = Q(X) Q(W)^T + S(Q(X - Q(X))) Q(W)^T
+ * X         : m x d bf16, row stride ldx (d as for resq_residual_sparsify).
+ * qw_codes, qw_scales : Q(W) for W (n x d), from resq_quantize(W, axis = 1) in the same
+ *             format; W is quantized once per policy update, not per call.
+ * Y         : output, float32 m x n, row stride ldy >= n.  Products of FP4 values are exact;
+ *             accumulation is float32.
+ */
+int resq_linear_fwd(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
+                    int64_t ldx, const uint8_t* qw_codes, const void* qw_scales, int64_t n,
+                    float* Y, int64_t ldy, void* workspace, size_t workspace_bytes,
+                    void* stream);
+
+/*
+ * resq_linear_bwd - the FP4 training-policy backward GEMMs of the linear Y = X W^T:
+ *     dX = Q_n(dY) Q_n(W)          (m x d, contraction over n)
+ *     dW = Q_m(dY)^T Q_m(X)        (n x d, contraction over m)
+ * where Q_a quantizes in blocks along axis a (each GEMM's contraction axis); no residual
+ * term (ResQ is applied to the rollout only).
+ * dY : m x n bf16, X : m x d bf16, W : n x d bf16, all contiguous (row stride = row length).
+ * n must be a multiple of the block size (for dX) and m as well (for dW).
+ * dX, dW : float32 outputs, contiguous; either may be NULL to skip that GEMM.
+ */
+int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uint16_t* W,
+                    int64_t m, int64_t d, int64_t n, float* dX, float* dW, void* workspace,
+                    size_t workspace_bytes, void* stream);
+
+/* Workspace bytes needed by `op` (a resq_op) for these arguments; 0 on bad arguments. */
+size_t resq_workspace_size(int op, int format, int sparsity, int64_t m, int64_t d, int64_t n);
+
+/* Human-readable description of the last non-OK status on this thread ("" if none). */
+const char* resq_last_error(void);
+
+/* Library version string. */
+const char* resq_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* RESQ_H */

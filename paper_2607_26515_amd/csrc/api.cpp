@@ -1,0 +1,342 @@
+// C ABI of the ResQ FP4 linear layer (declared in include/resq.h): argument validation,
+// workspace carving and kernel dispatch.  Nothing here allocates device memory.
+#include "resq.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return RESQ_OK;
+}
+
+int check_launch(const char* what) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(RESQ_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+int64_t block_of(int fmt) { return fmt == RESQ_MXFP4 ? 32 : 64; }
+size_t scale_bytes(int fmt, int64_t outer, int64_t K) {
+  return fmt == RESQ_MXFP4 ? (size_t)(outer * (K / 32)) : (size_t)(outer * (K / 64)) * 4;
+}
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+bool valid_format(int f) { return f == RESQ_MXFP4 || f == RESQ_HIF4; }
+bool valid_sparsity(int s) { return s >= RESQ_S_NONE && s <= RESQ_S_UNSTRUCT50; }
+bool global_kind(int s) {
+  return s == RESQ_S_CHANNEL50 || s == RESQ_S_BLOCK32X64_50 || s == RESQ_S_UNSTRUCT50;
+}
+
+int resid_mode(int sp) {
+  switch (sp) {
+    case RESQ_S_NONE: return resq::kResidNone;
+    case RESQ_S_IDENTITY: return resq::kResidIdentity;
+    case RESQ_S_2_4: return resq::kResid24;
+    default: return resq::kResidDense;
+  }
+}
+
+// Sequential carving of one workspace block.
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* b) : base((char*)b) {}
+  void* take(size_t bytes) {
+    void* p = base ? base + off : nullptr;
+    off += align256(bytes);
+    return p;
+  }
+};
+
+// Activation-side buffers used by resq_linear_fwd and the selection.
+struct ActWs {
+  uint8_t* qx_codes;
+  void* qx_scales;
+  uint8_t* qr_codes;
+  void* qr_scales;
+  double* partials;
+  uint8_t* group_bits;
+  uint8_t* frag_x;
+  uint8_t* c1_x;
+  uint8_t* frag_r;
+  uint8_t* c1_r;
+  resq::SelectWs sel;
+};
+
+size_t hif4_frag_bytes(int64_t rows, int64_t K) { return (size_t)((rows + 31) / 32) * (K / 64) * 3072; }
+size_t hif4_c1_bytes(int64_t rows, int64_t K) { return (size_t)((rows + 31) / 32) * (K / 64) * 64; }
+
+size_t carve_select(Carver& c, int fmt, int sp, int64_t m, int64_t d, double** partials,
+                    resq::SelectWs* sel) {
+  const size_t start = c.off;
+  void* part = (sp == RESQ_S_BLOCK32X64_50) ? c.take((size_t)m * (d / block_of(fmt)) * 8) : nullptr;
+  if (partials) *partials = (double*)part;
+  const size_t sb = global_kind(sp) ? resq::select_ws_bytes(sp, fmt, m, d) : 0;
+  void* sw = sb ? c.take(sb) : nullptr;
+  if (sel) {
+    *sel = resq::SelectWs{};
+    if (sw) resq::carve_select_ws(sw, sp, fmt, m, d, *sel);
+  }
+  return c.off - start;
+}
+
+size_t carve_fwd(void* base, int fmt, int sp, int64_t m, int64_t d, ActWs* w) {
+  Carver c(base);
+  ActWs t{};
+  t.qx_codes = (uint8_t*)c.take((size_t)m * d / 2);
+  t.qx_scales = c.take(scale_bytes(fmt, m, d));
+  if (sp != RESQ_S_NONE) {
+    t.qr_codes = (uint8_t*)c.take((size_t)m * d / 2);
+    t.qr_scales = c.take(scale_bytes(fmt, m, d));
+  }
+  carve_select(c, fmt, sp, m, d, &t.partials, &t.sel);
+  if (sp == RESQ_S_BLOCK32X64_50) t.group_bits = (uint8_t*)c.take((size_t)(((m + 31) / 32) * (d / 64) + 7) / 8);
+  if (fmt == RESQ_HIF4) {
+    t.frag_x = (uint8_t*)c.take(hif4_frag_bytes(m, d));
+    t.c1_x = (uint8_t*)c.take(hif4_c1_bytes(m, d));
+    if (sp != RESQ_S_NONE) {
+      t.frag_r = (uint8_t*)c.take(hif4_frag_bytes(m, d));
+      t.c1_r = (uint8_t*)c.take(hif4_c1_bytes(m, d));
+    }
+  }
+  if (w) *w = t;
+  return c.off;
+}
+
+struct BwdWs {
+  uint8_t *dyn_codes, *wn_codes, *dym_codes, *xm_codes;
+  void *dyn_scales, *wn_scales, *dym_scales, *xm_scales;
+  uint8_t *frag_dyn, *c1_dyn, *frag_dym, *c1_dym;
+};
+
+size_t carve_bwd(void* base, int fmt, int64_t m, int64_t d, int64_t n, BwdWs* w) {
+  Carver c(base);
+  BwdWs t{};
+  t.dyn_codes = (uint8_t*)c.take((size_t)m * n / 2);   // [m][n], blocks along n
+  t.dyn_scales = c.take(scale_bytes(fmt, m, n));
+  t.wn_codes = (uint8_t*)c.take((size_t)d * n / 2);    // [d][n], blocks along n
+  t.wn_scales = c.take(scale_bytes(fmt, d, n));
+  t.dym_codes = (uint8_t*)c.take((size_t)n * m / 2);   // [n][m], blocks along m
+  t.dym_scales = c.take(scale_bytes(fmt, n, m));
+  t.xm_codes = (uint8_t*)c.take((size_t)d * m / 2);    // [d][m], blocks along m
+  t.xm_scales = c.take(scale_bytes(fmt, d, m));
+  if (fmt == RESQ_HIF4) {
+    t.frag_dyn = (uint8_t*)c.take(hif4_frag_bytes(m, n));
+    t.c1_dyn = (uint8_t*)c.take(hif4_c1_bytes(m, n));
+    t.frag_dym = (uint8_t*)c.take(hif4_frag_bytes(n, m));
+    t.c1_dym = (uint8_t*)c.take(hif4_c1_bytes(n, m));
+  }
+  if (w) *w = t;
+  return c.off;
+}
+
+int check_ws(void* ws, size_t have, size_t need) {
+  if (need == 0) return ok();
+  if (ws == nullptr) return fail(RESQ_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed", need);
+  if ((uintptr_t)ws % 256 != 0) return fail(RESQ_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (have < need) return fail(RESQ_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", have, need);
+  return ok();
+}
+
+int check_activation_args(int format, int sparsity, const void* X, int64_t m, int64_t d,
+                          int64_t ldx) {
+  if (!valid_format(format)) return fail(RESQ_ERR_ARG, "unknown format %d", format);
+  if (!valid_sparsity(sparsity)) return fail(RESQ_ERR_ARG, "unknown sparsity %d", sparsity);
+  if (m < 0 || d < 0) return fail(RESQ_ERR_ARG, "negative size (m=%lld, d=%lld)", (long long)m, (long long)d);
+  if (ldx < d) return fail(RESQ_ERR_ARG, "ldx (%lld) < d (%lld)", (long long)ldx, (long long)d);
+  if (d % block_of(format) != 0)
+    return fail(RESQ_ERR_SHAPE, "d (%lld) is not a multiple of the block size %lld", (long long)d, (long long)block_of(format));
+  if (sparsity == RESQ_S_BLOCK32X64_50 && d % 64 != 0)
+    return fail(RESQ_ERR_SHAPE, "32x64 block sparsity needs d %% 64 == 0 (d=%lld)", (long long)d);
+  if (m > 0 && d > 0 && X == nullptr) return fail(RESQ_ERR_ARG, "X is NULL");
+  return ok();
+}
+
+int run_activation_side(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
+                        int64_t ldx, uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes,
+                        void* qr_scales, uint8_t* keep_mask, uint8_t* group_mask,
+                        double* partials, const resq::SelectWs& sel, hipStream_t s) {
+  resq::launch_residual(format, resid_mode(sparsity), X, m, d, ldx, qx_codes, qx_scales,
+                        qr_codes, qr_scales, keep_mask, partials, s);
+  if (global_kind(sparsity))
+    resq::launch_select(format, sparsity, m, d, qr_codes, qr_scales, partials, keep_mask,
+                        group_mask, sel, s);
+  return check_launch("residual/sparsify");
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* resq_last_error(void) { return g_err.c_str(); }
+
+const char* resq_version(void) { return "resq-gfx950 0.1"; }
+
+int resq_quantize(int format, const void* x, int in_dtype, int64_t rows, int64_t cols,
+                  int64_t ld, int axis, uint8_t* codes, void* scales, void* stream) {
+  if (!valid_format(format)) return fail(RESQ_ERR_ARG, "unknown format %d", format);
+  if (in_dtype != RESQ_IN_BF16 && in_dtype != RESQ_IN_F32) return fail(RESQ_ERR_ARG, "unknown input dtype %d", in_dtype);
+  if (axis != 0 && axis != 1) return fail(RESQ_ERR_ARG, "axis must be 0 or 1 (got %d)", axis);
+  if (rows < 0 || cols < 0) return fail(RESQ_ERR_ARG, "negative size");
+  if (ld < cols) return fail(RESQ_ERR_ARG, "ld (%lld) < cols (%lld)", (long long)ld, (long long)cols);
+  const int64_t K = axis == 1 ? cols : rows;
+  if (K % block_of(format) != 0)
+    return fail(RESQ_ERR_SHAPE, "blocked axis length %lld is not a multiple of %lld", (long long)K, (long long)block_of(format));
+  if (rows == 0 || cols == 0) return ok();
+  if (!x || !codes || !scales) return fail(RESQ_ERR_ARG, "NULL pointer argument");
+  hipStream_t s = (hipStream_t)stream;
+  if (axis == 1)
+    resq::launch_quant_rows(format, x, in_dtype == RESQ_IN_F32, rows, cols, ld, codes, scales, s);
+  else
+    resq::launch_quant_cols(format, x, in_dtype == RESQ_IN_F32, rows, cols, ld, codes, scales, s);
+  return check_launch("resq_quantize");
+}
+
+size_t resq_workspace_size(int op, int format, int sparsity, int64_t m, int64_t d, int64_t n) {
+  if (!valid_format(format) || !valid_sparsity(sparsity) || m < 0 || d < 0 || n < 0) return 0;
+  switch (op) {
+    case RESQ_OP_RESIDUAL_SPARSIFY: {
+      Carver c(nullptr);
+      carve_select(c, format, sparsity, m, d, nullptr, nullptr);
+      return c.off;
+    }
+    case RESQ_OP_LINEAR_FWD: return carve_fwd(nullptr, format, sparsity, m, d, nullptr);
+    case RESQ_OP_LINEAR_BWD: return carve_bwd(nullptr, format, m, d, n, nullptr);
+    default: return 0;
+  }
+}
+
+int resq_residual_sparsify(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
+                           int64_t ldx, uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes,
+                           void* qr_scales, uint8_t* keep_mask, uint8_t* group_mask,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_activation_args(format, sparsity, X, m, d, ldx);
+  if (rc != RESQ_OK) return rc;
+  if (sparsity == RESQ_S_2_4 && d % 4 != 0) return fail(RESQ_ERR_SHAPE, "S_2:4 needs d %% 4 == 0");
+  if (m == 0 || d == 0) return ok();
+  if (!qx_codes || !qx_scales) return fail(RESQ_ERR_ARG, "qx_codes / qx_scales is NULL");
+  if (sparsity != RESQ_S_NONE && (!qr_codes || !qr_scales))
+    return fail(RESQ_ERR_ARG, "qr_codes / qr_scales is NULL");
+  Carver c(workspace);
+  double* partials = nullptr;
+  resq::SelectWs sel{};
+  carve_select(c, format, sparsity, m, d, &partials, &sel);
+  rc = check_ws(workspace, workspace_bytes, c.off);
+  if (rc != RESQ_OK) return rc;
+  return run_activation_side(format, sparsity, X, m, d, ldx, qx_codes, qx_scales, qr_codes,
+                             qr_scales, keep_mask, group_mask, partials, sel,
+                             (hipStream_t)stream);
+}
+
+int resq_linear_fwd(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
+                    int64_t ldx, const uint8_t* qw_codes, const void* qw_scales, int64_t n,
+                    float* Y, int64_t ldy, void* workspace, size_t workspace_bytes,
+                    void* stream) {
+  int rc = check_activation_args(format, sparsity, X, m, d, ldx);
+  if (rc != RESQ_OK) return rc;
+  if (n < 0) return fail(RESQ_ERR_ARG, "negative n");
+  if (ldy < n) return fail(RESQ_ERR_ARG, "ldy (%lld) < n (%lld)", (long long)ldy, (long long)n);
+  if (m == 0 || n == 0) return ok();
+  if (!Y) return fail(RESQ_ERR_ARG, "Y is NULL");
+  if (d > 0 && (!qw_codes || !qw_scales)) return fail(RESQ_ERR_ARG, "qw_codes / qw_scales is NULL");
+  if ((uintptr_t)qw_codes % 16 != 0 || (format == RESQ_HIF4 && (uintptr_t)qw_scales % 4 != 0))
+    return fail(RESQ_ERR_ARG, "qw_codes must be 16-byte aligned (HiF4 scales 4-byte aligned)");
+  ActWs w{};
+  const size_t need = carve_fwd(workspace, format, sparsity, m, d, &w);
+  rc = check_ws(workspace, workspace_bytes, need);
+  if (rc != RESQ_OK) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  rc = run_activation_side(format, sparsity, X, m, d, ldx, w.qx_codes, w.qx_scales, w.qr_codes,
+                           w.qr_scales, nullptr, w.group_bits, w.partials, w.sel, s);
+  if (rc != RESQ_OK) return rc;
+  resq::GemmOperands op{};
+  op.fmt = format;
+  op.M = m; op.N = n; op.K = d;
+  op.n_terms = sparsity == RESQ_S_NONE ? 1 : 2;
+  op.blockmask = sparsity == RESQ_S_BLOCK32X64_50 ? w.group_bits : nullptr;
+  op.b_codes = qw_codes; op.b_scales = qw_scales;
+  op.Y = Y; op.ldy = ldy;
+  if (format == RESQ_MXFP4) {
+    op.a_codes[0] = w.qx_codes; op.a_scales[0] = (const uint8_t*)w.qx_scales;
+    op.a_codes[1] = w.qr_codes; op.a_scales[1] = (const uint8_t*)w.qr_scales;
+  } else {
+    const int64_t mpad = (m + 31) / 32 * 32;
+    resq::launch_pack_hif4(w.qx_codes, (const uint32_t*)w.qx_scales, m, mpad, d, w.frag_x, w.c1_x, s);
+    if (sparsity != RESQ_S_NONE)
+      resq::launch_pack_hif4(w.qr_codes, (const uint32_t*)w.qr_scales, m, mpad, d, w.frag_r, w.c1_r, s);
+    op.a_frag[0] = w.frag_x; op.a_c1[0] = w.c1_x;
+    op.a_frag[1] = w.frag_r; op.a_c1[1] = w.c1_r;
+  }
+  resq::launch_gemm(op, s);
+  return check_launch("resq_linear_fwd");
+}
+
+int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uint16_t* W,
+                    int64_t m, int64_t d, int64_t n, float* dX, float* dW, void* workspace,
+                    size_t workspace_bytes, void* stream) {
+  if (!valid_format(format)) return fail(RESQ_ERR_ARG, "unknown format %d", format);
+  if (m < 0 || d < 0 || n < 0) return fail(RESQ_ERR_ARG, "negative size");
+  const int64_t B = block_of(format);
+  if (dX && n % B != 0) return fail(RESQ_ERR_SHAPE, "dX needs n (%lld) %% %lld == 0", (long long)n, (long long)B);
+  if (dW && m % B != 0) return fail(RESQ_ERR_SHAPE, "dW needs m (%lld) %% %lld == 0", (long long)m, (long long)B);
+  if (m == 0 || d == 0 || n == 0) return ok();
+  if (!dY || (dX && !W) || (dW && !X)) return fail(RESQ_ERR_ARG, "NULL input pointer");
+  BwdWs w{};
+  const size_t need = carve_bwd(workspace, format, m, d, n, &w);
+  int rc = check_ws(workspace, workspace_bytes, need);
+  if (rc != RESQ_OK) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  if (dX) {
+    // dX[m][d] = Q_n(dY)[m][n] . Q_n(W)^T[d][n]^T : contraction over n
+    resq::launch_quant_rows(format, dY, false, m, n, n, w.dyn_codes, w.dyn_scales, s);
+    resq::launch_quant_cols(format, W, false, n, d, d, w.wn_codes, w.wn_scales, s);
+    resq::GemmOperands op{};
+    op.fmt = format; op.M = m; op.N = d; op.K = n; op.n_terms = 1;
+    op.b_codes = w.wn_codes; op.b_scales = w.wn_scales; op.Y = dX; op.ldy = d;
+    if (format == RESQ_MXFP4) {
+      op.a_codes[0] = w.dyn_codes; op.a_scales[0] = (const uint8_t*)w.dyn_scales;
+    } else {
+      resq::launch_pack_hif4(w.dyn_codes, (const uint32_t*)w.dyn_scales, m, (m + 31) / 32 * 32, n, w.frag_dyn, w.c1_dyn, s);
+      op.a_frag[0] = w.frag_dyn; op.a_c1[0] = w.c1_dyn;
+    }
+    resq::launch_gemm(op, s);
+  }
+  if (dW) {
+    // dW[n][d] = Q_m(dY)^T[n][m] . Q_m(X)^T[d][m]^T : contraction over m
+    resq::launch_quant_cols(format, dY, false, m, n, n, w.dym_codes, w.dym_scales, s);
+    resq::launch_quant_cols(format, X, false, m, d, d, w.xm_codes, w.xm_scales, s);
+    resq::GemmOperands op{};
+    op.fmt = format; op.M = n; op.N = d; op.K = m; op.n_terms = 1;
+    op.b_codes = w.xm_codes; op.b_scales = w.xm_scales; op.Y = dW; op.ldy = d;
+    if (format == RESQ_MXFP4) {
+      op.a_codes[0] = w.dym_codes; op.a_scales[0] = (const uint8_t*)w.dym_scales;
+    } else {
+      resq::launch_pack_hif4(w.dym_codes, (const uint32_t*)w.dym_scales, n, (n + 31) / 32 * 32, m, w.frag_dym, w.c1_dym, s);
+      op.a_frag[0] = w.frag_dym; op.a_c1[0] = w.c1_dym;
+    }
+    resq::launch_gemm(op, s);
+  }
+  return check_launch("resq_linear_bwd");
+}
+
+}  // extern "C"

@@ -1,0 +1,142 @@
+// Device-side FP4 arithmetic for gfx950: MXFP4 and HiF4 block quantization and the
+// operand encodings the scaled f8f6f4 MFMA consumes.
+//
+// Every decision (block scale, element code, level-2/3 bits) is made by exact comparisons:
+// thresholds are small integers times powers of two (exact in float32), and inputs are
+// rescaled by powers of two with v_ldexp_f32 (exact; fp32 denormals are kept).  No reciprocal
+// or division is used, since HiF4 scales are not powers of two.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace resq {
+
+constexpr int kMxBlock = 32;
+constexpr int kHiBlock = 64;
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+// floor(log2(a)) for finite a > 0, fp32 subnormals included.
+__device__ __forceinline__ int ilog2f(float a) {
+  const uint32_t u = __float_as_uint(a);
+  const int ef = (u >> 23) & 0xFF;
+  if (ef) return ef - 127;
+  return -149 + (31 - __clz(u & 0x7FFFFFu));
+}
+
+// Max of v over aligned groups of G lanes (G a power of two <= 64).
+template <int G>
+__device__ __forceinline__ float group_max(float v) {
+#pragma unroll
+  for (int o = 1; o < G; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+template <int G>
+__device__ __forceinline__ double group_sum(double v) {
+#pragma unroll
+  for (int o = 1; o < G; o <<= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// ------------------------------------------------------------------------------------------
+// MXFP4: E2M1 elements, one E8M0 scale per 32 elements (OCP MX conversion rule, paper Sec. 3)
+// ------------------------------------------------------------------------------------------
+// Shared exponent of a block with max magnitude amax: floor(log2 amax) - 2, clamped.
+__device__ __forceinline__ int mx_exponent(float amax) {
+  if (!(amax > 0.f)) return -127;
+  const int e = ilog2f(amax) - 2;
+  return e < -127 ? -127 : (e > 127 ? 127 : e);
+}
+
+// 4-bit code of x under exponent E: nearest E2M1 magnitude, ties to the even code, saturating.
+__device__ __forceinline__ uint32_t mx_code(float x, int E) {
+  const float y = ldexpf(fabsf(x), -E);  // exact power-of-two rescale
+  const uint32_t k = (y > 0.25f) + (y >= 0.75f) + (y > 1.25f) + (y >= 1.75f) + (y > 2.5f) +
+                     (y >= 3.5f) + (y > 5.0f);
+  return ((__float_as_uint(x) >> 28) & 8u) | k;
+}
+
+__device__ __forceinline__ float e2m1_mag(uint32_t k) {
+  // {0, .5, 1, 1.5, 2, 3, 4, 6}
+  const float lo = (float)(k & 1) * 0.5f + (float)((k >> 1) & 1) * 1.0f;  // k<4: k/2
+  if (k < 4) return lo;
+  return (k == 4) ? 2.f : (k == 5) ? 3.f : (k == 6) ? 4.f : 6.f;
+}
+
+__device__ __forceinline__ float mx_value(uint32_t code, int E) {
+  const float v = ldexpf(e2m1_mag(code & 7), E);
+  return (code & 8) ? -v : v;
+}
+
+// ------------------------------------------------------------------------------------------
+// HiF4 (reading stated in resq.h): 64-element blocks, E6M2 level-1 scale, one-bit level-2
+// (per 8) and level-3 (per 4) down-shifts, S1P2 elements k/4.
+//   s1 = 2^(e-31) (1 + m/4) for code c = 4e + m;  element value = k (4+m) 2^(e-35-b)
+// ------------------------------------------------------------------------------------------
+// Smallest code c with 1.75 * s1(c) >= A (saturating at 255).
+__device__ __forceinline__ int hif4_c1(float A) {
+  if (!(A > 0.f)) return 0;
+  const int ea = ilog2f(A);
+  if (ea < -31) return 0;
+  if (ea > 57) return 255;
+  // 1.75 * s1 for codes base..base+3 is {35, 42, 49, 56} * 2^(ea-5); base+4 always covers A
+  const int base = 4 * (ea + 30) + 1;
+  const int c = base + (ldexpf(35.f, ea - 5) < A) + (ldexpf(42.f, ea - 5) < A) +
+                (ldexpf(49.f, ea - 5) < A) + (ldexpf(56.f, ea - 5) < A);
+  return c < 0 ? 0 : (c > 255 ? 255 : c);
+}
+
+// 1.75 * s1 / 2 * 2^-shift = 7 (4+m) 2^(e-36-shift): the "fits at half the scale" threshold.
+__device__ __forceinline__ float hif4_half_fit(int c1, int shift) {
+  return ldexpf((float)(7 * (4 + (c1 & 3))), (c1 >> 2) - 36 - shift);
+}
+
+// Magnitude k (0..7) of |x| on the grid k/4 * s, s = s1 2^-b: nearest, ties to even k.
+__device__ __forceinline__ uint32_t hif4_k(float x, int c1, int b) {
+  const float y = ldexpf(fabsf(x), 36 + b - (c1 >> 2));  // midpoints are (2k'+1)(4+m)
+  const float q = (float)(4 + (c1 & 3));
+  return (y > q) + (y >= 3.f * q) + (y > 5.f * q) + (y >= 7.f * q) + (y > 9.f * q) +
+         (y >= 11.f * q) + (y > 13.f * q);
+}
+
+__device__ __forceinline__ float hif4_value(uint32_t code, int c1, int b) {
+  const float v = ldexpf((float)((code & 7) * (4 + (c1 & 3))), (c1 >> 2) - 35 - b);
+  return (code & 8) ? -v : v;
+}
+
+// Compress the even bits of a 16-bit value into 8 bits.
+__device__ __forceinline__ uint32_t even_bits16(uint32_t x) {
+  x &= 0x5555u;
+  x = (x | (x >> 1)) & 0x3333u;
+  x = (x | (x >> 2)) & 0x0F0Fu;
+  x = (x | (x >> 4)) & 0x00FFu;
+  return x;
+}
+
+// ------------------------------------------------------------------------------------------
+// MFMA operand encodings for HiF4 (f8f6f4 MFMA, formats: 2 = FP6 E2M3, 3 = BF6 E3M2)
+// ------------------------------------------------------------------------------------------
+// Activation side: V = k (4+m) 2^(2-b) <= 196 (value = V 2^(e-37)) is split V = 16 hi + lo;
+// hi, lo <= 15 are E2M3 codes of hi/8, lo/8 (E2M3 code t has value t/8 for t <= 15).
+// Scales: hi term 2^(e-30) -> E8M0 e + 97, lo term 2^(e-34) -> E8M0 e + 93.
+__device__ __forceinline__ void hif4_split_e2m3(uint32_t code, int c1, int b, uint32_t& hi,
+                                                uint32_t& lo) {
+  const uint32_t V = ((code & 7) * (4 + (c1 & 3))) << (2 - b);
+  const uint32_t s = (code & 8) << 2;  // sign -> bit 5
+  hi = s | (V >> 4);
+  lo = s | (V & 15);
+}
+
+// Weight side: k 2^-b as a BF6 E3M2 code (value exact), sign in bit 5; the remaining
+// factor (4+m) 2^(e-35) is the E8M0 scale e + 92 times the per-column factor (4+m).
+__device__ __forceinline__ uint32_t hif4_e3m2(uint32_t code, int b) {
+  const uint32_t k = code & 7;
+  // E3M2 (bias 3) of k: 0, 1.0 (e3,m0), 2.0 (e4), 3.0 (e4,m2), 4.0 (e5), 5, 6, 7
+  const uint32_t lut = (k == 0) ? 0u : (k == 1) ? 12u : (k == 2) ? 16u : (k == 3) ? 18u : 16u + k;
+  const uint32_t mag = k ? lut - ((uint32_t)b << 2) : 0u;
+  return ((code & 8) << 2) | mag;
+}
+
+}  // namespace resq

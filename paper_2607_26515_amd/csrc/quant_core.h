@@ -1,0 +1,85 @@
+// Cooperative quantization of one block-scaled FP4 block, four elements per lane.
+//
+// A lane owns 4 consecutive elements along the block axis.  An MXFP4 block (32 elements)
+// spans 8 aligned lanes, a HiF4 block (64) spans 16, a HiF4 level-2 group (8) spans 2 and a
+// level-3 group (4) is one lane.  All lanes of a block must be active.
+#pragma once
+
+#include "device_fp4.h"
+
+namespace resq {
+
+enum Fmt { kMX = 0, kHI = 1 };
+
+struct Quad {
+  uint32_t code[4];  // 4-bit codes (sign << 3 | magnitude)
+  float val[4];      // dequantized values (exact in float32)
+  uint32_t scale;    // MX: E8M0 byte; HiF4: metadata word (same on every lane of the block)
+  int c1;            // HiF4 level-1 code
+  int b;             // HiF4 level-2 + level-3 shift of this lane's 4 elements
+  int E;             // MX shared exponent
+};
+
+template <int FMT>
+__device__ __forceinline__ Quad quantize_quad(const float x[4]) {
+  Quad q;
+  float a = fmaxf(fmaxf(fabsf(x[0]), fabsf(x[1])), fmaxf(fabsf(x[2]), fabsf(x[3])));
+  if constexpr (FMT == kMX) {
+    const float amax = group_max<8>(a);
+    q.E = mx_exponent(amax);
+    q.scale = (uint32_t)(q.E + 127);
+    q.c1 = 0;
+    q.b = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      q.code[i] = mx_code(x[i], q.E);
+      q.val[i] = mx_value(q.code[i], q.E);
+    }
+  } else {
+    const float A = group_max<16>(a);
+    q.c1 = hif4_c1(A);
+    const float ag = fmaxf(a, __shfl_xor(a, 1, 64));
+    const int b2 = ag <= hif4_half_fit(q.c1, 0) ? 1 : 0;
+    const int b3 = a <= hif4_half_fit(q.c1, b2) ? 1 : 0;
+    q.b = b2 + b3;
+    q.E = 0;
+    const int lane = __lane_id();
+    const int base = lane & ~15;
+    const uint64_t m3 = __ballot(b3);
+    const uint64_t m2 = __ballot(b2 && ((lane & 1) == 0));
+    const uint32_t bits3 = (uint32_t)(m3 >> base) & 0xFFFFu;
+    const uint32_t bits2 = even_bits16((uint32_t)(m2 >> base) & 0xFFFFu);
+    q.scale = (uint32_t)q.c1 | (bits2 << 8) | (bits3 << 16);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t k = hif4_k(x[i], q.c1, q.b);
+      q.code[i] = ((__float_as_uint(x[i]) >> 28) & 8u) | k;
+      q.val[i] = hif4_value(q.code[i], q.c1, q.b);
+    }
+  }
+  return q;
+}
+
+__device__ __forceinline__ uint32_t pack_quad_codes(const uint32_t c[4]) {
+  return c[0] | (c[1] << 4) | (c[2] << 8) | (c[3] << 12);
+}
+
+// S_2:4 on one group of four: keep the two largest magnitudes, lower index on ties.
+// Magnitude codes are monotone in |value| within a block (shared scale), so codes compare.
+__device__ __forceinline__ uint32_t keep_2_of_4(const uint32_t c[4]) {
+  uint32_t keep = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    int rank = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (j == i) continue;
+      const uint32_t kj = c[j] & 7, ki = c[i] & 7;
+      rank += (kj > ki) || (kj == ki && j < i);
+    }
+    keep |= (rank < 2 ? 1u : 0u) << i;
+  }
+  return keep;
+}
+
+}  // namespace resq

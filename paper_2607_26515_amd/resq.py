@@ -1,0 +1,231 @@
+"""Python binding of libresq.so (the C ABI declared in include/resq.h).
+
+Two layers:
+
+* ``resq_quantize``, ``resq_residual_sparsify``, ``resq_linear_fwd``, ``resq_linear_bwd``,
+  ``resq_workspace_size``, ``resq_last_error``, ``resq_version``: the C entry points with the
+  same names and arguments (integers for device pointers and the stream); they return the
+  status code.
+* ``quantize``, ``residual_sparsify``, ``linear_fwd``, ``linear_bwd``: the same calls on
+  torch CUDA tensors.  They allocate outputs and the workspace with torch, pass pointers and
+  the current stream, and raise ``ResqError`` on a non-zero status.  Every computation runs
+  in the library's HIP kernels; nothing here touches the data.
+
+The library must have been built (``python -m paper_2607_26515_amd.build``); importing a
+function that needs it raises ``ResqError`` otherwise.  There is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libresq.so")
+_lib = None
+
+MXFP4, HIF4 = 0, 1
+FORMATS = {"mxfp4": MXFP4, "hif4": HIF4}
+S_NONE, S_IDENTITY, S_2_4, S_CHANNEL50, S_BLOCK32X64_50, S_UNSTRUCT50 = range(6)
+SPARSITY = {"none": S_NONE, "identity": S_IDENTITY, "2:4": S_2_4, "channel50": S_CHANNEL50,
+            "block32x64_50": S_BLOCK32X64_50, "unstructured50": S_UNSTRUCT50}
+OK, ERR_ARG, ERR_SHAPE, ERR_UNSUPPORTED, ERR_HIP, ERR_WORKSPACE = 0, -1, -2, -3, -4, -5
+IN_BF16, IN_F32 = 0, 1
+OP_RESIDUAL_SPARSIFY, OP_LINEAR_FWD, OP_LINEAR_BWD = 0, 1, 2
+
+EXPORTED = ("resq_quantize", "resq_residual_sparsify", "resq_linear_fwd", "resq_linear_bwd",
+            "resq_workspace_size", "resq_last_error", "resq_version")
+
+
+class ResqError(RuntimeError):
+    def __init__(self, msg: str, code: int = 0):
+        super().__init__(msg)
+        self.code = code
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load() -> ctypes.CDLL:
+    """Load libresq.so once (raises ResqError if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise ResqError(f"{_LIB_PATH} is missing: build it with `python -m paper_2607_26515_amd.build`")
+    lib = ctypes.CDLL(_LIB_PATH)
+    vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
+    lib.resq_quantize.argtypes = [i32, vp, i32, i64, i64, i64, i32, vp, vp, vp]
+    lib.resq_residual_sparsify.argtypes = [i32, i32, vp, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.resq_linear_fwd.argtypes = [i32, i32, vp, i64, i64, i64, vp, vp, i64, vp, i64, vp, sz, vp]
+    lib.resq_linear_bwd.argtypes = [i32, vp, vp, vp, i64, i64, i64, vp, vp, vp, sz, vp]
+    lib.resq_workspace_size.argtypes = [i32, i32, i32, i64, i64, i64]
+    for f in ("resq_quantize", "resq_residual_sparsify", "resq_linear_fwd", "resq_linear_bwd"):
+        getattr(lib, f).restype = i32
+    lib.resq_workspace_size.restype = sz
+    lib.resq_last_error.restype = ctypes.c_char_p
+    lib.resq_version.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+# ------------------------------------------------------------------------------------------
+# C entry points (pointers and the stream as integers; 0 = NULL / default stream)
+# ------------------------------------------------------------------------------------------
+def resq_quantize(fmt, x, in_dtype, rows, cols, ld, axis, codes, scales, stream=0) -> int:
+    return load().resq_quantize(fmt, x, in_dtype, rows, cols, ld, axis, codes, scales, stream)
+
+
+def resq_residual_sparsify(fmt, sparsity, X, m, d, ldx, qx_codes, qx_scales, qr_codes, qr_scales,
+                           keep_mask, group_mask, workspace, workspace_bytes, stream=0) -> int:
+    return load().resq_residual_sparsify(fmt, sparsity, X, m, d, ldx, qx_codes, qx_scales, qr_codes,
+                                         qr_scales, keep_mask, group_mask, workspace,
+                                         workspace_bytes, stream)
+
+
+def resq_linear_fwd(fmt, sparsity, X, m, d, ldx, qw_codes, qw_scales, n, Y, ldy, workspace,
+                    workspace_bytes, stream=0) -> int:
+    return load().resq_linear_fwd(fmt, sparsity, X, m, d, ldx, qw_codes, qw_scales, n, Y, ldy,
+                                  workspace, workspace_bytes, stream)
+
+
+def resq_linear_bwd(fmt, dY, X, W, m, d, n, dX, dW, workspace, workspace_bytes, stream=0) -> int:
+    return load().resq_linear_bwd(fmt, dY, X, W, m, d, n, dX, dW, workspace, workspace_bytes, stream)
+
+
+def resq_workspace_size(op, fmt, sparsity, m, d, n) -> int:
+    return load().resq_workspace_size(op, fmt, sparsity, m, d, n)
+
+
+def resq_last_error() -> str:
+    return load().resq_last_error().decode()
+
+
+def resq_version() -> str:
+    return load().resq_version().decode()
+
+
+# ------------------------------------------------------------------------------------------
+# torch helpers (argument marshalling only)
+# ------------------------------------------------------------------------------------------
+def _fmt(fmt) -> int:
+    return FORMATS[fmt] if isinstance(fmt, str) else int(fmt)
+
+
+def _sp(sp) -> int:
+    return SPARSITY[sp] if isinstance(sp, str) else int(sp)
+
+
+def _p(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+def _stream(stream) -> int:
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return int(s.cuda_stream)
+
+
+def _check(rc: int, what: str):
+    if rc != OK:
+        raise ResqError(f"{what} failed ({rc}): {resq_last_error()}", rc)
+
+
+def _empty_u8(n, device):
+    import torch
+    return torch.empty(int(n), dtype=torch.uint8, device=device)
+
+
+def scale_shape(fmt, outer, K):
+    """(shape, dtype name) of the scale array of a K-major quantized tensor."""
+    return ((outer, K // 32), "uint8") if _fmt(fmt) == MXFP4 else ((outer, K // 64), "int32")
+
+
+def _empty_scales(fmt, outer, K, device):
+    import torch
+    shape, dt = scale_shape(fmt, outer, K)
+    return torch.empty(shape, dtype=torch.uint8 if dt == "uint8" else torch.int32, device=device)
+
+
+def workspace(op, fmt, sparsity, m, d, n=0, device="cuda"):
+    import torch
+    nb = resq_workspace_size(op, _fmt(fmt), _sp(sparsity), m, d, n)
+    # torch's caching allocator returns 256-byte aligned blocks
+    return torch.empty(max(nb, 1), dtype=torch.uint8, device=device), nb
+
+
+def quantize(x, fmt, axis: int = 1, stream=None):
+    """Q(x) in blocks along `axis` (1: along columns; 0: along rows, output transposed)."""
+    import torch
+    rows, cols = x.shape
+    f32 = x.dtype == torch.float32
+    if not f32 and x.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
+        raise TypeError("x must be bfloat16 (or its uint16 bits) or float32")
+    outer, K = (rows, cols) if axis == 1 else (cols, rows)
+    codes = torch.empty((outer, K // 2), dtype=torch.uint8, device=x.device)
+    scales = _empty_scales(fmt, outer, K, x.device)
+    rc = resq_quantize(_fmt(fmt), _p(x), IN_F32 if f32 else IN_BF16, rows, cols, x.stride(0), axis,
+                       _p(codes), _p(scales), _stream(stream))
+    _check(rc, "resq_quantize")
+    return codes, scales
+
+
+def residual_sparsify(x, fmt, sparsity, stream=None):
+    """Q(X), S(Q(X - Q(X))) and the masks, as a dict of device tensors."""
+    import torch
+    m, d = x.shape
+    f, sp = _fmt(fmt), _sp(sparsity)
+    out = {
+        "qx_codes": torch.empty((m, d // 2), dtype=torch.uint8, device=x.device),
+        "qx_scales": _empty_scales(f, m, d, x.device),
+    }
+    if sp != S_NONE:
+        out["qr_codes"] = torch.empty((m, d // 2), dtype=torch.uint8, device=x.device)
+        out["qr_scales"] = _empty_scales(f, m, d, x.device)
+        out["keep_mask"] = torch.empty((m, d // 8), dtype=torch.uint8, device=x.device)
+    if sp == S_CHANNEL50:
+        out["group_mask"] = torch.zeros(((d + 7) // 8,), dtype=torch.uint8, device=x.device)
+    elif sp == S_BLOCK32X64_50:
+        nblk = ((m + 31) // 32) * (d // 64)
+        out["group_mask"] = torch.zeros(((nblk + 7) // 8,), dtype=torch.uint8, device=x.device)
+    ws, nb = workspace(OP_RESIDUAL_SPARSIFY, f, sp, m, d, 0, x.device)
+    rc = resq_residual_sparsify(f, sp, _p(x), m, d, x.stride(0), _p(out["qx_codes"]),
+                                _p(out["qx_scales"]), _p(out.get("qr_codes")),
+                                _p(out.get("qr_scales")), _p(out.get("keep_mask")),
+                                _p(out.get("group_mask")), _p(ws), nb, _stream(stream))
+    _check(rc, "resq_residual_sparsify")
+    return out
+
+
+def linear_fwd(x, qw_codes, qw_scales, fmt, sparsity, y=None, ws=None, stream=None):
+    """Y = Q(X) Q(W)^T + S(Q(X - Q(X))) Q(W)^T (float32)."""
+    import torch
+    m, d = x.shape
+    n = qw_codes.shape[0]
+    f, sp = _fmt(fmt), _sp(sparsity)
+    if y is None:
+        y = torch.empty((m, n), dtype=torch.float32, device=x.device)
+    if ws is None:
+        ws = workspace(OP_LINEAR_FWD, f, sp, m, d, n, x.device)
+    buf, nb = ws
+    rc = resq_linear_fwd(f, sp, _p(x), m, d, x.stride(0), _p(qw_codes), _p(qw_scales), n, _p(y),
+                         y.stride(0), _p(buf), nb, _stream(stream))
+    _check(rc, "resq_linear_fwd")
+    return y
+
+
+def linear_bwd(dy, x, w, fmt, want_dx=True, want_dw=True, ws=None, stream=None):
+    """dX = Q_n(dY) Q_n(W), dW = Q_m(dY)^T Q_m(X) (float32)."""
+    import torch
+    m, n = dy.shape
+    d = x.shape[1]
+    f = _fmt(fmt)
+    dx = torch.empty((m, d), dtype=torch.float32, device=dy.device) if want_dx else None
+    dw = torch.empty((n, d), dtype=torch.float32, device=dy.device) if want_dw else None
+    if ws is None:
+        ws = workspace(OP_LINEAR_BWD, f, S_NONE, m, d, n, dy.device)
+    buf, nb = ws
+    rc = resq_linear_bwd(f, _p(dy), _p(x), _p(w), m, d, n, _p(dx), _p(dw), _p(buf), nb,
+                         _stream(stream))
+    _check(rc, "resq_linear_bwd")
+    return dx, dw

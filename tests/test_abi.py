@@ -1,0 +1,95 @@
+"""C ABI contract tests that need no GPU: the library loads, exports every entry point that
+include/resq.h declares, and rejects bad arguments on the host before enqueueing anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_26515_amd as P
+from paper_2607_26515_amd import resq as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "resq.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(resq_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(P.library_path())
+    names = _declared()
+    assert {"resq_quantize", "resq_residual_sparsify", "resq_linear_fwd", "resq_linear_bwd"} <= set(names)
+    for name in names:
+        assert hasattr(lib, name), name
+    assert set(names) == set(B.EXPORTED)
+
+
+def test_version_and_empty_error():
+    assert P.resq_version().startswith("resq-gfx950")
+    assert P.resq_workspace_size(B.OP_LINEAR_FWD, B.HIF4, B.S_2_4, 16, 2048, 2048) > 0
+
+
+@pytest.mark.parametrize("args,code", [
+    ((7, 0, 0, 4, 64, 64, 1, 0, 0), B.ERR_ARG),          # bad format
+    ((0, 0, 3, 4, 64, 64, 1, 0, 0), B.ERR_ARG),          # bad dtype
+    ((0, 0, 0, 4, 64, 64, 2, 0, 0), B.ERR_ARG),          # bad axis
+    ((0, 0, 0, 4, 64, 32, 1, 0, 0), B.ERR_ARG),          # ld < cols
+    ((0, 0, 0, 4, 48, 48, 1, 0, 0), B.ERR_SHAPE),        # 48 % 32 != 0 along the blocked axis
+    ((1, 0, 0, 4, 96, 96, 1, 0, 0), B.ERR_SHAPE),        # 96 % 64 != 0 (HiF4)
+    ((1, 0, 0, 96, 64, 64, 0, 0, 0), B.ERR_SHAPE),       # axis 0 blocks along rows
+    ((0, 0, 0, 4, 64, 64, 1, 0, 0), B.ERR_ARG),          # NULL pointers
+    ((0, 0, 0, -1, 64, 64, 1, 0, 0), B.ERR_ARG),         # negative size
+])
+def test_quantize_rejects_bad_arguments(args, code):
+    assert P.resq_quantize(*args, 0) == code
+    assert P.resq_last_error() != ""
+
+
+def test_quantize_empty_is_ok():
+    assert P.resq_quantize(0, 0, 0, 0, 64, 64, 1, 0, 0, 0) == B.OK
+    assert P.resq_last_error() == ""
+
+
+@pytest.mark.parametrize("fmt,sp,m,d,ldx,code", [
+    (9, B.S_2_4, 4, 64, 64, B.ERR_ARG),
+    (B.MXFP4, 11, 4, 64, 64, B.ERR_ARG),
+    (B.MXFP4, B.S_2_4, 4, 64, 32, B.ERR_ARG),
+    (B.HIF4, B.S_2_4, 4, 96, 96, B.ERR_SHAPE),
+    (B.MXFP4, B.S_BLOCK32X64_50, 4, 96, 96, B.ERR_SHAPE),
+    (B.MXFP4, B.S_2_4, 4, 64, 64, B.ERR_ARG),  # X NULL
+])
+def test_residual_sparsify_rejects_bad_arguments(fmt, sp, m, d, ldx, code):
+    assert P.resq_residual_sparsify(fmt, sp, 0, m, d, ldx, 0, 0, 0, 0, 0, 0, 0, 0, 0) == code
+
+
+def test_linear_fwd_rejects_bad_arguments():
+    # ldy < n
+    assert P.resq_linear_fwd(0, 2, 16, 4, 64, 64, 16, 16, 8, 16, 4, 0, 0, 0) == B.ERR_ARG
+    # workspace missing (all pointers non-NULL and 256-aligned, but no workspace)
+    assert P.resq_linear_fwd(0, 2, 256, 4, 64, 64, 256, 256, 8, 256, 8, 0, 0, 0) == B.ERR_WORKSPACE
+    # misaligned workspace
+    assert P.resq_linear_fwd(0, 2, 256, 4, 64, 64, 256, 256, 8, 256, 8, 257, 1 << 20, 0) == B.ERR_WORKSPACE
+    # workspace too small
+    assert P.resq_linear_fwd(0, 2, 256, 4, 64, 64, 256, 256, 8, 256, 8, 256, 16, 0) == B.ERR_WORKSPACE
+    # Y NULL
+    assert P.resq_linear_fwd(0, 2, 256, 4, 64, 64, 256, 256, 8, 0, 8, 256, 1 << 20, 0) == B.ERR_ARG
+
+
+def test_linear_bwd_rejects_bad_arguments():
+    # n not a multiple of the block for dX
+    assert P.resq_linear_bwd(1, 256, 256, 256, 64, 64, 96, 256, 0, 256, 1 << 30, 0) == B.ERR_SHAPE
+    # m not a multiple of the block for dW
+    assert P.resq_linear_bwd(0, 256, 256, 256, 48, 64, 64, 0, 256, 256, 1 << 30, 0) == B.ERR_SHAPE
+    assert P.resq_linear_bwd(0, 256, 256, 256, 64, 64, 64, 256, 256, 0, 0, 0) == B.ERR_WORKSPACE
+    assert P.resq_linear_bwd(0, 0, 256, 256, 64, 64, 64, 256, 256, 256, 1 << 30, 0) == B.ERR_ARG
+
+
+def test_workspace_sizes_grow_with_shape():
+    a = P.resq_workspace_size(B.OP_LINEAR_FWD, B.HIF4, B.S_2_4, 256, 2048, 2048)
+    b = P.resq_workspace_size(B.OP_LINEAR_FWD, B.HIF4, B.S_2_4, 512, 2048, 2048)
+    assert 0 < a < b
+    assert P.resq_workspace_size(9, 0, 0, 1, 64, 1) == 0
+    assert P.resq_workspace_size(B.OP_LINEAR_BWD, B.MXFP4, 0, 64, 64, 64) > 0

@@ -1,0 +1,151 @@
+"""GPU <-> oracle parity through the C ABI: bit-exact codes, scales and masks; float32
+outputs within a normwise relative error of 1e-5.  Shapes span several tiles and ragged
+tails; inputs are seeded synthetic data with outlier channels plus adversarial blocks."""
+import numpy as np
+import pytest
+
+from oracle import formats as F
+from oracle import resq as Q
+from synth import activations, bf16_bits_to_f32, f32_to_bf16_bits, grad_output, rng_tree, weights
+from _gpu_util import (assert_close, assert_codes_equal, assert_scales_equal, dev_bf16, dev_f32,
+                       host, log, pack_bits)
+
+pytestmark = pytest.mark.gpu
+
+FMTS = ["mxfp4", "hif4"]
+
+
+def _adversarial_bits(rows, cols, seed):
+    """bf16 rows: outlier data plus zero rows, -0, subnormals, ties, a single outlier, a large
+    in-range block and exact E2M1/S1P2 midpoints."""
+    rng = rng_tree(seed, 1)[0]
+    x = bf16_bits_to_f32(activations(rng, rows, cols, 0.02, 50.0)).copy()
+    if rows >= 8:
+        x[0] = 0.0
+        x[1] = -0.0
+        x[2, :] = bf16_bits_to_f32(np.arange(1, cols + 1, dtype=np.uint16) % 128)  # subnormals
+        x[3, :] = 1.0  # all ties
+        x[4, :] = 0.01
+        x[4, cols // 2] = 300.0  # single outlier
+        x[5, :] = 2.0 ** 20 * np.sign(x[5])  # large, in range
+        x[6, :] = np.resize(np.array([6.0, 5.0, 3.5, 2.5, 1.75, 1.25, 0.75, 0.25], np.float32), cols)  # MX midpoints
+        x[7, :] = np.resize(np.array([1.75, 1.625, 1.375, 1.125, 0.875, 0.625, 0.375, 0.125], np.float32), cols)
+    return f32_to_bf16_bits(x)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("rows,cols", [(1, 64), (37, 256), (300, 2048), (8, 11008)])
+def test_quantize_rows_bf16(fmt, rows, cols):
+    import paper_2607_26515_amd as P
+    log(f"quantize rows bf16 {fmt} {rows}x{cols}")
+    bits = _adversarial_bits(rows, cols, seed=rows + cols)
+    codes, scales = P.quantize(dev_bf16(bits), fmt, axis=1)
+    oc, os_ = F.quantize(fmt, bf16_bits_to_f32(bits))
+    assert_codes_equal(codes, oc, "codes")
+    assert_scales_equal(fmt, scales, os_, "scales")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_quantize_rows_f32_midpoints(fmt):
+    import paper_2607_26515_amd as P
+    log(f"quantize rows f32 {fmt}")
+    rng = np.random.default_rng(21)
+    x = (rng.standard_normal((64, 512)) * np.exp2(rng.integers(-30, 30, (64, 1)))).astype(np.float32)
+    x[:8] = np.float32(1.0)
+    x[:8, 1:9] = np.float32(0.375)
+    x[8:16] = (rng.integers(-28, 29, (8, 512)) / 16.0).astype(np.float32)  # many exact ties
+    codes, scales = P.quantize(dev_f32(x), fmt, axis=1)
+    oc, os_ = F.quantize(fmt, x)
+    assert_codes_equal(codes, oc, "codes")
+    assert_scales_equal(fmt, scales, os_, "scales")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("rows,cols", [(64, 1), (128, 37), (192, 100), (2048, 130)])
+def test_quantize_cols(fmt, rows, cols):
+    import paper_2607_26515_amd as P
+    if rows % F.block_size(fmt):
+        pytest.skip("rows must be a multiple of the block size")
+    log(f"quantize cols {fmt} {rows}x{cols}")
+    bits = _adversarial_bits(rows, cols, seed=3 * rows + cols)
+    codes, scales = P.quantize(dev_bf16(bits), fmt, axis=0)
+    oc, os_ = F.quantize(fmt, bf16_bits_to_f32(bits).T.copy())
+    assert_codes_equal(codes, oc, "codes")
+    assert_scales_equal(fmt, scales, os_, "scales")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("sp", ["none", "identity", "2:4"])
+@pytest.mark.parametrize("m,d", [(1, 64), (37, 512), (256, 2048)])
+def test_residual_sparsify_local(fmt, sp, m, d):
+    import paper_2607_26515_amd as P
+    log(f"residual_sparsify {fmt} {sp} {m}x{d}")
+    bits = _adversarial_bits(m, d, seed=m * 7 + d)
+    out = P.residual_sparsify(dev_bf16(bits), fmt, sp)
+    o = Q.resq_quantize_residual(fmt, sp, bf16_bits_to_f32(bits))
+    assert_codes_equal(out["qx_codes"], o["qx_codes"], "Q(X) codes")
+    assert_scales_equal(fmt, out["qx_scales"], o["qx_scales"], "Q(X) scales")
+    if sp != "none":
+        assert_codes_equal(out["qr_codes"], o["qr_codes"], "S(Q(dX)) codes")
+        assert_scales_equal(fmt, out["qr_scales"], o["qr_scales"], "Q(dX) scales")
+        assert np.array_equal(host(out["keep_mask"]), pack_bits(o["keep"]))
+
+
+def _linear_case(fmt, sp, m, d, n, seed):
+    import paper_2607_26515_amd as P
+    rx, rw = rng_tree(seed, 2)
+    xb = activations(rx, m, d, 0.01, 50.0)
+    wb = weights(rw, n, d)
+    qw_codes, qw_scales = P.quantize(dev_bf16(wb), fmt, axis=1)
+    y = P.linear_fwd(dev_bf16(xb), qw_codes, qw_scales, fmt, sp)
+    o = Q.resq_forward(fmt, sp, bf16_bits_to_f32(xb), bf16_bits_to_f32(wb))
+    return host(y), o
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("sp", ["none", "identity", "2:4"])
+@pytest.mark.parametrize("m,d,n", [(1, 64, 1), (16, 256, 100), (37, 512, 33), (100, 2048, 300),
+                                   (256, 1024, 640)])
+def test_linear_fwd(fmt, sp, m, d, n):
+    log(f"linear_fwd {fmt} {sp} m={m} d={d} n={n}")
+    y, o = _linear_case(fmt, sp, m, d, n, seed=m + d + n)
+    assert y.shape == (m, n)
+    assert_close(y, o["y64"], f"Y {fmt} {sp}")
+
+
+@pytest.mark.parametrize("sp", ["none", "2:4"])
+@pytest.mark.parametrize("d", [32, 96, 480])
+def test_linear_fwd_mxfp4_half_step(sp, d):
+    """MXFP4 contraction lengths that end in a half (32-element) MFMA step."""
+    log(f"linear_fwd mxfp4 half step {sp} d={d}")
+    y, o = _linear_case("mxfp4", sp, 45, d, 77, seed=d)
+    assert_close(y, o["y64"], "Y")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_linear_fwd_is_deterministic(fmt):
+    import paper_2607_26515_amd as P
+    log(f"determinism {fmt}")
+    rx, rw = rng_tree(99, 2)
+    xb, wb = activations(rx, 130, 2048, 0.01, 50.0), weights(rw, 700, 2048)
+    qc, qs = P.quantize(dev_bf16(wb), fmt, axis=1)
+    x = dev_bf16(xb)
+    y1 = host(P.linear_fwd(x, qc, qs, fmt, "2:4"))
+    y2 = host(P.linear_fwd(x, qc, qs, fmt, "2:4"))
+    assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("m,d,n", [(64, 96, 64), (128, 33, 192), (256, 130, 128), (96, 40, 160)])
+def test_linear_bwd(fmt, m, d, n):
+    import paper_2607_26515_amd as P
+    b = F.block_size(fmt)
+    if m % b or n % b:
+        pytest.skip("m and n must be multiples of the block size")
+    log(f"linear_bwd {fmt} m={m} d={d} n={n}")
+    rx, rw, rg = rng_tree(m + n + d, 3)
+    xb, wb, gb = activations(rx, m, d, 0.01, 50.0), weights(rw, n, d), grad_output(rg, m, n)
+    dx, dw = P.linear_bwd(dev_bf16(gb), dev_bf16(xb), dev_bf16(wb), fmt)
+    o = Q.resq_backward(fmt, bf16_bits_to_f32(gb), bf16_bits_to_f32(xb), bf16_bits_to_f32(wb))
+    assert_close(host(dx), o["dx64"], "dX")
+    assert_close(host(dw), o["dw64"], "dW")
