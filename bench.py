@@ -1,0 +1,289 @@
+#!/usr/bin/env python3
+"""Throughput of the Rollout-ResQ FP4 linear layer on one MI355X.
+
+A step is one rollout forward of every linear projection of one transformer block (the hot
+path of Eq. 4): for each linear, quantize the bf16 activations, form and quantize the
+residual, apply S, and run the FP4 GEMM with the residual term, writing float32 Y.  Q(W) is
+computed once before timing: the weights change once per policy update, not per decode step.
+
+Default workload: the four linears of one Qwen2.5-3B block (qkv 2048->2560, o 2048->2048,
+gate_up 2048->22016, down 11008->2048) at m = 256 tokens, HiF4 with the S_2:4 residual,
+seeded synthetic bf16 activations with 1% outlier channels (x50) and N(0, 0.02) weights.
+
+Inputs are resident in HBM when timing starts.  Weight and activation copies rotate across
+steps so that the 256 MB last-level cache cannot serve a step from the previous one.
+
+Prints one JSON line: the layer's algorithmic TFLOP/s (value), the roofline of the dominant
+kernel (the GEMM, timed with HIP events on its stream through the library's profiler) and
+the oracle timed on this host on a bounded sample of the same workload (cpu_baseline).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+FP4_PEAK_TFLOPS = 10100.0      # MI355X dense MXFP4 / MXFP6 MFMA
+LLC_BYTES = 256 << 20          # MI355X last-level (Infinity) cache
+
+BYTES_PER_ELEM = {"hif4": 36 / 64, "mxfp4": 17 / 32}  # codes + block scales
+
+
+def alg_flops(m, d, n, sp):
+    """Sec. 5.4: 2mdn for the main GEMM; a 50% residual adds mdn, the dense one 2mdn."""
+    extra = {"none": 0, "identity": 2 * m * d * n}.get(sp, m * d * n)
+    return 2 * m * d * n + extra
+
+
+def exec_mfma_flops(m, d, n, fmt, sp):
+    """FP4-rate MFMA work issued by the GEMM (MFMA FLOPs at the FP4/FP6 rate).
+
+    MXFP4 runs one MFMA per K-step for Q(X) and one for the residual; HiF4 runs two
+    (hi/lo E2M3 operands) for each.  The 2:4 / channel / element-wise residuals are dense
+    operands with zeros on gfx950 (no FP4 sparse MFMA); pruned 32x64 blocks are skipped."""
+    per_term = 2 * m * d * n * (2 if fmt == "hif4" else 1)
+    if sp == "none":
+        return per_term
+    if sp == "block32x64_50":
+        return per_term * 1.5
+    return per_term * 2
+
+
+def step_bytes(m, d, n, fmt):
+    """Algorithmic HBM bytes of one linear: X (bf16) in, Q(W) in, Y (fp32) out."""
+    return 2 * m * d + BYTES_PER_ELEM[fmt] * n * d + 4 * m * n
+
+
+def gemm_bytes(m, d, n, fmt, sp):
+    """Algorithmic bytes of the GEMM launch: Q(W), Q(X) and S(Q(dX)) read once, Y written."""
+    terms = 1 if sp == "none" else 2
+    return BYTES_PER_ELEM[fmt] * (n * d + terms * m * d) + 4 * m * n
+
+
+def cpu_baseline(wl, fmt, sp, n_sample, min_seconds):
+    """The oracle, as it stands, on a bounded sample of the same workload (host cores)."""
+    import numpy as np
+    from oracle import formats as F
+    from oracle import resq as Q
+    from synth import bf16_bits_to_f32, workload_tensors
+
+    cores = len(os.sched_getaffinity(0))
+    blas_threads = None
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=None)
+    except Exception:
+        pass
+    prepared = []
+    for lin in wl.linears:
+        xb, wb = workload_tensors(wl, lin)
+        w = bf16_bits_to_f32(wb[:n_sample])
+        what = F.dequantize(fmt, *F.quantize(fmt, w))  # Q(W): once per policy update, untimed
+        prepared.append((bf16_bits_to_f32(xb), what))
+    flops = 0
+    t0 = time.perf_counter()
+    reps = 0
+    while True:
+        for x, what in prepared:
+            out = Q.resq_quantize_residual(fmt, sp, x)
+            y = out["xhat"] @ what.T
+            if sp != "none":
+                y = y + out["srhat"] @ what.T
+            y.astype(np.float32)
+            flops += alg_flops(x.shape[0], x.shape[1], what.shape[0], sp)
+        reps += 1
+        if time.perf_counter() - t0 >= min_seconds:
+            break
+    dt = time.perf_counter() - t0
+    return {
+        "value": flops / dt / 1e12,
+        "unit": "TFLOP/s",
+        "cores": int(blas_threads or cores),
+        "kind": "oracle",
+        "sample": (f"all {wl.m} rows of every linear of {wl.name} against the first {n_sample} "
+                   f"output features of each weight, {reps} repetition(s), {dt:.1f} s; Q(W) "
+                   f"untimed; numpy fp64 (quantizers single-threaded, matmul on "
+                   f"{blas_threads or '?'} BLAS threads of {cores} cores)"),
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="qwen3b_layer_m256")
+    ap.add_argument("--format", default="hif4", choices=["hif4", "mxfp4"])
+    ap.add_argument("--sparsity", default="2:4")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-cols", type=int, default=1024)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only copy a MIB-sized device buffer once (HBM counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              f"(the layer's multi-GPU sharding is described in the design notes, not run).",
+              file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2607_26515_amd as P
+    from synth import WORKLOADS, workload_tensors
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        return 1
+    if args.calibrate_copy:
+        n = args.calibrate_copy << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": n}), flush=True)
+        return 0
+    P.load()  # fails loudly when libresq.so is missing
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    sptr = int(stream.cuda_stream)
+    wl = WORKLOADS[args.workload]
+    fmt, sp = args.format, args.sparsity
+    f, s = P.FORMATS[fmt], P.SPARSITY[sp]
+
+    # ---- inputs, resident in HBM; enough copies to defeat the last-level cache ----
+    per_copy = sum(P.resq_prepared_weights_size(f, l.n, l.d) + 2 * wl.m * l.d for l in wl.linears)
+    copies = int(min(64, max(2, -(-2 * LLC_BYTES // int(per_copy)) + 1)))
+    lin_state = []
+    ws_bytes = max(P.resq_workspace_size(3, f, s, wl.m, l.d, l.n) for l in wl.linears)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    for lin in wl.linears:
+        xb, wb = workload_tensors(wl, lin)
+        x0 = torch.from_numpy(xb.view(np.int16)).to(dev)
+        w0 = torch.from_numpy(wb.view(np.int16)).to(dev)
+        xs, wps = [], []
+        for c in range(copies):
+            xs.append(x0.clone())
+            qc, qs = P.quantize(w0, fmt, axis=1)  # Q(W) and its GEMM layout: once per policy update
+            wps.append(P.prepare_weights(qc, qs, fmt))
+            del qc, qs
+        del w0
+        y = torch.empty((wl.m, lin.n), dtype=torch.float32, device=dev)
+        lin_state.append(dict(lin=lin, xs=xs, wps=wps, y=y,
+                              xp=[int(t.data_ptr()) for t in xs],
+                              wp=[int(t.data_ptr()) for t in wps]))
+    torch.cuda.synchronize()
+
+    lib = P.load()
+
+    def run_step(i):
+        c = i % copies
+        for st in lin_state:
+            lin = st["lin"]
+            rc = lib.resq_linear_fwd_prepared(f, s, st["xp"][c], wl.m, lin.d, lin.d, st["wp"][c],
+                                              lin.n, int(st["y"].data_ptr()), lin.n,
+                                              int(ws.data_ptr()), ws_bytes, sptr)
+            if rc != 0:
+                raise P.ResqError(f"resq_linear_fwd_prepared: {P.resq_last_error()}", rc)
+
+    for i in range(args.warmup):
+        run_step(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        run_step(i)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ms_per_step = dt * 1e3 / args.steps
+
+    flops = sum(alg_flops(wl.m, l.d, l.n, sp) for l in wl.linears)
+    sbytes = sum(step_bytes(wl.m, l.d, l.n, fmt) for l in wl.linears)
+    value = flops * args.steps / dt / 1e12
+
+    # ---- dominant kernel (GEMM): HIP events on its stream via the library profiler ----
+    P.resq_profile_enable(True)
+    P.resq_profile_reset()
+    for i in range(args.steps):
+        run_step(i)
+    torch.cuda.synchronize()
+    prof = {k: P.resq_profile_read(k) for k in ("residual", "pack_hif4", "select", "gemm")}
+    # per-linear breakdown of the same kernels
+    per_linear = {}
+    for st in lin_state:
+        lin = st["lin"]
+        P.resq_profile_reset()
+        for i in range(args.steps):
+            c = i % copies
+            lib.resq_linear_fwd_prepared(f, s, st["xp"][c], wl.m, lin.d, lin.d, st["wp"][c], lin.n,
+                                         int(st["y"].data_ptr()), lin.n, int(ws.data_ptr()),
+                                         ws_bytes, sptr)
+        torch.cuda.synchronize()
+        per_linear[lin.name] = {k: round(P.resq_profile_read(k)[1] / args.steps * 1e3, 2)
+                                for k in ("residual", "pack_hif4", "select", "gemm")}
+    P.resq_profile_enable(False)
+    g_launch, g_ms = prof["gemm"]
+    gemm_ms_step = g_ms / args.steps
+    gbytes = sum(gemm_bytes(wl.m, l.d, l.n, fmt, sp) for l in wl.linears)
+    gexec = sum(exec_mfma_flops(wl.m, l.d, l.n, fmt, sp) for l in wl.linears)
+    achieved = gbytes / (gemm_ms_step * 1e-3) / 1e9
+    mfma_tflops = gexec / (gemm_ms_step * 1e-3) / 1e12
+    roofline = {
+        "bound": "hbm",
+        "achieved": round(achieved, 1),
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBS, 4),
+        "traffic": None,
+        "kernel": "gemm_kernel (4 launches per step, one per linear)",
+        "avg_launch_us": round(g_ms / max(g_launch, 1) * 1e3, 2),
+        "mfma_exec_tflops": round(mfma_tflops, 1),
+        "mfma_exec_frac": round(mfma_tflops / FP4_PEAK_TFLOPS, 4),
+    }
+
+    out = {
+        "metric": "ResQ FP4 linear TFLOP/s + % roofline (HBM GB/s decode, MFMA FP4 prefill)",
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp4",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name,
+            "format": fmt,
+            "sparsity": sp,
+            "m": wl.m,
+            "linears": {l.name: [l.d, l.n] for l in wl.linears},
+            "weight_copies_rotated": copies,
+        },
+        "step_hbm": {
+            "alg_bytes": int(sbytes),
+            "achieved_gbs": round(sbytes / (ms_per_step * 1e-3) / 1e9, 1),
+            "frac": round(sbytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        },
+        "kernel_ms_per_step": {k: round(v[1] / args.steps, 5) for k, v in prof.items()},
+        "per_linear_us": per_linear,
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, fmt, sp, args.cpu_sample_cols, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

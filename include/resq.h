@@ -81,7 +81,8 @@ typedef enum { RESQ_IN_BF16 = 0, RESQ_IN_F32 = 1 } resq_dtype;
 typedef enum {
   RESQ_OP_RESIDUAL_SPARSIFY = 0,
   RESQ_OP_LINEAR_FWD = 1,
-  RESQ_OP_LINEAR_BWD = 2
+  RESQ_OP_LINEAR_BWD = 2,
+  RESQ_OP_LINEAR_FWD_PREPARED = 3
 } resq_op;
 
 /*
@@ -141,6 +142,23 @@ int resq_linear_fwd(int format, int sparsity, const uint16_t* X, int64_t m, int6
                     void* stream);
 
 /*
+ * resq_prepare_weights - lay Q(W) out as the GEMM's weight operand, once per policy update.
+ * qw_codes, qw_scales : Q(W) from resq_quantize(W, axis = 1), W being n x d.
+ * wprep     : output, device buffer of resq_prepared_weights_size(format, n, d) bytes,
+ *             256-byte aligned.  The contents are an internal layout (the MFMA operand
+ *             encoding of the same values: for MXFP4 the same E2M1/E8M0 codes, for HiF4 each
+ *             element k 2^-b as a BF6 E3M2 code next to the block's level-1 scale code).
+ * resq_linear_fwd_prepared is resq_linear_fwd with Q(W) given in this form; results are
+ * identical.  Its workspace size is resq_workspace_size(RESQ_OP_LINEAR_FWD_PREPARED, ...).
+ */
+size_t resq_prepared_weights_size(int format, int64_t n, int64_t d);
+int resq_prepare_weights(int format, const uint8_t* qw_codes, const void* qw_scales, int64_t n,
+                         int64_t d, void* wprep, void* stream);
+int resq_linear_fwd_prepared(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
+                             int64_t ldx, const void* wprep, int64_t n, float* Y, int64_t ldy,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * resq_linear_bwd - the FP4 training-policy backward GEMMs of the linear Y = X W^T:
  *     dX = Q_n(dY) Q_n(W)          (m x d, contraction over n)
  *     dW = Q_m(dY)^T Q_m(X)        (n x d, contraction over m)
@@ -162,6 +180,18 @@ const char* resq_last_error(void);
 
 /* Library version string. */
 const char* resq_version(void);
+
+/*
+ * Kernel timing (diagnostics; off by default).  While enabled, every kernel the library
+ * enqueues is bracketed by two HIP events recorded on the same stream (event objects are
+ * host-side handles; no device memory is allocated).  resq_profile_read synchronizes the
+ * recorded events and returns, for the kernel family `name` ("residual", "quant_rows",
+ * "quant_cols", "pack_hif4", "select", "gemm"), the number of launches and their summed
+ * duration in milliseconds since the last reset.  Returns RESQ_ERR_ARG for an unknown name.
+ */
+int resq_profile_enable(int on);
+void resq_profile_reset(void);
+int resq_profile_read(const char* name, int64_t* launches, double* total_ms);
 
 #ifdef __cplusplus
 }

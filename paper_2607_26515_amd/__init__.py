@@ -11,12 +11,20 @@ from .resq import (  # noqa: F401
     library_path,
     linear_bwd,
     linear_fwd,
+    linear_fwd_prepared,
+    prepare_weights,
     load,
     quantize,
     residual_sparsify,
     resq_last_error,
     resq_linear_bwd,
     resq_linear_fwd,
+    resq_linear_fwd_prepared,
+    resq_prepare_weights,
+    resq_prepared_weights_size,
+    resq_profile_enable,
+    resq_profile_read,
+    resq_profile_reset,
     resq_quantize,
     resq_residual_sparsify,
     resq_version,

@@ -5,10 +5,12 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdarg>
+#include <algorithm>
 #include <cstdio>
 #include <string>
 
 #include "kernels.h"
+#include "profiler.h"
 
 namespace {
 
@@ -77,14 +79,14 @@ struct ActWs {
   double* partials;
   uint8_t* group_bits;
   uint8_t* frag_x;
-  uint8_t* c1_x;
+  uint8_t* fsc_x;
   uint8_t* frag_r;
-  uint8_t* c1_r;
+  uint8_t* fsc_r;
   resq::SelectWs sel;
 };
 
-size_t hif4_frag_bytes(int64_t rows, int64_t K) { return (size_t)((rows + 31) / 32) * (K / 64) * 3072; }
-size_t hif4_c1_bytes(int64_t rows, int64_t K) { return (size_t)((rows + 31) / 32) * (K / 64) * 64; }
+int a_pack_mode(int fmt) { return fmt == RESQ_MXFP4 ? resq::kPackMx : resq::kPackHiA; }
+int b_pack_mode(int fmt) { return fmt == RESQ_MXFP4 ? resq::kPackMx : resq::kPackHiB; }
 
 size_t carve_select(Carver& c, int fmt, int sp, int64_t m, int64_t d, double** partials,
                     resq::SelectWs* sel) {
@@ -100,6 +102,18 @@ size_t carve_select(Carver& c, int fmt, int sp, int64_t m, int64_t d, double** p
   return c.off - start;
 }
 
+// Prepared weights: fragment-major codes, then one scale byte per lane record.
+size_t prepared_bytes(int fmt, int64_t n, int64_t d) {
+  return align256(resq::frag_bytes(b_pack_mode(fmt), n, d)) + align256(resq::frag_scale_bytes(n, d));
+}
+
+void carve_prepared(const void* base, int fmt, int64_t n, int64_t d, const uint8_t** frag,
+                    const uint8_t** fsc) {
+  const uint8_t* b = (const uint8_t*)base;
+  *frag = b;
+  *fsc = b + align256(resq::frag_bytes(b_pack_mode(fmt), n, d));
+}
+
 size_t carve_fwd(void* base, int fmt, int sp, int64_t m, int64_t d, ActWs* w) {
   Carver c(base);
   ActWs t{};
@@ -111,13 +125,11 @@ size_t carve_fwd(void* base, int fmt, int sp, int64_t m, int64_t d, ActWs* w) {
   }
   carve_select(c, fmt, sp, m, d, &t.partials, &t.sel);
   if (sp == RESQ_S_BLOCK32X64_50) t.group_bits = (uint8_t*)c.take((size_t)(((m + 31) / 32) * (d / 64) + 7) / 8);
-  if (fmt == RESQ_HIF4) {
-    t.frag_x = (uint8_t*)c.take(hif4_frag_bytes(m, d));
-    t.c1_x = (uint8_t*)c.take(hif4_c1_bytes(m, d));
-    if (sp != RESQ_S_NONE) {
-      t.frag_r = (uint8_t*)c.take(hif4_frag_bytes(m, d));
-      t.c1_r = (uint8_t*)c.take(hif4_c1_bytes(m, d));
-    }
+  t.frag_x = (uint8_t*)c.take(resq::frag_bytes(a_pack_mode(fmt), m, d));
+  t.fsc_x = (uint8_t*)c.take(resq::frag_scale_bytes(m, d));
+  if (sp != RESQ_S_NONE) {
+    t.frag_r = (uint8_t*)c.take(resq::frag_bytes(a_pack_mode(fmt), m, d));
+    t.fsc_r = (uint8_t*)c.take(resq::frag_scale_bytes(m, d));
   }
   if (w) *w = t;
   return c.off;
@@ -126,7 +138,7 @@ size_t carve_fwd(void* base, int fmt, int sp, int64_t m, int64_t d, ActWs* w) {
 struct BwdWs {
   uint8_t *dyn_codes, *wn_codes, *dym_codes, *xm_codes;
   void *dyn_scales, *wn_scales, *dym_scales, *xm_scales;
-  uint8_t *frag_dyn, *c1_dyn, *frag_dym, *c1_dym;
+  uint8_t *fa, *fa_sc, *fb, *fb_sc;
 };
 
 size_t carve_bwd(void* base, int fmt, int64_t m, int64_t d, int64_t n, BwdWs* w) {
@@ -140,12 +152,15 @@ size_t carve_bwd(void* base, int fmt, int64_t m, int64_t d, int64_t n, BwdWs* w)
   t.dym_scales = c.take(scale_bytes(fmt, n, m));
   t.xm_codes = (uint8_t*)c.take((size_t)d * m / 2);    // [d][m], blocks along m
   t.xm_scales = c.take(scale_bytes(fmt, d, m));
-  if (fmt == RESQ_HIF4) {
-    t.frag_dyn = (uint8_t*)c.take(hif4_frag_bytes(m, n));
-    t.c1_dyn = (uint8_t*)c.take(hif4_c1_bytes(m, n));
-    t.frag_dym = (uint8_t*)c.take(hif4_frag_bytes(n, m));
-    t.c1_dym = (uint8_t*)c.take(hif4_c1_bytes(n, m));
-  }
+  // GEMM operands, reused by the two GEMMs (the stream orders them)
+  const size_t fa = std::max(resq::frag_bytes(a_pack_mode(fmt), m, n), resq::frag_bytes(a_pack_mode(fmt), n, m));
+  const size_t fas = std::max(resq::frag_scale_bytes(m, n), resq::frag_scale_bytes(n, m));
+  const size_t fb = std::max(resq::frag_bytes(b_pack_mode(fmt), d, n), resq::frag_bytes(b_pack_mode(fmt), d, m));
+  const size_t fbs = std::max(resq::frag_scale_bytes(d, n), resq::frag_scale_bytes(d, m));
+  t.fa = (uint8_t*)c.take(fa);
+  t.fa_sc = (uint8_t*)c.take(fas);
+  t.fb = (uint8_t*)c.take(fb);
+  t.fb_sc = (uint8_t*)c.take(fbs);
   if (w) *w = t;
   return c.off;
 }
@@ -176,11 +191,16 @@ int run_activation_side(int format, int sparsity, const uint16_t* X, int64_t m, 
                         int64_t ldx, uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes,
                         void* qr_scales, uint8_t* keep_mask, uint8_t* group_mask,
                         double* partials, const resq::SelectWs& sel, hipStream_t s) {
-  resq::launch_residual(format, resid_mode(sparsity), X, m, d, ldx, qx_codes, qx_scales,
-                        qr_codes, qr_scales, keep_mask, partials, s);
-  if (global_kind(sparsity))
+  {
+    resq::ProfScope prof_(resq::kProfResidual, s);
+    resq::launch_residual(format, resid_mode(sparsity), X, m, d, ldx, qx_codes, qx_scales,
+                          qr_codes, qr_scales, keep_mask, partials, s);
+  }
+  if (global_kind(sparsity)) {
+    resq::ProfScope prof_(resq::kProfSelect, s);
     resq::launch_select(format, sparsity, m, d, qr_codes, qr_scales, partials, keep_mask,
                         group_mask, sel, s);
+  }
   return check_launch("residual/sparsify");
 }
 
@@ -206,9 +226,15 @@ int resq_quantize(int format, const void* x, int in_dtype, int64_t rows, int64_t
   if (!x || !codes || !scales) return fail(RESQ_ERR_ARG, "NULL pointer argument");
   hipStream_t s = (hipStream_t)stream;
   if (axis == 1)
-    resq::launch_quant_rows(format, x, in_dtype == RESQ_IN_F32, rows, cols, ld, codes, scales, s);
+    {
+      resq::ProfScope prof_(resq::kProfQuantRows, s);
+      resq::launch_quant_rows(format, x, in_dtype == RESQ_IN_F32, rows, cols, ld, codes, scales, s);
+    }
   else
-    resq::launch_quant_cols(format, x, in_dtype == RESQ_IN_F32, rows, cols, ld, codes, scales, s);
+    {
+      resq::ProfScope prof_(resq::kProfQuantCols, s);
+      resq::launch_quant_cols(format, x, in_dtype == RESQ_IN_F32, rows, cols, ld, codes, scales, s);
+    }
   return check_launch("resq_quantize");
 }
 
@@ -220,7 +246,9 @@ size_t resq_workspace_size(int op, int format, int sparsity, int64_t m, int64_t 
       carve_select(c, format, sparsity, m, d, nullptr, nullptr);
       return c.off;
     }
-    case RESQ_OP_LINEAR_FWD: return carve_fwd(nullptr, format, sparsity, m, d, nullptr);
+    case RESQ_OP_LINEAR_FWD:
+      return carve_fwd(nullptr, format, sparsity, m, d, nullptr) + prepared_bytes(format, n, d);
+    case RESQ_OP_LINEAR_FWD_PREPARED: return carve_fwd(nullptr, format, sparsity, m, d, nullptr);
     case RESQ_OP_LINEAR_BWD: return carve_bwd(nullptr, format, m, d, n, nullptr);
     default: return 0;
   }
@@ -232,7 +260,6 @@ int resq_residual_sparsify(int format, int sparsity, const uint16_t* X, int64_t 
                            void* workspace, size_t workspace_bytes, void* stream) {
   int rc = check_activation_args(format, sparsity, X, m, d, ldx);
   if (rc != RESQ_OK) return rc;
-  if (sparsity == RESQ_S_2_4 && d % 4 != 0) return fail(RESQ_ERR_SHAPE, "S_2:4 needs d %% 4 == 0");
   if (m == 0 || d == 0) return ok();
   if (!qx_codes || !qx_scales) return fail(RESQ_ERR_ARG, "qx_codes / qx_scales is NULL");
   if (sparsity != RESQ_S_NONE && (!qr_codes || !qr_scales))
@@ -248,47 +275,119 @@ int resq_residual_sparsify(int format, int sparsity, const uint16_t* X, int64_t 
                              (hipStream_t)stream);
 }
 
-int resq_linear_fwd(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
-                    int64_t ldx, const uint8_t* qw_codes, const void* qw_scales, int64_t n,
-                    float* Y, int64_t ldy, void* workspace, size_t workspace_bytes,
-                    void* stream) {
-  int rc = check_activation_args(format, sparsity, X, m, d, ldx);
-  if (rc != RESQ_OK) return rc;
-  if (n < 0) return fail(RESQ_ERR_ARG, "negative n");
-  if (ldy < n) return fail(RESQ_ERR_ARG, "ldy (%lld) < n (%lld)", (long long)ldy, (long long)n);
-  if (m == 0 || n == 0) return ok();
-  if (!Y) return fail(RESQ_ERR_ARG, "Y is NULL");
-  if (d > 0 && (!qw_codes || !qw_scales)) return fail(RESQ_ERR_ARG, "qw_codes / qw_scales is NULL");
-  if ((uintptr_t)qw_codes % 16 != 0 || (format == RESQ_HIF4 && (uintptr_t)qw_scales % 4 != 0))
-    return fail(RESQ_ERR_ARG, "qw_codes must be 16-byte aligned (HiF4 scales 4-byte aligned)");
-  ActWs w{};
-  const size_t need = carve_fwd(workspace, format, sparsity, m, d, &w);
-  rc = check_ws(workspace, workspace_bytes, need);
-  if (rc != RESQ_OK) return rc;
+size_t resq_prepared_weights_size(int format, int64_t n, int64_t d) {
+  if (!valid_format(format) || n < 0 || d < 0 || d % block_of(format) != 0) return 0;
+  return prepared_bytes(format, n, d);
+}
+
+int resq_prepare_weights(int format, const uint8_t* qw_codes, const void* qw_scales, int64_t n,
+                         int64_t d, void* wprep, void* stream) {
+  if (!valid_format(format)) return fail(RESQ_ERR_ARG, "unknown format %d", format);
+  if (n < 0 || d < 0) return fail(RESQ_ERR_ARG, "negative size");
+  if (d % block_of(format) != 0)
+    return fail(RESQ_ERR_SHAPE, "d (%lld) is not a multiple of the block size %lld", (long long)d, (long long)block_of(format));
+  if (n == 0 || d == 0) return ok();
+  if (!qw_codes || !qw_scales || !wprep) return fail(RESQ_ERR_ARG, "NULL pointer argument");
+  if ((uintptr_t)qw_codes % 16 != 0 || (uintptr_t)wprep % 256 != 0 ||
+      (format == RESQ_HIF4 && (uintptr_t)qw_scales % 4 != 0))
+    return fail(RESQ_ERR_ARG, "qw_codes must be 16-byte and wprep 256-byte aligned");
   hipStream_t s = (hipStream_t)stream;
-  rc = run_activation_side(format, sparsity, X, m, d, ldx, w.qx_codes, w.qx_scales, w.qr_codes,
-                           w.qr_scales, nullptr, w.group_bits, w.partials, w.sel, s);
-  if (rc != RESQ_OK) return rc;
+  const uint8_t *frag, *fsc;
+  carve_prepared(wprep, format, n, d, &frag, &fsc);
+  {
+    resq::ProfScope prof_(resq::kProfPack, s);
+    resq::launch_pack(b_pack_mode(format), qw_codes, qw_scales, n, d, (uint8_t*)frag, (uint8_t*)fsc, s);
+  }
+  return check_launch("resq_prepare_weights");
+}
+
+namespace {
+
+int linear_fwd_core(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
+                    int64_t ldx, const void* wprep, int64_t n, float* Y, int64_t ldy,
+                    const ActWs& w, hipStream_t s) {
+  if (global_kind(sparsity)) {
+    // the selection needs the whole K-major Q(dX); pack both operands afterwards
+    int rc = run_activation_side(format, sparsity, X, m, d, ldx, w.qx_codes, w.qx_scales,
+                                 w.qr_codes, w.qr_scales, nullptr, w.group_bits, w.partials,
+                                 w.sel, s);
+    if (rc != RESQ_OK) return rc;
+    resq::ProfScope prof_(resq::kProfPack, s);
+    resq::launch_pack(a_pack_mode(format), w.qx_codes, w.qx_scales, m, d, w.frag_x, w.fsc_x, s);
+    resq::launch_pack(a_pack_mode(format), w.qr_codes, w.qr_scales, m, d, w.frag_r, w.fsc_r, s);
+  } else {
+    // local kinds: the residual pass writes the MFMA fragments directly
+    resq::ProfScope prof_(resq::kProfResidual, s);
+    resq::launch_residual(format, resid_mode(sparsity), X, m, d, ldx, w.frag_x, w.fsc_x,
+                          w.frag_r, w.fsc_r, nullptr, nullptr, s, true);
+  }
   resq::GemmOperands op{};
   op.fmt = format;
   op.M = m; op.N = n; op.K = d;
   op.n_terms = sparsity == RESQ_S_NONE ? 1 : 2;
   op.blockmask = sparsity == RESQ_S_BLOCK32X64_50 ? w.group_bits : nullptr;
-  op.b_codes = qw_codes; op.b_scales = qw_scales;
+  op.a_frag[0] = w.frag_x; op.a_sc[0] = w.fsc_x;
+  op.a_frag[1] = w.frag_r; op.a_sc[1] = w.fsc_r;
+  carve_prepared(wprep, format, n, d, &op.b_frag, &op.b_sc);
   op.Y = Y; op.ldy = ldy;
-  if (format == RESQ_MXFP4) {
-    op.a_codes[0] = w.qx_codes; op.a_scales[0] = (const uint8_t*)w.qx_scales;
-    op.a_codes[1] = w.qr_codes; op.a_scales[1] = (const uint8_t*)w.qr_scales;
-  } else {
-    const int64_t mpad = (m + 31) / 32 * 32;
-    resq::launch_pack_hif4(w.qx_codes, (const uint32_t*)w.qx_scales, m, mpad, d, w.frag_x, w.c1_x, s);
-    if (sparsity != RESQ_S_NONE)
-      resq::launch_pack_hif4(w.qr_codes, (const uint32_t*)w.qr_scales, m, mpad, d, w.frag_r, w.c1_r, s);
-    op.a_frag[0] = w.frag_x; op.a_c1[0] = w.c1_x;
-    op.a_frag[1] = w.frag_r; op.a_c1[1] = w.c1_r;
+  {
+    resq::ProfScope prof_(resq::kProfGemm, s);
+    resq::launch_gemm(op, s);
   }
-  resq::launch_gemm(op, s);
   return check_launch("resq_linear_fwd");
+}
+
+int check_fwd_args(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
+                   int64_t ldx, int64_t n, float* Y, int64_t ldy) {
+  int rc = check_activation_args(format, sparsity, X, m, d, ldx);
+  if (rc != RESQ_OK) return rc;
+  if (n < 0) return fail(RESQ_ERR_ARG, "negative n");
+  if (ldy < n) return fail(RESQ_ERR_ARG, "ldy (%lld) < n (%lld)", (long long)ldy, (long long)n);
+  if (m > 0 && n > 0 && !Y) return fail(RESQ_ERR_ARG, "Y is NULL");
+  return ok();
+}
+
+}  // namespace
+
+int resq_linear_fwd_prepared(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
+                             int64_t ldx, const void* wprep, int64_t n, float* Y, int64_t ldy,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_fwd_args(format, sparsity, X, m, d, ldx, n, Y, ldy);
+  if (rc != RESQ_OK) return rc;
+  if (m == 0 || n == 0) return ok();
+  if (d > 0 && !wprep) return fail(RESQ_ERR_ARG, "wprep is NULL");
+  if ((uintptr_t)wprep % 256 != 0) return fail(RESQ_ERR_ARG, "wprep must be 256-byte aligned");
+  ActWs w{};
+  const size_t need = carve_fwd(workspace, format, sparsity, m, d, &w);
+  rc = check_ws(workspace, workspace_bytes, need);
+  if (rc != RESQ_OK) return rc;
+  return linear_fwd_core(format, sparsity, X, m, d, ldx, wprep, n, Y, ldy, w, (hipStream_t)stream);
+}
+
+int resq_linear_fwd(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
+                    int64_t ldx, const uint8_t* qw_codes, const void* qw_scales, int64_t n,
+                    float* Y, int64_t ldy, void* workspace, size_t workspace_bytes,
+                    void* stream) {
+  int rc = check_fwd_args(format, sparsity, X, m, d, ldx, n, Y, ldy);
+  if (rc != RESQ_OK) return rc;
+  if (m == 0 || n == 0) return ok();
+  if (d > 0 && (!qw_codes || !qw_scales)) return fail(RESQ_ERR_ARG, "qw_codes / qw_scales is NULL");
+  if ((uintptr_t)qw_codes % 16 != 0 || (format == RESQ_HIF4 && (uintptr_t)qw_scales % 4 != 0))
+    return fail(RESQ_ERR_ARG, "qw_codes must be 16-byte aligned (HiF4 scales 4-byte aligned)");
+  ActWs w{};
+  const size_t act = carve_fwd(workspace, format, sparsity, m, d, &w);
+  const size_t need = act + prepared_bytes(format, n, d);
+  rc = check_ws(workspace, workspace_bytes, need);
+  if (rc != RESQ_OK) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  void* wprep = (char*)workspace + act;
+  if (d > 0) {
+    const uint8_t *frag, *fsc;
+    carve_prepared(wprep, format, n, d, &frag, &fsc);
+    resq::ProfScope prof_(resq::kProfPack, s);
+    resq::launch_pack(b_pack_mode(format), qw_codes, qw_scales, n, d, (uint8_t*)frag, (uint8_t*)fsc, s);
+  }
+  return linear_fwd_core(format, sparsity, X, m, d, ldx, wprep, n, Y, ldy, w, s);
 }
 
 int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uint16_t* W,
@@ -307,33 +406,44 @@ int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uin
   if (rc != RESQ_OK) return rc;
   hipStream_t s = (hipStream_t)stream;
   if (dX) {
-    // dX[m][d] = Q_n(dY)[m][n] . Q_n(W)^T[d][n]^T : contraction over n
-    resq::launch_quant_rows(format, dY, false, m, n, n, w.dyn_codes, w.dyn_scales, s);
-    resq::launch_quant_cols(format, W, false, n, d, d, w.wn_codes, w.wn_scales, s);
+    // dX[m][d] = Q_n(dY)[m][n] . (Q_n(W)^T [d][n])^T : contraction over n
+    {
+      resq::ProfScope prof_(resq::kProfQuantRows, s);
+      resq::launch_quant_rows(format, dY, false, m, n, n, w.dyn_codes, w.dyn_scales, s);
+    }
+    {
+      resq::ProfScope prof_(resq::kProfQuantCols, s);
+      resq::launch_quant_cols(format, W, false, n, d, d, w.wn_codes, w.wn_scales, s);
+    }
+    {
+      resq::ProfScope prof_(resq::kProfPack, s);
+      resq::launch_pack(a_pack_mode(format), w.dyn_codes, w.dyn_scales, m, n, w.fa, w.fa_sc, s);
+      resq::launch_pack(b_pack_mode(format), w.wn_codes, w.wn_scales, d, n, w.fb, w.fb_sc, s);
+    }
     resq::GemmOperands op{};
     op.fmt = format; op.M = m; op.N = d; op.K = n; op.n_terms = 1;
-    op.b_codes = w.wn_codes; op.b_scales = w.wn_scales; op.Y = dX; op.ldy = d;
-    if (format == RESQ_MXFP4) {
-      op.a_codes[0] = w.dyn_codes; op.a_scales[0] = (const uint8_t*)w.dyn_scales;
-    } else {
-      resq::launch_pack_hif4(w.dyn_codes, (const uint32_t*)w.dyn_scales, m, (m + 31) / 32 * 32, n, w.frag_dyn, w.c1_dyn, s);
-      op.a_frag[0] = w.frag_dyn; op.a_c1[0] = w.c1_dyn;
-    }
+    op.a_frag[0] = w.fa; op.a_sc[0] = w.fa_sc;
+    op.b_frag = w.fb; op.b_sc = w.fb_sc; op.Y = dX; op.ldy = d;
+    resq::ProfScope prof_(resq::kProfGemm, s);
     resq::launch_gemm(op, s);
   }
   if (dW) {
-    // dW[n][d] = Q_m(dY)^T[n][m] . Q_m(X)^T[d][m]^T : contraction over m
-    resq::launch_quant_cols(format, dY, false, m, n, n, w.dym_codes, w.dym_scales, s);
-    resq::launch_quant_cols(format, X, false, m, d, d, w.xm_codes, w.xm_scales, s);
+    // dW[n][d] = Q_m(dY)^T [n][m] . (Q_m(X)^T [d][m])^T : contraction over m
+    {
+      resq::ProfScope prof_(resq::kProfQuantCols, s);
+      resq::launch_quant_cols(format, dY, false, m, n, n, w.dym_codes, w.dym_scales, s);
+      resq::launch_quant_cols(format, X, false, m, d, d, w.xm_codes, w.xm_scales, s);
+    }
+    {
+      resq::ProfScope prof_(resq::kProfPack, s);
+      resq::launch_pack(a_pack_mode(format), w.dym_codes, w.dym_scales, n, m, w.fa, w.fa_sc, s);
+      resq::launch_pack(b_pack_mode(format), w.xm_codes, w.xm_scales, d, m, w.fb, w.fb_sc, s);
+    }
     resq::GemmOperands op{};
     op.fmt = format; op.M = n; op.N = d; op.K = m; op.n_terms = 1;
-    op.b_codes = w.xm_codes; op.b_scales = w.xm_scales; op.Y = dW; op.ldy = d;
-    if (format == RESQ_MXFP4) {
-      op.a_codes[0] = w.dym_codes; op.a_scales[0] = (const uint8_t*)w.dym_scales;
-    } else {
-      resq::launch_pack_hif4(w.dym_codes, (const uint32_t*)w.dym_scales, n, (n + 31) / 32 * 32, m, w.frag_dym, w.c1_dym, s);
-      op.a_frag[0] = w.frag_dym; op.a_c1[0] = w.c1_dym;
-    }
+    op.a_frag[0] = w.fa; op.a_sc[0] = w.fa_sc;
+    op.b_frag = w.fb; op.b_sc = w.fb_sc; op.Y = dW; op.ldy = d;
+    resq::ProfScope prof_(resq::kProfGemm, s);
     resq::launch_gemm(op, s);
   }
   return check_launch("resq_linear_bwd");

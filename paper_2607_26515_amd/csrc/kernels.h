@@ -25,16 +25,19 @@ void launch_quant_cols(int fmt, const void* x, bool in_f32, int64_t rows, int64_
 
 // Q(X), dX = X - Q(X), Q(dX), and S_2:4 / identity / none.  keep_mask and partials may be
 // null.  partials (double [m][d/B]) receives the exact per-scale-block sums of squares of
-// the dequantized Q(dX) (used by the block selection).
+// the dequantized Q(dX) (used by the block selection).  frag = true writes MFMA fragments
+// (pack.hip layout; codes -> fragment records, scales -> per-lane scale bytes) for the local
+// kinds instead of K-major codes + scales.
 void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
                      uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes, void* qr_scales,
-                     uint8_t* keep_mask, double* partials, hipStream_t s);
+                     uint8_t* keep_mask, double* partials, hipStream_t s, bool frag = false);
 
-// HiF4 K-major codes + metadata -> the split FP6 (E2M3) MFMA operand fragments.
-// rows_pad (multiple of 32) rows are written; rows >= rows are zero.
-void launch_pack_hif4(const uint8_t* codes, const uint32_t* meta, int64_t rows,
-                      int64_t rows_pad, int64_t K, uint8_t* frag, uint8_t* frag_c1,
-                      hipStream_t s);
+// MFMA operand packing (pack.hip): K-major codes + scales -> fragment-major operands.
+enum PackMode { kPackMx = 0, kPackHiA = 1, kPackHiB = 2 };
+size_t frag_bytes(int mode, int64_t rows, int64_t K);
+size_t frag_scale_bytes(int64_t rows, int64_t K);
+void launch_pack(int mode, const uint8_t* codes, const void* scales, int64_t rows, int64_t K,
+                 uint8_t* frag, uint8_t* fscale, hipStream_t s);
 
 // Global selections for the channel, block and unstructured 50% residual patterns.
 // They read the dense Q(dX) (codes + scales), choose the kept set, then zero the pruned
@@ -52,21 +55,17 @@ void launch_select(int fmt, int sparsity, int64_t m, int64_t d, uint8_t* qr_code
                    const void* qr_scales, const double* partials, uint8_t* keep_mask,
                    uint8_t* group_mask, const SelectWs& ws, hipStream_t s);
 
-// FP4 GEMM  Y[M][N] = sum_t A_t[M][K] B[N][K]^T  with A_t = Q(X) and optionally S(Q(dX)).
+// FP4 GEMM  Y[M][N] = sum_t A_t[M][K] B[N][K]^T  with A_t = Q(X) and optionally S(Q(dX)),
+// all operands fragment-major (pack.hip).
 struct GemmOperands {
   int fmt;
   int64_t M, N, K;
-  // MXFP4: K-major codes + E8M0 scales of the A terms (row stride K/2 bytes)
-  const uint8_t* a_codes[2];
-  const uint8_t* a_scales[2];
-  // HiF4: packed split fragments of the A terms and their level-1 codes
   const uint8_t* a_frag[2];
-  const uint8_t* a_c1[2];
+  const uint8_t* a_sc[2];
   int n_terms;               // 1 (Eq. 1) or 2 (with the residual term)
   const uint8_t* blockmask;  // optional: residual kept-block bits, (ceil(M/32), K/64) row-major
-  // B: K-major codes + scales of Q(W) (row stride K/2 bytes)
-  const uint8_t* b_codes;
-  const void* b_scales;
+  const uint8_t* b_frag;
+  const uint8_t* b_sc;
   float* Y;
   int64_t ldy;
 };

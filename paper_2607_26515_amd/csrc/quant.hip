@@ -101,21 +101,72 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(const void* __rest
 }
 
 // ---------------------------------------------------------------------------------------
-// Residual pass of Eq. 2 / Eq. 4: Q(X), dX = X - Q(X) (float32, exact), Q(dX), S_2:4
+// Fragment-major output (see pack.hip): lane record of row `row`, K half of 64-block.
 // ---------------------------------------------------------------------------------------
-template <int FMT, int MODE, bool VEC>
+template <int FMT>
+__device__ __forceinline__ void store_frag(uint8_t* __restrict__ frag, uint8_t* __restrict__ fsc,
+                                           int64_t row, int64_t d, int64_t j4, const Quad& q,
+                                           const uint32_t c[4]) {
+  const int64_t nkb = (d + 63) / 64;
+  const int64_t kb = j4 >> 4;      // 16 lanes of 4 elements per 64-block
+  const int half = (int)((j4 >> 3) & 1);
+  const int64_t f = ((row >> 5) * nkb + kb) * 64 + (row & 31) + 32 * half;
+  if constexpr (FMT == kMX) {
+    *reinterpret_cast<uint16_t*>(frag + f * 16 + (j4 & 7) * 2) = (uint16_t)pack_quad_codes(c);
+    if ((j4 & 7) == 0) fsc[f] = (uint8_t)q.scale;
+    if ((d & 63) != 0 && kb == nkb - 1) {
+      // d % 64 == 32: the last K step has no second half; give it zero codes and a zero
+      // scale byte (never the E8M0 NaN code)
+      *reinterpret_cast<uint16_t*>(frag + (f + 32) * 16 + (j4 & 7) * 2) = 0;
+      if ((j4 & 7) == 0) fsc[f + 32] = 0;
+    }
+  } else {
+    // this lane's 4 elements as 24-bit E2M3 hi / lo runs; 8 lanes make one 48-byte record
+    uint32_t h = 0, l = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      uint32_t hk, lk;
+      hif4_split_e2m3(c[k], q.c1, q.b, hk, lk);
+      h |= hk << (6 * k);
+      l |= lk << (6 * k);
+    }
+    const int lane = __lane_id();
+    const int base = lane & ~7, qi = lane & 7;
+    const int qq = qi < 6 ? qi : 5;
+    const int L = (32 * qq) / 24, o = 32 * qq - 24 * L;  // dword qq = bits [32qq, 32qq+32)
+    const uint32_t h0 = __shfl(h, base + L, 64), h1 = __shfl(h, base + L + 1, 64);
+    const uint32_t l0 = __shfl(l, base + L, 64), l1 = __shfl(l, base + L + 1, 64);
+    if (qi < 6) {
+      uint32_t* rec = reinterpret_cast<uint32_t*>(frag + f * 48);
+      rec[qi] = (h0 >> o) | (h1 << (24 - o));
+      rec[6 + qi] = (l0 >> o) | (l1 << (24 - o));
+    }
+    if (qi == 0) fsc[f] = (uint8_t)q.c1;
+  }
+}
+
+// ---------------------------------------------------------------------------------------
+// Residual pass of Eq. 2 / Eq. 4: Q(X), dX = X - Q(X) (float32, exact), Q(dX), S_2:4.
+// FRAG: write MFMA fragments (rows m..m_rows-1 are zero padding of the last row tile)
+// instead of K-major codes + scales.
+// ---------------------------------------------------------------------------------------
+template <int FMT, int MODE, bool VEC, bool FRAG>
 __global__ __launch_bounds__(kThreads) void residual_kernel(
-    const uint16_t* __restrict__ X, int64_t m, int64_t d, int64_t ldx,
+    const uint16_t* __restrict__ X, int64_t m, int64_t m_rows, int64_t d, int64_t ldx,
     uint8_t* __restrict__ qx_codes, void* __restrict__ qx_scales, uint8_t* __restrict__ qr_codes,
     void* __restrict__ qr_scales, uint8_t* __restrict__ keep_mask, double* __restrict__ partials) {
   const int64_t j4 = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (4 * j4 >= d) return;
-  for (int64_t row = blockIdx.y; row < m; row += gridDim.y) {
-    float v[4];
-    load4<false, VEC>(X, row * ldx + 4 * j4, v);
+  for (int64_t row = blockIdx.y; row < m_rows; row += gridDim.y) {
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    if (row < m) load4<false, VEC>(X, row * ldx + 4 * j4, v);
     const Quad qx = quantize_quad<FMT>(v);
-    *reinterpret_cast<uint16_t*>(qx_codes + row * (d / 2) + 2 * j4) = (uint16_t)pack_quad_codes(qx.code);
-    store_scale<FMT>(qx_scales, row, d, j4, qx.scale);
+    if constexpr (FRAG) {
+      store_frag<FMT>(qx_codes, reinterpret_cast<uint8_t*>(qx_scales), row, d, j4, qx, qx.code);
+    } else {
+      *reinterpret_cast<uint16_t*>(qx_codes + row * (d / 2) + 2 * j4) = (uint16_t)pack_quad_codes(qx.code);
+      store_scale<FMT>(qx_scales, row, d, j4, qx.scale);
+    }
     if constexpr (MODE != kResidNone) {
       float r[4];
 #pragma unroll
@@ -126,70 +177,27 @@ __global__ __launch_bounds__(kThreads) void residual_kernel(
       uint32_t c[4];
 #pragma unroll
       for (int k = 0; k < 4; ++k) c[k] = ((keep >> k) & 1u) ? qr.code[k] : 0u;
-      *reinterpret_cast<uint16_t*>(qr_codes + row * (d / 2) + 2 * j4) = (uint16_t)pack_quad_codes(c);
-      store_scale<FMT>(qr_scales, row, d, j4, qr.scale);
-      if (keep_mask != nullptr && MODE != kResidDense) {
-        const uint32_t other = __shfl_xor(keep, 1, 64);
-        if ((threadIdx.x & 1) == 0) keep_mask[row * (d / 8) + j4 / 2] = (uint8_t)(keep | (other << 4));
-      }
-      if (partials != nullptr) {
-        // exact per-scale-block sum of squares (shared power-of-two factor, small integers)
-        double s = 0.0;
+      if constexpr (FRAG) {
+        store_frag<FMT>(qr_codes, reinterpret_cast<uint8_t*>(qr_scales), row, d, j4, qr, c);
+      } else {
+        *reinterpret_cast<uint16_t*>(qr_codes + row * (d / 2) + 2 * j4) = (uint16_t)pack_quad_codes(c);
+        store_scale<FMT>(qr_scales, row, d, j4, qr.scale);
+        if (keep_mask != nullptr && MODE != kResidDense) {
+          const uint32_t other = __shfl_xor(keep, 1, 64);
+          if ((threadIdx.x & 1) == 0) keep_mask[row * (d / 8) + j4 / 2] = (uint8_t)(keep | (other << 4));
+        }
+        if (partials != nullptr) {
+          // exact per-scale-block sum of squares (shared power-of-two factor, small integers)
+          double sq = 0.0;
 #pragma unroll
-        for (int k = 0; k < 4; ++k) s += (double)qr.val[k] * (double)qr.val[k];
-        constexpr int G = (FMT == kMX) ? 8 : 16;
-        s = group_sum<G>(s);
-        if ((threadIdx.x & (G - 1)) == 0) partials[row * (d / (4 * G)) + j4 / G] = s;
-      }
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------------------
-// HiF4 -> split E2M3 MFMA fragments.  Fragment (t, kb, term) holds, for lane l (row
-// 32t + l%32, K half l/32 of 64-block kb), 32 six-bit codes in 24 bytes; term 0 = hi, 1 = lo.
-// One thread per (row tile, k-block, lane).
-// ---------------------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void pack_hif4_kernel(
-    const uint8_t* __restrict__ codes, const uint32_t* __restrict__ meta, int64_t rows,
-    int64_t rows_pad, int64_t K, uint8_t* __restrict__ frag, uint8_t* __restrict__ frag_c1) {
-  const int64_t nkb = K / 64;
-  const int64_t gid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  const int64_t total = (rows_pad / 32) * nkb * 64;
-  if (gid >= total) return;
-  const int l = (int)(gid & 63);
-  const int64_t tk = gid >> 6;  // t * nkb + kb
-  const int64_t t = tk / nkb, kb = tk % nkb;
-  const int64_t row = t * 32 + (l & 31);
-  const int half = l >> 5;
-  uint32_t hi[6] = {0, 0, 0, 0, 0, 0}, lo[6] = {0, 0, 0, 0, 0, 0};
-  uint32_t c1 = 0;
-  if (row < rows) {
-    const uint32_t mt = meta[row * nkb + kb];
-    c1 = mt & 0xFFu;
-    const uint4 cw = *reinterpret_cast<const uint4*>(codes + row * (K / 2) + kb * 32 + half * 16);
-    const uint32_t words[4] = {cw.x, cw.y, cw.z, cw.w};
-#pragma unroll
-    for (int i = 0; i < 32; ++i) {
-      const uint32_t code = (words[i >> 3] >> (4 * (i & 7))) & 15u;
-      const int h = half * 8 + (i >> 2);  // level-3 group within the 64-block
-      const int b = (int)((mt >> (8 + (h >> 1))) & 1u) + (int)((mt >> (16 + h)) & 1u);
-      uint32_t ch, cl;
-      hif4_split_e2m3(code, (int)c1, b, ch, cl);
-      const int bit = 6 * i;
-      hi[bit >> 5] |= ch << (bit & 31);
-      lo[bit >> 5] |= cl << (bit & 31);
-      if ((bit & 31) > 26) {  // field straddles two words
-        hi[(bit >> 5) + 1] |= ch >> (32 - (bit & 31));
-        lo[(bit >> 5) + 1] |= cl >> (32 - (bit & 31));
+          for (int k = 0; k < 4; ++k) sq += (double)qr.val[k] * (double)qr.val[k];
+          constexpr int G = (FMT == kMX) ? 8 : 16;
+          sq = group_sum<G>(sq);
+          if ((threadIdx.x & (G - 1)) == 0) partials[row * (d / (4 * G)) + j4 / G] = sq;
+        }
       }
     }
   }
-  uint32_t* ph = reinterpret_cast<uint32_t*>(frag + ((tk * 2 + 0) * 64 + l) * 24);
-  uint32_t* pl = reinterpret_cast<uint32_t*>(frag + ((tk * 2 + 1) * 64 + l) * 24);
-#pragma unroll
-  for (int w = 0; w < 6; ++w) { ph[w] = hi[w]; pl[w] = lo[w]; }
-  frag_c1[tk * 64 + l] = (uint8_t)c1;
 }
 
 inline unsigned grid_rows(int64_t rows) { return (unsigned)(rows < 65535 ? rows : 65535); }
@@ -225,31 +233,25 @@ void launch_quant_cols(int fmt, const void* x, bool in_f32, int64_t rows, int64_
 
 void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
                      uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes, void* qr_scales,
-                     uint8_t* keep_mask, double* partials, hipStream_t s) {
+                     uint8_t* keep_mask, double* partials, hipStream_t s, bool frag) {
   if (m == 0 || d == 0) return;
-  const dim3 grid((unsigned)((d / 4 + kThreads - 1) / kThreads), grid_rows(m));
+  const int64_t m_rows = frag ? (m + 31) / 32 * 32 : m;
+  const dim3 grid((unsigned)((d / 4 + kThreads - 1) / kThreads), grid_rows(m_rows));
   const bool vec = ((uintptr_t)X % 8 == 0) && (ldx % 4 == 0);
-#define RESQ_RK(F, M, V) hipLaunchKernelGGL((residual_kernel<F, M, V>), grid, dim3(kThreads), 0, s, X, m, d, ldx, qx_codes, qx_scales, qr_codes, qr_scales, keep_mask, partials)
-#define RESQ_RK_MODE(F, V)                                  \
-  switch (mode) {                                          \
-    case kResidNone: RESQ_RK(F, kResidNone, V); break;     \
-    case kResidIdentity: RESQ_RK(F, kResidIdentity, V); break; \
-    case kResid24: RESQ_RK(F, kResid24, V); break;         \
-    default: RESQ_RK(F, kResidDense, V); break;            \
+#define RESQ_RK(F, M, V, G) hipLaunchKernelGGL((residual_kernel<F, M, V, G>), grid, dim3(kThreads), 0, s, X, m, m_rows, d, ldx, qx_codes, qx_scales, qr_codes, qr_scales, keep_mask, partials)
+#define RESQ_RK_MODE(F, V, G)                                       \
+  switch (mode) {                                                   \
+    case kResidNone: RESQ_RK(F, kResidNone, V, G); break;           \
+    case kResidIdentity: RESQ_RK(F, kResidIdentity, V, G); break;   \
+    case kResid24: RESQ_RK(F, kResid24, V, G); break;               \
+    default: RESQ_RK(F, kResidDense, V, false); break;              \
   }
-  if (fmt == kMX) { if (vec) { RESQ_RK_MODE(kMX, true) } else { RESQ_RK_MODE(kMX, false) } }
-  else { if (vec) { RESQ_RK_MODE(kHI, true) } else { RESQ_RK_MODE(kHI, false) } }
+#define RESQ_RK_VEC(F, G) if (vec) { RESQ_RK_MODE(F, true, G) } else { RESQ_RK_MODE(F, false, G) }
+  if (fmt == kMX) { if (frag) { RESQ_RK_VEC(kMX, true) } else { RESQ_RK_VEC(kMX, false) } }
+  else { if (frag) { RESQ_RK_VEC(kHI, true) } else { RESQ_RK_VEC(kHI, false) } }
+#undef RESQ_RK_VEC
 #undef RESQ_RK_MODE
 #undef RESQ_RK
-}
-
-void launch_pack_hif4(const uint8_t* codes, const uint32_t* meta, int64_t rows,
-                      int64_t rows_pad, int64_t K, uint8_t* frag, uint8_t* frag_c1,
-                      hipStream_t s) {
-  const int64_t total = (rows_pad / 32) * (K / 64) * 64;
-  if (total == 0) return;
-  hipLaunchKernelGGL(pack_hif4_kernel, dim3((unsigned)((total + kThreads - 1) / kThreads)),
-                     dim3(kThreads), 0, s, codes, meta, rows, rows_pad, K, frag, frag_c1);
 }
 
 }  // namespace resq

@@ -30,10 +30,12 @@ SPARSITY = {"none": S_NONE, "identity": S_IDENTITY, "2:4": S_2_4, "channel50": S
             "block32x64_50": S_BLOCK32X64_50, "unstructured50": S_UNSTRUCT50}
 OK, ERR_ARG, ERR_SHAPE, ERR_UNSUPPORTED, ERR_HIP, ERR_WORKSPACE = 0, -1, -2, -3, -4, -5
 IN_BF16, IN_F32 = 0, 1
-OP_RESIDUAL_SPARSIFY, OP_LINEAR_FWD, OP_LINEAR_BWD = 0, 1, 2
+OP_RESIDUAL_SPARSIFY, OP_LINEAR_FWD, OP_LINEAR_BWD, OP_LINEAR_FWD_PREPARED = 0, 1, 2, 3
 
 EXPORTED = ("resq_quantize", "resq_residual_sparsify", "resq_linear_fwd", "resq_linear_bwd",
-            "resq_workspace_size", "resq_last_error", "resq_version")
+            "resq_workspace_size", "resq_last_error", "resq_version", "resq_profile_enable",
+            "resq_profile_reset", "resq_profile_read", "resq_prepared_weights_size",
+            "resq_prepare_weights", "resq_linear_fwd_prepared")
 
 
 class ResqError(RuntimeError):
@@ -60,9 +62,21 @@ def load() -> ctypes.CDLL:
     lib.resq_linear_fwd.argtypes = [i32, i32, vp, i64, i64, i64, vp, vp, i64, vp, i64, vp, sz, vp]
     lib.resq_linear_bwd.argtypes = [i32, vp, vp, vp, i64, i64, i64, vp, vp, vp, sz, vp]
     lib.resq_workspace_size.argtypes = [i32, i32, i32, i64, i64, i64]
+    lib.resq_prepared_weights_size.argtypes = [i32, i64, i64]
+    lib.resq_prepared_weights_size.restype = sz
+    lib.resq_prepare_weights.argtypes = [i32, vp, vp, i64, i64, vp, vp]
+    lib.resq_prepare_weights.restype = i32
+    lib.resq_linear_fwd_prepared.argtypes = [i32, i32, vp, i64, i64, i64, vp, i64, vp, i64, vp, sz, vp]
+    lib.resq_linear_fwd_prepared.restype = i32
     for f in ("resq_quantize", "resq_residual_sparsify", "resq_linear_fwd", "resq_linear_bwd"):
         getattr(lib, f).restype = i32
     lib.resq_workspace_size.restype = sz
+    lib.resq_profile_enable.argtypes = [i32]
+    lib.resq_profile_enable.restype = i32
+    lib.resq_profile_reset.argtypes = []
+    lib.resq_profile_reset.restype = None
+    lib.resq_profile_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double)]
+    lib.resq_profile_read.restype = i32
     lib.resq_last_error.restype = ctypes.c_char_p
     lib.resq_version.restype = ctypes.c_char_p
     _lib = lib
@@ -93,6 +107,20 @@ def resq_linear_bwd(fmt, dY, X, W, m, d, n, dX, dW, workspace, workspace_bytes, 
     return load().resq_linear_bwd(fmt, dY, X, W, m, d, n, dX, dW, workspace, workspace_bytes, stream)
 
 
+def resq_prepared_weights_size(fmt, n, d) -> int:
+    return load().resq_prepared_weights_size(fmt, n, d)
+
+
+def resq_prepare_weights(fmt, qw_codes, qw_scales, n, d, wprep, stream=0) -> int:
+    return load().resq_prepare_weights(fmt, qw_codes, qw_scales, n, d, wprep, stream)
+
+
+def resq_linear_fwd_prepared(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy, workspace,
+                             workspace_bytes, stream=0) -> int:
+    return load().resq_linear_fwd_prepared(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy,
+                                           workspace, workspace_bytes, stream)
+
+
 def resq_workspace_size(op, fmt, sparsity, m, d, n) -> int:
     return load().resq_workspace_size(op, fmt, sparsity, m, d, n)
 
@@ -103,6 +131,23 @@ def resq_last_error() -> str:
 
 def resq_version() -> str:
     return load().resq_version().decode()
+
+
+def resq_profile_enable(on: bool) -> int:
+    return load().resq_profile_enable(1 if on else 0)
+
+
+def resq_profile_reset() -> None:
+    load().resq_profile_reset()
+
+
+def resq_profile_read(name: str):
+    """(launches, total milliseconds) of a kernel family since the last reset."""
+    n = ctypes.c_int64(0)
+    ms = ctypes.c_double(0.0)
+    rc = load().resq_profile_read(name.encode(), ctypes.byref(n), ctypes.byref(ms))
+    _check(rc, "resq_profile_read")
+    return n.value, ms.value
 
 
 # ------------------------------------------------------------------------------------------
@@ -211,6 +256,34 @@ def linear_fwd(x, qw_codes, qw_scales, fmt, sparsity, y=None, ws=None, stream=No
     rc = resq_linear_fwd(f, sp, _p(x), m, d, x.stride(0), _p(qw_codes), _p(qw_scales), n, _p(y),
                          y.stride(0), _p(buf), nb, _stream(stream))
     _check(rc, "resq_linear_fwd")
+    return y
+
+
+def prepare_weights(qw_codes, qw_scales, fmt, stream=None):
+    """Q(W) (K-major codes + scales) -> the GEMM's prepared weight operand (device tensor)."""
+    import torch
+    n, d = qw_codes.shape[0], qw_codes.shape[1] * 2
+    f = _fmt(fmt)
+    nb = resq_prepared_weights_size(f, n, d)
+    wprep = torch.empty(max(nb, 1), dtype=torch.uint8, device=qw_codes.device)
+    rc = resq_prepare_weights(f, _p(qw_codes), _p(qw_scales), n, d, _p(wprep), _stream(stream))
+    _check(rc, "resq_prepare_weights")
+    return wprep
+
+
+def linear_fwd_prepared(x, wprep, n, fmt, sparsity, y=None, ws=None, stream=None):
+    """Y = Q(X) Q(W)^T + S(Q(X - Q(X))) Q(W)^T with Q(W) in prepared form (float32)."""
+    import torch
+    m, d = x.shape
+    f, sp = _fmt(fmt), _sp(sparsity)
+    if y is None:
+        y = torch.empty((m, n), dtype=torch.float32, device=x.device)
+    if ws is None:
+        ws = workspace(OP_LINEAR_FWD_PREPARED, f, sp, m, d, n, x.device)
+    buf, nb = ws
+    rc = resq_linear_fwd_prepared(f, sp, _p(x), m, d, x.stride(0), _p(wprep), n, _p(y), y.stride(0),
+                                  _p(buf), nb, _stream(stream))
+    _check(rc, "resq_linear_fwd_prepared")
     return y
 
 

@@ -113,6 +113,26 @@ def test_linear_fwd(fmt, sp, m, d, n):
     assert_close(y, o["y64"], f"Y {fmt} {sp}")
 
 
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("sp", ["none", "2:4"])
+@pytest.mark.parametrize("m,d,n", [(16, 2048, 2048), (256, 2048, 2560), (256, 11008, 2048), (37, 512, 100)])
+def test_linear_fwd_prepared_matches_unprepared(fmt, sp, m, d, n):
+    """Prepared weights give bit-identical Y to the K-major Q(W) path, and match the oracle."""
+    import paper_2607_26515_amd as P
+    log(f"linear_fwd_prepared {fmt} {sp} m={m} d={d} n={n}")
+    rx, rw = rng_tree(m * 3 + n, 2)
+    xb, wb = activations(rx, m, d, 0.01, 50.0), weights(rw, n, d)
+    qc, qs = P.quantize(dev_bf16(wb), fmt, axis=1)
+    x = dev_bf16(xb)
+    y1 = host(P.linear_fwd(x, qc, qs, fmt, sp))
+    wprep = P.prepare_weights(qc, qs, fmt)
+    y2 = host(P.linear_fwd_prepared(x, wprep, n, fmt, sp))
+    assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
+    if m * d * n <= 2**31:
+        o = Q.resq_forward(fmt, sp, bf16_bits_to_f32(xb), bf16_bits_to_f32(wb))
+        assert_close(y2, o["y64"], "Y")
+
+
 @pytest.mark.parametrize("sp", ["none", "2:4"])
 @pytest.mark.parametrize("d", [32, 96, 480])
 def test_linear_fwd_mxfp4_half_step(sp, d):
