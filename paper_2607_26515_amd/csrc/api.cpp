@@ -77,7 +77,6 @@ struct ActWs {
   uint8_t* qr_codes;
   void* qr_scales;
   double* partials;
-  uint8_t* group_bits;
   uint8_t* frag_x;
   uint8_t* fsc_x;
   uint8_t* frag_r;
@@ -124,7 +123,6 @@ size_t carve_fwd(void* base, int fmt, int sp, int64_t m, int64_t d, ActWs* w) {
     t.qr_scales = c.take(scale_bytes(fmt, m, d));
   }
   carve_select(c, fmt, sp, m, d, &t.partials, &t.sel);
-  if (sp == RESQ_S_BLOCK32X64_50) t.group_bits = (uint8_t*)c.take((size_t)(((m + 31) / 32) * (d / 64) + 7) / 8);
   t.frag_x = (uint8_t*)c.take(resq::frag_bytes(a_pack_mode(fmt), m, d));
   t.fsc_x = (uint8_t*)c.take(resq::frag_scale_bytes(m, d));
   if (sp != RESQ_S_NONE) {
@@ -183,6 +181,8 @@ int check_activation_args(int format, int sparsity, const void* X, int64_t m, in
     return fail(RESQ_ERR_SHAPE, "d (%lld) is not a multiple of the block size %lld", (long long)d, (long long)block_of(format));
   if (sparsity == RESQ_S_BLOCK32X64_50 && d % 64 != 0)
     return fail(RESQ_ERR_SHAPE, "32x64 block sparsity needs d %% 64 == 0 (d=%lld)", (long long)d);
+  if (sparsity == RESQ_S_UNSTRUCT50 && m * d > ((int64_t)1 << 31))
+    return fail(RESQ_ERR_UNSUPPORTED, "element-wise 50%% selection supports m*d <= 2^31 (m*d=%lld)", (long long)(m * d));
   if (m > 0 && d > 0 && X == nullptr) return fail(RESQ_ERR_ARG, "X is NULL");
   return ok();
 }
@@ -264,6 +264,9 @@ int resq_residual_sparsify(int format, int sparsity, const uint16_t* X, int64_t 
   if (!qx_codes || !qx_scales) return fail(RESQ_ERR_ARG, "qx_codes / qx_scales is NULL");
   if (sparsity != RESQ_S_NONE && (!qr_codes || !qr_scales))
     return fail(RESQ_ERR_ARG, "qr_codes / qr_scales is NULL");
+  if ((uintptr_t)qx_codes % 16 || (uintptr_t)qr_codes % 16 || (uintptr_t)keep_mask % 4 ||
+      (format == RESQ_HIF4 && ((uintptr_t)qx_scales % 4 || (uintptr_t)qr_scales % 4)))
+    return fail(RESQ_ERR_ARG, "codes must be 16-byte, keep_mask and HiF4 scales 4-byte aligned");
   Carver c(workspace);
   double* partials = nullptr;
   resq::SelectWs sel{};
@@ -309,7 +312,7 @@ int linear_fwd_core(int format, int sparsity, const uint16_t* X, int64_t m, int6
   if (global_kind(sparsity)) {
     // the selection needs the whole K-major Q(dX); pack both operands afterwards
     int rc = run_activation_side(format, sparsity, X, m, d, ldx, w.qx_codes, w.qx_scales,
-                                 w.qr_codes, w.qr_scales, nullptr, w.group_bits, w.partials,
+                                 w.qr_codes, w.qr_scales, nullptr, nullptr, w.partials,
                                  w.sel, s);
     if (rc != RESQ_OK) return rc;
     resq::ProfScope prof_(resq::kProfPack, s);
@@ -325,7 +328,7 @@ int linear_fwd_core(int format, int sparsity, const uint16_t* X, int64_t m, int6
   op.fmt = format;
   op.M = m; op.N = n; op.K = d;
   op.n_terms = sparsity == RESQ_S_NONE ? 1 : 2;
-  op.blockmask = sparsity == RESQ_S_BLOCK32X64_50 ? w.group_bits : nullptr;
+  op.blockmask = sparsity == RESQ_S_BLOCK32X64_50 ? w.sel.group_bits : nullptr;
   op.a_frag[0] = w.frag_x; op.a_sc[0] = w.fsc_x;
   op.a_frag[1] = w.frag_r; op.a_sc[1] = w.fsc_r;
   carve_prepared(wprep, format, n, d, &op.b_frag, &op.b_sc);
