@@ -347,6 +347,9 @@ int check_fwd_args(int format, int sparsity, const uint16_t* X, int64_t m, int64
   if (n < 0) return fail(RESQ_ERR_ARG, "negative n");
   if (ldy < n) return fail(RESQ_ERR_ARG, "ldy (%lld) < n (%lld)", (long long)ldy, (long long)n);
   if (m > 0 && n > 0 && !Y) return fail(RESQ_ERR_ARG, "Y is NULL");
+  if (!resq::gemm_supported(format, m, n, d, sparsity == RESQ_S_BLOCK32X64_50))
+    return fail(RESQ_ERR_UNSUPPORTED, "GEMM operands too large for 32-bit offsets (m=%lld, d=%lld, n=%lld)",
+                (long long)m, (long long)d, (long long)n);
   return ok();
 }
 
@@ -403,6 +406,9 @@ int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uin
   if (dW && m % B != 0) return fail(RESQ_ERR_SHAPE, "dW needs m (%lld) %% %lld == 0", (long long)m, (long long)B);
   if (m == 0 || d == 0 || n == 0) return ok();
   if (!dY || (dX && !W) || (dW && !X)) return fail(RESQ_ERR_ARG, "NULL input pointer");
+  if ((dX && !resq::gemm_supported(format, m, d, n, false)) ||
+      (dW && !resq::gemm_supported(format, n, d, m, false)))
+    return fail(RESQ_ERR_UNSUPPORTED, "GEMM operands too large for 32-bit offsets");
   BwdWs w{};
   const size_t need = carve_bwd(workspace, format, m, d, n, &w);
   int rc = check_ws(workspace, workspace_bytes, need);

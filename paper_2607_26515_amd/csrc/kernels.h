@@ -70,5 +70,8 @@ struct GemmOperands {
   int64_t ldy;
 };
 void launch_gemm(const GemmOperands& op, hipStream_t s);
+// Whether launch_gemm handles these sizes (32-bit operand offsets; the block-skip mask of a
+// row tile fits the kernel's LDS table).
+bool gemm_supported(int fmt, int64_t M, int64_t N, int64_t K, bool block_skip);
 
 }  // namespace resq
