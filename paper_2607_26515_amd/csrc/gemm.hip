@@ -389,14 +389,20 @@ void launch_cfg(GemmParams p, int n_terms, hipStream_t s) {
     hipLaunchKernelGGL((gemm_kernel<FMT, WM, WN, TM, TN, 1, NS, false>), grid, block, G1::lds_bytes(false), s, p);
 }
 
+// Tile choice (measured on MI355X): a CU holds one or two workgroups (LDS-bound), so the
+// workgroup count decides how many rounds the grid takes.
+//  - grids too small for 128-row tiles to fill the chip: 64 x 64 tiles, deep pipeline;
+//  - M >= 512 (7B decode and prefill): 128 x 256 tiles (fewest A re-reads per byte of B);
+//  - otherwise (M = 256 decode): 128 x 192 tiles, one round on 256 CUs.
 template <int FMT>
 void launch_fmt(const GemmParams& p, int n_terms, hipStream_t s) {
   auto wgs = [&](int bm, int bn) { return ((p.mt_tiles + bm - 1) / bm) * ((p.nt_tiles + bn - 1) / bn); };
-  // 128 x 128 tiles when they give about one workgroup per CU, else 64 x 64.
-  if (wgs(4, 4) >= 240)
-    launch_cfg<FMT, 2, 2, 2, 2, FMT == 0 ? 8 : 4>(p, n_terms, s);
-  else
+  if (wgs(4, 4) < 240)
     launch_cfg<FMT, 2, 2, 1, 1, FMT == 0 ? 8 : 6>(p, n_terms, s);
+  else if (p.M >= 512)
+    launch_cfg<FMT, 2, 2, 2, 4, FMT == 0 ? 4 : 2>(p, n_terms, s);
+  else
+    launch_cfg<FMT, 2, 2, 2, 3, FMT == 0 ? 4 : 2>(p, n_terms, s);
 }
 
 }  // namespace
