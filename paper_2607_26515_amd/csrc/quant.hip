@@ -101,56 +101,10 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(const void* __rest
 }
 
 // ---------------------------------------------------------------------------------------
-// Fragment-major output (see pack.hip): lane record of row `row`, K half of 64-block.
+// Residual pass of Eq. 2 / Eq. 4 with K-major output: Q(X), dX = X - Q(X) (float32,
+// exact), Q(dX), and S_2:4 / identity / the dense Q(dX) a global selection prunes later.
 // ---------------------------------------------------------------------------------------
-template <int FMT>
-__device__ __forceinline__ void store_frag(uint8_t* __restrict__ frag, uint8_t* __restrict__ fsc,
-                                           int64_t row, int64_t d, int64_t j4, const Quad& q,
-                                           const uint32_t c[4]) {
-  const int64_t nkb = (d + 63) / 64;
-  const int64_t kb = j4 >> 4;      // 16 lanes of 4 elements per 64-block
-  const int half = (int)((j4 >> 3) & 1);
-  const int64_t f = ((row >> 5) * nkb + kb) * 64 + (row & 31) + 32 * half;
-  if constexpr (FMT == kMX) {
-    *reinterpret_cast<uint16_t*>(frag + f * 16 + (j4 & 7) * 2) = (uint16_t)pack_quad_codes(c);
-    if ((j4 & 7) == 0) fsc[f] = (uint8_t)q.scale;
-    if ((d & 63) != 0 && kb == nkb - 1) {
-      // d % 64 == 32: the last K step has no second half; give it zero codes and a zero
-      // scale byte (never the E8M0 NaN code)
-      *reinterpret_cast<uint16_t*>(frag + (f + 32) * 16 + (j4 & 7) * 2) = 0;
-      if ((j4 & 7) == 0) fsc[f + 32] = 0;
-    }
-  } else {
-    // this lane's 4 elements as 24-bit E2M3 hi / lo runs; 8 lanes make one 48-byte record
-    uint32_t h = 0, l = 0;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      uint32_t hk, lk;
-      hif4_split_e2m3(c[k], q.c1, q.b, hk, lk);
-      h |= hk << (6 * k);
-      l |= lk << (6 * k);
-    }
-    const int lane = __lane_id();
-    const int base = lane & ~7, qi = lane & 7;
-    const int qq = qi < 6 ? qi : 5;
-    const int L = (32 * qq) / 24, o = 32 * qq - 24 * L;  // dword qq = bits [32qq, 32qq+32)
-    const uint32_t h0 = __shfl(h, base + L, 64), h1 = __shfl(h, base + L + 1, 64);
-    const uint32_t l0 = __shfl(l, base + L, 64), l1 = __shfl(l, base + L + 1, 64);
-    if (qi < 6) {
-      uint32_t* rec = reinterpret_cast<uint32_t*>(frag + f * 48);
-      rec[qi] = (h0 >> o) | (h1 << (24 - o));
-      rec[6 + qi] = (l0 >> o) | (l1 << (24 - o));
-    }
-    if (qi == 0) fsc[f] = (uint8_t)q.c1;
-  }
-}
-
-// ---------------------------------------------------------------------------------------
-// Residual pass of Eq. 2 / Eq. 4: Q(X), dX = X - Q(X) (float32, exact), Q(dX), S_2:4.
-// FRAG: write MFMA fragments (rows m..m_rows-1 are zero padding of the last row tile)
-// instead of K-major codes + scales.
-// ---------------------------------------------------------------------------------------
-template <int FMT, int MODE, bool VEC, bool FRAG>
+template <int FMT, int MODE, bool VEC>
 __global__ __launch_bounds__(kThreads) void residual_kernel(
     const uint16_t* __restrict__ X, int64_t m, int64_t m_rows, int64_t d, int64_t ldx,
     uint8_t* __restrict__ qx_codes, void* __restrict__ qx_scales, uint8_t* __restrict__ qr_codes,
@@ -161,12 +115,8 @@ __global__ __launch_bounds__(kThreads) void residual_kernel(
     float v[4] = {0.f, 0.f, 0.f, 0.f};
     if (row < m) load4<false, VEC>(X, row * ldx + 4 * j4, v);
     const Quad qx = quantize_quad<FMT>(v);
-    if constexpr (FRAG) {
-      store_frag<FMT>(qx_codes, reinterpret_cast<uint8_t*>(qx_scales), row, d, j4, qx, qx.code);
-    } else {
-      *reinterpret_cast<uint16_t*>(qx_codes + row * (d / 2) + 2 * j4) = (uint16_t)pack_quad_codes(qx.code);
-      store_scale<FMT>(qx_scales, row, d, j4, qx.scale);
-    }
+    *reinterpret_cast<uint16_t*>(qx_codes + row * (d / 2) + 2 * j4) = (uint16_t)pack_quad_codes(qx.code);
+    store_scale<FMT>(qx_scales, row, d, j4, qx.scale);
     if constexpr (MODE != kResidNone) {
       float r[4];
 #pragma unroll
@@ -177,26 +127,166 @@ __global__ __launch_bounds__(kThreads) void residual_kernel(
       uint32_t c[4];
 #pragma unroll
       for (int k = 0; k < 4; ++k) c[k] = ((keep >> k) & 1u) ? qr.code[k] : 0u;
-      if constexpr (FRAG) {
-        store_frag<FMT>(qr_codes, reinterpret_cast<uint8_t*>(qr_scales), row, d, j4, qr, c);
-      } else {
-        *reinterpret_cast<uint16_t*>(qr_codes + row * (d / 2) + 2 * j4) = (uint16_t)pack_quad_codes(c);
-        store_scale<FMT>(qr_scales, row, d, j4, qr.scale);
-        if (keep_mask != nullptr && MODE != kResidDense) {
-          const uint32_t other = __shfl_xor(keep, 1, 64);
-          if ((threadIdx.x & 1) == 0) keep_mask[row * (d / 8) + j4 / 2] = (uint8_t)(keep | (other << 4));
-        }
-        if (partials != nullptr) {
-          // exact per-scale-block sum of squares (shared power-of-two factor, small integers)
-          double sq = 0.0;
+      *reinterpret_cast<uint16_t*>(qr_codes + row * (d / 2) + 2 * j4) = (uint16_t)pack_quad_codes(c);
+      store_scale<FMT>(qr_scales, row, d, j4, qr.scale);
+      if (keep_mask != nullptr && MODE != kResidDense) {
+        const uint32_t other = __shfl_xor(keep, 1, 64);
+        if ((threadIdx.x & 1) == 0) keep_mask[row * (d / 8) + j4 / 2] = (uint8_t)(keep | (other << 4));
+      }
+      if (partials != nullptr) {
+        // exact per-scale-block sum of squares (shared power-of-two factor, small integers)
+        double sq = 0.0;
 #pragma unroll
-          for (int k = 0; k < 4; ++k) sq += (double)qr.val[k] * (double)qr.val[k];
-          constexpr int G = (FMT == kMX) ? 8 : 16;
-          sq = group_sum<G>(sq);
-          if ((threadIdx.x & (G - 1)) == 0) partials[row * (d / (4 * G)) + j4 / G] = sq;
-        }
+        for (int k = 0; k < 4; ++k) sq += (double)qr.val[k] * (double)qr.val[k];
+        constexpr int G = (FMT == kMX) ? 8 : 16;
+        sq = group_sum<G>(sq);
+        if ((threadIdx.x & (G - 1)) == 0) partials[row * (d / (4 * G)) + j4 / G] = sq;
       }
     }
+  }
+}
+
+// ---------------------------------------------------------------------------------------
+// Residual pass writing MFMA fragments: one workgroup of 256 threads per fragment (row tile
+// t, K step kb).  Fragment lane record r (row 32t + r%32, elements 64kb + 32(r/32) .. +31)
+// is handled by 4 threads of 8 elements each; thread i of the workgroup takes row i/8 of the
+// tile, half (i/4)%2 and the 8-element slice i%4.  An MXFP4 scale block (32 elements) is 4
+// consecutive lanes, a HiF4 64-block 8 consecutive lanes, a HiF4 level-2 group one lane.
+// Each thread quantizes its slice, forms dX = X - Q(X) (exact in float32), quantizes dX,
+// applies S_2:4, and the 4 threads of a record write it as one contiguous 16-byte (MXFP4) or
+// 48-byte (HiF4 E2M3 hi | lo) run.  Rows past m, and the missing half of an MXFP4 K step
+// when d % 64 == 32, quantize zeros.
+// ---------------------------------------------------------------------------------------
+template <int FMT>
+__device__ __forceinline__ void quantize8(const float x[8], uint32_t code[8], float val[8],
+                                          uint32_t& scale_byte, int& c1, int b[2]) {
+  float a = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) a = fmaxf(a, fabsf(x[i]));
+  if constexpr (FMT == kMX) {
+    const int E = mx_exponent(group_max<4>(a));
+    scale_byte = (uint32_t)(E + 127);
+    c1 = 0;
+    b[0] = b[1] = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      code[i] = mx_code(x[i], E);
+      val[i] = mx_value(code[i], E);
+    }
+  } else {
+    c1 = hif4_c1(group_max<8>(a));
+    scale_byte = (uint32_t)c1;
+    const float fit0 = hif4_half_fit(c1, 0), fit1 = hif4_half_fit(c1, 1);
+    const int b2 = a <= fit0 ? 1 : 0;  // this lane's 8 elements are one level-2 group
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      float a4 = 0.f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) a4 = fmaxf(a4, fabsf(x[4 * hh + e]));
+      b[hh] = b2 + (a4 <= (b2 ? fit1 : fit0) ? 1 : 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t k = hif4_k(x[i], c1, b[i / 4]);
+      code[i] = ((__float_as_uint(x[i]) >> 28) & 8u) | k;
+      val[i] = hif4_value(code[i], c1, b[i / 4]);
+    }
+  }
+}
+
+// The 4 threads of lane record `rec` (slice s = lane % 4) write it.
+template <int FMT>
+__device__ __forceinline__ void store_record8(uint8_t* __restrict__ frag, uint8_t* __restrict__ fsc,
+                                              int64_t rec, int s, const uint32_t code[8],
+                                              uint32_t scale_byte, int c1, const int b[2]) {
+  if constexpr (FMT == kMX) {
+    uint32_t w = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) w |= code[i] << (4 * i);
+    reinterpret_cast<uint32_t*>(frag + rec * 16)[s] = w;
+  } else {
+    // 8 six-bit fields = 48 bits each of hi and lo; record = hi bits [0,192) then lo
+    uint64_t h = 0, l = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      uint32_t hi, lo;
+      hif4_split_e2m3(code[i], c1, b[i / 4], hi, lo);
+      h |= (uint64_t)hi << (6 * i);
+      l |= (uint64_t)lo << (6 * i);
+    }
+    // thread s writes record dwords 3s .. 3s+2: hi of slices 0,1 / hi of 2,3 / lo of 0,1 /
+    // lo of 2,3, i.e. 96 bits assembled from two slices' 48-bit runs
+    const int lane = __lane_id();
+    const int base = lane & ~3, src = base + 2 * (s & 1);
+    const uint32_t hl0 = __shfl((uint32_t)h, src, 64), hh0 = __shfl((uint32_t)(h >> 32), src, 64);
+    const uint32_t hl1 = __shfl((uint32_t)h, src + 1, 64), hh1 = __shfl((uint32_t)(h >> 32), src + 1, 64);
+    const uint32_t ll0 = __shfl((uint32_t)l, src, 64), lh0 = __shfl((uint32_t)(l >> 32), src, 64);
+    const uint32_t ll1 = __shfl((uint32_t)l, src + 1, 64), lh1 = __shfl((uint32_t)(l >> 32), src + 1, 64);
+    const bool lo_part = s >= 2;
+    const uint64_t p0 = ((uint64_t)(lo_part ? lh0 : hh0) << 32) | (lo_part ? ll0 : hl0);  // 48 bits
+    const uint64_t p1 = ((uint64_t)(lo_part ? lh1 : hh1) << 32) | (lo_part ? ll1 : hl1);
+    const uint32_t d0 = (uint32_t)p0;
+    const uint32_t d1 = (uint32_t)(p0 >> 32) | ((uint32_t)p1 << 16);
+    const uint32_t d2 = (uint32_t)(p1 >> 16);
+    uint32_t* w = reinterpret_cast<uint32_t*>(frag + rec * 48) + 3 * s;
+    w[0] = d0;
+    w[1] = d1;
+    w[2] = d2;
+  }
+  if (s == 0) fsc[rec] = (uint8_t)scale_byte;
+}
+
+template <int FMT, int MODE, bool VEC>
+__global__ __launch_bounds__(256) void residual_frag_kernel(
+    const uint16_t* __restrict__ X, int64_t m, int64_t d, int64_t ldx, int64_t nkb,
+    uint8_t* __restrict__ fx, uint8_t* __restrict__ fsx, uint8_t* __restrict__ fr,
+    uint8_t* __restrict__ fsr) {
+  const int64_t f = blockIdx.x;  // fragment index t * nkb + kb
+  const int64_t t = f / nkb, kb = f % nkb;
+  const int tid = threadIdx.x;
+  const int rr = tid >> 3, half = (tid >> 2) & 1, s = tid & 3;
+  const int64_t row = t * 32 + rr;
+  const int64_t col0 = kb * 64 + 32 * half + 8 * s;
+  float x[8];
+  if (row < m && col0 < d) {
+    const uint16_t* src = X + row * ldx + col0;
+    if constexpr (VEC) {
+      const uint4 u = *reinterpret_cast<const uint4*>(src);
+      const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x[2 * e] = bf16_to_f32(w[e] & 0xFFFFu);
+        x[2 * e + 1] = bf16_to_f32(w[e] >> 16);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) x[i] = bf16_to_f32(src[i]);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = 0.f;
+  }
+  const int64_t rec = f * 64 + rr + 32 * half;
+  uint32_t code[8], scale_byte;
+  float val[8];
+  int c1, b[2];
+  quantize8<FMT>(x, code, val, scale_byte, c1, b);
+  store_record8<FMT>(fx, fsx, rec, s, code, scale_byte, c1, b);
+  if constexpr (MODE != kResidNone) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] -= val[i];  // dX, exact in float32
+    quantize8<FMT>(x, code, val, scale_byte, c1, b);
+    if constexpr (MODE == kResid24) {
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        const uint32_t c4[4] = {code[4 * g], code[4 * g + 1], code[4 * g + 2], code[4 * g + 3]};
+        const uint32_t keep = keep_2_of_4(c4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (!((keep >> e) & 1u)) code[4 * g + e] = 0u;
+      }
+    }
+    store_record8<FMT>(fr, fsr, rec, s, code, scale_byte, c1, b);
   }
 }
 
@@ -235,21 +325,35 @@ void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d,
                      uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes, void* qr_scales,
                      uint8_t* keep_mask, double* partials, hipStream_t s, bool frag) {
   if (m == 0 || d == 0) return;
-  const int64_t m_rows = frag ? (m + 31) / 32 * 32 : m;
-  const dim3 grid((unsigned)((d / 4 + kThreads - 1) / kThreads), grid_rows(m_rows));
-  const bool vec = ((uintptr_t)X % 8 == 0) && (ldx % 4 == 0);
-#define RESQ_RK(F, M, V, G) hipLaunchKernelGGL((residual_kernel<F, M, V, G>), grid, dim3(kThreads), 0, s, X, m, m_rows, d, ldx, qx_codes, qx_scales, qr_codes, qr_scales, keep_mask, partials)
-#define RESQ_RK_MODE(F, V, G)                                       \
-  switch (mode) {                                                   \
-    case kResidNone: RESQ_RK(F, kResidNone, V, G); break;           \
-    case kResidIdentity: RESQ_RK(F, kResidIdentity, V, G); break;   \
-    case kResid24: RESQ_RK(F, kResid24, V, G); break;               \
-    default: RESQ_RK(F, kResidDense, V, false); break;              \
+  if (frag) {
+    const int64_t nkb = (d + 63) / 64;
+    const dim3 grid((unsigned)(((m + 31) / 32) * nkb));
+    const bool vec16 = ((uintptr_t)X % 16 == 0) && (ldx % 8 == 0);
+#define RESQ_RF(F, M, V) hipLaunchKernelGGL((residual_frag_kernel<F, M, V>), grid, dim3(256), 0, s, X, m, d, ldx, nkb, qx_codes, (uint8_t*)qx_scales, qr_codes, (uint8_t*)qr_scales)
+#define RESQ_RF_MODE(F, V)                                        \
+    switch (mode) {                                               \
+      case kResidNone: RESQ_RF(F, kResidNone, V); break;          \
+      case kResidIdentity: RESQ_RF(F, kResidIdentity, V); break;  \
+      default: RESQ_RF(F, kResid24, V); break;                    \
+    }
+    if (fmt == kMX) { if (vec16) { RESQ_RF_MODE(kMX, true) } else { RESQ_RF_MODE(kMX, false) } }
+    else { if (vec16) { RESQ_RF_MODE(kHI, true) } else { RESQ_RF_MODE(kHI, false) } }
+#undef RESQ_RF_MODE
+#undef RESQ_RF
+    return;
   }
-#define RESQ_RK_VEC(F, G) if (vec) { RESQ_RK_MODE(F, true, G) } else { RESQ_RK_MODE(F, false, G) }
-  if (fmt == kMX) { if (frag) { RESQ_RK_VEC(kMX, true) } else { RESQ_RK_VEC(kMX, false) } }
-  else { if (frag) { RESQ_RK_VEC(kHI, true) } else { RESQ_RK_VEC(kHI, false) } }
-#undef RESQ_RK_VEC
+  const dim3 grid((unsigned)((d / 4 + kThreads - 1) / kThreads), grid_rows(m));
+  const bool vec = ((uintptr_t)X % 8 == 0) && (ldx % 4 == 0);
+#define RESQ_RK(F, M, V) hipLaunchKernelGGL((residual_kernel<F, M, V>), grid, dim3(kThreads), 0, s, X, m, m, d, ldx, qx_codes, qx_scales, qr_codes, qr_scales, keep_mask, partials)
+#define RESQ_RK_MODE(F, V)                                       \
+  switch (mode) {                                                \
+    case kResidNone: RESQ_RK(F, kResidNone, V); break;           \
+    case kResidIdentity: RESQ_RK(F, kResidIdentity, V); break;   \
+    case kResid24: RESQ_RK(F, kResid24, V); break;               \
+    default: RESQ_RK(F, kResidDense, V); break;                  \
+  }
+  if (fmt == kMX) { if (vec) { RESQ_RK_MODE(kMX, true) } else { RESQ_RK_MODE(kMX, false) } }
+  else { if (vec) { RESQ_RK_MODE(kHI, true) } else { RESQ_RK_MODE(kHI, false) } }
 #undef RESQ_RK_MODE
 #undef RESQ_RK
 }
