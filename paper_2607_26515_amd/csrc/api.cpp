@@ -81,6 +81,7 @@ struct ActWs {
   uint8_t* fsc_x;
   uint8_t* frag_r;
   uint8_t* fsc_r;
+  float* gemm_partial;       // split-K partial tiles
   resq::SelectWs sel;
 };
 
@@ -113,7 +114,7 @@ void carve_prepared(const void* base, int fmt, int64_t n, int64_t d, const uint8
   *fsc = b + align256(resq::frag_bytes(b_pack_mode(fmt), n, d));
 }
 
-size_t carve_fwd(void* base, int fmt, int sp, int64_t m, int64_t d, ActWs* w) {
+size_t carve_fwd(void* base, int fmt, int sp, int64_t m, int64_t d, int64_t n, ActWs* w) {
   Carver c(base);
   ActWs t{};
   t.qx_codes = (uint8_t*)c.take((size_t)m * d / 2);
@@ -129,6 +130,8 @@ size_t carve_fwd(void* base, int fmt, int sp, int64_t m, int64_t d, ActWs* w) {
     t.frag_r = (uint8_t*)c.take(resq::frag_bytes(a_pack_mode(fmt), m, d));
     t.fsc_r = (uint8_t*)c.take(resq::frag_scale_bytes(m, d));
   }
+  const size_t pb = resq::gemm_split_scratch(fmt, m, n, d);
+  if (pb > 0) t.gemm_partial = (float*)c.take(pb);
   if (w) *w = t;
   return c.off;
 }
@@ -247,8 +250,8 @@ size_t resq_workspace_size(int op, int format, int sparsity, int64_t m, int64_t 
       return c.off;
     }
     case RESQ_OP_LINEAR_FWD:
-      return carve_fwd(nullptr, format, sparsity, m, d, nullptr) + prepared_bytes(format, n, d);
-    case RESQ_OP_LINEAR_FWD_PREPARED: return carve_fwd(nullptr, format, sparsity, m, d, nullptr);
+      return carve_fwd(nullptr, format, sparsity, m, d, n, nullptr) + prepared_bytes(format, n, d);
+    case RESQ_OP_LINEAR_FWD_PREPARED: return carve_fwd(nullptr, format, sparsity, m, d, n, nullptr);
     case RESQ_OP_LINEAR_BWD: return carve_bwd(nullptr, format, m, d, n, nullptr);
     default: return 0;
   }
@@ -333,6 +336,7 @@ int linear_fwd_core(int format, int sparsity, const uint16_t* X, int64_t m, int6
   op.a_frag[1] = w.frag_r; op.a_sc[1] = w.fsc_r;
   carve_prepared(wprep, format, n, d, &op.b_frag, &op.b_sc);
   op.Y = Y; op.ldy = ldy;
+  op.partial = w.gemm_partial;
   {
     resq::ProfScope prof_(resq::kProfGemm, s);
     resq::launch_gemm(op, s);
@@ -364,7 +368,7 @@ int resq_linear_fwd_prepared(int format, int sparsity, const uint16_t* X, int64_
   if (d > 0 && !wprep) return fail(RESQ_ERR_ARG, "wprep is NULL");
   if ((uintptr_t)wprep % 256 != 0) return fail(RESQ_ERR_ARG, "wprep must be 256-byte aligned");
   ActWs w{};
-  const size_t need = carve_fwd(workspace, format, sparsity, m, d, &w);
+  const size_t need = carve_fwd(workspace, format, sparsity, m, d, n, &w);
   rc = check_ws(workspace, workspace_bytes, need);
   if (rc != RESQ_OK) return rc;
   return linear_fwd_core(format, sparsity, X, m, d, ldx, wprep, n, Y, ldy, w, (hipStream_t)stream);
@@ -381,7 +385,7 @@ int resq_linear_fwd(int format, int sparsity, const uint16_t* X, int64_t m, int6
   if ((uintptr_t)qw_codes % 16 != 0 || (format == RESQ_HIF4 && (uintptr_t)qw_scales % 4 != 0))
     return fail(RESQ_ERR_ARG, "qw_codes must be 16-byte aligned (HiF4 scales 4-byte aligned)");
   ActWs w{};
-  const size_t act = carve_fwd(workspace, format, sparsity, m, d, &w);
+  const size_t act = carve_fwd(workspace, format, sparsity, m, d, n, &w);
   const size_t need = act + prepared_bytes(format, n, d);
   rc = check_ws(workspace, workspace_bytes, need);
   if (rc != RESQ_OK) return rc;

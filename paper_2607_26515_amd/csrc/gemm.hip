@@ -55,6 +55,11 @@ struct GemmParams {
   float* Y;
   int64_t ldy;
   int64_t grid_m, grid_n, per_xcd;
+  // split-K: ksplit workgroups per tile, each over kper K steps, each writing its partial
+  // tile (summed by splitk_reduce_kernel)
+  int ksplit;
+  int64_t kper;
+  float* partial;
 };
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
@@ -139,14 +144,18 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(GemmParams p) {
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
 
   const int64_t b = blockIdx.x;
-  const int64_t tile = (b % kXcds) * p.per_xcd + b / kXcds;
-  if (tile >= p.grid_m * p.grid_n) return;
+  const int64_t wgid = (b % kXcds) * p.per_xcd + b / kXcds;  // the K splits of a tile are adjacent
+  if (wgid >= p.grid_m * p.grid_n * p.ksplit) return;
+  const int64_t tile = wgid / p.ksplit;
+  const int split = (int)(wgid % p.ksplit);
   const int64_t wg_m = tile % p.grid_m, wg_n = tile / p.grid_m;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int wm = wave % WM, wn = wave / WM;
   const uint32_t T0 = (uint32_t)(wg_m * G::MTW), N0 = (uint32_t)(wg_n * G::NTW);
   const uint32_t nkb = (uint32_t)p.nkb;
+  const uint32_t kbeg = (uint32_t)(split * p.kper);                    // this split's K steps:
+  const uint32_t klen = (uint32_t)min((int64_t)p.kper, p.nkb - kbeg);  // kbeg .. kbeg+klen-1
 
   // ---- this wave's copy list: copy jc of a size class goes to wave jc % W ----
   const Copy pad{p.b_frag, 0u, kBad, 0u, (uint32_t)G::DUMP_OFF};
@@ -195,9 +204,11 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(GemmParams p) {
     c4[x] = c;
   }
 
-  // Copy K step kb into stage buffer `buf` (kb >= nkb copies zeros).
-  auto issue = [&](int buf, uint32_t kb) {
-    const bool in = kb < nkb;
+  // Copy this split's K step k (absolute step kbeg + k) into stage buffer `buf`; steps
+  // past the split's end copy zeros.
+  auto issue = [&](int buf, uint32_t k) {
+    const bool in = k < klen;
+    const uint32_t kb = kbeg + k;
     uint8_t* st = smem + buf * G::STAGE;
 #pragma unroll
     for (int x = 0; x < G::S16; ++x)
@@ -343,7 +354,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(GemmParams p) {
   wait_vmcnt<(NS - 1) * G::JW>();
   __syncthreads();  // also publishes the block-skip table
   read(F[0], 0);
-  for (uint32_t k0 = 0; k0 < nkb; k0 += U) {
+  for (uint32_t k0 = 0; k0 < klen; k0 += U) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const uint32_t k = k0 + u;
@@ -351,11 +362,24 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(GemmParams p) {
       lds_barrier();
       issue(u % NS, k + NS);
       read(F[(u + 1) & 1], (u + 1) % NS);
-      mma(F[u & 1], k);
+      mma(F[u & 1], k < klen ? kbeg + k : nkb);
       __builtin_amdgcn_sched_barrier(0);  // keep step k's MFMAs ahead of step k+1's barrier
     }
   }
   wait_vmcnt<0>();
+
+  if (p.ksplit > 1) {
+    // split K: write this split's partial tile in register order (coalesced per wave)
+    constexpr int TE = G::kThreads * TM * TN * 16;  // floats per tile
+    float* part = p.partial + ((size_t)tile * p.ksplit + split) * TE + (size_t)wave * TM * TN * 16 * 64;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) part[((i * TN + j) * 16 + r) * 64 + lane] = acc[i][j][r];
+    return;
+  }
 
   const int half = lane >> 5, l32 = lane & 31;
 #pragma unroll
@@ -371,12 +395,35 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(GemmParams p) {
     }
 }
 
+// Sum the ksplit partial tiles of each output tile in split order (deterministic) and store
+// Y.  One workgroup per tile; partial element e = wave, tile (i, j), accumulator register r,
+// lane -- the gemm_kernel register order.
+template <int WM, int WN, int TM, int TN>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ partial,
+                                                            int ksplit, int64_t grid_m, int64_t M,
+                                                            int64_t N, float* __restrict__ Y,
+                                                            int64_t ldy) {
+  constexpr int TE = 64 * WM * WN * TM * TN * 16;
+  const int64_t tile = blockIdx.x;
+  const int64_t wg_m = tile % grid_m, wg_n = tile / grid_m;
+  const float* part = partial + (size_t)tile * ksplit * TE;
+  for (int e = threadIdx.x; e < TE; e += 256) {
+    const int lane = e & 63, r = (e >> 6) & 15, ij = (e >> 10) % (TM * TN), wave = e / (1024 * TM * TN);
+    const int i = ij / TN, j = ij % TN, wm = wave % WM, wn = wave / WM;
+    float v = part[e];
+    for (int q = 1; q < ksplit; ++q) v += part[(size_t)q * TE + e];
+    const int64_t row = (wg_m * WM * TM + wm * TM + i) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+    const int64_t col = (wg_n * WN * TN + wn * TN + j) * 32 + (lane & 31);
+    if (row < M && col < N) Y[row * ldy + col] = v;
+  }
+}
+
 template <int FMT, int WM, int WN, int TM, int TN, int NS>
 void launch_cfg(GemmParams p, int n_terms, hipStream_t s) {
   p.grid_m = (p.mt_tiles + WM * TM - 1) / (WM * TM);
   p.grid_n = (p.nt_tiles + WN * TN - 1) / (WN * TN);
-  const int64_t tiles = p.grid_m * p.grid_n;
-  p.per_xcd = (tiles + kXcds - 1) / kXcds;
+  const int64_t wgs = p.grid_m * p.grid_n * p.ksplit;
+  p.per_xcd = (wgs + kXcds - 1) / kXcds;
   const dim3 grid((unsigned)(p.per_xcd * kXcds));
   const dim3 block(64 * WM * WN);
   using G2 = Geo<FMT, WM, WN, TM, TN, 2, NS>;
@@ -387,19 +434,59 @@ void launch_cfg(GemmParams p, int n_terms, hipStream_t s) {
     hipLaunchKernelGGL((gemm_kernel<FMT, WM, WN, TM, TN, 2, NS, false>), grid, block, G2::lds_bytes(false), s, p);
   else
     hipLaunchKernelGGL((gemm_kernel<FMT, WM, WN, TM, TN, 1, NS, false>), grid, block, G1::lds_bytes(false), s, p);
+  if (p.ksplit > 1)
+    hipLaunchKernelGGL((splitk_reduce_kernel<WM, WN, TM, TN>), dim3((unsigned)(p.grid_m * p.grid_n)), dim3(256), 0, s,
+                       (const float*)p.partial, p.ksplit, p.grid_m, p.M, p.N, p.Y, p.ldy);
 }
 
 // Tile choice (measured on MI355X): a CU holds one or two workgroups (LDS-bound), so the
 // workgroup count decides how many rounds the grid takes.
-//  - grids too small for 128-row tiles to fill the chip: 64 x 64 tiles, deep pipeline;
+//  - grids too small for 128-row tiles to fill the chip: 64 x 64 tiles, deep pipeline, and
+//    for long K (at least 64 steps per split) K split in two when that fills the CUs;
 //  - M >= 512 (7B decode and prefill): 128 x 256 tiles (fewest A re-reads per byte of B);
 //  - otherwise (M = 256 decode): 128 x 192 tiles, one round on 256 CUs.
+enum TileCfg { kSmall = 0, kWide = 1, kMid = 2 };
+constexpr int kCUs = 256;
+
+struct Plan {
+  int cfg, ksplit;
+  int64_t kper, tiles;
+  size_t partial_bytes;
+};
+
+Plan plan(int fmt, int64_t M, int64_t N, int64_t K, bool may_split) {
+  const int64_t mt = (M + 31) / 32, nt = (N + 31) / 32, nkb = (K + 63) / 64;
+  auto wgs = [&](int64_t bm, int64_t bn) { return ((mt + bm - 1) / bm) * ((nt + bn - 1) / bn); };
+  Plan pl{};
+  pl.ksplit = 1;
+  pl.kper = nkb;
+  if (wgs(4, 4) < 240) {
+    pl.cfg = kSmall;
+    pl.tiles = wgs(2, 2);
+    const int per_cu = fmt == 0 ? 2 : 1;  // small-tile workgroups resident per CU (LDS)
+    if (may_split && pl.tiles > 0) {
+      // a split pays only for long K: its partial tiles and the reduction launch cost
+      // about as much as a short K range (measured)
+      // (MXFP4 small tiles already run two workgroups per CU: no gain there)
+      int64_t ks = per_cu == 1 ? kCUs / pl.tiles : 1;
+      ks = ks < 1 ? 1 : (ks > 2 ? 2 : ks);
+      while (ks > 1 && nkb / ks < 64) --ks;
+      pl.ksplit = (int)ks;
+      pl.kper = (nkb + ks - 1) / ks;
+      if (pl.ksplit > 1) pl.partial_bytes = (size_t)pl.tiles * pl.ksplit * (256 * 16) * sizeof(float);
+    }
+  } else {
+    pl.cfg = M >= 512 ? kWide : kMid;
+    pl.tiles = M >= 512 ? wgs(4, 8) : wgs(4, 6);
+  }
+  return pl;
+}
+
 template <int FMT>
-void launch_fmt(const GemmParams& p, int n_terms, hipStream_t s) {
-  auto wgs = [&](int bm, int bn) { return ((p.mt_tiles + bm - 1) / bm) * ((p.nt_tiles + bn - 1) / bn); };
-  if (wgs(4, 4) < 240)
+void launch_fmt(const GemmParams& p, int cfg, int n_terms, hipStream_t s) {
+  if (cfg == kSmall)
     launch_cfg<FMT, 2, 2, 1, 1, FMT == 0 ? 8 : 6>(p, n_terms, s);
-  else if (p.M >= 512)
+  else if (cfg == kWide)
     launch_cfg<FMT, 2, 2, 2, 4, FMT == 0 ? 4 : 2>(p, n_terms, s);
   else
     launch_cfg<FMT, 2, 2, 2, 3, FMT == 0 ? 4 : 2>(p, n_terms, s);
@@ -415,9 +502,17 @@ bool gemm_supported(int fmt, int64_t M, int64_t N, int64_t K, bool block_skip) {
   return true;
 }
 
+size_t gemm_split_scratch(int fmt, int64_t M, int64_t N, int64_t K) {
+  return plan(fmt, M, N, K, true).partial_bytes;
+}
+
 void launch_gemm(const GemmOperands& op, hipStream_t s) {
   if (op.M == 0 || op.N == 0) return;
+  const Plan pl = plan(op.fmt, op.M, op.N, op.K, op.partial != nullptr);
   GemmParams p{};
+  p.ksplit = pl.ksplit;
+  p.kper = pl.kper;
+  p.partial = op.partial;
   p.M = op.M; p.N = op.N; p.K = op.K;
   p.nkb = (op.K + 63) / 64;
   p.mt_tiles = (op.M + 31) / 32;
@@ -431,8 +526,8 @@ void launch_gemm(const GemmOperands& op, hipStream_t s) {
   p.a_sc_bytes = (uint32_t)frag_scale_bytes(op.M, op.K);
   p.b_frag_bytes = (uint32_t)frag_bytes(bmode, op.N, op.K);
   p.b_sc_bytes = (uint32_t)frag_scale_bytes(op.N, op.K);
-  if (op.fmt == 0) launch_fmt<0>(p, op.n_terms, s);
-  else launch_fmt<1>(p, op.n_terms, s);
+  if (op.fmt == 0) launch_fmt<0>(p, pl.cfg, op.n_terms, s);
+  else launch_fmt<1>(p, pl.cfg, op.n_terms, s);
 }
 
 }  // namespace resq

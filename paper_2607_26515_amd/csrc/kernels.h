@@ -68,8 +68,12 @@ struct GemmOperands {
   const uint8_t* b_sc;
   float* Y;
   int64_t ldy;
+  // optional split-K scratch of gemm_split_scratch bytes (null: no K split)
+  float* partial;
 };
 void launch_gemm(const GemmOperands& op, hipStream_t s);
+// Scratch bytes a launch_gemm of this shape uses for its K split (0: it does not split).
+size_t gemm_split_scratch(int fmt, int64_t M, int64_t N, int64_t K);
 // Whether launch_gemm handles these sizes (32-bit operand offsets; the block-skip mask of a
 // row tile fits the kernel's LDS table).
 bool gemm_supported(int fmt, int64_t M, int64_t N, int64_t K, bool block_skip);

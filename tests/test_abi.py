@@ -88,8 +88,8 @@ def test_linear_bwd_rejects_bad_arguments():
 
 
 def test_workspace_sizes_grow_with_shape():
-    a = P.resq_workspace_size(B.OP_LINEAR_FWD, B.HIF4, B.S_2_4, 256, 2048, 2048)
-    b = P.resq_workspace_size(B.OP_LINEAR_FWD, B.HIF4, B.S_2_4, 512, 2048, 2048)
+    a = P.resq_workspace_size(B.OP_LINEAR_FWD, B.HIF4, B.S_2_4, 256, 2048, 22016)
+    b = P.resq_workspace_size(B.OP_LINEAR_FWD, B.HIF4, B.S_2_4, 512, 2048, 22016)
     assert 0 < a < b
     assert P.resq_workspace_size(9, 0, 0, 1, 64, 1) == 0
     assert P.resq_workspace_size(B.OP_LINEAR_BWD, B.MXFP4, 0, 64, 64, 64) > 0
