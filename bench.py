@@ -81,7 +81,7 @@ def gemm_traffic(workload, fmt, sp):
     return None if entry is None else round(entry["bytes_per_launch"])
 
 
-def cpu_baseline(wl, fmt, sp, n_sample, min_seconds):
+def cpu_baseline(wl, fmt, sp, n_sample, n_rows, min_seconds):
     """The oracle, as it stands, on a bounded sample of the same workload (host cores)."""
     import numpy as np
     from oracle import formats as F
@@ -95,37 +95,118 @@ def cpu_baseline(wl, fmt, sp, n_sample, min_seconds):
         blas_threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=None)
     except Exception:
         pass
+    rows = min(wl.m, n_rows)
     prepared = []
     for lin in wl.linears:
-        xb, wb = workload_tensors(wl, lin)
-        w = bf16_bits_to_f32(wb[:n_sample])
-        what = F.dequantize(fmt, *F.quantize(fmt, w))  # Q(W): once per policy update, untimed
-        prepared.append((bf16_bits_to_f32(xb), what))
+        t = workload_tensors(wl, lin, m=rows)
+        if wl.backward:
+            xb, wb, gb = t
+            prepared.append((bf16_bits_to_f32(xb), bf16_bits_to_f32(wb[:n_sample]),
+                             bf16_bits_to_f32(gb[:, :n_sample])))
+        else:
+            xb, wb = t
+            w = bf16_bits_to_f32(wb[:n_sample])
+            what = F.dequantize(fmt, *F.quantize(fmt, w))  # Q(W): once per policy update, untimed
+            prepared.append((bf16_bits_to_f32(xb), what, None))
     flops = 0
     t0 = time.perf_counter()
     reps = 0
     while True:
-        for x, what in prepared:
-            out = Q.resq_quantize_residual(fmt, sp, x)
-            y = out["xhat"] @ what.T
-            if sp != "none":
-                y = y + out["srhat"] @ what.T
-            y.astype(np.float32)
-            flops += alg_flops(x.shape[0], x.shape[1], what.shape[0], sp)
+        for x, w, gy in prepared:
+            if wl.backward:
+                Q.resq_backward(fmt, gy, x, w)
+                flops += 4 * x.shape[0] * x.shape[1] * w.shape[0]
+            else:
+                out = Q.resq_quantize_residual(fmt, sp, x)
+                y = out["xhat"] @ w.T
+                if sp != "none":
+                    y = y + out["srhat"] @ w.T
+                y.astype(np.float32)
+                flops += alg_flops(x.shape[0], x.shape[1], w.shape[0], sp)
         reps += 1
         if time.perf_counter() - t0 >= min_seconds:
             break
     dt = time.perf_counter() - t0
+    what_ = ("dY, X and W restricted to" if wl.backward else "X restricted to")
     return {
         "value": flops / dt / 1e12,
         "unit": "TFLOP/s",
         "cores": int(blas_threads or cores),
         "kind": "oracle",
-        "sample": (f"all {wl.m} rows of every linear of {wl.name} against the first {n_sample} "
-                   f"output features of each weight, {reps} repetition(s), {dt:.1f} s; Q(W) "
-                   f"untimed; numpy fp64 (quantizers single-threaded, matmul on "
-                   f"{blas_threads or '?'} BLAS threads of {cores} cores)"),
+        "sample": (f"{wl.name}: {what_} the first {rows} rows and the first {n_sample} output "
+                   f"features of every linear, {reps} repetition(s), {dt:.1f} s"
+                   f"{'' if wl.backward else '; Q(W) untimed'}; numpy fp64 (quantizers "
+                   f"single-threaded, matmul on {blas_threads or '?'} BLAS threads of {cores} cores)"),
     }
+
+
+def setup_forward(P, torch, np, wl, fmt, sp, dev, sptr):
+    """Inputs resident in HBM (enough rotating copies to defeat the last-level cache) and a
+    step function running every linear of the workload through resq_linear_fwd_prepared."""
+    from synth import workload_tensors
+    f, s = P.FORMATS[fmt], P.SPARSITY[sp]
+    per_copy = sum(P.resq_prepared_weights_size(f, l.n, l.d) + 2 * wl.m * l.d for l in wl.linears)
+    copies = int(min(64, max(2, -(-2 * LLC_BYTES // int(per_copy)) + 1)))
+    ws_bytes = max(P.resq_workspace_size(3, f, s, wl.m, l.d, l.n) for l in wl.linears)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    lin_state = []
+    for lin in wl.linears:
+        xb, wb = workload_tensors(wl, lin)
+        x0 = torch.from_numpy(xb.view(np.int16)).to(dev)
+        w0 = torch.from_numpy(wb.view(np.int16)).to(dev)
+        xs, wps = [], []
+        for c in range(copies):
+            xs.append(x0.clone())
+            qc, qs = P.quantize(w0, fmt, axis=1)  # Q(W) and its GEMM layout: once per policy update
+            wps.append(P.prepare_weights(qc, qs, fmt))
+            del qc, qs
+        del w0, x0
+        y = torch.empty((wl.m, lin.n), dtype=torch.float32, device=dev)
+        lin_state.append(dict(lin=lin, xs=xs, wps=wps, y=y, xp=[int(t.data_ptr()) for t in xs],
+                              wp=[int(t.data_ptr()) for t in wps]))
+    torch.cuda.synchronize()
+    lib = P.load()
+
+    def run_linear(st, i):
+        lin, c = st["lin"], i % copies
+        rc = lib.resq_linear_fwd_prepared(f, s, st["xp"][c], wl.m, lin.d, lin.d, st["wp"][c], lin.n,
+                                          int(st["y"].data_ptr()), lin.n, int(ws.data_ptr()),
+                                          ws_bytes, sptr)
+        if rc != 0:
+            raise P.ResqError(f"resq_linear_fwd_prepared: {P.resq_last_error()}", rc)
+
+    return lin_state, run_linear, copies
+
+
+def setup_backward(P, torch, np, wl, fmt, dev, sptr):
+    """dY, X, W resident in HBM (rotating copies) and a step running resq_linear_bwd."""
+    from synth import workload_tensors
+    f = P.FORMATS[fmt]
+    lin = wl.linears[0]
+    m, d, n = wl.m, lin.d, lin.n
+    per_copy = 2 * (m * n + m * d + n * d)
+    copies = int(min(16, max(2, -(-2 * LLC_BYTES // per_copy) + 1)))
+    xb, wb, gb = workload_tensors(wl, lin)
+    base = [torch.from_numpy(a.view(np.int16)).to(dev) for a in (gb, xb, wb)]
+    sets = [[t.clone() for t in base] for _ in range(copies)]
+    del base
+    dx = torch.empty((m, d), dtype=torch.float32, device=dev)
+    dw = torch.empty((n, d), dtype=torch.float32, device=dev)
+    ws_bytes = P.resq_workspace_size(P.OP_LINEAR_BWD, f, 0, m, d, n)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    lib = P.load()
+    st = dict(lin=lin)
+
+    def run_linear(_st, i):
+        g, x, w = sets[i % copies]
+        rc = lib.resq_linear_bwd(f, int(g.data_ptr()), int(x.data_ptr()), int(w.data_ptr()), m, d, n,
+                                 int(dx.data_ptr()), int(dw.data_ptr()), int(ws.data_ptr()), ws_bytes,
+                                 sptr)
+        if rc != 0:
+            raise P.ResqError(f"resq_linear_bwd: {P.resq_last_error()}", rc)
+
+    return [st], run_linear, copies
 
 
 def main() -> int:
@@ -138,6 +219,7 @@ def main() -> int:
     ap.add_argument("--sparsity", default="2:4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-cols", type=int, default=1024)
+    ap.add_argument("--cpu-sample-rows", type=int, default=512)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized device buffer once (HBM counter calibration)")
@@ -153,7 +235,7 @@ def main() -> int:
     import torch
 
     import paper_2607_26515_amd as P
-    from synth import WORKLOADS, workload_tensors
+    from synth import WORKLOADS
 
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
@@ -169,46 +251,18 @@ def main() -> int:
         return 0
     P.load()  # fails loudly when libresq.so is missing
     dev = torch.device("cuda:0")
-    stream = torch.cuda.current_stream()
-    sptr = int(stream.cuda_stream)
+    sptr = int(torch.cuda.current_stream().cuda_stream)
     wl = WORKLOADS[args.workload]
-    fmt, sp = args.format, args.sparsity
-    f, s = P.FORMATS[fmt], P.SPARSITY[sp]
-
-    # ---- inputs, resident in HBM; enough copies to defeat the last-level cache ----
-    per_copy = sum(P.resq_prepared_weights_size(f, l.n, l.d) + 2 * wl.m * l.d for l in wl.linears)
-    copies = int(min(64, max(2, -(-2 * LLC_BYTES // int(per_copy)) + 1)))
-    lin_state = []
-    ws_bytes = max(P.resq_workspace_size(3, f, s, wl.m, l.d, l.n) for l in wl.linears)
-    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
-    for lin in wl.linears:
-        xb, wb = workload_tensors(wl, lin)
-        x0 = torch.from_numpy(xb.view(np.int16)).to(dev)
-        w0 = torch.from_numpy(wb.view(np.int16)).to(dev)
-        xs, wps = [], []
-        for c in range(copies):
-            xs.append(x0.clone())
-            qc, qs = P.quantize(w0, fmt, axis=1)  # Q(W) and its GEMM layout: once per policy update
-            wps.append(P.prepare_weights(qc, qs, fmt))
-            del qc, qs
-        del w0
-        y = torch.empty((wl.m, lin.n), dtype=torch.float32, device=dev)
-        lin_state.append(dict(lin=lin, xs=xs, wps=wps, y=y,
-                              xp=[int(t.data_ptr()) for t in xs],
-                              wp=[int(t.data_ptr()) for t in wps]))
-    torch.cuda.synchronize()
-
-    lib = P.load()
+    fmt = args.format
+    sp = "none" if wl.backward else args.sparsity
+    if wl.backward:
+        lin_state, run_linear, copies = setup_backward(P, torch, np, wl, fmt, dev, sptr)
+    else:
+        lin_state, run_linear, copies = setup_forward(P, torch, np, wl, fmt, sp, dev, sptr)
 
     def run_step(i):
-        c = i % copies
         for st in lin_state:
-            lin = st["lin"]
-            rc = lib.resq_linear_fwd_prepared(f, s, st["xp"][c], wl.m, lin.d, lin.d, st["wp"][c],
-                                              lin.n, int(st["y"].data_ptr()), lin.n,
-                                              int(ws.data_ptr()), ws_bytes, sptr)
-            if rc != 0:
-                raise P.ResqError(f"resq_linear_fwd_prepared: {P.resq_last_error()}", rc)
+            run_linear(st, i)
 
     for i in range(args.warmup):
         run_step(i)
@@ -220,49 +274,60 @@ def main() -> int:
     dt = time.perf_counter() - t0
     ms_per_step = dt * 1e3 / args.steps
 
-    flops = sum(alg_flops(wl.m, l.d, l.n, sp) for l in wl.linears)
-    sbytes = sum(step_bytes(wl.m, l.d, l.n, fmt) for l in wl.linears)
-    value = flops * args.steps / dt / 1e12
-
-    # ---- dominant kernel (GEMM): HIP events on its stream via the library profiler ----
+    # ---- kernel times: HIP events on the launch stream via the library profiler ----
+    kinds = ("quant_rows", "quant_cols", "pack_hif4", "gemm") if wl.backward else \
+            ("residual", "pack_hif4", "select", "gemm")
     P.resq_profile_enable(True)
     P.resq_profile_reset()
     for i in range(args.steps):
         run_step(i)
     torch.cuda.synchronize()
-    prof = {k: P.resq_profile_read(k) for k in ("residual", "pack_hif4", "select", "gemm")}
-    # per-linear breakdown of the same kernels
+    prof = {k: P.resq_profile_read(k) for k in kinds}
     per_linear = {}
-    for st in lin_state:
-        lin = st["lin"]
-        P.resq_profile_reset()
-        for i in range(args.steps):
-            c = i % copies
-            lib.resq_linear_fwd_prepared(f, s, st["xp"][c], wl.m, lin.d, lin.d, st["wp"][c], lin.n,
-                                         int(st["y"].data_ptr()), lin.n, int(ws.data_ptr()),
-                                         ws_bytes, sptr)
-        torch.cuda.synchronize()
-        per_linear[lin.name] = {k: round(P.resq_profile_read(k)[1] / args.steps * 1e3, 2)
-                                for k in ("residual", "pack_hif4", "select", "gemm")}
+    if len(lin_state) > 1:
+        for st in lin_state:
+            P.resq_profile_reset()
+            for i in range(args.steps):
+                run_linear(st, i)
+            torch.cuda.synchronize()
+            per_linear[st["lin"].name] = {k: round(P.resq_profile_read(k)[1] / args.steps * 1e3, 2)
+                                          for k in kinds}
     P.resq_profile_enable(False)
+
+    lins = wl.linears
+    if wl.backward:
+        flops = sum(4 * wl.m * l.d * l.n for l in lins)  # dX and dW, 2mdn each
+        gexec = flops * (2 if fmt == "hif4" else 1)      # HiF4: hi and lo MFMA per term
+        gbytes = sum(BYTES_PER_ELEM[fmt] * 2 * (wl.m * l.n + l.n * l.d + wl.m * l.d)
+                     + 4 * (wl.m * l.d + l.n * l.d) for l in lins)
+        sbytes = sum(2 * (wl.m * l.n + wl.m * l.d + l.n * l.d) + 4 * (wl.m * l.d + l.n * l.d)
+                     for l in lins)
+        n_launch = 2 * len(lins)
+    else:
+        flops = sum(alg_flops(wl.m, l.d, l.n, sp) for l in lins)
+        gexec = sum(exec_mfma_flops(wl.m, l.d, l.n, fmt, sp) for l in lins)
+        gbytes = sum(gemm_bytes(wl.m, l.d, l.n, fmt, sp) for l in lins)
+        sbytes = sum(step_bytes(wl.m, l.d, l.n, fmt) for l in lins)
+        n_launch = len(lins)
+    value = flops * args.steps / dt / 1e12
     g_launch, g_ms = prof["gemm"]
     gemm_ms_step = g_ms / args.steps
-    gbytes = sum(gemm_bytes(wl.m, l.d, l.n, fmt, sp) for l in wl.linears)
-    gexec = sum(exec_mfma_flops(wl.m, l.d, l.n, fmt, sp) for l in wl.linears)
-    n_lin = len(wl.linears)
-    launch_s = gemm_ms_step / n_lin * 1e-3  # average GEMM launch (one per linear)
-    achieved = gbytes / n_lin / launch_s / 1e9  # algorithmic bytes per launch / launch time
+    launch_s = gemm_ms_step / n_launch * 1e-3  # average GEMM launch
     mfma_tflops = gexec / (gemm_ms_step * 1e-3) / 1e12
+    hbm_gbs = gbytes / n_launch / launch_s / 1e9  # algorithmic bytes per launch / launch time
+    mfma_bound = wl.backward or wl.m >= 2048
     roofline = {
-        "bound": "hbm",
-        "achieved": round(achieved, 1),
-        "peak": HBM_PEAK_GBS,
-        "unit": "GB/s",
-        "frac": round(achieved / HBM_PEAK_GBS, 4),
+        "bound": "mfma" if mfma_bound else "hbm",
+        "achieved": round(mfma_tflops if mfma_bound else hbm_gbs, 1),
+        "peak": FP4_PEAK_TFLOPS if mfma_bound else HBM_PEAK_GBS,
+        "unit": "TFLOP/s" if mfma_bound else "GB/s",
+        "frac": round(mfma_tflops / FP4_PEAK_TFLOPS if mfma_bound else hbm_gbs / HBM_PEAK_GBS, 4),
         "traffic": gemm_traffic(wl.name, fmt, sp),
-        "kernel": f"gemm_kernel ({n_lin} launches per step, one per linear)",
-        "alg_bytes_per_launch": round(gbytes / n_lin),
+        "kernel": f"gemm_kernel ({n_launch} launches per step)",
+        "alg_bytes_per_launch": round(gbytes / n_launch),
+        "alg_flops_per_launch": round(gexec / n_launch),
         "avg_launch_us": round(launch_s * 1e6, 2),
+        "hbm_gbs": round(hbm_gbs, 1),
         "mfma_exec_tflops": round(mfma_tflops, 1),
         "mfma_exec_frac": round(mfma_tflops / FP4_PEAK_TFLOPS, 4),
     }
@@ -284,9 +349,10 @@ def main() -> int:
             "workload": wl.name,
             "format": fmt,
             "sparsity": sp,
+            "pass": "backward (dX, dW)" if wl.backward else "forward",
             "m": wl.m,
-            "linears": {l.name: [l.d, l.n] for l in wl.linears},
-            "weight_copies_rotated": copies,
+            "linears": {l.name: [l.d, l.n] for l in lins},
+            "copies_rotated": copies,
         },
         "step_hbm": {
             "alg_bytes": int(sbytes),
@@ -298,7 +364,8 @@ def main() -> int:
         "roofline": roofline,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, fmt, sp, args.cpu_sample_cols, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(wl, fmt, sp, args.cpu_sample_cols, args.cpu_sample_rows,
+                                           args.cpu_seconds)
     print(json.dumps(out), flush=True)
     return 0
 

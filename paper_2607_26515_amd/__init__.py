@@ -6,6 +6,10 @@ The computation lives in ``libresq.so`` (hand-written HIP kernels behind the C A
 from .resq import (  # noqa: F401
     EXPORTED,
     FORMATS,
+    OP_LINEAR_BWD,
+    OP_LINEAR_FWD,
+    OP_LINEAR_FWD_PREPARED,
+    OP_RESIDUAL_SPARSIFY,
     SPARSITY,
     ResqError,
     library_path,
