@@ -184,6 +184,12 @@ int check_activation_args(int format, int sparsity, const void* X, int64_t m, in
     return fail(RESQ_ERR_SHAPE, "d (%lld) is not a multiple of the block size %lld", (long long)d, (long long)block_of(format));
   if (sparsity == RESQ_S_BLOCK32X64_50 && d % 64 != 0)
     return fail(RESQ_ERR_SHAPE, "32x64 block sparsity needs d %% 64 == 0 (d=%lld)", (long long)d);
+  if (sparsity == RESQ_S_CHANNEL50 && d > resq::select_max_items())
+    return fail(RESQ_ERR_UNSUPPORTED, "channel selection supports d <= %lld (d=%lld)",
+                (long long)resq::select_max_items(), (long long)d);
+  if (sparsity == RESQ_S_BLOCK32X64_50 && ((m + 31) / 32) * (d / 64) > resq::select_max_items())
+    return fail(RESQ_ERR_UNSUPPORTED, "block selection supports ceil(m/32)*(d/64) <= %lld blocks",
+                (long long)resq::select_max_items());
   if (sparsity == RESQ_S_UNSTRUCT50 && m * d > ((int64_t)1 << 31))
     return fail(RESQ_ERR_UNSUPPORTED, "element-wise 50%% selection supports m*d <= 2^31 (m*d=%lld)", (long long)(m * d));
   if (m > 0 && d > 0 && X == nullptr) return fail(RESQ_ERR_ARG, "X is NULL");

@@ -50,6 +50,7 @@ struct SelectWs {
   uint32_t* tie_counts;  // per-workgroup tie counts (unstructured)
 };
 size_t select_ws_bytes(int sparsity, int fmt, int64_t m, int64_t d);
+int64_t select_max_items();  // most channels / blocks a channel or block selection ranks
 void carve_select_ws(void* base, int sparsity, int fmt, int64_t m, int64_t d, SelectWs& ws);
 void launch_select(int fmt, int sparsity, int64_t m, int64_t d, uint8_t* qr_codes,
                    const void* qr_scales, const double* partials, uint8_t* keep_mask,

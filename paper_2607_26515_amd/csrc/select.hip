@@ -8,7 +8,8 @@
 //                    (exact; written by the residual pass) in column order, float64
 //   element (i, j) : |value(i, j)| (exact in float32), index i * d + j
 // Non-negative IEEE keys order like their bit patterns, so the k-th largest key is found by a
-// most-significant-digit-first radix select on the bits (8-bit digits), after which the keys
+// most-significant-digit-first radix select on the bits (8-bit digits for the float64 channel
+// and block keys; exponent then mantissa digits for the element keys), after which the keys
 // equal to it are ranked by index.  Pruned codes become the +0 code in place.
 #include "kernels.h"
 #include "device_fp4.h"
@@ -48,43 +49,59 @@ __device__ __forceinline__ uint32_t scale_at(const void* scales, int64_t row, in
 }
 
 // ---------------------------------------------------------------------------------------
-// Channel keys.  Workgroup = 64 channels; its four waves decode 64-row chunks into LDS in
-// parallel, then wave 0 adds them row by row (the fixed sequential order).
+// Channel keys.  Workgroup = 64 channels.  Its four waves load a 64-row chunk (16 independent
+// rows per wave, issued together) and decode it into LDS; wave 0 then adds the chunk row by
+// row (the fixed sequential order) while the waves already load the next chunk.
 // ---------------------------------------------------------------------------------------
 constexpr int kChunk = 64;
+
+template <int FMT>
+__device__ __forceinline__ float decode_at(uint32_t cbyte, uint32_t sc, int64_t j) {
+  const uint32_t c = (cbyte >> (4 * (j & 1))) & 15u;
+  if constexpr (FMT == 0) {
+    return mx_value(c, (int)sc - 127);
+  } else {
+    const int p = (int)(j & 63);
+    const int b = (int)((sc >> (8 + p / 8)) & 1u) + (int)((sc >> (16 + p / 4)) & 1u);
+    return hif4_value(c, (int)(sc & 0xFFu), b);
+  }
+}
 
 template <int FMT>
 __global__ __launch_bounds__(kThreads) void channel_keys_kernel(const uint8_t* __restrict__ codes,
                                                                 const void* __restrict__ scales,
                                                                 int64_t m, int64_t d,
                                                                 double* __restrict__ keys) {
-  __shared__ double sq[kChunk][64];
+  constexpr int RPW = kChunk / (kThreads / 64);  // rows per wave per chunk
+  __shared__ float val[kChunk][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t j = (int64_t)blockIdx.x * 64 + lane;
+  uint32_t cb[RPW], sc[RPW];
+  auto load = [&](int64_t r0) {
+#pragma unroll
+    for (int q = 0; q < RPW; ++q) {
+      const int64_t row = r0 + wave + 4 * q;
+      cb[q] = 0;
+      sc[q] = 0;
+      if (row < m && j < d) {
+        cb[q] = codes[row * (d / 2) + j / 2];
+        sc[q] = scale_at<FMT>(scales, row, d, j);
+      }
+    }
+  };
   double acc = 0.0;
+  load(0);
   for (int64_t r0 = 0; r0 < m; r0 += kChunk) {
     const int rows = (int)((m - r0) < kChunk ? (m - r0) : kChunk);
-    for (int rr = wave; rr < rows; rr += kThreads / 64) {
-      double v2 = 0.0;
-      if (j < d) {
-        const int64_t row = r0 + rr;
-        const uint32_t c = (codes[row * (d / 2) + j / 2] >> (4 * (j & 1))) & 15u;
-        const uint32_t sc = scale_at<FMT>(scales, row, d, j);
-        float v;
-        if constexpr (FMT == 0) {
-          v = mx_value(c, (int)sc - 127);
-        } else {
-          const int p = (int)(j & 63);
-          const int b = (int)((sc >> (8 + p / 8)) & 1u) + (int)((sc >> (16 + p / 4)) & 1u);
-          v = hif4_value(c, (int)(sc & 0xFFu), b);
-        }
-        v2 = (double)v * (double)v;  // exact: at most 6 significant bits in v
-      }
-      sq[rr][lane] = v2;
-    }
+#pragma unroll
+    for (int q = 0; q < RPW; ++q) val[wave + 4 * q][lane] = j < d ? decode_at<FMT>(cb[q], sc[q], j) : 0.f;
     __syncthreads();
+    if (r0 + kChunk < m) load(r0 + kChunk);  // in flight while wave 0 adds this chunk
     if (wave == 0)
-      for (int rr = 0; rr < rows; ++rr) acc += sq[rr][lane];
+      for (int rr = 0; rr < rows; ++rr) {
+        const double v = (double)val[rr][lane];
+        acc += v * v;  // the square is exact: at most 6 significant bits in v
+      }
     __syncthreads();
   }
   if (wave == 0 && j < d) keys[j] = acc;
@@ -104,10 +121,17 @@ __global__ __launch_bounds__(kThreads) void block_keys_kernel(const double* __re
   const int64_t I = t / nJ, J = t % nJ;
   const int64_t r1 = (32 * I + 32 < m) ? 32 * I + 32 : m;
   const int64_t ld = d / (FMT == 0 ? 32 : 64);
-  double acc = 0.0;
-  for (int64_t i = 32 * I; i < r1; ++i)
+  double v[32][P];
 #pragma unroll
-    for (int q = 0; q < P; ++q) acc += partials[i * ld + J * P + q];
+  for (int i = 0; i < 32; ++i)  // independent loads, issued together
+#pragma unroll
+    for (int q = 0; q < P; ++q) v[i][q] = 32 * I + i < r1 ? partials[(32 * I + i) * ld + J * P + q] : 0.0;
+  double acc = 0.0;
+#pragma unroll
+  for (int i = 0; i < 32; ++i)  // rows in order, scale blocks in column order
+#pragma unroll
+    for (int q = 0; q < P; ++q)
+      if (32 * I + i < r1) acc += v[i][q];
   keys[t] = acc;
 }
 
@@ -137,71 +161,95 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* w
   return before + x - v;
 }
 
-// Radix digit choice over a 256-bin histogram: the digit holding the krem-th largest key
-// among those matching the prefix; krem becomes its rank among keys with that digit.
-__device__ __forceinline__ void choose_digit(const uint32_t* hist, uint64_t& digit, uint64_t& krem) {
-  uint64_t cum = 0;
-  int b = 255;
-  for (; b > 0; --b) {
-    if (cum + hist[b] >= krem) break;
-    cum += hist[b];
+// Radix digit choice over an LDS histogram of nb <= NT bins: the digit holding the k-th
+// largest key (k >= 1; k = 0 picks the top digit) and k's rank among the keys with that digit.
+// A suffix scan over the bins runs on all threads; every thread of the block must call this,
+// and all read the result from out[0] (digit) and out[1] (rank) after it returns.
+template <int NT>
+__device__ __forceinline__ void choose_digit(const uint32_t* hist, int nb, uint32_t k,
+                                             uint32_t* wsum, uint32_t* out) {
+  const int tid = threadIdx.x;
+  const uint32_t v = tid < nb ? hist[nb - 1 - tid] : 0u;  // bins from the top down
+  uint32_t total;
+  const uint32_t above = block_exclusive_scan<NT>(v, wsum, total);  // keys in higher bins
+  if (tid < nb && ((above < k && k <= above + v) || (k == 0 && tid == 0))) {
+    out[0] = (uint32_t)(nb - 1 - tid);
+    out[1] = k - above;
   }
-  digit = (uint64_t)b;
-  krem -= cum;
+  __syncthreads();
+}
+
+// h[digit] += 1 for every active lane of the wave.  Lanes that share a digit are counted
+// with one LDS atomic (the keys of a selection pass often share a few digits, and per-lane
+// atomics on one address serialize); after four such rounds the rest add one by one.  Every
+// lane of the wave must call this (the digit and active flag may differ per lane).
+__device__ __forceinline__ void hist_add(uint32_t* h, uint32_t digit, bool active) {
+  uint64_t pending = __ballot(active);
+  for (int it = 0; it < 4 && pending != 0; ++it) {
+    const int leader = __ffsll((unsigned long long)pending) - 1;
+    const uint32_t dl = __shfl(digit, leader, 64);
+    const uint64_t same = __ballot(digit == dl) & pending;
+    if (__lane_id() == leader) atomicAdd(&h[dl], (uint32_t)__popcll(same));
+    pending &= ~same;
+  }
+  if ((pending >> __lane_id()) & 1ull) atomicAdd(&h[digit], 1u);
 }
 
 // ---------------------------------------------------------------------------------------
 // Single-workgroup top-k over n float64 keys -> bit mask (bit b of byte i = item 8i + b).
+// Thread t holds keys t, t + 1024, ... in registers (KPT of them: n <= 1024 KPT), loaded once.
 // ---------------------------------------------------------------------------------------
+constexpr int kKeysPerThread = 24;  // n <= 24576: channels of d <= 24576, blocks of m*d <= 50M
+
 __global__ __launch_bounds__(kSelThreads) void select_top_kernel(const uint64_t* __restrict__ keys,
                                                                  int64_t n, int64_t k,
                                                                  uint8_t* __restrict__ bits,
                                                                  uint8_t* __restrict__ bits_copy) {
   __shared__ uint32_t hist[256];
-  __shared__ uint64_t s_prefix, s_krem;
+  __shared__ uint32_t ch[2];
   __shared__ uint32_t wsum[kSelThreads / 64];
   const int tid = threadIdx.x;
+  uint64_t kr[kKeysPerThread];
+#pragma unroll
+  for (int q = 0; q < kKeysPerThread; ++q) {
+    const int64_t i = (int64_t)q * kSelThreads + tid;
+    kr[q] = i < n ? keys[i] : 0;
+  }
   uint64_t prefix = 0, mask = 0;
-  if (tid == 0) { s_prefix = 0; s_krem = (uint64_t)k; }
+  uint32_t krem = (uint32_t)k;
   for (int shift = 56; shift >= 0; shift -= 8) {
     if (tid < 256) hist[tid] = 0;
     __syncthreads();
-    for (int64_t i = tid; i < n; i += kSelThreads) {
-      const uint64_t key = keys[i];
-      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+#pragma unroll
+    for (int q = 0; q < kKeysPerThread; ++q) {
+      const int64_t i = (int64_t)q * kSelThreads + tid;
+      hist_add(hist, (uint32_t)((kr[q] >> shift) & 255u), i < n && (kr[q] & mask) == prefix);
     }
     __syncthreads();
-    if (tid == 0) {
-      uint64_t digit, krem = s_krem;
-      choose_digit(hist, digit, krem);
-      s_prefix |= digit << shift;
-      s_krem = krem;
-    }
-    __syncthreads();
-    prefix = s_prefix;
+    choose_digit<kSelThreads>(hist, 256, krem, wsum, ch);
+    prefix |= (uint64_t)ch[0] << shift;
+    krem = ch[1];
     mask |= (uint64_t)255 << shift;
+    __syncthreads();  // ch and hist are reused by the next pass
   }
-  const uint64_t T = prefix, krem = s_krem;  // threshold key; ties of T to keep (in index order)
-  // each thread owns a contiguous run of whole mask bytes
-  const int64_t nbytes = (n + 7) / 8;
-  const int64_t per = (nbytes + kSelThreads - 1) / kSelThreads;
-  const int64_t b0 = tid * per, b1 = (b0 + per < nbytes) ? b0 + per : nbytes;
-  uint32_t ties = 0;
-  for (int64_t i = 8 * b0; i < 8 * b1 && i < n; ++i) ties += keys[i] == T;
-  uint32_t total;
-  uint64_t rank = block_exclusive_scan<kSelThreads>(ties, wsum, total);
-  for (int64_t bi = b0; bi < b1; ++bi) {
-    uint32_t byte = 0;
-    for (int e = 0; e < 8; ++e) {
-      const int64_t i = 8 * bi + e;
-      if (i >= n) break;
-      const uint64_t key = keys[i];
-      bool keep = key > T;
-      if (key == T) keep = rank++ < krem;
-      byte |= (uint32_t)keep << e;
+  const uint64_t T = prefix;  // threshold key; krem of its ties are kept (in index order)
+  // rank the ties in index order, 1024 consecutive indices per round
+  uint64_t seen = 0;  // ties in earlier rounds
+  const int lane = tid & 63;
+#pragma unroll
+  for (int q = 0; q < kKeysPerThread; ++q) {
+    const int64_t i = (int64_t)q * kSelThreads + tid;
+    const bool in = i < n, tie = in && kr[q] == T;
+    uint32_t total;
+    const uint32_t before = block_exclusive_scan<kSelThreads>(tie ? 1u : 0u, wsum, total);
+    const bool keep = in && (kr[q] > T || (tie && seen + before < krem));
+    const uint64_t bal = __ballot(keep);
+    if ((lane & 7) == 0 && in) {
+      const uint8_t byte = (uint8_t)(bal >> lane);
+      bits[i >> 3] = byte;
+      if (bits_copy) bits_copy[i >> 3] = byte;
     }
-    bits[bi] = (uint8_t)byte;
-    if (bits_copy) bits_copy[bi] = (uint8_t)byte;
+    seen += total;
   }
 }
 
@@ -234,14 +282,18 @@ __global__ __launch_bounds__(kThreads) void apply_groups_kernel(uint32_t* __rest
 }
 
 // ---------------------------------------------------------------------------------------
-// Element-wise 50%: multi-workgroup radix select over float32 |value| bit patterns.
-// state (uint32): [0..3] finished-workgroup counters of the four passes, [4] prefix,
-// [5] ties of the threshold still to keep; hist: four 256-bin histograms.
+// Element-wise 50%: radix select over the float32 |value| patterns of the decoded Q(dX).
+// FP4 values of both formats have no set bits below mantissa bit 17 (MXFP4: at most two
+// significant bits, subnormal only in bits 21-22; HiF4: k (4+m) < 64 at a normal exponent),
+// so two digit passes fix the threshold exactly: the exponent field (bits 23-30, 256 bins),
+// then mantissa bits 17-22 (64 bins) among the keys with the chosen exponent.
+// hist: [0, 256) exponent counts, [256, 320) mantissa counts.  Each kernel after the first
+// recomputes the choice from the histograms, so no workgroup waits for another.
 // ---------------------------------------------------------------------------------------
-__global__ void unstructured_init_kernel(uint32_t* hist, uint32_t* state, uint32_t k) {
-  const int t = threadIdx.x;
-  for (int i = t; i < 4 * 256; i += blockDim.x) hist[i] = 0;
-  if (t < 8) state[t] = t == 5 ? k : 0u;
+constexpr int kUHist = 320;
+
+__global__ void uzero_kernel(uint32_t* hist) {
+  for (int i = threadIdx.x; i < kUHist; i += blockDim.x) hist[i] = 0;
 }
 
 template <int FMT>
@@ -257,61 +309,77 @@ __device__ __forceinline__ void thread_keys(const uint8_t* codes, const void* sc
   word_keys<FMT>(cw.w, sc, jpos + 24, key + 24);
 }
 
-template <int FMT>
-__global__ __launch_bounds__(kThreads) void unstructured_hist_kernel(const uint8_t* __restrict__ codes,
-                                                                     const void* __restrict__ scales,
-                                                                     int64_t m, int64_t d, int pass,
-                                                                     uint32_t* __restrict__ hist,
-                                                                     uint32_t* __restrict__ state) {
-  __shared__ uint32_t lh[256];
-  __shared__ bool last;
+// Load the histograms into LDS and resolve the threshold (all threads call this): out[0] =
+// exponent digit, out[1] = rank within it; with full, out[2] = threshold key T and out[3] =
+// the number of keys equal to T that are kept.
+__device__ __forceinline__ void load_choice(const uint32_t* hist, uint32_t* lh, uint32_t k, bool full,
+                                            uint32_t* wsum, uint32_t* out) {
+  for (int i = threadIdx.x; i < kUHist; i += blockDim.x) lh[i] = hist[i];
+  __syncthreads();
+  choose_digit<kThreads>(lh, 256, k, wsum, out);
+  if (full) {
+    const uint32_t de = out[0], ke = out[1];
+    __syncthreads();
+    choose_digit<kThreads>(lh + 256, 64, ke, wsum, out + 2);
+    const uint32_t dm = out[2];
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      out[0] = de;
+      out[1] = ke;
+      out[2] = (de << 23) | (dm << 17);
+    }
+    __syncthreads();
+  }
+}
+
+template <int FMT, int PASS>
+__global__ __launch_bounds__(kThreads) void uhist_kernel(const uint8_t* __restrict__ codes,
+                                                         const void* __restrict__ scales, int64_t m,
+                                                         int64_t d, uint32_t* __restrict__ hist) {
+  __shared__ uint32_t lh[kUHist];
+  __shared__ uint32_t ch[4];
+  __shared__ uint32_t wsum[kThreads / 64];
   const int tid = threadIdx.x;
-  lh[tid] = 0;
+  uint32_t want = 0;
+  if constexpr (PASS == 1) {
+    load_choice(hist, lh, (uint32_t)(m * d / 2), false, wsum, ch);
+    want = ch[0];
+    __syncthreads();  // lh is cleared below
+  }
+  for (int i = tid; i < kUHist; i += kThreads) lh[i] = 0;
   __syncthreads();
-  const int shift = 24 - 8 * pass;
-  const uint32_t mask = pass == 0 ? 0u : (0xFFFFFFFFu << (32 - 8 * pass));
-  const uint32_t prefix = state[4];
-  const int64_t words = m * (d / 8);
   const int64_t w0 = ((int64_t)blockIdx.x * kThreads + tid) * kWordsPerThread;
-  if (w0 < words) {
-    uint32_t key[32];
-    thread_keys<FMT>(codes, scales, d, w0, key);
+  const bool in = w0 < m * (d / 8);
+  uint32_t key[32];
+  if (in) thread_keys<FMT>(codes, scales, d, w0, key);
+  else
 #pragma unroll
-    for (int e = 0; e < 32; ++e)
-      if ((key[e] & mask) == prefix) atomicAdd(&lh[(key[e] >> shift) & 255u], 1u);
+    for (int e = 0; e < 32; ++e) key[e] = 0;
+#pragma unroll
+  for (int e = 0; e < 32; ++e) {
+    if constexpr (PASS == 0) hist_add(lh, key[e] >> 23, in);
+    else hist_add(lh, (key[e] >> 17) & 63u, in && (key[e] >> 23) == want);
   }
   __syncthreads();
-  if (lh[tid]) atomicAdd(&hist[pass * 256 + tid], lh[tid]);
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) last = atomicAdd(&state[pass], 1u) == gridDim.x - 1;
-  __syncthreads();
-  if (!last) return;
-  // the last workgroup to finish picks the digit for the next pass
-  __threadfence();
-  lh[tid] = __hip_atomic_load(&hist[pass * 256 + tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  __syncthreads();
-  if (tid == 0) {
-    uint64_t digit, krem = state[5];
-    choose_digit(lh, digit, krem);
-    state[4] = prefix | ((uint32_t)digit << shift);
-    state[5] = (uint32_t)krem;
-  }
+  constexpr int NB = PASS == 0 ? 256 : 64, OFF = PASS == 0 ? 0 : 256;
+  for (int b = tid; b < NB; b += kThreads)
+    if (lh[b]) atomicAdd(&hist[OFF + b], lh[b]);
 }
 
 // Threshold ties per workgroup (index order = workgroup order, then thread order).
 template <int FMT>
-__global__ __launch_bounds__(kThreads) void unstructured_ties_kernel(const uint8_t* __restrict__ codes,
-                                                                     const void* __restrict__ scales,
-                                                                     int64_t m, int64_t d,
-                                                                     const uint32_t* __restrict__ state,
-                                                                     uint32_t* __restrict__ tie_counts) {
+__global__ __launch_bounds__(kThreads) void uties_kernel(const uint8_t* __restrict__ codes,
+                                                         const void* __restrict__ scales, int64_t m,
+                                                         int64_t d, const uint32_t* __restrict__ hist,
+                                                         uint32_t* __restrict__ tie_counts) {
+  __shared__ uint32_t lh[kUHist];
+  __shared__ uint32_t ch[4];
   __shared__ uint32_t wsum[kThreads / 64];
-  const uint32_t T = state[4];
-  const int64_t words = m * (d / 8);
+  load_choice(hist, lh, (uint32_t)(m * d / 2), true, wsum, ch);
+  const uint32_t T = ch[2];
   const int64_t w0 = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * kWordsPerThread;
   uint32_t ties = 0;
-  if (w0 < words) {
+  if (w0 < m * (d / 8)) {
     uint32_t key[32];
     thread_keys<FMT>(codes, scales, d, w0, key);
 #pragma unroll
@@ -322,46 +390,33 @@ __global__ __launch_bounds__(kThreads) void unstructured_ties_kernel(const uint8
   if (threadIdx.x == 0) tie_counts[blockIdx.x] = total;
 }
 
-// Exclusive scan of the per-workgroup tie counts, in place (one workgroup).
-__global__ __launch_bounds__(kSelThreads) void scan_counts_kernel(uint32_t* __restrict__ c, int64_t n) {
-  __shared__ uint32_t wsum[kSelThreads / 64];
-  __shared__ uint32_t carry;
-  if (threadIdx.x == 0) carry = 0;
-  __syncthreads();
-  for (int64_t base = 0; base < n; base += kSelThreads) {
-    const int64_t i = base + threadIdx.x;
-    const uint32_t v = i < n ? c[i] : 0u;
-    uint32_t total;
-    const uint32_t ex = block_exclusive_scan<kSelThreads>(v, wsum, total);
-    const uint32_t cy = carry;
-    if (i < n) c[i] = cy + ex;
-    __syncthreads();
-    if (threadIdx.x == 0) carry = cy + total;
-    __syncthreads();
-  }
-}
-
 template <int FMT>
-__global__ __launch_bounds__(kThreads) void unstructured_apply_kernel(uint8_t* __restrict__ codes,
-                                                                      const void* __restrict__ scales,
-                                                                      int64_t m, int64_t d,
-                                                                      const uint32_t* __restrict__ state,
-                                                                      const uint32_t* __restrict__ tie_offsets,
-                                                                      uint8_t* __restrict__ keep_mask) {
+__global__ __launch_bounds__(kThreads) void uapply_kernel(uint8_t* __restrict__ codes,
+                                                          const void* __restrict__ scales, int64_t m,
+                                                          int64_t d, const uint32_t* __restrict__ hist,
+                                                          const uint32_t* __restrict__ tie_counts,
+                                                          uint8_t* __restrict__ keep_mask) {
+  __shared__ uint32_t lh[kUHist];
+  __shared__ uint32_t ch[4];
   __shared__ uint32_t wsum[kThreads / 64];
-  const uint32_t T = state[4], krem = state[5];
-  const int64_t words = m * (d / 8);
+  load_choice(hist, lh, (uint32_t)(m * d / 2), true, wsum, ch);
+  const uint32_t T = ch[2], krem = ch[3];
+  // ties kept by earlier workgroups
+  uint32_t before = 0;
+  for (int64_t w = threadIdx.x; w < (int64_t)blockIdx.x; w += kThreads) before += tie_counts[w];
+  uint32_t tot_before;
+  block_exclusive_scan<kThreads>(before, wsum, tot_before);
   const int64_t w0 = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * kWordsPerThread;
+  const bool in = w0 < m * (d / 8);
   uint32_t key[32];
   uint32_t ties = 0;
-  const bool in = w0 < words;
   if (in) {
     thread_keys<FMT>(codes, scales, d, w0, key);
 #pragma unroll
     for (int e = 0; e < 32; ++e) ties += key[e] == T;
   }
   uint32_t total;
-  uint32_t rank = tie_offsets[blockIdx.x] + block_exclusive_scan<kThreads>(ties, wsum, total);
+  uint32_t rank = tot_before + block_exclusive_scan<kThreads>(ties, wsum, total);
   if (!in) return;
   uint32_t kept = 0;  // 32 keep bits
 #pragma unroll
@@ -391,6 +446,8 @@ int64_t n_blocks(int64_t m, int64_t d) { return ((m + 31) / 32) * (d / 64); }
 
 }  // namespace
 
+int64_t select_max_items() { return (int64_t)kKeysPerThread * kSelThreads; }
+
 size_t select_ws_bytes(int sparsity, int fmt, int64_t m, int64_t d) {
   (void)fmt;
   switch (sparsity) {
@@ -399,7 +456,7 @@ size_t select_ws_bytes(int sparsity, int fmt, int64_t m, int64_t d) {
     case 4:  // block
       return a256((size_t)n_blocks(m, d) * 8) + a256((size_t)(n_blocks(m, d) + 31) / 32 * 4);
     case 5:  // element-wise
-      return a256(4 * 256 * 4) + a256(8 * 4) + a256((size_t)unstructured_wgs(m, d) * 4);
+      return a256(kUHist * 4) + a256((size_t)unstructured_wgs(m, d) * 4);
     default:
       return 0;
   }
@@ -415,8 +472,7 @@ void carve_select_ws(void* base, int sparsity, int fmt, int64_t m, int64_t d, Se
     ws.group_bits = (uint8_t*)(p + a256((size_t)n * 8));
   } else if (sparsity == 5) {
     ws.hist = (uint32_t*)p;
-    ws.state = (uint32_t*)(p + a256(4 * 256 * 4));
-    ws.tie_counts = (uint32_t*)(p + a256(4 * 256 * 4) + a256(8 * 4));
+    ws.tie_counts = (uint32_t*)(p + a256(kUHist * 4));
   }
 }
 
@@ -444,18 +500,17 @@ void launch_select(int fmt, int sparsity, int64_t m, int64_t d, uint8_t* qr_code
     hipLaunchKernelGGL((apply_groups_kernel<1>), dim3(gw), dim3(kThreads), 0, s,
                        (uint32_t*)qr_codes, m, d, (const uint8_t*)ws.group_bits, keep_mask);
   } else if (sparsity == 5) {
-    const int64_t nwg = unstructured_wgs(m, d);
-    hipLaunchKernelGGL(unstructured_init_kernel, dim3(1), dim3(kThreads), 0, s, ws.hist, ws.state,
-                       (uint32_t)(m * d / 2));
-    for (int pass = 0; pass < 4; ++pass) {
-      if (fmt == 0) hipLaunchKernelGGL((unstructured_hist_kernel<0>), dim3((unsigned)nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, pass, ws.hist, ws.state);
-      else hipLaunchKernelGGL((unstructured_hist_kernel<1>), dim3((unsigned)nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, pass, ws.hist, ws.state);
-    }
-    if (fmt == 0) hipLaunchKernelGGL((unstructured_ties_kernel<0>), dim3((unsigned)nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, (const uint32_t*)ws.state, ws.tie_counts);
-    else hipLaunchKernelGGL((unstructured_ties_kernel<1>), dim3((unsigned)nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, (const uint32_t*)ws.state, ws.tie_counts);
-    hipLaunchKernelGGL(scan_counts_kernel, dim3(1), dim3(kSelThreads), 0, s, ws.tie_counts, nwg);
-    if (fmt == 0) hipLaunchKernelGGL((unstructured_apply_kernel<0>), dim3((unsigned)nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, (const uint32_t*)ws.state, (const uint32_t*)ws.tie_counts, keep_mask);
-    else hipLaunchKernelGGL((unstructured_apply_kernel<1>), dim3((unsigned)nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, (const uint32_t*)ws.state, (const uint32_t*)ws.tie_counts, keep_mask);
+    const unsigned nwg = (unsigned)unstructured_wgs(m, d);
+    hipLaunchKernelGGL(uzero_kernel, dim3(1), dim3(kThreads), 0, s, ws.hist);
+#define RESQ_U(F)                                                                                          \
+    hipLaunchKernelGGL((uhist_kernel<F, 0>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, ws.hist);   \
+    hipLaunchKernelGGL((uhist_kernel<F, 1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, ws.hist);   \
+    hipLaunchKernelGGL((uties_kernel<F>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d,                 \
+                       (const uint32_t*)ws.hist, ws.tie_counts);                                                      \
+    hipLaunchKernelGGL((uapply_kernel<F>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d,                \
+                       (const uint32_t*)ws.hist, (const uint32_t*)ws.tie_counts, keep_mask);
+    if (fmt == 0) { RESQ_U(0) } else { RESQ_U(1) }
+#undef RESQ_U
   }
 }
 
