@@ -45,14 +45,10 @@ def exec_mfma_flops(m, d, n, fmt, sp):
     """FP4-rate MFMA work issued by the GEMM (MFMA FLOPs at the FP4/FP6 rate).
 
     MXFP4 runs one MFMA per K-step for Q(X) and one for the residual; HiF4 runs two
-    (hi/lo E2M3 operands) for each.  The 2:4 / channel / element-wise residuals are dense
-    operands with zeros on gfx950 (no FP4 sparse MFMA); pruned 32x64 blocks are skipped."""
+    (hi/lo E2M3 operands) for each.  Every residual kind runs as a dense operand with zeros
+    on gfx950 (no FP4 sparse MFMA)."""
     per_term = 2 * m * d * n * (2 if fmt == "hif4" else 1)
-    if sp == "none":
-        return per_term
-    if sp == "block32x64_50":
-        return per_term * 1.5
-    return per_term * 2
+    return per_term if sp == "none" else 2 * per_term
 
 
 def step_bytes(m, d, n, fmt):

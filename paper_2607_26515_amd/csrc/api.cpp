@@ -337,7 +337,6 @@ int linear_fwd_core(int format, int sparsity, const uint16_t* X, int64_t m, int6
   op.fmt = format;
   op.M = m; op.N = n; op.K = d;
   op.n_terms = sparsity == RESQ_S_NONE ? 1 : 2;
-  op.blockmask = sparsity == RESQ_S_BLOCK32X64_50 ? w.sel.group_bits : nullptr;
   op.a_frag[0] = w.frag_x; op.a_sc[0] = w.fsc_x;
   op.a_frag[1] = w.frag_r; op.a_sc[1] = w.fsc_r;
   carve_prepared(wprep, format, n, d, &op.b_frag, &op.b_sc);
@@ -357,7 +356,7 @@ int check_fwd_args(int format, int sparsity, const uint16_t* X, int64_t m, int64
   if (n < 0) return fail(RESQ_ERR_ARG, "negative n");
   if (ldy < n) return fail(RESQ_ERR_ARG, "ldy (%lld) < n (%lld)", (long long)ldy, (long long)n);
   if (m > 0 && n > 0 && !Y) return fail(RESQ_ERR_ARG, "Y is NULL");
-  if (!resq::gemm_supported(format, m, n, d, sparsity == RESQ_S_BLOCK32X64_50))
+  if (!resq::gemm_supported(format, m, n, d))
     return fail(RESQ_ERR_UNSUPPORTED, "GEMM operands too large for 32-bit offsets (m=%lld, d=%lld, n=%lld)",
                 (long long)m, (long long)d, (long long)n);
   return ok();
@@ -416,8 +415,8 @@ int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uin
   if (dW && m % B != 0) return fail(RESQ_ERR_SHAPE, "dW needs m (%lld) %% %lld == 0", (long long)m, (long long)B);
   if (m == 0 || d == 0 || n == 0) return ok();
   if (!dY || (dX && !W) || (dW && !X)) return fail(RESQ_ERR_ARG, "NULL input pointer");
-  if ((dX && !resq::gemm_supported(format, m, d, n, false)) ||
-      (dW && !resq::gemm_supported(format, n, d, m, false)))
+  if ((dX && !resq::gemm_supported(format, m, d, n)) ||
+      (dW && !resq::gemm_supported(format, n, d, m)))
     return fail(RESQ_ERR_UNSUPPORTED, "GEMM operands too large for 32-bit offsets");
   BwdWs w{};
   const size_t need = carve_bwd(workspace, format, m, d, n, &w);

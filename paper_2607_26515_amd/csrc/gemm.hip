@@ -42,14 +42,12 @@ typedef __attribute__((address_space(3))) void* lds_ptr_t;
 constexpr int kXcds = 8;
 constexpr uint32_t kBad = 0xFFFFFFF0u;  // an offset past every operand: the load returns 0
 constexpr int kDumpBytes = 1024;         // LDS target of the padding copies (never read)
-constexpr int kMaxMaskWords = 64;        // block-skip bits per row tile held in LDS
 
 struct GemmParams {
   int64_t M, N, K, nkb, mt_tiles, nt_tiles;
   const uint8_t* a_frag[2];
   const uint8_t* a_sc[2];
   uint32_t a_frag_bytes, a_sc_bytes, b_frag_bytes, b_sc_bytes;
-  const uint8_t* blockmask;  // kept 32x64 residual blocks, bits row-major over (mt_tiles, nkb)
   const uint8_t* b_frag;
   const uint8_t* b_sc;
   float* Y;
@@ -118,14 +116,13 @@ struct Geo {
   static constexpr int SB_OFF = SA_OFF + NT * SAJ * 256;
   static constexpr int DUMP_OFF = (SB_OFF + SBJ * 256 + 255) / 256 * 256;  // padding copies
   static constexpr int STAGE = DUMP_OFF + kDumpBytes;
-  static constexpr int MASK_OFF = NS * STAGE;
   // copy instructions per stage by size class, and per wave (padded to a multiple of W)
   static constexpr int J16 = NT * MTW * PA + (FMT == 0 ? NTW : 0);
   static constexpr int J12 = FMT == 0 ? 0 : 2 * NTW;
   static constexpr int J4 = NT * SAJ + SBJ;
   static constexpr int S16 = (J16 + W - 1) / W, S12 = (J12 + W - 1) / W, S4 = (J4 + W - 1) / W;
   static constexpr int JW = S16 + S12 + S4;
-  static size_t lds_bytes(bool bs) { return (size_t)MASK_OFF + (bs ? MTW * kMaxMaskWords * 4 : 0); }
+  static size_t lds_bytes() { return (size_t)NS * STAGE; }
   static_assert(NS >= 2, "at least two stages");
 };
 
@@ -138,7 +135,7 @@ struct Copy {
   uint32_t bytes, off, step, lds;
 };
 
-template <int FMT, int WM, int WN, int TM, int TN, int NT, int NS, bool BS>
+template <int FMT, int WM, int WN, int TM, int TN, int NT, int NS>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(GemmParams p) {
   using G = Geo<FMT, WM, WN, TM, TN, NT, NS>;
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
@@ -221,22 +218,6 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(GemmParams p) {
       copy_to_lds<4>(c4[x].base, in ? c4[x].bytes : 0u, st + c4[x].lds, c4[x].off + kb * c4[x].step);
   };
 
-  // Block-skip bits of this workgroup's row tiles, all K steps, held in LDS.
-  uint32_t* maskw = reinterpret_cast<uint32_t*>(smem + G::MASK_OFF);
-  if constexpr (BS) {
-    const int words = (int)((nkb + 31) / 32);
-    for (int e = tid; e < G::MTW * words; e += G::kThreads) {
-      const int i = e / words, w = e % words;
-      uint32_t v = 0;
-      if (T0 + i < (uint32_t)p.mt_tiles)
-        for (int bit = 0; bit < 32 && 32 * w + bit < (int)nkb; ++bit) {
-          const int64_t idx = (int64_t)(T0 + i) * nkb + 32 * w + bit;
-          v |= (uint32_t)((p.blockmask[idx >> 3] >> (idx & 7)) & 1) << bit;
-        }
-      maskw[i * kMaxMaskWords + w] = v;
-    }
-  }
-
   v16f acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
@@ -293,20 +274,12 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(GemmParams p) {
   // Tiles past the edge of the output hold zero operands, so they are computed like the
   // others (their results are never stored) and the MFMAs stay branch-free.  Term-major
   // order keeps the TM x TN independent accumulator chains interleaved.
-  auto mma = [&](const Frag& f, uint32_t kb) {
-    bool res[TM];
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      res[i] = NT > 1;
-      if constexpr (BS)
-        res[i] = kb < nkb && ((maskw[(wm * TM + i) * kMaxMaskWords + kb / 32] >> (kb % 32)) & 1u);
-    }
+  auto mma = [&](const Frag& f) {
     if constexpr (FMT == 0) {
 #pragma unroll
       for (int t = 0; t < NT; ++t)
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
-          if (t > 0 && !res[i]) continue;  // wave-uniform (32x64 block skip)
 #pragma unroll
           for (int j = 0; j < TN; ++j)
             acc[i][j] = mfma<4, 4>(f.a[t][i][0], f.b[j], acc[i][j], f.sa[t][i], f.sb[j]);
@@ -325,7 +298,6 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(GemmParams p) {
         for (int h = 0; h < 2; ++h)
 #pragma unroll
           for (int i = 0; i < TM; ++i) {
-            if (t > 0 && !res[i]) continue;  // wave-uniform (32x64 block skip)
             const int sa = (f.sa[t][i] >> 2) + (h == 0 ? 97 : 93);
 #pragma unroll
             for (int j = 0; j < TN; ++j)
@@ -352,7 +324,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(GemmParams p) {
 #pragma unroll
   for (int s = 0; s < NS; ++s) issue(s, (uint32_t)s);
   wait_vmcnt<(NS - 1) * G::JW>();
-  __syncthreads();  // also publishes the block-skip table
+  __syncthreads();
   read(F[0], 0);
   for (uint32_t k0 = 0; k0 < klen; k0 += U) {
 #pragma unroll
@@ -362,7 +334,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(GemmParams p) {
       lds_barrier();
       issue(u % NS, k + NS);
       read(F[(u + 1) & 1], (u + 1) % NS);
-      mma(F[u & 1], k < klen ? kbeg + k : nkb);
+      mma(F[u & 1]);
       __builtin_amdgcn_sched_barrier(0);  // keep step k's MFMAs ahead of step k+1's barrier
     }
   }
@@ -428,12 +400,10 @@ void launch_cfg(GemmParams p, int n_terms, hipStream_t s) {
   const dim3 block(64 * WM * WN);
   using G2 = Geo<FMT, WM, WN, TM, TN, 2, NS>;
   using G1 = Geo<FMT, WM, WN, TM, TN, 1, NS>;
-  if (n_terms > 1 && p.blockmask != nullptr)
-    hipLaunchKernelGGL((gemm_kernel<FMT, WM, WN, TM, TN, 2, NS, true>), grid, block, G2::lds_bytes(true), s, p);
-  else if (n_terms > 1)
-    hipLaunchKernelGGL((gemm_kernel<FMT, WM, WN, TM, TN, 2, NS, false>), grid, block, G2::lds_bytes(false), s, p);
+  if (n_terms > 1)
+    hipLaunchKernelGGL((gemm_kernel<FMT, WM, WN, TM, TN, 2, NS>), grid, block, G2::lds_bytes(), s, p);
   else
-    hipLaunchKernelGGL((gemm_kernel<FMT, WM, WN, TM, TN, 1, NS, false>), grid, block, G1::lds_bytes(false), s, p);
+    hipLaunchKernelGGL((gemm_kernel<FMT, WM, WN, TM, TN, 1, NS>), grid, block, G1::lds_bytes(), s, p);
   if (p.ksplit > 1)
     hipLaunchKernelGGL((splitk_reduce_kernel<WM, WN, TM, TN>), dim3((unsigned)(p.grid_m * p.grid_n)), dim3(256), 0, s,
                        (const float*)p.partial, p.ksplit, p.grid_m, p.M, p.N, p.Y, p.ldy);
@@ -494,12 +464,10 @@ void launch_fmt(const GemmParams& p, int cfg, int n_terms, hipStream_t s) {
 
 }  // namespace
 
-bool gemm_supported(int fmt, int64_t M, int64_t N, int64_t K, bool block_skip) {
+bool gemm_supported(int fmt, int64_t M, int64_t N, int64_t K) {
   const int amode = fmt == 0 ? kPackMx : kPackHiA, bmode = fmt == 0 ? kPackMx : kPackHiB;
   const size_t lim = (size_t)kBad - (1u << 20);  // 32-bit buffer offsets with headroom
-  if (frag_bytes(amode, M, K) >= lim || frag_bytes(bmode, N, K) >= lim) return false;
-  if (block_skip && (K + 63) / 64 > (int64_t)kMaxMaskWords * 32) return false;
-  return true;
+  return frag_bytes(amode, M, K) < lim && frag_bytes(bmode, N, K) < lim;
 }
 
 size_t gemm_split_scratch(int fmt, int64_t M, int64_t N, int64_t K) {
@@ -518,7 +486,6 @@ void launch_gemm(const GemmOperands& op, hipStream_t s) {
   p.mt_tiles = (op.M + 31) / 32;
   p.nt_tiles = (op.N + 31) / 32;
   for (int t = 0; t < 2; ++t) { p.a_frag[t] = op.a_frag[t]; p.a_sc[t] = op.a_sc[t]; }
-  p.blockmask = op.blockmask;
   p.b_frag = op.b_frag; p.b_sc = op.b_sc;
   p.Y = op.Y; p.ldy = op.ldy;
   const int amode = op.fmt == 0 ? kPackMx : kPackHiA, bmode = op.fmt == 0 ? kPackMx : kPackHiB;

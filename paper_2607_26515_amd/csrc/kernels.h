@@ -64,7 +64,6 @@ struct GemmOperands {
   const uint8_t* a_frag[2];
   const uint8_t* a_sc[2];
   int n_terms;               // 1 (Eq. 1) or 2 (with the residual term)
-  const uint8_t* blockmask;  // optional: residual kept-block bits, (ceil(M/32), K/64) row-major
   const uint8_t* b_frag;
   const uint8_t* b_sc;
   float* Y;
@@ -75,8 +74,7 @@ struct GemmOperands {
 void launch_gemm(const GemmOperands& op, hipStream_t s);
 // Scratch bytes a launch_gemm of this shape uses for its K split (0: it does not split).
 size_t gemm_split_scratch(int fmt, int64_t M, int64_t N, int64_t K);
-// Whether launch_gemm handles these sizes (32-bit operand offsets; the block-skip mask of a
-// row tile fits the kernel's LDS table).
-bool gemm_supported(int fmt, int64_t M, int64_t N, int64_t K, bool block_skip);
+// Whether launch_gemm handles these sizes (32-bit operand offsets).
+bool gemm_supported(int fmt, int64_t M, int64_t N, int64_t K);
 
 }  // namespace resq
