@@ -88,6 +88,32 @@ struct ActWs {
 int a_pack_mode(int fmt) { return fmt == RESQ_MXFP4 ? resq::kPackMx : resq::kPackHiA; }
 int b_pack_mode(int fmt) { return fmt == RESQ_MXFP4 ? resq::kPackMx : resq::kPackHiB; }
 
+// GEMM operands from fragment / scale arrays: every array of A lies at or after a_frag[0]
+// (its buffer starts there), every array of B at or after b_frag.  launch_gemm rejects
+// offsets outside the buffers.
+resq::GemmOperands gemm_operands(int fmt, int64_t M, int64_t N, int64_t K, int n_terms,
+                                 const uint8_t* const a_frag[2], const uint8_t* const a_sc[2],
+                                 const uint8_t* b_frag, const uint8_t* b_sc, float* Y, int64_t ldy) {
+  resq::GemmOperands op{};
+  op.fmt = fmt;
+  op.M = M; op.N = N; op.K = K;
+  op.n_terms = n_terms;
+  const size_t af = resq::frag_bytes(a_pack_mode(fmt), M, K), bf = resq::frag_bytes(b_pack_mode(fmt), N, K);
+  const size_t as = resq::frag_scale_bytes(M, K), bs = resq::frag_scale_bytes(N, K);
+  op.a = a_frag[0];
+  for (int t = 0; t < n_terms; ++t) {
+    op.a_frag_off[t] = (size_t)(a_frag[t] - op.a);
+    op.a_sc_off[t] = (size_t)(a_sc[t] - op.a);
+    op.a_bytes = std::max(op.a_bytes, std::max(op.a_frag_off[t] + af, op.a_sc_off[t] + as));
+  }
+  op.b = b_frag;
+  op.b_frag_off = 0;
+  op.b_sc_off = (size_t)(b_sc - b_frag);
+  op.b_bytes = std::max(bf, op.b_sc_off + bs);
+  op.Y = Y; op.ldy = ldy;
+  return op;
+}
+
 size_t carve_select(Carver& c, int fmt, int sp, int64_t m, int64_t d, double** partials,
                     resq::SelectWs* sel) {
   const size_t start = c.off;
@@ -333,18 +359,16 @@ int linear_fwd_core(int format, int sparsity, const uint16_t* X, int64_t m, int6
     resq::launch_residual(format, resid_mode(sparsity), X, m, d, ldx, w.frag_x, w.fsc_x,
                           w.frag_r, w.fsc_r, nullptr, nullptr, s, true);
   }
-  resq::GemmOperands op{};
-  op.fmt = format;
-  op.M = m; op.N = n; op.K = d;
-  op.n_terms = sparsity == RESQ_S_NONE ? 1 : 2;
-  op.a_frag[0] = w.frag_x; op.a_sc[0] = w.fsc_x;
-  op.a_frag[1] = w.frag_r; op.a_sc[1] = w.fsc_r;
-  carve_prepared(wprep, format, n, d, &op.b_frag, &op.b_sc);
-  op.Y = Y; op.ldy = ldy;
+  const uint8_t* af[2] = {w.frag_x, w.frag_r};
+  const uint8_t* asc[2] = {w.fsc_x, w.fsc_r};
+  const uint8_t *bf, *bsc;
+  carve_prepared(wprep, format, n, d, &bf, &bsc);
+  resq::GemmOperands op = gemm_operands(format, m, n, d, sparsity == RESQ_S_NONE ? 1 : 2, af, asc,
+                                        bf, bsc, Y, ldy);
   op.partial = w.gemm_partial;
   {
     resq::ProfScope prof_(resq::kProfGemm, s);
-    resq::launch_gemm(op, s);
+    if (!resq::launch_gemm(op, s)) return fail(RESQ_ERR_UNSUPPORTED, "GEMM operand layout rejected");
   }
   return check_launch("resq_linear_fwd");
 }
@@ -356,7 +380,7 @@ int check_fwd_args(int format, int sparsity, const uint16_t* X, int64_t m, int64
   if (n < 0) return fail(RESQ_ERR_ARG, "negative n");
   if (ldy < n) return fail(RESQ_ERR_ARG, "ldy (%lld) < n (%lld)", (long long)ldy, (long long)n);
   if (m > 0 && n > 0 && !Y) return fail(RESQ_ERR_ARG, "Y is NULL");
-  if (!resq::gemm_supported(format, m, n, d))
+  if (!resq::gemm_supported(format, m, n, d, sparsity == RESQ_S_NONE ? 1 : 2))
     return fail(RESQ_ERR_UNSUPPORTED, "GEMM operands too large for 32-bit offsets (m=%lld, d=%lld, n=%lld)",
                 (long long)m, (long long)d, (long long)n);
   return ok();
@@ -415,8 +439,8 @@ int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uin
   if (dW && m % B != 0) return fail(RESQ_ERR_SHAPE, "dW needs m (%lld) %% %lld == 0", (long long)m, (long long)B);
   if (m == 0 || d == 0 || n == 0) return ok();
   if (!dY || (dX && !W) || (dW && !X)) return fail(RESQ_ERR_ARG, "NULL input pointer");
-  if ((dX && !resq::gemm_supported(format, m, d, n)) ||
-      (dW && !resq::gemm_supported(format, n, d, m)))
+  if ((dX && !resq::gemm_supported(format, m, d, n, 1)) ||
+      (dW && !resq::gemm_supported(format, n, d, m, 1)))
     return fail(RESQ_ERR_UNSUPPORTED, "GEMM operands too large for 32-bit offsets");
   BwdWs w{};
   const size_t need = carve_bwd(workspace, format, m, d, n, &w);
@@ -438,12 +462,11 @@ int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uin
       resq::launch_pack(a_pack_mode(format), w.dyn_codes, w.dyn_scales, m, n, w.fa, w.fa_sc, s);
       resq::launch_pack(b_pack_mode(format), w.wn_codes, w.wn_scales, d, n, w.fb, w.fb_sc, s);
     }
-    resq::GemmOperands op{};
-    op.fmt = format; op.M = m; op.N = d; op.K = n; op.n_terms = 1;
-    op.a_frag[0] = w.fa; op.a_sc[0] = w.fa_sc;
-    op.b_frag = w.fb; op.b_sc = w.fb_sc; op.Y = dX; op.ldy = d;
+    const uint8_t* af[2] = {w.fa, w.fa};
+    const uint8_t* asc[2] = {w.fa_sc, w.fa_sc};
+    const resq::GemmOperands op = gemm_operands(format, m, d, n, 1, af, asc, w.fb, w.fb_sc, dX, d);
     resq::ProfScope prof_(resq::kProfGemm, s);
-    resq::launch_gemm(op, s);
+    if (!resq::launch_gemm(op, s)) return fail(RESQ_ERR_UNSUPPORTED, "GEMM operand layout rejected");
   }
   if (dW) {
     // dW[n][d] = Q_m(dY)^T [n][m] . (Q_m(X)^T [d][m])^T : contraction over m
@@ -457,12 +480,11 @@ int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uin
       resq::launch_pack(a_pack_mode(format), w.dym_codes, w.dym_scales, n, m, w.fa, w.fa_sc, s);
       resq::launch_pack(b_pack_mode(format), w.xm_codes, w.xm_scales, d, m, w.fb, w.fb_sc, s);
     }
-    resq::GemmOperands op{};
-    op.fmt = format; op.M = n; op.N = d; op.K = m; op.n_terms = 1;
-    op.a_frag[0] = w.fa; op.a_sc[0] = w.fa_sc;
-    op.b_frag = w.fb; op.b_sc = w.fb_sc; op.Y = dW; op.ldy = d;
+    const uint8_t* af[2] = {w.fa, w.fa};
+    const uint8_t* asc[2] = {w.fa_sc, w.fa_sc};
+    const resq::GemmOperands op = gemm_operands(format, n, d, m, 1, af, asc, w.fb, w.fb_sc, dW, d);
     resq::ProfScope prof_(resq::kProfGemm, s);
-    resq::launch_gemm(op, s);
+    if (!resq::launch_gemm(op, s)) return fail(RESQ_ERR_UNSUPPORTED, "GEMM operand layout rejected");
   }
   return check_launch("resq_linear_bwd");
 }

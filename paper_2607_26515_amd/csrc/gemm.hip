@@ -6,7 +6,8 @@
 // bits (FP6) per element from bit 0 upwards; its E8M0 scale covers those 32 elements.
 // Accumulator register r of lane l is row 8*(r/4) + 4*(l/32) + r%4, column l%32.
 // Operands arrive "fragment-major" (pack.hip): fragment (tile, kb) is 64 consecutive lane
-// records, plus one scale byte per lane in a separate array.
+// records, plus one scale byte per lane in a separate array; all arrays of operand A (every
+// term) share one buffer, and so do those of operand B.
 //
 // MXFP4 maps directly: E2M1 codes and E8M0 scales are the MFMA's own formats.
 // HiF4: the level-1 scale s1 = 2^e (1 + m/4) is not a power of two, so no FP4/FP6 operand
@@ -22,8 +23,10 @@
 // 12- and 4-byte copy instructions per stage, so one explicit vmcnt wait per step tells a
 // wave that its share of the next stage has landed, and one barrier publishes the stage to
 // the other waves.  NS stages are in flight; the waves read their MFMA operands for step
-// k+1 from LDS while the MFMAs of step k run.  Buffer loads return zero past the end of an
-// operand, and K steps past the end are copied as zeros, so the loop has no data branches.
+// k+1 from LDS while the MFMAs of step k run.  The buffer descriptors and each lane's
+// offsets are fixed for the whole loop (the K advance is the instruction's scalar offset);
+// lanes of tiles past the edge copy zeros, and K steps past the end are copied through a
+// zero-size buffer, so the loop has no data branches.
 //
 // Workgroups are mapped to tiles in contiguous chunks per XCD (workgroup b runs on XCD
 // b % 8), so tiles that share a weight column block run on the same XCD and share its L2.
@@ -45,11 +48,12 @@ constexpr int kDumpBytes = 1024;         // LDS target of the padding copies (ne
 
 struct GemmParams {
   int64_t M, N, K, nkb, mt_tiles, nt_tiles;
-  const uint8_t* a_frag[2];
-  const uint8_t* a_sc[2];
-  uint32_t a_frag_bytes, a_sc_bytes, b_frag_bytes, b_sc_bytes;
-  const uint8_t* b_frag;
-  const uint8_t* b_sc;
+  // Operand A: one buffer with the fragments and scale bytes of every term at these byte
+  // offsets; operand B: one buffer with its fragments and scale bytes.
+  const uint8_t* a;
+  const uint8_t* b;
+  uint32_t a_bytes, b_bytes;
+  uint32_t a_frag_off[2], a_sc_off[2], b_frag_off, b_sc_off;
   float* Y;
   int64_t ldy;
   int64_t grid_m, grid_n, per_xcd;
@@ -70,13 +74,14 @@ __device__ __forceinline__ v16f mfma(const v8i& a, const v8i& b, const v16f& c, 
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, FA, FB, 0, sa, 0, sb);
 }
 
-// Buffer load of SZ bytes per lane into LDS: lane l's bytes land at lds + SZ * l.
+// Buffer load of SZ bytes per lane into LDS: lane l's bytes land at lds + SZ * l.  The lane's
+// offset is voff + soff (soff: the wave-uniform K advance); lanes whose voff lies past the
+// buffer's num_records read zeros, and a zero-size buffer makes the whole copy read zeros.
 template <int SZ>
-__device__ __forceinline__ void copy_to_lds(const uint8_t* base, uint32_t bytes, void* lds, uint32_t off) {
-  const __amdgpu_buffer_rsrc_t r = make_rsrc(base, bytes);
-  if constexpr (SZ == 16) __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)lds, 16, off, 0, 0, 0);
-  else if constexpr (SZ == 12) __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)lds, 12, off, 0, 0, 0);
-  else __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)lds, 4, off, 0, 0, 0);
+__device__ __forceinline__ void copy_to_lds(__amdgpu_buffer_rsrc_t r, void* lds, uint32_t voff, uint32_t soff) {
+  if constexpr (SZ == 16) __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)lds, 16, voff, soff, 0, 0);
+  else if constexpr (SZ == 12) __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)lds, 12, voff, soff, 0, 0);
+  else __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)lds, 4, voff, soff, 0, 0);
 }
 
 // s_waitcnt on vmcnt only (expcnt and lgkmcnt left at their maxima).
@@ -116,23 +121,24 @@ struct Geo {
   static constexpr int SB_OFF = SA_OFF + NT * SAJ * 256;
   static constexpr int DUMP_OFF = (SB_OFF + SBJ * 256 + 255) / 256 * 256;  // padding copies
   static constexpr int STAGE = DUMP_OFF + kDumpBytes;
-  // copy instructions per stage by size class, and per wave (padded to a multiple of W)
-  static constexpr int J16 = NT * MTW * PA + (FMT == 0 ? NTW : 0);
-  static constexpr int J12 = FMT == 0 ? 0 : 2 * NTW;
-  static constexpr int J4 = NT * SAJ + SBJ;
-  static constexpr int S16 = (J16 + W - 1) / W, S12 = (J12 + W - 1) / W, S4 = (J4 + W - 1) / W;
-  static constexpr int JW = S16 + S12 + S4;
+  // copy instructions per stage by class: A fragments (16 B per lane), B fragments (16 B
+  // per lane for MXFP4; two 12-byte halves for HiF4), scale bytes of A and B (4 B per lane);
+  // per wave: the class count rounded up to a multiple of W
+  static constexpr int JA = NT * MTW * PA, JB = FMT == 0 ? NTW : 2 * NTW, JS = NT * SAJ + SBJ;
+  static constexpr int XA = (JA + W - 1) / W, XB = (JB + W - 1) / W, XS = (JS + W - 1) / W;
+  static constexpr int JW = XA + XB + XS;
+  static constexpr int SZB = FMT == 0 ? 16 : 12;
   static size_t lds_bytes() { return (size_t)NS * STAGE; }
   static_assert(NS >= 2, "at least two stages");
 };
 
-// One copy instruction of a wave: source base and size, this lane's source offset at kb = 0
-// and its per-K-step advance (kBad and 0 for lanes without a source: they copy zeros), and
-// the stage-relative LDS destination (the dump area for copies that only pad the wave's
-// count).  A K step past the end is copied through a zero-size buffer, so it reads zeros.
-struct Copy {
-  const uint8_t* base;
-  uint32_t bytes, off, step, lds;
+// One copy instruction of a wave: this lane's source offset at K step 0 (kBad: no source,
+// the lane copies zeros) and the stage-relative LDS destination (the dump area for copies
+// that only pad the wave's count).  Each K step adds the class's step to the offset through
+// the instruction's scalar offset; a K step past the end is copied through a zero-size
+// buffer, so it reads zeros.
+struct Slot {
+  uint32_t voff, lds;
 };
 
 template <int FMT, int WM, int WN, int TM, int TN, int NT, int NS>
@@ -154,51 +160,51 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(GemmParams p) {
   const uint32_t kbeg = (uint32_t)(split * p.kper);                    // this split's K steps:
   const uint32_t klen = (uint32_t)min((int64_t)p.kper, p.nkb - kbeg);  // kbeg .. kbeg+klen-1
 
-  // ---- this wave's copy list: copy jc of a size class goes to wave jc % W ----
-  const Copy pad{p.b_frag, 0u, kBad, 0u, (uint32_t)G::DUMP_OFF};
-  Copy c16[G::S16 > 0 ? G::S16 : 1], c12[G::S12 > 0 ? G::S12 : 1], c4[G::S4 > 0 ? G::S4 : 1];
+  // ---- this wave's copy slots: copy jc of a class goes to wave jc % W ----
+  const uint32_t mt = (uint32_t)p.mt_tiles, nt = (uint32_t)p.nt_tiles;
+  Slot sa[G::XA], sb[G::XB], ss[G::XS];
+  bool ss_a[G::XS];  // scale slot reads operand A's buffer
 #pragma unroll
-  for (int x = 0; x < G::S16; ++x) {
+  for (int x = 0; x < G::XA; ++x) {
     const int jc = wave + G::W * x;
-    Copy c = pad;
-    if (jc < NT * G::MTW * G::PA) {
+    Slot c{kBad, (uint32_t)G::DUMP_OFF};
+    if (jc < G::JA) {
       const int t = jc / (G::MTW * G::PA), i = (jc / G::PA) % G::MTW, q = jc % G::PA;
-      c = Copy{p.a_frag[t], p.a_frag_bytes, (T0 + i) * nkb * G::A_FRAG + lane * G::FA + q * 16,
-               (uint32_t)G::A_FRAG, (uint32_t)((t * G::MTW + i) * G::A_FRAG + q * 1024)};
-    } else if (FMT == 0 && jc < G::J16) {
-      const int j = jc - NT * G::MTW;
-      c = Copy{p.b_frag, p.b_frag_bytes, (N0 + j) * nkb * G::B_FRAG + lane * 16, (uint32_t)G::B_FRAG,
-               (uint32_t)(G::B_OFF + j * G::B_LDS)};
+      c.voff = T0 + i < mt ? p.a_frag_off[t] + (T0 + i) * nkb * G::A_FRAG + lane * G::FA + q * 16 : kBad;
+      c.lds = (uint32_t)((t * G::MTW + i) * G::A_FRAG + q * 1024);
     }
-    c16[x] = c;
+    sa[x] = c;
   }
 #pragma unroll
-  for (int x = 0; x < G::S12; ++x) {
+  for (int x = 0; x < G::XB; ++x) {
     const int jc = wave + G::W * x;
-    Copy c = pad;
-    if (jc < G::J12) {
-      const int j = jc / 2, q = jc % 2;
-      c = Copy{p.b_frag, p.b_frag_bytes, (N0 + j) * nkb * G::B_FRAG + lane * 24 + q * 12,
-               (uint32_t)G::B_FRAG, (uint32_t)(G::B_OFF + j * G::B_LDS + q * 1024)};
+    Slot c{kBad, (uint32_t)G::DUMP_OFF};
+    if (jc < G::JB) {
+      const int j = FMT == 0 ? jc : jc / 2, q = FMT == 0 ? 0 : jc % 2;
+      c.voff = N0 + j < nt ? p.b_frag_off + (N0 + j) * nkb * G::B_FRAG + lane * G::FB + q * 12 : kBad;
+      c.lds = (uint32_t)(G::B_OFF + j * G::B_LDS + q * 1024);
     }
-    c12[x] = c;
+    sb[x] = c;
   }
 #pragma unroll
-  for (int x = 0; x < G::S4; ++x) {
+  for (int x = 0; x < G::XS; ++x) {
     const int jc = wave + G::W * x;
-    Copy c = pad;
+    Slot c{kBad, (uint32_t)G::DUMP_OFF};
+    bool is_a = true;
     if (jc < NT * G::SAJ) {  // A scales: 4 fragments of one term, 16 lanes x 4 bytes each
       const int t = jc / G::SAJ, i = 4 * (jc % G::SAJ) + lane / 16;
-      const bool ok = i < G::MTW;
-      c = Copy{p.a_sc[t], p.a_sc_bytes, ok ? (T0 + i) * nkb * 64 + (lane % 16) * 4 : kBad,
-               ok ? 64u : 0u, (uint32_t)(G::SA_OFF + jc * 256)};
-    } else if (jc < G::J4) {
+      const bool ok = i < G::MTW && T0 + i < mt;
+      c.voff = ok ? p.a_sc_off[t] + (T0 + i) * nkb * 64 + (lane % 16) * 4 : kBad;
+      c.lds = (uint32_t)(G::SA_OFF + jc * 256);
+    } else if (jc < G::JS) {
       const int q = jc - NT * G::SAJ, j = 4 * q + lane / 16;
-      const bool ok = j < G::NTW;
-      c = Copy{p.b_sc, p.b_sc_bytes, ok ? (N0 + j) * nkb * 64 + (lane % 16) * 4 : kBad,
-               ok ? 64u : 0u, (uint32_t)(G::SB_OFF + q * 256)};
+      const bool ok = j < G::NTW && N0 + j < nt;
+      c.voff = ok ? p.b_sc_off + (N0 + j) * nkb * 64 + (lane % 16) * 4 : kBad;
+      c.lds = (uint32_t)(G::SB_OFF + q * 256);
+      is_a = false;
     }
-    c4[x] = c;
+    ss[x] = c;
+    ss_a[x] = is_a;
   }
 
   // Copy this split's K step k (absolute step kbeg + k) into stage buffer `buf`; steps
@@ -206,16 +212,15 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(GemmParams p) {
   auto issue = [&](int buf, uint32_t k) {
     const bool in = k < klen;
     const uint32_t kb = kbeg + k;
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.a, in ? p.a_bytes : 0u);
+    const __amdgpu_buffer_rsrc_t rb = make_rsrc(p.b, in ? p.b_bytes : 0u);
     uint8_t* st = smem + buf * G::STAGE;
 #pragma unroll
-    for (int x = 0; x < G::S16; ++x)
-      copy_to_lds<16>(c16[x].base, in ? c16[x].bytes : 0u, st + c16[x].lds, c16[x].off + kb * c16[x].step);
+    for (int x = 0; x < G::XA; ++x) copy_to_lds<16>(ra, st + sa[x].lds, sa[x].voff, kb * G::A_FRAG);
 #pragma unroll
-    for (int x = 0; x < G::S12; ++x)
-      copy_to_lds<12>(c12[x].base, in ? c12[x].bytes : 0u, st + c12[x].lds, c12[x].off + kb * c12[x].step);
+    for (int x = 0; x < G::XB; ++x) copy_to_lds<G::SZB>(rb, st + sb[x].lds, sb[x].voff, kb * G::B_FRAG);
 #pragma unroll
-    for (int x = 0; x < G::S4; ++x)
-      copy_to_lds<4>(c4[x].base, in ? c4[x].bytes : 0u, st + c4[x].lds, c4[x].off + kb * c4[x].step);
+    for (int x = 0; x < G::XS; ++x) copy_to_lds<4>(ss_a[x] ? ra : rb, st + ss[x].lds, ss[x].voff, kb * 64u);
   };
 
   v16f acc[TM][TN];
@@ -464,18 +469,31 @@ void launch_fmt(const GemmParams& p, int cfg, int n_terms, hipStream_t s) {
 
 }  // namespace
 
-bool gemm_supported(int fmt, int64_t M, int64_t N, int64_t K) {
+namespace {
+constexpr size_t kOffsetLimit = (size_t)kBad - (1u << 20);  // 32-bit buffer offsets with headroom
+size_t al256(size_t x) { return (x + 255) / 256 * 256; }
+}  // namespace
+
+bool gemm_supported(int fmt, int64_t M, int64_t N, int64_t K, int n_terms) {
   const int amode = fmt == 0 ? kPackMx : kPackHiA, bmode = fmt == 0 ? kPackMx : kPackHiB;
-  const size_t lim = (size_t)kBad - (1u << 20);  // 32-bit buffer offsets with headroom
-  return frag_bytes(amode, M, K) < lim && frag_bytes(bmode, N, K) < lim;
+  const size_t a = (size_t)n_terms * (al256(frag_bytes(amode, M, K)) + al256(frag_scale_bytes(M, K)));
+  const size_t b = al256(frag_bytes(bmode, N, K)) + al256(frag_scale_bytes(N, K));
+  return a < kOffsetLimit && b < kOffsetLimit;
 }
 
 size_t gemm_split_scratch(int fmt, int64_t M, int64_t N, int64_t K) {
   return plan(fmt, M, N, K, true).partial_bytes;
 }
 
-void launch_gemm(const GemmOperands& op, hipStream_t s) {
-  if (op.M == 0 || op.N == 0) return;
+bool launch_gemm(const GemmOperands& op, hipStream_t s) {
+  if (op.M == 0 || op.N == 0) return true;
+  const int amode = op.fmt == 0 ? kPackMx : kPackHiA, bmode = op.fmt == 0 ? kPackMx : kPackHiB;
+  const size_t af = frag_bytes(amode, op.M, op.K), as = frag_scale_bytes(op.M, op.K);
+  const size_t bf = frag_bytes(bmode, op.N, op.K), bs = frag_scale_bytes(op.N, op.K);
+  if (op.a_bytes >= kOffsetLimit || op.b_bytes >= kOffsetLimit) return false;
+  for (int t = 0; t < op.n_terms; ++t)
+    if (op.a_frag_off[t] + af > op.a_bytes || op.a_sc_off[t] + as > op.a_bytes) return false;
+  if (op.b_frag_off + bf > op.b_bytes || op.b_sc_off + bs > op.b_bytes) return false;
   const Plan pl = plan(op.fmt, op.M, op.N, op.K, op.partial != nullptr);
   GemmParams p{};
   p.ksplit = pl.ksplit;
@@ -485,16 +503,18 @@ void launch_gemm(const GemmOperands& op, hipStream_t s) {
   p.nkb = (op.K + 63) / 64;
   p.mt_tiles = (op.M + 31) / 32;
   p.nt_tiles = (op.N + 31) / 32;
-  for (int t = 0; t < 2; ++t) { p.a_frag[t] = op.a_frag[t]; p.a_sc[t] = op.a_sc[t]; }
-  p.b_frag = op.b_frag; p.b_sc = op.b_sc;
+  p.a = op.a; p.b = op.b;
+  p.a_bytes = (uint32_t)op.a_bytes; p.b_bytes = (uint32_t)op.b_bytes;
+  for (int t = 0; t < 2; ++t) {
+    const int u = t < op.n_terms ? t : 0;
+    p.a_frag_off[t] = (uint32_t)op.a_frag_off[u];
+    p.a_sc_off[t] = (uint32_t)op.a_sc_off[u];
+  }
+  p.b_frag_off = (uint32_t)op.b_frag_off; p.b_sc_off = (uint32_t)op.b_sc_off;
   p.Y = op.Y; p.ldy = op.ldy;
-  const int amode = op.fmt == 0 ? kPackMx : kPackHiA, bmode = op.fmt == 0 ? kPackMx : kPackHiB;
-  p.a_frag_bytes = (uint32_t)frag_bytes(amode, op.M, op.K);
-  p.a_sc_bytes = (uint32_t)frag_scale_bytes(op.M, op.K);
-  p.b_frag_bytes = (uint32_t)frag_bytes(bmode, op.N, op.K);
-  p.b_sc_bytes = (uint32_t)frag_scale_bytes(op.N, op.K);
   if (op.fmt == 0) launch_fmt<0>(p, pl.cfg, op.n_terms, s);
   else launch_fmt<1>(p, pl.cfg, op.n_terms, s);
+  return true;
 }
 
 }  // namespace resq

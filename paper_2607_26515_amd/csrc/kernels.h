@@ -57,24 +57,31 @@ void launch_select(int fmt, int sparsity, int64_t m, int64_t d, uint8_t* qr_code
                    uint8_t* group_mask, const SelectWs& ws, hipStream_t s);
 
 // FP4 GEMM  Y[M][N] = sum_t A_t[M][K] B[N][K]^T  with A_t = Q(X) and optionally S(Q(dX)),
-// all operands fragment-major (pack.hip).
+// all operands fragment-major (pack.hip).  Operand A is one buffer holding the fragments and
+// scale bytes of every term at the given byte offsets; operand B is one buffer holding its
+// fragments and scale bytes.  Each buffer is below 4 GiB (32-bit offsets).
 struct GemmOperands {
   int fmt;
   int64_t M, N, K;
-  const uint8_t* a_frag[2];
-  const uint8_t* a_sc[2];
   int n_terms;               // 1 (Eq. 1) or 2 (with the residual term)
-  const uint8_t* b_frag;
-  const uint8_t* b_sc;
+  const uint8_t* a;
+  size_t a_bytes;
+  size_t a_frag_off[2], a_sc_off[2];
+  const uint8_t* b;
+  size_t b_bytes;
+  size_t b_frag_off, b_sc_off;
   float* Y;
   int64_t ldy;
   // optional split-K scratch of gemm_split_scratch bytes (null: no K split)
   float* partial;
 };
-void launch_gemm(const GemmOperands& op, hipStream_t s);
+// Returns false (and launches nothing) when an operand buffer or offset does not fit the
+// 32-bit offsets or an operand region lies outside its buffer.
+bool launch_gemm(const GemmOperands& op, hipStream_t s);
 // Scratch bytes a launch_gemm of this shape uses for its K split (0: it does not split).
 size_t gemm_split_scratch(int fmt, int64_t M, int64_t N, int64_t K);
-// Whether launch_gemm handles these sizes (32-bit operand offsets).
-bool gemm_supported(int fmt, int64_t M, int64_t N, int64_t K);
+// Whether launch_gemm handles these sizes: the A buffer of n_terms terms (fragments and
+// scales, each 256-byte aligned) and the B buffer fit 32-bit offsets.
+bool gemm_supported(int fmt, int64_t M, int64_t N, int64_t K, int n_terms);
 
 }  // namespace resq
