@@ -14,7 +14,8 @@
 // can carry it.  The activation value V 2^(e-37) (V <= 196) is split into two exact E2M3
 // operands (hi, lo) and the weight element k 2^-b is an exact BF6 E3M2 operand with E8M0
 // 2^(e_w - 35); the remaining weight factor (4 + m_w) is constant per output column, i.e. per
-// lane, and is applied once per 64-K step: acc += (4 + m_w) * P_step.
+// lane, and is applied once per 64-K step: acc += (4 + m_w) * P_step.  Each tile's fold is
+// issued after the next tile's MFMAs, so it runs under MFMA execution.
 //
 // Data movement.  A workgroup of WM x WN waves owns a (WM*TM*32) x (WN*TN*32) output tile.
 // Each K step's operand bytes (A fragments of every term, B fragments, their scale bytes)
@@ -32,6 +33,7 @@
 // b % 8), so tiles that share a weight column block run on the same XCD and share its L2.
 #include "kernels.h"
 #include "device_fp4.h"
+
 
 namespace resq {
 namespace {
@@ -141,8 +143,13 @@ struct Slot {
   uint32_t voff, lds;
 };
 
+// HiF4 with more than one tile per wave keeps one register set and runs two waves per SIMD.
+template <int FMT, int TM, int TN>
+constexpr bool kSingleSet = FMT == 1 && TM * TN > 1;
+
 template <int FMT, int WM, int WN, int TM, int TN, int NT, int NS>
-__global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(GemmParams p) {
+__global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(kSingleSet<FMT, TM, TN> ? 2 : 1)))
+void gemm_kernel(GemmParams p) {
   using G = Geo<FMT, WM, WN, TM, TN, NT, NS>;
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
 
@@ -231,6 +238,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(GemmParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+  constexpr bool SB = kSingleSet<FMT, TM, TN>;
+  constexpr int TT = TM * TN;
+  v16f Pp = {};    // single register set: partial sums of the tile whose fold is pending
+  float fp = 0.f;  // and its weight factor 4 + m_w
   // One K step's MFMA operands of this wave, read from an LDS stage.
   struct Frag {
     v8i b[TN];
@@ -319,28 +330,102 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(GemmParams p) {
     }
   };
 
-  // Pipeline.  Before step k, stages k+1 .. k+NS-1 are in flight and step k's operands are
-  // in registers.  Step k: wait for this wave's copies of stage k+1 (the NS-2 later stages
-  // stay outstanding), barrier (stage k+1 is visible to every wave, and every wave has read
-  // stage k's buffer), refill that buffer with stage k+NS, read stage k+1's operands, run
-  // step k's MFMAs.  Steps past the end multiply zeros.  U unrolls the loop so that every
-  // buffer and register-set index is a constant.
-  constexpr int U = NS % 2 == 0 ? NS : 2 * NS;
+  // HiF4 with one register set (TM x TN > 1): the step's B fragments first, then per row
+  // tile its A fragments (both terms, hi and lo) and its TN tiles.  Each tile's partial sums
+  // P are folded (acc += (4 + m_w) P) after the next tile's MFMAs are issued, so the fold's
+  // VALU work runs under MFMA execution; the last tile's fold is pending across steps.
+  auto step_single = [&](int buf) {
+    const uint8_t* st = smem + buf * G::STAGE;
+    v8i b[TN];
+    int sbs[TN];
+    float fbs[TN];
 #pragma unroll
-  for (int s = 0; s < NS; ++s) issue(s, (uint32_t)s);
-  wait_vmcnt<(NS - 1) * G::JW>();
-  __syncthreads();
-  read(F[0], 0);
-  for (uint32_t k0 = 0; k0 < klen; k0 += U) {
+    for (int j = 0; j < TN; ++j) {
+      const int lj = wn * TN + j;
+      const uint8_t* bb = st + G::B_OFF + lj * G::B_LDS;
+      const v4i x = *reinterpret_cast<const v4i*>(bb + lane * 16);  // 12 bytes used
+      const v4i y = *reinterpret_cast<const v4i*>(bb + 1024 + lane * 16);
+      b[j] = v8i{x[0], x[1], x[2], y[0], y[1], y[2], 0, 0};
+      const int sc = st[G::SB_OFF + lj * 64 + lane];
+      sbs[j] = (sc >> 2) + 92;
+      fbs[j] = (float)(4 + (sc & 3));
+    }
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const uint32_t k = k0 + u;
-      wait_vmcnt<(NS - 2) * G::JW>();
-      lds_barrier();
-      issue(u % NS, k + NS);
-      read(F[(u + 1) & 1], (u + 1) % NS);
-      mma(F[u & 1]);
-      __builtin_amdgcn_sched_barrier(0);  // keep step k's MFMAs ahead of step k+1's barrier
+    for (int i = 0; i < TM; ++i) {
+      const int li = wm * TM + i;
+      v8i a[NT][2];
+      int sas[NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const uint8_t* a0 = st + (t * G::MTW + li) * G::A_FRAG;
+        const v4i p0 = *reinterpret_cast<const v4i*>(a0 + lane * 16);
+        const v4i p1 = *reinterpret_cast<const v4i*>(a0 + 1024 + lane * 16);
+        const v4i p2 = *reinterpret_cast<const v4i*>(a0 + 2048 + lane * 16);
+        a[t][0] = v8i{p0[0], p0[1], p0[2], p0[3], p1[0], p1[1], 0, 0};
+        a[t][1] = v8i{p1[2], p1[3], p2[0], p2[1], p2[2], p2[3], 0, 0};
+        sas[t] = st[G::SA_OFF + (t * G::SAJ * 4 + li) * 64 + lane] >> 2;
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int x = i * TN + j, xp = x == 0 ? TT - 1 : x - 1, ip = xp / TN, jp = xp % TN;
+        v16f Pc;
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+            Pc = mfma<2, 3>(a[t][h], b[j], (t == 0 && h == 0) ? v16f{} : Pc, sas[t] + (h == 0 ? 97 : 93), sbs[j]);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[ip][jp][r] = fmaf(Pp[r], fp, acc[ip][jp][r]);
+        Pp = Pc;
+        fp = fbs[j];
+      }
+    }
+  };
+
+  if constexpr (SB) {
+    // One register set.  Before step k, stages k .. k+NS-2 are in flight.  Step k: wait for
+    // this wave's copies of stage k (NS-2 later stages stay outstanding), barrier (stage k is
+    // visible to every wave, and every wave has read stage k-1's buffer), refill that buffer
+    // with stage k+NS-1, read stage k and run its MFMAs.  Steps past the end multiply zeros.
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s) issue(s, (uint32_t)s);
+    for (uint32_t k0 = 0; k0 < klen; k0 += NS) {
+#pragma unroll
+      for (int u = 0; u < NS; ++u) {
+        const uint32_t k = k0 + u;
+        wait_vmcnt<(NS - 2) * G::JW>();
+        lds_barrier();
+        issue((u + NS - 1) % NS, k + NS - 1);
+        step_single(u);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[TM - 1][TN - 1][r] = fmaf(Pp[r], fp, acc[TM - 1][TN - 1][r]);
+  } else {
+    // Two register sets.  Before step k, stages k+1 .. k+NS-1 are in flight and step k's
+    // operands are in registers.  Step k: wait for this wave's copies of stage k+1 (the NS-2
+    // later stages stay outstanding), barrier (stage k+1 is visible to every wave, and every
+    // wave has read stage k's buffer), refill that buffer with stage k+NS, read stage k+1's
+    // operands, run step k's MFMAs.  Steps past the end multiply zeros.  U unrolls the loop
+    // so that every buffer and register-set index is a constant.
+    constexpr int U = NS % 2 == 0 ? NS : 2 * NS;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) issue(s, (uint32_t)s);
+    wait_vmcnt<(NS - 1) * G::JW>();
+    __syncthreads();
+    read(F[0], 0);
+    for (uint32_t k0 = 0; k0 < klen; k0 += U) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const uint32_t k = k0 + u;
+        wait_vmcnt<(NS - 2) * G::JW>();
+        lds_barrier();
+        issue(u % NS, k + NS);
+        read(F[(u + 1) & 1], (u + 1) % NS);
+        mma(F[u & 1]);
+        __builtin_amdgcn_sched_barrier(0);  // keep step k's MFMAs ahead of step k+1's barrier
+      }
     }
   }
   wait_vmcnt<0>();
@@ -414,12 +499,15 @@ void launch_cfg(GemmParams p, int n_terms, hipStream_t s) {
                        (const float*)p.partial, p.ksplit, p.grid_m, p.M, p.N, p.Y, p.ldy);
 }
 
-// Tile choice (measured on MI355X): a CU holds one or two workgroups (LDS-bound), so the
-// workgroup count decides how many rounds the grid takes.
+// Tile choice (measured on MI355X): a CU holds one or two workgroups (LDS- and
+// register-bound), so the workgroup count decides how many rounds the grid takes.
 //  - grids too small for 128-row tiles to fill the chip: 64 x 64 tiles, deep pipeline, and
 //    for long K (at least 64 steps per split) K split in two when that fills the CUs;
-//  - M >= 512 (7B decode and prefill): 128 x 256 tiles (fewest A re-reads per byte of B);
-//  - otherwise (M = 256 decode): 128 x 192 tiles, one round on 256 CUs.
+//  - MXFP4 with M >= 512 (7B decode and prefill): 128 x 256 tiles (fewest A re-reads per
+//    byte of B), two workgroups per CU;
+//  - otherwise: 128 x 192 tiles.  HiF4 always takes these: with one register set they fit
+//    two waves per SIMD (two workgroups per CU at NS = 2), which hides the LDS reads and the
+//    fold behind the other workgroup's MFMAs; 128 x 256 HiF4 tiles would spill.
 enum TileCfg { kSmall = 0, kWide = 1, kMid = 2 };
 constexpr int kCUs = 256;
 
@@ -451,20 +539,22 @@ Plan plan(int fmt, int64_t M, int64_t N, int64_t K, bool may_split) {
       if (pl.ksplit > 1) pl.partial_bytes = (size_t)pl.tiles * pl.ksplit * (256 * 16) * sizeof(float);
     }
   } else {
-    pl.cfg = M >= 512 ? kWide : kMid;
-    pl.tiles = M >= 512 ? wgs(4, 8) : wgs(4, 6);
+    const bool wide = M >= 512 && fmt == 0;
+    pl.cfg = wide ? kWide : kMid;
+    pl.tiles = wide ? wgs(4, 8) : wgs(4, 6);
   }
   return pl;
 }
 
 template <int FMT>
 void launch_fmt(const GemmParams& p, int cfg, int n_terms, hipStream_t s) {
-  if (cfg == kSmall)
+  if (cfg == kSmall) {
     launch_cfg<FMT, 2, 2, 1, 1, FMT == 0 ? 8 : 6>(p, n_terms, s);
-  else if (cfg == kWide)
-    launch_cfg<FMT, 2, 2, 2, 4, FMT == 0 ? 4 : 2>(p, n_terms, s);
-  else
+  } else if (cfg == kWide) {
+    if constexpr (FMT == 0) launch_cfg<FMT, 2, 2, 2, 4, 4>(p, n_terms, s);  // MXFP4 only
+  } else {
     launch_cfg<FMT, 2, 2, 2, 3, FMT == 0 ? 4 : 2>(p, n_terms, s);
+  }
 }
 
 }  // namespace
