@@ -66,6 +66,21 @@ struct GemmParams {
   float* partial;
 };
 
+// Output tile of linear tile index `tile`: tiles run in groups of kGroupRows row tiles;
+// within a group, row tiles vary fastest, then column tiles.  A run of consecutive tiles (the
+// workgroups resident on one XCD at a time) then covers a compact block of rows and columns
+// that share their A row strips and B column strips in that XCD's L2.
+constexpr int64_t kGroupRows = 8;
+__device__ __forceinline__ void tile_coords(int64_t tile, int64_t grid_m, int64_t grid_n, int64_t& wg_m,
+                                            int64_t& wg_n) {
+  const int64_t group = tile / (kGroupRows * grid_n);
+  const int64_t first = group * kGroupRows;
+  const int64_t rows = min(kGroupRows, grid_m - first);
+  const int64_t in = tile - first * grid_n;
+  wg_m = first + in % rows;
+  wg_n = in / rows;
+}
+
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
   // raw buffer (32-bit dwords, no swizzle); num_records = bytes bounds every access
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
@@ -158,7 +173,8 @@ void gemm_kernel(GemmParams p) {
   if (wgid >= p.grid_m * p.grid_n * p.ksplit) return;
   const int64_t tile = wgid / p.ksplit;
   const int split = (int)(wgid % p.ksplit);
-  const int64_t wg_m = tile % p.grid_m, wg_n = tile / p.grid_m;
+  int64_t wg_m, wg_n;
+  tile_coords(tile, p.grid_m, p.grid_n, wg_m, wg_n);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int wm = wave % WM, wn = wave / WM;
@@ -458,22 +474,27 @@ void gemm_kernel(GemmParams p) {
 }
 
 // Sum the ksplit partial tiles of each output tile in split order (deterministic) and store
-// Y.  One workgroup per tile; partial element e = wave, tile (i, j), accumulator register r,
-// lane -- the gemm_kernel register order.
+// Y.  Partial element e = wave, tile (i, j), accumulator register r, lane -- the gemm_kernel
+// register order; workgroup b handles the 1024 elements of one (wave, i, j) of one tile.
 template <int WM, int WN, int TM, int TN>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ partial,
-                                                            int ksplit, int64_t grid_m, int64_t M,
-                                                            int64_t N, float* __restrict__ Y,
+                                                            int ksplit, int64_t grid_m, int64_t grid_n,
+                                                            int64_t M, int64_t N, float* __restrict__ Y,
                                                             int64_t ldy) {
-  constexpr int TE = 64 * WM * WN * TM * TN * 16;
-  const int64_t tile = blockIdx.x;
-  const int64_t wg_m = tile % grid_m, wg_n = tile / grid_m;
-  const float* part = partial + (size_t)tile * ksplit * TE;
-  for (int e = threadIdx.x; e < TE; e += 256) {
-    const int lane = e & 63, r = (e >> 6) & 15, ij = (e >> 10) % (TM * TN), wave = e / (1024 * TM * TN);
-    const int i = ij / TN, j = ij % TN, wm = wave % WM, wn = wave / WM;
-    float v = part[e];
-    for (int q = 1; q < ksplit; ++q) v += part[(size_t)q * TE + e];
+  constexpr int PARTS = WM * WN * TM * TN, TE = 1024 * PARTS;
+  const int64_t tile = blockIdx.x / PARTS;
+  const int part = (int)(blockIdx.x % PARTS);
+  int64_t wg_m, wg_n;
+  tile_coords(tile, grid_m, grid_n, wg_m, wg_n);
+  const float* src = partial + (size_t)tile * ksplit * TE + part * 1024;
+  const int ij = part % (TM * TN), wave = part / (TM * TN);
+  const int i = ij / TN, j = ij % TN, wm = wave % WM, wn = wave / WM;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = threadIdx.x + 256 * q;  // register r = e / 64, lane = e % 64
+    const int lane = e & 63, r = e >> 6;
+    float v = src[e];
+    for (int k = 1; k < ksplit; ++k) v += src[(size_t)k * TE + e];
     const int64_t row = (wg_m * WM * TM + wm * TM + i) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
     const int64_t col = (wg_n * WN * TN + wn * TN + j) * 32 + (lane & 31);
     if (row < M && col < N) Y[row * ldy + col] = v;
@@ -495,8 +516,8 @@ void launch_cfg(GemmParams p, int n_terms, hipStream_t s) {
   else
     hipLaunchKernelGGL((gemm_kernel<FMT, WM, WN, TM, TN, 1, NS>), grid, block, G1::lds_bytes(), s, p);
   if (p.ksplit > 1)
-    hipLaunchKernelGGL((splitk_reduce_kernel<WM, WN, TM, TN>), dim3((unsigned)(p.grid_m * p.grid_n)), dim3(256), 0, s,
-                       (const float*)p.partial, p.ksplit, p.grid_m, p.M, p.N, p.Y, p.ldy);
+    hipLaunchKernelGGL((splitk_reduce_kernel<WM, WN, TM, TN>), dim3((unsigned)(p.grid_m * p.grid_n * WM * WN * TM * TN)),
+                       dim3(256), 0, s, (const float*)p.partial, p.ksplit, p.grid_m, p.grid_n, p.M, p.N, p.Y, p.ldy);
 }
 
 // Tile choice (measured on MI355X): a CU holds one or two workgroups (LDS- and
