@@ -528,8 +528,10 @@ void launch_cfg(GemmParams p, int n_terms, hipStream_t s) {
 //    byte of B), two workgroups per CU;
 //  - otherwise: 128 x 192 tiles.  HiF4 always takes these: with one register set they fit
 //    two waves per SIMD (two workgroups per CU at NS = 2), which hides the LDS reads and the
-//    fold behind the other workgroup's MFMAs; 128 x 256 HiF4 tiles would spill.
-enum TileCfg { kSmall = 0, kWide = 1, kMid = 2 };
+//    fold behind the other workgroup's MFMAs; 128 x 256 HiF4 tiles would spill.  When the
+//    HiF4 grid has fewer than two workgroups per CU (M = 256 decode), the tile runs as eight
+//    waves of 32 x 96 instead, so each SIMD still holds two waves.
+enum TileCfg { kSmall = 0, kWide = 1, kMid = 2, kMid8 = 3 };
 constexpr int kCUs = 256;
 
 struct Plan {
@@ -563,6 +565,8 @@ Plan plan(int fmt, int64_t M, int64_t N, int64_t K, bool may_split) {
     const bool wide = M >= 512 && fmt == 0;
     pl.cfg = wide ? kWide : kMid;
     pl.tiles = wide ? wgs(4, 8) : wgs(4, 6);
+    // HiF4 grids below two workgroups per CU: eight waves per 128 x 192 tile (two per SIMD)
+    if (fmt == 1 && pl.tiles < 2 * kCUs) pl.cfg = kMid8;
   }
   return pl;
 }
@@ -573,6 +577,8 @@ void launch_fmt(const GemmParams& p, int cfg, int n_terms, hipStream_t s) {
     launch_cfg<FMT, 2, 2, 1, 1, FMT == 0 ? 8 : 6>(p, n_terms, s);
   } else if (cfg == kWide) {
     if constexpr (FMT == 0) launch_cfg<FMT, 2, 2, 2, 4, 4>(p, n_terms, s);  // MXFP4 only
+  } else if (cfg == kMid8) {
+    if constexpr (FMT == 1) launch_cfg<FMT, 4, 2, 1, 3, 2>(p, n_terms, s);  // HiF4 only
   } else {
     launch_cfg<FMT, 2, 2, 2, 3, FMT == 0 ? 4 : 2>(p, n_terms, s);
   }
