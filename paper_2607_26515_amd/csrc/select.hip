@@ -179,13 +179,15 @@ __device__ __forceinline__ void choose_digit(const uint32_t* hist, int nb, uint3
   __syncthreads();
 }
 
-// h[digit] += 1 for every active lane of the wave.  Lanes that share a digit are counted
-// with one LDS atomic (the keys of a selection pass often share a few digits, and per-lane
-// atomics on one address serialize); after four such rounds the rest add one by one.  Every
+// h[digit] += 1 for every active lane of the wave.  The lanes sharing the digit of the first
+// two leaders are counted with one LDS atomic each (the keys of a selection pass often share
+// a digit, and per-lane atomics on one address serialize); the rest add one by one.  Every
 // lane of the wave must call this (the digit and active flag may differ per lane).
 __device__ __forceinline__ void hist_add(uint32_t* h, uint32_t digit, bool active) {
   uint64_t pending = __ballot(active);
-  for (int it = 0; it < 4 && pending != 0; ++it) {
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    if (pending == 0) return;
     const int leader = __ffsll((unsigned long long)pending) - 1;
     const uint32_t dl = __shfl(digit, leader, 64);
     const uint64_t same = __ballot(digit == dl) & pending;
@@ -197,7 +199,9 @@ __device__ __forceinline__ void hist_add(uint32_t* h, uint32_t digit, bool activ
 
 // ---------------------------------------------------------------------------------------
 // Single-workgroup top-k over n float64 keys -> bit mask (bit b of byte i = item 8i + b).
-// Thread t holds keys t, t + 1024, ... in registers (KPT of them: n <= 1024 KPT), loaded once.
+// Thread t holds the KPT consecutive keys t*KPT .. t*KPT+KPT-1 in registers (n <= 1024 KPT),
+// so thread order is index order: the threshold's ties are ranked with one scan of per-thread
+// tie counts, and each thread writes its own KPT/8 mask bytes.
 // ---------------------------------------------------------------------------------------
 constexpr int kKeysPerThread = 24;  // n <= 24576: channels of d <= 24576, blocks of m*d <= 50M
 
@@ -209,22 +213,18 @@ __global__ __launch_bounds__(kSelThreads) void select_top_kernel(const uint64_t*
   __shared__ uint32_t ch[2];
   __shared__ uint32_t wsum[kSelThreads / 64];
   const int tid = threadIdx.x;
+  const int64_t i0 = (int64_t)tid * kKeysPerThread;
   uint64_t kr[kKeysPerThread];
 #pragma unroll
-  for (int q = 0; q < kKeysPerThread; ++q) {
-    const int64_t i = (int64_t)q * kSelThreads + tid;
-    kr[q] = i < n ? keys[i] : 0;
-  }
+  for (int q = 0; q < kKeysPerThread; ++q) kr[q] = i0 + q < n ? keys[i0 + q] : 0;
   uint64_t prefix = 0, mask = 0;
   uint32_t krem = (uint32_t)k;
   for (int shift = 56; shift >= 0; shift -= 8) {
     if (tid < 256) hist[tid] = 0;
     __syncthreads();
 #pragma unroll
-    for (int q = 0; q < kKeysPerThread; ++q) {
-      const int64_t i = (int64_t)q * kSelThreads + tid;
-      hist_add(hist, (uint32_t)((kr[q] >> shift) & 255u), i < n && (kr[q] & mask) == prefix);
-    }
+    for (int q = 0; q < kKeysPerThread; ++q)
+      hist_add(hist, (uint32_t)((kr[q] >> shift) & 255u), i0 + q < n && (kr[q] & mask) == prefix);
     __syncthreads();
     choose_digit<kSelThreads>(hist, 256, krem, wsum, ch);
     prefix |= (uint64_t)ch[0] << shift;
@@ -233,23 +233,26 @@ __global__ __launch_bounds__(kSelThreads) void select_top_kernel(const uint64_t*
     __syncthreads();  // ch and hist are reused by the next pass
   }
   const uint64_t T = prefix;  // threshold key; krem of its ties are kept (in index order)
-  // rank the ties in index order, 1024 consecutive indices per round
-  uint64_t seen = 0;  // ties in earlier rounds
-  const int lane = tid & 63;
+  uint32_t ties = 0;
 #pragma unroll
-  for (int q = 0; q < kKeysPerThread; ++q) {
-    const int64_t i = (int64_t)q * kSelThreads + tid;
-    const bool in = i < n, tie = in && kr[q] == T;
-    uint32_t total;
-    const uint32_t before = block_exclusive_scan<kSelThreads>(tie ? 1u : 0u, wsum, total);
-    const bool keep = in && (kr[q] > T || (tie && seen + before < krem));
-    const uint64_t bal = __ballot(keep);
-    if ((lane & 7) == 0 && in) {
-      const uint8_t byte = (uint8_t)(bal >> lane);
-      bits[i >> 3] = byte;
-      if (bits_copy) bits_copy[i >> 3] = byte;
+  for (int q = 0; q < kKeysPerThread; ++q) ties += (i0 + q < n && kr[q] == T) ? 1u : 0u;
+  uint32_t total;
+  uint32_t seen = block_exclusive_scan<kSelThreads>(ties, wsum, total);  // ties before this thread
+#pragma unroll
+  for (int b = 0; b < kKeysPerThread / 8; ++b) {
+    uint32_t byte = 0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int q = 8 * b + e;
+      const bool in = i0 + q < n, tie = in && kr[q] == T;
+      const bool keep = in && (kr[q] > T || (tie && seen < krem));
+      seen += tie ? 1u : 0u;
+      byte |= (keep ? 1u : 0u) << e;
     }
-    seen += total;
+    if (i0 + 8 * b < n) {
+      bits[(i0 >> 3) + b] = (uint8_t)byte;
+      if (bits_copy) bits_copy[(i0 >> 3) + b] = (uint8_t)byte;
+    }
   }
 }
 
