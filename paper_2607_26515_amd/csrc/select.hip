@@ -53,7 +53,8 @@ __device__ __forceinline__ uint32_t scale_at(const void* scales, int64_t row, in
 // rows per wave, issued together) and decode it into LDS; wave 0 then adds the chunk row by
 // row (the fixed sequential order) while the waves already load the next chunk.
 // ---------------------------------------------------------------------------------------
-constexpr int kChunk = 64;
+constexpr int kChunk = 256;        // channel keys: rows per chunk
+constexpr int kChanThreads = 1024;  // channel keys: 16 waves load and decode, wave 0 adds
 
 template <int FMT>
 __device__ __forceinline__ float decode_at(uint32_t cbyte, uint32_t sc, int64_t j) {
@@ -68,11 +69,11 @@ __device__ __forceinline__ float decode_at(uint32_t cbyte, uint32_t sc, int64_t 
 }
 
 template <int FMT>
-__global__ __launch_bounds__(kThreads) void channel_keys_kernel(const uint8_t* __restrict__ codes,
-                                                                const void* __restrict__ scales,
-                                                                int64_t m, int64_t d,
-                                                                double* __restrict__ keys) {
-  constexpr int RPW = kChunk / (kThreads / 64);  // rows per wave per chunk
+__global__ __launch_bounds__(kChanThreads) void channel_keys_kernel(const uint8_t* __restrict__ codes,
+                                                                    const void* __restrict__ scales,
+                                                                    int64_t m, int64_t d,
+                                                                    double* __restrict__ keys) {
+  constexpr int NW = kChanThreads / 64, RPW = kChunk / NW;  // waves; rows per wave per chunk
   __shared__ float val[kChunk][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t j = (int64_t)blockIdx.x * 64 + lane;
@@ -80,7 +81,7 @@ __global__ __launch_bounds__(kThreads) void channel_keys_kernel(const uint8_t* _
   auto load = [&](int64_t r0) {
 #pragma unroll
     for (int q = 0; q < RPW; ++q) {
-      const int64_t row = r0 + wave + 4 * q;
+      const int64_t row = r0 + wave + NW * q;
       cb[q] = 0;
       sc[q] = 0;
       if (row < m && j < d) {
@@ -92,15 +93,19 @@ __global__ __launch_bounds__(kThreads) void channel_keys_kernel(const uint8_t* _
   double acc = 0.0;
   load(0);
   for (int64_t r0 = 0; r0 < m; r0 += kChunk) {
-    const int rows = (int)((m - r0) < kChunk ? (m - r0) : kChunk);
 #pragma unroll
-    for (int q = 0; q < RPW; ++q) val[wave + 4 * q][lane] = j < d ? decode_at<FMT>(cb[q], sc[q], j) : 0.f;
+    for (int q = 0; q < RPW; ++q) val[wave + NW * q][lane] = j < d ? decode_at<FMT>(cb[q], sc[q], j) : 0.f;
     __syncthreads();
     if (r0 + kChunk < m) load(r0 + kChunk);  // in flight while wave 0 adds this chunk
+    // Rows past m were decoded from zero codes, so the whole chunk is summed: they add +0.0,
+    // which leaves the (non-negative) sum unchanged.  Reads run 16 rows ahead of the chain.
     if (wave == 0)
-      for (int rr = 0; rr < rows; ++rr) {
-        const double v = (double)val[rr][lane];
-        acc += v * v;  // the square is exact: at most 6 significant bits in v
+      for (int r16 = 0; r16 < kChunk; r16 += 16) {
+        double v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) v[u] = (double)val[r16 + u][lane];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) acc += v[u] * v[u];  // exact square: at most 6 significant bits in v
       }
     __syncthreads();
   }
@@ -199,9 +204,9 @@ __device__ __forceinline__ void hist_add(uint32_t* h, uint32_t digit, bool activ
 
 // ---------------------------------------------------------------------------------------
 // Single-workgroup top-k over n float64 keys -> bit mask (bit b of byte i = item 8i + b).
-// Thread t holds the KPT consecutive keys t*KPT .. t*KPT+KPT-1 in registers (n <= 1024 KPT),
-// so thread order is index order: the threshold's ties are ranked with one scan of per-thread
-// tie counts, and each thread writes its own KPT/8 mask bytes.
+// Thread t holds keys t, t + 1024, ... in registers (KPT of them: n <= 1024 KPT), loaded once
+// with coalesced loads.  The threshold's ties are ranked in index order from one table of
+// per-slot, per-wave tie counts (one barrier).
 // ---------------------------------------------------------------------------------------
 constexpr int kKeysPerThread = 24;  // n <= 24576: channels of d <= 24576, blocks of m*d <= 50M
 
@@ -209,22 +214,28 @@ __global__ __launch_bounds__(kSelThreads) void select_top_kernel(const uint64_t*
                                                                  int64_t n, int64_t k,
                                                                  uint8_t* __restrict__ bits,
                                                                  uint8_t* __restrict__ bits_copy) {
+  constexpr int NW = kSelThreads / 64;
   __shared__ uint32_t hist[256];
   __shared__ uint32_t ch[2];
-  __shared__ uint32_t wsum[kSelThreads / 64];
-  const int tid = threadIdx.x;
-  const int64_t i0 = (int64_t)tid * kKeysPerThread;
+  __shared__ uint32_t wsum[NW];
+  __shared__ uint32_t tcnt[kKeysPerThread][NW];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   uint64_t kr[kKeysPerThread];
 #pragma unroll
-  for (int q = 0; q < kKeysPerThread; ++q) kr[q] = i0 + q < n ? keys[i0 + q] : 0;
+  for (int q = 0; q < kKeysPerThread; ++q) {
+    const int64_t i = (int64_t)q * kSelThreads + tid;
+    kr[q] = i < n ? keys[i] : 0;
+  }
   uint64_t prefix = 0, mask = 0;
   uint32_t krem = (uint32_t)k;
   for (int shift = 56; shift >= 0; shift -= 8) {
     if (tid < 256) hist[tid] = 0;
     __syncthreads();
 #pragma unroll
-    for (int q = 0; q < kKeysPerThread; ++q)
-      hist_add(hist, (uint32_t)((kr[q] >> shift) & 255u), i0 + q < n && (kr[q] & mask) == prefix);
+    for (int q = 0; q < kKeysPerThread; ++q) {
+      const int64_t i = (int64_t)q * kSelThreads + tid;
+      hist_add(hist, (uint32_t)((kr[q] >> shift) & 255u), i < n && (kr[q] & mask) == prefix);
+    }
     __syncthreads();
     choose_digit<kSelThreads>(hist, 256, krem, wsum, ch);
     prefix |= (uint64_t)ch[0] << shift;
@@ -233,26 +244,36 @@ __global__ __launch_bounds__(kSelThreads) void select_top_kernel(const uint64_t*
     __syncthreads();  // ch and hist are reused by the next pass
   }
   const uint64_t T = prefix;  // threshold key; krem of its ties are kept (in index order)
-  uint32_t ties = 0;
+  uint64_t tb[kKeysPerThread];  // tie ballots per slot
 #pragma unroll
-  for (int q = 0; q < kKeysPerThread; ++q) ties += (i0 + q < n && kr[q] == T) ? 1u : 0u;
-  uint32_t total;
-  uint32_t seen = block_exclusive_scan<kSelThreads>(ties, wsum, total);  // ties before this thread
+  for (int q = 0; q < kKeysPerThread; ++q) {
+    const int64_t i = (int64_t)q * kSelThreads + tid;
+    tb[q] = __ballot(i < n && kr[q] == T);
+    if (lane == 0) tcnt[q][wave] = (uint32_t)__popcll(tb[q]);
+  }
+  __syncthreads();
+  const uint64_t below = (1ull << lane) - 1ull;  // lanes before this one
+  uint32_t seen = 0;                             // ties in earlier slots
 #pragma unroll
-  for (int b = 0; b < kKeysPerThread / 8; ++b) {
-    uint32_t byte = 0;
+  for (int q = 0; q < kKeysPerThread; ++q) {
+    const int64_t i = (int64_t)q * kSelThreads + tid;
+    uint32_t before = 0, total = 0;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int q = 8 * b + e;
-      const bool in = i0 + q < n, tie = in && kr[q] == T;
-      const bool keep = in && (kr[q] > T || (tie && seen < krem));
-      seen += tie ? 1u : 0u;
-      byte |= (keep ? 1u : 0u) << e;
+    for (int w = 0; w < NW; ++w) {
+      const uint32_t c = tcnt[q][w];
+      total += c;
+      before += w < wave ? c : 0u;
     }
-    if (i0 + 8 * b < n) {
-      bits[(i0 >> 3) + b] = (uint8_t)byte;
-      if (bits_copy) bits_copy[(i0 >> 3) + b] = (uint8_t)byte;
+    const bool in = i < n, tie = ((tb[q] >> lane) & 1ull) != 0;
+    const uint32_t rank = seen + before + (uint32_t)__popcll(tb[q] & below);
+    const bool keep = in && (kr[q] > T || (tie && rank < krem));
+    const uint64_t bal = __ballot(keep);
+    if ((lane & 7) == 0 && in) {
+      const uint8_t byte = (uint8_t)(bal >> lane);
+      bits[i >> 3] = byte;
+      if (bits_copy) bits_copy[i >> 3] = byte;
     }
+    seen += total;
   }
 }
 
@@ -294,9 +315,13 @@ __global__ __launch_bounds__(kThreads) void apply_groups_kernel(uint32_t* __rest
 // recomputes the choice from the histograms, so no workgroup waits for another.
 // ---------------------------------------------------------------------------------------
 constexpr int kUHist = 320;
+// The global histogram is kept in kHistCopies copies; workgroup b adds into copy
+// b % kHistCopies, so the few populated bins are not one contended address for every
+// workgroup's atomics.  Readers sum the copies.
+constexpr int kHistCopies = 32;
 
 __global__ void uzero_kernel(uint32_t* hist) {
-  for (int i = threadIdx.x; i < kUHist; i += blockDim.x) hist[i] = 0;
+  for (int i = threadIdx.x; i < kHistCopies * kUHist; i += blockDim.x) hist[i] = 0;
 }
 
 template <int FMT>
@@ -317,7 +342,12 @@ __device__ __forceinline__ void thread_keys(const uint8_t* codes, const void* sc
 // the number of keys equal to T that are kept.
 __device__ __forceinline__ void load_choice(const uint32_t* hist, uint32_t* lh, uint32_t k, bool full,
                                             uint32_t* wsum, uint32_t* out) {
-  for (int i = threadIdx.x; i < kUHist; i += blockDim.x) lh[i] = hist[i];
+  for (int i = threadIdx.x; i < kUHist; i += blockDim.x) {
+    uint32_t v = 0;
+#pragma unroll 8
+    for (int c = 0; c < kHistCopies; ++c) v += hist[c * kUHist + i];
+    lh[i] = v;
+  }
   __syncthreads();
   choose_digit<kThreads>(lh, 256, k, wsum, out);
   if (full) {
@@ -366,7 +396,7 @@ __global__ __launch_bounds__(kThreads) void uhist_kernel(const uint8_t* __restri
   __syncthreads();
   constexpr int NB = PASS == 0 ? 256 : 64, OFF = PASS == 0 ? 0 : 256;
   for (int b = tid; b < NB; b += kThreads)
-    if (lh[b]) atomicAdd(&hist[OFF + b], lh[b]);
+    if (lh[b]) atomicAdd(&hist[(blockIdx.x % kHistCopies) * kUHist + OFF + b], lh[b]);
 }
 
 // Threshold ties per workgroup (index order = workgroup order, then thread order).
@@ -459,7 +489,7 @@ size_t select_ws_bytes(int sparsity, int fmt, int64_t m, int64_t d) {
     case 4:  // block
       return a256((size_t)n_blocks(m, d) * 8) + a256((size_t)(n_blocks(m, d) + 31) / 32 * 4);
     case 5:  // element-wise
-      return a256(kUHist * 4) + a256((size_t)unstructured_wgs(m, d) * 4);
+      return a256(kHistCopies * kUHist * 4) + a256((size_t)unstructured_wgs(m, d) * 4);
     default:
       return 0;
   }
@@ -475,7 +505,7 @@ void carve_select_ws(void* base, int sparsity, int fmt, int64_t m, int64_t d, Se
     ws.group_bits = (uint8_t*)(p + a256((size_t)n * 8));
   } else if (sparsity == 5) {
     ws.hist = (uint32_t*)p;
-    ws.tie_counts = (uint32_t*)(p + a256(kUHist * 4));
+    ws.tie_counts = (uint32_t*)(p + a256(kHistCopies * kUHist * 4));
   }
 }
 
@@ -487,8 +517,8 @@ void launch_select(int fmt, int sparsity, int64_t m, int64_t d, uint8_t* qr_code
   const unsigned gw = (unsigned)((words + kThreads - 1) / kThreads);
   if (sparsity == 3) {
     const dim3 g((unsigned)((d + 63) / 64));
-    if (fmt == 0) hipLaunchKernelGGL((channel_keys_kernel<0>), g, dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, ws.keys);
-    else hipLaunchKernelGGL((channel_keys_kernel<1>), g, dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, ws.keys);
+    if (fmt == 0) hipLaunchKernelGGL((channel_keys_kernel<0>), g, dim3(kChanThreads), 0, s, qr_codes, qr_scales, m, d, ws.keys);
+    else hipLaunchKernelGGL((channel_keys_kernel<1>), g, dim3(kChanThreads), 0, s, qr_codes, qr_scales, m, d, ws.keys);
     hipLaunchKernelGGL(select_top_kernel, dim3(1), dim3(kSelThreads), 0, s,
                        (const uint64_t*)ws.keys, d, d / 2, ws.group_bits, group_mask);
     hipLaunchKernelGGL((apply_groups_kernel<0>), dim3(gw), dim3(kThreads), 0, s,
