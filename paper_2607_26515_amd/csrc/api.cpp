@@ -163,23 +163,14 @@ size_t carve_fwd(void* base, int fmt, int sp, int64_t m, int64_t d, int64_t n, A
 }
 
 struct BwdWs {
-  uint8_t *dyn_codes, *wn_codes, *dym_codes, *xm_codes;
-  void *dyn_scales, *wn_scales, *dym_scales, *xm_scales;
   uint8_t *fa, *fa_sc, *fb, *fb_sc;
 };
 
+// The backward's GEMM operands, written fragment-major straight from bf16 dY, W and X and
+// reused by the two GEMMs (the stream orders them).
 size_t carve_bwd(void* base, int fmt, int64_t m, int64_t d, int64_t n, BwdWs* w) {
   Carver c(base);
   BwdWs t{};
-  t.dyn_codes = (uint8_t*)c.take((size_t)m * n / 2);   // [m][n], blocks along n
-  t.dyn_scales = c.take(scale_bytes(fmt, m, n));
-  t.wn_codes = (uint8_t*)c.take((size_t)d * n / 2);    // [d][n], blocks along n
-  t.wn_scales = c.take(scale_bytes(fmt, d, n));
-  t.dym_codes = (uint8_t*)c.take((size_t)n * m / 2);   // [n][m], blocks along m
-  t.dym_scales = c.take(scale_bytes(fmt, n, m));
-  t.xm_codes = (uint8_t*)c.take((size_t)d * m / 2);    // [d][m], blocks along m
-  t.xm_scales = c.take(scale_bytes(fmt, d, m));
-  // GEMM operands, reused by the two GEMMs (the stream orders them)
   const size_t fa = std::max(resq::frag_bytes(a_pack_mode(fmt), m, n), resq::frag_bytes(a_pack_mode(fmt), n, m));
   const size_t fas = std::max(resq::frag_scale_bytes(m, n), resq::frag_scale_bytes(n, m));
   const size_t fb = std::max(resq::frag_bytes(b_pack_mode(fmt), d, n), resq::frag_bytes(b_pack_mode(fmt), d, m));
@@ -451,16 +442,12 @@ int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uin
     // dX[m][d] = Q_n(dY)[m][n] . (Q_n(W)^T [d][n])^T : contraction over n
     {
       resq::ProfScope prof_(resq::kProfQuantRows, s);
-      resq::launch_quant_rows(format, dY, false, m, n, n, w.dyn_codes, w.dyn_scales, s);
+      resq::launch_residual(format, resq::kResidNone, dY, m, n, n, w.fa, w.fa_sc, nullptr, nullptr,
+                            nullptr, nullptr, s, true);
     }
     {
       resq::ProfScope prof_(resq::kProfQuantCols, s);
-      resq::launch_quant_cols(format, W, false, n, d, d, w.wn_codes, w.wn_scales, s);
-    }
-    {
-      resq::ProfScope prof_(resq::kProfPack, s);
-      resq::launch_pack(a_pack_mode(format), w.dyn_codes, w.dyn_scales, m, n, w.fa, w.fa_sc, s);
-      resq::launch_pack(b_pack_mode(format), w.wn_codes, w.wn_scales, d, n, w.fb, w.fb_sc, s);
+      resq::launch_quant_cols_frag(b_pack_mode(format), W, n, d, d, w.fb, w.fb_sc, s);
     }
     const uint8_t* af[2] = {w.fa, w.fa};
     const uint8_t* asc[2] = {w.fa_sc, w.fa_sc};
@@ -472,13 +459,8 @@ int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uin
     // dW[n][d] = Q_m(dY)^T [n][m] . (Q_m(X)^T [d][m])^T : contraction over m
     {
       resq::ProfScope prof_(resq::kProfQuantCols, s);
-      resq::launch_quant_cols(format, dY, false, m, n, n, w.dym_codes, w.dym_scales, s);
-      resq::launch_quant_cols(format, X, false, m, d, d, w.xm_codes, w.xm_scales, s);
-    }
-    {
-      resq::ProfScope prof_(resq::kProfPack, s);
-      resq::launch_pack(a_pack_mode(format), w.dym_codes, w.dym_scales, n, m, w.fa, w.fa_sc, s);
-      resq::launch_pack(b_pack_mode(format), w.xm_codes, w.xm_scales, d, m, w.fb, w.fb_sc, s);
+      resq::launch_quant_cols_frag(a_pack_mode(format), dY, m, n, n, w.fa, w.fa_sc, s);
+      resq::launch_quant_cols_frag(b_pack_mode(format), X, m, d, d, w.fb, w.fb_sc, s);
     }
     const uint8_t* af[2] = {w.fa, w.fa};
     const uint8_t* asc[2] = {w.fa_sc, w.fa_sc};

@@ -290,6 +290,84 @@ __global__ __launch_bounds__(256) void residual_frag_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------------------
+// Q along columns written as MFMA fragments.  The operand's rows are x's columns and its K
+// axis is x's rows (blocks along the rows of x).  One workgroup per 64-row x 128-column
+// tile of x, i.e. K step kb of the four operand row tiles 4T .. 4T+3: the tile is staged in
+// LDS with 16-byte loads, then for each row tile every thread quantizes 8 consecutive K
+// elements of one operand row with the thread -> (row, half, slice) map of
+// residual_frag_kernel and writes its part of the lane record.  Rows of x past R (the
+// missing half of an MXFP4 K step) and columns past C quantize zeros.
+// ---------------------------------------------------------------------------------------
+
+// HiF4 weight-side record: the 4 threads of lane record `rec` hold 8 BF6 E3M2 fields each
+// (48 bits); threads s and s+1 (s even) write record dwords 3s/2 .. 3s/2+2.
+__device__ __forceinline__ void store_record8_e3m2(uint8_t* __restrict__ frag, uint8_t* __restrict__ fsc,
+                                                   int64_t rec, int s, const uint32_t code[8],
+                                                   uint32_t scale_byte, const int b[2]) {
+  uint64_t h = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) h |= (uint64_t)hif4_e3m2(code[i], b[i / 4]) << (6 * i);
+  const uint32_t plo = __shfl_xor((uint32_t)h, 1, 64), phi = __shfl_xor((uint32_t)(h >> 32), 1, 64);
+  if ((s & 1) == 0) {
+    const uint64_t p1 = ((uint64_t)phi << 32) | plo;  // the odd partner's 48 bits
+    uint32_t* w = reinterpret_cast<uint32_t*>(frag + rec * 24) + 3 * (s >> 1);
+    w[0] = (uint32_t)h;
+    w[1] = (uint32_t)(h >> 32) | ((uint32_t)p1 << 16);
+    w[2] = (uint32_t)(p1 >> 16);
+  }
+  if (s == 0) fsc[rec] = (uint8_t)scale_byte;
+}
+
+template <int FMT, int PMODE, bool VEC>
+__global__ __launch_bounds__(256) void quant_cols_frag_kernel(const uint16_t* __restrict__ x, int64_t R,
+                                                              int64_t C, int64_t ld, int64_t nkb,
+                                                              int64_t nt, uint8_t* __restrict__ frag,
+                                                              uint8_t* __restrict__ fsc) {
+  constexpr int kPitch = 128 + 2;  // bf16 per LDS row (padding spreads the column reads)
+  __shared__ uint16_t tile[64 * kPitch];
+  const int64_t T = blockIdx.x / nkb, kb = blockIdx.x % nkb;
+  const int64_t r0 = kb * 64, c0 = T * 128;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int idx = tid + 256 * q, rr = idx >> 4, cc = (idx & 15) * 8;
+    const int64_t row = r0 + rr, col = c0 + cc;
+    uint32_t w[4] = {0u, 0u, 0u, 0u};
+    if (row < R) {
+      const uint16_t* src = x + row * ld + col;
+      if (VEC && col + 8 <= C) {
+        const uint4 u = *reinterpret_cast<const uint4*>(src);
+        w[0] = u.x; w[1] = u.y; w[2] = u.z; w[3] = u.w;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (col + e < C) w[e >> 1] |= (uint32_t)src[e] << (16 * (e & 1));
+      }
+    }
+    uint32_t* dst = reinterpret_cast<uint32_t*>(tile + rr * kPitch + cc);  // 4-byte aligned
+#pragma unroll
+    for (int e = 0; e < 4; ++e) dst[e] = w[e];
+  }
+  __syncthreads();
+  const int rr = tid >> 3, half = (tid >> 2) & 1, s = tid & 3;
+#pragma unroll
+  for (int tt = 0; tt < 4; ++tt) {
+    const int64_t t = T * 4 + tt;
+    if (t >= nt) break;  // uniform over the workgroup
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = bf16_to_f32(tile[(32 * half + 8 * s + e) * kPitch + 32 * tt + rr]);
+    uint32_t code[8], scale_byte;
+    float val[8];
+    int c1, b[2];
+    quantize8<FMT>(v, code, val, scale_byte, c1, b);
+    const int64_t rec = (t * nkb + kb) * 64 + rr + 32 * half;
+    if constexpr (PMODE == kPackHiB) store_record8_e3m2(frag, fsc, rec, s, code, scale_byte, b);
+    else store_record8<FMT>(frag, fsc, rec, s, code, scale_byte, c1, b);
+  }
+}
+
 inline unsigned grid_rows(int64_t rows) { return (unsigned)(rows < 65535 ? rows : 65535); }
 
 }  // namespace
@@ -309,6 +387,19 @@ void launch_quant_rows(int fmt, const void* x, bool in_f32, int64_t rows, int64_
     else { if (vec) RESQ_QR(kHI, false, true); else RESQ_QR(kHI, false, false); }
   }
 #undef RESQ_QR
+}
+
+void launch_quant_cols_frag(int mode, const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
+                            uint8_t* frag, uint8_t* fscale, hipStream_t s) {
+  if (rows == 0 || cols == 0) return;
+  const int64_t nkb = (rows + 63) / 64, nt = (cols + 31) / 32;
+  const dim3 grid((unsigned)(((nt + 3) / 4) * nkb));
+  const bool vec = ((uintptr_t)x % 16 == 0) && (ld % 8 == 0);
+#define RESQ_QCF(F, P, V) hipLaunchKernelGGL((quant_cols_frag_kernel<F, P, V>), grid, dim3(256), 0, s, x, rows, cols, ld, nkb, nt, frag, fscale)
+  if (mode == kPackMx) { if (vec) RESQ_QCF(kMX, kPackMx, true); else RESQ_QCF(kMX, kPackMx, false); }
+  else if (mode == kPackHiA) { if (vec) RESQ_QCF(kHI, kPackHiA, true); else RESQ_QCF(kHI, kPackHiA, false); }
+  else { if (vec) RESQ_QCF(kHI, kPackHiB, true); else RESQ_QCF(kHI, kPackHiB, false); }
+#undef RESQ_QCF
 }
 
 void launch_quant_cols(int fmt, const void* x, bool in_f32, int64_t rows, int64_t cols,
