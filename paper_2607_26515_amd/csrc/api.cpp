@@ -164,6 +164,7 @@ size_t carve_fwd(void* base, int fmt, int sp, int64_t m, int64_t d, int64_t n, A
 
 struct BwdWs {
   uint8_t *fa, *fa_sc, *fb, *fb_sc;
+  uint8_t *fr, *fr_sc;  // Q_n(dY) for dX when both gradients are computed (one pass over dY)
 };
 
 // The backward's GEMM operands, written fragment-major straight from bf16 dY, W and X and
@@ -179,6 +180,8 @@ size_t carve_bwd(void* base, int fmt, int64_t m, int64_t d, int64_t n, BwdWs* w)
   t.fa_sc = (uint8_t*)c.take(fas);
   t.fb = (uint8_t*)c.take(fb);
   t.fb_sc = (uint8_t*)c.take(fbs);
+  t.fr = (uint8_t*)c.take(resq::frag_bytes(a_pack_mode(fmt), m, n));
+  t.fr_sc = (uint8_t*)c.take(resq::frag_scale_bytes(m, n));
   if (w) *w = t;
   return c.off;
 }
@@ -438,33 +441,37 @@ int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uin
   int rc = check_ws(workspace, workspace_bytes, need);
   if (rc != RESQ_OK) return rc;
   hipStream_t s = (hipStream_t)stream;
+  // dW first when both are wanted: one pass over dY writes Q_m(dY)^T (for dW) and Q_n(dY)
+  // (for dX, into its own buffer).
+  const bool both = dX && dW;
+  if (dW) {
+    // dW[n][d] = Q_m(dY)^T [n][m] . (Q_m(X)^T [d][m])^T : contraction over m
+    {
+      resq::ProfScope prof_(resq::kProfQuantCols, s);
+      resq::launch_quant_cols_frag(a_pack_mode(format), dY, m, n, n, w.fa, w.fa_sc, s,
+                                   both ? w.fr : nullptr, both ? w.fr_sc : nullptr);
+      resq::launch_quant_cols_frag(b_pack_mode(format), X, m, d, d, w.fb, w.fb_sc, s);
+    }
+    const uint8_t* af[2] = {w.fa, w.fa};
+    const uint8_t* asc[2] = {w.fa_sc, w.fa_sc};
+    const resq::GemmOperands op = gemm_operands(format, n, d, m, 1, af, asc, w.fb, w.fb_sc, dW, d);
+    resq::ProfScope prof_(resq::kProfGemm, s);
+    if (!resq::launch_gemm(op, s)) return fail(RESQ_ERR_UNSUPPORTED, "GEMM operand layout rejected");
+  }
   if (dX) {
     // dX[m][d] = Q_n(dY)[m][n] . (Q_n(W)^T [d][n])^T : contraction over n
-    {
+    if (!both) {
       resq::ProfScope prof_(resq::kProfQuantRows, s);
-      resq::launch_residual(format, resq::kResidNone, dY, m, n, n, w.fa, w.fa_sc, nullptr, nullptr,
+      resq::launch_residual(format, resq::kResidNone, dY, m, n, n, w.fr, w.fr_sc, nullptr, nullptr,
                             nullptr, nullptr, s, true);
     }
     {
       resq::ProfScope prof_(resq::kProfQuantCols, s);
       resq::launch_quant_cols_frag(b_pack_mode(format), W, n, d, d, w.fb, w.fb_sc, s);
     }
-    const uint8_t* af[2] = {w.fa, w.fa};
-    const uint8_t* asc[2] = {w.fa_sc, w.fa_sc};
+    const uint8_t* af[2] = {w.fr, w.fr};
+    const uint8_t* asc[2] = {w.fr_sc, w.fr_sc};
     const resq::GemmOperands op = gemm_operands(format, m, d, n, 1, af, asc, w.fb, w.fb_sc, dX, d);
-    resq::ProfScope prof_(resq::kProfGemm, s);
-    if (!resq::launch_gemm(op, s)) return fail(RESQ_ERR_UNSUPPORTED, "GEMM operand layout rejected");
-  }
-  if (dW) {
-    // dW[n][d] = Q_m(dY)^T [n][m] . (Q_m(X)^T [d][m])^T : contraction over m
-    {
-      resq::ProfScope prof_(resq::kProfQuantCols, s);
-      resq::launch_quant_cols_frag(a_pack_mode(format), dY, m, n, n, w.fa, w.fa_sc, s);
-      resq::launch_quant_cols_frag(b_pack_mode(format), X, m, d, d, w.fb, w.fb_sc, s);
-    }
-    const uint8_t* af[2] = {w.fa, w.fa};
-    const uint8_t* asc[2] = {w.fa_sc, w.fa_sc};
-    const resq::GemmOperands op = gemm_operands(format, n, d, m, 1, af, asc, w.fb, w.fb_sc, dW, d);
     resq::ProfScope prof_(resq::kProfGemm, s);
     if (!resq::launch_gemm(op, s)) return fail(RESQ_ERR_UNSUPPORTED, "GEMM operand layout rejected");
   }

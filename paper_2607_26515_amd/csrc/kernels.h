@@ -21,9 +21,11 @@ void launch_quant_rows(int fmt, const void* x, bool in_f32, int64_t rows, int64_
 
 // Column-wise quantization (blocks along rows) of a bf16 matrix written as fragment-major
 // MFMA operands (pack.hip layout, PackMode `mode`): operand rows = the matrix's columns,
-// operand K = its rows.
+// operand K = its rows.  With rfrag (activation modes only), the same pass also writes the
+// row-wise quantization (operand [rows][cols], blocks along cols) to rfrag / rfscale.
 void launch_quant_cols_frag(int mode, const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
-                            uint8_t* frag, uint8_t* fscale, hipStream_t s);
+                            uint8_t* frag, uint8_t* fscale, hipStream_t s, uint8_t* rfrag = nullptr,
+                            uint8_t* rfscale = nullptr);
 
 // Column-wise quantization (blocks along rows), output transposed [cols][rows].
 void launch_quant_cols(int fmt, const void* x, bool in_f32, int64_t rows, int64_t cols,

@@ -319,11 +319,16 @@ __device__ __forceinline__ void store_record8_e3m2(uint8_t* __restrict__ frag, u
   if (s == 0) fsc[rec] = (uint8_t)scale_byte;
 }
 
-template <int FMT, int PMODE, bool VEC>
+// With DUAL, the same tile also yields the row quantization (blocks along the columns of x)
+// as fragments of the operand [R][C]: row tiles 2kb, 2kb+1 and K steps 2T, 2T+1 (written
+// to rfrag / rfsc, activation layout), so x is read once for both.
+template <int FMT, int PMODE, bool VEC, bool DUAL>
 __global__ __launch_bounds__(256) void quant_cols_frag_kernel(const uint16_t* __restrict__ x, int64_t R,
                                                               int64_t C, int64_t ld, int64_t nkb,
                                                               int64_t nt, uint8_t* __restrict__ frag,
-                                                              uint8_t* __restrict__ fsc) {
+                                                              uint8_t* __restrict__ fsc,
+                                                              uint8_t* __restrict__ rfrag,
+                                                              uint8_t* __restrict__ rfsc) {
   constexpr int kPitch = 128 + 2;  // bf16 per LDS row (padding spreads the column reads)
   __shared__ uint16_t tile[64 * kPitch];
   const int64_t T = blockIdx.x / nkb, kb = blockIdx.x % nkb;
@@ -366,6 +371,28 @@ __global__ __launch_bounds__(256) void quant_cols_frag_kernel(const uint16_t* __
     if constexpr (PMODE == kPackHiB) store_record8_e3m2(frag, fsc, rec, s, code, scale_byte, b);
     else store_record8<FMT>(frag, fsc, rec, s, code, scale_byte, c1, b);
   }
+  if constexpr (DUAL) {
+    const int64_t rkb = (C + 63) / 64, rnt = (R + 31) / 32;  // row operand: K steps, row tiles
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int rt = q >> 1, ks = q & 1;
+      const int64_t t = 2 * kb + rt, k = 2 * T + ks;
+      if (t >= rnt || k >= rkb) continue;  // uniform over the workgroup
+      const uint32_t* src = reinterpret_cast<const uint32_t*>(tile + (32 * rt + rr) * kPitch + 64 * ks + 32 * half + 8 * s);
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t w = src[e];
+        v[2 * e] = bf16_to_f32(w & 0xFFFFu);
+        v[2 * e + 1] = bf16_to_f32(w >> 16);
+      }
+      uint32_t code[8], scale_byte;
+      float val[8];
+      int c1, b[2];
+      quantize8<FMT>(v, code, val, scale_byte, c1, b);
+      store_record8<FMT>(rfrag, rfsc, (t * rkb + k) * 64 + rr + 32 * half, s, code, scale_byte, c1, b);
+    }
+  }
 }
 
 inline unsigned grid_rows(int64_t rows) { return (unsigned)(rows < 65535 ? rows : 65535); }
@@ -390,15 +417,21 @@ void launch_quant_rows(int fmt, const void* x, bool in_f32, int64_t rows, int64_
 }
 
 void launch_quant_cols_frag(int mode, const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
-                            uint8_t* frag, uint8_t* fscale, hipStream_t s) {
+                            uint8_t* frag, uint8_t* fscale, hipStream_t s, uint8_t* rfrag,
+                            uint8_t* rfscale) {
   if (rows == 0 || cols == 0) return;
   const int64_t nkb = (rows + 63) / 64, nt = (cols + 31) / 32;
   const dim3 grid((unsigned)(((nt + 3) / 4) * nkb));
   const bool vec = ((uintptr_t)x % 16 == 0) && (ld % 8 == 0);
-#define RESQ_QCF(F, P, V) hipLaunchKernelGGL((quant_cols_frag_kernel<F, P, V>), grid, dim3(256), 0, s, x, rows, cols, ld, nkb, nt, frag, fscale)
-  if (mode == kPackMx) { if (vec) RESQ_QCF(kMX, kPackMx, true); else RESQ_QCF(kMX, kPackMx, false); }
-  else if (mode == kPackHiA) { if (vec) RESQ_QCF(kHI, kPackHiA, true); else RESQ_QCF(kHI, kPackHiA, false); }
-  else { if (vec) RESQ_QCF(kHI, kPackHiB, true); else RESQ_QCF(kHI, kPackHiB, false); }
+  const bool dual = rfrag != nullptr;
+#define RESQ_QCF(F, P, V, D) hipLaunchKernelGGL((quant_cols_frag_kernel<F, P, V, D>), grid, dim3(256), 0, s, x, rows, cols, ld, nkb, nt, frag, fscale, rfrag, rfscale)
+#define RESQ_QCF_V(F, P)                                                                   \
+  if (dual) { if (vec) RESQ_QCF(F, P, true, true); else RESQ_QCF(F, P, false, true); }    \
+  else { if (vec) RESQ_QCF(F, P, true, false); else RESQ_QCF(F, P, false, false); }
+  if (mode == kPackMx) { RESQ_QCF_V(kMX, kPackMx) }
+  else if (mode == kPackHiA) { RESQ_QCF_V(kHI, kPackHiA) }
+  else { if (vec) RESQ_QCF(kHI, kPackHiB, true, false); else RESQ_QCF(kHI, kPackHiB, false, false); }
+#undef RESQ_QCF_V
 #undef RESQ_QCF
 }
 
