@@ -70,6 +70,26 @@ __device__ __forceinline__ float mx_value(uint32_t code, int E) {
   return (code & 8) ? -v : v;
 }
 
+// 2^E as a float for the MX exponent range E in [-127, 127] (2^-127 is subnormal).
+__device__ __forceinline__ float mx_scale_f32(int E) {
+  return E >= -126 ? __uint_as_float((uint32_t)(E + 127) << 23) : __uint_as_float(0x00400000u);
+}
+
+// The same quantization on gfx950's scaled conversions, two elements per instruction:
+// v_cvt_scalef32_pk_fp4_f32 with scale 2^E rounds x / 2^E to the nearest E2M1 magnitude,
+// ties to the even code, saturates at 6 and keeps the sign of a zero result, which is
+// mx_code's definition; v_cvt_scalef32_pk_f32_fp4 returns mx_value.  (A GPU test compares
+// both against the software forms on ties, saturation, signed zeros and subnormals.)
+// Codes of x0, x1: bits 0-3 and 4-7 of the result.
+__device__ __forceinline__ uint32_t mx_code2(float x0, float x1, float scale) {
+  return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, x0, x1, scale, 0) & 0xFFu;
+}
+__device__ __forceinline__ void mx_value2(uint32_t codes2, float scale, float& v0, float& v1) {
+  const auto v = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(codes2, scale, 0);
+  v0 = v[0];
+  v1 = v[1];
+}
+
 // ------------------------------------------------------------------------------------------
 // HiF4 (reading stated in resq.h): 64-element blocks, E6M2 level-1 scale, one-bit level-2
 // (per 8) and level-3 (per 4) down-shifts, S1P2 elements k/4.

@@ -168,10 +168,13 @@ __device__ __forceinline__ void quantize8(const float x[8], uint32_t code[8], fl
     scale_byte = (uint32_t)(E + 127);
     c1 = 0;
     b[0] = b[1] = 0;
+    const float sc = mx_scale_f32(E);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      code[i] = mx_code(x[i], E);
-      val[i] = mx_value(code[i], E);
+    for (int i = 0; i < 8; i += 2) {
+      const uint32_t c2 = mx_code2(x[i], x[i + 1], sc);
+      code[i] = c2 & 15u;
+      code[i + 1] = c2 >> 4;
+      mx_value2(c2, sc, val[i], val[i + 1]);
     }
   } else {
     c1 = hif4_c1(group_max<8>(a));

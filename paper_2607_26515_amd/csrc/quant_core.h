@@ -30,10 +30,13 @@ __device__ __forceinline__ Quad quantize_quad(const float x[4]) {
     q.scale = (uint32_t)(q.E + 127);
     q.c1 = 0;
     q.b = 0;
+    const float sc = mx_scale_f32(q.E);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      q.code[i] = mx_code(x[i], q.E);
-      q.val[i] = mx_value(q.code[i], q.E);
+    for (int i = 0; i < 4; i += 2) {
+      const uint32_t c2 = mx_code2(x[i], x[i + 1], sc);
+      q.code[i] = c2 & 15u;
+      q.code[i + 1] = c2 >> 4;
+      mx_value2(c2, sc, q.val[i], q.val[i + 1]);
     }
   } else {
     const float A = group_max<16>(a);

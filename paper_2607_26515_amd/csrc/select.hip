@@ -26,6 +26,18 @@ constexpr int kWordsPerThread = 4;  // element-wise passes: 4 code words = 32 el
 // element inside its scale block.
 template <int FMT>
 __device__ __forceinline__ void word_keys(uint32_t cw, uint32_t scale, int jpos, uint32_t key[8]) {
+  if constexpr (FMT == 0) {
+    const uint32_t mag = cw & 0x77777777u;  // magnitudes only
+    const float sc = mx_scale_f32((int)scale - 127);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float v0, v1;
+      mx_value2((mag >> (8 * q)) & 0xFFu, sc, v0, v1);
+      key[2 * q] = __float_as_uint(v0);
+      key[2 * q + 1] = __float_as_uint(v1);
+    }
+    return;
+  }
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const uint32_t c = (cw >> (4 * e)) & 7u;  // magnitude only
@@ -60,7 +72,9 @@ template <int FMT>
 __device__ __forceinline__ float decode_at(uint32_t cbyte, uint32_t sc, int64_t j) {
   const uint32_t c = (cbyte >> (4 * (j & 1))) & 15u;
   if constexpr (FMT == 0) {
-    return mx_value(c, (int)sc - 127);
+    float v0, v1;
+    mx_value2(c, mx_scale_f32((int)sc - 127), v0, v1);
+    return v0;
   } else {
     const int p = (int)(j & 63);
     const int b = (int)((sc >> (8 + p / 8)) & 1u) + (int)((sc >> (16 + p / 4)) & 1u);

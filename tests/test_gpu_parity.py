@@ -60,6 +60,31 @@ def test_quantize_rows_f32_midpoints(fmt):
     assert_scales_equal(fmt, scales, os_, "scales")
 
 
+def test_quantize_mx_block_edges():
+    """MXFP4 blocks built around fixed shared exponents E (the block holds 4 * 2^E, so E is
+    floor(log2 amax) - 2): every E2M1 tie and threshold, values that saturate at 6, +-0 and
+    near-tie neighbours, at E from -127 (2^E subnormal) to 124.  Codes and scales must match
+    the oracle exactly."""
+    import paper_2607_26515_amd as P
+    log("quantize mx block edges")
+    ladder = np.array([4.0, -4.0, 7.99, -7.0, 6.0, 6.5, 5.0, 3.5, 2.5, 1.75, 1.25, 0.75, 0.25, -0.25,
+                       0.2499, 0.2501, 0.0, -0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 5.0001, 4.9999, 0.74999,
+                       0.75001, -1.25, -2.5, -3.5, -5.0, 0.125], dtype=np.float64)
+    assert ladder.size == 32
+    exps = [-127, -126, -125, -100, -20, -1, 0, 1, 7, 60, 120, 124]
+    rng = np.random.default_rng(5)
+    rows = []
+    for e in exps:
+        for r in range(4):
+            perm = ladder if r == 0 else rng.permutation(ladder)
+            rows.append(np.concatenate([perm, -perm]) * 2.0 ** e)  # two blocks per row
+    x = np.array(rows, dtype=np.float32)
+    codes, scales = P.quantize(dev_f32(x), "mxfp4", axis=1)
+    oc, os_ = F.quantize("mxfp4", x)
+    assert_codes_equal(codes, oc, "codes")
+    assert_scales_equal("mxfp4", scales, os_, "scales")
+
+
 @pytest.mark.parametrize("fmt", FMTS)
 @pytest.mark.parametrize("rows,cols", [(64, 1), (128, 37), (192, 100), (2048, 130)])
 def test_quantize_cols(fmt, rows, cols):
