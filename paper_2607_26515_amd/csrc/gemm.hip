@@ -29,6 +29,13 @@
 // lanes of tiles past the edge copy zeros, and K steps past the end are copied through a
 // zero-size buffer, so the loop has no data branches.
 //
+// K groups.  A workgroup may hold KG groups of WM x WN waves that share the output tile and
+// split each stage's K range: a stage carries KG consecutive K steps and group g multiplies
+// step g of it, so each barrier is amortised over KG steps and every SIMD holds KG waves
+// with independent MFMA chains.  At the end the groups' accumulators are summed through LDS
+// in group order (deterministic).  Decode-sized grids, which cannot fill the SIMDs with
+// output tiles, use this.
+//
 // Workgroups are mapped to tiles in contiguous chunks per XCD (workgroup b runs on XCD
 // b % 8), so tiles that share a weight column block run on the same XCD and share its L2.
 #include "kernels.h"
@@ -58,10 +65,11 @@ struct GemmParams {
   uint32_t a_frag_off[2], a_sc_off[2], b_frag_off, b_sc_off;
   float* Y;
   int64_t ldy;
-  int64_t grid_m, grid_n, per_xcd;
+  // grid bookkeeping (32-bit: the workgroup count is far below 2^31)
+  uint32_t grid_m, grid_n, per_xcd, n_wg;
   // split-K: ksplit workgroups per tile, each over kper K steps, each writing its partial
   // tile (summed by splitk_reduce_kernel)
-  int ksplit;
+  uint32_t ksplit;
   int64_t kper;
   float* partial;
 };
@@ -70,13 +78,13 @@ struct GemmParams {
 // within a group, row tiles vary fastest, then column tiles.  A run of consecutive tiles (the
 // workgroups resident on one XCD at a time) then covers a compact block of rows and columns
 // that share their A row strips and B column strips in that XCD's L2.
-constexpr int64_t kGroupRows = 8;
-__device__ __forceinline__ void tile_coords(int64_t tile, int64_t grid_m, int64_t grid_n, int64_t& wg_m,
-                                            int64_t& wg_n) {
-  const int64_t group = tile / (kGroupRows * grid_n);
-  const int64_t first = group * kGroupRows;
-  const int64_t rows = min(kGroupRows, grid_m - first);
-  const int64_t in = tile - first * grid_n;
+constexpr uint32_t kGroupRows = 8;
+__device__ __forceinline__ void tile_coords(uint32_t tile, uint32_t grid_m, uint32_t grid_n, uint32_t& wg_m,
+                                            uint32_t& wg_n) {
+  const uint32_t group = tile / (kGroupRows * grid_n);
+  const uint32_t first = group * kGroupRows;
+  const uint32_t rows = min(kGroupRows, grid_m - first);
+  const uint32_t in = tile - first * grid_n;
   wg_m = first + in % rows;
   wg_n = in / rows;
 }
@@ -117,9 +125,10 @@ __device__ __forceinline__ void lds_barrier() {
 }
 
 // Compile-time geometry of one configuration.
-template <int FMT, int WM, int WN, int TM, int TN, int NT, int NS>
+template <int FMT, int WM, int WN, int TM, int TN, int NT, int NS, int KG>
 struct Geo {
-  static constexpr int W = WM * WN;                   // waves
+  static constexpr int WT = WM * WN;                  // waves per K group
+  static constexpr int W = WT * KG;                   // waves
   static constexpr int kThreads = 64 * W;
   static constexpr int MTW = WM * TM, NTW = WN * TN;  // row / column tiles per workgroup
   static constexpr int FA = FMT == 0 ? 16 : 48;       // A lane record bytes (global)
@@ -130,23 +139,29 @@ struct Geo {
   static constexpr int B_LDS = FMT == 0 ? 1024 : 2048;
   static constexpr int SAJ = (MTW + 3) / 4;           // scale copies per A term (4 fragments each)
   static constexpr int SBJ = (NTW + 3) / 4;
-  // LDS stage: A [term][row tile][plane][64 x 16 B]; B [col tile] one 16-byte plane (MXFP4)
-  // or two planes of 12 bytes per lane at a 16-byte stride (HiF4); A scales [term][copy][4 x
-  // 64 B]; B scales [copy][4 x 64 B]
+  // LDS image of one K step: A [term][row tile][plane][64 x 16 B]; B [col tile] one 16-byte
+  // plane (MXFP4) or two planes of 12 bytes per lane at a 16-byte stride (HiF4); A scales
+  // [term][copy][4 x 64 B]; B scales [copy][4 x 64 B].  A stage holds KG such images (BLK
+  // bytes apart), then the padding copies' dump area.
   static constexpr int B_OFF = NT * MTW * A_FRAG;
   static constexpr int SA_OFF = B_OFF + NTW * B_LDS;
   static constexpr int SB_OFF = SA_OFF + NT * SAJ * 256;
-  static constexpr int DUMP_OFF = (SB_OFF + SBJ * 256 + 255) / 256 * 256;  // padding copies
+  static constexpr int BLK = (SB_OFF + SBJ * 256 + 255) / 256 * 256;
+  static constexpr int DUMP_OFF = KG * BLK;  // padding copies
   static constexpr int STAGE = DUMP_OFF + kDumpBytes;
-  // copy instructions per stage by class: A fragments (16 B per lane), B fragments (16 B
+  // copy instructions per K step by class: A fragments (16 B per lane), B fragments (16 B
   // per lane for MXFP4; two 12-byte halves for HiF4), scale bytes of A and B (4 B per lane);
-  // per wave: the class count rounded up to a multiple of W
-  static constexpr int JA = NT * MTW * PA, JB = FMT == 0 ? NTW : 2 * NTW, JS = NT * SAJ + SBJ;
+  // per stage KG times that; per wave: the class count rounded up to a multiple of W
+  static constexpr int JA1 = NT * MTW * PA, JB1 = FMT == 0 ? NTW : 2 * NTW, JS1 = NT * SAJ + SBJ;
+  static constexpr int JA = KG * JA1, JB = KG * JB1, JS = KG * JS1;
   static constexpr int XA = (JA + W - 1) / W, XB = (JB + W - 1) / W, XS = (JS + W - 1) / W;
   static constexpr int JW = XA + XB + XS;
   static constexpr int SZB = FMT == 0 ? 16 : 12;
+  // the K groups' accumulators are summed through the (then idle) stage buffers
+  static constexpr int RED = (KG - 1) * WT * TM * TN * 16 * 64 * 4;
   static size_t lds_bytes() { return (size_t)NS * STAGE; }
   static_assert(NS >= 2, "at least two stages");
+  static constexpr bool kRedFits = RED <= NS * STAGE;
 };
 
 // One copy instruction of a wave: this lane's source offset at K step 0 (kBad: no source,
@@ -155,30 +170,33 @@ struct Geo {
 // the instruction's scalar offset; a K step past the end is copied through a zero-size
 // buffer, so it reads zeros.
 struct Slot {
-  uint32_t voff, lds;
+  uint32_t voff, lds, kk;  // kk: the copy's K step within the stage
 };
 
 // HiF4 with more than one tile per wave keeps one register set and runs two waves per SIMD.
 template <int FMT, int TM, int TN>
 constexpr bool kSingleSet = FMT == 1 && TM * TN > 1;
 
-template <int FMT, int WM, int WN, int TM, int TN, int NT, int NS>
-__global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(kSingleSet<FMT, TM, TN> ? 2 : 1)))
+template <int FMT, int WM, int WN, int TM, int TN, int NT, int NS, int KG>
+__global__ __launch_bounds__(64 * WM * WN * KG)
+__attribute__((amdgpu_waves_per_eu(kSingleSet<FMT, TM, TN> ? 2 : KG)))
 void gemm_kernel(GemmParams p) {
-  using G = Geo<FMT, WM, WN, TM, TN, NT, NS>;
+  using G = Geo<FMT, WM, WN, TM, TN, NT, NS, KG>;
+  static_assert(G::kRedFits, "the K-group reduction must fit in the stage buffers");
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
 
-  const int64_t b = blockIdx.x;
-  const int64_t wgid = (b % kXcds) * p.per_xcd + b / kXcds;  // the K splits of a tile are adjacent
-  if (wgid >= p.grid_m * p.grid_n * p.ksplit) return;
-  const int64_t tile = wgid / p.ksplit;
-  const int split = (int)(wgid % p.ksplit);
-  int64_t wg_m, wg_n;
+  const uint32_t b = blockIdx.x;
+  const uint32_t wgid = (b % kXcds) * p.per_xcd + b / kXcds;  // the K splits of a tile are adjacent
+  if (wgid >= p.n_wg) return;
+  const uint32_t tile = p.ksplit == 1 ? wgid : wgid / p.ksplit;
+  const uint32_t split = wgid - tile * p.ksplit;
+  uint32_t wg_m, wg_n;
   tile_coords(tile, p.grid_m, p.grid_n, wg_m, wg_n);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
-  const int wm = wave % WM, wn = wave / WM;
-  const uint32_t T0 = (uint32_t)(wg_m * G::MTW), N0 = (uint32_t)(wg_n * G::NTW);
+  const int kg = wave / G::WT, wt = wave % G::WT;             // K group, wave within it
+  const int wm = wt % WM, wn = wt / WM;
+  const uint32_t T0 = wg_m * G::MTW, N0 = wg_n * G::NTW;
   const uint32_t nkb = (uint32_t)p.nkb;
   const uint32_t kbeg = (uint32_t)(split * p.kper);                    // this split's K steps:
   const uint32_t klen = (uint32_t)min((int64_t)p.kper, p.nkb - kbeg);  // kbeg .. kbeg+klen-1
@@ -190,60 +208,75 @@ void gemm_kernel(GemmParams p) {
 #pragma unroll
   for (int x = 0; x < G::XA; ++x) {
     const int jc = wave + G::W * x;
-    Slot c{kBad, (uint32_t)G::DUMP_OFF};
+    Slot c{kBad, (uint32_t)G::DUMP_OFF, 0u};
     if (jc < G::JA) {
-      const int t = jc / (G::MTW * G::PA), i = (jc / G::PA) % G::MTW, q = jc % G::PA;
-      c.voff = T0 + i < mt ? p.a_frag_off[t] + (T0 + i) * nkb * G::A_FRAG + lane * G::FA + q * 16 : kBad;
-      c.lds = (uint32_t)((t * G::MTW + i) * G::A_FRAG + q * 1024);
+      const int kk = jc / G::JA1, jl = jc % G::JA1;
+      const int t = jl / (G::MTW * G::PA), i = (jl / G::PA) % G::MTW, q = jl % G::PA;
+      c.voff = T0 + i < mt ? p.a_frag_off[t] + ((T0 + i) * nkb + kk) * G::A_FRAG + lane * G::FA + q * 16 : kBad;
+      c.lds = (uint32_t)(kk * G::BLK + (t * G::MTW + i) * G::A_FRAG + q * 1024);
+      c.kk = (uint32_t)kk;
     }
     sa[x] = c;
   }
 #pragma unroll
   for (int x = 0; x < G::XB; ++x) {
     const int jc = wave + G::W * x;
-    Slot c{kBad, (uint32_t)G::DUMP_OFF};
+    Slot c{kBad, (uint32_t)G::DUMP_OFF, 0u};
     if (jc < G::JB) {
-      const int j = FMT == 0 ? jc : jc / 2, q = FMT == 0 ? 0 : jc % 2;
-      c.voff = N0 + j < nt ? p.b_frag_off + (N0 + j) * nkb * G::B_FRAG + lane * G::FB + q * 12 : kBad;
-      c.lds = (uint32_t)(G::B_OFF + j * G::B_LDS + q * 1024);
+      const int kk = jc / G::JB1, jl = jc % G::JB1;
+      const int j = FMT == 0 ? jl : jl / 2, q = FMT == 0 ? 0 : jl % 2;
+      c.voff = N0 + j < nt ? p.b_frag_off + ((N0 + j) * nkb + kk) * G::B_FRAG + lane * G::FB + q * 12 : kBad;
+      c.lds = (uint32_t)(kk * G::BLK + G::B_OFF + j * G::B_LDS + q * 1024);
+      c.kk = (uint32_t)kk;
     }
     sb[x] = c;
   }
 #pragma unroll
   for (int x = 0; x < G::XS; ++x) {
     const int jc = wave + G::W * x;
-    Slot c{kBad, (uint32_t)G::DUMP_OFF};
+    Slot c{kBad, (uint32_t)G::DUMP_OFF, 0u};
     bool is_a = true;
-    if (jc < NT * G::SAJ) {  // A scales: 4 fragments of one term, 16 lanes x 4 bytes each
-      const int t = jc / G::SAJ, i = 4 * (jc % G::SAJ) + lane / 16;
-      const bool ok = i < G::MTW && T0 + i < mt;
-      c.voff = ok ? p.a_sc_off[t] + (T0 + i) * nkb * 64 + (lane % 16) * 4 : kBad;
-      c.lds = (uint32_t)(G::SA_OFF + jc * 256);
-    } else if (jc < G::JS) {
-      const int q = jc - NT * G::SAJ, j = 4 * q + lane / 16;
-      const bool ok = j < G::NTW && N0 + j < nt;
-      c.voff = ok ? p.b_sc_off + (N0 + j) * nkb * 64 + (lane % 16) * 4 : kBad;
-      c.lds = (uint32_t)(G::SB_OFF + q * 256);
-      is_a = false;
+    if (jc < G::JS) {
+      const int kk = jc / G::JS1, jl = jc % G::JS1;
+      c.kk = (uint32_t)kk;
+      if (jl < NT * G::SAJ) {  // A scales: 4 fragments of one term, 16 lanes x 4 bytes each
+        const int t = jl / G::SAJ, i = 4 * (jl % G::SAJ) + lane / 16;
+        const bool ok = i < G::MTW && T0 + i < mt;
+        c.voff = ok ? p.a_sc_off[t] + ((T0 + i) * nkb + kk) * 64 + (lane % 16) * 4 : kBad;
+        c.lds = (uint32_t)(kk * G::BLK + G::SA_OFF + jl * 256);
+      } else {
+        const int q = jl - NT * G::SAJ, j = 4 * q + lane / 16;
+        const bool ok = j < G::NTW && N0 + j < nt;
+        c.voff = ok ? p.b_sc_off + ((N0 + j) * nkb + kk) * 64 + (lane % 16) * 4 : kBad;
+        c.lds = (uint32_t)(kk * G::BLK + G::SB_OFF + q * 256);
+        is_a = false;
+      }
     }
     ss[x] = c;
     ss_a[x] = is_a;
   }
 
-  // Copy this split's K step k (absolute step kbeg + k) into stage buffer `buf`; steps
-  // past the split's end copy zeros.
-  auto issue = [&](int buf, uint32_t k) {
-    const bool in = k < klen;
-    const uint32_t kb = kbeg + k;
-    const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.a, in ? p.a_bytes : 0u);
-    const __amdgpu_buffer_rsrc_t rb = make_rsrc(p.b, in ? p.b_bytes : 0u);
+  // Copy stage s of this split (its K steps kbeg + s*KG + kk, kk < KG) into stage buffer
+  // `buf`; K steps past the split's end copy zeros (through a zero-size buffer).
+  const uint32_t nsteps = (klen + KG - 1) / KG;
+  auto issue = [&](int buf, uint32_t s) {
+    const uint32_t k0 = s * KG;
+    const uint32_t kb = kbeg + k0;
+    // K steps of this stage inside the split (wave-uniform: it selects scalar descriptors)
+    const uint32_t left = __builtin_amdgcn_readfirstlane(k0 < klen ? klen - k0 : 0u);
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.a, p.a_bytes), rb = make_rsrc(p.b, p.b_bytes);
+    const __amdgpu_buffer_rsrc_t za = make_rsrc(p.a, 0u), zb = make_rsrc(p.b, 0u);
+    auto inside = [&](const Slot& c) { return KG == 1 ? left > 0u : c.kk < left; };
     uint8_t* st = smem + buf * G::STAGE;
 #pragma unroll
-    for (int x = 0; x < G::XA; ++x) copy_to_lds<16>(ra, st + sa[x].lds, sa[x].voff, kb * G::A_FRAG);
+    for (int x = 0; x < G::XA; ++x)
+      copy_to_lds<16>(inside(sa[x]) ? ra : za, st + sa[x].lds, sa[x].voff, kb * G::A_FRAG);
 #pragma unroll
-    for (int x = 0; x < G::XB; ++x) copy_to_lds<G::SZB>(rb, st + sb[x].lds, sb[x].voff, kb * G::B_FRAG);
+    for (int x = 0; x < G::XB; ++x)
+      copy_to_lds<G::SZB>(inside(sb[x]) ? rb : zb, st + sb[x].lds, sb[x].voff, kb * G::B_FRAG);
 #pragma unroll
-    for (int x = 0; x < G::XS; ++x) copy_to_lds<4>(ss_a[x] ? ra : rb, st + ss[x].lds, ss[x].voff, kb * 64u);
+    for (int x = 0; x < G::XS; ++x)
+      copy_to_lds<4>(inside(ss[x]) ? (ss_a[x] ? ra : rb) : za, st + ss[x].lds, ss[x].voff, kb * 64u);
   };
 
   v16f acc[TM][TN];
@@ -268,7 +301,7 @@ void gemm_kernel(GemmParams p) {
   Frag F[2];
 
   auto read = [&](Frag& f, int buf) {
-    const uint8_t* st = smem + buf * G::STAGE;
+    const uint8_t* st = smem + buf * G::STAGE + kg * G::BLK;
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
       const int lj = wn * TN + j;
@@ -351,7 +384,7 @@ void gemm_kernel(GemmParams p) {
   // P are folded (acc += (4 + m_w) P) after the next tile's MFMAs are issued, so the fold's
   // VALU work runs under MFMA execution; the last tile's fold is pending across steps.
   auto step_single = [&](int buf) {
-    const uint8_t* st = smem + buf * G::STAGE;
+    const uint8_t* st = smem + buf * G::STAGE + kg * G::BLK;
     v8i b[TN];
     int sbs[TN];
     float fbs[TN];
@@ -405,7 +438,7 @@ void gemm_kernel(GemmParams p) {
     // with stage k+NS-1, read stage k and run its MFMAs.  Steps past the end multiply zeros.
 #pragma unroll
     for (int s = 0; s < NS - 1; ++s) issue(s, (uint32_t)s);
-    for (uint32_t k0 = 0; k0 < klen; k0 += NS) {
+    for (uint32_t k0 = 0; k0 < nsteps; k0 += NS) {
 #pragma unroll
       for (int u = 0; u < NS; ++u) {
         const uint32_t k = k0 + u;
@@ -431,7 +464,7 @@ void gemm_kernel(GemmParams p) {
     wait_vmcnt<(NS - 1) * G::JW>();
     __syncthreads();
     read(F[0], 0);
-    for (uint32_t k0 = 0; k0 < klen; k0 += U) {
+    for (uint32_t k0 = 0; k0 < nsteps; k0 += U) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const uint32_t k = k0 + u;
@@ -446,10 +479,39 @@ void gemm_kernel(GemmParams p) {
   }
   wait_vmcnt<0>();
 
+  if constexpr (KG > 1) {
+    // sum the K groups' accumulators in group order: groups 1.. park theirs in LDS, group 0
+    // adds them and stores the tile
+    __syncthreads();  // every wave is done with the stage buffers
+    float* red = reinterpret_cast<float*>(smem);
+    constexpr int PER = TM * TN * 16 * 64;  // floats per wave
+    if (kg > 0) {
+      float* dst = red + ((size_t)(kg - 1) * G::WT + wt) * PER;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) dst[((i * TN + j) * 16 + r) * 64 + lane] = acc[i][j][r];
+    }
+    __syncthreads();
+    if (kg > 0) return;
+#pragma unroll
+    for (int g = 1; g < KG; ++g) {
+      const float* src = red + ((size_t)(g - 1) * G::WT + wt) * PER;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[i][j][r] += src[((i * TN + j) * 16 + r) * 64 + lane];
+    }
+  }
+
   if (p.ksplit > 1) {
     // split K: write this split's partial tile in register order (coalesced per wave)
-    constexpr int TE = G::kThreads * TM * TN * 16;  // floats per tile
-    float* part = p.partial + ((size_t)tile * p.ksplit + split) * TE + (size_t)wave * TM * TN * 16 * 64;
+    constexpr int TE = 64 * G::WT * TM * TN * 16;  // floats per tile
+    float* part = p.partial + ((size_t)tile * p.ksplit + split) * TE + (size_t)wt * TM * TN * 16 * 64;
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -478,13 +540,13 @@ void gemm_kernel(GemmParams p) {
 // register order; workgroup b handles the 1024 elements of one (wave, i, j) of one tile.
 template <int WM, int WN, int TM, int TN>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ partial,
-                                                            int ksplit, int64_t grid_m, int64_t grid_n,
+                                                            int ksplit, uint32_t grid_m, uint32_t grid_n,
                                                             int64_t M, int64_t N, float* __restrict__ Y,
                                                             int64_t ldy) {
   constexpr int PARTS = WM * WN * TM * TN, TE = 1024 * PARTS;
-  const int64_t tile = blockIdx.x / PARTS;
+  const uint32_t tile = blockIdx.x / PARTS;
   const int part = (int)(blockIdx.x % PARTS);
-  int64_t wg_m, wg_n;
+  uint32_t wg_m, wg_n;
   tile_coords(tile, grid_m, grid_n, wg_m, wg_n);
   const float* src = partial + (size_t)tile * ksplit * TE + part * 1024;
   const int ij = part % (TM * TN), wave = part / (TM * TN);
@@ -495,35 +557,36 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
     const int lane = e & 63, r = e >> 6;
     float v = src[e];
     for (int k = 1; k < ksplit; ++k) v += src[(size_t)k * TE + e];
-    const int64_t row = (wg_m * WM * TM + wm * TM + i) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-    const int64_t col = (wg_n * WN * TN + wn * TN + j) * 32 + (lane & 31);
+    const int64_t row = ((int64_t)wg_m * WM * TM + wm * TM + i) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+    const int64_t col = ((int64_t)wg_n * WN * TN + wn * TN + j) * 32 + (lane & 31);
     if (row < M && col < N) Y[row * ldy + col] = v;
   }
 }
 
-template <int FMT, int WM, int WN, int TM, int TN, int NS>
+template <int FMT, int WM, int WN, int TM, int TN, int NS, int KG = 1>
 void launch_cfg(GemmParams p, int n_terms, hipStream_t s) {
-  p.grid_m = (p.mt_tiles + WM * TM - 1) / (WM * TM);
-  p.grid_n = (p.nt_tiles + WN * TN - 1) / (WN * TN);
-  const int64_t wgs = p.grid_m * p.grid_n * p.ksplit;
-  p.per_xcd = (wgs + kXcds - 1) / kXcds;
-  const dim3 grid((unsigned)(p.per_xcd * kXcds));
-  const dim3 block(64 * WM * WN);
-  using G2 = Geo<FMT, WM, WN, TM, TN, 2, NS>;
-  using G1 = Geo<FMT, WM, WN, TM, TN, 1, NS>;
+  p.grid_m = (uint32_t)((p.mt_tiles + WM * TM - 1) / (WM * TM));
+  p.grid_n = (uint32_t)((p.nt_tiles + WN * TN - 1) / (WN * TN));
+  p.n_wg = p.grid_m * p.grid_n * p.ksplit;
+  p.per_xcd = (p.n_wg + kXcds - 1) / kXcds;
+  const dim3 grid(p.per_xcd * kXcds);
+  const dim3 block(64 * WM * WN * KG);
+  using G2 = Geo<FMT, WM, WN, TM, TN, 2, NS, KG>;
+  using G1 = Geo<FMT, WM, WN, TM, TN, 1, NS, KG>;
   if (n_terms > 1)
-    hipLaunchKernelGGL((gemm_kernel<FMT, WM, WN, TM, TN, 2, NS>), grid, block, G2::lds_bytes(), s, p);
+    hipLaunchKernelGGL((gemm_kernel<FMT, WM, WN, TM, TN, 2, NS, KG>), grid, block, G2::lds_bytes(), s, p);
   else
-    hipLaunchKernelGGL((gemm_kernel<FMT, WM, WN, TM, TN, 1, NS>), grid, block, G1::lds_bytes(), s, p);
+    hipLaunchKernelGGL((gemm_kernel<FMT, WM, WN, TM, TN, 1, NS, KG>), grid, block, G1::lds_bytes(), s, p);
   if (p.ksplit > 1)
-    hipLaunchKernelGGL((splitk_reduce_kernel<WM, WN, TM, TN>), dim3((unsigned)(p.grid_m * p.grid_n * WM * WN * TM * TN)),
-                       dim3(256), 0, s, (const float*)p.partial, p.ksplit, p.grid_m, p.grid_n, p.M, p.N, p.Y, p.ldy);
+    hipLaunchKernelGGL((splitk_reduce_kernel<WM, WN, TM, TN>), dim3(p.grid_m * p.grid_n * WM * WN * TM * TN),
+                       dim3(256), 0, s, (const float*)p.partial, (int)p.ksplit, p.grid_m, p.grid_n, p.M, p.N, p.Y, p.ldy);
 }
 
 // Tile choice (measured on MI355X): a CU holds one or two workgroups (LDS- and
 // register-bound), so the workgroup count decides how many rounds the grid takes.
-//  - grids too small for 128-row tiles to fill the chip: 64 x 64 tiles, deep pipeline, and
-//    for long K (at least 64 steps per split) K split in two when that fills the CUs;
+//  - grids too small for 128-row tiles to fill the chip: 64 x 64 tiles in K groups (two or
+//    four groups of four waves, see plan()), and for HiF4 with long K (at least 64 steps per
+//    split) K split in two when that fills the CUs;
 //  - MXFP4 with M >= 512 (7B decode and prefill): 128 x 256 tiles (fewest A re-reads per
 //    byte of B), two workgroups per CU;
 //  - otherwise: 128 x 192 tiles.  HiF4 always takes these: with one register set they fit
@@ -536,6 +599,7 @@ constexpr int kCUs = 256;
 
 struct Plan {
   int cfg, ksplit;
+  int kg, ns;  // small tiles: K groups and stages
   int64_t kper, tiles;
   size_t partial_bytes;
 };
@@ -561,6 +625,16 @@ Plan plan(int fmt, int64_t M, int64_t N, int64_t K, bool may_split) {
       pl.kper = (nkb + ks - 1) / ks;
       if (pl.ksplit > 1) pl.partial_bytes = (size_t)pl.tiles * pl.ksplit * (256 * 16) * sizeof(float);
     }
+    // K groups (measured): MXFP4 takes four for long K ranges (>= 128 steps per workgroup)
+    // and two otherwise (two workgroups then share a CU); HiF4 takes two, with two stages
+    // when the grid has more workgroups than CUs (so two share a CU), four otherwise.
+    pl.ns = 4;
+    if (fmt == 0) {
+      pl.kg = pl.kper >= 128 ? 4 : 2;
+    } else {
+      pl.kg = 2;
+      if (pl.tiles * pl.ksplit > kCUs) pl.ns = 2;
+    }
   } else {
     const bool wide = M >= 512 && fmt == 0;
     pl.cfg = wide ? kWide : kMid;
@@ -572,9 +646,15 @@ Plan plan(int fmt, int64_t M, int64_t N, int64_t K, bool may_split) {
 }
 
 template <int FMT>
-void launch_fmt(const GemmParams& p, int cfg, int n_terms, hipStream_t s) {
+void launch_fmt(const GemmParams& p, int cfg, int kg, int ns, int n_terms, hipStream_t s) {
   if (cfg == kSmall) {
-    launch_cfg<FMT, 2, 2, 1, 1, FMT == 0 ? 8 : 6>(p, n_terms, s);
+    if constexpr (FMT == 0) {
+      if (kg == 4) launch_cfg<FMT, 2, 2, 1, 1, 4, 4>(p, n_terms, s);
+      else launch_cfg<FMT, 2, 2, 1, 1, 4, 2>(p, n_terms, s);
+    } else {
+      if (ns == 2) launch_cfg<FMT, 2, 2, 1, 1, 2, 2>(p, n_terms, s);
+      else launch_cfg<FMT, 2, 2, 1, 1, 4, 2>(p, n_terms, s);
+    }
   } else if (cfg == kWide) {
     if constexpr (FMT == 0) launch_cfg<FMT, 2, 2, 2, 4, 4>(p, n_terms, s);  // MXFP4 only
   } else if (cfg == kMid8) {
@@ -613,7 +693,7 @@ bool launch_gemm(const GemmOperands& op, hipStream_t s) {
   if (op.b_frag_off + bf > op.b_bytes || op.b_sc_off + bs > op.b_bytes) return false;
   const Plan pl = plan(op.fmt, op.M, op.N, op.K, op.partial != nullptr);
   GemmParams p{};
-  p.ksplit = pl.ksplit;
+  p.ksplit = (uint32_t)pl.ksplit;
   p.kper = pl.kper;
   p.partial = op.partial;
   p.M = op.M; p.N = op.N; p.K = op.K;
@@ -629,8 +709,8 @@ bool launch_gemm(const GemmOperands& op, hipStream_t s) {
   }
   p.b_frag_off = (uint32_t)op.b_frag_off; p.b_sc_off = (uint32_t)op.b_sc_off;
   p.Y = op.Y; p.ldy = op.ldy;
-  if (op.fmt == 0) launch_fmt<0>(p, pl.cfg, op.n_terms, s);
-  else launch_fmt<1>(p, pl.cfg, op.n_terms, s);
+  if (op.fmt == 0) launch_fmt<0>(p, pl.cfg, pl.kg, pl.ns, op.n_terms, s);
+  else launch_fmt<1>(p, pl.cfg, pl.kg, pl.ns, op.n_terms, s);
   return true;
 }
 
