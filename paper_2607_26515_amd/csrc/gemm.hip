@@ -157,11 +157,11 @@ struct Geo {
   static constexpr int XA = (JA + W - 1) / W, XB = (JB + W - 1) / W, XS = (JS + W - 1) / W;
   static constexpr int JW = XA + XB + XS;
   static constexpr int SZB = FMT == 0 ? 16 : 12;
-  // the K groups' accumulators are summed through the (then idle) stage buffers
+  // the K groups' accumulators are summed through the (then idle) LDS of the stages
   static constexpr int RED = (KG - 1) * WT * TM * TN * 16 * 64 * 4;
-  static size_t lds_bytes() { return (size_t)NS * STAGE; }
+  static constexpr size_t LDS = (size_t)(NS * STAGE > RED ? NS * STAGE : RED);
+  static size_t lds_bytes() { return LDS; }
   static_assert(NS >= 2, "at least two stages");
-  static constexpr bool kRedFits = RED <= NS * STAGE;
 };
 
 // One copy instruction of a wave: this lane's source offset at K step 0 (kBad: no source,
@@ -182,7 +182,8 @@ __global__ __launch_bounds__(64 * WM * WN * KG)
 __attribute__((amdgpu_waves_per_eu(kSingleSet<FMT, TM, TN> ? 2 : KG)))
 void gemm_kernel(GemmParams p) {
   using G = Geo<FMT, WM, WN, TM, TN, NT, NS, KG>;
-  static_assert(G::kRedFits, "the K-group reduction must fit in the stage buffers");
+  static_assert(G::LDS <= 160 * 1024, "a workgroup's LDS is at most 160 KB on gfx950");
+  static_assert((NS - 1) * G::JW < 64, "the vmcnt waits must fit the 6-bit counter");
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
 
   const uint32_t b = blockIdx.x;

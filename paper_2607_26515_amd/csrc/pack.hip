@@ -24,18 +24,12 @@ __device__ __forceinline__ void put6(uint32_t* out, int i, uint32_t f) {
   if ((bit & 31) > 26) out[(bit >> 5) + 1] |= f >> (32 - (bit & 31));
 }
 
+// Lane record l of K step kb of row tile t.
 template <int MODE>
-__global__ __launch_bounds__(kThreads) void pack_kernel(const uint8_t* __restrict__ codes,
-                                                        const void* __restrict__ scales,
-                                                        int64_t rows, int64_t K, int64_t nfrag_rows,
-                                                        uint8_t* __restrict__ frag,
-                                                        uint8_t* __restrict__ fscale) {
-  const int64_t nkb = (K + 63) / 64;
-  const int64_t gid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (gid >= nfrag_rows * nkb * 64) return;
-  const int l = (int)(gid & 63);
-  const int64_t tk = gid >> 6;  // t * nkb + kb
-  const int64_t t = tk / nkb, kb = tk % nkb;
+__device__ __forceinline__ void pack_record(const uint8_t* __restrict__ codes, const void* __restrict__ scales,
+                                            int64_t rows, int64_t K, int64_t nkb, uint8_t* __restrict__ frag,
+                                            uint8_t* __restrict__ fscale, int64_t t, int64_t kb, int l) {
+  const int64_t gid = (t * nkb + kb) * 64 + l;
   const int64_t row = t * 32 + (l & 31);
   const int half = l >> 5;
   const bool in = row < rows && kb * 64 + half * 32 < K;
@@ -81,6 +75,20 @@ __global__ __launch_bounds__(kThreads) void pack_kernel(const uint8_t* __restric
   }
 }
 
+// grid: x covers the lane records of one row tile (64 per K step), y = row tiles (grid-stride)
+template <int MODE>
+__global__ __launch_bounds__(kThreads) void pack_kernel(const uint8_t* __restrict__ codes,
+                                                        const void* __restrict__ scales,
+                                                        int64_t rows, int64_t K, int64_t nfrag_rows,
+                                                        uint8_t* __restrict__ frag,
+                                                        uint8_t* __restrict__ fscale) {
+  const int64_t nkb = (K + 63) / 64;
+  const int64_t local = (int64_t)blockIdx.x * kThreads + threadIdx.x;  // kb * 64 + lane
+  if (local >= nkb * 64) return;
+  for (int64_t t = blockIdx.y; t < nfrag_rows; t += gridDim.y)
+    pack_record<MODE>(codes, scales, rows, K, nkb, frag, fscale, t, local >> 6, (int)(local & 63));
+}
+
 }  // namespace
 
 size_t frag_bytes(int mode, int64_t rows, int64_t K) {
@@ -95,10 +103,9 @@ size_t frag_scale_bytes(int64_t rows, int64_t K) {
 
 void launch_pack(int mode, const uint8_t* codes, const void* scales, int64_t rows, int64_t K,
                  uint8_t* frag, uint8_t* fscale, hipStream_t s) {
-  const int64_t nfr = (rows + 31) / 32;
-  const int64_t total = nfr * ((K + 63) / 64) * 64;
-  if (total == 0) return;
-  const dim3 grid((unsigned)((total + kThreads - 1) / kThreads));
+  const int64_t nfr = (rows + 31) / 32, per_tile = ((K + 63) / 64) * 64;
+  if (nfr == 0 || per_tile == 0) return;
+  const dim3 grid((unsigned)((per_tile + kThreads - 1) / kThreads), (unsigned)(nfr < 65535 ? nfr : 65535));
   if (mode == kPackMx)
     hipLaunchKernelGGL((pack_kernel<kPackMx>), grid, dim3(kThreads), 0, s, codes, scales, rows, K, nfr, frag, fscale);
   else if (mode == kPackHiA)

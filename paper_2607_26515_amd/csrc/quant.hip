@@ -239,13 +239,13 @@ __device__ __forceinline__ void store_record8(uint8_t* __restrict__ frag, uint8_
   if (s == 0) fsc[rec] = (uint8_t)scale_byte;
 }
 
+// Row tile t, K step kb of the fused residual pass (one workgroup of 256 threads).
 template <int FMT, int MODE, bool VEC>
-__global__ __launch_bounds__(256) void residual_frag_kernel(
+__device__ __forceinline__ void residual_frag_tile(
     const uint16_t* __restrict__ X, int64_t m, int64_t d, int64_t ldx, int64_t nkb,
     uint8_t* __restrict__ fx, uint8_t* __restrict__ fsx, uint8_t* __restrict__ fr,
-    uint8_t* __restrict__ fsr) {
-  const int64_t f = blockIdx.x;  // fragment index t * nkb + kb
-  const int64_t t = f / nkb, kb = f % nkb;
+    uint8_t* __restrict__ fsr, int64_t t, int64_t kb) {
+  const int64_t f = t * nkb + kb;  // fragment index
   const int tid = threadIdx.x;
   const int rr = tid >> 3, half = (tid >> 2) & 1, s = tid & 3;
   const int64_t row = t * 32 + rr;
@@ -293,6 +293,17 @@ __global__ __launch_bounds__(256) void residual_frag_kernel(
   }
 }
 
+// grid: x = K step, y = row tiles (grid-stride)
+template <int FMT, int MODE, bool VEC>
+__global__ __launch_bounds__(256) void residual_frag_kernel(
+    const uint16_t* __restrict__ X, int64_t m, int64_t d, int64_t ldx, int64_t nkb,
+    uint8_t* __restrict__ fx, uint8_t* __restrict__ fsx, uint8_t* __restrict__ fr,
+    uint8_t* __restrict__ fsr) {
+  const int64_t mtiles = (m + 31) / 32;
+  for (int64_t t = blockIdx.y; t < mtiles; t += gridDim.y)
+    residual_frag_tile<FMT, MODE, VEC>(X, m, d, ldx, nkb, fx, fsx, fr, fsr, t, blockIdx.x);
+}
+
 // ---------------------------------------------------------------------------------------
 // Q along columns written as MFMA fragments.  The operand's rows are x's columns and its K
 // axis is x's rows (blocks along the rows of x).  One workgroup per 64-row x 128-column
@@ -325,16 +336,15 @@ __device__ __forceinline__ void store_record8_e3m2(uint8_t* __restrict__ frag, u
 // With DUAL, the same tile also yields the row quantization (blocks along the columns of x)
 // as fragments of the operand [R][C]: row tiles 2kb, 2kb+1 and K steps 2T, 2T+1 (written
 // to rfrag / rfsc, activation layout), so x is read once for both.
+// Operand row tiles 4T .. 4T+3, K step kb (one workgroup of 256 threads; `tile` is its
+// 64 x 128 staging buffer).
 template <int FMT, int PMODE, bool VEC, bool DUAL>
-__global__ __launch_bounds__(256) void quant_cols_frag_kernel(const uint16_t* __restrict__ x, int64_t R,
-                                                              int64_t C, int64_t ld, int64_t nkb,
-                                                              int64_t nt, uint8_t* __restrict__ frag,
-                                                              uint8_t* __restrict__ fsc,
-                                                              uint8_t* __restrict__ rfrag,
-                                                              uint8_t* __restrict__ rfsc) {
+__device__ __forceinline__ void quant_cols_frag_tile(const uint16_t* __restrict__ x, int64_t R,
+                                                     int64_t C, int64_t ld, int64_t nkb, int64_t nt,
+                                                     uint8_t* __restrict__ frag, uint8_t* __restrict__ fsc,
+                                                     uint8_t* __restrict__ rfrag, uint8_t* __restrict__ rfsc,
+                                                     uint16_t* tile, int64_t T, int64_t kb) {
   constexpr int kPitch = 128 + 2;  // bf16 per LDS row (padding spreads the column reads)
-  __shared__ uint16_t tile[64 * kPitch];
-  const int64_t T = blockIdx.x / nkb, kb = blockIdx.x % nkb;
   const int64_t r0 = kb * 64, c0 = T * 128;
   const int tid = threadIdx.x;
 #pragma unroll
@@ -398,6 +408,23 @@ __global__ __launch_bounds__(256) void quant_cols_frag_kernel(const uint16_t* __
   }
 }
 
+// grid: x = K step, y = groups of four operand row tiles (grid-stride)
+template <int FMT, int PMODE, bool VEC, bool DUAL>
+__global__ __launch_bounds__(256) void quant_cols_frag_kernel(const uint16_t* __restrict__ x, int64_t R,
+                                                              int64_t C, int64_t ld, int64_t nkb,
+                                                              int64_t nt, uint8_t* __restrict__ frag,
+                                                              uint8_t* __restrict__ fsc,
+                                                              uint8_t* __restrict__ rfrag,
+                                                              uint8_t* __restrict__ rfsc) {
+  constexpr int kPitch = 128 + 2;
+  __shared__ uint16_t tile[64 * kPitch];
+  const int64_t ngroups = (nt + 3) / 4;
+  for (int64_t T = blockIdx.y; T < ngroups; T += gridDim.y) {
+    if (T != blockIdx.y) __syncthreads();  // the previous group's reads of the tile are done
+    quant_cols_frag_tile<FMT, PMODE, VEC, DUAL>(x, R, C, ld, nkb, nt, frag, fsc, rfrag, rfsc, tile, T, blockIdx.x);
+  }
+}
+
 inline unsigned grid_rows(int64_t rows) { return (unsigned)(rows < 65535 ? rows : 65535); }
 
 }  // namespace
@@ -424,7 +451,7 @@ void launch_quant_cols_frag(int mode, const uint16_t* x, int64_t rows, int64_t c
                             uint8_t* rfscale) {
   if (rows == 0 || cols == 0) return;
   const int64_t nkb = (rows + 63) / 64, nt = (cols + 31) / 32;
-  const dim3 grid((unsigned)(((nt + 3) / 4) * nkb));
+  const dim3 grid((unsigned)nkb, grid_rows((nt + 3) / 4));
   const bool vec = ((uintptr_t)x % 16 == 0) && (ld % 8 == 0);
   const bool dual = rfrag != nullptr;
 #define RESQ_QCF(F, P, V, D) hipLaunchKernelGGL((quant_cols_frag_kernel<F, P, V, D>), grid, dim3(256), 0, s, x, rows, cols, ld, nkb, nt, frag, fscale, rfrag, rfscale)
@@ -454,7 +481,7 @@ void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d,
   if (m == 0 || d == 0) return;
   if (frag) {
     const int64_t nkb = (d + 63) / 64;
-    const dim3 grid((unsigned)(((m + 31) / 32) * nkb));
+    const dim3 grid((unsigned)nkb, grid_rows((m + 31) / 32));
     const bool vec16 = ((uintptr_t)X % 16 == 0) && (ldx % 8 == 0);
 #define RESQ_RF(F, M, V) hipLaunchKernelGGL((residual_frag_kernel<F, M, V>), grid, dim3(256), 0, s, X, m, d, ldx, nkb, qx_codes, (uint8_t*)qx_scales, qr_codes, (uint8_t*)qr_scales)
 #define RESQ_RF_MODE(F, V)                                        \
