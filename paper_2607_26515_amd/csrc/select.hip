@@ -61,12 +61,17 @@ __device__ __forceinline__ uint32_t scale_at(const void* scales, int64_t row, in
 }
 
 // ---------------------------------------------------------------------------------------
-// Channel keys.  Workgroup = 64 channels.  Its four waves load a 64-row chunk (16 independent
-// rows per wave, issued together) and decode it into LDS; wave 0 then adds the chunk row by
-// row (the fixed sequential order) while the waves already load the next chunk.
+// Channel keys.  Workgroup = 64 channels (lane = channel) x 16 waves; wave w sums the squares
+// of a contiguous range of rows in float64 and the ranges are added in wave order.  That
+// equals the defined row-by-row sum exactly whenever no float64 addition of either order
+// rounds: every square v^2 is a multiple of 2^L, L = twice the exponent of the lowest set
+// bit of the smallest such v in the channel, so if the total is below 2^(L+53) every partial
+// sum, in any order, is a multiple of 2^L below 2^(L+53) and thus exact.  The check uses
+// 2^(L+52) to absorb any rounding of the computed total; a channel that fails it is summed
+// again row by row in the defined order.
 // ---------------------------------------------------------------------------------------
-constexpr int kChunk = 256;        // channel keys: rows per chunk
-constexpr int kChanThreads = 1024;  // channel keys: 16 waves load and decode, wave 0 adds
+constexpr int kChanThreads = 1024;  // channel keys: 16 waves, one row range each
+constexpr int kNoBit = 1 << 20;      // "no nonzero term yet" for the lowest-bit exponent
 
 template <int FMT>
 __device__ __forceinline__ float decode_at(uint32_t cbyte, uint32_t sc, int64_t j) {
@@ -82,48 +87,62 @@ __device__ __forceinline__ float decode_at(uint32_t cbyte, uint32_t sc, int64_t 
   }
 }
 
+// Exponent of the lowest set bit of a nonzero float32 (subnormals included).
+__device__ __forceinline__ int lowest_bit_exp(float v) {
+  const uint32_t u = __float_as_uint(v) & 0x7FFFFFFFu;
+  const int ef = (int)(u >> 23);
+  const uint32_t sig = ef ? ((u & 0x7FFFFFu) | 0x800000u) : u;
+  return (ef ? ef - 150 : -149) + __builtin_ctz(sig);
+}
+
 template <int FMT>
 __global__ __launch_bounds__(kChanThreads) void channel_keys_kernel(const uint8_t* __restrict__ codes,
                                                                     const void* __restrict__ scales,
                                                                     int64_t m, int64_t d,
                                                                     double* __restrict__ keys) {
-  constexpr int NW = kChanThreads / 64, RPW = kChunk / NW;  // waves; rows per wave per chunk
-  __shared__ float val[kChunk][64];
+  constexpr int NW = kChanThreads / 64, U = 8;
+  __shared__ double part[NW][64];
+  __shared__ int low[NW][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t j = (int64_t)blockIdx.x * 64 + lane;
-  uint32_t cb[RPW], sc[RPW];
-  auto load = [&](int64_t r0) {
-#pragma unroll
-    for (int q = 0; q < RPW; ++q) {
-      const int64_t row = r0 + wave + NW * q;
-      cb[q] = 0;
-      sc[q] = 0;
-      if (row < m && j < d) {
-        cb[q] = codes[row * (d / 2) + j / 2];
-        sc[q] = scale_at<FMT>(scales, row, d, j);
-      }
-    }
+  const int64_t per = (m + NW - 1) / NW;
+  const int64_t r0 = min((int64_t)wave * per, m), r1 = min(r0 + per, m);
+  auto value = [&](int64_t row) {
+    return decode_at<FMT>(codes[row * (d / 2) + j / 2], scale_at<FMT>(scales, row, d, j), j);
   };
   double acc = 0.0;
-  load(0);
-  for (int64_t r0 = 0; r0 < m; r0 += kChunk) {
+  int lo = kNoBit;
+  if (j < d) {
+    for (int64_t r = r0; r < r1; r += U) {
+      float v[U];
 #pragma unroll
-    for (int q = 0; q < RPW; ++q) val[wave + NW * q][lane] = j < d ? decode_at<FMT>(cb[q], sc[q], j) : 0.f;
-    __syncthreads();
-    if (r0 + kChunk < m) load(r0 + kChunk);  // in flight while wave 0 adds this chunk
-    // Rows past m were decoded from zero codes, so the whole chunk is summed: they add +0.0,
-    // which leaves the (non-negative) sum unchanged.  Reads run 16 rows ahead of the chain.
-    if (wave == 0)
-      for (int r16 = 0; r16 < kChunk; r16 += 16) {
-        double v[16];
+      for (int u = 0; u < U; ++u) v[u] = r + u < r1 ? value(r + u) : 0.f;  // loads issued together
 #pragma unroll
-        for (int u = 0; u < 16; ++u) v[u] = (double)val[r16 + u][lane];
-#pragma unroll
-        for (int u = 0; u < 16; ++u) acc += v[u] * v[u];  // exact square: at most 6 significant bits in v
+      for (int u = 0; u < U; ++u) {
+        acc += (double)v[u] * (double)v[u];  // exact square: at most 6 significant bits in v
+        if (v[u] != 0.f) lo = min(lo, 2 * lowest_bit_exp(v[u]));
       }
-    __syncthreads();
+    }
   }
-  if (wave == 0 && j < d) keys[j] = acc;
+  part[wave][lane] = acc;
+  low[wave][lane] = lo;
+  __syncthreads();
+  if (wave != 0 || j >= d) return;
+  double sum = 0.0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    sum += part[w][lane];
+    lo = min(lo, low[w][lane]);
+  }
+  if (sum != 0.0 && !(sum < ldexp(1.0, lo + 52))) {
+    // some addition may round: the defined order, rows 0 .. m-1
+    sum = 0.0;
+    for (int64_t r = 0; r < m; ++r) {
+      const float v = value(r);
+      sum += (double)v * (double)v;
+    }
+  }
+  keys[j] = sum;
 }
 
 // ---------------------------------------------------------------------------------------
@@ -137,7 +156,7 @@ __global__ __launch_bounds__(kThreads) void block_keys_kernel(const double* __re
   const int64_t nJ = d / 64, nI = (m + 31) / 32;
   const int64_t t = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (t >= nI * nJ) return;
-  const int64_t I = t / nJ, J = t % nJ;
+  const int64_t I = (uint32_t)t / (uint32_t)nJ, J = t - I * nJ;  // t < 2^15 (at most 24576 blocks)
   const int64_t r1 = (32 * I + 32 < m) ? 32 * I + 32 : m;
   const int64_t ld = d / (FMT == 0 ? 32 : 64);
   double v[32][P];
@@ -240,6 +259,7 @@ __global__ __launch_bounds__(kSelThreads) void select_top_kernel(const uint64_t*
     const int64_t i = (int64_t)q * kSelThreads + tid;
     kr[q] = i < n ? keys[i] : 0;
   }
+  __shared__ uint64_t found;
   uint64_t prefix = 0, mask = 0;
   uint32_t krem = (uint32_t)k;
   for (int shift = 56; shift >= 0; shift -= 8) {
@@ -255,7 +275,19 @@ __global__ __launch_bounds__(kSelThreads) void select_top_kernel(const uint64_t*
     prefix |= (uint64_t)ch[0] << shift;
     krem = ch[1];
     mask |= (uint64_t)255 << shift;
+    const uint32_t in_bin = hist[ch[0]];  // keys sharing the threshold's digits so far
     __syncthreads();  // ch and hist are reused by the next pass
+    if (in_bin == 1 && shift > 0) {
+      // a single key has this prefix: it is the threshold (krem = 1), no further digit needed
+#pragma unroll
+      for (int q = 0; q < kKeysPerThread; ++q) {
+        const int64_t i = (int64_t)q * kSelThreads + tid;
+        if (i < n && (kr[q] & mask) == prefix) found = kr[q];
+      }
+      __syncthreads();
+      prefix = found;
+      break;
+    }
   }
   const uint64_t T = prefix;  // threshold key; krem of its ties are kept (in index order)
   uint64_t tb[kKeysPerThread];  // tie ballots per slot
@@ -299,24 +331,27 @@ __device__ __forceinline__ uint32_t nibble_mask(uint32_t kb) {
   return m;
 }
 
-// Apply kept channels (KIND 0) or kept blocks (KIND 1): one thread per code word.
+// Apply kept channels (KIND 0) or kept blocks (KIND 1): one thread per code word; grid x
+// covers the d/8 words of a row, y the rows (grid-stride).
 template <int KIND>
 __global__ __launch_bounds__(kThreads) void apply_groups_kernel(uint32_t* __restrict__ codes,
                                                                 int64_t m, int64_t d,
                                                                 const uint8_t* __restrict__ gbits,
                                                                 uint8_t* __restrict__ keep_mask) {
-  const int64_t w = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (w >= m * (d / 8)) return;
-  const int64_t row = w / (d / 8), c8 = w % (d / 8);
-  uint32_t kb;
-  if constexpr (KIND == 0) {
-    kb = gbits[c8];
-  } else {
-    const int64_t bit = (row / 32) * (d / 64) + (8 * c8) / 64;
-    kb = ((gbits[bit >> 3] >> (bit & 7)) & 1u) ? 0xFFu : 0u;
+  const int64_t c8 = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (c8 >= d / 8) return;
+  for (int64_t row = blockIdx.y; row < m; row += gridDim.y) {
+    uint32_t kb;
+    if constexpr (KIND == 0) {
+      kb = gbits[c8];
+    } else {
+      const int64_t bit = (row / 32) * (d / 64) + c8 / 8;
+      kb = ((gbits[bit >> 3] >> (bit & 7)) & 1u) ? 0xFFu : 0u;
+    }
+    const int64_t w = row * (d / 8) + c8;
+    codes[w] &= nibble_mask(kb);
+    if (keep_mask) keep_mask[w] = (uint8_t)kb;
   }
-  codes[w] &= nibble_mask(kb);
-  if (keep_mask) keep_mask[w] = (uint8_t)kb;
 }
 
 // ---------------------------------------------------------------------------------------
@@ -342,7 +377,7 @@ template <int FMT>
 __device__ __forceinline__ void thread_keys(const uint8_t* codes, const void* scales, int64_t d,
                                             int64_t w0, uint32_t key[32]) {
   const uint4 cw = *reinterpret_cast<const uint4*>(codes + 4 * w0);
-  const int64_t e0 = 8 * w0, row = e0 / d, j = e0 % d;  // 32 elements inside one scale block
+  const uint32_t e0 = (uint32_t)(8 * w0), row = e0 / (uint32_t)d, j = e0 - row * (uint32_t)d;  // 32 elements, one scale block
   const uint32_t sc = scale_at<FMT>(scales, row, d, j);
   const int jpos = FMT == 0 ? 0 : (int)(j & 63);
   word_keys<FMT>(cw.x, sc, jpos, key);
@@ -527,15 +562,14 @@ void launch_select(int fmt, int sparsity, int64_t m, int64_t d, uint8_t* qr_code
                    const void* qr_scales, const double* partials, uint8_t* keep_mask,
                    uint8_t* group_mask, const SelectWs& ws, hipStream_t s) {
   if (m == 0 || d == 0) return;
-  const int64_t words = m * (d / 8);
-  const unsigned gw = (unsigned)((words + kThreads - 1) / kThreads);
+  const dim3 gw((unsigned)((d / 8 + kThreads - 1) / kThreads), (unsigned)(m < 65535 ? m : 65535));
   if (sparsity == 3) {
     const dim3 g((unsigned)((d + 63) / 64));
     if (fmt == 0) hipLaunchKernelGGL((channel_keys_kernel<0>), g, dim3(kChanThreads), 0, s, qr_codes, qr_scales, m, d, ws.keys);
     else hipLaunchKernelGGL((channel_keys_kernel<1>), g, dim3(kChanThreads), 0, s, qr_codes, qr_scales, m, d, ws.keys);
     hipLaunchKernelGGL(select_top_kernel, dim3(1), dim3(kSelThreads), 0, s,
                        (const uint64_t*)ws.keys, d, d / 2, ws.group_bits, group_mask);
-    hipLaunchKernelGGL((apply_groups_kernel<0>), dim3(gw), dim3(kThreads), 0, s,
+    hipLaunchKernelGGL((apply_groups_kernel<0>), gw, dim3(kThreads), 0, s,
                        (uint32_t*)qr_codes, m, d, (const uint8_t*)ws.group_bits, keep_mask);
   } else if (sparsity == 4) {
     const int64_t nb = n_blocks(m, d);
@@ -544,7 +578,7 @@ void launch_select(int fmt, int sparsity, int64_t m, int64_t d, uint8_t* qr_code
     else hipLaunchKernelGGL((block_keys_kernel<1>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
     hipLaunchKernelGGL(select_top_kernel, dim3(1), dim3(kSelThreads), 0, s,
                        (const uint64_t*)ws.keys, nb, nb / 2, ws.group_bits, group_mask);
-    hipLaunchKernelGGL((apply_groups_kernel<1>), dim3(gw), dim3(kThreads), 0, s,
+    hipLaunchKernelGGL((apply_groups_kernel<1>), gw, dim3(kThreads), 0, s,
                        (uint32_t*)qr_codes, m, d, (const uint8_t*)ws.group_bits, keep_mask);
   } else if (sparsity == 5) {
     const unsigned nwg = (unsigned)unstructured_wgs(m, d);

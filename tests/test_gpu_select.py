@@ -116,3 +116,20 @@ def test_linear_fwd_global(fmt, sp, m, d, n):
     assert_close(y, o["y64"], f"Y {fmt} {sp}")
     y2 = host(P.linear_fwd_prepared(x, P.prepare_weights(qc, qs, fmt), n, fmt, sp))
     assert np.array_equal(y.view(np.uint32), y2.view(np.uint32))
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("sp", ["channel50", "block32x64_50"])
+def test_select_wide_range_channels(fmt, sp):
+    """Channels whose residual magnitudes span ~2^56: their float64 sums of squares can round,
+    so the GPU must reproduce the defined row-by-row order (the channel keys' sequential path)
+    while the other channels take the order-free path; masks must still match the oracle."""
+    log(f"select wide range {fmt} {sp}")
+    m, d = 96, 256
+    rng = np.random.default_rng(21)
+    x = rng.standard_normal((m, d)).astype(np.float32)
+    for col in (5, 70, 200):
+        x[0::2, col] = 2.0 ** 28 * (1 + 2.0 ** -6)
+        x[1::2, col] = -(2.0 ** -28) * (1 + 3 * 2.0 ** -7)
+    x[::7, 130] = 2.0 ** 20 * 1.015625  # a channel between the two ranges
+    _check_select(fmt, sp, f32_to_bf16_bits(x))
