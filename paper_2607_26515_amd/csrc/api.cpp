@@ -72,9 +72,7 @@ struct Carver {
 
 // Activation-side buffers used by resq_linear_fwd and the selection.
 struct ActWs {
-  uint8_t* qx_codes;
-  void* qx_scales;
-  uint8_t* qr_codes;
+  uint8_t* qr_codes;  // dense K-major Q(dX) (global selections only)
   void* qr_scales;
   double* partials;
   uint8_t* frag_x;
@@ -143,9 +141,7 @@ void carve_prepared(const void* base, int fmt, int64_t n, int64_t d, const uint8
 size_t carve_fwd(void* base, int fmt, int sp, int64_t m, int64_t d, int64_t n, ActWs* w) {
   Carver c(base);
   ActWs t{};
-  t.qx_codes = (uint8_t*)c.take((size_t)m * d / 2);
-  t.qx_scales = c.take(scale_bytes(fmt, m, d));
-  if (sp != RESQ_S_NONE) {
+  if (global_kind(sp)) {  // the dense K-major Q(dX) the selection ranks
     t.qr_codes = (uint8_t*)c.take((size_t)m * d / 2);
     t.qr_scales = c.take(scale_bytes(fmt, m, d));
   }
@@ -339,14 +335,18 @@ int linear_fwd_core(int format, int sparsity, const uint16_t* X, int64_t m, int6
                     int64_t ldx, const void* wprep, int64_t n, float* Y, int64_t ldy,
                     const ActWs& w, hipStream_t s) {
   if (global_kind(sparsity)) {
-    // the selection needs the whole K-major Q(dX); pack both operands afterwards
-    int rc = run_activation_side(format, sparsity, X, m, d, ldx, w.qx_codes, w.qx_scales,
-                                 w.qr_codes, w.qr_scales, nullptr, nullptr, w.partials,
-                                 w.sel, s);
-    if (rc != RESQ_OK) return rc;
-    resq::ProfScope prof_(resq::kProfPack, s);
-    resq::launch_pack(a_pack_mode(format), w.qx_codes, w.qx_scales, m, d, w.frag_x, w.fsc_x, s);
-    resq::launch_pack(a_pack_mode(format), w.qr_codes, w.qr_scales, m, d, w.frag_r, w.fsc_r, s);
+    // the residual pass writes Q(X) as MFMA fragments and the dense Q(dX) K-major (the
+    // selection ranks all of it); the selection then writes S(Q(dX)) as fragments
+    {
+      resq::ProfScope prof_(resq::kProfResidual, s);
+      const bool elem = sparsity == RESQ_S_UNSTRUCT50;
+      resq::launch_residual(format, resq::kResidDense, X, m, d, ldx, w.frag_x, w.fsc_x, w.qr_codes,
+                            w.qr_scales, nullptr, sparsity == RESQ_S_BLOCK32X64_50 ? w.partials : nullptr,
+                            s, true, elem ? w.sel.hist : nullptr, elem ? resq::select_hist_words() : 0);
+    }
+    resq::ProfScope prof_(resq::kProfSelect, s);
+    resq::launch_select_frag(format, sparsity, m, d, w.qr_codes, w.qr_scales, w.partials, w.sel,
+                             a_pack_mode(format), w.frag_r, w.fsc_r, s);
   } else {
     // local kinds: the residual pass writes the MFMA fragments directly
     resq::ProfScope prof_(resq::kProfResidual, s);

@@ -1,0 +1,67 @@
+// One lane record of a fragment-major MFMA operand (layout in pack.hip): the 32 K-major codes
+// (one uint4, element 2i in the low nibble of byte i) of row 32t + l%32, K elements
+// 64kb + 32(l/32) .. +31, and their scale word (MX: the E8M0 byte; HiF4: the metadata word
+// of the 64-block), written as record `gid` of `frag` plus its scale byte in `fscale`.
+#pragma once
+
+#include "device_fp4.h"
+#include "kernels.h"
+
+namespace resq {
+
+// OR a 6-bit field into bit position 6i of a little-endian bit string.
+__device__ __forceinline__ void put6(uint32_t* out, int i, uint32_t f) {
+  const int bit = 6 * i;
+  out[bit >> 5] |= f << (bit & 31);
+  if ((bit & 31) > 26) out[(bit >> 5) + 1] |= f >> (32 - (bit & 31));
+}
+
+// Nibble mask keeping the elements whose bit is set in `keep` (bit e = element e of a word).
+__device__ __forceinline__ uint32_t nibble_mask8(uint32_t keep) {
+  uint32_t m = 0;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) m |= ((keep >> e) & 1u) * (0xFu << (4 * e));
+  return m;
+}
+
+// half = l / 32 (which 32-element half of the 64-element HiF4 block the record holds).
+template <int MODE>
+__device__ __forceinline__ void store_frag_record(uint8_t* __restrict__ frag, uint8_t* __restrict__ fscale,
+                                                  int64_t gid, uint4 cw, uint32_t scale, int half) {
+  if constexpr (MODE == kPackMx) {
+    *reinterpret_cast<uint4*>(frag + gid * 16) = cw;
+    fscale[gid] = (uint8_t)scale;
+  } else {
+    const uint32_t c1 = scale & 0xFFu;
+    const uint32_t words[4] = {cw.x, cw.y, cw.z, cw.w};
+    uint32_t a[6] = {0, 0, 0, 0, 0, 0}, b[6] = {0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+      const uint32_t code = (words[i >> 3] >> (4 * (i & 7))) & 15u;
+      const int h = half * 8 + (i >> 2);
+      const int sh = (int)((scale >> (8 + (h >> 1))) & 1u) + (int)((scale >> (16 + h)) & 1u);
+      if constexpr (MODE == kPackHiA) {
+        uint32_t hi, lo;
+        hif4_split_e2m3(code, (int)c1, sh, hi, lo);
+        put6(a, i, hi);
+        put6(b, i, lo);
+      } else {
+        put6(a, i, hif4_e3m2(code, sh));
+      }
+    }
+    if constexpr (MODE == kPackHiA) {
+      uint4* p = reinterpret_cast<uint4*>(frag + gid * 48);
+      p[0] = make_uint4(a[0], a[1], a[2], a[3]);
+      p[1] = make_uint4(a[4], a[5], b[0], b[1]);
+      p[2] = make_uint4(b[2], b[3], b[4], b[5]);
+    } else {
+      uint2* p = reinterpret_cast<uint2*>(frag + gid * 24);
+      p[0] = make_uint2(a[0], a[1]);
+      p[1] = make_uint2(a[2], a[3]);
+      p[2] = make_uint2(a[4], a[5]);
+    }
+    fscale[gid] = (uint8_t)c1;
+  }
+}
+
+}  // namespace resq

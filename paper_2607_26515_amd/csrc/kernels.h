@@ -34,18 +34,25 @@ void launch_quant_cols(int fmt, const void* x, bool in_f32, int64_t rows, int64_
 // Q(X), dX = X - Q(X), Q(dX), and S_2:4 / identity / none.  keep_mask and partials may be
 // null.  partials (double [m][d/B]) receives the exact per-scale-block sums of squares of
 // the dequantized Q(dX) (used by the block selection).  frag = true writes MFMA fragments
-// (pack.hip layout; codes -> fragment records, scales -> per-lane scale bytes) for the local
-// kinds instead of K-major codes + scales.
+// (pack.hip layout; codes -> fragment records, scales -> per-lane scale bytes) instead of
+// K-major codes + scales: for both Q(X) and Q(dX) with the local kinds; with kResidDense
+// Q(X) as fragments and Q(dX) K-major (qr_codes, qr_scales) for the selection that follows,
+// and `zero` (zero_words 32-bit words, may be null) cleared by the same launch.  keep_mask
+// is ignored when frag is set.
 void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
                      uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes, void* qr_scales,
-                     uint8_t* keep_mask, double* partials, hipStream_t s, bool frag = false);
+                     uint8_t* keep_mask, double* partials, hipStream_t s, bool frag = false,
+                     uint32_t* zero = nullptr, int zero_words = 0);
 
 // MFMA operand packing (pack.hip): K-major codes + scales -> fragment-major operands.
 enum PackMode { kPackMx = 0, kPackHiA = 1, kPackHiB = 2 };
 size_t frag_bytes(int mode, int64_t rows, int64_t K);
 size_t frag_scale_bytes(int64_t rows, int64_t K);
+// mask: 0 none; 1 kept channels, 2 kept 32 x 64 blocks (bit masks in gbits, as the channel
+// and block selections write them): pruned elements are packed as the +0 code.
 void launch_pack(int mode, const uint8_t* codes, const void* scales, int64_t rows, int64_t K,
-                 uint8_t* frag, uint8_t* fscale, hipStream_t s);
+                 uint8_t* frag, uint8_t* fscale, hipStream_t s, int mask = 0,
+                 const uint8_t* gbits = nullptr);
 
 // Global selections for the channel, block and unstructured 50% residual patterns.
 // They read the dense Q(dX) (codes + scales), choose the kept set, then zero the pruned
@@ -63,6 +70,14 @@ void carve_select_ws(void* base, int sparsity, int fmt, int64_t m, int64_t d, Se
 void launch_select(int fmt, int sparsity, int64_t m, int64_t d, uint8_t* qr_codes,
                    const void* qr_scales, const double* partials, uint8_t* keep_mask,
                    uint8_t* group_mask, const SelectWs& ws, hipStream_t s);
+// The same selections for the forward GEMM: S(Q(dX)) is written as fragment-major operand
+// records (PackMode pack_mode) to frag / fscale; the K-major codes are left unpruned and no
+// masks are written.  For the element-wise kind the histogram (select_hist_words() words at
+// ws.hist) must have been cleared beforehand (the residual pass does it).
+void launch_select_frag(int fmt, int sparsity, int64_t m, int64_t d, uint8_t* qr_codes,
+                        const void* qr_scales, const double* partials, const SelectWs& ws,
+                        int pack_mode, uint8_t* frag, uint8_t* fscale, hipStream_t s);
+int select_hist_words();
 
 // FP4 GEMM  Y[M][N] = sum_t A_t[M][K] B[N][K]^T  with A_t = Q(X) and optionally S(Q(dX)),
 // all operands fragment-major (pack.hip).  Operand A is one buffer holding the fragments and

@@ -159,7 +159,7 @@ __global__ __launch_bounds__(kThreads) void residual_kernel(
 // ---------------------------------------------------------------------------------------
 template <int FMT>
 __device__ __forceinline__ void quantize8(const float x[8], uint32_t code[8], float val[8],
-                                          uint32_t& scale_byte, int& c1, int b[2]) {
+                                          uint32_t& scale_byte, int& c1, int b[2], int& b2o) {
   float a = 0.f;
 #pragma unroll
   for (int i = 0; i < 8; ++i) a = fmaxf(a, fabsf(x[i]));
@@ -168,6 +168,7 @@ __device__ __forceinline__ void quantize8(const float x[8], uint32_t code[8], fl
     scale_byte = (uint32_t)(E + 127);
     c1 = 0;
     b[0] = b[1] = 0;
+    b2o = 0;
     const float sc = mx_scale_f32(E);
 #pragma unroll
     for (int i = 0; i < 8; i += 2) {
@@ -181,6 +182,7 @@ __device__ __forceinline__ void quantize8(const float x[8], uint32_t code[8], fl
     scale_byte = (uint32_t)c1;
     const float fit0 = hif4_half_fit(c1, 0), fit1 = hif4_half_fit(c1, 1);
     const int b2 = a <= fit0 ? 1 : 0;  // this lane's 8 elements are one level-2 group
+    b2o = b2;
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
       float a4 = 0.f;
@@ -239,12 +241,58 @@ __device__ __forceinline__ void store_record8(uint8_t* __restrict__ frag, uint8_
   if (s == 0) fsc[rec] = (uint8_t)scale_byte;
 }
 
+// K-major output of one thread's 8 codes (row `row`, elements 64kb + 32half + 8s .. +7) for
+// a global selection: the codes as one 32-bit word, the block's scale (MXFP4: the E8M0 byte
+// of the 32-element half; HiF4: the metadata word of the 64-block, assembled from the 8
+// lanes of the row, lane g = level-2 group g), and the exact per-scale-block sum of squares
+// of the dequantized values.  Every lane must call this (ballots, shuffles); `in` = the
+// elements lie inside the matrix.
+__device__ __forceinline__ uint32_t spread8(uint32_t x) {  // bit i -> bit 2i
+  x = (x | (x << 4)) & 0x0F0Fu;
+  x = (x | (x << 2)) & 0x3333u;
+  return (x | (x << 1)) & 0x5555u;
+}
+
+template <int FMT>
+__device__ __forceinline__ void store_kmajor8(uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
+                                              double* __restrict__ partials, bool in, int64_t row,
+                                              int64_t d, int64_t kb, int half, int s,
+                                              const uint32_t code[8], const float val[8],
+                                              uint32_t scale_byte, const int b[2], int b2) {
+  const int64_t col0 = kb * 64 + 32 * half + 8 * s;
+  uint32_t w = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) w |= code[i] << (4 * i);
+  if (in) *reinterpret_cast<uint32_t*>(codes + row * (d / 2) + col0 / 2) = w;
+  double sq = 0.0;  // exact: squares of a shared scale times small integers
+#pragma unroll
+  for (int i = 0; i < 8; ++i) sq += (double)val[i] * (double)val[i];
+  if constexpr (FMT == kMX) {
+    sq = group_sum<4>(sq);
+    if (in && s == 0) {
+      scales[row * (d / 32) + kb * 2 + half] = (uint8_t)scale_byte;
+      if (partials) partials[row * (d / 32) + kb * 2 + half] = sq;
+    }
+  } else {
+    const int base = __lane_id() & ~7;  // the row's 8 lanes
+    const uint32_t bits2 = (uint32_t)(__ballot(b2 != 0) >> base) & 0xFFu;
+    const uint32_t b3a = (uint32_t)(__ballot(b[0] != b2) >> base) & 0xFFu;
+    const uint32_t b3b = (uint32_t)(__ballot(b[1] != b2) >> base) & 0xFFu;
+    const uint32_t meta = scale_byte | (bits2 << 8) | ((spread8(b3a) | (spread8(b3b) << 1)) << 16);
+    sq = group_sum<8>(sq);
+    if (in && half == 0 && s == 0) {
+      reinterpret_cast<uint32_t*>(scales)[row * (d / 64) + kb] = meta;
+      if (partials) partials[row * (d / 64) + kb] = sq;
+    }
+  }
+}
+
 // Row tile t, K step kb of the fused residual pass (one workgroup of 256 threads).
 template <int FMT, int MODE, bool VEC>
 __device__ __forceinline__ void residual_frag_tile(
     const uint16_t* __restrict__ X, int64_t m, int64_t d, int64_t ldx, int64_t nkb,
     uint8_t* __restrict__ fx, uint8_t* __restrict__ fsx, uint8_t* __restrict__ fr,
-    uint8_t* __restrict__ fsr, int64_t t, int64_t kb) {
+    uint8_t* __restrict__ fsr, double* __restrict__ partials, int64_t t, int64_t kb) {
   const int64_t f = t * nkb + kb;  // fragment index
   const int tid = threadIdx.x;
   const int rr = tid >> 3, half = (tid >> 2) & 1, s = tid & 3;
@@ -272,13 +320,13 @@ __device__ __forceinline__ void residual_frag_tile(
   const int64_t rec = f * 64 + rr + 32 * half;
   uint32_t code[8], scale_byte;
   float val[8];
-  int c1, b[2];
-  quantize8<FMT>(x, code, val, scale_byte, c1, b);
+  int c1, b[2], b2;
+  quantize8<FMT>(x, code, val, scale_byte, c1, b, b2);
   store_record8<FMT>(fx, fsx, rec, s, code, scale_byte, c1, b);
   if constexpr (MODE != kResidNone) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) x[i] -= val[i];  // dX, exact in float32
-    quantize8<FMT>(x, code, val, scale_byte, c1, b);
+    quantize8<FMT>(x, code, val, scale_byte, c1, b, b2);
     if constexpr (MODE == kResid24) {
 #pragma unroll
       for (int g = 0; g < 2; ++g) {
@@ -289,19 +337,30 @@ __device__ __forceinline__ void residual_frag_tile(
           if (!((keep >> e) & 1u)) code[4 * g + e] = 0u;
       }
     }
-    store_record8<FMT>(fr, fsr, rec, s, code, scale_byte, c1, b);
+    if constexpr (MODE == kResidDense) {
+      store_kmajor8<FMT>(fr, fsr, partials, row < m && col0 < d, row, d, kb, half, s, code, val,
+                         scale_byte, b, b2);
+    } else {
+      store_record8<FMT>(fr, fsr, rec, s, code, scale_byte, c1, b);
+    }
   }
 }
 
-// grid: x = K step, y = row tiles (grid-stride)
+// grid: x = K step, y = row tiles (grid-stride).  kResidDense (a global selection follows):
+// fr / fsr receive the K-major Q(dX) codes and scales and `partials` its per-scale-block
+// sums of squares (may be null); workgroup (0, 0) also clears zero_words words at zero (may
+// be null), the histogram the element-wise selection accumulates into.
 template <int FMT, int MODE, bool VEC>
 __global__ __launch_bounds__(256) void residual_frag_kernel(
     const uint16_t* __restrict__ X, int64_t m, int64_t d, int64_t ldx, int64_t nkb,
     uint8_t* __restrict__ fx, uint8_t* __restrict__ fsx, uint8_t* __restrict__ fr,
-    uint8_t* __restrict__ fsr) {
+    uint8_t* __restrict__ fsr, double* __restrict__ partials, uint32_t* __restrict__ zero,
+    int zero_words) {
+  if (zero != nullptr && blockIdx.x == 0 && blockIdx.y == 0)
+    for (int i = threadIdx.x; i < zero_words; i += blockDim.x) zero[i] = 0u;
   const int64_t mtiles = (m + 31) / 32;
   for (int64_t t = blockIdx.y; t < mtiles; t += gridDim.y)
-    residual_frag_tile<FMT, MODE, VEC>(X, m, d, ldx, nkb, fx, fsx, fr, fsr, t, blockIdx.x);
+    residual_frag_tile<FMT, MODE, VEC>(X, m, d, ldx, nkb, fx, fsx, fr, fsr, partials, t, blockIdx.x);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -378,8 +437,8 @@ __device__ __forceinline__ void quant_cols_frag_tile(const uint16_t* __restrict_
     for (int e = 0; e < 8; ++e) v[e] = bf16_to_f32(tile[(32 * half + 8 * s + e) * kPitch + 32 * tt + rr]);
     uint32_t code[8], scale_byte;
     float val[8];
-    int c1, b[2];
-    quantize8<FMT>(v, code, val, scale_byte, c1, b);
+    int c1, b[2], b2;
+    quantize8<FMT>(v, code, val, scale_byte, c1, b, b2);
     const int64_t rec = (t * nkb + kb) * 64 + rr + 32 * half;
     if constexpr (PMODE == kPackHiB) store_record8_e3m2(frag, fsc, rec, s, code, scale_byte, b);
     else store_record8<FMT>(frag, fsc, rec, s, code, scale_byte, c1, b);
@@ -401,8 +460,8 @@ __device__ __forceinline__ void quant_cols_frag_tile(const uint16_t* __restrict_
       }
       uint32_t code[8], scale_byte;
       float val[8];
-      int c1, b[2];
-      quantize8<FMT>(v, code, val, scale_byte, c1, b);
+      int c1, b[2], b2;
+      quantize8<FMT>(v, code, val, scale_byte, c1, b, b2);
       store_record8<FMT>(rfrag, rfsc, (t * rkb + k) * 64 + rr + 32 * half, s, code, scale_byte, c1, b);
     }
   }
@@ -477,17 +536,19 @@ void launch_quant_cols(int fmt, const void* x, bool in_f32, int64_t rows, int64_
 
 void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
                      uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes, void* qr_scales,
-                     uint8_t* keep_mask, double* partials, hipStream_t s, bool frag) {
+                     uint8_t* keep_mask, double* partials, hipStream_t s, bool frag,
+                     uint32_t* zero, int zero_words) {
   if (m == 0 || d == 0) return;
   if (frag) {
     const int64_t nkb = (d + 63) / 64;
     const dim3 grid((unsigned)nkb, grid_rows((m + 31) / 32));
     const bool vec16 = ((uintptr_t)X % 16 == 0) && (ldx % 8 == 0);
-#define RESQ_RF(F, M, V) hipLaunchKernelGGL((residual_frag_kernel<F, M, V>), grid, dim3(256), 0, s, X, m, d, ldx, nkb, qx_codes, (uint8_t*)qx_scales, qr_codes, (uint8_t*)qr_scales)
+#define RESQ_RF(F, M, V) hipLaunchKernelGGL((residual_frag_kernel<F, M, V>), grid, dim3(256), 0, s, X, m, d, ldx, nkb, qx_codes, (uint8_t*)qx_scales, qr_codes, (uint8_t*)qr_scales, partials, zero, zero_words)
 #define RESQ_RF_MODE(F, V)                                        \
     switch (mode) {                                               \
       case kResidNone: RESQ_RF(F, kResidNone, V); break;          \
       case kResidIdentity: RESQ_RF(F, kResidIdentity, V); break;  \
+      case kResidDense: RESQ_RF(F, kResidDense, V); break;        \
       default: RESQ_RF(F, kResid24, V); break;                    \
     }
     if (fmt == kMX) { if (vec16) { RESQ_RF_MODE(kMX, true) } else { RESQ_RF_MODE(kMX, false) } }

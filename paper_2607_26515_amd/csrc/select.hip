@@ -12,7 +12,7 @@
 // and block keys; exponent then mantissa digits for the element keys), after which the keys
 // equal to it are ranked by index.  Pruned codes become the +0 code in place.
 #include "kernels.h"
-#include "device_fp4.h"
+#include "frag.h"
 
 namespace resq {
 namespace {
@@ -323,14 +323,6 @@ __global__ __launch_bounds__(kSelThreads) void select_top_kernel(const uint64_t*
   }
 }
 
-// Expand 8 keep bits into a nibble mask for one code word.
-__device__ __forceinline__ uint32_t nibble_mask(uint32_t kb) {
-  uint32_t m = 0;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) m |= ((kb >> e) & 1u) * (0xFu << (4 * e));
-  return m;
-}
-
 // Apply kept channels (KIND 0) or kept blocks (KIND 1): one thread per code word; grid x
 // covers the d/8 words of a row, y the rows (grid-stride).
 template <int KIND>
@@ -349,7 +341,7 @@ __global__ __launch_bounds__(kThreads) void apply_groups_kernel(uint32_t* __rest
       kb = ((gbits[bit >> 3] >> (bit & 7)) & 1u) ? 0xFFu : 0u;
     }
     const int64_t w = row * (d / 8) + c8;
-    codes[w] &= nibble_mask(kb);
+    codes[w] &= nibble_mask8(kb);
     if (keep_mask) keep_mask[w] = (uint8_t)kb;
   }
 }
@@ -472,12 +464,18 @@ __global__ __launch_bounds__(kThreads) void uties_kernel(const uint8_t* __restri
   if (threadIdx.x == 0) tie_counts[blockIdx.x] = total;
 }
 
-template <int FMT>
+// PMODE < 0: prune the codes in place (and write the keep mask).  PMODE >= 0: leave the codes
+// and write S(Q(dX)) as fragment-major MFMA records (pack.hip layout, PackMode PMODE) to
+// frag / fscale, including the zero records of rows past m (up to a multiple of 32) and of
+// the missing half K step when d % 64 == 32.
+template <int FMT, int PMODE>
 __global__ __launch_bounds__(kThreads) void uapply_kernel(uint8_t* __restrict__ codes,
                                                           const void* __restrict__ scales, int64_t m,
                                                           int64_t d, const uint32_t* __restrict__ hist,
                                                           const uint32_t* __restrict__ tie_counts,
-                                                          uint8_t* __restrict__ keep_mask) {
+                                                          uint8_t* __restrict__ keep_mask,
+                                                          uint8_t* __restrict__ frag,
+                                                          uint8_t* __restrict__ fscale) {
   __shared__ uint32_t lh[kUHist];
   __shared__ uint32_t ch[4];
   __shared__ uint32_t wsum[kThreads / 64];
@@ -509,12 +507,31 @@ __global__ __launch_bounds__(kThreads) void uapply_kernel(uint8_t* __restrict__ 
   }
   uint4* cw = reinterpret_cast<uint4*>(codes + 4 * w0);
   uint4 v = *cw;
-  v.x &= nibble_mask(kept & 0xFFu);
-  v.y &= nibble_mask((kept >> 8) & 0xFFu);
-  v.z &= nibble_mask((kept >> 16) & 0xFFu);
-  v.w &= nibble_mask(kept >> 24);
-  *cw = v;
-  if (keep_mask) *reinterpret_cast<uint32_t*>(keep_mask + w0) = kept;
+  v.x &= nibble_mask8(kept & 0xFFu);
+  v.y &= nibble_mask8((kept >> 8) & 0xFFu);
+  v.z &= nibble_mask8((kept >> 16) & 0xFFu);
+  v.w &= nibble_mask8(kept >> 24);
+  if constexpr (PMODE < 0) {
+    *cw = v;
+    if (keep_mask) *reinterpret_cast<uint32_t*>(keep_mask + w0) = kept;
+  } else {
+    // this thread's 32 elements are one lane record: row `row`, K elements j .. j+31
+    const uint32_t e0 = (uint32_t)(8 * w0), row = e0 / (uint32_t)d, j = e0 - row * (uint32_t)d;
+    const int64_t nkb = (d + 63) / 64, kb = j / 64;
+    const int half = (int)((j / 32) & 1u);
+    const uint32_t sc = scale_at<FMT>(scales, row, d, j);
+    const int64_t rec = ((int64_t)(row / 32) * nkb + kb) * 64 + (row & 31) + 32 * half;
+    store_frag_record<PMODE>(frag, fscale, rec, v, sc, half);
+    const uint4 z = make_uint4(0, 0, 0, 0);
+    if ((d & 63) == 32 && j + 32 == (uint32_t)d)  // the missing half K step: zero codes, scale 0
+      store_frag_record<PMODE>(frag, fscale, rec + 32, z, 0u, 1);
+    if (row + 1 == (uint32_t)m)  // rows past m inside the last row tile: zero records
+      for (uint32_t r = row + 1; r % 32 != 0; ++r) {
+        const int64_t pr = ((int64_t)(r / 32) * nkb + kb) * 64 + (r & 31);
+        store_frag_record<PMODE>(frag, fscale, pr + 32 * half, z, 0u, half);
+        if ((d & 63) == 32 && j + 32 == (uint32_t)d) store_frag_record<PMODE>(frag, fscale, pr + 32, z, 0u, 1);
+      }
+  }
 }
 
 int64_t unstructured_wgs(int64_t m, int64_t d) {
@@ -588,11 +605,46 @@ void launch_select(int fmt, int sparsity, int64_t m, int64_t d, uint8_t* qr_code
     hipLaunchKernelGGL((uhist_kernel<F, 1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, ws.hist);   \
     hipLaunchKernelGGL((uties_kernel<F>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d,                 \
                        (const uint32_t*)ws.hist, ws.tie_counts);                                                      \
-    hipLaunchKernelGGL((uapply_kernel<F>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d,                \
-                       (const uint32_t*)ws.hist, (const uint32_t*)ws.tie_counts, keep_mask);
+    hipLaunchKernelGGL((uapply_kernel<F, -1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d,            \
+                       (const uint32_t*)ws.hist, (const uint32_t*)ws.tie_counts, keep_mask, nullptr, nullptr);
     if (fmt == 0) { RESQ_U(0) } else { RESQ_U(1) }
 #undef RESQ_U
   }
 }
+
+void launch_select_frag(int fmt, int sparsity, int64_t m, int64_t d, uint8_t* qr_codes,
+                        const void* qr_scales, const double* partials, const SelectWs& ws,
+                        int pack_mode, uint8_t* frag, uint8_t* fscale, hipStream_t s) {
+  if (m == 0 || d == 0) return;
+  if (sparsity == 3 || sparsity == 4) {
+    const bool chan = sparsity == 3;
+    const int64_t n = chan ? d : n_blocks(m, d);
+    if (chan) {
+      const dim3 g((unsigned)((d + 63) / 64));
+      if (fmt == 0) hipLaunchKernelGGL((channel_keys_kernel<0>), g, dim3(kChanThreads), 0, s, qr_codes, qr_scales, m, d, ws.keys);
+      else hipLaunchKernelGGL((channel_keys_kernel<1>), g, dim3(kChanThreads), 0, s, qr_codes, qr_scales, m, d, ws.keys);
+    } else {
+      const dim3 g((unsigned)((n + kThreads - 1) / kThreads));
+      if (fmt == 0) hipLaunchKernelGGL((block_keys_kernel<0>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
+      else hipLaunchKernelGGL((block_keys_kernel<1>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
+    }
+    hipLaunchKernelGGL(select_top_kernel, dim3(1), dim3(kSelThreads), 0, s, (const uint64_t*)ws.keys, n, n / 2,
+                       ws.group_bits, (uint8_t*)nullptr);
+    launch_pack(pack_mode, qr_codes, qr_scales, m, d, frag, fscale, s, chan ? 1 : 2, ws.group_bits);
+  } else if (sparsity == 5) {
+    const unsigned nwg = (unsigned)unstructured_wgs(m, d);  // the histogram was cleared by the residual pass
+#define RESQ_UF(F, P)                                                                                      \
+    hipLaunchKernelGGL((uhist_kernel<F, 0>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, ws.hist);   \
+    hipLaunchKernelGGL((uhist_kernel<F, 1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, ws.hist);   \
+    hipLaunchKernelGGL((uties_kernel<F>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d,                 \
+                       (const uint32_t*)ws.hist, ws.tie_counts);                                                      \
+    hipLaunchKernelGGL((uapply_kernel<F, P>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d,             \
+                       (const uint32_t*)ws.hist, (const uint32_t*)ws.tie_counts, (uint8_t*)nullptr, frag, fscale);
+    if (fmt == 0) { RESQ_UF(0, kPackMx) } else { RESQ_UF(1, kPackHiA) }
+#undef RESQ_UF
+  }
+}
+
+int select_hist_words() { return kHistCopies * kUHist; }
 
 }  // namespace resq

@@ -133,3 +133,20 @@ def test_select_wide_range_channels(fmt, sp):
         x[1::2, col] = -(2.0 ** -28) * (1 + 3 * 2.0 ** -7)
     x[::7, 130] = 2.0 ** 20 * 1.015625  # a channel between the two ranges
     _check_select(fmt, sp, f32_to_bf16_bits(x))
+
+
+@pytest.mark.parametrize("sp", ["channel50", "unstructured50"])  # 32x64 blocks need d % 64 == 0
+@pytest.mark.parametrize("m,d,n", [(45, 96, 70), (33, 160, 64), (1, 32, 5)])
+def test_linear_fwd_global_mx_half_step(sp, m, d, n):
+    """MXFP4 with d % 64 == 32: the last K step's second half is outside the matrix, so the
+    selection must write zero operand records there (a stray scale byte would poison every
+    output); m % 32 != 0 leaves padding rows in the last row tile."""
+    import paper_2607_26515_amd as P
+    log(f"linear_fwd mxfp4 {sp} half step m={m} d={d} n={n}")
+    rx, rw = rng_tree(7 * m + d + n, 2)
+    xb, wb = activations(rx, m, d, 0.05, 50.0), weights(rw, n, d)
+    qc, qs = P.quantize(dev_bf16(wb), "mxfp4", axis=1)
+    y = host(P.linear_fwd(dev_bf16(xb), qc, qs, "mxfp4", sp))
+    o = Q.resq_forward("mxfp4", sp, bf16_bits_to_f32(xb), bf16_bits_to_f32(wb))
+    assert np.isfinite(y).all()
+    assert_close(y, o["y64"], f"Y mxfp4 {sp}")
