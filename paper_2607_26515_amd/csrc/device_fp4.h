@@ -78,8 +78,9 @@ __device__ __forceinline__ float mx_scale_f32(int E) {
 // The same quantization on gfx950's scaled conversions, two elements per instruction:
 // v_cvt_scalef32_pk_fp4_f32 with scale 2^E rounds x / 2^E to the nearest E2M1 magnitude,
 // ties to the even code, saturates at 6 and keeps the sign of a zero result, which is
-// mx_code's definition; v_cvt_scalef32_pk_f32_fp4 returns mx_value.  (A GPU test compares
-// both against the software forms on ties, saturation, signed zeros and subnormals.)
+// mx_code's definition; v_cvt_scalef32_pk_f32_fp4 returns mx_value.  (GPU tests compare the
+// resulting codes and scales with the oracle's on every E2M1 tie and threshold, saturation,
+// signed zeros and shared exponents from -127, where 2^E is subnormal, to 124.)
 // Codes of x0, x1: bits 0-3 and 4-7 of the result.
 __device__ __forceinline__ uint32_t mx_code2(float x0, float x1, float scale) {
   return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, x0, x1, scale, 0) & 0xFFu;
