@@ -69,19 +69,18 @@ __device__ __forceinline__ uint32_t pack_quad_codes(const uint32_t c[4]) {
 
 // S_2:4 on one group of four: keep the two largest magnitudes, lower index on ties.
 // Magnitude codes are monotone in |value| within a block (shared scale), so codes compare.
+// Key i = magnitude << 2 | (3 - i) is distinct per element and orders by magnitude, then by
+// lower index; the kept pair are the keys at or above the second largest.
 __device__ __forceinline__ uint32_t keep_2_of_4(const uint32_t c[4]) {
+  uint32_t k[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) k[i] = ((c[i] & 7u) << 2) | (uint32_t)(3 - i);
+  const uint32_t hi01 = max(k[0], k[1]), lo01 = min(k[0], k[1]);
+  const uint32_t hi23 = max(k[2], k[3]), lo23 = min(k[2], k[3]);
+  const uint32_t second = max(min(hi01, hi23), max(lo01, lo23));
   uint32_t keep = 0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    int rank = 0;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (j == i) continue;
-      const uint32_t kj = c[j] & 7, ki = c[i] & 7;
-      rank += (kj > ki) || (kj == ki && j < i);
-    }
-    keep |= (rank < 2 ? 1u : 0u) << i;
-  }
+  for (int i = 0; i < 4; ++i) keep |= (k[i] >= second ? 1u : 0u) << i;
   return keep;
 }
 
