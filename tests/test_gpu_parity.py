@@ -194,3 +194,20 @@ def test_linear_bwd(fmt, m, d, n):
     o = Q.resq_backward(fmt, bf16_bits_to_f32(gb), bf16_bits_to_f32(xb), bf16_bits_to_f32(wb))
     assert_close(host(dx), o["dx64"], "dX")
     assert_close(host(dw), o["dw64"], "dW")
+
+
+@pytest.mark.parametrize("sp", ["none", "2:4"])
+@pytest.mark.parametrize("fmt,m,d,n", [
+    ("mxfp4", 64, 320, 128),    # 5 K steps, two K groups: the last stage is half empty
+    ("mxfp4", 64, 8384, 96),    # 131 K steps, four K groups: three steps in the last stage
+    ("hif4", 64, 320, 128),     # 5 K steps, two K groups
+    ("hif4", 32, 8384, 64),     # K split in two (66 + 65 steps), two K groups each
+    ("hif4", 640, 320, 2048),   # more small tiles than CUs: two stages, two workgroups per CU
+])
+def test_linear_fwd_k_groups(fmt, sp, m, d, n):
+    """Decode-sized grids run K groups (several wave groups splitting each stage's K steps);
+    K lengths that leave the last stage partly empty, a K split with an odd half and the
+    two-stage plan must all match the oracle."""
+    log(f"linear_fwd k groups {fmt} {sp} m={m} d={d} n={n}")
+    y, o = _linear_case(fmt, sp, m, d, n, seed=m + 3 * d + n)
+    assert_close(y, o["y64"], f"Y {fmt} {sp}")
