@@ -51,18 +51,18 @@ def exec_mfma_flops(m, d, n, fmt, sp):
     return per_term if sp == "none" else 2 * per_term
 
 
-def step_bytes(m, d, n, fmt):
-    """Algorithmic HBM bytes of one linear: X (bf16) in, Q(W) in, Y (fp32) out."""
-    return 2 * m * d + BYTES_PER_ELEM[fmt] * n * d + 4 * m * n
+def step_bytes(m, d, n, fmt, y_bytes=4):
+    """Algorithmic HBM bytes of one linear: X (bf16) in, Q(W) in, Y (fp32 or bf16) out."""
+    return 2 * m * d + BYTES_PER_ELEM[fmt] * n * d + y_bytes * m * n
 
 
-def gemm_bytes(m, d, n, fmt, sp):
+def gemm_bytes(m, d, n, fmt, sp, y_bytes=4):
     """Algorithmic bytes of the GEMM launch: Q(W), Q(X) and S(Q(dX)) read once, Y written."""
     terms = 1 if sp == "none" else 2
-    return BYTES_PER_ELEM[fmt] * (n * d + terms * m * d) + 4 * m * n
+    return BYTES_PER_ELEM[fmt] * (n * d + terms * m * d) + y_bytes * m * n
 
 
-def gemm_traffic(workload, fmt, sp):
+def gemm_traffic(workload, fmt, sp, out="f32"):
     """HBM bytes per GEMM launch from the committed rocprofv3 counter summary, or None when
     the summary does not cover this workload or the GEMM source changed since it was taken."""
     import hashlib
@@ -73,7 +73,8 @@ def gemm_traffic(workload, fmt, sp):
         return None
     if rec.get("gemm_source_sha256") != hashlib.sha256(src).hexdigest():
         return None
-    entry = rec.get("entries", {}).get(f"{workload}/{fmt}/{sp}")
+    key = f"{workload}/{fmt}/{sp}" + ("" if out == "f32" else f"/{out}")
+    entry = rec.get("entries", {}).get(key)
     return None if entry is None else round(entry["bytes_per_launch"])
 
 
@@ -136,9 +137,10 @@ def cpu_baseline(wl, fmt, sp, n_sample, n_rows, min_seconds):
     }
 
 
-def setup_forward(P, torch, np, wl, fmt, sp, dev, sptr):
+def setup_forward(P, torch, np, wl, fmt, sp, dev, sptr, out="f32"):
     """Inputs resident in HBM (enough rotating copies to defeat the last-level cache) and a
-    step function running every linear of the workload through resq_linear_fwd_prepared."""
+    step function running every linear of the workload through resq_linear_fwd_prepared
+    (float32 Y) or resq_linear_fwd_prepared_bf16 (bf16 Y)."""
     from synth import workload_tensors
     f, s = P.FORMATS[fmt], P.SPARSITY[sp]
     per_copy = sum(P.resq_prepared_weights_size(f, l.n, l.d) + 2 * wl.m * l.d for l in wl.linears)
@@ -157,19 +159,20 @@ def setup_forward(P, torch, np, wl, fmt, sp, dev, sptr):
             wps.append(P.prepare_weights(qc, qs, fmt))
             del qc, qs
         del w0, x0
-        y = torch.empty((wl.m, lin.n), dtype=torch.float32, device=dev)
+        y = torch.empty((wl.m, lin.n), dtype=torch.float32 if out == "f32" else torch.int16,
+                        device=dev)
         lin_state.append(dict(lin=lin, xs=xs, wps=wps, y=y, xp=[int(t.data_ptr()) for t in xs],
                               wp=[int(t.data_ptr()) for t in wps]))
     torch.cuda.synchronize()
     lib = P.load()
+    entry = lib.resq_linear_fwd_prepared if out == "f32" else lib.resq_linear_fwd_prepared_bf16
 
     def run_linear(st, i):
         lin, c = st["lin"], i % copies
-        rc = lib.resq_linear_fwd_prepared(f, s, st["xp"][c], wl.m, lin.d, lin.d, st["wp"][c], lin.n,
-                                          int(st["y"].data_ptr()), lin.n, int(ws.data_ptr()),
-                                          ws_bytes, sptr)
+        rc = entry(f, s, st["xp"][c], wl.m, lin.d, lin.d, st["wp"][c], lin.n,
+                   int(st["y"].data_ptr()), lin.n, int(ws.data_ptr()), ws_bytes, sptr)
         if rc != 0:
-            raise P.ResqError(f"resq_linear_fwd_prepared: {P.resq_last_error()}", rc)
+            raise P.ResqError(f"{entry.__name__}: {P.resq_last_error()}", rc)
 
     return lin_state, run_linear, copies
 
@@ -213,6 +216,8 @@ def main() -> int:
     ap.add_argument("--workload", default="qwen3b_layer_m256")
     ap.add_argument("--format", default="hif4", choices=["hif4", "mxfp4"])
     ap.add_argument("--sparsity", default="2:4")
+    ap.add_argument("--out", default="f32", choices=["f32", "bf16"],
+                    help="forward output type: float32, or its bf16 rounding written by the GEMM")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-cols", type=int, default=1024)
     ap.add_argument("--cpu-sample-rows", type=int, default=512)
@@ -251,10 +256,13 @@ def main() -> int:
     wl = WORKLOADS[args.workload]
     fmt = args.format
     sp = "none" if wl.backward else args.sparsity
+    out_t = "f32" if wl.backward else args.out
+    y_bytes = 4 if out_t == "f32" else 2
     if wl.backward:
         lin_state, run_linear, copies = setup_backward(P, torch, np, wl, fmt, dev, sptr)
     else:
-        lin_state, run_linear, copies = setup_forward(P, torch, np, wl, fmt, sp, dev, sptr)
+        lin_state, run_linear, copies = setup_forward(P, torch, np, wl, fmt, sp, dev, sptr,
+                                                      args.out)
 
     def run_step(i):
         for st in lin_state:
@@ -302,8 +310,8 @@ def main() -> int:
     else:
         flops = sum(alg_flops(wl.m, l.d, l.n, sp) for l in lins)
         gexec = sum(exec_mfma_flops(wl.m, l.d, l.n, fmt, sp) for l in lins)
-        gbytes = sum(gemm_bytes(wl.m, l.d, l.n, fmt, sp) for l in lins)
-        sbytes = sum(step_bytes(wl.m, l.d, l.n, fmt) for l in lins)
+        gbytes = sum(gemm_bytes(wl.m, l.d, l.n, fmt, sp, y_bytes) for l in lins)
+        sbytes = sum(step_bytes(wl.m, l.d, l.n, fmt, y_bytes) for l in lins)
         n_launch = len(lins)
     value = flops * args.steps / dt / 1e12
     g_launch, g_ms = prof["gemm"]
@@ -318,7 +326,7 @@ def main() -> int:
         "peak": FP4_PEAK_TFLOPS if mfma_bound else HBM_PEAK_GBS,
         "unit": "TFLOP/s" if mfma_bound else "GB/s",
         "frac": round(mfma_tflops / FP4_PEAK_TFLOPS if mfma_bound else hbm_gbs / HBM_PEAK_GBS, 4),
-        "traffic": gemm_traffic(wl.name, fmt, sp),
+        "traffic": gemm_traffic(wl.name, fmt, sp, out_t),
         "kernel": f"gemm_kernel ({n_launch} launches per step)",
         "alg_bytes_per_launch": round(gbytes / n_launch),
         "alg_flops_per_launch": round(gexec / n_launch),
@@ -346,6 +354,7 @@ def main() -> int:
             "format": fmt,
             "sparsity": sp,
             "pass": "backward (dX, dW)" if wl.backward else "forward",
+            "output": "float32" if out_t == "f32" else "bf16",
             "m": wl.m,
             "linears": {l.name: [l.d, l.n] for l in lins},
             "copies_rotated": copies,

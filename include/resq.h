@@ -163,6 +163,19 @@ int resq_linear_fwd_prepared(int format, int sparsity, const uint16_t* X, int64_
                              void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * resq_linear_fwd_prepared_bf16 - resq_linear_fwd_prepared with a bf16 output: Y is m x n
+ * bf16 (bit patterns, row stride ldy >= n), each element the float32 result of Eq. 4 (as
+ * resq_linear_fwd_prepared computes it) rounded to the nearest bf16, ties to even.  Halves
+ * the output bytes, which dominate the decode shapes' HBM traffic after Q(W).  Arguments,
+ * workspace (resq_workspace_size(RESQ_OP_LINEAR_FWD_PREPARED, ...)) and errors are those of
+ * resq_linear_fwd_prepared.
+ */
+int resq_linear_fwd_prepared_bf16(int format, int sparsity, const uint16_t* X, int64_t m,
+                                  int64_t d, int64_t ldx, const void* wprep, int64_t n,
+                                  uint16_t* Y, int64_t ldy, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+
+/*
  * resq_linear_bwd - the FP4 training-policy backward GEMMs of the linear Y = X W^T:
  *     dX = Q_n(dY) Q_n(W)          (m x d, contraction over n)
  *     dW = Q_m(dY)^T Q_m(X)        (n x d, contraction over m)

@@ -23,6 +23,8 @@ Readings of points the paper leaves open (also listed in the design notes):
   T1  backward: dY, W and X are quantized along the contraction axis of each backward GEMM
       (dX = Q_n(dY) Q_n(W), dW = Q_m(dY)^T Q_m(X)), no residual (ResQ is rollout-only).
   Y1  Y, dX and dW are float32: the exact float64 result rounded once.
+  Y2  the optional bf16 output is that float32 result rounded again, to the nearest bf16
+      (ties to even): the rounding of the float32 result, not of the float64 one.
 """
 from __future__ import annotations
 
@@ -180,6 +182,17 @@ def resq_forward(fmt: str, sparsity: str, x: np.ndarray, w: np.ndarray) -> dict:
     out.update(qw_codes=qw_codes, qw_scales=qw_scales, what=what, y=y.astype(np.float32),
                y64=y)
     return out
+
+
+def round_to_bf16(y32: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns of finite float32 values, round to nearest, ties to even (reading Y2).
+
+    A bf16 keeps the sign, the 8 exponent bits and the top 7 fraction bits of a float32; the
+    16 dropped bits are compared with half of the kept part's last place."""
+    u = np.asarray(y32, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    kept, dropped = u >> 16, u & 0xFFFF
+    up = (dropped > 0x8000) | ((dropped == 0x8000) & ((kept & 1) == 1))
+    return (kept + up).astype(np.uint16)
 
 
 # ----------------------------------------------------------------------------------------

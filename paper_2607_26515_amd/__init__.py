@@ -24,6 +24,7 @@ from .resq import (  # noqa: F401
     resq_linear_bwd,
     resq_linear_fwd,
     resq_linear_fwd_prepared,
+    resq_linear_fwd_prepared_bf16,
     resq_prepare_weights,
     resq_prepared_weights_size,
     resq_profile_enable,

@@ -91,7 +91,8 @@ int b_pack_mode(int fmt) { return fmt == RESQ_MXFP4 ? resq::kPackMx : resq::kPac
 // offsets outside the buffers.
 resq::GemmOperands gemm_operands(int fmt, int64_t M, int64_t N, int64_t K, int n_terms,
                                  const uint8_t* const a_frag[2], const uint8_t* const a_sc[2],
-                                 const uint8_t* b_frag, const uint8_t* b_sc, float* Y, int64_t ldy) {
+                                 const uint8_t* b_frag, const uint8_t* b_sc, void* Y, int64_t ldy,
+                                 bool out_bf16 = false) {
   resq::GemmOperands op{};
   op.fmt = fmt;
   op.M = M; op.N = N; op.K = K;
@@ -108,7 +109,7 @@ resq::GemmOperands gemm_operands(int fmt, int64_t M, int64_t N, int64_t K, int n
   op.b_frag_off = 0;
   op.b_sc_off = (size_t)(b_sc - b_frag);
   op.b_bytes = std::max(bf, op.b_sc_off + bs);
-  op.Y = Y; op.ldy = ldy;
+  op.Y = Y; op.ldy = ldy; op.out_bf16 = out_bf16;
   return op;
 }
 
@@ -332,7 +333,7 @@ int resq_prepare_weights(int format, const uint8_t* qw_codes, const void* qw_sca
 namespace {
 
 int linear_fwd_core(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
-                    int64_t ldx, const void* wprep, int64_t n, float* Y, int64_t ldy,
+                    int64_t ldx, const void* wprep, int64_t n, void* Y, int64_t ldy, bool out_bf16,
                     const ActWs& w, hipStream_t s) {
   if (global_kind(sparsity)) {
     // the residual pass writes Q(X) as MFMA fragments and the dense Q(dX) K-major (the
@@ -358,7 +359,7 @@ int linear_fwd_core(int format, int sparsity, const uint16_t* X, int64_t m, int6
   const uint8_t *bf, *bsc;
   carve_prepared(wprep, format, n, d, &bf, &bsc);
   resq::GemmOperands op = gemm_operands(format, m, n, d, sparsity == RESQ_S_NONE ? 1 : 2, af, asc,
-                                        bf, bsc, Y, ldy);
+                                        bf, bsc, Y, ldy, out_bf16);
   op.partial = w.gemm_partial;
   {
     resq::ProfScope prof_(resq::kProfGemm, s);
@@ -368,7 +369,7 @@ int linear_fwd_core(int format, int sparsity, const uint16_t* X, int64_t m, int6
 }
 
 int check_fwd_args(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
-                   int64_t ldx, int64_t n, float* Y, int64_t ldy) {
+                   int64_t ldx, int64_t n, const void* Y, int64_t ldy) {
   int rc = check_activation_args(format, sparsity, X, m, d, ldx);
   if (rc != RESQ_OK) return rc;
   if (n < 0) return fail(RESQ_ERR_ARG, "negative n");
@@ -380,11 +381,9 @@ int check_fwd_args(int format, int sparsity, const uint16_t* X, int64_t m, int64
   return ok();
 }
 
-}  // namespace
-
-int resq_linear_fwd_prepared(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
-                             int64_t ldx, const void* wprep, int64_t n, float* Y, int64_t ldy,
-                             void* workspace, size_t workspace_bytes, void* stream) {
+int linear_fwd_prepared(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
+                        int64_t ldx, const void* wprep, int64_t n, void* Y, int64_t ldy, bool out_bf16,
+                        void* workspace, size_t workspace_bytes, void* stream) {
   int rc = check_fwd_args(format, sparsity, X, m, d, ldx, n, Y, ldy);
   if (rc != RESQ_OK) return rc;
   if (m == 0 || n == 0) return ok();
@@ -394,7 +393,25 @@ int resq_linear_fwd_prepared(int format, int sparsity, const uint16_t* X, int64_
   const size_t need = carve_fwd(workspace, format, sparsity, m, d, n, &w);
   rc = check_ws(workspace, workspace_bytes, need);
   if (rc != RESQ_OK) return rc;
-  return linear_fwd_core(format, sparsity, X, m, d, ldx, wprep, n, Y, ldy, w, (hipStream_t)stream);
+  return linear_fwd_core(format, sparsity, X, m, d, ldx, wprep, n, Y, ldy, out_bf16, w,
+                         (hipStream_t)stream);
+}
+
+}  // namespace
+
+int resq_linear_fwd_prepared(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
+                             int64_t ldx, const void* wprep, int64_t n, float* Y, int64_t ldy,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  return linear_fwd_prepared(format, sparsity, X, m, d, ldx, wprep, n, Y, ldy, false, workspace,
+                             workspace_bytes, stream);
+}
+
+int resq_linear_fwd_prepared_bf16(int format, int sparsity, const uint16_t* X, int64_t m,
+                                  int64_t d, int64_t ldx, const void* wprep, int64_t n,
+                                  uint16_t* Y, int64_t ldy, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  return linear_fwd_prepared(format, sparsity, X, m, d, ldx, wprep, n, Y, ldy, true, workspace,
+                             workspace_bytes, stream);
 }
 
 int resq_linear_fwd(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
@@ -420,7 +437,7 @@ int resq_linear_fwd(int format, int sparsity, const uint16_t* X, int64_t m, int6
     resq::ProfScope prof_(resq::kProfPack, s);
     resq::launch_pack(b_pack_mode(format), qw_codes, qw_scales, n, d, (uint8_t*)frag, (uint8_t*)fsc, s);
   }
-  return linear_fwd_core(format, sparsity, X, m, d, ldx, wprep, n, Y, ldy, w, s);
+  return linear_fwd_core(format, sparsity, X, m, d, ldx, wprep, n, Y, ldy, false, w, s);
 }
 
 int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uint16_t* W,

@@ -63,8 +63,9 @@ struct GemmParams {
   const uint8_t* b;
   uint32_t a_bytes, b_bytes;
   uint32_t a_frag_off[2], a_sc_off[2], b_frag_off, b_sc_off;
-  float* Y;
+  void* Y;        // float32, or bf16 bits when out_bf16
   int64_t ldy;
+  int out_bf16;   // store Y as bf16 (round to nearest, ties to even) instead of float32
   // grid bookkeeping (32-bit: the workgroup count is far below 2^31)
   uint32_t grid_m, grid_n, per_xcd, n_wg;
   // split-K: ksplit workgroups per tile, each over kper K steps, each writing its partial
@@ -87,6 +88,17 @@ __device__ __forceinline__ void tile_coords(uint32_t tile, uint32_t grid_m, uint
   const uint32_t in = tile - first * grid_n;
   wg_m = first + in % rows;
   wg_n = in / rows;
+}
+
+// float32 -> bf16 bits, round to nearest, ties to even (finite inputs).
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+__device__ __forceinline__ void store_y(void* Y, int64_t idx, float v, int out_bf16) {
+  if (out_bf16) reinterpret_cast<uint16_t*>(Y)[idx] = f32_to_bf16_rne(v);
+  else reinterpret_cast<float*>(Y)[idx] = v;
 }
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
@@ -531,7 +543,7 @@ void gemm_kernel(GemmParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int64_t row = ((int64_t)T0 + wm * TM + i) * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        if (row < p.M && col < p.N) p.Y[row * p.ldy + col] = acc[i][j][r];
+        if (row < p.M && col < p.N) store_y(p.Y, row * p.ldy + col, acc[i][j][r], p.out_bf16);
       }
     }
 }
@@ -542,8 +554,8 @@ void gemm_kernel(GemmParams p) {
 template <int WM, int WN, int TM, int TN>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ partial,
                                                             int ksplit, uint32_t grid_m, uint32_t grid_n,
-                                                            int64_t M, int64_t N, float* __restrict__ Y,
-                                                            int64_t ldy) {
+                                                            int64_t M, int64_t N, void* __restrict__ Y,
+                                                            int64_t ldy, int out_bf16) {
   constexpr int PARTS = WM * WN * TM * TN, TE = 1024 * PARTS;
   const uint32_t tile = blockIdx.x / PARTS;
   const int part = (int)(blockIdx.x % PARTS);
@@ -560,7 +572,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
     for (int k = 1; k < ksplit; ++k) v += src[(size_t)k * TE + e];
     const int64_t row = ((int64_t)wg_m * WM * TM + wm * TM + i) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
     const int64_t col = ((int64_t)wg_n * WN * TN + wn * TN + j) * 32 + (lane & 31);
-    if (row < M && col < N) Y[row * ldy + col] = v;
+    if (row < M && col < N) store_y(Y, row * ldy + col, v, out_bf16);
   }
 }
 
@@ -580,7 +592,8 @@ void launch_cfg(GemmParams p, int n_terms, hipStream_t s) {
     hipLaunchKernelGGL((gemm_kernel<FMT, WM, WN, TM, TN, 1, NS, KG>), grid, block, G1::lds_bytes(), s, p);
   if (p.ksplit > 1)
     hipLaunchKernelGGL((splitk_reduce_kernel<WM, WN, TM, TN>), dim3(p.grid_m * p.grid_n * WM * WN * TM * TN),
-                       dim3(256), 0, s, (const float*)p.partial, (int)p.ksplit, p.grid_m, p.grid_n, p.M, p.N, p.Y, p.ldy);
+                       dim3(256), 0, s, (const float*)p.partial, (int)p.ksplit, p.grid_m, p.grid_n, p.M, p.N, p.Y, p.ldy,
+                       p.out_bf16);
 }
 
 // Tile choice (measured on MI355X): a CU holds one or two workgroups (LDS- and
@@ -709,7 +722,7 @@ bool launch_gemm(const GemmOperands& op, hipStream_t s) {
     p.a_sc_off[t] = (uint32_t)op.a_sc_off[u];
   }
   p.b_frag_off = (uint32_t)op.b_frag_off; p.b_sc_off = (uint32_t)op.b_sc_off;
-  p.Y = op.Y; p.ldy = op.ldy;
+  p.Y = op.Y; p.ldy = op.ldy; p.out_bf16 = op.out_bf16 ? 1 : 0;
   if (op.fmt == 0) launch_fmt<0>(p, pl.cfg, pl.kg, pl.ns, op.n_terms, s);
   else launch_fmt<1>(p, pl.cfg, pl.kg, pl.ns, op.n_terms, s);
   return true;

@@ -93,8 +93,9 @@ struct GemmOperands {
   const uint8_t* b;
   size_t b_bytes;
   size_t b_frag_off, b_sc_off;
-  float* Y;
+  void* Y;                   // float32, or bf16 bits when out_bf16
   int64_t ldy;
+  bool out_bf16;             // Y rounded to bf16 (nearest, ties to even) from float32
   // optional split-K scratch of gemm_split_scratch bytes (null: no K split)
   float* partial;
 };

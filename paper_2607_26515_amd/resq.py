@@ -35,7 +35,7 @@ OP_RESIDUAL_SPARSIFY, OP_LINEAR_FWD, OP_LINEAR_BWD, OP_LINEAR_FWD_PREPARED = 0, 
 EXPORTED = ("resq_quantize", "resq_residual_sparsify", "resq_linear_fwd", "resq_linear_bwd",
             "resq_workspace_size", "resq_last_error", "resq_version", "resq_profile_enable",
             "resq_profile_reset", "resq_profile_read", "resq_prepared_weights_size",
-            "resq_prepare_weights", "resq_linear_fwd_prepared")
+            "resq_prepare_weights", "resq_linear_fwd_prepared", "resq_linear_fwd_prepared_bf16")
 
 
 class ResqError(RuntimeError):
@@ -68,6 +68,8 @@ def load() -> ctypes.CDLL:
     lib.resq_prepare_weights.restype = i32
     lib.resq_linear_fwd_prepared.argtypes = [i32, i32, vp, i64, i64, i64, vp, i64, vp, i64, vp, sz, vp]
     lib.resq_linear_fwd_prepared.restype = i32
+    lib.resq_linear_fwd_prepared_bf16.argtypes = [i32, i32, vp, i64, i64, i64, vp, i64, vp, i64, vp, sz, vp]
+    lib.resq_linear_fwd_prepared_bf16.restype = i32
     for f in ("resq_quantize", "resq_residual_sparsify", "resq_linear_fwd", "resq_linear_bwd"):
         getattr(lib, f).restype = i32
     lib.resq_workspace_size.restype = sz
@@ -119,6 +121,12 @@ def resq_linear_fwd_prepared(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy, work
                              workspace_bytes, stream=0) -> int:
     return load().resq_linear_fwd_prepared(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy,
                                            workspace, workspace_bytes, stream)
+
+
+def resq_linear_fwd_prepared_bf16(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy, workspace,
+                                  workspace_bytes, stream=0) -> int:
+    return load().resq_linear_fwd_prepared_bf16(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy,
+                                                workspace, workspace_bytes, stream)
 
 
 def resq_workspace_size(op, fmt, sparsity, m, d, n) -> int:
@@ -271,19 +279,24 @@ def prepare_weights(qw_codes, qw_scales, fmt, stream=None):
     return wprep
 
 
-def linear_fwd_prepared(x, wprep, n, fmt, sparsity, y=None, ws=None, stream=None):
-    """Y = Q(X) Q(W)^T + S(Q(X - Q(X))) Q(W)^T with Q(W) in prepared form (float32)."""
+def linear_fwd_prepared(x, wprep, n, fmt, sparsity, y=None, ws=None, stream=None, out="f32"):
+    """Y = Q(X) Q(W)^T + S(Q(X - Q(X))) Q(W)^T with Q(W) in prepared form: float32, or with
+    out="bf16" the bf16 rounding of the float32 result (returned as an int16 tensor of bf16
+    bit patterns)."""
     import torch
     m, d = x.shape
     f, sp = _fmt(fmt), _sp(sparsity)
+    if out not in ("f32", "bf16"):
+        raise ValueError(f"out must be 'f32' or 'bf16', not {out!r}")
     if y is None:
-        y = torch.empty((m, n), dtype=torch.float32, device=x.device)
+        y = torch.empty((m, n), dtype=torch.float32 if out == "f32" else torch.int16, device=x.device)
     if ws is None:
         ws = workspace(OP_LINEAR_FWD_PREPARED, f, sp, m, d, n, x.device)
     buf, nb = ws
-    rc = resq_linear_fwd_prepared(f, sp, _p(x), m, d, x.stride(0), _p(wprep), n, _p(y), y.stride(0),
-                                  _p(buf), nb, _stream(stream))
-    _check(rc, "resq_linear_fwd_prepared")
+    call = resq_linear_fwd_prepared if out == "f32" else resq_linear_fwd_prepared_bf16
+    rc = call(f, sp, _p(x), m, d, x.stride(0), _p(wprep), n, _p(y), y.stride(0), _p(buf), nb,
+              _stream(stream))
+    _check(rc, call.__name__)
     return y
 
 

@@ -211,3 +211,36 @@ def test_linear_fwd_k_groups(fmt, sp, m, d, n):
     log(f"linear_fwd k groups {fmt} {sp} m={m} d={d} n={n}")
     y, o = _linear_case(fmt, sp, m, d, n, seed=m + 3 * d + n)
     assert_close(y, o["y64"], f"Y {fmt} {sp}")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("sp", ["none", "2:4", "unstructured50"])
+@pytest.mark.parametrize("m,d,n", [(37, 512, 100), (256, 2048, 2560), (32, 8384, 64),
+                                   (1024, 2048, 640)])
+def test_linear_fwd_prepared_bf16(fmt, sp, m, d, n):
+    """bf16 output: the float32 result rounded to bf16 (nearest, ties to even) by the GEMM's
+    epilogue, also on the split-K path (m=32, d=8384)."""
+    import torch
+    import paper_2607_26515_amd as P
+    log(f"linear_fwd_prepared bf16 {fmt} {sp} m={m} d={d} n={n}")
+    rx, rw = rng_tree(m * 5 + n + d, 2)
+    xb, wb = activations(rx, m, d, 0.01, 50.0), weights(rw, n, d)
+    qc, qs = P.quantize(dev_bf16(wb), fmt, axis=1)
+    x = dev_bf16(xb)
+    wprep = P.prepare_weights(qc, qs, fmt)
+    y32 = P.linear_fwd_prepared(x, wprep, n, fmt, sp)
+    yb = P.linear_fwd_prepared(x, wprep, n, fmt, sp, out="bf16")
+    assert yb.dtype == torch.int16 and yb.shape == (m, n)
+    got = host(yb).view(np.uint16)
+    # the epilogue's rounding is the bf16 rounding of the float32 result, bit for bit
+    want_from_f32 = host(y32.cpu().to(torch.bfloat16).view(torch.int16)).view(np.uint16)
+    assert np.array_equal(got, want_from_f32)
+    o = Q.resq_forward(fmt, sp, bf16_bits_to_f32(xb), bf16_bits_to_f32(wb))
+    assert_close(host(y32), o["y64"], "Y float32")
+    # bf16 keeps 8 significant bits: unit roundoff 2^-9, plus the float32 path's error
+    assert_close(bf16_bits_to_f32(got), o["y64"], "Y bf16", tol=2.0**-8)
+    ob = Q.round_to_bf16(o["y"])
+    diff = np.abs(got.astype(np.int32) - ob.astype(np.int32))
+    big = np.abs(o["y64"]) > 2.0**-4 * np.sqrt(np.mean(o["y64"] ** 2))
+    assert diff[big].max(initial=0) <= 1, "bf16 outputs more than one step from the oracle's"
+    assert np.mean(diff == 0) > 0.99

@@ -275,3 +275,50 @@ def test_overhead_model_matches_golden():
     assert Q.effective_cost(m, d, n, "none") == g["effective_dense_fp4_gemm"] * mdn
     assert Q.speedup_vs_fp16("identity") == g["speedup_resq_dense_vs_fp16"]
     assert Q.speedup_vs_fp16("2:4") == pytest.approx(g["speedup_resq_2_4_vs_fp16"], abs=1e-4)
+
+
+# ----------------------------------------------------------------------------------------
+# Optional bf16 output: the float32 result rounded to bf16, nearest, ties to even
+# ----------------------------------------------------------------------------------------
+def _bf16_nearest_exact(v32: np.float32) -> int:
+    """Nearest bf16 by exact rational distance to the two bf16 values around v (ties: even)."""
+    from fractions import Fraction
+    u = int(np.float32(v32).view(np.uint32))
+    lo = u & 0xFFFF0000
+    cands = [lo >> 16, (lo >> 16) + 1]
+    vals = [Fraction(float(np.uint32(c << 16).view(np.float32))) for c in cands]
+    x = Fraction(float(v32))
+    d = [abs(x - c) for c in vals]
+    if d[0] != d[1]:
+        return cands[0] if d[0] < d[1] else cands[1]
+    return cands[0] if cands[0] % 2 == 0 else cands[1]
+
+
+def test_round_to_bf16_special_values():
+    one = 0x3F80
+    cases = [(1.0, one), (1.0 + 2.0**-8, one), (1.0 + 3 * 2.0**-8, 0x3F82),
+             (1.0 + 2.0**-8 + 2.0**-20, 0x3F81), (-(1.0 + 3 * 2.0**-8), 0xBF82),
+             (0.0, 0), (-0.0, 0x8000), (2.0**-149, 0), (1.5 * 2.0**-133, 0x0002), (3 * 2.0**-133, 0x0003)]
+    x = np.array([c[0] for c in cases], dtype=np.float32)
+    got = Q.round_to_bf16(x)
+    assert [int(g) for g in got] == [c[1] for c in cases]
+    # values that are already bf16 are kept bit for bit
+    b = R.finite_bf16_as_f32_bits()
+    assert np.array_equal(Q.round_to_bf16(b.view(np.float32)), (b >> 16).astype(np.uint16))
+
+
+def test_round_to_bf16_exact_distance_and_torch():
+    import torch
+    rng = np.random.default_rng(11)
+    u = rng.integers(0, 0x7F7F0000, size=4000, dtype=np.uint64).astype(np.uint32)
+    # half of them forced onto a tie or next to it
+    u[:1000] = (u[:1000] & 0xFFFF0000) | 0x8000
+    u[1000:1500] = (u[1000:1500] & 0xFFFF0000) | 0x7FFF
+    u[1500:2000] = (u[1500:2000] & 0xFFFF0000) | 0x8001
+    u[2000:3000] |= 0x80000000
+    v = u.view(np.float32)
+    got = Q.round_to_bf16(v)
+    for k in range(0, len(v), 7):
+        assert int(got[k]) == _bf16_nearest_exact(v[k]), hex(int(u[k]))
+    t = torch.from_numpy(v.copy()).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(got, t)
