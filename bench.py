@@ -35,10 +35,21 @@ LLC_BYTES = 256 << 20          # MI355X last-level (Infinity) cache
 BYTES_PER_ELEM = {"hif4": 36 / 64, "mxfp4": 17 / 32}  # codes + block scales
 
 
+def kept_fraction(sp):
+    """Nominal fraction of the residual a sparsity keeps: k/g for "k:g", p/100 for the
+    "channel<p>", "block32x64_<p>" and "unstructured<p>" levels."""
+    if sp in ("none", "identity"):
+        return 0.0 if sp == "none" else 1.0
+    if ":" in sp:
+        k, g = (int(v) for v in sp.split(":"))
+        return k / g
+    return int(sp.replace("block32x64_", "").replace("channel", "").replace("unstructured", "")) / 100
+
+
 def alg_flops(m, d, n, sp):
-    """Sec. 5.4: 2mdn for the main GEMM; a 50% residual adds mdn, the dense one 2mdn."""
-    extra = {"none": 0, "identity": 2 * m * d * n}.get(sp, m * d * n)
-    return 2 * m * d * n + extra
+    """Sec. 5.4: 2mdn for the main GEMM; a 50% residual adds mdn, the dense one 2mdn (other
+    levels: their kept fraction of 2mdn)."""
+    return 2 * m * d * n + round(2 * m * d * n * kept_fraction(sp))
 
 
 def exec_mfma_flops(m, d, n, fmt, sp):
@@ -142,7 +153,7 @@ def setup_forward(P, torch, np, wl, fmt, sp, dev, sptr, out="f32"):
     step function running every linear of the workload through resq_linear_fwd_prepared
     (float32 Y) or resq_linear_fwd_prepared_bf16 (bf16 Y)."""
     from synth import workload_tensors
-    f, s = P.FORMATS[fmt], P.SPARSITY[sp]
+    f, s = P.FORMATS[fmt], P.sparsity_code(sp)
     per_copy = sum(P.resq_prepared_weights_size(f, l.n, l.d) + 2 * wl.m * l.d for l in wl.linears)
     copies = int(min(64, max(2, -(-2 * LLC_BYTES // int(per_copy)) + 1)))
     ws_bytes = max(P.resq_workspace_size(3, f, s, wl.m, l.d, l.n) for l in wl.linears)

@@ -67,6 +67,26 @@ typedef enum {
   RESQ_S_UNSTRUCT50 = 5     /* keep the floor(m*d/2) largest |values| of the tensor */
 } resq_sparsity;
 
+/*
+ * Other levels and N:M patterns of the same sparsity functions.  Sec. 4.3 defines the
+ * semi-structured pattern for any M:N and the channel and block patterns for any kept
+ * fraction alpha; the paper evaluates 50% only and leaves other levels open (Sec. 7).  These
+ * codes are accepted wherever a sparsity argument is:
+ *   RESQ_S_NM(k, g)       keep the k largest |values| of every g consecutive elements along d;
+ *                         g = 4 or 8, 1 <= k < g; d must be a multiple of g.
+ *                         RESQ_S_NM(2, 4) computes exactly what RESQ_S_2_4 does.
+ *   RESQ_S_CHANNEL(p)     keep the floor(d * p / 100) channels of largest L2 norm
+ *   RESQ_S_BLOCK32X64(p)  keep floor(nblocks * p / 100) of the ceil(m/32) * (d/64) blocks
+ *   RESQ_S_UNSTRUCT(p)    keep the floor(m * d * p / 100) largest |values|
+ * with 1 <= p <= 99 (p = 50 is the matching RESQ_S_*50 kind).  Ranking, ties and limits are
+ * those of the 50% kinds; a count that rounds down to 0 keeps nothing.  Any other value is
+ * rejected with RESQ_ERR_ARG.
+ */
+#define RESQ_S_NM(k, g) (0x100 | ((k) << 4) | (g))
+#define RESQ_S_CHANNEL(p) (0x200 | (p))
+#define RESQ_S_BLOCK32X64(p) (0x300 | (p))
+#define RESQ_S_UNSTRUCT(p) (0x400 | (p))
+
 typedef enum {
   RESQ_OK = 0,
   RESQ_ERR_ARG = -1,         /* NULL pointer, bad enum, negative size, ld too small */
@@ -109,21 +129,21 @@ int resq_quantize(int format, const void* x, int in_dtype, int64_t rows, int64_t
  * block scales, and S(Q(dX)) (Sec. 4.3), the activation side of Eq. 4.
  *
  * X         : m x d bf16, row stride ldx; d must be a multiple of 64 for HiF4, 32 for
- *             MXFP4, and of 4 for S_2:4.
+ *             MXFP4, of 4 for S_2:4 (of g for RESQ_S_NM(k, g)) and of 64 for the block kinds.
  * qx_codes, qx_scales : output Q(X), layout [m][d] K-major.
  * qr_codes, qr_scales : output S(Q(dX)): pruned elements hold the +0 code, scales are those
  *             of Q(dX).  May be NULL when sparsity == RESQ_S_NONE.
  * keep_mask : output, uint8 [m][d/8], 1 = element kept by S (NULL to skip).
- * group_mask: output, kept channels (uint8 [d/8]) for RESQ_S_CHANNEL50, kept blocks
- *             (uint8 [ceil(ceil(m/32) * (d/64) / 8)], blocks row-major) for
- *             RESQ_S_BLOCK32X64_50; ignored otherwise (NULL allowed).
+ * group_mask: output, kept channels (uint8 [d/8]) for the channel kinds, kept blocks
+ *             (uint8 [ceil(ceil(m/32) * (d/64) / 8)], blocks row-major) for the
+ *             32 x 64 block kinds; ignored otherwise (NULL allowed).
  * Ranking (channel, block, unstructured): by sum of squares of the dequantized Q(dX) values
  * (|value| for unstructured) in float64, ties to the lowest index; a channel's sum runs over
  * rows 0..m-1 in order; a block's over its rows in order, each row adding its per-scale-block
  * partial sums (exact) in column order.
  * Alignment: codes 16 bytes, keep_mask and HiF4 scales 4 bytes (RESQ_ERR_ARG otherwise).
- * Limits (RESQ_ERR_UNSUPPORTED beyond): RESQ_S_CHANNEL50 d <= 24576; RESQ_S_BLOCK32X64_50
- * ceil(m/32) * (d/64) <= 24576 blocks; RESQ_S_UNSTRUCT50 m * d <= 2^31.
+ * Limits (RESQ_ERR_UNSUPPORTED beyond): channel kinds d <= 24576; block kinds
+ * ceil(m/32) * (d/64) <= 24576 blocks; element-wise kinds m * d <= 2^31.
  * Workspace: resq_workspace_size(RESQ_OP_RESIDUAL_SPARSIFY, ...) bytes (0 for the local kinds).
  */
 int resq_residual_sparsify(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,

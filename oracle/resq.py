@@ -18,6 +18,10 @@ Readings of points the paper leaves open (also listed in the design notes):
       fewer than 32 rows is a smaller block.
   S4  ranking uses the sum of squares (same order as the L2 norm); ties go to the lowest
       index; floor(count / 2) items are kept.
+  S6  other levels and patterns (Sec. 4.3 defines S_alpha%, S_{M:N} and S^{MxN}_alpha% for
+      any alpha, M, N; Sec. 7 leaves levels other than 50% open): alpha is the kept percent,
+      floor(count * alpha / 100) items are kept, with the ranking and ties of S4; "k:g" keeps
+      the k largest of every g consecutive elements along d (ties to the lower index).
   S5  sums of squares are float64 in a fixed order (stated at each function), so near-ties
       are decided the same way on every implementation that keeps that order.
   T1  backward: dY, W and X are quantized along the contraction axis of each backward GEMM
@@ -35,6 +39,39 @@ from . import formats as F
 SPARSITY = ("none", "identity", "2:4", "channel50", "block32x64_50", "unstructured50")
 
 
+def parse_sparsity(kind: str):
+    """Family and parameters of a sparsity name (reading S6).
+
+    "none", "identity"; "k:g" (local k of g); "channel<p>", "block32x64_<p>",
+    "unstructured<p>" (global, p percent kept)."""
+    if kind in ("none", "identity"):
+        return kind, None
+    if ":" in kind:
+        k, g = (int(v) for v in kind.split(":"))
+        if g not in (4, 8) or not 1 <= k < g:
+            raise ValueError(kind)
+        return "local", (k, g)
+    for fam, prefix in (("channel", "channel"), ("block", "block32x64_"), ("unstructured", "unstructured")):
+        if kind.startswith(prefix) and kind[len(prefix):].isdigit():
+            p = int(kind[len(prefix):])
+            if not 1 <= p <= 99:
+                raise ValueError(kind)
+            return fam, p
+    raise ValueError(kind)
+
+
+def kept_fraction(kind: str) -> float:
+    """Nominal fraction of Q(Delta X) a sparsity function keeps (1 for identity, 0 for none)."""
+    fam, par = parse_sparsity(kind)
+    if fam == "none":
+        return 0.0
+    if fam == "identity":
+        return 1.0
+    if fam == "local":
+        return par[0] / par[1]
+    return par / 100.0
+
+
 # ----------------------------------------------------------------------------------------
 # Eq. 2: the activation residual
 # ----------------------------------------------------------------------------------------
@@ -46,22 +83,27 @@ def residual(x: np.ndarray, xhat: np.ndarray) -> np.ndarray:
 # ----------------------------------------------------------------------------------------
 # Sec. 4.3: sparsity functions applied to Q(Delta X)
 # ----------------------------------------------------------------------------------------
-def keep_2_4(rhat: np.ndarray) -> np.ndarray:
-    """S_{2:4}: in every group of 4 consecutive elements along d, keep the 2 largest |value|.
+def keep_k_of_g(rhat: np.ndarray, k: int, g: int) -> np.ndarray:
+    """S_{k:g}: in every group of g consecutive elements along d, keep the k largest |value|.
 
     An element's rank in its group is the number of elements that beat it: larger magnitude,
-    or equal magnitude and a lower index.  Ranks 0 and 1 are kept.
+    or equal magnitude and a lower index.  Ranks 0 .. k-1 are kept.
     """
     m, d = rhat.shape
-    a = np.abs(rhat).reshape(m, d // 4, 4)
+    a = np.abs(rhat).reshape(m, d // g, g)
     rank = np.zeros(a.shape, dtype=np.int64)
-    for i in range(4):
-        for j in range(4):
+    for i in range(g):
+        for j in range(g):
             if j == i:
                 continue
             beats = (a[..., j] > a[..., i]) | ((a[..., j] == a[..., i]) & (j < i))
             rank[..., i] += beats
-    return (rank < 2).reshape(m, d)
+    return (rank < k).reshape(m, d)
+
+
+def keep_2_4(rhat: np.ndarray) -> np.ndarray:
+    """S_{2:4}: in every group of 4 consecutive elements along d, keep the 2 largest |value|."""
+    return keep_k_of_g(rhat, 2, 4)
 
 
 def channel_keys(rhat: np.ndarray) -> np.ndarray:
@@ -72,19 +114,24 @@ def channel_keys(rhat: np.ndarray) -> np.ndarray:
     return acc
 
 
-def _top_half(keys: np.ndarray) -> np.ndarray:
-    """Boolean mask of the floor(len/2) largest keys; ties go to the lower index."""
+def _top(keys: np.ndarray, pct: int = 50) -> np.ndarray:
+    """Boolean mask of the floor(len * pct / 100) largest keys; ties go to the lower index."""
     idx = np.arange(keys.size)
     order = np.lexsort((idx, -keys))  # primary: key descending, secondary: index ascending
     keep = np.zeros(keys.size, dtype=bool)
-    keep[order[: keys.size // 2]] = True
+    keep[order[: keys.size * pct // 100]] = True
     return keep
 
 
-def keep_channel50(rhat: np.ndarray):
-    """S_50% (structured, channel-wise): keep the top half of the d channels by L2 norm."""
-    ch = _top_half(channel_keys(rhat))
+def keep_channel(rhat: np.ndarray, pct: int = 50):
+    """S_alpha% (structured, channel-wise): keep the top alpha% of the d channels by L2 norm."""
+    ch = _top(channel_keys(rhat), pct)
     return np.broadcast_to(ch[None, :], rhat.shape).copy(), ch
+
+
+def keep_channel50(rhat: np.ndarray):
+    """S_50%: keep the top half of the d channels by L2 norm."""
+    return keep_channel(rhat, 50)
 
 
 def block_keys(rhat: np.ndarray, fmt: str) -> np.ndarray:
@@ -111,17 +158,27 @@ def block_keys(rhat: np.ndarray, fmt: str) -> np.ndarray:
     return keys
 
 
-def keep_block50(rhat: np.ndarray, fmt: str):
-    """S^{32x64}_50%: keep the top half of the 32 x 64 blocks by L2 norm (row-major index)."""
+def keep_block(rhat: np.ndarray, fmt: str, pct: int = 50):
+    """S^{32x64}_alpha%: keep the top alpha% of the 32 x 64 blocks by L2 norm (row-major index)."""
     keys = block_keys(rhat, fmt)
-    blk = _top_half(keys.ravel()).reshape(keys.shape)
+    blk = _top(keys.ravel(), pct).reshape(keys.shape)
     elem = np.repeat(np.repeat(blk, 32, axis=0)[: rhat.shape[0]], 64, axis=1)
     return elem, blk
 
 
+def keep_block50(rhat: np.ndarray, fmt: str):
+    """S^{32x64}_50%: keep the top half of the 32 x 64 blocks by L2 norm."""
+    return keep_block(rhat, fmt, 50)
+
+
+def keep_unstructured(rhat: np.ndarray, pct: int = 50) -> np.ndarray:
+    """Element-wise alpha%: keep the floor(m*d*alpha/100) largest |value| (row-major index)."""
+    return _top(np.abs(rhat).ravel(), pct).reshape(rhat.shape)
+
+
 def keep_unstructured50(rhat: np.ndarray) -> np.ndarray:
-    """Element-wise 50%: keep the floor(m*d/2) largest |value| of the tensor (row-major index)."""
-    return _top_half(np.abs(rhat).ravel()).reshape(rhat.shape)
+    """Element-wise 50%: keep the floor(m*d/2) largest |value| of the tensor."""
+    return keep_unstructured(rhat, 50)
 
 
 def sparsify(kind: str, fmt: str, rcodes: np.ndarray, rhat: np.ndarray):
@@ -132,16 +189,17 @@ def sparsify(kind: str, fmt: str, rcodes: np.ndarray, rhat: np.ndarray):
     the channel and block kinds (None otherwise).
     """
     groups = None
-    if kind == "identity":
+    fam, par = parse_sparsity(kind)
+    if fam == "identity":
         keep = np.ones(rhat.shape, dtype=bool)
-    elif kind == "2:4":
-        keep = keep_2_4(rhat)
-    elif kind == "channel50":
-        keep, groups = keep_channel50(rhat)
-    elif kind == "block32x64_50":
-        keep, groups = keep_block50(rhat, fmt)
-    elif kind == "unstructured50":
-        keep = keep_unstructured50(rhat)
+    elif fam == "local":
+        keep = keep_k_of_g(rhat, *par)
+    elif fam == "channel":
+        keep, groups = keep_channel(rhat, par)
+    elif fam == "block":
+        keep, groups = keep_block(rhat, fmt, par)
+    elif fam == "unstructured":
+        keep = keep_unstructured(rhat, par)
     else:
         raise ValueError(kind)
     return np.where(keep, rcodes, 0).astype(np.uint8), keep, groups
@@ -224,10 +282,11 @@ def flops_resq(m: int, d: int, n: int, sparsity: str) -> int:
     """Algorithmic FLOPs of a ResQ linear: the FP4 main GEMM plus the kept residual part.
 
     S_2:4, S_50% (channel or element-wise) and the 50% block pattern keep half of the residual
-    (mdn); the identity keeps all of it (2mdn); no residual adds nothing.
+    (mdn); the identity keeps all of it (2mdn); no residual adds nothing.  Other levels and
+    patterns cost their nominal kept fraction of 2mdn (reading S6).
     """
     main = flops_dense(m, d, n)
-    extra = {"none": 0, "identity": 2 * m * d * n}.get(sparsity, m * d * n)
+    extra = round(2 * m * d * n * kept_fraction(sparsity))
     return main + extra
 
 

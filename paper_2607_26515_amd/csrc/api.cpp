@@ -44,16 +44,54 @@ size_t scale_bytes(int fmt, int64_t outer, int64_t K) {
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 bool valid_format(int f) { return f == RESQ_MXFP4 || f == RESQ_HIF4; }
-bool valid_sparsity(int s) { return s >= RESQ_S_NONE && s <= RESQ_S_UNSTRUCT50; }
-bool global_kind(int s) {
-  return s == RESQ_S_CHANNEL50 || s == RESQ_S_BLOCK32X64_50 || s == RESQ_S_UNSTRUCT50;
+
+// A decoded sparsity argument: the family (named by its 50% enum value: RESQ_S_2_4 stands
+// for every k:g pattern, RESQ_S_CHANNEL50 / _BLOCK32X64_50 / _UNSTRUCT50 for every level of
+// the global kinds) and its parameters.
+struct Sp {
+  int kind = -1;           // -1: not a valid sparsity code
+  int keep = 2, group = 4;  // k:g patterns
+  int pct = 50;             // global kinds: percent of the channels / blocks / elements kept
+};
+
+Sp decode_sparsity(int code) {
+  Sp sp;
+  if (code >= RESQ_S_NONE && code <= RESQ_S_UNSTRUCT50) {
+    sp.kind = code;
+    return sp;
+  }
+  const int family = code >> 8, low = code & 0xFF;
+  if (family == 1) {
+    const int k = low >> 4, g = low & 15;
+    if ((g == 4 || g == 8) && k >= 1 && k < g) {
+      sp.kind = RESQ_S_2_4;
+      sp.keep = k;
+      sp.group = g;
+    }
+  } else if (family >= 2 && family <= 4 && low >= 1 && low <= 99) {
+    sp.kind = family == 2 ? RESQ_S_CHANNEL50 : family == 3 ? RESQ_S_BLOCK32X64_50 : RESQ_S_UNSTRUCT50;
+    sp.pct = low;
+  }
+  return sp;
 }
 
-int resid_mode(int sp) {
-  switch (sp) {
+bool global_kind(const Sp& sp) {
+  return sp.kind == RESQ_S_CHANNEL50 || sp.kind == RESQ_S_BLOCK32X64_50 || sp.kind == RESQ_S_UNSTRUCT50;
+}
+
+// Items a global selection keeps: floor(count * pct / 100).
+int64_t keep_count(const Sp& sp, int64_t m, int64_t d) {
+  const int64_t count = sp.kind == RESQ_S_CHANNEL50 ? d
+                        : sp.kind == RESQ_S_BLOCK32X64_50 ? ((m + 31) / 32) * (d / 64)
+                                                          : m * d;
+  return count * sp.pct / 100;
+}
+
+int resid_mode(const Sp& sp) {
+  switch (sp.kind) {
     case RESQ_S_NONE: return resq::kResidNone;
     case RESQ_S_IDENTITY: return resq::kResidIdentity;
-    case RESQ_S_2_4: return resq::kResid24;
+    case RESQ_S_2_4: return sp.group == 8 ? resq::kResidNM8 : resq::kResidNM4;
     default: return resq::kResidDense;
   }
 }
@@ -113,16 +151,16 @@ resq::GemmOperands gemm_operands(int fmt, int64_t M, int64_t N, int64_t K, int n
   return op;
 }
 
-size_t carve_select(Carver& c, int fmt, int sp, int64_t m, int64_t d, double** partials,
+size_t carve_select(Carver& c, int fmt, const Sp& sp, int64_t m, int64_t d, double** partials,
                     resq::SelectWs* sel) {
   const size_t start = c.off;
-  void* part = (sp == RESQ_S_BLOCK32X64_50) ? c.take((size_t)m * (d / block_of(fmt)) * 8) : nullptr;
+  void* part = (sp.kind == RESQ_S_BLOCK32X64_50) ? c.take((size_t)m * (d / block_of(fmt)) * 8) : nullptr;
   if (partials) *partials = (double*)part;
-  const size_t sb = global_kind(sp) ? resq::select_ws_bytes(sp, fmt, m, d) : 0;
+  const size_t sb = global_kind(sp) ? resq::select_ws_bytes(sp.kind, fmt, m, d) : 0;
   void* sw = sb ? c.take(sb) : nullptr;
   if (sel) {
     *sel = resq::SelectWs{};
-    if (sw) resq::carve_select_ws(sw, sp, fmt, m, d, *sel);
+    if (sw) resq::carve_select_ws(sw, sp.kind, fmt, m, d, *sel);
   }
   return c.off - start;
 }
@@ -139,7 +177,7 @@ void carve_prepared(const void* base, int fmt, int64_t n, int64_t d, const uint8
   *fsc = b + align256(resq::frag_bytes(b_pack_mode(fmt), n, d));
 }
 
-size_t carve_fwd(void* base, int fmt, int sp, int64_t m, int64_t d, int64_t n, ActWs* w) {
+size_t carve_fwd(void* base, int fmt, const Sp& sp, int64_t m, int64_t d, int64_t n, ActWs* w) {
   Carver c(base);
   ActWs t{};
   if (global_kind(sp)) {  // the dense K-major Q(dX) the selection ranks
@@ -149,7 +187,7 @@ size_t carve_fwd(void* base, int fmt, int sp, int64_t m, int64_t d, int64_t n, A
   carve_select(c, fmt, sp, m, d, &t.partials, &t.sel);
   t.frag_x = (uint8_t*)c.take(resq::frag_bytes(a_pack_mode(fmt), m, d));
   t.fsc_x = (uint8_t*)c.take(resq::frag_scale_bytes(m, d));
-  if (sp != RESQ_S_NONE) {
+  if (sp.kind != RESQ_S_NONE) {
     t.frag_r = (uint8_t*)c.take(resq::frag_bytes(a_pack_mode(fmt), m, d));
     t.fsc_r = (uint8_t*)c.take(resq::frag_scale_bytes(m, d));
   }
@@ -191,41 +229,43 @@ int check_ws(void* ws, size_t have, size_t need) {
   return ok();
 }
 
-int check_activation_args(int format, int sparsity, const void* X, int64_t m, int64_t d,
-                          int64_t ldx) {
+int check_activation_args(int format, int sparsity, const Sp& sp, const void* X, int64_t m,
+                          int64_t d, int64_t ldx) {
   if (!valid_format(format)) return fail(RESQ_ERR_ARG, "unknown format %d", format);
-  if (!valid_sparsity(sparsity)) return fail(RESQ_ERR_ARG, "unknown sparsity %d", sparsity);
+  if (sp.kind < 0) return fail(RESQ_ERR_ARG, "unknown sparsity %d", sparsity);
   if (m < 0 || d < 0) return fail(RESQ_ERR_ARG, "negative size (m=%lld, d=%lld)", (long long)m, (long long)d);
   if (ldx < d) return fail(RESQ_ERR_ARG, "ldx (%lld) < d (%lld)", (long long)ldx, (long long)d);
   if (d % block_of(format) != 0)
     return fail(RESQ_ERR_SHAPE, "d (%lld) is not a multiple of the block size %lld", (long long)d, (long long)block_of(format));
-  if (sparsity == RESQ_S_BLOCK32X64_50 && d % 64 != 0)
+  if (sp.kind == RESQ_S_2_4 && d % sp.group != 0)
+    return fail(RESQ_ERR_SHAPE, "%d:%d sparsity needs d %% %d == 0 (d=%lld)", sp.keep, sp.group, sp.group, (long long)d);
+  if (sp.kind == RESQ_S_BLOCK32X64_50 && d % 64 != 0)
     return fail(RESQ_ERR_SHAPE, "32x64 block sparsity needs d %% 64 == 0 (d=%lld)", (long long)d);
-  if (sparsity == RESQ_S_CHANNEL50 && d > resq::select_max_items())
+  if (sp.kind == RESQ_S_CHANNEL50 && d > resq::select_max_items())
     return fail(RESQ_ERR_UNSUPPORTED, "channel selection supports d <= %lld (d=%lld)",
                 (long long)resq::select_max_items(), (long long)d);
-  if (sparsity == RESQ_S_BLOCK32X64_50 && ((m + 31) / 32) * (d / 64) > resq::select_max_items())
+  if (sp.kind == RESQ_S_BLOCK32X64_50 && ((m + 31) / 32) * (d / 64) > resq::select_max_items())
     return fail(RESQ_ERR_UNSUPPORTED, "block selection supports ceil(m/32)*(d/64) <= %lld blocks",
                 (long long)resq::select_max_items());
-  if (sparsity == RESQ_S_UNSTRUCT50 && m * d > ((int64_t)1 << 31))
-    return fail(RESQ_ERR_UNSUPPORTED, "element-wise 50%% selection supports m*d <= 2^31 (m*d=%lld)", (long long)(m * d));
+  if (sp.kind == RESQ_S_UNSTRUCT50 && m * d > ((int64_t)1 << 31))
+    return fail(RESQ_ERR_UNSUPPORTED, "element-wise selection supports m*d <= 2^31 (m*d=%lld)", (long long)(m * d));
   if (m > 0 && d > 0 && X == nullptr) return fail(RESQ_ERR_ARG, "X is NULL");
   return ok();
 }
 
-int run_activation_side(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
+int run_activation_side(int format, const Sp& sp, const uint16_t* X, int64_t m, int64_t d,
                         int64_t ldx, uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes,
                         void* qr_scales, uint8_t* keep_mask, uint8_t* group_mask,
                         double* partials, const resq::SelectWs& sel, hipStream_t s) {
   {
     resq::ProfScope prof_(resq::kProfResidual, s);
-    resq::launch_residual(format, resid_mode(sparsity), X, m, d, ldx, qx_codes, qx_scales,
-                          qr_codes, qr_scales, keep_mask, partials, s);
+    resq::launch_residual(format, resid_mode(sp), X, m, d, ldx, qx_codes, qx_scales, qr_codes,
+                          qr_scales, keep_mask, partials, s, false, nullptr, 0, sp.keep);
   }
-  if (global_kind(sparsity)) {
+  if (global_kind(sp)) {
     resq::ProfScope prof_(resq::kProfSelect, s);
-    resq::launch_select(format, sparsity, m, d, qr_codes, qr_scales, partials, keep_mask,
-                        group_mask, sel, s);
+    resq::launch_select(format, sp.kind, m, d, keep_count(sp, m, d), qr_codes, qr_scales, partials,
+                        keep_mask, group_mask, sel, s);
   }
   return check_launch("residual/sparsify");
 }
@@ -265,16 +305,17 @@ int resq_quantize(int format, const void* x, int in_dtype, int64_t rows, int64_t
 }
 
 size_t resq_workspace_size(int op, int format, int sparsity, int64_t m, int64_t d, int64_t n) {
-  if (!valid_format(format) || !valid_sparsity(sparsity) || m < 0 || d < 0 || n < 0) return 0;
+  const Sp sp = decode_sparsity(sparsity);
+  if (!valid_format(format) || sp.kind < 0 || m < 0 || d < 0 || n < 0) return 0;
   switch (op) {
     case RESQ_OP_RESIDUAL_SPARSIFY: {
       Carver c(nullptr);
-      carve_select(c, format, sparsity, m, d, nullptr, nullptr);
+      carve_select(c, format, sp, m, d, nullptr, nullptr);
       return c.off;
     }
     case RESQ_OP_LINEAR_FWD:
-      return carve_fwd(nullptr, format, sparsity, m, d, n, nullptr) + prepared_bytes(format, n, d);
-    case RESQ_OP_LINEAR_FWD_PREPARED: return carve_fwd(nullptr, format, sparsity, m, d, n, nullptr);
+      return carve_fwd(nullptr, format, sp, m, d, n, nullptr) + prepared_bytes(format, n, d);
+    case RESQ_OP_LINEAR_FWD_PREPARED: return carve_fwd(nullptr, format, sp, m, d, n, nullptr);
     case RESQ_OP_LINEAR_BWD: return carve_bwd(nullptr, format, m, d, n, nullptr);
     default: return 0;
   }
@@ -284,11 +325,12 @@ int resq_residual_sparsify(int format, int sparsity, const uint16_t* X, int64_t 
                            int64_t ldx, uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes,
                            void* qr_scales, uint8_t* keep_mask, uint8_t* group_mask,
                            void* workspace, size_t workspace_bytes, void* stream) {
-  int rc = check_activation_args(format, sparsity, X, m, d, ldx);
+  const Sp sp = decode_sparsity(sparsity);
+  int rc = check_activation_args(format, sparsity, sp, X, m, d, ldx);
   if (rc != RESQ_OK) return rc;
   if (m == 0 || d == 0) return ok();
   if (!qx_codes || !qx_scales) return fail(RESQ_ERR_ARG, "qx_codes / qx_scales is NULL");
-  if (sparsity != RESQ_S_NONE && (!qr_codes || !qr_scales))
+  if (sp.kind != RESQ_S_NONE && (!qr_codes || !qr_scales))
     return fail(RESQ_ERR_ARG, "qr_codes / qr_scales is NULL");
   if ((uintptr_t)qx_codes % 16 || (uintptr_t)qr_codes % 16 || (uintptr_t)keep_mask % 4 ||
       (format == RESQ_HIF4 && ((uintptr_t)qx_scales % 4 || (uintptr_t)qr_scales % 4)))
@@ -296,10 +338,10 @@ int resq_residual_sparsify(int format, int sparsity, const uint16_t* X, int64_t 
   Carver c(workspace);
   double* partials = nullptr;
   resq::SelectWs sel{};
-  carve_select(c, format, sparsity, m, d, &partials, &sel);
+  carve_select(c, format, sp, m, d, &partials, &sel);
   rc = check_ws(workspace, workspace_bytes, c.off);
   if (rc != RESQ_OK) return rc;
-  return run_activation_side(format, sparsity, X, m, d, ldx, qx_codes, qx_scales, qr_codes,
+  return run_activation_side(format, sp, X, m, d, ldx, qx_codes, qx_scales, qr_codes,
                              qr_scales, keep_mask, group_mask, partials, sel,
                              (hipStream_t)stream);
 }
@@ -332,33 +374,33 @@ int resq_prepare_weights(int format, const uint8_t* qw_codes, const void* qw_sca
 
 namespace {
 
-int linear_fwd_core(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
+int linear_fwd_core(int format, const Sp& sp, const uint16_t* X, int64_t m, int64_t d,
                     int64_t ldx, const void* wprep, int64_t n, void* Y, int64_t ldy, bool out_bf16,
                     const ActWs& w, hipStream_t s) {
-  if (global_kind(sparsity)) {
+  if (global_kind(sp)) {
     // the residual pass writes Q(X) as MFMA fragments and the dense Q(dX) K-major (the
     // selection ranks all of it); the selection then writes S(Q(dX)) as fragments
     {
       resq::ProfScope prof_(resq::kProfResidual, s);
-      const bool elem = sparsity == RESQ_S_UNSTRUCT50;
+      const bool elem = sp.kind == RESQ_S_UNSTRUCT50;
       resq::launch_residual(format, resq::kResidDense, X, m, d, ldx, w.frag_x, w.fsc_x, w.qr_codes,
-                            w.qr_scales, nullptr, sparsity == RESQ_S_BLOCK32X64_50 ? w.partials : nullptr,
+                            w.qr_scales, nullptr, sp.kind == RESQ_S_BLOCK32X64_50 ? w.partials : nullptr,
                             s, true, elem ? w.sel.hist : nullptr, elem ? resq::select_hist_words() : 0);
     }
     resq::ProfScope prof_(resq::kProfSelect, s);
-    resq::launch_select_frag(format, sparsity, m, d, w.qr_codes, w.qr_scales, w.partials, w.sel,
-                             a_pack_mode(format), w.frag_r, w.fsc_r, s);
+    resq::launch_select_frag(format, sp.kind, m, d, keep_count(sp, m, d), w.qr_codes, w.qr_scales,
+                             w.partials, w.sel, a_pack_mode(format), w.frag_r, w.fsc_r, s);
   } else {
     // local kinds: the residual pass writes the MFMA fragments directly
     resq::ProfScope prof_(resq::kProfResidual, s);
-    resq::launch_residual(format, resid_mode(sparsity), X, m, d, ldx, w.frag_x, w.fsc_x,
-                          w.frag_r, w.fsc_r, nullptr, nullptr, s, true);
+    resq::launch_residual(format, resid_mode(sp), X, m, d, ldx, w.frag_x, w.fsc_x, w.frag_r,
+                          w.fsc_r, nullptr, nullptr, s, true, nullptr, 0, sp.keep);
   }
   const uint8_t* af[2] = {w.frag_x, w.frag_r};
   const uint8_t* asc[2] = {w.fsc_x, w.fsc_r};
   const uint8_t *bf, *bsc;
   carve_prepared(wprep, format, n, d, &bf, &bsc);
-  resq::GemmOperands op = gemm_operands(format, m, n, d, sparsity == RESQ_S_NONE ? 1 : 2, af, asc,
+  resq::GemmOperands op = gemm_operands(format, m, n, d, sp.kind == RESQ_S_NONE ? 1 : 2, af, asc,
                                         bf, bsc, Y, ldy, out_bf16);
   op.partial = w.gemm_partial;
   {
@@ -368,14 +410,14 @@ int linear_fwd_core(int format, int sparsity, const uint16_t* X, int64_t m, int6
   return check_launch("resq_linear_fwd");
 }
 
-int check_fwd_args(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
-                   int64_t ldx, int64_t n, const void* Y, int64_t ldy) {
-  int rc = check_activation_args(format, sparsity, X, m, d, ldx);
+int check_fwd_args(int format, int sparsity, const Sp& sp, const uint16_t* X, int64_t m,
+                   int64_t d, int64_t ldx, int64_t n, const void* Y, int64_t ldy) {
+  int rc = check_activation_args(format, sparsity, sp, X, m, d, ldx);
   if (rc != RESQ_OK) return rc;
   if (n < 0) return fail(RESQ_ERR_ARG, "negative n");
   if (ldy < n) return fail(RESQ_ERR_ARG, "ldy (%lld) < n (%lld)", (long long)ldy, (long long)n);
   if (m > 0 && n > 0 && !Y) return fail(RESQ_ERR_ARG, "Y is NULL");
-  if (!resq::gemm_supported(format, m, n, d, sparsity == RESQ_S_NONE ? 1 : 2))
+  if (!resq::gemm_supported(format, m, n, d, sp.kind == RESQ_S_NONE ? 1 : 2))
     return fail(RESQ_ERR_UNSUPPORTED, "GEMM operands too large for 32-bit offsets (m=%lld, d=%lld, n=%lld)",
                 (long long)m, (long long)d, (long long)n);
   return ok();
@@ -384,16 +426,17 @@ int check_fwd_args(int format, int sparsity, const uint16_t* X, int64_t m, int64
 int linear_fwd_prepared(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,
                         int64_t ldx, const void* wprep, int64_t n, void* Y, int64_t ldy, bool out_bf16,
                         void* workspace, size_t workspace_bytes, void* stream) {
-  int rc = check_fwd_args(format, sparsity, X, m, d, ldx, n, Y, ldy);
+  const Sp sp = decode_sparsity(sparsity);
+  int rc = check_fwd_args(format, sparsity, sp, X, m, d, ldx, n, Y, ldy);
   if (rc != RESQ_OK) return rc;
   if (m == 0 || n == 0) return ok();
   if (d > 0 && !wprep) return fail(RESQ_ERR_ARG, "wprep is NULL");
   if ((uintptr_t)wprep % 256 != 0) return fail(RESQ_ERR_ARG, "wprep must be 256-byte aligned");
   ActWs w{};
-  const size_t need = carve_fwd(workspace, format, sparsity, m, d, n, &w);
+  const size_t need = carve_fwd(workspace, format, sp, m, d, n, &w);
   rc = check_ws(workspace, workspace_bytes, need);
   if (rc != RESQ_OK) return rc;
-  return linear_fwd_core(format, sparsity, X, m, d, ldx, wprep, n, Y, ldy, out_bf16, w,
+  return linear_fwd_core(format, sp, X, m, d, ldx, wprep, n, Y, ldy, out_bf16, w,
                          (hipStream_t)stream);
 }
 
@@ -418,14 +461,15 @@ int resq_linear_fwd(int format, int sparsity, const uint16_t* X, int64_t m, int6
                     int64_t ldx, const uint8_t* qw_codes, const void* qw_scales, int64_t n,
                     float* Y, int64_t ldy, void* workspace, size_t workspace_bytes,
                     void* stream) {
-  int rc = check_fwd_args(format, sparsity, X, m, d, ldx, n, Y, ldy);
+  const Sp sp = decode_sparsity(sparsity);
+  int rc = check_fwd_args(format, sparsity, sp, X, m, d, ldx, n, Y, ldy);
   if (rc != RESQ_OK) return rc;
   if (m == 0 || n == 0) return ok();
   if (d > 0 && (!qw_codes || !qw_scales)) return fail(RESQ_ERR_ARG, "qw_codes / qw_scales is NULL");
   if ((uintptr_t)qw_codes % 16 != 0 || (format == RESQ_HIF4 && (uintptr_t)qw_scales % 4 != 0))
     return fail(RESQ_ERR_ARG, "qw_codes must be 16-byte aligned (HiF4 scales 4-byte aligned)");
   ActWs w{};
-  const size_t act = carve_fwd(workspace, format, sparsity, m, d, n, &w);
+  const size_t act = carve_fwd(workspace, format, sp, m, d, n, &w);
   const size_t need = act + prepared_bytes(format, n, d);
   rc = check_ws(workspace, workspace_bytes, need);
   if (rc != RESQ_OK) return rc;
@@ -437,7 +481,7 @@ int resq_linear_fwd(int format, int sparsity, const uint16_t* X, int64_t m, int6
     resq::ProfScope prof_(resq::kProfPack, s);
     resq::launch_pack(b_pack_mode(format), qw_codes, qw_scales, n, d, (uint8_t*)frag, (uint8_t*)fsc, s);
   }
-  return linear_fwd_core(format, sparsity, X, m, d, ldx, wprep, n, Y, ldy, false, w, s);
+  return linear_fwd_core(format, sp, X, m, d, ldx, wprep, n, Y, ldy, false, w, s);
 }
 
 int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uint16_t* W,

@@ -11,8 +11,9 @@ namespace resq {
 enum ResidMode {
   kResidNone = 0,      // Q(X) only
   kResidIdentity = 1,  // Q(dX) kept whole
-  kResid24 = 2,        // S_2:4 applied in the pass
-  kResidDense = 3      // Q(dX) written whole; a global selection prunes it afterwards
+  kResidNM4 = 2,       // S_k:4 applied in the pass (k = nm_keep; S_2:4 with k = 2)
+  kResidDense = 3,     // Q(dX) written whole; a global selection prunes it afterwards
+  kResidNM8 = 4        // S_k:8 applied in the pass
 };
 
 // Row-wise quantization (blocks along columns) of a bf16 or f32 matrix.
@@ -31,8 +32,8 @@ void launch_quant_cols_frag(int mode, const uint16_t* x, int64_t rows, int64_t c
 void launch_quant_cols(int fmt, const void* x, bool in_f32, int64_t rows, int64_t cols,
                        int64_t ld, uint8_t* codes, void* scales, hipStream_t s);
 
-// Q(X), dX = X - Q(X), Q(dX), and S_2:4 / identity / none.  keep_mask and partials may be
-// null.  partials (double [m][d/B]) receives the exact per-scale-block sums of squares of
+// Q(X), dX = X - Q(X), Q(dX), and S_k:4 / S_k:8 (k = nm_keep) / identity / none.  keep_mask
+// and partials may be null.  partials (double [m][d/B]) receives the exact per-scale-block sums of squares of
 // the dequantized Q(dX) (used by the block selection).  frag = true writes MFMA fragments
 // (pack.hip layout; codes -> fragment records, scales -> per-lane scale bytes) instead of
 // K-major codes + scales: for both Q(X) and Q(dX) with the local kinds; with kResidDense
@@ -42,7 +43,7 @@ void launch_quant_cols(int fmt, const void* x, bool in_f32, int64_t rows, int64_
 void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
                      uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes, void* qr_scales,
                      uint8_t* keep_mask, double* partials, hipStream_t s, bool frag = false,
-                     uint32_t* zero = nullptr, int zero_words = 0);
+                     uint32_t* zero = nullptr, int zero_words = 0, int nm_keep = 2);
 
 // MFMA operand packing (pack.hip): K-major codes + scales -> fragment-major operands.
 enum PackMode { kPackMx = 0, kPackHiA = 1, kPackHiB = 2 };
@@ -54,9 +55,10 @@ void launch_pack(int mode, const uint8_t* codes, const void* scales, int64_t row
                  uint8_t* frag, uint8_t* fscale, hipStream_t s, int mask = 0,
                  const uint8_t* gbits = nullptr);
 
-// Global selections for the channel, block and unstructured 50% residual patterns.
-// They read the dense Q(dX) (codes + scales), choose the kept set, then zero the pruned
-// codes in place and write the element keep mask (and the channel/block mask).
+// Global selections for the channel, block and element-wise residual patterns (sparsity
+// 3, 4, 5).  They read the dense Q(dX) (codes + scales), keep the `keep` largest channels,
+// blocks or elements, then zero the pruned codes in place and write the element keep mask
+// (and the channel/block mask).
 struct SelectWs {
   double* keys;       // channel or block keys
   uint32_t* hist;     // radix-select histograms / counters
@@ -67,14 +69,14 @@ struct SelectWs {
 size_t select_ws_bytes(int sparsity, int fmt, int64_t m, int64_t d);
 int64_t select_max_items();  // most channels / blocks a channel or block selection ranks
 void carve_select_ws(void* base, int sparsity, int fmt, int64_t m, int64_t d, SelectWs& ws);
-void launch_select(int fmt, int sparsity, int64_t m, int64_t d, uint8_t* qr_codes,
+void launch_select(int fmt, int sparsity, int64_t m, int64_t d, int64_t keep, uint8_t* qr_codes,
                    const void* qr_scales, const double* partials, uint8_t* keep_mask,
                    uint8_t* group_mask, const SelectWs& ws, hipStream_t s);
 // The same selections for the forward GEMM: S(Q(dX)) is written as fragment-major operand
 // records (PackMode pack_mode) to frag / fscale; the K-major codes are left unpruned and no
 // masks are written.  For the element-wise kind the histogram (select_hist_words() words at
 // ws.hist) must have been cleared beforehand (the residual pass does it).
-void launch_select_frag(int fmt, int sparsity, int64_t m, int64_t d, uint8_t* qr_codes,
+void launch_select_frag(int fmt, int sparsity, int64_t m, int64_t d, int64_t keep, uint8_t* qr_codes,
                         const void* qr_scales, const double* partials, const SelectWs& ws,
                         int pack_mode, uint8_t* frag, uint8_t* fscale, hipStream_t s);
 int select_hist_words();

@@ -102,13 +102,16 @@ __global__ __launch_bounds__(kThreads) void quant_cols_kernel(const void* __rest
 
 // ---------------------------------------------------------------------------------------
 // Residual pass of Eq. 2 / Eq. 4 with K-major output: Q(X), dX = X - Q(X) (float32,
-// exact), Q(dX), and S_2:4 / identity / the dense Q(dX) a global selection prunes later.
+// exact), Q(dX), and S_k:4 / S_k:8 / identity / the dense Q(dX) a global selection prunes
+// later.  A lane holds 4 consecutive elements; an S_k:8 group is the lane pair (2i, 2i+1),
+// which d % 8 == 0 keeps active or inactive together.
 // ---------------------------------------------------------------------------------------
 template <int FMT, int MODE, bool VEC>
 __global__ __launch_bounds__(kThreads) void residual_kernel(
     const uint16_t* __restrict__ X, int64_t m, int64_t m_rows, int64_t d, int64_t ldx,
     uint8_t* __restrict__ qx_codes, void* __restrict__ qx_scales, uint8_t* __restrict__ qr_codes,
-    void* __restrict__ qr_scales, uint8_t* __restrict__ keep_mask, double* __restrict__ partials) {
+    void* __restrict__ qr_scales, uint8_t* __restrict__ keep_mask, double* __restrict__ partials,
+    int nm_keep) {
   const int64_t j4 = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (4 * j4 >= d) return;
   for (int64_t row = blockIdx.y; row < m_rows; row += gridDim.y) {
@@ -123,7 +126,30 @@ __global__ __launch_bounds__(kThreads) void residual_kernel(
       for (int k = 0; k < 4; ++k) r[k] = v[k] - qx.val[k];  // exact in float32
       const Quad qr = quantize_quad<FMT>(r);
       uint32_t keep = 0xFu;
-      if constexpr (MODE == kResid24) keep = keep_2_of_4(qr.code);
+      if constexpr (MODE == kResidNM4) {
+        if (nm_keep == 2) {
+          keep = keep_2_of_4(qr.code);
+        } else {
+          uint32_t mag[4];
+#pragma unroll
+          for (int k = 0; k < 4; ++k) mag[k] = qr.code[k] & 7u;
+          keep = keep_k_of_g<4>(mag, nm_keep);
+        }
+      } else if constexpr (MODE == kResidNM8) {
+        // the pair's 8 codes and their shifts (HiF4 level-3 groups may differ)
+        const uint32_t mine = pack_quad_codes(qr.code) | ((uint32_t)qr.b << 16);
+        const uint32_t other = __shfl_xor(mine, 1, 64);
+        const bool odd = (threadIdx.x & 1) != 0;
+        const uint32_t lo = odd ? other : mine, hi = odd ? mine : other;
+        uint32_t c8[8];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          c8[k] = (lo >> (4 * k)) & 15u;
+          c8[4 + k] = (hi >> (4 * k)) & 15u;
+        }
+        const int b2[2] = {(int)(lo >> 16), (int)(hi >> 16)};
+        keep = (keep_local8<8>(c8, b2, nm_keep) >> (odd ? 4 : 0)) & 0xFu;
+      }
       uint32_t c[4];
 #pragma unroll
       for (int k = 0; k < 4; ++k) c[k] = ((keep >> k) & 1u) ? qr.code[k] : 0u;
@@ -153,7 +179,7 @@ __global__ __launch_bounds__(kThreads) void residual_kernel(
 // tile, half (i/4)%2 and the 8-element slice i%4.  An MXFP4 scale block (32 elements) is 4
 // consecutive lanes, a HiF4 64-block 8 consecutive lanes, a HiF4 level-2 group one lane.
 // Each thread quantizes its slice, forms dX = X - Q(X) (exact in float32), quantizes dX,
-// applies S_2:4, and the 4 threads of a record write it as one contiguous 16-byte (MXFP4) or
+// applies S_k:4 or S_k:8 (whole groups inside the slice), and the 4 threads of a record write it as one contiguous 16-byte (MXFP4) or
 // 48-byte (HiF4 E2M3 hi | lo) run.  Rows past m, and the missing half of an MXFP4 K step
 // when d % 64 == 32, quantize zeros.
 // ---------------------------------------------------------------------------------------
@@ -292,7 +318,7 @@ template <int FMT, int MODE, bool VEC>
 __device__ __forceinline__ void residual_frag_tile(
     const uint16_t* __restrict__ X, int64_t m, int64_t d, int64_t ldx, int64_t nkb,
     uint8_t* __restrict__ fx, uint8_t* __restrict__ fsx, uint8_t* __restrict__ fr,
-    uint8_t* __restrict__ fsr, double* __restrict__ partials, int64_t t, int64_t kb) {
+    uint8_t* __restrict__ fsr, double* __restrict__ partials, int nm_keep, int64_t t, int64_t kb) {
   const int64_t f = t * nkb + kb;  // fragment index
   const int tid = threadIdx.x;
   const int rr = tid >> 3, half = (tid >> 2) & 1, s = tid & 3;
@@ -327,15 +353,11 @@ __device__ __forceinline__ void residual_frag_tile(
 #pragma unroll
     for (int i = 0; i < 8; ++i) x[i] -= val[i];  // dX, exact in float32
     quantize8<FMT>(x, code, val, scale_byte, c1, b, b2);
-    if constexpr (MODE == kResid24) {
+    if constexpr (MODE == kResidNM4 || MODE == kResidNM8) {
+      const uint32_t keep = keep_local8<MODE == kResidNM4 ? 4 : 8>(code, b, nm_keep);
 #pragma unroll
-      for (int g = 0; g < 2; ++g) {
-        const uint32_t c4[4] = {code[4 * g], code[4 * g + 1], code[4 * g + 2], code[4 * g + 3]};
-        const uint32_t keep = keep_2_of_4(c4);
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (!((keep >> e) & 1u)) code[4 * g + e] = 0u;
-      }
+      for (int e = 0; e < 8; ++e)
+        if (!((keep >> e) & 1u)) code[e] = 0u;
     }
     if constexpr (MODE == kResidDense) {
       store_kmajor8<FMT>(fr, fsr, partials, row < m && col0 < d, row, d, kb, half, s, code, val,
@@ -355,12 +377,13 @@ __global__ __launch_bounds__(256) void residual_frag_kernel(
     const uint16_t* __restrict__ X, int64_t m, int64_t d, int64_t ldx, int64_t nkb,
     uint8_t* __restrict__ fx, uint8_t* __restrict__ fsx, uint8_t* __restrict__ fr,
     uint8_t* __restrict__ fsr, double* __restrict__ partials, uint32_t* __restrict__ zero,
-    int zero_words) {
+    int zero_words, int nm_keep) {
   if (zero != nullptr && blockIdx.x == 0 && blockIdx.y == 0)
     for (int i = threadIdx.x; i < zero_words; i += blockDim.x) zero[i] = 0u;
   const int64_t mtiles = (m + 31) / 32;
   for (int64_t t = blockIdx.y; t < mtiles; t += gridDim.y)
-    residual_frag_tile<FMT, MODE, VEC>(X, m, d, ldx, nkb, fx, fsx, fr, fsr, partials, t, blockIdx.x);
+    residual_frag_tile<FMT, MODE, VEC>(X, m, d, ldx, nkb, fx, fsx, fr, fsr, partials, nm_keep, t,
+                                       blockIdx.x);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -537,19 +560,20 @@ void launch_quant_cols(int fmt, const void* x, bool in_f32, int64_t rows, int64_
 void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
                      uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes, void* qr_scales,
                      uint8_t* keep_mask, double* partials, hipStream_t s, bool frag,
-                     uint32_t* zero, int zero_words) {
+                     uint32_t* zero, int zero_words, int nm_keep) {
   if (m == 0 || d == 0) return;
   if (frag) {
     const int64_t nkb = (d + 63) / 64;
     const dim3 grid((unsigned)nkb, grid_rows((m + 31) / 32));
     const bool vec16 = ((uintptr_t)X % 16 == 0) && (ldx % 8 == 0);
-#define RESQ_RF(F, M, V) hipLaunchKernelGGL((residual_frag_kernel<F, M, V>), grid, dim3(256), 0, s, X, m, d, ldx, nkb, qx_codes, (uint8_t*)qx_scales, qr_codes, (uint8_t*)qr_scales, partials, zero, zero_words)
+#define RESQ_RF(F, M, V) hipLaunchKernelGGL((residual_frag_kernel<F, M, V>), grid, dim3(256), 0, s, X, m, d, ldx, nkb, qx_codes, (uint8_t*)qx_scales, qr_codes, (uint8_t*)qr_scales, partials, zero, zero_words, nm_keep)
 #define RESQ_RF_MODE(F, V)                                        \
     switch (mode) {                                               \
       case kResidNone: RESQ_RF(F, kResidNone, V); break;          \
       case kResidIdentity: RESQ_RF(F, kResidIdentity, V); break;  \
       case kResidDense: RESQ_RF(F, kResidDense, V); break;        \
-      default: RESQ_RF(F, kResid24, V); break;                    \
+      case kResidNM8: RESQ_RF(F, kResidNM8, V); break;            \
+      default: RESQ_RF(F, kResidNM4, V); break;                   \
     }
     if (fmt == kMX) { if (vec16) { RESQ_RF_MODE(kMX, true) } else { RESQ_RF_MODE(kMX, false) } }
     else { if (vec16) { RESQ_RF_MODE(kHI, true) } else { RESQ_RF_MODE(kHI, false) } }
@@ -559,12 +583,13 @@ void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d,
   }
   const dim3 grid((unsigned)((d / 4 + kThreads - 1) / kThreads), grid_rows(m));
   const bool vec = ((uintptr_t)X % 8 == 0) && (ldx % 4 == 0);
-#define RESQ_RK(F, M, V) hipLaunchKernelGGL((residual_kernel<F, M, V>), grid, dim3(kThreads), 0, s, X, m, m, d, ldx, qx_codes, qx_scales, qr_codes, qr_scales, keep_mask, partials)
+#define RESQ_RK(F, M, V) hipLaunchKernelGGL((residual_kernel<F, M, V>), grid, dim3(kThreads), 0, s, X, m, m, d, ldx, qx_codes, qx_scales, qr_codes, qr_scales, keep_mask, partials, nm_keep)
 #define RESQ_RK_MODE(F, V)                                       \
   switch (mode) {                                                \
     case kResidNone: RESQ_RK(F, kResidNone, V); break;           \
     case kResidIdentity: RESQ_RK(F, kResidIdentity, V); break;   \
-    case kResid24: RESQ_RK(F, kResid24, V); break;               \
+    case kResidNM4: RESQ_RK(F, kResidNM4, V); break;             \
+    case kResidNM8: RESQ_RK(F, kResidNM8, V); break;             \
     default: RESQ_RK(F, kResidDense, V); break;                  \
   }
   if (fmt == kMX) { if (vec) { RESQ_RK_MODE(kMX, true) } else { RESQ_RK_MODE(kMX, false) } }

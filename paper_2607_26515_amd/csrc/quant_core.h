@@ -84,4 +84,49 @@ __device__ __forceinline__ uint32_t keep_2_of_4(const uint32_t c[4]) {
   return keep;
 }
 
+// S_k:g on one group of G (4 or 8) consecutive elements given as magnitudes on one common
+// grid: keep the k largest, lower index on ties.  Key i = mag << 3 | (G - 1 - i) is distinct per
+// element and orders by magnitude, then by lower index; element i is kept when fewer than k
+// keys exceed its own.
+template <int G>
+__device__ __forceinline__ uint32_t keep_k_of_g(const uint32_t mag[G], int k) {
+  uint32_t key[G];
+#pragma unroll
+  for (int i = 0; i < G; ++i) key[i] = (mag[i] << 3) | (uint32_t)(G - 1 - i);
+  uint32_t keep = 0;
+#pragma unroll
+  for (int i = 0; i < G; ++i) {
+    int above = 0;
+#pragma unroll
+    for (int j = 0; j < G; ++j) above += (j != i && key[j] > key[i]) ? 1 : 0;
+    keep |= (above < k ? 1u : 0u) << i;
+  }
+  return keep;
+}
+
+// The keep bits of the local pattern S_k:G for 8 consecutive codes (two groups when G = 4).
+// b[h] is the HiF4 level-2 + level-3 shift of elements 4h .. 4h+3 (0 for MXFP4, whose 8
+// aligned elements share one scale).  A 4-group shares its scale, so its codes compare
+// directly; an 8-group spans two HiF4 level-3 groups, so each magnitude code k is put on the
+// finer common grid as k << (2 - b) (value = k/4 * s1 * 2^-b).
+template <int G>
+__device__ __forceinline__ uint32_t keep_local8(const uint32_t c[8], const int b[2], int k) {
+  if constexpr (G == 8) {
+    uint32_t mag[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) mag[i] = (c[i] & 7u) << (2 - b[i / 4]);
+    return keep_k_of_g<8>(mag, k);
+  } else {
+    const uint32_t a[4] = {c[0], c[1], c[2], c[3]}, e[4] = {c[4], c[5], c[6], c[7]};
+    if (k == 2) return keep_2_of_4(a) | (keep_2_of_4(e) << 4);
+    uint32_t ma[4], me[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      ma[i] = a[i] & 7u;
+      me[i] = e[i] & 7u;
+    }
+    return keep_k_of_g<4>(ma, k) | (keep_k_of_g<4>(me, k) << 4);
+  }
+}
+
 }  // namespace resq

@@ -1,8 +1,9 @@
-// Global selections of the residual sparsity functions (paper Sec. 4.3): S_50% over
-// channels, S^{32x64}_50% over 32-row x 64-column blocks, and an element-wise 50% variant.
+// Global selections of the residual sparsity functions (paper Sec. 4.3): S_alpha% over
+// channels, S^{32x64}_alpha% over 32-row x 64-column blocks, and an element-wise variant.
 //
 // Each one ranks items by a key computed from the dense Q(dX) (dequantized values), keeps the
-// floor(count / 2) largest, and breaks ties by the lowest index:
+// `keep` largest (floor(count * alpha / 100), the caller's count; alpha = 50 in the paper's
+// experiments), and breaks ties by the lowest index:
 //   channel j      : sum over rows i = 0, 1, ..., m-1 of value(i, j)^2, float64, in that order
 //   block (I, J)   : over the block's rows in order, each row adding its per-scale-block sums
 //                    (exact; written by the residual pass) in column order, float64
@@ -409,14 +410,15 @@ __device__ __forceinline__ void load_choice(const uint32_t* hist, uint32_t* lh, 
 template <int FMT, int PASS>
 __global__ __launch_bounds__(kThreads) void uhist_kernel(const uint8_t* __restrict__ codes,
                                                          const void* __restrict__ scales, int64_t m,
-                                                         int64_t d, uint32_t* __restrict__ hist) {
+                                                         int64_t d, uint32_t keep,
+                                                         uint32_t* __restrict__ hist) {
   __shared__ uint32_t lh[kUHist];
   __shared__ uint32_t ch[4];
   __shared__ uint32_t wsum[kThreads / 64];
   const int tid = threadIdx.x;
   uint32_t want = 0;
   if constexpr (PASS == 1) {
-    load_choice(hist, lh, (uint32_t)(m * d / 2), false, wsum, ch);
+    load_choice(hist, lh, keep, false, wsum, ch);
     want = ch[0];
     __syncthreads();  // lh is cleared below
   }
@@ -444,12 +446,13 @@ __global__ __launch_bounds__(kThreads) void uhist_kernel(const uint8_t* __restri
 template <int FMT>
 __global__ __launch_bounds__(kThreads) void uties_kernel(const uint8_t* __restrict__ codes,
                                                          const void* __restrict__ scales, int64_t m,
-                                                         int64_t d, const uint32_t* __restrict__ hist,
+                                                         int64_t d, uint32_t keep,
+                                                         const uint32_t* __restrict__ hist,
                                                          uint32_t* __restrict__ tie_counts) {
   __shared__ uint32_t lh[kUHist];
   __shared__ uint32_t ch[4];
   __shared__ uint32_t wsum[kThreads / 64];
-  load_choice(hist, lh, (uint32_t)(m * d / 2), true, wsum, ch);
+  load_choice(hist, lh, keep, true, wsum, ch);
   const uint32_t T = ch[2];
   const int64_t w0 = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * kWordsPerThread;
   uint32_t ties = 0;
@@ -471,7 +474,8 @@ __global__ __launch_bounds__(kThreads) void uties_kernel(const uint8_t* __restri
 template <int FMT, int PMODE>
 __global__ __launch_bounds__(kThreads) void uapply_kernel(uint8_t* __restrict__ codes,
                                                           const void* __restrict__ scales, int64_t m,
-                                                          int64_t d, const uint32_t* __restrict__ hist,
+                                                          int64_t d, uint32_t keep,
+                                                          const uint32_t* __restrict__ hist,
                                                           const uint32_t* __restrict__ tie_counts,
                                                           uint8_t* __restrict__ keep_mask,
                                                           uint8_t* __restrict__ frag,
@@ -479,7 +483,7 @@ __global__ __launch_bounds__(kThreads) void uapply_kernel(uint8_t* __restrict__ 
   __shared__ uint32_t lh[kUHist];
   __shared__ uint32_t ch[4];
   __shared__ uint32_t wsum[kThreads / 64];
-  load_choice(hist, lh, (uint32_t)(m * d / 2), true, wsum, ch);
+  load_choice(hist, lh, keep, true, wsum, ch);
   const uint32_t T = ch[2], krem = ch[3];
   // ties kept by earlier workgroups
   uint32_t before = 0;
@@ -575,7 +579,7 @@ void carve_select_ws(void* base, int sparsity, int fmt, int64_t m, int64_t d, Se
   }
 }
 
-void launch_select(int fmt, int sparsity, int64_t m, int64_t d, uint8_t* qr_codes,
+void launch_select(int fmt, int sparsity, int64_t m, int64_t d, int64_t keep, uint8_t* qr_codes,
                    const void* qr_scales, const double* partials, uint8_t* keep_mask,
                    uint8_t* group_mask, const SelectWs& ws, hipStream_t s) {
   if (m == 0 || d == 0) return;
@@ -585,7 +589,7 @@ void launch_select(int fmt, int sparsity, int64_t m, int64_t d, uint8_t* qr_code
     if (fmt == 0) hipLaunchKernelGGL((channel_keys_kernel<0>), g, dim3(kChanThreads), 0, s, qr_codes, qr_scales, m, d, ws.keys);
     else hipLaunchKernelGGL((channel_keys_kernel<1>), g, dim3(kChanThreads), 0, s, qr_codes, qr_scales, m, d, ws.keys);
     hipLaunchKernelGGL(select_top_kernel, dim3(1), dim3(kSelThreads), 0, s,
-                       (const uint64_t*)ws.keys, d, d / 2, ws.group_bits, group_mask);
+                       (const uint64_t*)ws.keys, d, keep, ws.group_bits, group_mask);
     hipLaunchKernelGGL((apply_groups_kernel<0>), gw, dim3(kThreads), 0, s,
                        (uint32_t*)qr_codes, m, d, (const uint8_t*)ws.group_bits, keep_mask);
   } else if (sparsity == 4) {
@@ -594,25 +598,26 @@ void launch_select(int fmt, int sparsity, int64_t m, int64_t d, uint8_t* qr_code
     if (fmt == 0) hipLaunchKernelGGL((block_keys_kernel<0>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
     else hipLaunchKernelGGL((block_keys_kernel<1>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
     hipLaunchKernelGGL(select_top_kernel, dim3(1), dim3(kSelThreads), 0, s,
-                       (const uint64_t*)ws.keys, nb, nb / 2, ws.group_bits, group_mask);
+                       (const uint64_t*)ws.keys, nb, keep, ws.group_bits, group_mask);
     hipLaunchKernelGGL((apply_groups_kernel<1>), gw, dim3(kThreads), 0, s,
                        (uint32_t*)qr_codes, m, d, (const uint8_t*)ws.group_bits, keep_mask);
   } else if (sparsity == 5) {
     const unsigned nwg = (unsigned)unstructured_wgs(m, d);
     hipLaunchKernelGGL(uzero_kernel, dim3(1), dim3(kThreads), 0, s, ws.hist);
+    const uint32_t k = (uint32_t)keep;
 #define RESQ_U(F)                                                                                          \
-    hipLaunchKernelGGL((uhist_kernel<F, 0>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, ws.hist);   \
-    hipLaunchKernelGGL((uhist_kernel<F, 1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, ws.hist);   \
-    hipLaunchKernelGGL((uties_kernel<F>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d,                 \
+    hipLaunchKernelGGL((uhist_kernel<F, 0>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k, ws.hist); \
+    hipLaunchKernelGGL((uhist_kernel<F, 1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k, ws.hist); \
+    hipLaunchKernelGGL((uties_kernel<F>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k,              \
                        (const uint32_t*)ws.hist, ws.tie_counts);                                                      \
-    hipLaunchKernelGGL((uapply_kernel<F, -1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d,            \
+    hipLaunchKernelGGL((uapply_kernel<F, -1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k,         \
                        (const uint32_t*)ws.hist, (const uint32_t*)ws.tie_counts, keep_mask, nullptr, nullptr);
     if (fmt == 0) { RESQ_U(0) } else { RESQ_U(1) }
 #undef RESQ_U
   }
 }
 
-void launch_select_frag(int fmt, int sparsity, int64_t m, int64_t d, uint8_t* qr_codes,
+void launch_select_frag(int fmt, int sparsity, int64_t m, int64_t d, int64_t keep, uint8_t* qr_codes,
                         const void* qr_scales, const double* partials, const SelectWs& ws,
                         int pack_mode, uint8_t* frag, uint8_t* fscale, hipStream_t s) {
   if (m == 0 || d == 0) return;
@@ -628,17 +633,18 @@ void launch_select_frag(int fmt, int sparsity, int64_t m, int64_t d, uint8_t* qr
       if (fmt == 0) hipLaunchKernelGGL((block_keys_kernel<0>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
       else hipLaunchKernelGGL((block_keys_kernel<1>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
     }
-    hipLaunchKernelGGL(select_top_kernel, dim3(1), dim3(kSelThreads), 0, s, (const uint64_t*)ws.keys, n, n / 2,
+    hipLaunchKernelGGL(select_top_kernel, dim3(1), dim3(kSelThreads), 0, s, (const uint64_t*)ws.keys, n, keep,
                        ws.group_bits, (uint8_t*)nullptr);
     launch_pack(pack_mode, qr_codes, qr_scales, m, d, frag, fscale, s, chan ? 1 : 2, ws.group_bits);
   } else if (sparsity == 5) {
     const unsigned nwg = (unsigned)unstructured_wgs(m, d);  // the histogram was cleared by the residual pass
+    const uint32_t k = (uint32_t)keep;
 #define RESQ_UF(F, P)                                                                                      \
-    hipLaunchKernelGGL((uhist_kernel<F, 0>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, ws.hist);   \
-    hipLaunchKernelGGL((uhist_kernel<F, 1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, ws.hist);   \
-    hipLaunchKernelGGL((uties_kernel<F>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d,                 \
+    hipLaunchKernelGGL((uhist_kernel<F, 0>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k, ws.hist); \
+    hipLaunchKernelGGL((uhist_kernel<F, 1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k, ws.hist); \
+    hipLaunchKernelGGL((uties_kernel<F>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k,              \
                        (const uint32_t*)ws.hist, ws.tie_counts);                                                      \
-    hipLaunchKernelGGL((uapply_kernel<F, P>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d,             \
+    hipLaunchKernelGGL((uapply_kernel<F, P>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k,          \
                        (const uint32_t*)ws.hist, (const uint32_t*)ws.tie_counts, (uint8_t*)nullptr, frag, fscale);
     if (fmt == 0) { RESQ_UF(0, kPackMx) } else { RESQ_UF(1, kPackHiA) }
 #undef RESQ_UF

@@ -28,6 +28,47 @@ FORMATS = {"mxfp4": MXFP4, "hif4": HIF4}
 S_NONE, S_IDENTITY, S_2_4, S_CHANNEL50, S_BLOCK32X64_50, S_UNSTRUCT50 = range(6)
 SPARSITY = {"none": S_NONE, "identity": S_IDENTITY, "2:4": S_2_4, "channel50": S_CHANNEL50,
             "block32x64_50": S_BLOCK32X64_50, "unstructured50": S_UNSTRUCT50}
+
+
+# Other levels and k:g patterns (the RESQ_S_NM / _CHANNEL / _BLOCK32X64 / _UNSTRUCT codes).
+def S_NM(k, g):
+    return 0x100 | (k << 4) | g
+
+
+def S_CHANNEL(p):
+    return 0x200 | p
+
+
+def S_BLOCK32X64(p):
+    return 0x300 | p
+
+
+def S_UNSTRUCT(p):
+    return 0x400 | p
+
+
+def sparsity_code(name: str) -> int:
+    """Library code of a sparsity name: the six names of SPARSITY, "k:g" (keep k of every g
+    along d), "channel<p>", "block32x64_<p>" or "unstructured<p>" (keep p percent)."""
+    if name in SPARSITY:
+        return SPARSITY[name]
+    if ":" in name:
+        k, g = (int(v) for v in name.split(":"))
+        return S_NM(k, g)
+    for prefix, code in (("channel", S_CHANNEL), ("block32x64_", S_BLOCK32X64),
+                         ("unstructured", S_UNSTRUCT)):
+        if name.startswith(prefix) and name[len(prefix):].isdigit():
+            return code(int(name[len(prefix):]))
+    raise ValueError(f"unknown sparsity {name!r}")
+
+
+def sparsity_family(code: int) -> str:
+    """"none", "identity", "local", "channel", "block" or "unstructured" for a library code."""
+    fam = {S_NONE: "none", S_IDENTITY: "identity", S_2_4: "local", S_CHANNEL50: "channel",
+           S_BLOCK32X64_50: "block", S_UNSTRUCT50: "unstructured"}
+    if code in fam:
+        return fam[code]
+    return {1: "local", 2: "channel", 3: "block", 4: "unstructured"}.get(code >> 8, "invalid")
 OK, ERR_ARG, ERR_SHAPE, ERR_UNSUPPORTED, ERR_HIP, ERR_WORKSPACE = 0, -1, -2, -3, -4, -5
 IN_BF16, IN_F32 = 0, 1
 OP_RESIDUAL_SPARSIFY, OP_LINEAR_FWD, OP_LINEAR_BWD, OP_LINEAR_FWD_PREPARED = 0, 1, 2, 3
@@ -166,7 +207,7 @@ def _fmt(fmt) -> int:
 
 
 def _sp(sp) -> int:
-    return SPARSITY[sp] if isinstance(sp, str) else int(sp)
+    return sparsity_code(sp) if isinstance(sp, str) else int(sp)
 
 
 def _p(t) -> int:
@@ -232,13 +273,14 @@ def residual_sparsify(x, fmt, sparsity, stream=None):
         "qx_codes": torch.empty((m, d // 2), dtype=torch.uint8, device=x.device),
         "qx_scales": _empty_scales(f, m, d, x.device),
     }
+    fam = sparsity_family(sp)
     if sp != S_NONE:
         out["qr_codes"] = torch.empty((m, d // 2), dtype=torch.uint8, device=x.device)
         out["qr_scales"] = _empty_scales(f, m, d, x.device)
         out["keep_mask"] = torch.empty((m, d // 8), dtype=torch.uint8, device=x.device)
-    if sp == S_CHANNEL50:
+    if fam == "channel":
         out["group_mask"] = torch.zeros(((d + 7) // 8,), dtype=torch.uint8, device=x.device)
-    elif sp == S_BLOCK32X64_50:
+    elif fam == "block":
         nblk = ((m + 31) // 32) * (d // 64)
         out["group_mask"] = torch.zeros(((nblk + 7) // 8,), dtype=torch.uint8, device=x.device)
     ws, nb = workspace(OP_RESIDUAL_SPARSIFY, f, sp, m, d, 0, x.device)

@@ -65,6 +65,35 @@ def test_residual_sparsify_rejects_bad_arguments(fmt, sp, m, d, ldx, code):
     assert P.resq_residual_sparsify(fmt, sp, 0, m, d, ldx, 0, 0, 0, 0, 0, 0, 0, 0, 0) == code
 
 
+@pytest.mark.parametrize("sp", [B.S_NM(0, 4), B.S_NM(4, 4), B.S_NM(2, 6), B.S_NM(8, 8),
+                                B.S_CHANNEL(0), B.S_CHANNEL(100), B.S_BLOCK32X64(0),
+                                B.S_UNSTRUCT(100), 0x500 | 50, 6, -1])
+def test_invalid_sparsity_codes_are_rejected(sp):
+    ptr = 1 << 20  # never dereferenced: the code is checked before anything else
+    assert P.resq_residual_sparsify(B.MXFP4, sp, ptr, 4, 64, 64, ptr, ptr, ptr, ptr, 0, 0, 0, 0, 0) == B.ERR_ARG
+    assert "sparsity" in P.resq_last_error()
+    assert P.resq_workspace_size(B.OP_LINEAR_FWD_PREPARED, B.MXFP4, sp, 4, 64, 64) == 0
+
+
+def test_parametric_codes_match_the_fifty_percent_kinds():
+    """The parametric codes name the same functions: the 50% levels need the workspace of the
+    50% kinds, other levels of a family the same, and the local patterns none for selection."""
+    for op in (B.OP_RESIDUAL_SPARSIFY, B.OP_LINEAR_FWD_PREPARED):
+        for kind, code in ((B.S_CHANNEL50, B.S_CHANNEL), (B.S_BLOCK32X64_50, B.S_BLOCK32X64),
+                           (B.S_UNSTRUCT50, B.S_UNSTRUCT)):
+            want = P.resq_workspace_size(op, B.HIF4, kind, 100, 2048, 256)
+            assert want > 0
+            for p in (1, 50, 99):
+                assert P.resq_workspace_size(op, B.HIF4, code(p), 100, 2048, 256) == want
+        want = P.resq_workspace_size(op, B.HIF4, B.S_2_4, 100, 2048, 256)
+        for k, g in ((1, 4), (2, 4), (3, 4), (1, 8), (7, 8)):
+            assert P.resq_workspace_size(op, B.HIF4, B.S_NM(k, g), 100, 2048, 256) == want
+    assert B.sparsity_code("2:4") == B.S_2_4 and B.sparsity_code("3:8") == B.S_NM(3, 8)
+    assert B.sparsity_code("channel25") == B.S_CHANNEL(25)
+    assert B.sparsity_code("block32x64_75") == B.S_BLOCK32X64(75)
+    assert B.sparsity_code("unstructured10") == B.S_UNSTRUCT(10)
+
+
 def test_linear_fwd_rejects_bad_arguments():
     # ldy < n
     assert P.resq_linear_fwd(0, 2, 16, 4, 64, 64, 16, 16, 8, 16, 4, 0, 0, 0) == B.ERR_ARG

@@ -133,15 +133,81 @@ def test_unstructured50_brute_force_and_invariants():
         assert set(np.nonzero(keep.ravel())[0]) == _brute_top_half(flat)
 
 
+@pytest.mark.parametrize("k,g", [(1, 4), (3, 4), (1, 8), (2, 8), (4, 8), (7, 8)])
+def test_keep_k_of_g_brute_force_and_invariants(k, g):
+    """S_{k:g} (Sec. 4.3 defines S_{M:N} for any M, N): the k largest |value| of every g, ties
+    to the lower index, by sorting each group."""
+    rng = np.random.default_rng(10 + 8 * k + g)
+    m, d = 13, 64
+    v = _tie_heavy(rng, m, d)
+    keep = Q.keep_k_of_g(v, k, g)
+    assert (keep.reshape(m, d // g, g).sum(-1) == k).all()
+    for i in range(m):
+        for q in range(d // g):
+            grp = [(-abs(v[i, g * q + t]), t) for t in range(g)]
+            want = {t for _, t in sorted(grp)[:k]}
+            assert {t for t in range(g) if keep[i, g * q + t]} == want
+
+
+def _brute_top(keys, pct):
+    order = sorted(range(len(keys)), key=lambda i: (-keys[i], i))
+    return set(order[: len(keys) * pct // 100])
+
+
+@pytest.mark.parametrize("pct", [1, 25, 30, 75, 99])
+def test_global_levels_brute_force_and_nesting(pct):
+    """S_alpha% over channels, 32 x 64 blocks and elements for alpha != 50: floor(count *
+    alpha / 100) kept by a full sort; a higher level keeps a superset."""
+    rng = np.random.default_rng(pct)
+    m, d = 70, 192
+    v = _tie_heavy(rng, m, d)
+    keep, ch = Q.keep_channel(v, pct)
+    keys = [math.fsum(float(t) ** 2 for t in v[:, j]) for j in range(d)]
+    assert set(np.nonzero(ch)[0]) == _brute_top(keys, pct) and ch.sum() == d * pct // 100
+    assert (keep == ch[None, :]).all()
+    keep, blk = Q.keep_block(v, "hif4", pct)
+    nI, nJ = (m + 31) // 32, d // 64
+    bkeys = [math.fsum(float(t) ** 2 for t in v[32 * I:32 * I + 32, 64 * J:64 * J + 64].ravel())
+             for I in range(nI) for J in range(nJ)]
+    assert set(np.nonzero(blk.ravel())[0]) == _brute_top(bkeys, pct)
+    keep = Q.keep_unstructured(v, pct)
+    flat = [abs(t) for t in v.ravel()]
+    assert set(np.nonzero(keep.ravel())[0]) == _brute_top(flat, pct)
+    if pct < 99:
+        assert (Q.keep_unstructured(v, pct) <= Q.keep_unstructured(v, pct + 1)).all()
+        assert (Q.keep_channel(v, pct)[1] <= Q.keep_channel(v, pct + 1)[1]).all()
+
+
+def test_levels_that_round_to_zero_keep_nothing():
+    v = _tie_heavy(np.random.default_rng(4), 3, 64)
+    assert not Q.keep_channel(v, 1)[1].any()          # floor(64 / 100) = 0
+    assert not Q.keep_block(v, "mxfp4", 99)[1].any()  # one block: floor(99 / 100) = 0
+    assert Q.keep_unstructured(v, 1).sum() == 1       # floor(192 / 100) = 1: the largest |value|
+
+
+def test_sparsity_names():
+    assert Q.parse_sparsity("2:4") == ("local", (2, 4))
+    assert Q.parse_sparsity("4:8") == ("local", (4, 8))
+    assert Q.parse_sparsity("channel25") == ("channel", 25)
+    assert Q.parse_sparsity("block32x64_75") == ("block", 75)
+    assert Q.parse_sparsity("unstructured50") == ("unstructured", 50)
+    for bad in ("0:4", "4:4", "2:6", "channel0", "channel100", "block64x64_50", "dense"):
+        with pytest.raises(ValueError):
+            Q.parse_sparsity(bad)
+    assert Q.flops_resq(2, 8, 4, "1:4") == 2 * 2 * 8 * 4 + 2 * 8 * 4 // 2
+    assert Q.flops_resq(2, 8, 4, "unstructured75") == 2 * 2 * 8 * 4 + 3 * 2 * 8 * 4 // 2
+
+
 @pytest.mark.parametrize("fmt", F.FORMATS)
-@pytest.mark.parametrize("sp", ["2:4", "channel50", "block32x64_50", "unstructured50"])
+@pytest.mark.parametrize("sp", ["2:4", "channel50", "block32x64_50", "unstructured50", "1:4",
+                                "4:8", "channel25", "block32x64_75", "unstructured30"])
 def test_sparsify_zeroes_pruned_codes_and_keeps_scales(fmt, sp):
     x = _outlier_x(64, 256, seed=5)
     out = Q.resq_quantize_residual(fmt, sp, x)
     dense, kept, keep = out["qr_codes_dense"], out["qr_codes"], out["keep"]
     assert (kept[~keep] == 0).all()
     assert np.array_equal(kept[keep], dense[keep])
-    assert abs(keep.mean() - 0.5) < 0.02
+    assert abs(keep.mean() - Q.kept_fraction(sp)) < 0.02
 
 
 # ----------------------------------------------------------------------------------------
