@@ -70,7 +70,7 @@ typedef enum {
 /*
  * Other levels and N:M patterns of the same sparsity functions.  Sec. 4.3 defines the
  * semi-structured pattern for any M:N and the channel and block patterns for any kept
- * fraction alpha; the paper evaluates 50% only and leaves other levels open (Sec. 7).  These
+ * fraction alpha; the paper evaluates 50% only and leaves other levels open (Sec. 6).  These
  * codes are accepted wherever a sparsity argument is:
  *   RESQ_S_NM(k, g)       keep the k largest |values| of every g consecutive elements along d;
  *                         g = 4 or 8, 1 <= k < g; d must be a multiple of g.

@@ -19,7 +19,7 @@ Readings of points the paper leaves open (also listed in the design notes):
   S4  ranking uses the sum of squares (same order as the L2 norm); ties go to the lowest
       index; floor(count / 2) items are kept.
   S6  other levels and patterns (Sec. 4.3 defines S_alpha%, S_{M:N} and S^{MxN}_alpha% for
-      any alpha, M, N; Sec. 7 leaves levels other than 50% open): alpha is the kept percent,
+      any alpha, M, N; Sec. 6 leaves levels other than 50% open): alpha is the kept percent,
       floor(count * alpha / 100) items are kept, with the ranking and ties of S4; "k:g" keeps
       the k largest of every g consecutive elements along d (ties to the lower index).
   S5  sums of squares are float64 in a fixed order (stated at each function), so near-ties

@@ -1,6 +1,6 @@
 """GPU <-> oracle parity of the other levels and k:g patterns of the residual sparsity
 functions.  Sec. 4.3 defines S_{M:N}, S_alpha% and S^{MxN}_alpha% for any level; the paper's
-experiments use 50% only and Sec. 7 leaves other levels open.  Covered here: the local S_k:4
+experiments use 50% only and Sec. 6 leaves other levels open.  Covered here: the local S_k:4
 and S_k:8 patterns applied inside the residual pass (both output layouts), and the channel,
 32 x 64 block and element-wise selections at levels other than 50%.  Codes and masks must be
 bit-identical to the oracle's, ties included; Y must match within the float32 tolerance."""
