@@ -148,6 +148,88 @@ def cpu_baseline(wl, fmt, sp, n_sample, n_rows, min_seconds):
     }
 
 
+def bench_diagnostics(args, P, torch, np, wl, fmt, dev, sptr):
+    """--op diagnostics: resq_diagnostics (the Figs. 2-4 statistics) over every linear's input
+    X of the workload; algorithmic bytes = X read once (2 B per element)."""
+    from synth import workload_tensors
+    f = P.FORMATS[fmt]
+    per_copy = sum(2 * wl.m * l.d for l in wl.linears)
+    copies = int(min(64, max(2, -(-2 * LLC_BYTES // per_copy) + 1)))
+    ws_bytes = max(P.resq_workspace_size(P.OP_DIAGNOSTICS, f, 0, wl.m, l.d, 0) for l in wl.linears)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    stats = torch.empty(len(P.DIAG_STATS), dtype=torch.float64, device=dev)
+    xs = []
+    for lin in wl.linears:
+        xb, _ = workload_tensors(wl, lin)
+        x0 = torch.from_numpy(xb.view(np.int16)).to(dev)
+        xs.append((lin, [x0.clone() for _ in range(copies)]))
+    lib = P.load()
+    thr = args.outlier_threshold
+
+    def step(i):
+        for lin, xc in xs:
+            rc = lib.resq_diagnostics(f, int(xc[i % copies].data_ptr()), wl.m, lin.d, lin.d, thr,
+                                      int(stats.data_ptr()), int(ws.data_ptr()), ws_bytes, sptr)
+            if rc != 0:
+                raise P.ResqError(f"resq_diagnostics: {P.resq_last_error()}", rc)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    P.resq_profile_enable(True)
+    P.resq_profile_reset()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    n_launch, k_ms = P.resq_profile_read("diagnostics")
+    P.resq_profile_enable(False)
+    nbytes = per_copy
+    launch_s = k_ms / n_launch * 1e-3
+    achieved = nbytes / len(wl.linears) / launch_s / 1e9
+    out = {
+        "metric": "Figs. 2-4 activation statistics pass (zeros, outlier blocks, S_2:4 error), GB/s of X",
+        "value": round(nbytes * args.steps / dt / 1e9, 1),
+        "unit": "GB/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(dt * 1e3 / args.steps, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "fp4", "data": "synthetic",
+        "config": {"workload": wl.name, "format": fmt, "op": "diagnostics", "m": wl.m,
+                   "inputs": {l.name: [wl.m, l.d] for l in wl.linears},
+                   "outlier_threshold": thr, "copies_rotated": copies},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": f"diag_kernel + diag_finish_kernel ({len(wl.linears)} calls per step)",
+                     "alg_bytes_per_launch": round(nbytes / len(wl.linears)),
+                     "avg_launch_us": round(launch_s * 1e6, 2)},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import diagnostics as OD
+        from synth import bf16_bits_to_f32
+        rows = min(wl.m, args.cpu_sample_rows)
+        xs_cpu = [bf16_bits_to_f32(workload_tensors(wl, l, m=rows)[0]) for l in wl.linears]
+        t0, reps, nb = time.perf_counter(), 0, 0
+        while True:
+            for x in xs_cpu:
+                OD.diagnostics(fmt, x, thr)
+                nb += 2 * x.size
+            reps += 1
+            if time.perf_counter() - t0 >= args.cpu_seconds:
+                break
+        cdt = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": round(nb / cdt / 1e9, 4), "unit": "GB/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": f"{wl.name}: the first {rows} rows of every linear's X, "
+                                         f"{reps} repetition(s), {cdt:.1f} s, numpy (single-threaded)"}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def setup_forward(P, torch, np, wl, fmt, sp, dev, sptr, out="f32"):
     """Inputs resident in HBM (enough rotating copies to defeat the last-level cache) and a
     step function running every linear of the workload through resq_linear_fwd_prepared
@@ -227,6 +309,10 @@ def main() -> int:
     ap.add_argument("--workload", default="qwen3b_layer_m256")
     ap.add_argument("--format", default="hif4", choices=["hif4", "mxfp4"])
     ap.add_argument("--sparsity", default="2:4")
+    ap.add_argument("--op", default="linear", choices=["linear", "diagnostics"],
+                    help="linear: the ResQ layer step; diagnostics: the Figs. 2-4 statistics pass")
+    ap.add_argument("--outlier-threshold", type=float, default=10.0,
+                    help="--op diagnostics: |x| above which a block counts as holding an outlier")
     ap.add_argument("--out", default="f32", choices=["f32", "bf16"],
                     help="forward output type: float32, or its bf16 rounding written by the GEMM")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -266,6 +352,11 @@ def main() -> int:
     sptr = int(torch.cuda.current_stream().cuda_stream)
     wl = WORKLOADS[args.workload]
     fmt = args.format
+    if args.op == "diagnostics":
+        if wl.backward:
+            print("bench.py: --op diagnostics needs a forward workload", file=sys.stderr)
+            return 2
+        return bench_diagnostics(args, P, torch, np, wl, args.format, dev, sptr)
     sp = "none" if wl.backward else args.sparsity
     out_t = "f32" if wl.backward else args.out
     y_bytes = 4 if out_t == "f32" else 2

@@ -102,7 +102,8 @@ typedef enum {
   RESQ_OP_RESIDUAL_SPARSIFY = 0,
   RESQ_OP_LINEAR_FWD = 1,
   RESQ_OP_LINEAR_BWD = 2,
-  RESQ_OP_LINEAR_FWD_PREPARED = 3
+  RESQ_OP_LINEAR_FWD_PREPARED = 3,
+  RESQ_OP_DIAGNOSTICS = 4
 } resq_op;
 
 /*
@@ -209,6 +210,29 @@ int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uin
                     int64_t m, int64_t d, int64_t n, float* dX, float* dW, void* workspace,
                     size_t workspace_bytes, void* stream);
 
+/*
+ * resq_diagnostics - the activation statistics behind Figs. 2-4 (Sec. 4.2: zero values before
+ * and after quantization, blocks holding outliers; Sec. 4.3: the error S_2:4 causes on Q(X)
+ * and on Q(dX)) for one activation tensor X (m x d bf16, row stride ldx) and one format:
+ *   stats[0] m * d                      stats[1] zeros of X (+0 or -0)
+ *   stats[2] zeros of Q(X) (dequantized value 0, either sign)
+ *   stats[3] quantization blocks, m * d / B (B = 32 MXFP4, 64 HiF4)
+ *   stats[4] blocks holding some |x| > outlier_threshold (compared in float32; the paper
+ *            does not define an outlier, so the threshold is the caller's)
+ *   stats[5] sum of Q(X)^2              stats[6] sum of the squares S_2:4 prunes from Q(X)
+ *   stats[7] sum of Q(dX)^2             stats[8] sum of the squares S_2:4 prunes from Q(dX)
+ * The MSE of S_2:4 on Q(X) is stats[6] / stats[0] (on Q(dX) stats[8] / stats[0]); the RMSE is
+ * its square root.  S_2:4 is the function RESQ_S_2_4 applies.
+ * stats     : output, device buffer of RESQ_DIAG_STATS doubles.  Counts are exact; the sums
+ *             are float64 additions of exact squares in a fixed order (the same on every run).
+ * d must be a multiple of B.  Workspace: resq_workspace_size(RESQ_OP_DIAGNOSTICS, format,
+ * 0, m, d, 0) bytes (256-byte aligned).
+ */
+#define RESQ_DIAG_STATS 9
+int resq_diagnostics(int format, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
+                     float outlier_threshold, double* stats, void* workspace,
+                     size_t workspace_bytes, void* stream);
+
 /* Workspace bytes needed by `op` (a resq_op) for these arguments; 0 on bad arguments. */
 size_t resq_workspace_size(int op, int format, int sparsity, int64_t m, int64_t d, int64_t n);
 
@@ -223,7 +247,7 @@ const char* resq_version(void);
  * enqueues is bracketed by two HIP events recorded on the same stream (event objects are
  * host-side handles; no device memory is allocated).  resq_profile_read synchronizes the
  * recorded events and returns, for the kernel family `name` ("residual", "quant_rows",
- * "quant_cols", "pack_hif4", "select", "gemm"), the number of launches and their summed
+ * "quant_cols", "pack_hif4", "select", "gemm", "diagnostics"), the number of launches and their summed
  * duration in milliseconds since the last reset.  Returns RESQ_ERR_ARG for an unknown name.
  */
 int resq_profile_enable(int on);

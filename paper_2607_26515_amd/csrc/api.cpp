@@ -317,6 +317,7 @@ size_t resq_workspace_size(int op, int format, int sparsity, int64_t m, int64_t 
       return carve_fwd(nullptr, format, sp, m, d, n, nullptr) + prepared_bytes(format, n, d);
     case RESQ_OP_LINEAR_FWD_PREPARED: return carve_fwd(nullptr, format, sp, m, d, n, nullptr);
     case RESQ_OP_LINEAR_BWD: return carve_bwd(nullptr, format, m, d, n, nullptr);
+    case RESQ_OP_DIAGNOSTICS: return resq::diag_ws_bytes(m, d);
     default: return 0;
   }
 }
@@ -482,6 +483,27 @@ int resq_linear_fwd(int format, int sparsity, const uint16_t* X, int64_t m, int6
     resq::launch_pack(b_pack_mode(format), qw_codes, qw_scales, n, d, (uint8_t*)frag, (uint8_t*)fsc, s);
   }
   return linear_fwd_core(format, sp, X, m, d, ldx, wprep, n, Y, ldy, false, w, s);
+}
+
+int resq_diagnostics(int format, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
+                     float outlier_threshold, double* stats, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+  if (!valid_format(format)) return fail(RESQ_ERR_ARG, "unknown format %d", format);
+  if (m < 0 || d < 0) return fail(RESQ_ERR_ARG, "negative size (m=%lld, d=%lld)", (long long)m, (long long)d);
+  if (ldx < d) return fail(RESQ_ERR_ARG, "ldx (%lld) < d (%lld)", (long long)ldx, (long long)d);
+  if (d % block_of(format) != 0)
+    return fail(RESQ_ERR_SHAPE, "d (%lld) is not a multiple of the block size %lld", (long long)d, (long long)block_of(format));
+  if (!stats) return fail(RESQ_ERR_ARG, "stats is NULL");
+  if (m > 0 && d > 0 && !X) return fail(RESQ_ERR_ARG, "X is NULL");
+  if ((uintptr_t)stats % 8 != 0) return fail(RESQ_ERR_ARG, "stats must be 8-byte aligned");
+  int rc = check_ws(workspace, workspace_bytes, resq::diag_ws_bytes(m, d));
+  if (rc != RESQ_OK) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  {
+    resq::ProfScope prof_(resq::kProfDiag, s);
+    resq::launch_diagnostics(format, X, m, d, ldx, outlier_threshold, stats, (double*)workspace, s);
+  }
+  return check_launch("resq_diagnostics");
 }
 
 int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uint16_t* W,

@@ -110,4 +110,10 @@ size_t gemm_split_scratch(int fmt, int64_t M, int64_t N, int64_t K);
 // scales, each 256-byte aligned) and the B buffer fit 32-bit offsets.
 bool gemm_supported(int fmt, int64_t M, int64_t N, int64_t K, int n_terms);
 
+// Activation statistics (diag.hip): stats receives 9 doubles (see resq_diagnostics);
+// partials is diag_ws_bytes(m, d) bytes of scratch.
+size_t diag_ws_bytes(int64_t m, int64_t d);
+void launch_diagnostics(int fmt, const uint16_t* X, int64_t m, int64_t d, int64_t ldx, float thr,
+                        double* stats, double* partials, hipStream_t s);
+
 }  // namespace resq

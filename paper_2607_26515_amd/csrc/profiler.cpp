@@ -46,7 +46,8 @@ void fold_locked() {
   g_recs.clear();
 }
 
-const char* kNames[kProfCount] = {"residual", "quant_rows", "quant_cols", "pack_hif4", "select", "gemm"};
+const char* kNames[kProfCount] = {"residual", "quant_rows", "quant_cols", "pack_hif4", "select", "gemm",
+                                  "diagnostics"};
 
 }  // namespace
 

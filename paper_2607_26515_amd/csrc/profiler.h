@@ -5,7 +5,10 @@
 
 namespace resq {
 
-enum ProfKernel { kProfResidual = 0, kProfQuantRows, kProfQuantCols, kProfPack, kProfSelect, kProfGemm, kProfCount };
+enum ProfKernel {
+  kProfResidual = 0, kProfQuantRows, kProfQuantCols, kProfPack, kProfSelect, kProfGemm, kProfDiag,
+  kProfCount
+};
 
 // Returns a token for prof_end (negative when profiling is off).
 int prof_begin(int kernel, hipStream_t s);

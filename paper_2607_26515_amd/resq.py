@@ -71,12 +71,15 @@ def sparsity_family(code: int) -> str:
     return {1: "local", 2: "channel", 3: "block", 4: "unstructured"}.get(code >> 8, "invalid")
 OK, ERR_ARG, ERR_SHAPE, ERR_UNSUPPORTED, ERR_HIP, ERR_WORKSPACE = 0, -1, -2, -3, -4, -5
 IN_BF16, IN_F32 = 0, 1
-OP_RESIDUAL_SPARSIFY, OP_LINEAR_FWD, OP_LINEAR_BWD, OP_LINEAR_FWD_PREPARED = 0, 1, 2, 3
+OP_RESIDUAL_SPARSIFY, OP_LINEAR_FWD, OP_LINEAR_BWD, OP_LINEAR_FWD_PREPARED, OP_DIAGNOSTICS = 0, 1, 2, 3, 4
+DIAG_STATS = ("elements", "zeros_x", "zeros_qx", "blocks", "outlier_blocks", "energy_qx",
+              "sse24_qx", "energy_qr", "sse24_qr")
 
 EXPORTED = ("resq_quantize", "resq_residual_sparsify", "resq_linear_fwd", "resq_linear_bwd",
             "resq_workspace_size", "resq_last_error", "resq_version", "resq_profile_enable",
             "resq_profile_reset", "resq_profile_read", "resq_prepared_weights_size",
-            "resq_prepare_weights", "resq_linear_fwd_prepared", "resq_linear_fwd_prepared_bf16")
+            "resq_prepare_weights", "resq_linear_fwd_prepared", "resq_linear_fwd_prepared_bf16",
+            "resq_diagnostics")
 
 
 class ResqError(RuntimeError):
@@ -111,6 +114,8 @@ def load() -> ctypes.CDLL:
     lib.resq_linear_fwd_prepared.restype = i32
     lib.resq_linear_fwd_prepared_bf16.argtypes = [i32, i32, vp, i64, i64, i64, vp, i64, vp, i64, vp, sz, vp]
     lib.resq_linear_fwd_prepared_bf16.restype = i32
+    lib.resq_diagnostics.argtypes = [i32, vp, i64, i64, i64, ctypes.c_float, vp, vp, sz, vp]
+    lib.resq_diagnostics.restype = i32
     for f in ("resq_quantize", "resq_residual_sparsify", "resq_linear_fwd", "resq_linear_bwd"):
         getattr(lib, f).restype = i32
     lib.resq_workspace_size.restype = sz
@@ -168,6 +173,12 @@ def resq_linear_fwd_prepared_bf16(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy,
                                   workspace_bytes, stream=0) -> int:
     return load().resq_linear_fwd_prepared_bf16(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy,
                                                 workspace, workspace_bytes, stream)
+
+
+def resq_diagnostics(fmt, X, m, d, ldx, outlier_threshold, stats, workspace, workspace_bytes,
+                     stream=0) -> int:
+    return load().resq_diagnostics(fmt, X, m, d, ldx, outlier_threshold, stats, workspace,
+                                   workspace_bytes, stream)
 
 
 def resq_workspace_size(op, fmt, sparsity, m, d, n) -> int:
@@ -357,3 +368,17 @@ def linear_bwd(dy, x, w, fmt, want_dx=True, want_dw=True, ws=None, stream=None):
                          _stream(stream))
     _check(rc, "resq_linear_bwd")
     return dx, dw
+
+
+def diagnostics(x, fmt, outlier_threshold, stream=None):
+    """The Figs. 2-4 statistics of activations x (m x d bf16) as a float64 device tensor of
+    len(DIAG_STATS) values, in the order of DIAG_STATS."""
+    import torch
+    m, d = x.shape
+    f = _fmt(fmt)
+    stats = torch.empty(len(DIAG_STATS), dtype=torch.float64, device=x.device)
+    ws, nb = workspace(OP_DIAGNOSTICS, f, S_NONE, m, d, 0, x.device)
+    rc = resq_diagnostics(f, _p(x), m, d, x.stride(0), float(outlier_threshold), _p(stats), _p(ws),
+                          nb, _stream(stream))
+    _check(rc, "resq_diagnostics")
+    return stats

@@ -122,3 +122,16 @@ def test_workspace_sizes_grow_with_shape():
     assert 0 < a < b
     assert P.resq_workspace_size(9, 0, 0, 1, 64, 1) == 0
     assert P.resq_workspace_size(B.OP_LINEAR_BWD, B.MXFP4, 0, 64, 64, 64) > 0
+
+
+def test_diagnostics_rejects_bad_arguments():
+    ptr = 1 << 20  # never dereferenced
+    assert P.resq_diagnostics(7, ptr, 4, 64, 64, 1.0, ptr, 0, 0, 0) == B.ERR_ARG
+    assert P.resq_diagnostics(B.HIF4, ptr, 4, 96, 96, 1.0, ptr, 0, 0, 0) == B.ERR_SHAPE
+    assert P.resq_diagnostics(B.MXFP4, ptr, 4, 64, 32, 1.0, ptr, 0, 0, 0) == B.ERR_ARG
+    assert P.resq_diagnostics(B.MXFP4, ptr, 4, 64, 64, 1.0, 0, 0, 0, 0) == B.ERR_ARG
+    assert P.resq_diagnostics(B.MXFP4, 0, 4, 64, 64, 1.0, ptr, 0, 0, 0) == B.ERR_ARG
+    need = P.resq_workspace_size(B.OP_DIAGNOSTICS, B.MXFP4, 0, 4, 64, 0)
+    assert need > 0
+    assert P.resq_diagnostics(B.MXFP4, ptr, 4, 64, 64, 1.0, ptr, 0, 0, 0) == B.ERR_WORKSPACE
+    assert P.resq_workspace_size(B.OP_DIAGNOSTICS, B.MXFP4, 0, 0, 64, 0) == 0
