@@ -29,6 +29,10 @@ Readings of points the paper leaves open (also listed in the design notes):
   Y1  Y, dX and dW are float32: the exact float64 result rounded once.
   Y2  the optional bf16 output is that float32 result rounded again, to the nearest bf16
       (ties to even): the rounding of the float32 result, not of the float64 one.
+  F1  the fused producer of the down projection's input (the SwiGLU of the gate and up
+      projections, X = silu(G) * U, silu(g) = g / (1 + exp(-g))): X is the bf16 nearest to the
+      float64 value of silu(g) * u (ties to even), rounded once, so it is the bf16 activation
+      the unfused model would hand to the linear up to that single rounding.
 """
 from __future__ import annotations
 
@@ -251,6 +255,32 @@ def round_to_bf16(y32: np.ndarray) -> np.ndarray:
     kept, dropped = u >> 16, u & 0xFFFF
     up = (dropped > 0x8000) | ((dropped == 0x8000) & ((kept & 1) == 1))
     return (kept + up).astype(np.uint16)
+
+
+def round_f64_to_bf16(v: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns of finite float64 values, nearest, ties to even, in one rounding.
+
+    The bf16 grid spacing at |v| in [2^e, 2^(e+1)) is 2^(e-7) (e >= -126; below that the
+    subnormal spacing 2^-133): v / spacing is exact in float64, rounded half to even with
+    rint, and scaled back.  Magnitudes that round past the largest finite bf16 become inf."""
+    v = np.asarray(v, dtype=np.float64)
+    a = np.abs(v)
+    e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
+    # log2 may land one off near powers of two: fix e so that 2^e <= a < 2^(e+1)
+    e = np.where(np.exp2(e) > a, e - 1, e)
+    e = np.where(np.exp2(e + 1) <= a, e + 1, e)
+    step = np.exp2(np.maximum(e, -126.0) - 7.0)
+    q = np.rint(a / step) * step
+    f32 = np.where(q > float(np.finfo(np.float32).max), np.inf, q).astype(np.float32)
+    bits = (f32.view(np.uint32) >> 16).astype(np.uint16)
+    return bits | np.where(np.signbit(v), np.uint16(0x8000), np.uint16(0))
+
+
+def swiglu_bf16(g: np.ndarray, u: np.ndarray) -> np.ndarray:
+    """X = silu(G) * U as bf16 bit patterns (reading F1): float64 value, rounded once."""
+    g = np.asarray(g, dtype=np.float64)
+    u = np.asarray(u, dtype=np.float64)
+    return round_f64_to_bf16(g / (1.0 + np.exp(-g)) * u)
 
 
 # ----------------------------------------------------------------------------------------

@@ -388,3 +388,65 @@ def test_round_to_bf16_exact_distance_and_torch():
         assert int(got[k]) == _bf16_nearest_exact(v[k]), hex(int(u[k]))
     t = torch.from_numpy(v.copy()).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
     assert np.array_equal(got, t)
+
+
+# ----------------------------------------------------------------------------------------
+# Fused producer of the down projection's input: X = silu(G) * U rounded once to bf16
+# ----------------------------------------------------------------------------------------
+def _bf16_nearest_f64_exact(v: float) -> int:
+    """Nearest bf16 to a float64 by exact rational distance over the bf16 grid (ties: even)."""
+    from fractions import Fraction
+    x = Fraction(v)
+    best = None
+    lo = int(np.float32(v).view(np.uint32)) >> 16  # a bf16 near v: search its neighbours
+    for c in range(max(lo - 2, 0) if v >= 0 else lo - 2, lo + 3):
+        c &= 0xFFFF
+        f = np.uint32(c << 16).view(np.float32)
+        if not np.isfinite(f):
+            continue
+        dist = abs(x - Fraction(float(f)))
+        key = (dist, c & 1)
+        if best is None or key < best[0]:
+            best = (key, c)
+    return best[1]
+
+
+def test_round_f64_to_bf16_exact_distance():
+    rng = np.random.default_rng(12)
+    b = rng.integers(0x0001, 0x7F7F, size=600).astype(np.uint32)
+    mids = (b << 16 | 0x8000).view(np.float32).astype(np.float64)  # exact bf16 midpoints
+    ulp = np.spacing(mids)
+    v = np.concatenate([mids, mids + ulp, mids - ulp, rng.normal(0, 1, 300) * 10.0 ** rng.integers(-30, 30, 300)])
+    v = np.concatenate([v, -v[::3]])
+    got = Q.round_f64_to_bf16(v)
+    for k in range(0, len(v), 3):
+        assert int(got[k]) == _bf16_nearest_f64_exact(float(v[k])), (v[k], hex(int(got[k])))
+    # a float32 value is rounded once either way
+    f = rng.normal(0, 1, 2000).astype(np.float32) * np.float32(3.0)
+    assert np.array_equal(Q.round_f64_to_bf16(f.astype(np.float64)), Q.round_to_bf16(f))
+    # ties go to even, in the subnormal range too
+    assert int(Q.round_f64_to_bf16(np.array([1.0 + 2.0**-8]))[0]) == 0x3F80
+    assert int(Q.round_f64_to_bf16(np.array([1.5 * 2.0**-133]))[0]) == 0x0002
+    assert int(Q.round_f64_to_bf16(np.array([-2.5 * 2.0**-133]))[0]) == 0x8002
+
+
+def test_swiglu_matches_library_sigmoid():
+    """silu(g) * u against scipy's logistic function (an independent implementation); the two
+    float64 values may differ in the last bits, which can move the bf16 result only when the
+    value sits on a rounding midpoint."""
+    from scipy.special import expit
+    rng = np.random.default_rng(13)
+    g = bf16_bits_to_f32(f32_to_bf16_bits(rng.normal(0, 3, 20000).astype(np.float32))).astype(np.float64)
+    u = bf16_bits_to_f32(f32_to_bf16_bits(rng.normal(0, 2, 20000).astype(np.float32))).astype(np.float64)
+    ref = g * expit(g) * u
+    got = Q.swiglu_bf16(g, u)
+    want = Q.round_f64_to_bf16(ref)
+    diff = np.nonzero(got != want)[0]
+    for k in diff:
+        step = np.exp2(np.floor(np.log2(abs(ref[k]))) - 7)
+        frac = abs(ref[k]) / step - np.floor(abs(ref[k]) / step)
+        assert abs(frac - 0.5) < 1e-9, (g[k], u[k])
+    assert len(diff) <= 2
+    # closed forms: silu(0) = 0; u = 0 gives a zero; silu(g) -> g for large g
+    z = Q.swiglu_bf16(np.array([0.0, 3.0, 80.0]), np.array([5.0, 0.0, 1.0]))
+    assert bf16_bits_to_f32(z[:2]).tolist() == [0.0, 0.0] and bf16_bits_to_f32(z[2:]).tolist() == [80.0]
