@@ -230,6 +230,82 @@ def bench_diagnostics(args, P, torch, np, wl, fmt, dev, sptr):
     return 0
 
 
+def bench_swiglu_down(args, P, torch, np, wl, fmt, sp, dev, sptr):
+    """--op swiglu_down: the workload's down projection with its SwiGLU input formed inside the
+    quantization pass (resq_linear_fwd_prepared_swiglu, G and U bf16), against the same linear
+    fed by a separate torch silu * mul kernel that writes X (bf16) first."""
+    from synth import activations, rng_tree, workload_tensors
+    lin = next(l for l in wl.linears if l.name == "down")
+    m, d, n = wl.m, lin.d, lin.n
+    f, s = P.FORMATS[fmt], P.sparsity_code(sp)
+    _, wb = workload_tensors(wl, lin)
+    w0 = torch.from_numpy(wb.view(np.int16)).to(dev)
+    qc, qs = P.quantize(w0, fmt, axis=1)
+    per_copy = P.resq_prepared_weights_size(f, n, d) + 2 * 2 * m * d
+    copies = int(min(32, max(2, -(-2 * LLC_BYTES // per_copy) + 1)))
+    wps = [P.prepare_weights(qc, qs, fmt) for _ in range(copies)]
+    rg, ru = rng_tree(7, 2)
+    g0 = torch.from_numpy(activations(rg, m, d, 0.01, 8.0).view(np.int16)).to(dev)
+    u0 = torch.from_numpy(activations(ru, m, d, 0.01, 30.0).view(np.int16)).to(dev)
+    gs = [g0.clone() for _ in range(copies)]
+    us = [u0.clone() for _ in range(copies)]
+    y = torch.empty((m, n), dtype=torch.float32, device=dev)
+    ws_bytes = P.resq_workspace_size(P.OP_LINEAR_FWD_PREPARED, f, s, m, d, n)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    lib = P.load()
+
+    def fused(i):
+        c = i % copies
+        rc = lib.resq_linear_fwd_prepared_swiglu(f, s, int(gs[c].data_ptr()), int(us[c].data_ptr()),
+                                                 P.IN_BF16, m, d, d, d, int(wps[c].data_ptr()), n,
+                                                 int(y.data_ptr()), n, int(ws.data_ptr()), ws_bytes, sptr)
+        if rc != 0:
+            raise P.ResqError(f"resq_linear_fwd_prepared_swiglu: {P.resq_last_error()}", rc)
+
+    def unfused(i):
+        c = i % copies
+        g, u = gs[c].view(torch.bfloat16), us[c].view(torch.bfloat16)
+        x = (torch.nn.functional.silu(g.float()) * u.float()).to(torch.bfloat16).view(torch.int16)
+        rc = lib.resq_linear_fwd_prepared(f, s, int(x.data_ptr()), m, d, d, int(wps[c].data_ptr()), n,
+                                          int(y.data_ptr()), n, int(ws.data_ptr()), ws_bytes, sptr)
+        if rc != 0:
+            raise P.ResqError(f"resq_linear_fwd_prepared: {P.resq_last_error()}", rc)
+
+    def timed(fn):
+        for i in range(args.warmup):
+            fn(i)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            fn(i)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / args.steps
+
+    t_f, t_u = timed(fused), timed(unfused)
+    P.resq_profile_enable(True)
+    P.resq_profile_reset()
+    for i in range(args.steps):
+        fused(i)
+    torch.cuda.synchronize()
+    res = P.resq_profile_read("residual")
+    P.resq_profile_enable(False)
+    flops = alg_flops(m, d, n, sp)
+    out = {
+        "metric": "ResQ down projection with the SwiGLU producer fused into its quantization pass, TFLOP/s",
+        "value": round(flops / t_f / 1e12, 3), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(t_f * 1e3, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "fp4",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "linear": f"down {d}->{n}", "m": m, "format": fmt,
+                   "sparsity": sp, "op": "swiglu_down", "inputs": "G, U bf16", "copies_rotated": copies},
+        "unfused_ms": round(t_u * 1e3, 5),
+        "speedup_vs_unfused": round(t_u / t_f, 3),
+        "fused_activation_pass_us": round(res[1] / res[0] * 1e3, 2) if res[0] else None,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def setup_forward(P, torch, np, wl, fmt, sp, dev, sptr, out="f32"):
     """Inputs resident in HBM (enough rotating copies to defeat the last-level cache) and a
     step function running every linear of the workload through resq_linear_fwd_prepared
@@ -309,8 +385,9 @@ def main() -> int:
     ap.add_argument("--workload", default="qwen3b_layer_m256")
     ap.add_argument("--format", default="hif4", choices=["hif4", "mxfp4"])
     ap.add_argument("--sparsity", default="2:4")
-    ap.add_argument("--op", default="linear", choices=["linear", "diagnostics"],
-                    help="linear: the ResQ layer step; diagnostics: the Figs. 2-4 statistics pass")
+    ap.add_argument("--op", default="linear", choices=["linear", "diagnostics", "swiglu_down"],
+                    help="linear: the ResQ layer step; diagnostics: the Figs. 2-4 statistics pass; "
+                         "swiglu_down: the down projection with its SwiGLU input fused")
     ap.add_argument("--outlier-threshold", type=float, default=10.0,
                     help="--op diagnostics: |x| above which a block counts as holding an outlier")
     ap.add_argument("--out", default="f32", choices=["f32", "bf16"],
@@ -357,6 +434,11 @@ def main() -> int:
             print("bench.py: --op diagnostics needs a forward workload", file=sys.stderr)
             return 2
         return bench_diagnostics(args, P, torch, np, wl, args.format, dev, sptr)
+    if args.op == "swiglu_down":
+        if wl.backward or not any(l.name == "down" for l in wl.linears):
+            print("bench.py: --op swiglu_down needs a forward workload with a down projection", file=sys.stderr)
+            return 2
+        return bench_swiglu_down(args, P, torch, np, wl, args.format, args.sparsity, dev, sptr)
     sp = "none" if wl.backward else args.sparsity
     out_t = "f32" if wl.backward else args.out
     y_bytes = 4 if out_t == "f32" else 2

@@ -197,6 +197,26 @@ int resq_linear_fwd_prepared_bf16(int format, int sparsity, const uint16_t* X, i
                                   size_t workspace_bytes, void* stream);
 
 /*
+ * resq_linear_fwd_prepared_swiglu - resq_linear_fwd_prepared for the down projection of a
+ * SwiGLU MLP, with the activation formed inside the quantization pass instead of being read:
+ *     X = silu(G) * U,   silu(g) = g / (1 + exp(-g)),
+ * each element the bf16 nearest to the float64 value of silu(g) * u (ties to even), i.e. the
+ * bf16 activation the unfused model hands to the linear, up to that one rounding.  X is never
+ * written to memory: the pass reads G and U, forms X, then computes Q(X), dX, Q(dX) and S as
+ * the other forward entry points do (Eq. 4).
+ * G, U      : m x d, bf16 (in_dtype = RESQ_IN_BF16) or float32 (RESQ_IN_F32), row strides
+ *             ldg, ldu >= d (for a gate/up projection output laid out [gate | up] with row
+ *             stride 2d: G = base, U = base + d, ldg = ldu = 2d); element-size aligned.
+ *             |silu(g) * u| must stay below the largest bf16 (3.39e38).
+ * wprep, n, Y, ldy, workspace (resq_workspace_size(RESQ_OP_LINEAR_FWD_PREPARED, ...)) and
+ * errors: as resq_linear_fwd_prepared; Y is float32.
+ */
+int resq_linear_fwd_prepared_swiglu(int format, int sparsity, const void* G, const void* U,
+                                    int in_dtype, int64_t m, int64_t d, int64_t ldg, int64_t ldu,
+                                    const void* wprep, int64_t n, float* Y, int64_t ldy,
+                                    void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * resq_linear_bwd - the FP4 training-policy backward GEMMs of the linear Y = X W^T:
  *     dX = Q_n(dY) Q_n(W)          (m x d, contraction over n)
  *     dW = Q_m(dY)^T Q_m(X)        (n x d, contraction over m)

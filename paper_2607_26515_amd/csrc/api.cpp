@@ -91,7 +91,8 @@ int resid_mode(const Sp& sp) {
   switch (sp.kind) {
     case RESQ_S_NONE: return resq::kResidNone;
     case RESQ_S_IDENTITY: return resq::kResidIdentity;
-    case RESQ_S_2_4: return sp.group == 8 ? resq::kResidNM8 : resq::kResidNM4;
+    case RESQ_S_2_4:
+      return sp.group == 8 ? resq::kResidNM8 : sp.keep == 2 ? resq::kResid24 : resq::kResidNM4;
     default: return resq::kResidDense;
   }
 }
@@ -377,7 +378,7 @@ namespace {
 
 int linear_fwd_core(int format, const Sp& sp, const uint16_t* X, int64_t m, int64_t d,
                     int64_t ldx, const void* wprep, int64_t n, void* Y, int64_t ldy, bool out_bf16,
-                    const ActWs& w, hipStream_t s) {
+                    const ActWs& w, hipStream_t s, const resq::Producer* prod = nullptr) {
   if (global_kind(sp)) {
     // the residual pass writes Q(X) as MFMA fragments and the dense Q(dX) K-major (the
     // selection ranks all of it); the selection then writes S(Q(dX)) as fragments
@@ -386,7 +387,8 @@ int linear_fwd_core(int format, const Sp& sp, const uint16_t* X, int64_t m, int6
       const bool elem = sp.kind == RESQ_S_UNSTRUCT50;
       resq::launch_residual(format, resq::kResidDense, X, m, d, ldx, w.frag_x, w.fsc_x, w.qr_codes,
                             w.qr_scales, nullptr, sp.kind == RESQ_S_BLOCK32X64_50 ? w.partials : nullptr,
-                            s, true, elem ? w.sel.hist : nullptr, elem ? resq::select_hist_words() : 0);
+                            s, true, elem ? w.sel.hist : nullptr, elem ? resq::select_hist_words() : 0,
+                            2, prod);
     }
     resq::ProfScope prof_(resq::kProfSelect, s);
     resq::launch_select_frag(format, sp.kind, m, d, keep_count(sp, m, d), w.qr_codes, w.qr_scales,
@@ -395,7 +397,7 @@ int linear_fwd_core(int format, const Sp& sp, const uint16_t* X, int64_t m, int6
     // local kinds: the residual pass writes the MFMA fragments directly
     resq::ProfScope prof_(resq::kProfResidual, s);
     resq::launch_residual(format, resid_mode(sp), X, m, d, ldx, w.frag_x, w.fsc_x, w.frag_r,
-                          w.fsc_r, nullptr, nullptr, s, true, nullptr, 0, sp.keep);
+                          w.fsc_r, nullptr, nullptr, s, true, nullptr, 0, sp.keep, prod);
   }
   const uint8_t* af[2] = {w.frag_x, w.frag_r};
   const uint8_t* asc[2] = {w.fsc_x, w.fsc_r};
@@ -456,6 +458,31 @@ int resq_linear_fwd_prepared_bf16(int format, int sparsity, const uint16_t* X, i
                                   size_t workspace_bytes, void* stream) {
   return linear_fwd_prepared(format, sparsity, X, m, d, ldx, wprep, n, Y, ldy, true, workspace,
                              workspace_bytes, stream);
+}
+
+int resq_linear_fwd_prepared_swiglu(int format, int sparsity, const void* G, const void* U,
+                                    int in_dtype, int64_t m, int64_t d, int64_t ldg, int64_t ldu,
+                                    const void* wprep, int64_t n, float* Y, int64_t ldy,
+                                    void* workspace, size_t workspace_bytes, void* stream) {
+  const Sp sp = decode_sparsity(sparsity);
+  if (in_dtype != RESQ_IN_BF16 && in_dtype != RESQ_IN_F32)
+    return fail(RESQ_ERR_ARG, "unknown input dtype %d", in_dtype);
+  int rc = check_fwd_args(format, sparsity, sp, (const uint16_t*)G, m, d, std::min(ldg, ldu), n, Y, ldy);
+  if (rc != RESQ_OK) return rc;
+  if (m > 0 && d > 0 && !U) return fail(RESQ_ERR_ARG, "U is NULL");
+  if (m == 0 || n == 0) return ok();
+  if (d > 0 && !wprep) return fail(RESQ_ERR_ARG, "wprep is NULL");
+  if ((uintptr_t)wprep % 256 != 0) return fail(RESQ_ERR_ARG, "wprep must be 256-byte aligned");
+  const size_t esz = in_dtype == RESQ_IN_F32 ? 4 : 2;
+  if ((uintptr_t)G % esz != 0 || (uintptr_t)U % esz != 0)
+    return fail(RESQ_ERR_ARG, "G and U must be aligned to their element size");
+  ActWs w{};
+  const size_t need = carve_fwd(workspace, format, sp, m, d, n, &w);
+  rc = check_ws(workspace, workspace_bytes, need);
+  if (rc != RESQ_OK) return rc;
+  const resq::Producer prod{G, U, ldg, ldu, in_dtype == RESQ_IN_F32};
+  return linear_fwd_core(format, sp, nullptr, m, d, 0, wprep, n, Y, ldy, false, w,
+                         (hipStream_t)stream, &prod);
 }
 
 int resq_linear_fwd(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,

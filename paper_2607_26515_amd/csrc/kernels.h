@@ -11,9 +11,10 @@ namespace resq {
 enum ResidMode {
   kResidNone = 0,      // Q(X) only
   kResidIdentity = 1,  // Q(dX) kept whole
-  kResidNM4 = 2,       // S_k:4 applied in the pass (k = nm_keep; S_2:4 with k = 2)
+  kResid24 = 2,        // S_2:4 applied in the pass
   kResidDense = 3,     // Q(dX) written whole; a global selection prunes it afterwards
-  kResidNM8 = 4        // S_k:8 applied in the pass
+  kResidNM8 = 4,       // S_k:8 applied in the pass (k = nm_keep)
+  kResidNM4 = 5        // S_k:4 applied in the pass (k = nm_keep, k != 2)
 };
 
 // Row-wise quantization (blocks along columns) of a bf16 or f32 matrix.
@@ -32,8 +33,18 @@ void launch_quant_cols_frag(int mode, const uint16_t* x, int64_t rows, int64_t c
 void launch_quant_cols(int fmt, const void* x, bool in_f32, int64_t rows, int64_t cols,
                        int64_t ld, uint8_t* codes, void* scales, hipStream_t s);
 
+// A producer fused into the forward's activation pass: instead of reading X, the pass forms
+// X = silu(G) * U (the SwiGLU feeding a down projection) from G and U (m x d, row strides ldg
+// and ldu, bf16 or float32), each element the bf16 nearest to its float64 value.
+struct Producer {
+  const void* g;
+  const void* u;
+  int64_t ldg, ldu;
+  bool f32;
+};
+
 // Q(X), dX = X - Q(X), Q(dX), and S_k:4 / S_k:8 (k = nm_keep) / identity / none.  keep_mask
-// and partials may be null.  partials (double [m][d/B]) receives the exact per-scale-block sums of squares of
+// and partials may be null.  prod (frag = true only): X comes from that producer.  partials (double [m][d/B]) receives the exact per-scale-block sums of squares of
 // the dequantized Q(dX) (used by the block selection).  frag = true writes MFMA fragments
 // (pack.hip layout; codes -> fragment records, scales -> per-lane scale bytes) instead of
 // K-major codes + scales: for both Q(X) and Q(dX) with the local kinds; with kResidDense
@@ -43,7 +54,8 @@ void launch_quant_cols(int fmt, const void* x, bool in_f32, int64_t rows, int64_
 void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
                      uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes, void* qr_scales,
                      uint8_t* keep_mask, double* partials, hipStream_t s, bool frag = false,
-                     uint32_t* zero = nullptr, int zero_words = 0, int nm_keep = 2);
+                     uint32_t* zero = nullptr, int zero_words = 0, int nm_keep = 2,
+                     const Producer* prod = nullptr);
 
 // MFMA operand packing (pack.hip): K-major codes + scales -> fragment-major operands.
 enum PackMode { kPackMx = 0, kPackHiA = 1, kPackHiB = 2 };

@@ -126,15 +126,13 @@ __global__ __launch_bounds__(kThreads) void residual_kernel(
       for (int k = 0; k < 4; ++k) r[k] = v[k] - qx.val[k];  // exact in float32
       const Quad qr = quantize_quad<FMT>(r);
       uint32_t keep = 0xFu;
-      if constexpr (MODE == kResidNM4) {
-        if (nm_keep == 2) {
-          keep = keep_2_of_4(qr.code);
-        } else {
-          uint32_t mag[4];
+      if constexpr (MODE == kResid24) {
+        keep = keep_2_of_4(qr.code);
+      } else if constexpr (MODE == kResidNM4) {
+        uint32_t mag[4];
 #pragma unroll
-          for (int k = 0; k < 4; ++k) mag[k] = qr.code[k] & 7u;
-          keep = keep_k_of_g<4>(mag, nm_keep);
-        }
+        for (int k = 0; k < 4; ++k) mag[k] = qr.code[k] & 7u;
+        keep = keep_k_of_g<4>(mag, nm_keep);
       } else if constexpr (MODE == kResidNM8) {
         // the pair's 8 codes and their shifts (HiF4 level-3 groups may differ)
         const uint32_t mine = pack_quad_codes(qr.code) | ((uint32_t)qr.b << 16);
@@ -313,19 +311,107 @@ __device__ __forceinline__ void store_kmajor8(uint8_t* __restrict__ codes, uint8
   }
 }
 
-// Row tile t, K step kb of the fused residual pass (one workgroup of 256 threads).
-template <int FMT, int MODE, bool VEC>
+// The bf16 nearest to a float64 (ties to even), in one rounding: round to float32 with
+// round-to-odd (the float32 grid has 16 more bits than bf16's, so the sticky lowest bit keeps
+// every tie decision of the final step), then round that to bf16 to nearest even.  Values past
+// the largest finite bf16 give inf.
+__device__ __forceinline__ float f64_to_bf16_value(double v) {
+  float f = (float)v;
+  if ((double)f != v) {
+    uint32_t b = __float_as_uint(f);
+    if (fabs((double)f) > fabs(v)) b -= 1u;  // rounded away from zero: step back
+    f = __uint_as_float(b | 1u);
+  }
+  const uint32_t u = __float_as_uint(f);
+  return __uint_as_float(((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16) << 16);
+}
+
+// X = silu(G) * U for 8 consecutive elements: float64 sigmoid and product, one rounding.
+template <bool VEC>
+__device__ __forceinline__ void swiglu8(const Producer& p, int64_t row, int64_t col0, float x[8]) {
+  float g[8], u[8];
+  if (p.f32) {
+    const float* gs = reinterpret_cast<const float*>(p.g) + row * p.ldg + col0;
+    const float* us = reinterpret_cast<const float*>(p.u) + row * p.ldu + col0;
+    if constexpr (VEC) {
+      const float4 g0 = reinterpret_cast<const float4*>(gs)[0], g1 = reinterpret_cast<const float4*>(gs)[1];
+      const float4 u0 = reinterpret_cast<const float4*>(us)[0], u1 = reinterpret_cast<const float4*>(us)[1];
+      g[0] = g0.x; g[1] = g0.y; g[2] = g0.z; g[3] = g0.w; g[4] = g1.x; g[5] = g1.y; g[6] = g1.z; g[7] = g1.w;
+      u[0] = u0.x; u[1] = u0.y; u[2] = u0.z; u[3] = u0.w; u[4] = u1.x; u[5] = u1.y; u[6] = u1.z; u[7] = u1.w;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) { g[i] = gs[i]; u[i] = us[i]; }
+    }
+  } else {
+    const uint16_t* gs = reinterpret_cast<const uint16_t*>(p.g) + row * p.ldg + col0;
+    const uint16_t* us = reinterpret_cast<const uint16_t*>(p.u) + row * p.ldu + col0;
+    if constexpr (VEC) {
+      const uint4 gw = *reinterpret_cast<const uint4*>(gs), uw = *reinterpret_cast<const uint4*>(us);
+      const uint32_t gv[4] = {gw.x, gw.y, gw.z, gw.w}, uv[4] = {uw.x, uw.y, uw.z, uw.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        g[2 * e] = bf16_to_f32(gv[e] & 0xFFFFu); g[2 * e + 1] = bf16_to_f32(gv[e] >> 16);
+        u[2 * e] = bf16_to_f32(uv[e] & 0xFFFFu); u[2 * e + 1] = bf16_to_f32(uv[e] >> 16);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) { g[i] = bf16_to_f32(gs[i]); u[i] = bf16_to_f32(us[i]); }
+    }
+  }
+  // Fast path in float32: e = expf(-g) (about 1 ulp), 1 + e, g / (1 + e) and the product
+  // with u (0.5 ulp each) put s within 5 float32 ulps of the exact value (e's error enters
+  // silu scaled by e / (1 + e) <= 1).  A bf16 midpoint lies 2^15 float32 ulps from each bf16
+  // value, so when s is more than 64 ulps from the nearest midpoint its bf16 rounding is that
+  // of the exact value.  The rest (about 0.2% of elements), and inputs outside the bound's
+  // premises (g < -80, where exp(-g) nears float32 overflow; 0 < |g| < 2^-100, where g / 2
+  // may lose bits; a non-finite s), take the float64 path one element at a time, so a wave
+  // repeats it only as often as its busiest lane needs it.
+  uint32_t pending = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float gi = g[i];
+    const float sv = gi / (1.0f + expf(-gi)) * u[i];
+    const uint32_t b = __float_as_uint(sv);
+    const int dist = abs((int)(b & 0xFFFFu) - 0x8000);
+    const bool premise = gi >= -80.f && (gi == 0.f || fabsf(gi) >= 0x1p-100f) && isfinite(sv);
+    if (premise && dist > 64) {
+      x[i] = __uint_as_float(((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16) << 16);
+    } else {
+      pending |= 1u << i;
+    }
+  }
+  while (pending != 0) {
+    const int i = __builtin_ctz(pending);
+    pending &= pending - 1u;
+    float gi = 0.f, ui = 0.f;
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if (k == i) { gi = g[k]; ui = u[k]; }
+    const double gd = (double)gi;
+    const float xv = f64_to_bf16_value(gd / (1.0 + exp(-gd)) * (double)ui);
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if (k == i) x[k] = xv;
+  }
+}
+
+// Row tile t, K step kb of the fused residual pass (one workgroup of 256 threads).  SWIGLU:
+// X comes from the producer `prod` instead of from X.
+template <int FMT, int MODE, bool VEC, bool SWIGLU>
 __device__ __forceinline__ void residual_frag_tile(
     const uint16_t* __restrict__ X, int64_t m, int64_t d, int64_t ldx, int64_t nkb,
     uint8_t* __restrict__ fx, uint8_t* __restrict__ fsx, uint8_t* __restrict__ fr,
-    uint8_t* __restrict__ fsr, double* __restrict__ partials, int nm_keep, int64_t t, int64_t kb) {
+    uint8_t* __restrict__ fsr, double* __restrict__ partials, int nm_keep, const Producer& prod,
+    int64_t t, int64_t kb) {
   const int64_t f = t * nkb + kb;  // fragment index
   const int tid = threadIdx.x;
   const int rr = tid >> 3, half = (tid >> 2) & 1, s = tid & 3;
   const int64_t row = t * 32 + rr;
   const int64_t col0 = kb * 64 + 32 * half + 8 * s;
   float x[8];
-  if (row < m && col0 < d) {
+  if (SWIGLU && row < m && col0 < d) {
+    swiglu8<VEC>(prod, row, col0, x);
+  } else if (row < m && col0 < d) {
     const uint16_t* src = X + row * ldx + col0;
     if constexpr (VEC) {
       const uint4 u = *reinterpret_cast<const uint4*>(src);
@@ -353,7 +439,16 @@ __device__ __forceinline__ void residual_frag_tile(
 #pragma unroll
     for (int i = 0; i < 8; ++i) x[i] -= val[i];  // dX, exact in float32
     quantize8<FMT>(x, code, val, scale_byte, c1, b, b2);
-    if constexpr (MODE == kResidNM4 || MODE == kResidNM8) {
+    if constexpr (MODE == kResid24) {
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        const uint32_t c4[4] = {code[4 * g], code[4 * g + 1], code[4 * g + 2], code[4 * g + 3]};
+        const uint32_t keep = keep_2_of_4(c4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (!((keep >> e) & 1u)) code[4 * g + e] = 0u;
+      }
+    } else if constexpr (MODE == kResidNM4 || MODE == kResidNM8) {
       const uint32_t keep = keep_local8<MODE == kResidNM4 ? 4 : 8>(code, b, nm_keep);
 #pragma unroll
       for (int e = 0; e < 8; ++e)
@@ -372,18 +467,18 @@ __device__ __forceinline__ void residual_frag_tile(
 // fr / fsr receive the K-major Q(dX) codes and scales and `partials` its per-scale-block
 // sums of squares (may be null); workgroup (0, 0) also clears zero_words words at zero (may
 // be null), the histogram the element-wise selection accumulates into.
-template <int FMT, int MODE, bool VEC>
+template <int FMT, int MODE, bool VEC, bool SWIGLU>
 __global__ __launch_bounds__(256) void residual_frag_kernel(
     const uint16_t* __restrict__ X, int64_t m, int64_t d, int64_t ldx, int64_t nkb,
     uint8_t* __restrict__ fx, uint8_t* __restrict__ fsx, uint8_t* __restrict__ fr,
     uint8_t* __restrict__ fsr, double* __restrict__ partials, uint32_t* __restrict__ zero,
-    int zero_words, int nm_keep) {
+    int zero_words, int nm_keep, Producer prod) {
   if (zero != nullptr && blockIdx.x == 0 && blockIdx.y == 0)
     for (int i = threadIdx.x; i < zero_words; i += blockDim.x) zero[i] = 0u;
   const int64_t mtiles = (m + 31) / 32;
   for (int64_t t = blockIdx.y; t < mtiles; t += gridDim.y)
-    residual_frag_tile<FMT, MODE, VEC>(X, m, d, ldx, nkb, fx, fsx, fr, fsr, partials, nm_keep, t,
-                                       blockIdx.x);
+    residual_frag_tile<FMT, MODE, VEC, SWIGLU>(X, m, d, ldx, nkb, fx, fsx, fr, fsr, partials, nm_keep,
+                                               prod, t, blockIdx.x);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -560,23 +655,34 @@ void launch_quant_cols(int fmt, const void* x, bool in_f32, int64_t rows, int64_
 void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
                      uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes, void* qr_scales,
                      uint8_t* keep_mask, double* partials, hipStream_t s, bool frag,
-                     uint32_t* zero, int zero_words, int nm_keep) {
+                     uint32_t* zero, int zero_words, int nm_keep, const Producer* prod) {
   if (m == 0 || d == 0) return;
   if (frag) {
     const int64_t nkb = (d + 63) / 64;
     const dim3 grid((unsigned)nkb, grid_rows((m + 31) / 32));
-    const bool vec16 = ((uintptr_t)X % 16 == 0) && (ldx % 8 == 0);
-#define RESQ_RF(F, M, V) hipLaunchKernelGGL((residual_frag_kernel<F, M, V>), grid, dim3(256), 0, s, X, m, d, ldx, nkb, qx_codes, (uint8_t*)qx_scales, qr_codes, (uint8_t*)qr_scales, partials, zero, zero_words, nm_keep)
-#define RESQ_RF_MODE(F, V)                                        \
-    switch (mode) {                                               \
-      case kResidNone: RESQ_RF(F, kResidNone, V); break;          \
-      case kResidIdentity: RESQ_RF(F, kResidIdentity, V); break;  \
-      case kResidDense: RESQ_RF(F, kResidDense, V); break;        \
-      case kResidNM8: RESQ_RF(F, kResidNM8, V); break;            \
-      default: RESQ_RF(F, kResidNM4, V); break;                   \
+    const Producer pr = prod ? *prod : Producer{nullptr, nullptr, 0, 0, false};
+    // 16-byte loads: 8 bf16 of X (or of G and U), or 2 x 4 floats of G and U
+    const int64_t ve = prod ? (prod->f32 ? 4 : 8) : 8;
+    const bool vec16 = prod ? ((uintptr_t)pr.g % 16 == 0 && (uintptr_t)pr.u % 16 == 0 &&
+                               pr.ldg % ve == 0 && pr.ldu % ve == 0)
+                            : ((uintptr_t)X % 16 == 0 && ldx % 8 == 0);
+#define RESQ_RF(F, M, V, P) hipLaunchKernelGGL((residual_frag_kernel<F, M, V, P>), grid, dim3(256), 0, s, X, m, d, ldx, nkb, qx_codes, (uint8_t*)qx_scales, qr_codes, (uint8_t*)qr_scales, partials, zero, zero_words, nm_keep, pr)
+#define RESQ_RF_MODE(F, V, P)                                        \
+    switch (mode) {                                                  \
+      case kResidNone: RESQ_RF(F, kResidNone, V, P); break;          \
+      case kResidIdentity: RESQ_RF(F, kResidIdentity, V, P); break;  \
+      case kResidDense: RESQ_RF(F, kResidDense, V, P); break;        \
+      case kResidNM8: RESQ_RF(F, kResidNM8, V, P); break;            \
+      case kResidNM4: RESQ_RF(F, kResidNM4, V, P); break;            \
+      default: RESQ_RF(F, kResid24, V, P); break;                    \
     }
-    if (fmt == kMX) { if (vec16) { RESQ_RF_MODE(kMX, true) } else { RESQ_RF_MODE(kMX, false) } }
-    else { if (vec16) { RESQ_RF_MODE(kHI, true) } else { RESQ_RF_MODE(kHI, false) } }
+#define RESQ_RF_VEC(F, P) if (vec16) { RESQ_RF_MODE(F, true, P) } else { RESQ_RF_MODE(F, false, P) }
+    if (prod) {
+      if (fmt == kMX) { RESQ_RF_VEC(kMX, true) } else { RESQ_RF_VEC(kHI, true) }
+    } else {
+      if (fmt == kMX) { RESQ_RF_VEC(kMX, false) } else { RESQ_RF_VEC(kHI, false) }
+    }
+#undef RESQ_RF_VEC
 #undef RESQ_RF_MODE
 #undef RESQ_RF
     return;
@@ -588,6 +694,7 @@ void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d,
   switch (mode) {                                                \
     case kResidNone: RESQ_RK(F, kResidNone, V); break;           \
     case kResidIdentity: RESQ_RK(F, kResidIdentity, V); break;   \
+    case kResid24: RESQ_RK(F, kResid24, V); break;               \
     case kResidNM4: RESQ_RK(F, kResidNM4, V); break;             \
     case kResidNM8: RESQ_RK(F, kResidNM8, V); break;             \
     default: RESQ_RK(F, kResidDense, V); break;                  \

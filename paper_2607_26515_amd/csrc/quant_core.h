@@ -104,7 +104,8 @@ __device__ __forceinline__ uint32_t keep_k_of_g(const uint32_t mag[G], int k) {
   return keep;
 }
 
-// The keep bits of the local pattern S_k:G for 8 consecutive codes (two groups when G = 4).
+// The keep bits of the local pattern S_k:G for 8 consecutive codes (two groups when G = 4;
+// S_2:4 itself takes keep_2_of_4).
 // b[h] is the HiF4 level-2 + level-3 shift of elements 4h .. 4h+3 (0 for MXFP4, whose 8
 // aligned elements share one scale).  A 4-group shares its scale, so its codes compare
 // directly; an 8-group spans two HiF4 level-3 groups, so each magnitude code k is put on the
@@ -118,7 +119,6 @@ __device__ __forceinline__ uint32_t keep_local8(const uint32_t c[8], const int b
     return keep_k_of_g<8>(mag, k);
   } else {
     const uint32_t a[4] = {c[0], c[1], c[2], c[3]}, e[4] = {c[4], c[5], c[6], c[7]};
-    if (k == 2) return keep_2_of_4(a) | (keep_2_of_4(e) << 4);
     uint32_t ma[4], me[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {

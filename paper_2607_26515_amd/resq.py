@@ -79,7 +79,7 @@ EXPORTED = ("resq_quantize", "resq_residual_sparsify", "resq_linear_fwd", "resq_
             "resq_workspace_size", "resq_last_error", "resq_version", "resq_profile_enable",
             "resq_profile_reset", "resq_profile_read", "resq_prepared_weights_size",
             "resq_prepare_weights", "resq_linear_fwd_prepared", "resq_linear_fwd_prepared_bf16",
-            "resq_diagnostics")
+            "resq_diagnostics", "resq_linear_fwd_prepared_swiglu")
 
 
 class ResqError(RuntimeError):
@@ -116,6 +116,9 @@ def load() -> ctypes.CDLL:
     lib.resq_linear_fwd_prepared_bf16.restype = i32
     lib.resq_diagnostics.argtypes = [i32, vp, i64, i64, i64, ctypes.c_float, vp, vp, sz, vp]
     lib.resq_diagnostics.restype = i32
+    lib.resq_linear_fwd_prepared_swiglu.argtypes = [i32, i32, vp, vp, i32, i64, i64, i64, i64, vp, i64,
+                                                    vp, i64, vp, sz, vp]
+    lib.resq_linear_fwd_prepared_swiglu.restype = i32
     for f in ("resq_quantize", "resq_residual_sparsify", "resq_linear_fwd", "resq_linear_bwd"):
         getattr(lib, f).restype = i32
     lib.resq_workspace_size.restype = sz
@@ -173,6 +176,12 @@ def resq_linear_fwd_prepared_bf16(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy,
                                   workspace_bytes, stream=0) -> int:
     return load().resq_linear_fwd_prepared_bf16(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy,
                                                 workspace, workspace_bytes, stream)
+
+
+def resq_linear_fwd_prepared_swiglu(fmt, sparsity, G, U, in_dtype, m, d, ldg, ldu, wprep, n, Y, ldy,
+                                    workspace, workspace_bytes, stream=0) -> int:
+    return load().resq_linear_fwd_prepared_swiglu(fmt, sparsity, G, U, in_dtype, m, d, ldg, ldu,
+                                                  wprep, n, Y, ldy, workspace, workspace_bytes, stream)
 
 
 def resq_diagnostics(fmt, X, m, d, ldx, outlier_threshold, stats, workspace, workspace_bytes,
@@ -382,3 +391,24 @@ def diagnostics(x, fmt, outlier_threshold, stream=None):
                           nb, _stream(stream))
     _check(rc, "resq_diagnostics")
     return stats
+
+
+def linear_fwd_swiglu(g, u, wprep, n, fmt, sparsity, y=None, ws=None, stream=None):
+    """Y = ResQ linear of X = silu(G) * U (bf16-rounded, formed inside the quantization pass);
+    G and U are m x d bf16 (int16 bit patterns or bfloat16) or float32 views with unit column
+    stride and the same dtype."""
+    import torch
+    m, d = g.shape
+    f, sp = _fmt(fmt), _sp(sparsity)
+    if g.dtype != u.dtype or g.shape != u.shape:
+        raise ValueError("G and U must have the same shape and dtype")
+    in_dtype = IN_F32 if g.dtype == torch.float32 else IN_BF16
+    if y is None:
+        y = torch.empty((m, n), dtype=torch.float32, device=g.device)
+    if ws is None:
+        ws = workspace(OP_LINEAR_FWD_PREPARED, f, sp, m, d, n, g.device)
+    buf, nb = ws
+    rc = resq_linear_fwd_prepared_swiglu(f, sp, _p(g), _p(u), in_dtype, m, d, g.stride(0), u.stride(0),
+                                         _p(wprep), n, _p(y), y.stride(0), _p(buf), nb, _stream(stream))
+    _check(rc, "resq_linear_fwd_prepared_swiglu")
+    return y
