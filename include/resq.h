@@ -264,8 +264,12 @@ const char* resq_version(void);
 
 /*
  * Kernel timing (diagnostics; off by default).  While enabled, every kernel the library
- * enqueues is bracketed by two HIP events recorded on the same stream (event objects are
- * host-side handles; no device memory is allocated).  resq_profile_read synchronizes the
+ * enqueues is timed with two HIP events on the same stream (event objects are host-side
+ * handles; no device memory is allocated).  The GEMMs ("gemm", with a K split's reduction),
+ * the forward's activation pass ("residual" in the forward entry points) and "diagnostics"
+ * carry the events in their kernel dispatches, so the interval is the kernels' execution as a
+ * kernel trace measures it; the other families record them around the enqueue, which adds
+ * the dispatch gap (a few microseconds).  resq_profile_read synchronizes the
  * recorded events and returns, for the kernel family `name` ("residual", "quant_rows",
  * "quant_cols", "pack_hif4", "select", "gemm", "diagnostics"), the number of launches and their summed
  * duration in milliseconds since the last reset.  Returns RESQ_ERR_ARG for an unknown name.

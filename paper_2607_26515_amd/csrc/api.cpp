@@ -383,7 +383,7 @@ int linear_fwd_core(int format, const Sp& sp, const uint16_t* X, int64_t m, int6
     // the residual pass writes Q(X) as MFMA fragments and the dense Q(dX) K-major (the
     // selection ranks all of it); the selection then writes S(Q(dX)) as fragments
     {
-      resq::ProfScope prof_(resq::kProfResidual, s);
+      resq::ProfScope prof_(resq::kProfResidual, s, true);
       const bool elem = sp.kind == RESQ_S_UNSTRUCT50;
       resq::launch_residual(format, resq::kResidDense, X, m, d, ldx, w.frag_x, w.fsc_x, w.qr_codes,
                             w.qr_scales, nullptr, sp.kind == RESQ_S_BLOCK32X64_50 ? w.partials : nullptr,
@@ -395,7 +395,7 @@ int linear_fwd_core(int format, const Sp& sp, const uint16_t* X, int64_t m, int6
                              w.partials, w.sel, a_pack_mode(format), w.frag_r, w.fsc_r, s);
   } else {
     // local kinds: the residual pass writes the MFMA fragments directly
-    resq::ProfScope prof_(resq::kProfResidual, s);
+    resq::ProfScope prof_(resq::kProfResidual, s, true);
     resq::launch_residual(format, resid_mode(sp), X, m, d, ldx, w.frag_x, w.fsc_x, w.frag_r,
                           w.fsc_r, nullptr, nullptr, s, true, nullptr, 0, sp.keep, prod);
   }
@@ -407,7 +407,7 @@ int linear_fwd_core(int format, const Sp& sp, const uint16_t* X, int64_t m, int6
                                         bf, bsc, Y, ldy, out_bf16);
   op.partial = w.gemm_partial;
   {
-    resq::ProfScope prof_(resq::kProfGemm, s);
+    resq::ProfScope prof_(resq::kProfGemm, s, true);
     if (!resq::launch_gemm(op, s)) return fail(RESQ_ERR_UNSUPPORTED, "GEMM operand layout rejected");
   }
   return check_launch("resq_linear_fwd");
@@ -527,7 +527,7 @@ int resq_diagnostics(int format, const uint16_t* X, int64_t m, int64_t d, int64_
   if (rc != RESQ_OK) return rc;
   hipStream_t s = (hipStream_t)stream;
   {
-    resq::ProfScope prof_(resq::kProfDiag, s);
+    resq::ProfScope prof_(resq::kProfDiag, s, true);
     resq::launch_diagnostics(format, X, m, d, ldx, outlier_threshold, stats, (double*)workspace, s);
   }
   return check_launch("resq_diagnostics");
@@ -565,7 +565,7 @@ int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uin
     const uint8_t* af[2] = {w.fa, w.fa};
     const uint8_t* asc[2] = {w.fa_sc, w.fa_sc};
     const resq::GemmOperands op = gemm_operands(format, n, d, m, 1, af, asc, w.fb, w.fb_sc, dW, d);
-    resq::ProfScope prof_(resq::kProfGemm, s);
+    resq::ProfScope prof_(resq::kProfGemm, s, true);
     if (!resq::launch_gemm(op, s)) return fail(RESQ_ERR_UNSUPPORTED, "GEMM operand layout rejected");
   }
   if (dX) {
@@ -582,7 +582,7 @@ int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uin
     const uint8_t* af[2] = {w.fr, w.fr};
     const uint8_t* asc[2] = {w.fr_sc, w.fr_sc};
     const resq::GemmOperands op = gemm_operands(format, m, d, n, 1, af, asc, w.fb, w.fb_sc, dX, d);
-    resq::ProfScope prof_(resq::kProfGemm, s);
+    resq::ProfScope prof_(resq::kProfGemm, s, true);
     if (!resq::launch_gemm(op, s)) return fail(RESQ_ERR_UNSUPPORTED, "GEMM operand layout rejected");
   }
   return check_launch("resq_linear_bwd");

@@ -9,6 +9,7 @@
 // a fixed order.  Counts are exact; the sums of squares are float64 (every square is exact)
 // and the same on every run.
 #include "kernels.h"
+#include "profiler.h"
 #include "quant_core.h"
 
 namespace resq {
@@ -134,13 +135,13 @@ void launch_diagnostics(int fmt, const uint16_t* X, int64_t m, int64_t d, int64_
     const dim3 g = diag_grid(m, d);
     rows = (int64_t)g.x * g.y;
     const bool vec = ((uintptr_t)X % 8 == 0) && (ldx % 4 == 0);
-#define RESQ_DG(F, V) hipLaunchKernelGGL((diag_kernel<F, V>), g, dim3(kThreads), 0, s, X, m, d, ldx, thr, partials)
+#define RESQ_DG(F, V) launch_timed(diag_kernel<F, V>, g, dim3(kThreads), 0u, s, X, m, d, ldx, thr, partials)
     if (fmt == kMX) { if (vec) RESQ_DG(kMX, true); else RESQ_DG(kMX, false); }
     else { if (vec) RESQ_DG(kHI, true); else RESQ_DG(kHI, false); }
 #undef RESQ_DG
   }
-  hipLaunchKernelGGL(diag_finish_kernel, dim3(1), dim3(kThreads), 0, s, (const double*)partials,
-                     rows, (double)(m * d), (double)(m * (d / B)), stats);
+  launch_timed(diag_finish_kernel, dim3(1), dim3(kThreads), 0u, s, (const double*)partials, rows,
+               (double)(m * d), (double)(m * (d / B)), stats);
 }
 
 }  // namespace resq

@@ -40,6 +40,7 @@
 // b % 8), so tiles that share a weight column block run on the same XCD and share its L2.
 #include "kernels.h"
 #include "device_fp4.h"
+#include "profiler.h"
 
 
 namespace resq {
@@ -587,13 +588,13 @@ void launch_cfg(GemmParams p, int n_terms, hipStream_t s) {
   using G2 = Geo<FMT, WM, WN, TM, TN, 2, NS, KG>;
   using G1 = Geo<FMT, WM, WN, TM, TN, 1, NS, KG>;
   if (n_terms > 1)
-    hipLaunchKernelGGL((gemm_kernel<FMT, WM, WN, TM, TN, 2, NS, KG>), grid, block, G2::lds_bytes(), s, p);
+    launch_timed(gemm_kernel<FMT, WM, WN, TM, TN, 2, NS, KG>, grid, block, (uint32_t)G2::lds_bytes(), s, p);
   else
-    hipLaunchKernelGGL((gemm_kernel<FMT, WM, WN, TM, TN, 1, NS, KG>), grid, block, G1::lds_bytes(), s, p);
+    launch_timed(gemm_kernel<FMT, WM, WN, TM, TN, 1, NS, KG>, grid, block, (uint32_t)G1::lds_bytes(), s, p);
   if (p.ksplit > 1)
-    hipLaunchKernelGGL((splitk_reduce_kernel<WM, WN, TM, TN>), dim3(p.grid_m * p.grid_n * WM * WN * TM * TN),
-                       dim3(256), 0, s, (const float*)p.partial, (int)p.ksplit, p.grid_m, p.grid_n, p.M, p.N, p.Y, p.ldy,
-                       p.out_bf16);
+    launch_timed(splitk_reduce_kernel<WM, WN, TM, TN>, dim3(p.grid_m * p.grid_n * WM * WN * TM * TN), dim3(256),
+                 0u, s, (const float*)p.partial, (int)p.ksplit, p.grid_m, p.grid_n, p.M, p.N, p.Y, p.ldy,
+                 p.out_bf16);
 }
 
 // Tile choice (measured on MI355X): a CU holds one or two workgroups (LDS- and

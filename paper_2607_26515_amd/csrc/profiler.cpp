@@ -49,14 +49,24 @@ void fold_locked() {
 const char* kNames[kProfCount] = {"residual", "quant_rows", "quant_cols", "pack_hif4", "select", "gemm",
                                   "diagnostics"};
 
+thread_local KernelEvents t_ev;
+thread_local bool t_ev_open = false;
+
 }  // namespace
 
-int prof_begin(int kernel, hipStream_t s) {
+KernelEvents* prof_kernel_events() { return t_ev_open ? &t_ev : nullptr; }
+
+int prof_begin(int kernel, hipStream_t s, bool kernel_events) {
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_on) return -1;
   if (g_recs.size() > 4096) fold_locked();
   Rec r{kernel, take_event(), take_event()};
-  if (r.a) hipEventRecord(r.a, s);
+  if (kernel_events && r.a && r.b) {
+    t_ev = KernelEvents{r.a, r.b, true};
+    t_ev_open = true;
+  } else if (r.a) {
+    hipEventRecord(r.a, s);
+  }
   g_recs.push_back(r);
   return (int)g_recs.size() - 1;
 }
@@ -64,6 +74,12 @@ int prof_begin(int kernel, hipStream_t s) {
 void prof_end(int token, hipStream_t s) {
   if (token < 0) return;
   std::lock_guard<std::mutex> lk(g_mu);
+  if (t_ev_open) {
+    t_ev_open = false;
+    if (!t_ev.first) return;  // the launches carried the events
+    // no kernel was launched: an empty interval
+    if (token < (int)g_recs.size() && g_recs[token].a) hipEventRecord(g_recs[token].a, s);
+  }
   if (token < (int)g_recs.size() && g_recs[token].b) hipEventRecord(g_recs[token].b, s);
 }
 

@@ -1,6 +1,7 @@
 // Quantization passes: Q along rows or columns, the fused residual pass of the ResQ linear
 // (Q(X), dX = X - Q(X), Q(dX), S_2:4) and the HiF4 MFMA operand packing.
 #include "kernels.h"
+#include "profiler.h"
 #include "quant_core.h"
 
 namespace resq {
@@ -666,7 +667,7 @@ void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d,
     const bool vec16 = prod ? ((uintptr_t)pr.g % 16 == 0 && (uintptr_t)pr.u % 16 == 0 &&
                                pr.ldg % ve == 0 && pr.ldu % ve == 0)
                             : ((uintptr_t)X % 16 == 0 && ldx % 8 == 0);
-#define RESQ_RF(F, M, V, P) hipLaunchKernelGGL((residual_frag_kernel<F, M, V, P>), grid, dim3(256), 0, s, X, m, d, ldx, nkb, qx_codes, (uint8_t*)qx_scales, qr_codes, (uint8_t*)qr_scales, partials, zero, zero_words, nm_keep, pr)
+#define RESQ_RF(F, M, V, P) launch_timed(residual_frag_kernel<F, M, V, P>, grid, dim3(256), 0u, s, X, m, d, ldx, nkb, qx_codes, (uint8_t*)qx_scales, qr_codes, (uint8_t*)qr_scales, partials, zero, zero_words, nm_keep, pr)
 #define RESQ_RF_MODE(F, V, P)                                        \
     switch (mode) {                                                  \
       case kResidNone: RESQ_RF(F, kResidNone, V, P); break;          \
