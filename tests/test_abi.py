@@ -135,3 +135,20 @@ def test_diagnostics_rejects_bad_arguments():
     assert need > 0
     assert P.resq_diagnostics(B.MXFP4, ptr, 4, 64, 64, 1.0, ptr, 0, 0, 0) == B.ERR_WORKSPACE
     assert P.resq_workspace_size(B.OP_DIAGNOSTICS, B.MXFP4, 0, 0, 64, 0) == 0
+
+
+def test_swiglu_forward_rejects_bad_arguments():
+    ptr = 1 << 20  # never dereferenced
+    ws = P.resq_workspace_size(B.OP_LINEAR_FWD_PREPARED, B.MXFP4, B.S_2_4, 4, 64, 8)
+    call = P.resq_linear_fwd_prepared_swiglu
+    # bad input dtype, unknown sparsity, ld < d, NULL U, misaligned G, missing workspace
+    assert call(B.MXFP4, B.S_2_4, ptr, ptr, 7, 4, 64, 64, 64, ptr, 8, ptr, 8, 0, 0, 0) == B.ERR_ARG
+    assert call(B.MXFP4, 99, ptr, ptr, B.IN_BF16, 4, 64, 64, 64, ptr, 8, ptr, 8, 0, 0, 0) == B.ERR_ARG
+    assert call(B.MXFP4, B.S_2_4, ptr, ptr, B.IN_BF16, 4, 64, 63, 64, ptr, 8, ptr, 8, 0, 0, 0) == B.ERR_ARG
+    assert call(B.MXFP4, B.S_2_4, ptr, 0, B.IN_BF16, 4, 64, 64, 64, ptr, 8, ptr, 8, 0, 0, 0) == B.ERR_ARG
+    assert call(B.MXFP4, B.S_2_4, ptr + 2, ptr, B.IN_F32, 4, 64, 64, 64, ptr, 8, ptr, 8, 0, 0, 0) == B.ERR_ARG
+    assert call(B.HIF4, B.S_2_4, ptr, ptr, B.IN_BF16, 4, 96, 96, 96, ptr, 8, ptr, 8, 0, 0, 0) == B.ERR_SHAPE
+    assert ws > 0
+    assert call(B.MXFP4, B.S_2_4, ptr, ptr, B.IN_BF16, 4, 64, 64, 64, ptr, 8, ptr, 8, 0, 0, 0) == B.ERR_WORKSPACE
+    # nothing to do: m = 0
+    assert call(B.MXFP4, B.S_2_4, 0, 0, B.IN_BF16, 0, 64, 64, 64, 0, 8, 0, 8, 0, 0, 0) == B.OK
