@@ -224,7 +224,8 @@ int resq_linear_fwd_prepared_swiglu(int format, int sparsity, const void* G, con
  * term (ResQ is applied to the rollout only).
  * dY : m x n bf16, X : m x d bf16, W : n x d bf16, all contiguous (row stride = row length).
  * n must be a multiple of the block size (for dX) and m as well (for dW).
- * dX, dW : float32 outputs, contiguous; either may be NULL to skip that GEMM.
+ * dX, dW : float32 outputs, contiguous; either may be NULL to skip that GEMM.  An empty
+ *          contraction (n = 0 for dX, m = 0 for dW) writes zeros.
  */
 int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uint16_t* W,
                     int64_t m, int64_t d, int64_t n, float* dX, float* dW, void* workspace,

@@ -541,7 +541,14 @@ int resq_linear_bwd(int format, const uint16_t* dY, const uint16_t* X, const uin
   const int64_t B = block_of(format);
   if (dX && n % B != 0) return fail(RESQ_ERR_SHAPE, "dX needs n (%lld) %% %lld == 0", (long long)n, (long long)B);
   if (dW && m % B != 0) return fail(RESQ_ERR_SHAPE, "dW needs m (%lld) %% %lld == 0", (long long)m, (long long)B);
-  if (m == 0 || d == 0 || n == 0) return ok();
+  if (d == 0) return ok();
+  if (m == 0 || n == 0) {
+    // an empty contraction: the gradient that still has elements is all zeros
+    hipStream_t s = (hipStream_t)stream;
+    if (m == 0 && dW) resq::launch_zero_f32(dW, n * d, s);
+    if (n == 0 && dX) resq::launch_zero_f32(dX, m * d, s);
+    return check_launch("resq_linear_bwd");
+  }
   if (!dY || (dX && !W) || (dW && !X)) return fail(RESQ_ERR_ARG, "NULL input pointer");
   if ((dX && !resq::gemm_supported(format, m, d, n, 1)) ||
       (dW && !resq::gemm_supported(format, n, d, m, 1)))

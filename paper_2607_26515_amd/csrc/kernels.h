@@ -122,6 +122,9 @@ size_t gemm_split_scratch(int fmt, int64_t M, int64_t N, int64_t K);
 // scales, each 256-byte aligned) and the B buffer fit 32-bit offsets.
 bool gemm_supported(int fmt, int64_t M, int64_t N, int64_t K, int n_terms);
 
+// p[0 .. n) = 0 (a fill kernel: callers may capture the library's launches in a graph).
+void launch_zero_f32(float* p, int64_t n, hipStream_t s);
+
 // Activation statistics (diag.hip): stats receives 9 doubles (see resq_diagnostics);
 // partials is diag_ws_bytes(m, d) bytes of scratch.
 size_t diag_ws_bytes(int64_t m, int64_t d);

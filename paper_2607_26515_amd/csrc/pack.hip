@@ -66,7 +66,19 @@ __global__ __launch_bounds__(kThreads) void pack_kernel(const uint8_t* __restric
     pack_record<MODE, MASK>(codes, scales, rows, K, nkb, gbits, frag, fscale, t, local >> 6, (int)(local & 63));
 }
 
+// Zero fill of n floats (grid-stride).
+__global__ __launch_bounds__(kThreads) void zero_f32_kernel(float* __restrict__ p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += (int64_t)gridDim.x * kThreads)
+    p[i] = 0.f;
+}
+
 }  // namespace
+
+void launch_zero_f32(float* p, int64_t n, hipStream_t s) {
+  if (n <= 0) return;
+  const int64_t blocks = (n + kThreads - 1) / kThreads;
+  hipLaunchKernelGGL(zero_f32_kernel, dim3((unsigned)(blocks < 4096 ? blocks : 4096)), dim3(kThreads), 0, s, p, n);
+}
 
 size_t frag_bytes(int mode, int64_t rows, int64_t K) {
   const int64_t n = ((rows + 31) / 32) * ((K + 63) / 64) * 64;
