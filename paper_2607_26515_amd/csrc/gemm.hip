@@ -628,12 +628,11 @@ Plan plan(int fmt, int64_t M, int64_t N, int64_t K, bool may_split) {
   if (wgs(4, 4) < 240) {
     pl.cfg = kSmall;
     pl.tiles = wgs(2, 2);
-    const int per_cu = fmt == 0 ? 2 : 1;  // small-tile workgroups resident per CU (LDS)
     if (may_split && pl.tiles > 0) {
       // a split pays only for long K: its partial tiles and the reduction launch cost
-      // about as much as a short K range (measured)
-      // (MXFP4 small tiles already run two workgroups per CU: no gain there)
-      int64_t ks = per_cu == 1 ? kCUs / pl.tiles : 1;
+      // about as much as a short K range (measured; MXFP4 at m = 256, K = 11008: 18.8 us
+      // unsplit in four K groups, 17.4 us split in two)
+      int64_t ks = kCUs / pl.tiles;
       ks = ks < 1 ? 1 : (ks > 2 ? 2 : ks);
       while (ks > 1 && nkb / ks < 64) --ks;
       pl.ksplit = (int)ks;
@@ -641,11 +640,13 @@ Plan plan(int fmt, int64_t M, int64_t N, int64_t K, bool may_split) {
       if (pl.ksplit > 1) pl.partial_bytes = (size_t)pl.tiles * pl.ksplit * (256 * 16) * sizeof(float);
     }
     // K groups (measured): MXFP4 takes four for long K ranges (>= 128 steps per workgroup)
-    // and two otherwise (two workgroups then share a CU); HiF4 takes two, with two stages
-    // when the grid has more workgroups than CUs (so two share a CU), four otherwise.
+    // and two otherwise (two workgroups then share a CU); HiF4 takes two.  Both take two
+    // stages when the grid has more workgroups than CUs, so that two share a CU (MXFP4 at
+    // m = 512, K = 18944: 73.0 us with four stages, 68.7 us with two), four otherwise.
     pl.ns = 4;
     if (fmt == 0) {
       pl.kg = pl.kper >= 128 ? 4 : 2;
+      if (pl.kg == 4 && pl.tiles * pl.ksplit > kCUs) pl.ns = 2;
     } else {
       pl.kg = 2;
       if (pl.tiles * pl.ksplit > kCUs) pl.ns = 2;
@@ -664,8 +665,12 @@ template <int FMT>
 void launch_fmt(const GemmParams& p, int cfg, int kg, int ns, int n_terms, hipStream_t s) {
   if (cfg == kSmall) {
     if constexpr (FMT == 0) {
-      if (kg == 4) launch_cfg<FMT, 2, 2, 1, 1, 4, 4>(p, n_terms, s);
-      else launch_cfg<FMT, 2, 2, 1, 1, 4, 2>(p, n_terms, s);
+      if (kg == 4) {
+        if (ns == 2) launch_cfg<FMT, 2, 2, 1, 1, 2, 4>(p, n_terms, s);
+        else launch_cfg<FMT, 2, 2, 1, 1, 4, 4>(p, n_terms, s);
+      } else {
+        launch_cfg<FMT, 2, 2, 1, 1, 4, 2>(p, n_terms, s);
+      }
     } else {
       if (ns == 2) launch_cfg<FMT, 2, 2, 1, 1, 2, 2>(p, n_terms, s);
       else launch_cfg<FMT, 2, 2, 1, 1, 4, 2>(p, n_terms, s);

@@ -199,7 +199,9 @@ def test_linear_bwd(fmt, m, d, n):
 @pytest.mark.parametrize("sp", ["none", "2:4"])
 @pytest.mark.parametrize("fmt,m,d,n", [
     ("mxfp4", 64, 320, 128),    # 5 K steps, two K groups: the last stage is half empty
-    ("mxfp4", 64, 8384, 96),    # 131 K steps, four K groups: three steps in the last stage
+    ("mxfp4", 64, 8384, 96),    # K split in two (66 + 65 steps), two K groups each
+    ("mxfp4", 512, 8384, 1152),  # 131 K steps, four K groups: three steps in the last stage
+    ("mxfp4", 1024, 8384, 1152),  # more workgroups than CUs: four K groups, two stages
     ("hif4", 64, 320, 128),     # 5 K steps, two K groups
     ("hif4", 32, 8384, 64),     # K split in two (66 + 65 steps), two K groups each
     ("hif4", 640, 320, 2048),   # more small tiles than CUs: two stages, two workgroups per CU
