@@ -639,17 +639,26 @@ Plan plan(int fmt, int64_t M, int64_t N, int64_t K, bool may_split) {
       pl.kper = (nkb + ks - 1) / ks;
       if (pl.ksplit > 1) pl.partial_bytes = (size_t)pl.tiles * pl.ksplit * (256 * 16) * sizeof(float);
     }
-    // K groups (measured): MXFP4 takes four for long K ranges (>= 128 steps per workgroup)
-    // and two otherwise (two workgroups then share a CU); HiF4 takes two.  Both take two
-    // stages when the grid has more workgroups than CUs, so that two share a CU (MXFP4 at
-    // m = 512, K = 18944: 73.0 us with four stages, 68.7 us with two), four otherwise.
+    // K groups and stages (measured).  Grids within the CUs: MXFP4 takes four K groups for
+    // long K ranges (>= 128 steps per workgroup) and two otherwise, HiF4 two, with four
+    // stages.  Grids beyond the CUs, where workgroups share CUs: long K ranges keep their
+    // K groups with two stages (MXFP4 at m = 512, K = 18944: 73.0 us with four stages, 68.7
+    // with two); shorter ones take one K group (HiF4 at m = 512, 3584 -> 4608: 47 us with
+    // two K groups, 35 us with one and two stages; MXFP4: 21.6 us, 19.4 with one and four).
+    const bool crowded = pl.tiles * pl.ksplit > kCUs;
     pl.ns = 4;
     if (fmt == 0) {
       pl.kg = pl.kper >= 128 ? 4 : 2;
-      if (pl.kg == 4 && pl.tiles * pl.ksplit > kCUs) pl.ns = 2;
+      if (crowded) {
+        if (pl.kg == 4) pl.ns = 2;
+        else pl.kg = 1;
+      }
     } else {
       pl.kg = 2;
-      if (pl.tiles * pl.ksplit > kCUs) pl.ns = 2;
+      if (crowded) {
+        pl.ns = 2;
+        if (pl.kper < 128) pl.kg = 1;
+      }
     }
   } else {
     const bool wide = M >= 512 && fmt == 0;
@@ -668,11 +677,14 @@ void launch_fmt(const GemmParams& p, int cfg, int kg, int ns, int n_terms, hipSt
       if (kg == 4) {
         if (ns == 2) launch_cfg<FMT, 2, 2, 1, 1, 2, 4>(p, n_terms, s);
         else launch_cfg<FMT, 2, 2, 1, 1, 4, 4>(p, n_terms, s);
+      } else if (kg == 1) {
+        launch_cfg<FMT, 2, 2, 1, 1, 4, 1>(p, n_terms, s);
       } else {
         launch_cfg<FMT, 2, 2, 1, 1, 4, 2>(p, n_terms, s);
       }
     } else {
-      if (ns == 2) launch_cfg<FMT, 2, 2, 1, 1, 2, 2>(p, n_terms, s);
+      if (kg == 1) launch_cfg<FMT, 2, 2, 1, 1, 2, 1>(p, n_terms, s);
+      else if (ns == 2) launch_cfg<FMT, 2, 2, 1, 1, 2, 2>(p, n_terms, s);
       else launch_cfg<FMT, 2, 2, 1, 1, 4, 2>(p, n_terms, s);
     }
   } else if (cfg == kWide) {

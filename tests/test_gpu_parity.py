@@ -204,7 +204,9 @@ def test_linear_bwd(fmt, m, d, n):
     ("mxfp4", 1024, 8384, 1152),  # more workgroups than CUs: four K groups, two stages
     ("hif4", 64, 320, 128),     # 5 K steps, two K groups
     ("hif4", 32, 8384, 64),     # K split in two (66 + 65 steps), two K groups each
-    ("hif4", 640, 320, 2048),   # more small tiles than CUs: two stages, two workgroups per CU
+    ("hif4", 640, 320, 2048),   # more small tiles than CUs, short K: one K group, two stages
+    ("hif4", 640, 8384, 2048),  # more small tiles than CUs, long K: two K groups, two stages
+    ("mxfp4", 640, 320, 2048),  # more small tiles than CUs, short K: one K group, four stages
 ])
 def test_linear_fwd_k_groups(fmt, sp, m, d, n):
     """Decode-sized grids run K groups (several wave groups splitting each stage's K steps);
