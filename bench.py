@@ -401,8 +401,8 @@ def main() -> int:
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
-              f"(the layer's multi-GPU sharding is described in the design notes, not run).",
+        print(f"bench.py: the benchmark runs the layer on one GPU; --gpus {args.gpus} is not "
+              f"supported (how the layer shards over several GPUs is described, not run).",
               file=sys.stderr)
         return 2
 
