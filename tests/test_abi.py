@@ -152,3 +152,15 @@ def test_swiglu_forward_rejects_bad_arguments():
     assert call(B.MXFP4, B.S_2_4, ptr, ptr, B.IN_BF16, 4, 64, 64, 64, ptr, 8, ptr, 8, 0, 0, 0) == B.ERR_WORKSPACE
     # nothing to do: m = 0
     assert call(B.MXFP4, B.S_2_4, 0, 0, B.IN_BF16, 0, 64, 64, 64, 0, 8, 0, 8, 0, 0, 0) == B.OK
+
+
+def test_profiler_names_and_reset():
+    import ctypes
+    n, ms = ctypes.c_int64(-1), ctypes.c_double(-1.0)
+    lib = P.load()
+    P.resq_profile_enable(False)
+    P.resq_profile_reset()
+    for name in (b"residual", b"quant_rows", b"quant_cols", b"pack_hif4", b"select", b"gemm", b"diagnostics"):
+        assert lib.resq_profile_read(name, ctypes.byref(n), ctypes.byref(ms)) == B.OK
+        assert n.value == 0 and ms.value == 0.0
+    assert lib.resq_profile_read(b"no_such_kernel", ctypes.byref(n), ctypes.byref(ms)) == B.ERR_ARG

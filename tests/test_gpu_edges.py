@@ -76,3 +76,28 @@ def test_backward_empty_contractions_give_zeros(fmt):
     c, e = P.linear_bwd(dev_bf16(gb), x, w, fmt)
     torch.cuda.synchronize()
     assert torch.equal(a, c) and torch.equal(b, e)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("m,d,n", [(256, 2048, 2560), (256, 11008, 2048)])  # the second splits K
+def test_profiler_counts_launch_families(fmt, m, d, n):
+    """The library profiler sees one residual pass and one GEMM family interval per forward
+    call (a K split's reduction is inside the GEMM's interval), with positive durations."""
+    import torch
+    import paper_2607_26515_amd as P
+    log(f"profiler {fmt} m={m} d={d} n={n}")
+    xb, wb = activations(rng_tree(6, 1)[0], m, d, 0.01, 50.0), weights(rng_tree(7, 1)[0], n, d)
+    qc, qs = P.quantize(dev_bf16(wb), fmt, axis=1)
+    wp = P.prepare_weights(qc, qs, fmt)
+    x = dev_bf16(xb)
+    P.linear_fwd_prepared(x, wp, n, fmt, "2:4")
+    torch.cuda.synchronize()
+    P.resq_profile_enable(True)
+    P.resq_profile_reset()
+    for _ in range(3):
+        P.linear_fwd_prepared(x, wp, n, fmt, "2:4")
+    torch.cuda.synchronize()
+    g, r = P.resq_profile_read("gemm"), P.resq_profile_read("residual")
+    P.resq_profile_enable(False)
+    assert g[0] == 3 and r[0] == 3
+    assert 0.0 < g[1] < 3 * 10.0 and 0.0 < r[1] < 3 * 10.0  # milliseconds
