@@ -75,3 +75,30 @@ def test_every_bf16_value_under_a_fixed_block_max(fmt, amax):
         x[:, pos] = v
     y, want = _identity_forward(fmt, x)
     _check(y, want, f"under max {amax}")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("seed", [0, 1])
+def test_backward_every_bf16_value(fmt, seed):
+    """Every finite bf16 value in dY (256 x 256, a seeded permutation) through the backward's
+    two quantizations of dY and its GEMMs, with X = W = I: dX = Q_n(dY) Q_n(W) has one
+    product per output, Q_n(dY)[i, c] Q_n(W)[c, c], and dW = Q_m(dY)^T Q_m(X) has
+    Q_m(dY)[c, j] Q_m(X)[c, c]; both exact in float32."""
+    import paper_2607_26515_amd as P
+    log(f"exhaustive backward {fmt} seed={seed}")
+    n = 256
+    v = _finite_bf16()
+    flat = np.zeros(n * n, dtype=np.uint16)
+    flat[: v.size] = v
+    dy = np.random.default_rng(seed).permutation(flat).reshape(n, n)
+    eye = f32_to_bf16_bits(np.eye(n, dtype=np.float32))
+    dx, dw = P.linear_bwd(dev_bf16(dy), dev_bf16(eye), dev_bf16(eye), fmt)
+    g = bf16_bits_to_f32(dy)
+    i32 = np.eye(n, dtype=np.float32)
+    qn_dy = F.dequantize(fmt, *F.quantize(fmt, g))               # blocks along n (rows of dY)
+    qm_dy = F.dequantize(fmt, *F.quantize(fmt, g.T.copy())).T     # blocks along m (columns)
+    wdiag = np.diag(F.dequantize(fmt, *F.quantize(fmt, i32)))     # Q of I, either axis
+    want_dx = (qn_dy * wdiag[None, :]).astype(np.float32) + np.float32(0.0)
+    want_dw = (qm_dy.T * wdiag[None, :]).astype(np.float32) + np.float32(0.0)
+    _check(host(dx), want_dx, "dX")
+    _check(host(dw), want_dw, "dW")
