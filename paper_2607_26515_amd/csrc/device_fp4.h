@@ -1,10 +1,11 @@
 // Device-side FP4 arithmetic for gfx950: MXFP4 and HiF4 block quantization and the
 // operand encodings the scaled f8f6f4 MFMA consumes.
 //
-// Every decision (block scale, element code, level-2/3 bits) is made by exact comparisons:
-// thresholds are small integers times powers of two (exact in float32), and inputs are
-// rescaled by powers of two with v_ldexp_f32 (exact; fp32 denormals are kept).  No reciprocal
-// or division is used, since HiF4 scales are not powers of two.
+// Every decision (block scale, element code, level-2/3 bits) is exact: scales are read from
+// the exponent and fraction fields of the block maximum, and element codes come from
+// comparisons with thresholds that are small integers times powers of two (exact in float32),
+// after a power-of-two rescale with v_ldexp_f32 (exact; fp32 denormals are kept).  No
+// reciprocal or division is used, since HiF4 scales are not powers of two.  Inputs are finite.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -17,20 +18,36 @@ constexpr int kHiBlock = 64;
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
 
-// floor(log2(a)) for finite a > 0, fp32 subnormals included.
-__device__ __forceinline__ int ilog2f(float a) {
-  const uint32_t u = __float_as_uint(a);
-  const int ef = (u >> 23) & 0xFF;
-  if (ef) return ef - 127;
-  return -149 + (31 - __clz(u & 0x7FFFFFu));
+// v from another lane of the same row of 16 through a DPP lane pattern (every pattern used
+// reads inside the row; all lanes active).
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, true);
+}
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;  // lane i of 8 <- lane 7-i
+constexpr int kDppMirror = 0x140;      // lane i of 16 <- lane 15-i
+
+// Larger of two magnitudes (finite, +0 or positive): their bit patterns order as integers.
+__device__ __forceinline__ float max_mag(float a, float b) {
+  return __uint_as_float(max(__float_as_uint(a), __float_as_uint(b)));
 }
 
-// Max of v over aligned groups of G lanes (G a power of two <= 64).
+// Max of a magnitude v (finite, +0 or positive) over aligned groups of G lanes (G a power of
+// two <= 64).  Up to 16 lanes the partners come through DPP: after the maxima over lane pairs
+// and quads, the mirrored lane of an 8-group lies in the other quad and that of a 16-group in
+// the other 8-group.
 template <int G>
 __device__ __forceinline__ float group_max(float v) {
+  uint32_t u = __float_as_uint(v);
+  if constexpr (G >= 2) u = max(u, dpp_u32<kDppXor1>(u));
+  if constexpr (G >= 4) u = max(u, dpp_u32<kDppXor2>(u));
+  if constexpr (G >= 8) u = max(u, dpp_u32<kDppHalfMirror>(u));
+  if constexpr (G >= 16) u = max(u, dpp_u32<kDppMirror>(u));
 #pragma unroll
-  for (int o = 1; o < G; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+  for (int o = 16; o < G; o <<= 1) u = max(u, (uint32_t)__shfl_xor((int)u, o, 64));
+  return __uint_as_float(u);
 }
 
 template <int G>
@@ -43,11 +60,12 @@ __device__ __forceinline__ double group_sum(double v) {
 // ------------------------------------------------------------------------------------------
 // MXFP4: E2M1 elements, one E8M0 scale per 32 elements (OCP MX conversion rule, paper Sec. 3)
 // ------------------------------------------------------------------------------------------
-// Shared exponent of a block with max magnitude amax: floor(log2 amax) - 2, clamped.
+// Shared exponent of a block with max magnitude amax (finite, +0 or positive):
+// floor(log2 amax) - 2, clamped to [-127, 127].  For normal amax that is the biased exponent
+// field minus 129 (at most 125); a subnormal amax or zero has field 0 and clamps to -127.
 __device__ __forceinline__ int mx_exponent(float amax) {
-  if (!(amax > 0.f)) return -127;
-  const int e = ilog2f(amax) - 2;
-  return e < -127 ? -127 : (e > 127 ? 127 : e);
+  const int e = (int)(__float_as_uint(amax) >> 23) - 129;
+  return e < -127 ? -127 : e;
 }
 
 // 4-bit code of x under exponent E: nearest E2M1 magnitude, ties to the even code, saturating.
@@ -96,16 +114,17 @@ __device__ __forceinline__ void mx_value2(uint32_t codes2, float scale, float& v
 // (per 8) and level-3 (per 4) down-shifts, S1P2 elements k/4.
 //   s1 = 2^(e-31) (1 + m/4) for code c = 4e + m;  element value = k (4+m) 2^(e-35-b)
 // ------------------------------------------------------------------------------------------
-// Smallest code c with 1.75 * s1(c) >= A (saturating at 255).
+// Smallest code c with 1.75 * s1(c) >= A (saturating at 255), for a magnitude A (finite, +0 or
+// positive).  For A in [2^ea, 2^(ea+1)) the values 1.75 * s1 of codes 4(ea+30)+1 .. +4 are
+// {35, 42, 49, 56, 63} 2^(ea-5), i.e. mantissas 1.09375, 1.3125, 1.53125, 1.75 and above 1.875,
+// so c is that base code plus the number of the first four that A's mantissa exceeds, read
+// straight from its exponent and fraction fields.  Subnormal A (ea < -126) and every A below
+// 2^-31 give a negative count, clamped to code 0.
 __device__ __forceinline__ int hif4_c1(float A) {
-  if (!(A > 0.f)) return 0;
-  const int ea = ilog2f(A);
-  if (ea < -31) return 0;
-  if (ea > 57) return 255;
-  // 1.75 * s1 for codes base..base+3 is {35, 42, 49, 56} * 2^(ea-5); base+4 always covers A
-  const int base = 4 * (ea + 30) + 1;
-  const int c = base + (ldexpf(35.f, ea - 5) < A) + (ldexpf(42.f, ea - 5) < A) +
-                (ldexpf(49.f, ea - 5) < A) + (ldexpf(56.f, ea - 5) < A);
+  const uint32_t u = __float_as_uint(A);
+  const int E = (int)(u >> 23);  // biased exponent ea + 127
+  const uint32_t f = u & 0x7FFFFFu;
+  const int c = 4 * E - 387 + (f > 0x0C0000u) + (f > 0x280000u) + (f > 0x440000u) + (f > 0x600000u);
   return c < 0 ? 0 : (c > 255 ? 255 : c);
 }
 
@@ -114,12 +133,35 @@ __device__ __forceinline__ float hif4_half_fit(int c1, int shift) {
   return ldexpf((float)(7 * (4 + (c1 & 3))), (c1 >> 2) - 36 - shift);
 }
 
-// Magnitude k (0..7) of |x| on the grid k/4 * s, s = s1 2^-b: nearest, ties to even k.
-__device__ __forceinline__ uint32_t hif4_k(float x, int c1, int b) {
-  const float y = ldexpf(fabsf(x), 36 + b - (c1 >> 2));  // midpoints are (2k'+1)(4+m)
+// The midpoints of the element grid of level-1 code c1 that hif4_k compares with, in units of
+// 2^(e-36-b): q, 3q, 7q and 11q, and the step 2q (q = 4+m; small integers, exact).
+struct Hif4Mid {
+  float q, q2, q3, q7, q11;
+};
+__device__ __forceinline__ Hif4Mid hif4_mid(int c1) {
   const float q = (float)(4 + (c1 & 3));
-  return (y > q) + (y >= 3.f * q) + (y > 5.f * q) + (y >= 7.f * q) + (y > 9.f * q) +
-         (y >= 11.f * q) + (y > 13.f * q);
+  Hif4Mid t{q, 2.f * q, 3.f * q, 7.f * q, 11.f * q};
+  // Kept opaque: the optimiser would otherwise turn the per-element choice between 3q and 11q
+  // into an integer multiply and a conversion.
+  asm("" : "+v"(t.q3), "+v"(t.q11));
+  return t;
+}
+
+// Magnitude k (0..7) of |x| on the grid k/4 * s, s = s1 2^-b: nearest, ties to even k.
+// On the rescaled y = |x| 2^(36+b-e) the midpoint between j and j+1 is (2j+1) q; a tie goes to
+// the even neighbour, so y must exceed the midpoint above an even j and reach the one above an
+// odd j.  k is the number of midpoints passed, found by a three-step binary search: 3|4 (7q),
+// then 1|2 (3q) or 5|6 (11q), then the midpoint above the even k so far, 2q further up or
+// down.  NaN passes none (k = 0), +inf all (k = 7).
+__device__ __forceinline__ uint32_t hif4_k(float x, int c1, int b, const Hif4Mid& t) {
+  const float y = ldexpf(fabsf(x), 36 + b - (c1 >> 2));
+  const bool h4 = y >= t.q7;
+  const float t2 = h4 ? t.q11 : t.q3;
+  const bool h2 = y >= t2;
+  const float t1 = t2 + (h2 ? t.q2 : -t.q2);
+  const bool h1 = y > t1;
+  const uint32_t j = (h4 ? 2u : 0u) + (h2 ? 1u : 0u);
+  return j + j + (h1 ? 1u : 0u);
 }
 
 __device__ __forceinline__ float hif4_value(uint32_t code, int c1, int b) {

@@ -215,9 +215,10 @@ __device__ __forceinline__ void quantize8(const float x[8], uint32_t code[8], fl
       for (int e = 0; e < 4; ++e) a4 = fmaxf(a4, fabsf(x[4 * hh + e]));
       b[hh] = b2 + (a4 <= (b2 ? fit1 : fit0) ? 1 : 0);
     }
+    const Hif4Mid mid = hif4_mid(c1);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const uint32_t k = hif4_k(x[i], c1, b[i / 4]);
+      const uint32_t k = hif4_k(x[i], c1, b[i / 4], mid);
       code[i] = ((__float_as_uint(x[i]) >> 28) & 8u) | k;
       val[i] = hif4_value(code[i], c1, b[i / 4]);
     }
@@ -235,15 +236,22 @@ __device__ __forceinline__ void store_record8(uint8_t* __restrict__ frag, uint8_
     for (int i = 0; i < 8; ++i) w |= code[i] << (4 * i);
     reinterpret_cast<uint32_t*>(frag + rec * 16)[s] = w;
   } else {
-    // 8 six-bit fields = 48 bits each of hi and lo; record = hi bits [0,192) then lo
-    uint64_t h = 0, l = 0;
+    // 8 six-bit fields = 48 bits each of hi and lo; record = hi bits [0,192) then lo.  Each
+    // 48-bit run is built as two 24-bit runs of 4 fields (one level-3 shift each) in 32-bit
+    // words.
+    uint32_t rh[2], rl[2];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      uint32_t hi, lo;
-      hif4_split_e2m3(code[i], c1, b[i / 4], hi, lo);
-      h |= (uint64_t)hi << (6 * i);
-      l |= (uint64_t)lo << (6 * i);
+    for (int hh = 0; hh < 2; ++hh) {
+      rh[hh] = rl[hh] = 0u;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        uint32_t hi, lo;
+        hif4_split_e2m3(code[4 * hh + e], c1, b[hh], hi, lo);
+        rh[hh] |= hi << (6 * e);
+        rl[hh] |= lo << (6 * e);
+      }
     }
+    const uint64_t h = rh[0] | ((uint64_t)rh[1] << 24), l = rl[0] | ((uint64_t)rl[1] << 24);
     // thread s writes record dwords 3s .. 3s+2: hi of slices 0,1 / hi of 2,3 / lo of 0,1 /
     // lo of 2,3, i.e. 96 bits assembled from two slices' 48-bit runs
     const int lane = __lane_id();
@@ -497,9 +505,10 @@ __global__ __launch_bounds__(256) void residual_frag_kernel(
 __device__ __forceinline__ void store_record8_e3m2(uint8_t* __restrict__ frag, uint8_t* __restrict__ fsc,
                                                    int64_t rec, int s, const uint32_t code[8],
                                                    uint32_t scale_byte, const int b[2]) {
-  uint64_t h = 0;
+  uint32_t r[2] = {0u, 0u};  // two 24-bit runs of 4 fields
 #pragma unroll
-  for (int i = 0; i < 8; ++i) h |= (uint64_t)hif4_e3m2(code[i], b[i / 4]) << (6 * i);
+  for (int i = 0; i < 8; ++i) r[i / 4] |= hif4_e3m2(code[i], b[i / 4]) << (6 * (i % 4));
+  const uint64_t h = r[0] | ((uint64_t)r[1] << 24);
   const uint32_t plo = __shfl_xor((uint32_t)h, 1, 64), phi = __shfl_xor((uint32_t)(h >> 32), 1, 64);
   if ((s & 1) == 0) {
     const uint64_t p1 = ((uint64_t)phi << 32) | plo;  // the odd partner's 48 bits

@@ -41,7 +41,7 @@ __device__ __forceinline__ Quad quantize_quad(const float x[4]) {
   } else {
     const float A = group_max<16>(a);
     q.c1 = hif4_c1(A);
-    const float ag = fmaxf(a, __shfl_xor(a, 1, 64));
+    const float ag = max_mag(a, __uint_as_float(dpp_u32<kDppXor1>(__float_as_uint(a))));
     const int b2 = ag <= hif4_half_fit(q.c1, 0) ? 1 : 0;
     const int b3 = a <= hif4_half_fit(q.c1, b2) ? 1 : 0;
     q.b = b2 + b3;
@@ -53,9 +53,10 @@ __device__ __forceinline__ Quad quantize_quad(const float x[4]) {
     const uint32_t bits3 = (uint32_t)(m3 >> base) & 0xFFFFu;
     const uint32_t bits2 = even_bits16((uint32_t)(m2 >> base) & 0xFFFFu);
     q.scale = (uint32_t)q.c1 | (bits2 << 8) | (bits3 << 16);
+    const Hif4Mid mid = hif4_mid(q.c1);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const uint32_t k = hif4_k(x[i], q.c1, q.b);
+      const uint32_t k = hif4_k(x[i], q.c1, q.b, mid);
       q.code[i] = ((__float_as_uint(x[i]) >> 28) & 8u) | k;
       q.val[i] = hif4_value(q.code[i], q.c1, q.b);
     }
