@@ -38,6 +38,9 @@
 //
 // Workgroups are mapped to tiles in contiguous chunks per XCD (workgroup b runs on XCD
 // b % 8), so tiles that share a weight column block run on the same XCD and share its L2.
+// With a K split the split index varies slowest: an XCD's chunk then covers one K range of
+// a block of tiles, whose A rows and B columns over that range it reads once, instead of
+// every K range of fewer tiles (the ranges share no operand bytes).
 #include "kernels.h"
 #include "device_fp4.h"
 #include "profiler.h"
@@ -200,10 +203,11 @@ void gemm_kernel(GemmParams p) {
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
 
   const uint32_t b = blockIdx.x;
-  const uint32_t wgid = (b % kXcds) * p.per_xcd + b / kXcds;  // the K splits of a tile are adjacent
+  const uint32_t wgid = (b % kXcds) * p.per_xcd + b / kXcds;
   if (wgid >= p.n_wg) return;
-  const uint32_t tile = p.ksplit == 1 ? wgid : wgid / p.ksplit;
-  const uint32_t split = wgid - tile * p.ksplit;
+  const uint32_t ntiles = p.grid_m * p.grid_n;
+  const uint32_t split = p.ksplit == 1 ? 0u : wgid / ntiles;  // split-major
+  const uint32_t tile = wgid - split * ntiles;
   uint32_t wg_m, wg_n;
   tile_coords(tile, p.grid_m, p.grid_n, wg_m, wg_n);
   const int tid = threadIdx.x, lane = tid & 63;
