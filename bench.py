@@ -10,7 +10,8 @@ Default workload: the four linears of one Qwen2.5-3B block (qkv 2048->2560, o 20
 gate_up 2048->22016, down 11008->2048) at m = 256 tokens, HiF4 with the S_2:4 residual,
 seeded synthetic bf16 activations with 1% outlier channels (x50) and N(0, 0.02) weights.
 
-Inputs are resident in HBM when timing starts.  Weight and activation copies rotate across
+Steps are timed as eager launches on one stream (--graph 1 also times HIP graph replays of
+the same launches and reports them beside).  Inputs are resident in HBM when timing starts.  Weight and activation copies rotate across
 steps so that the 256 MB last-level cache cannot serve a step from the previous one.
 
 Prints one JSON line: the layer's algorithmic TFLOP/s (value), the roofline of the dominant
@@ -392,6 +393,10 @@ def main() -> int:
                     help="--op diagnostics: |x| above which a block counts as holding an outlier")
     ap.add_argument("--out", default="f32", choices=["f32", "bf16"],
                     help="forward output type: float32, or its bf16 rounding written by the GEMM")
+    ap.add_argument("--graph", type=int, default=0, choices=[0, 1],
+                    help="linear op: time the steps as eager launches (0), or also as HIP graph "
+                         "replays, one graph per rotated input copy (1; measured slower on "
+                         "ROCm 7, reported beside the eager time, which stays the value)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-cols", type=int, default=1024)
     ap.add_argument("--cpu-sample-rows", type=int, default=512)
@@ -426,7 +431,11 @@ def main() -> int:
         return 0
     P.load()  # fails loudly when libresq.so is missing
     dev = torch.device("cuda:0")
-    sptr = int(torch.cuda.current_stream().cuda_stream)
+    # one stream of the default priority for the whole run (graph capture needs a stream
+    # other than the null stream)
+    run_stream = torch.cuda.Stream()
+    torch.cuda.set_stream(run_stream)
+    sptr = int(run_stream.cuda_stream)
     wl = WORKLOADS[args.workload]
     fmt = args.format
     if args.op == "diagnostics":
@@ -452,15 +461,28 @@ def main() -> int:
         for st in lin_state:
             run_linear(st, i)
 
-    for i in range(args.warmup):
-        run_step(i)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        run_step(i)
-    torch.cuda.synchronize()
-    dt = time.perf_counter() - t0
+    def timed_loop(step):
+        for i in range(args.warmup):
+            step(i)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            step(i)
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0
+
+    dt = timed_loop(run_step)
     ms_per_step = dt * 1e3 / args.steps
+    ms_graph = None
+    if args.graph:
+        # The same launches, captured once per rotated copy and replayed.
+        graphs = []
+        for c in range(copies):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=run_stream):
+                run_step(c)
+            graphs.append(g)
+        ms_graph = timed_loop(lambda i: graphs[i % copies].replay()) * 1e3 / args.steps
 
     # ---- kernel times: HIP events on the launch stream via the library profiler ----
     kinds = ("quant_rows", "quant_cols", "pack_hif4", "gemm") if wl.backward else \
@@ -552,6 +574,8 @@ def main() -> int:
         "per_linear_us": per_linear,
         "roofline": roofline,
     }
+    if ms_graph is not None:
+        out["ms_per_step_graph_replay"] = round(ms_graph, 5)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, fmt, sp, args.cpu_sample_cols, args.cpu_sample_rows,
                                            args.cpu_seconds)
