@@ -160,8 +160,7 @@ __device__ __forceinline__ uint32_t hif4_k(float x, int c1, int b, const Hif4Mid
   const bool h2 = y >= t2;
   const float t1 = t2 + (h2 ? t.q2 : -t.q2);
   const bool h1 = y > t1;
-  const uint32_t j = (h4 ? 2u : 0u) + (h2 ? 1u : 0u);
-  return j + j + (h1 ? 1u : 0u);
+  return (h4 ? 4u : 0u) + (h2 ? 2u : 0u) + (h1 ? 1u : 0u);
 }
 
 __device__ __forceinline__ float hif4_value(uint32_t code, int c1, int b) {
