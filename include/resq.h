@@ -257,6 +257,18 @@ int resq_diagnostics(int format, const uint16_t* X, int64_t m, int64_t d, int64_
 /* Workspace bytes needed by `op` (a resq_op) for these arguments; 0 on bad arguments. */
 size_t resq_workspace_size(int op, int format, int sparsity, int64_t m, int64_t d, int64_t n);
 
+/*
+ * The GEMM plan a call of these sizes runs (host-side query; nothing is enqueued and no GPU
+ * is needed).  The GEMM computes Y[M][N] = sum over K: the forward linear has M = m, N = n,
+ * K = d and may split K (split_allowed = 1); the backward's dX GEMM has M = m, N = d, K = n,
+ * and its dW GEMM M = n, N = d, K = m, neither split (split_allowed = 0).
+ * info receives four values: [0] tile configuration (RESQ_TILE_*), [1] K split count,
+ * [2] K groups per workgroup, [3] LDS pipeline stages.  Returns RESQ_ERR_ARG for an unknown
+ * format, negative sizes or a NULL info.
+ */
+enum { RESQ_TILE_64x64 = 0, RESQ_TILE_128x256 = 1, RESQ_TILE_128x192 = 2, RESQ_TILE_128x192_8W = 3 };
+int resq_gemm_plan(int format, int64_t M, int64_t N, int64_t K, int split_allowed, int32_t info[4]);
+
 /* Human-readable description of the last non-OK status on this thread ("" if none). */
 const char* resq_last_error(void);
 

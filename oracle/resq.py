@@ -141,10 +141,19 @@ def keep_channel50(rhat: np.ndarray):
 def block_keys(rhat: np.ndarray, fmt: str) -> np.ndarray:
     """Sum of squares of every 32 x 64 block, shape (ceil(m/32), d/64).
 
-    Order: rows of the block in increasing order; within a row, the block's format scale
-    blocks in increasing column order (one for HiF4, two 32-wide halves for MXFP4), each
-    added as its own sum.  All elements of one scale block share one power-of-two factor and
-    have at most 6 significant bits, so that inner sum is exact in any order.
+    Order (reading S5): rows of the block in increasing order; within a row, the block's
+    format scale blocks in increasing column order (one for HiF4, two 32-wide halves for
+    MXFP4), each added as its own sum.  Every inner sum is exact in float64, in any order:
+    - MXFP4: each square is q^2 2^(2E) with q in the E2M1 grid, i.e. an integer multiple of
+      2^(2E-2) below 2^8, so 32 of them add to an integer multiple of 2^(2E-2) below 2^13;
+    - HiF4: each value is k (4+m) 2^(e-35-b) with k <= 7, m <= 3 and the element's own
+      level-2/3 shift b in 0..2 (b differs inside a block), so each square is an integer
+      multiple of 2^(2e-74) below 2401 * 2^4, and 64 of them add to an integer below 2^22 in
+      those units.
+    So the grouping by scale block is the plain sequential sum of the block's squares with
+    its exact partial sums formed first; it can differ from an element-by-element sequential
+    order only where a row-level addition rounds, and it is the grouping the GPU forms from
+    its per-scale-block partials.
     """
     m, d = rhat.shape
     sb = F.block_size(fmt)

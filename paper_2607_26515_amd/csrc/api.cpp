@@ -277,7 +277,15 @@ extern "C" {
 
 const char* resq_last_error(void) { return g_err.c_str(); }
 
-const char* resq_version(void) { return "resq-gfx950 0.1"; }
+const char* resq_version(void) { return "resq-gfx950 0.2"; }
+
+int resq_gemm_plan(int format, int64_t M, int64_t N, int64_t K, int split_allowed, int32_t info[4]) {
+  if (!valid_format(format)) return fail(RESQ_ERR_ARG, "unknown format %d", format);
+  if (M < 0 || N < 0 || K < 0) return fail(RESQ_ERR_ARG, "negative size");
+  if (!info) return fail(RESQ_ERR_ARG, "info is NULL");
+  resq::gemm_plan_info(format, M, N, K, split_allowed != 0, info);
+  return ok();
+}
 
 int resq_quantize(int format, const void* x, int in_dtype, int64_t rows, int64_t cols,
                   int64_t ld, int axis, uint8_t* codes, void* scales, void* stream) {

@@ -718,6 +718,14 @@ size_t gemm_split_scratch(int fmt, int64_t M, int64_t N, int64_t K) {
   return plan(fmt, M, N, K, true).partial_bytes;
 }
 
+void gemm_plan_info(int fmt, int64_t M, int64_t N, int64_t K, bool may_split, int32_t info[4]) {
+  const Plan pl = plan(fmt, M, N, K, may_split);
+  info[0] = pl.cfg;
+  info[1] = pl.ksplit;
+  info[2] = pl.cfg == kSmall ? pl.kg : 1;
+  info[3] = pl.cfg == kSmall ? pl.ns : pl.cfg == kWide ? 4 : pl.cfg == kMid8 ? 2 : (fmt == 0 ? 4 : 2);
+}
+
 bool launch_gemm(const GemmOperands& op, hipStream_t s) {
   if (op.M == 0 || op.N == 0) return true;
   const int amode = op.fmt == 0 ? kPackMx : kPackHiA, bmode = op.fmt == 0 ? kPackMx : kPackHiB;

@@ -79,7 +79,8 @@ EXPORTED = ("resq_quantize", "resq_residual_sparsify", "resq_linear_fwd", "resq_
             "resq_workspace_size", "resq_last_error", "resq_version", "resq_profile_enable",
             "resq_profile_reset", "resq_profile_read", "resq_prepared_weights_size",
             "resq_prepare_weights", "resq_linear_fwd_prepared", "resq_linear_fwd_prepared_bf16",
-            "resq_diagnostics", "resq_linear_fwd_prepared_swiglu")
+            "resq_diagnostics", "resq_linear_fwd_prepared_swiglu", "resq_gemm_plan")
+GEMM_TILES = {0: "64x64", 1: "128x256", 2: "128x192", 3: "128x192_8w"}
 
 
 class ResqError(RuntimeError):
@@ -128,6 +129,8 @@ def load() -> ctypes.CDLL:
     lib.resq_profile_reset.restype = None
     lib.resq_profile_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double)]
     lib.resq_profile_read.restype = i32
+    lib.resq_gemm_plan.argtypes = [i32, i64, i64, i64, i32, ctypes.POINTER(ctypes.c_int32)]
+    lib.resq_gemm_plan.restype = i32
     lib.resq_last_error.restype = ctypes.c_char_p
     lib.resq_version.restype = ctypes.c_char_p
     _lib = lib
@@ -188,6 +191,17 @@ def resq_diagnostics(fmt, X, m, d, ldx, outlier_threshold, stats, workspace, wor
                      stream=0) -> int:
     return load().resq_diagnostics(fmt, X, m, d, ldx, outlier_threshold, stats, workspace,
                                    workspace_bytes, stream)
+
+
+def resq_gemm_plan(fmt, M, N, K, split_allowed, info) -> int:
+    return load().resq_gemm_plan(fmt, M, N, K, split_allowed, info)
+
+
+def gemm_plan(fmt, M, N, K, split_allowed=True):
+    """The GEMM plan for Y[M][N] over K: dict(tile, ksplit, kgroups, stages) (host query)."""
+    info = (ctypes.c_int32 * 4)()
+    _check(resq_gemm_plan(_fmt(fmt), M, N, K, 1 if split_allowed else 0, info), "resq_gemm_plan")
+    return {"tile": GEMM_TILES[info[0]], "ksplit": info[1], "kgroups": info[2], "stages": info[3]}
 
 
 def resq_workspace_size(op, fmt, sparsity, m, d, n) -> int:

@@ -76,7 +76,7 @@ def test_qwen3b_layer_m256_full(fmt, linear):
 
 @pytest.mark.parametrize("fmt", FMTS)
 @pytest.mark.parametrize("sp", ["unstructured50", "block32x64_50", "channel50"])
-@pytest.mark.parametrize("linear", ["qkv", "down"])
+@pytest.mark.parametrize("linear", ["qkv", "o", "gate_up", "down"])
 def test_qwen7b_layer_m512_full(fmt, sp, linear):
     _fwd_full(fmt, sp, "qwen7b_layer_m512", linear)
 
