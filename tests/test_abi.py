@@ -164,3 +164,12 @@ def test_profiler_names_and_reset():
         assert lib.resq_profile_read(name, ctypes.byref(n), ctypes.byref(ms)) == B.OK
         assert n.value == 0 and ms.value == 0.0
     assert lib.resq_profile_read(b"no_such_kernel", ctypes.byref(n), ctypes.byref(ms)) == B.ERR_ARG
+
+
+def test_gemm_plan_query():
+    info = (ctypes.c_int32 * 4)()
+    assert P.resq_gemm_plan(B.MXFP4, 256, 2560, 2048, 1, info) == B.OK
+    assert list(info) == [0, 1, 2, 4]
+    assert P.resq_gemm_plan(5, 256, 2560, 2048, 1, info) == B.ERR_ARG
+    assert P.resq_gemm_plan(B.MXFP4, -1, 2560, 2048, 1, info) == B.ERR_ARG
+    assert P.gemm_plan("mxfp4", 8192, 37888, 3584) == {"tile": "128x256", "ksplit": 1, "kgroups": 1, "stages": 4}
