@@ -184,6 +184,26 @@ int resq_linear_fwd_prepared(int format, int sparsity, const uint16_t* X, int64_
                              void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * resq_linear_fwd_prepared_noalloc - resq_linear_fwd_prepared for callers that cannot
+ * allocate device memory or hand the library a workspace (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation).  Same arguments without the
+ * workspace, same kernels, same result bit for bit.  Its scratch (the MFMA operands of Q(X)
+ * and S(Q(dX)), the selection's keys and counters, split-K partial tiles) is a static
+ * device array of RESQ_NOALLOC_SCRATCH_BYTES in the library, one copy per GPU, held until
+ * the process ends; the first call on a device looks up that device's copy.  The call
+ * allocates nothing.  It runs on the current HIP device (`stream` must belong to it).
+ * Calls whose scratch need (resq_workspace_size(RESQ_OP_LINEAR_FWD_PREPARED, ...)) exceeds
+ * RESQ_NOALLOC_SCRATCH_BYTES return RESQ_ERR_UNSUPPORTED before enqueueing anything.
+ * Every call on one GPU shares that GPU's array and leaves its contents behind (the kernels
+ * clear what they count into): calls that can overlap on one GPU (other streams, other
+ * threads) race on it and must be serialized by the caller.
+ */
+#define RESQ_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int resq_linear_fwd_prepared_noalloc(int format, int sparsity, const uint16_t* X, int64_t m,
+                                     int64_t d, int64_t ldx, const void* wprep, int64_t n,
+                                     float* Y, int64_t ldy, void* stream);
+
+/*
  * resq_linear_fwd_prepared_bf16 - resq_linear_fwd_prepared with a bf16 output: Y is m x n
  * bf16 (bit patterns, row stride ldy >= n), each element the float32 result of Eq. 4 (as
  * resq_linear_fwd_prepared computes it) rounded to the nearest bf16, ties to even.  Halves

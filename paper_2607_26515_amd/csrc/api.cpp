@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <algorithm>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "kernels.h"
@@ -458,6 +459,58 @@ int resq_linear_fwd_prepared(int format, int sparsity, const uint16_t* X, int64_
                              void* workspace, size_t workspace_bytes, void* stream) {
   return linear_fwd_prepared(format, sparsity, X, m, d, ldx, wprep, n, Y, ldy, false, workspace,
                              workspace_bytes, stream);
+}
+
+namespace {
+
+// Scratch of resq_linear_fwd_prepared_noalloc: one static device array per GPU.  Host code
+// never uses the array's name as an address; it uses the device address looked up once per
+// device with hipGetSymbolAddress.
+static __device__ __align__(256) uint8_t scratch[RESQ_NOALLOC_SCRATCH_BYTES];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int device_scratch(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(RESQ_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(RESQ_ERR_UNSUPPORTED, "device %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(RESQ_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return ok();
+}
+
+}  // namespace
+
+int resq_linear_fwd_prepared_noalloc(int format, int sparsity, const uint16_t* X, int64_t m,
+                                     int64_t d, int64_t ldx, const void* wprep, int64_t n,
+                                     float* Y, int64_t ldy, void* stream) {
+  const Sp sp = decode_sparsity(sparsity);
+  int rc = check_fwd_args(format, sparsity, sp, X, m, d, ldx, n, Y, ldy);
+  if (rc != RESQ_OK) return rc;
+  if (m == 0 || n == 0) return ok();
+  if (d > 0 && !wprep) return fail(RESQ_ERR_ARG, "wprep is NULL");
+  if ((uintptr_t)wprep % 256 != 0) return fail(RESQ_ERR_ARG, "wprep must be 256-byte aligned");
+  const size_t need = carve_fwd(nullptr, format, sp, m, d, n, nullptr);
+  if (need > RESQ_NOALLOC_SCRATCH_BYTES)
+    return fail(RESQ_ERR_UNSUPPORTED,
+                "resq_linear_fwd_prepared_noalloc: these sizes need %zu bytes of scratch, the static "
+                "buffer holds %zu (use resq_linear_fwd_prepared with a workspace)",
+                need, (size_t)RESQ_NOALLOC_SCRATCH_BYTES);
+  void* base = nullptr;
+  rc = device_scratch(&base);
+  if (rc != RESQ_OK) return rc;
+  ActWs w{};
+  carve_fwd(base, format, sp, m, d, n, &w);
+  return linear_fwd_core(format, sp, X, m, d, ldx, wprep, n, Y, ldy, false, w, (hipStream_t)stream);
 }
 
 int resq_linear_fwd_prepared_bf16(int format, int sparsity, const uint16_t* X, int64_t m,

@@ -71,6 +71,7 @@ def sparsity_family(code: int) -> str:
     return {1: "local", 2: "channel", 3: "block", 4: "unstructured"}.get(code >> 8, "invalid")
 OK, ERR_ARG, ERR_SHAPE, ERR_UNSUPPORTED, ERR_HIP, ERR_WORKSPACE = 0, -1, -2, -3, -4, -5
 IN_BF16, IN_F32 = 0, 1
+NOALLOC_SCRATCH_BYTES = 64 << 20  # RESQ_NOALLOC_SCRATCH_BYTES
 OP_RESIDUAL_SPARSIFY, OP_LINEAR_FWD, OP_LINEAR_BWD, OP_LINEAR_FWD_PREPARED, OP_DIAGNOSTICS = 0, 1, 2, 3, 4
 DIAG_STATS = ("elements", "zeros_x", "zeros_qx", "blocks", "outlier_blocks", "energy_qx",
               "sse24_qx", "energy_qr", "sse24_qr")
@@ -79,7 +80,8 @@ EXPORTED = ("resq_quantize", "resq_residual_sparsify", "resq_linear_fwd", "resq_
             "resq_workspace_size", "resq_last_error", "resq_version", "resq_profile_enable",
             "resq_profile_reset", "resq_profile_read", "resq_prepared_weights_size",
             "resq_prepare_weights", "resq_linear_fwd_prepared", "resq_linear_fwd_prepared_bf16",
-            "resq_diagnostics", "resq_linear_fwd_prepared_swiglu", "resq_gemm_plan")
+            "resq_diagnostics", "resq_linear_fwd_prepared_swiglu", "resq_gemm_plan",
+            "resq_linear_fwd_prepared_noalloc")
 GEMM_TILES = {0: "64x64", 1: "128x256", 2: "128x192", 3: "128x192_8w"}
 
 
@@ -129,6 +131,8 @@ def load() -> ctypes.CDLL:
     lib.resq_profile_reset.restype = None
     lib.resq_profile_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double)]
     lib.resq_profile_read.restype = i32
+    lib.resq_linear_fwd_prepared_noalloc.argtypes = [i32, i32, vp, i64, i64, i64, vp, i64, vp, i64, vp]
+    lib.resq_linear_fwd_prepared_noalloc.restype = i32
     lib.resq_gemm_plan.argtypes = [i32, i64, i64, i64, i32, ctypes.POINTER(ctypes.c_int32)]
     lib.resq_gemm_plan.restype = i32
     lib.resq_last_error.restype = ctypes.c_char_p
@@ -173,6 +177,10 @@ def resq_linear_fwd_prepared(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy, work
                              workspace_bytes, stream=0) -> int:
     return load().resq_linear_fwd_prepared(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy,
                                            workspace, workspace_bytes, stream)
+
+
+def resq_linear_fwd_prepared_noalloc(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy, stream=0) -> int:
+    return load().resq_linear_fwd_prepared_noalloc(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy, stream)
 
 
 def resq_linear_fwd_prepared_bf16(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy, workspace,

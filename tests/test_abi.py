@@ -173,3 +173,16 @@ def test_gemm_plan_query():
     assert P.resq_gemm_plan(5, 256, 2560, 2048, 1, info) == B.ERR_ARG
     assert P.resq_gemm_plan(B.MXFP4, -1, 2560, 2048, 1, info) == B.ERR_ARG
     assert P.gemm_plan("mxfp4", 8192, 37888, 3584) == {"tile": "128x256", "ksplit": 1, "kgroups": 1, "stages": 4}
+
+
+def test_noalloc_rejects_oversized_calls_on_the_host():
+    """resq_linear_fwd_prepared_noalloc checks its scratch need before any HIP call: sizes
+    beyond RESQ_NOALLOC_SCRATCH_BYTES return RESQ_ERR_UNSUPPORTED (no GPU needed)."""
+    ptr = 1 << 20  # never dereferenced
+    m, d, n = 8192, 18944, 64
+    need = P.resq_workspace_size(B.OP_LINEAR_FWD_PREPARED, B.HIF4, B.S_2_4, m, d, n)
+    assert need > B.NOALLOC_SCRATCH_BYTES
+    rc = P.resq_linear_fwd_prepared_noalloc(B.HIF4, B.S_2_4, ptr, m, d, d, ptr, n, ptr, n, 0)
+    assert rc == B.ERR_UNSUPPORTED and "scratch" in P.resq_last_error()
+    assert P.resq_linear_fwd_prepared_noalloc(B.HIF4, 99, ptr, 4, 64, 64, ptr, n, ptr, n, 0) == B.ERR_ARG
+    assert P.resq_linear_fwd_prepared_noalloc(B.HIF4, B.S_2_4, ptr, 0, 64, 64, ptr, n, ptr, n, 0) == B.OK
