@@ -1,6 +1,12 @@
 #!/usr/bin/env python3
 """Throughput of the Rollout-ResQ FP4 linear layer on one MI355X.
 
+A default run prints one JSON line whose headline (value, roofline, cpu_baseline) is the
+default workload below, and which carries, under one key each (EXTRA_ENTRIES), the same
+measurement of the rest of the metric taken in the same process: MXFP4 on the same block,
+the Qwen2.5-7B block at m = 512 with the channel, 32x64-block and element-wise residuals in
+both formats, the m = 8192 prefill linears and the m = 8192 training backward in both formats.
+
 A step is one rollout forward of every linear projection of one transformer block (the hot
 path of Eq. 4): for each linear, quantize the bf16 activations, form and quantize the
 residual, apply S, and run the FP4 GEMM with the residual term, writing float32 Y.  Q(W) is
@@ -34,6 +40,22 @@ FP4_PEAK_TFLOPS = 10100.0      # MI355X dense MXFP4 / MXFP6 MFMA
 LLC_BYTES = 256 << 20          # MI355X last-level (Infinity) cache
 
 BYTES_PER_ELEM = {"hif4": 36 / 64, "mxfp4": 17 / 32}  # codes + block scales
+METRIC = "ResQ FP4 linear TFLOP/s + % roofline (HBM GB/s decode, MFMA FP4 prefill)"
+DEFAULT_WORKLOAD = "qwen3b_layer_m256"
+# Entries measured after the headline in a default run: (key, workload, format, sparsity)
+EXTRA_ENTRIES = (
+    ("qwen3b_layer_m256_mxfp4", "qwen3b_layer_m256", "mxfp4", "2:4"),
+    ("qwen7b_layer_m512_hif4_block", "qwen7b_layer_m512", "hif4", "block32x64_50"),
+    ("qwen7b_layer_m512_mxfp4_block", "qwen7b_layer_m512", "mxfp4", "block32x64_50"),
+    ("qwen7b_layer_m512_hif4_unstructured", "qwen7b_layer_m512", "hif4", "unstructured50"),
+    ("qwen7b_layer_m512_mxfp4_unstructured", "qwen7b_layer_m512", "mxfp4", "unstructured50"),
+    ("qwen7b_layer_m512_hif4_channel", "qwen7b_layer_m512", "hif4", "channel50"),
+    ("qwen7b_layer_m512_mxfp4_channel", "qwen7b_layer_m512", "mxfp4", "channel50"),
+    ("qwen7b_prefill_m8192_hif4", "qwen7b_prefill_m8192", "hif4", "2:4"),
+    ("qwen7b_prefill_m8192_mxfp4", "qwen7b_prefill_m8192", "mxfp4", "2:4"),
+    ("qwen3b_gateup_bwd_m8192_hif4", "qwen3b_gateup_bwd_m8192", "hif4", "none"),
+    ("qwen3b_gateup_bwd_m8192_mxfp4", "qwen3b_gateup_bwd_m8192", "mxfp4", "none"),
+)
 
 
 def kept_fraction(sp):
@@ -53,14 +75,16 @@ def alg_flops(m, d, n, sp):
     return 2 * m * d * n + round(2 * m * d * n * kept_fraction(sp))
 
 
-def exec_mfma_flops(m, d, n, fmt, sp):
-    """FP4-rate MFMA work issued by the GEMM (MFMA FLOPs at the FP4/FP6 rate).
+def executed_flops(m, d, n, sp):
+    """Sec. 5.4 work as the GEMM executes it on gfx950: 2mdn per term; every residual kind
+    runs as a dense FP4 operand (no FP4 sparse MFMA), so a residual adds a full 2mdn."""
+    return 2 * m * d * n * (1 if sp == "none" else 2)
 
-    MXFP4 runs one MFMA per K-step for Q(X) and one for the residual; HiF4 runs two
-    (hi/lo E2M3 operands) for each.  Every residual kind runs as a dense operand with zeros
-    on gfx950 (no FP4 sparse MFMA)."""
-    per_term = 2 * m * d * n * (2 if fmt == "hif4" else 1)
-    return per_term if sp == "none" else 2 * per_term
+
+def issued_mfma_flops(m, d, n, fmt, sp):
+    """MFMA work the GEMM issues at the FP4/FP6 rate: the executed work, twice for HiF4
+    (each HiF4 term runs as two E2M3 operands, hi and lo, so its level-1 scale fits)."""
+    return executed_flops(m, d, n, sp) * (2 if fmt == "hif4" else 1)
 
 
 def step_bytes(m, d, n, fmt, y_bytes=4):
@@ -107,7 +131,7 @@ def cpu_baseline(wl, fmt, sp, n_sample, n_rows, min_seconds):
     rows = min(wl.m, n_rows)
     prepared = []
     for lin in wl.linears:
-        t = workload_tensors(wl, lin, m=rows)
+        t = workload_tensors(wl, lin, m=rows, n_w=n_sample)
         if wl.backward:
             xb, wb, gb = t
             prepared.append((bf16_bits_to_f32(xb), bf16_bits_to_f32(wb[:n_sample]),
@@ -383,7 +407,7 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="qwen3b_layer_m256")
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--format", default="hif4", choices=["hif4", "mxfp4"])
     ap.add_argument("--sparsity", default="2:4")
     ap.add_argument("--op", default="linear", choices=["linear", "diagnostics", "swiglu_down"],
@@ -398,6 +422,11 @@ def main() -> int:
                          "replays, one graph per rotated input copy (1; measured slower on "
                          "ROCm 7, reported beside the eager time, which stays the value)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="measure only the selected workload (a default run also measures the "
+                         "entries of EXTRA_ENTRIES and adds them to the JSON line)")
+    ap.add_argument("--extra-cpu-seconds", type=float, default=4.0,
+                    help="oracle time per extra entry's cpu_baseline")
     ap.add_argument("--cpu-sample-cols", type=int, default=1024)
     ap.add_argument("--cpu-sample-rows", type=int, default=512)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
@@ -448,14 +477,51 @@ def main() -> int:
             print("bench.py: --op swiglu_down needs a forward workload with a down projection", file=sys.stderr)
             return 2
         return bench_swiglu_down(args, P, torch, np, wl, args.format, args.sparsity, dev, sptr)
-    sp = "none" if wl.backward else args.sparsity
-    out_t = "f32" if wl.backward else args.out
+    result = measure(args, P, torch, np, wl, fmt, args.sparsity, args.out, dev, sptr, run_stream,
+                     args.cpu_seconds, graph=bool(args.graph))
+    out = {
+        "metric": METRIC,
+        "value": result.pop("value"),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": result.pop("ms_per_step"),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp4",
+        "data": "synthetic",
+    }
+    out.update(result)
+    if not args.no_extra and args.workload == DEFAULT_WORKLOAD:
+        # the rest of the metric, measured in the same process: the other format on the
+        # same workload, the m = 512 block, prefill and the training backward
+        for name, wl_name, f, sp in EXTRA_ENTRIES:
+            torch.cuda.empty_cache()
+            if wl_name == args.workload and f == fmt:
+                continue
+            e = measure(args, P, torch, np, WORKLOADS[wl_name], f, sp, "f32", dev, sptr, run_stream,
+                        args.extra_cpu_seconds)
+            out[name] = e
+            print(f"bench.py: {name}: {e['ms_per_step']} ms/step, roofline frac "
+                  f"{e['roofline']['frac']}", file=sys.stderr, flush=True)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def measure(args, P, torch, np, wl, fmt, sparsity, out_t, dev, sptr, run_stream, cpu_seconds,
+            graph=False):
+    """One workload: setup (inputs resident in HBM, rotated copies), warmup, the timed steps,
+    kernel times from the library profiler, roofline of the GEMM and the oracle baseline.
+    Returns the result fields (value, ms_per_step, config, roofline, cpu_baseline, ...)."""
+    sp = "none" if wl.backward else sparsity
+    out_t = "f32" if wl.backward else out_t
     y_bytes = 4 if out_t == "f32" else 2
     if wl.backward:
         lin_state, run_linear, copies = setup_backward(P, torch, np, wl, fmt, dev, sptr)
     else:
-        lin_state, run_linear, copies = setup_forward(P, torch, np, wl, fmt, sp, dev, sptr,
-                                                      args.out)
+        lin_state, run_linear, copies = setup_forward(P, torch, np, wl, fmt, sp, dev, sptr, out_t)
 
     def run_step(i):
         for st in lin_state:
@@ -474,7 +540,7 @@ def main() -> int:
     dt = timed_loop(run_step)
     ms_per_step = dt * 1e3 / args.steps
     ms_graph = None
-    if args.graph:
+    if graph:
         # The same launches, captured once per rotated copy and replayed.
         graphs = []
         for c in range(copies):
@@ -483,6 +549,7 @@ def main() -> int:
                 run_step(c)
             graphs.append(g)
         ms_graph = timed_loop(lambda i: graphs[i % copies].replay()) * 1e3 / args.steps
+        del graphs
 
     # ---- kernel times: HIP events on the launch stream via the library profiler ----
     kinds = ("quant_rows", "quant_cols", "pack_hif4", "gemm") if wl.backward else \
@@ -503,11 +570,13 @@ def main() -> int:
             per_linear[st["lin"].name] = {k: round(P.resq_profile_read(k)[1] / args.steps * 1e3, 2)
                                           for k in kinds}
     P.resq_profile_enable(False)
+    del lin_state, run_linear
 
     lins = wl.linears
     if wl.backward:
         flops = sum(4 * wl.m * l.d * l.n for l in lins)  # dX and dW, 2mdn each
-        gexec = flops * (2 if fmt == "hif4" else 1)      # HiF4: hi and lo MFMA per term
+        gexec = flops                                    # no residual in the backward
+        gissued = flops * (2 if fmt == "hif4" else 1)
         gbytes = sum(BYTES_PER_ELEM[fmt] * 2 * (wl.m * l.n + l.n * l.d + wl.m * l.d)
                      + 4 * (wl.m * l.d + l.n * l.d) for l in lins)
         sbytes = sum(2 * (wl.m * l.n + wl.m * l.d + l.n * l.d) + 4 * (wl.m * l.d + l.n * l.d)
@@ -515,7 +584,8 @@ def main() -> int:
         n_launch = 2 * len(lins)
     else:
         flops = sum(alg_flops(wl.m, l.d, l.n, sp) for l in lins)
-        gexec = sum(exec_mfma_flops(wl.m, l.d, l.n, fmt, sp) for l in lins)
+        gexec = sum(executed_flops(wl.m, l.d, l.n, sp) for l in lins)
+        gissued = sum(issued_mfma_flops(wl.m, l.d, l.n, fmt, sp) for l in lins)
         gbytes = sum(gemm_bytes(wl.m, l.d, l.n, fmt, sp, y_bytes) for l in lins)
         sbytes = sum(step_bytes(wl.m, l.d, l.n, fmt, y_bytes) for l in lins)
         n_launch = len(lins)
@@ -523,38 +593,30 @@ def main() -> int:
     g_launch, g_ms = prof["gemm"]
     gemm_ms_step = g_ms / args.steps
     launch_s = gemm_ms_step / n_launch * 1e-3  # average GEMM launch
-    mfma_tflops = gexec / (gemm_ms_step * 1e-3) / 1e12
+    exec_tflops = gexec / (gemm_ms_step * 1e-3) / 1e12
     hbm_gbs = gbytes / n_launch / launch_s / 1e9  # algorithmic bytes per launch / launch time
     mfma_bound = wl.backward or wl.m >= 2048
     roofline = {
         "bound": "mfma" if mfma_bound else "hbm",
-        "achieved": round(mfma_tflops if mfma_bound else hbm_gbs, 1),
+        "achieved": round(exec_tflops if mfma_bound else hbm_gbs, 1),
         "peak": FP4_PEAK_TFLOPS if mfma_bound else HBM_PEAK_GBS,
         "unit": "TFLOP/s" if mfma_bound else "GB/s",
-        "frac": round(mfma_tflops / FP4_PEAK_TFLOPS if mfma_bound else hbm_gbs / HBM_PEAK_GBS, 4),
+        "frac": round(exec_tflops / FP4_PEAK_TFLOPS if mfma_bound else hbm_gbs / HBM_PEAK_GBS, 4),
         "traffic": gemm_traffic(wl.name, fmt, sp, out_t),
         "kernel": f"gemm_kernel ({n_launch} launches per step)",
         "alg_bytes_per_launch": round(gbytes / n_launch),
-        "alg_flops_per_launch": round(gexec / n_launch),
+        "exec_flops_per_launch": round(gexec / n_launch),
+        "flops_counted": "executed: 2mnd per term, the residual as a dense FP4 operand (Sec. 5.4 on gfx950)",
         "avg_launch_us": round(launch_s * 1e6, 2),
         "hbm_gbs": round(hbm_gbs, 1),
-        "mfma_exec_tflops": round(mfma_tflops, 1),
-        "mfma_exec_frac": round(mfma_tflops / FP4_PEAK_TFLOPS, 4),
+        "exec_tflops": round(exec_tflops, 1),
+        "exec_frac": round(exec_tflops / FP4_PEAK_TFLOPS, 4),
+        "alg_tflops": round(flops / (gemm_ms_step * 1e-3) / 1e12, 1),
+        "mfma_issued_tflops": round(gissued / (gemm_ms_step * 1e-3) / 1e12, 1),
     }
-
-    out = {
-        "metric": "ResQ FP4 linear TFLOP/s + % roofline (HBM GB/s decode, MFMA FP4 prefill)",
+    res = {
         "value": round(value, 3),
-        "unit": "TFLOP/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "fp4",
-        "data": "synthetic",
         "config": {
             "workload": wl.name,
             "format": fmt,
@@ -575,12 +637,12 @@ def main() -> int:
         "roofline": roofline,
     }
     if ms_graph is not None:
-        out["ms_per_step_graph_replay"] = round(ms_graph, 5)
+        res["ms_per_step_graph_replay"] = round(ms_graph, 5)
+    torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, fmt, sp, args.cpu_sample_cols, args.cpu_sample_rows,
-                                           args.cpu_seconds)
-    print(json.dumps(out), flush=True)
-    return 0
+        res["cpu_baseline"] = cpu_baseline(wl, fmt, sp, args.cpu_sample_cols, args.cpu_sample_rows,
+                                           cpu_seconds)
+    return res
 
 
 if __name__ == "__main__":

@@ -46,9 +46,12 @@ def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
 
     Inputs must be finite (the generators never produce NaN or Inf).
     """
-    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    lsb = (u >> 16) & 1
-    r = (u + 0x7FFF + lsb) >> 16
+    # for a finite float32 the sum below stays under 2^32 (the largest pattern, 0xFF7FFFFF,
+    # plus 0x8000), so 32-bit arithmetic is exact
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    r = u + np.uint32(0x7FFF)
+    r += (u >> 16) & np.uint32(1)
+    r >>= 16
     return r.astype(np.uint16)
 
 
@@ -151,18 +154,20 @@ WORKLOADS: Dict[str, Workload] = {
 }
 
 
-def workload_tensors(wl: Workload, linear: Linear, seed: int = 0, m: int | None = None):
+def workload_tensors(wl: Workload, linear: Linear, seed: int = 0, m: int | None = None,
+                     n_w: int | None = None):
     """Seeded (X, W[, dY]) bf16 bit arrays for one linear of a workload.
 
     Every linear gets its own child streams (keyed by its position in the workload), so a
     linear's tensors do not depend on which other linears are generated.  ``m`` overrides
-    the token count (used to take a bounded row sample of the same distribution).
+    the token count and ``n_w`` the number of weight rows (output features) drawn; both give
+    a prefix of the full draw (used to take a bounded sample of the same tensors).
     """
     idx = [l.name for l in wl.linears].index(linear.name)
     rx, rw, rg = rng_tree(seed * 1000 + idx, 3)
     mm = wl.m if m is None else m
     x = activations(rx, mm, linear.d, wl.outlier_frac, wl.outlier_scale, wl.dist)
-    w = weights(rw, linear.n, linear.d)
+    w = weights(rw, linear.n if n_w is None else min(n_w, linear.n), linear.d)
     if wl.backward:
         return x, w, grad_output(rg, mm, linear.n)
     return x, w

@@ -58,13 +58,28 @@ def test_gemm_bytes_by_hand():
     assert bench.step_bytes(m, d, n, "hif4") == 2 * m * d + n * d * 36 / 64 + 4 * m * n
 
 
-def test_issued_mfma_work():
-    """HiF4 issues two MFMAs (hi/lo operands) per term, MXFP4 one; every residual kind runs
-    as a dense operand."""
+def test_executed_and_issued_mfma_work():
+    """Executed work (the roofline's count): 2mdn per term, the residual dense on gfx950.
+    Issued MFMA work: HiF4 runs two MFMAs (hi/lo operands) per term, MXFP4 one."""
     m, d, n = 256, 2048, 2560
-    assert bench.exec_mfma_flops(m, d, n, "mxfp4", "none") == 2 * m * d * n
-    assert bench.exec_mfma_flops(m, d, n, "mxfp4", "2:4") == 4 * m * d * n
-    assert bench.exec_mfma_flops(m, d, n, "hif4", "unstructured25") == 8 * m * d * n
+    assert bench.executed_flops(m, d, n, "none") == 2 * m * d * n
+    assert bench.executed_flops(m, d, n, "2:4") == 4 * m * d * n
+    assert bench.executed_flops(m, d, n, "block32x64_50") == 4 * m * d * n
+    assert bench.issued_mfma_flops(m, d, n, "mxfp4", "2:4") == 4 * m * d * n
+    assert bench.issued_mfma_flops(m, d, n, "hif4", "none") == 4 * m * d * n
+    assert bench.issued_mfma_flops(m, d, n, "hif4", "unstructured25") == 8 * m * d * n
+
+
+def test_extra_entries_cover_the_metric():
+    """A default run also measures MXFP4 on the default block, the m = 512 block with each
+    global kind, prefill and the backward, each in both formats."""
+    names = {(w, f, s) for _, w, f, s in bench.EXTRA_ENTRIES} | {(bench.DEFAULT_WORKLOAD, "hif4", "2:4")}
+    for wl in ("qwen3b_layer_m256", "qwen7b_prefill_m8192"):
+        assert {(wl, "hif4", "2:4"), (wl, "mxfp4", "2:4")} <= names
+    for sp in ("channel50", "block32x64_50", "unstructured50"):
+        assert {("qwen7b_layer_m512", f, sp) for f in ("hif4", "mxfp4")} <= names
+    assert {("qwen3b_gateup_bwd_m8192", f, "none") for f in ("hif4", "mxfp4")} <= names
+    assert len({k for k, *_ in bench.EXTRA_ENTRIES}) == len(bench.EXTRA_ENTRIES)
 
 
 def test_traffic_lookup_misses_give_none():
