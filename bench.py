@@ -55,6 +55,11 @@ EXTRA_ENTRIES = (
     ("qwen7b_prefill_m8192_mxfp4", "qwen7b_prefill_m8192", "mxfp4", "2:4"),
     ("qwen3b_gateup_bwd_m8192_hif4", "qwen3b_gateup_bwd_m8192", "hif4", "none"),
     ("qwen3b_gateup_bwd_m8192_mxfp4", "qwen3b_gateup_bwd_m8192", "mxfp4", "none"),
+    # the mixed-precision alternatives of Table 1 on the default block
+    ("qwen3b_layer_m256_hif4_w4a16", "qwen3b_layer_m256", "hif4", "w4a16"),
+    ("qwen3b_layer_m256_hif4_w16a4", "qwen3b_layer_m256", "hif4", "w16a4"),
+    ("qwen3b_layer_m256_mxfp4_w4a16", "qwen3b_layer_m256", "mxfp4", "w4a16"),
+    ("qwen3b_layer_m256_mxfp4_w16a4", "qwen3b_layer_m256", "mxfp4", "w16a4"),
 )
 
 
@@ -331,6 +336,117 @@ def bench_swiglu_down(args, P, torch, np, wl, fmt, sp, dev, sptr):
     return 0
 
 
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+
+
+def measure_mixed(args, P, torch, np, wl, fmt, op, dev, sptr, cpu_seconds):
+    """The mixed-precision rollout linears of Table 1 on every linear of a forward workload:
+    op "w4a16" (Y = X Q(W)^T, Q(W) K-major, computed once before timing) or "w16a4" (Y =
+    Q(X) W^T, W bf16).  Both run on the bf16 MFMA; the roofline is the larger of the HBM time
+    of their algorithmic bytes and the bf16 MFMA time of 2mdn per linear."""
+    from synth import workload_tensors
+    f = P.FORMATS[fmt]
+    w4 = op == "w4a16"
+    wbytes = BYTES_PER_ELEM[fmt] if w4 else 2.0
+    per_copy = sum(wbytes * l.n * l.d + 2 * wl.m * l.d for l in wl.linears)
+    copies = int(min(64, max(2, -(-2 * LLC_BYTES // int(per_copy)) + 1)))
+    ws_bytes = max(P.resq_workspace_size(P.OP_LINEAR_W16A4, f, 0, wl.m, l.d, l.n) for l in wl.linears)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    lib = P.load()
+    state = []
+    for lin in wl.linears:
+        xb, wb = workload_tensors(wl, lin)
+        x0 = torch.from_numpy(xb.view(np.int16)).to(dev)
+        w0 = torch.from_numpy(wb.view(np.int16)).to(dev)
+        xs = [x0.clone() for _ in range(copies)]
+        ops = [P.quantize(w0, fmt, axis=1) for _ in range(copies)] if w4 else [w0.clone() for _ in range(copies)]
+        y = torch.empty((wl.m, lin.n), dtype=torch.float32, device=dev)
+        state.append((lin, xs, ops, y))
+        del x0, w0
+    torch.cuda.synchronize()
+
+    def step(i):
+        c = i % copies
+        for lin, xs, ops, y in state:
+            x = xs[c]
+            if w4:
+                qc, qs = ops[c]
+                rc = lib.resq_linear_w4a16(f, int(x.data_ptr()), wl.m, lin.d, lin.d, int(qc.data_ptr()),
+                                           int(qs.data_ptr()), lin.n, int(y.data_ptr()), lin.n, sptr)
+            else:
+                rc = lib.resq_linear_w16a4(f, int(x.data_ptr()), wl.m, lin.d, lin.d, int(ops[c].data_ptr()),
+                                           lin.d, lin.n, int(y.data_ptr()), lin.n, int(ws.data_ptr()),
+                                           ws_bytes, sptr)
+            if rc != 0:
+                raise P.ResqError(f"resq_linear_{op}: {P.resq_last_error()}", rc)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    P.resq_profile_enable(True)
+    P.resq_profile_reset()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    n_mixed, ms_mixed = P.resq_profile_read("mixed")
+    n_q, ms_q = P.resq_profile_read("quant_rows")
+    P.resq_profile_enable(False)
+    del state
+    torch.cuda.empty_cache()
+    flops = sum(2 * wl.m * l.d * l.n for l in wl.linears)
+    gbytes = sum(2 * wl.m * l.d + wbytes * l.n * l.d + 4 * wl.m * l.n for l in wl.linears)
+    gemm_s = ms_mixed / args.steps * 1e-3
+    t_hbm, t_mfma = gbytes / (HBM_PEAK_GBS * 1e9), flops / (BF16_PEAK_TFLOPS * 1e12)
+    mfma_bound = t_mfma > t_hbm
+    achieved = (flops / gemm_s / 1e12) if mfma_bound else (gbytes / gemm_s / 1e9)
+    peak = BF16_PEAK_TFLOPS if mfma_bound else HBM_PEAK_GBS
+    res = {
+        "value": round(flops * args.steps / dt / 1e12, 3),
+        "unit": "TFLOP/s",
+        "ms_per_step": round(dt * 1e3 / args.steps, 5),
+        "config": {"workload": wl.name, "format": fmt, "op": op,
+                   "precision": "weights FP4, activations bf16" if w4 else "activations FP4, weights bf16",
+                   "m": wl.m, "linears": {l.name: [l.d, l.n] for l in wl.linears}, "copies_rotated": copies},
+        "kernel_ms_per_step": {"mixed_gemm": round(ms_mixed / args.steps, 5),
+                               "quant_rows": round(ms_q / args.steps, 5)},
+        "roofline": {"bound": "mfma" if mfma_bound else "hbm", "achieved": round(achieved, 1), "peak": peak,
+                     "unit": "TFLOP/s" if mfma_bound else "GB/s", "frac": round(achieved / peak, 4),
+                     "traffic": None,
+                     "kernel": f"mixed_gemm_kernel ({len(wl.linears)} launches per step, bf16 MFMA)",
+                     "alg_bytes_per_launch": round(gbytes / len(wl.linears)),
+                     "alg_flops_per_launch": round(flops / len(wl.linears)),
+                     "avg_launch_us": round(gemm_s / len(wl.linears) * 1e6, 2)},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import resq as Q
+        from synth import bf16_bits_to_f32
+        rows, cols = min(wl.m, args.cpu_sample_rows), args.cpu_sample_cols
+        sample = []
+        for lin in wl.linears:
+            xb, wb = workload_tensors(wl, lin, m=rows, n_w=cols)
+            sample.append((bf16_bits_to_f32(xb), bf16_bits_to_f32(wb)))
+        fn = Q.w4a16_forward if w4 else Q.w16a4_forward
+        t0, reps, fl = time.perf_counter(), 0, 0
+        while True:
+            for x, w in sample:
+                fn(fmt, x, w)
+                fl += 2 * x.shape[0] * x.shape[1] * w.shape[0]
+            reps += 1
+            if time.perf_counter() - t0 >= cpu_seconds:
+                break
+        cdt = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": fl / cdt / 1e12, "unit": "TFLOP/s",
+                               "cores": len(os.sched_getaffinity(0)), "kind": "oracle",
+                               "sample": f"{wl.name}: the first {rows} rows and {cols} output features of "
+                                         f"every linear, {reps} repetition(s), {cdt:.1f} s; numpy fp64"}
+    return res
+
+
 def setup_forward(P, torch, np, wl, fmt, sp, dev, sptr, out="f32"):
     """Inputs resident in HBM (enough rotating copies to defeat the last-level cache) and a
     step function running every linear of the workload through resq_linear_fwd_prepared
@@ -410,9 +526,10 @@ def main() -> int:
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--format", default="hif4", choices=["hif4", "mxfp4"])
     ap.add_argument("--sparsity", default="2:4")
-    ap.add_argument("--op", default="linear", choices=["linear", "diagnostics", "swiglu_down"],
+    ap.add_argument("--op", default="linear", choices=["linear", "diagnostics", "swiglu_down", "w4a16", "w16a4"],
                     help="linear: the ResQ layer step; diagnostics: the Figs. 2-4 statistics pass; "
-                         "swiglu_down: the down projection with its SwiGLU input fused")
+                         "swiglu_down: the down projection with its SwiGLU input fused; w4a16 / "
+                         "w16a4: the mixed-precision linears of Table 1 on every linear")
     ap.add_argument("--outlier-threshold", type=float, default=10.0,
                     help="--op diagnostics: |x| above which a block counts as holding an outlier")
     ap.add_argument("--out", default="f32", choices=["f32", "bf16"],
@@ -477,6 +594,18 @@ def main() -> int:
             print("bench.py: --op swiglu_down needs a forward workload with a down projection", file=sys.stderr)
             return 2
         return bench_swiglu_down(args, P, torch, np, wl, args.format, args.sparsity, dev, sptr)
+    if args.op in ("w4a16", "w16a4"):
+        if wl.backward:
+            print(f"bench.py: --op {args.op} needs a forward workload", file=sys.stderr)
+            return 2
+        r = measure_mixed(args, P, torch, np, wl, fmt, args.op, dev, sptr, args.cpu_seconds)
+        out = {"metric": f"{args.op} rollout linear (Table 1) TFLOP/s", "value": r.pop("value"),
+               "unit": r.pop("unit"), "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+               "ms_per_step": r.pop("ms_per_step"), "higher_is_better": True, "scaling": "weak",
+               "vs_baseline": None, "dtype": "bf16", "data": "synthetic"}
+        out.update(r)
+        print(json.dumps(out), flush=True)
+        return 0
     result = measure(args, P, torch, np, wl, fmt, args.sparsity, args.out, dev, sptr, run_stream,
                      args.cpu_seconds, graph=bool(args.graph))
     out = {
@@ -501,8 +630,12 @@ def main() -> int:
             torch.cuda.empty_cache()
             if wl_name == args.workload and f == fmt:
                 continue
-            e = measure(args, P, torch, np, WORKLOADS[wl_name], f, sp, "f32", dev, sptr, run_stream,
-                        args.extra_cpu_seconds)
+            if sp in ("w4a16", "w16a4"):
+                e = measure_mixed(args, P, torch, np, WORKLOADS[wl_name], f, sp, dev, sptr,
+                                  args.extra_cpu_seconds)
+            else:
+                e = measure(args, P, torch, np, WORKLOADS[wl_name], f, sp, "f32", dev, sptr, run_stream,
+                            args.extra_cpu_seconds)
             out[name] = e
             print(f"bench.py: {name}: {e['ms_per_step']} ms/step, roofline frac "
                   f"{e['roofline']['frac']}", file=sys.stderr, flush=True)

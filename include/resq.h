@@ -103,7 +103,8 @@ typedef enum {
   RESQ_OP_LINEAR_FWD = 1,
   RESQ_OP_LINEAR_BWD = 2,
   RESQ_OP_LINEAR_FWD_PREPARED = 3,
-  RESQ_OP_DIAGNOSTICS = 4
+  RESQ_OP_DIAGNOSTICS = 4,
+  RESQ_OP_LINEAR_W16A4 = 5
 } resq_op;
 
 /*
@@ -278,6 +279,29 @@ int resq_diagnostics(int format, const uint16_t* X, int64_t m, int64_t d, int64_
 size_t resq_workspace_size(int op, int format, int sparsity, int64_t m, int64_t d, int64_t n);
 
 /*
+ * Mixed-precision rollout linears of the precision ablation (Sec. 4.2, Table 1, the W4A16
+ * and W16A4 rows): only one GEMM operand is FP4, the other stays bf16.  They measure the
+ * mixed-precision alternatives against which the paper argues for full FP4 GEMMs (Sec. 1).
+ *
+ * resq_linear_w4a16 - weight-only FP4: Y = X Q(W)^T (m x n float32, row stride ldy >= n).
+ *   X: m x d bf16, row stride ldx (ldx % 8 == 0, X 16-byte aligned).  Q(W): K-major codes
+ *   (n x d/2, 16-byte aligned) and scales (MXFP4 uint8 n x d/32; HiF4 uint32 n x d/64), as
+ *   resq_quantize writes them.  d must be a multiple of the format's block.  No workspace.
+ * resq_linear_w16a4 - activation-only FP4: Y = Q(X) W^T with Q(X) quantized along d inside
+ *   the call and W: n x d bf16, row stride ldw (ldw % 8 == 0, W 16-byte aligned).  Workspace:
+ *   resq_workspace_size(RESQ_OP_LINEAR_W16A4, format, 0, m, d, n) bytes (Q(X) codes and
+ *   scales), 256-byte aligned.
+ * Both compute in float32 on the bf16 MFMA: every FP4 value is exact in bf16, so every
+ * product is exact and only the accumulation rounds.  Errors as resq_linear_fwd.
+ */
+int resq_linear_w4a16(int format, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
+                      const uint8_t* qw_codes, const void* qw_scales, int64_t n, float* Y,
+                      int64_t ldy, void* stream);
+int resq_linear_w16a4(int format, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
+                      const uint16_t* W, int64_t ldw, int64_t n, float* Y, int64_t ldy,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * The GEMM plan a call of these sizes runs (host-side query; nothing is enqueued and no GPU
  * is needed).  The GEMM computes Y[M][N] = sum over K: the forward linear has M = m, N = n,
  * K = d and may split K (split_allowed = 1); the backward's dX GEMM has M = m, N = d, K = n,
@@ -304,7 +328,7 @@ const char* resq_version(void);
  * kernel trace measures it; the other families record them around the enqueue, which adds
  * the dispatch gap (a few microseconds).  resq_profile_read synchronizes the
  * recorded events and returns, for the kernel family `name` ("residual", "quant_rows",
- * "quant_cols", "pack_hif4", "select", "gemm", "diagnostics"), the number of launches and their summed
+ * "quant_cols", "pack_hif4", "select", "gemm", "diagnostics", "mixed"), the number of launches and their summed
  * duration in milliseconds since the last reset.  Returns RESQ_ERR_ARG for an unknown name.
  */
 int resq_profile_enable(int on);

@@ -14,8 +14,8 @@ Contents
 ``formats``  E2M1 / MXFP4 (paper Sec. 3, OCP MX block scaling) and HiF4 (paper Sec. 3,
              three-level hierarchical scaling, under the reading stated in that module).
 ``resq``     residual (Eq. 2), the sparsity functions S (Sec. 4.3), the forward of Eq. 1,
-             Eq. 3 and Eq. 4, the FP4 backward GEMMs of the training policy, and the
-             overhead cost model of Sec. 5.4.
+             Eq. 3 and Eq. 4, the mixed-precision W4A16 / W16A4 linears of Table 1, the FP4
+             backward GEMMs of the training policy, and the overhead cost model of Sec. 5.4.
 
 Pins: every function here is checked by ``tests/test_oracle_*.py`` against facts fixed
 outside this package (value sets, exhaustive bf16 sweeps against independent integer

@@ -29,6 +29,9 @@ Readings of points the paper leaves open (also listed in the design notes):
   Y1  Y, dX and dW are float32: the exact float64 result rounded once.
   Y2  the optional bf16 output is that float32 result rounded again, to the nearest bf16
       (ties to even): the rounding of the float32 result, not of the float64 one.
+  M1  the mixed-precision rollout linears of Table 1 keep one operand in its 16-bit form:
+      W4A16 is X Q(W)^T and W16A4 is Q(X) W^T, with Q along d as in Eq. 1 (the W4A8 row
+      needs an 8-bit activation format that the paper does not name, and is not built).
   F1  the fused producer of the down projection's input (the SwiGLU of the gate and up
       projections, X = silu(G) * U, silu(g) = g / (1 + exp(-g))): X is the bf16 nearest to the
       float64 value of silu(g) * u (ties to even), rounded once, so it is the bf16 activation
@@ -253,6 +256,24 @@ def resq_forward(fmt: str, sparsity: str, x: np.ndarray, w: np.ndarray) -> dict:
     out.update(qw_codes=qw_codes, qw_scales=qw_scales, what=what, y=y.astype(np.float32),
                y64=y)
     return out
+
+
+def w4a16_forward(fmt: str, x: np.ndarray, w: np.ndarray) -> dict:
+    """Weight-only FP4 rollout linear (Table 1, "W4A16"): the weights are quantized, the
+    activations stay in their 16-bit form.  Y = X Q(W)^T with Q(W) blocked along d, float64
+    products rounded to float32 once."""
+    what = F.dequantize(fmt, *F.quantize(fmt, w))
+    y = np.asarray(x, np.float64) @ what.astype(np.float64).T
+    return {"what": what, "y64": y, "y": y.astype(np.float32)}
+
+
+def w16a4_forward(fmt: str, x: np.ndarray, w: np.ndarray) -> dict:
+    """Activation-only FP4 rollout linear (Table 1, "W16A4"): the activations are quantized
+    (blocked along d, as in Eq. 1), the weights stay in their 16-bit form.  Y = Q(X) W^T,
+    float64 products rounded to float32 once."""
+    xhat = F.dequantize(fmt, *F.quantize(fmt, x))
+    y = xhat.astype(np.float64) @ np.asarray(w, np.float64).T
+    return {"xhat": xhat, "y64": y, "y": y.astype(np.float32)}
 
 
 def round_to_bf16(y32: np.ndarray) -> np.ndarray:

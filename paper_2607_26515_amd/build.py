@@ -16,7 +16,7 @@ OUT_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libresq.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["quant.hip", "pack.hip", "select.hip", "gemm.hip", "diag.hip", "api.cpp", "profiler.cpp"]
+SOURCES = ["quant.hip", "pack.hip", "select.hip", "gemm.hip", "diag.hip", "mixed.hip", "api.cpp", "profiler.cpp"]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     # packed-FP32 VALU forms are kept off; fp32 denormals are kept (exact FP4 rounding)

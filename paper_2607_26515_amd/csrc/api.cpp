@@ -328,6 +328,8 @@ size_t resq_workspace_size(int op, int format, int sparsity, int64_t m, int64_t 
     case RESQ_OP_LINEAR_FWD_PREPARED: return carve_fwd(nullptr, format, sp, m, d, n, nullptr);
     case RESQ_OP_LINEAR_BWD: return carve_bwd(nullptr, format, m, d, n, nullptr);
     case RESQ_OP_DIAGNOSTICS: return resq::diag_ws_bytes(m, d);
+    case RESQ_OP_LINEAR_W16A4:
+      return d % block_of(format) ? 0 : align256((size_t)m * d / 2) + align256(scale_bytes(format, m, d));
     default: return 0;
   }
 }
@@ -571,6 +573,76 @@ int resq_linear_fwd(int format, int sparsity, const uint16_t* X, int64_t m, int6
     resq::launch_pack(b_pack_mode(format), qw_codes, qw_scales, n, d, (uint8_t*)frag, (uint8_t*)fsc, s);
   }
   return linear_fwd_core(format, sp, X, m, d, ldx, wprep, n, Y, ldy, false, w, s);
+}
+
+namespace {
+
+int check_mixed_args(int format, const uint16_t* X, int64_t m, int64_t d, int64_t ldx, int64_t n,
+                     const void* Y, int64_t ldy) {
+  if (!valid_format(format)) return fail(RESQ_ERR_ARG, "unknown format %d", format);
+  if (m < 0 || d < 0 || n < 0) return fail(RESQ_ERR_ARG, "negative size");
+  if (ldx < d || ldy < n) return fail(RESQ_ERR_ARG, "ldx < d or ldy < n");
+  if (d % block_of(format) != 0)
+    return fail(RESQ_ERR_SHAPE, "d (%lld) is not a multiple of the block size %lld", (long long)d,
+                (long long)block_of(format));
+  if (m > 0 && n > 0 && !Y) return fail(RESQ_ERR_ARG, "Y is NULL");
+  if (m > 0 && d > 0 && (!X || (uintptr_t)X % 16 != 0 || ldx % 8 != 0))
+    return fail(RESQ_ERR_ARG, "X must be non-NULL, 16-byte aligned, with ldx %% 8 == 0");
+  return ok();
+}
+
+}  // namespace
+
+int resq_linear_w4a16(int format, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
+                      const uint8_t* qw_codes, const void* qw_scales, int64_t n, float* Y,
+                      int64_t ldy, void* stream) {
+  int rc = check_mixed_args(format, X, m, d, ldx, n, Y, ldy);
+  if (rc != RESQ_OK) return rc;
+  if (m == 0 || n == 0) return ok();
+  hipStream_t s = (hipStream_t)stream;
+  if (d == 0) {
+    if (ldy == n) resq::launch_zero_f32(Y, m * n, s);
+    else return fail(RESQ_ERR_UNSUPPORTED, "d = 0 needs ldy == n");
+    return check_launch("resq_linear_w4a16");
+  }
+  if (!qw_codes || !qw_scales || (uintptr_t)qw_codes % 16 != 0 ||
+      (format == RESQ_HIF4 && (uintptr_t)qw_scales % 4 != 0))
+    return fail(RESQ_ERR_ARG, "qw_codes must be 16-byte aligned (HiF4 scales 4-byte aligned)");
+  {
+    resq::ProfScope prof_(resq::kProfMixed, s, true);
+    resq::launch_mixed_gemm(format, false, m, n, d, X, ldx, qw_codes, qw_scales, Y, ldy, s);
+  }
+  return check_launch("resq_linear_w4a16");
+}
+
+int resq_linear_w16a4(int format, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
+                      const uint16_t* W, int64_t ldw, int64_t n, float* Y, int64_t ldy,
+                      void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_mixed_args(format, X, m, d, ldx, n, Y, ldy);
+  if (rc != RESQ_OK) return rc;
+  if (m == 0 || n == 0) return ok();
+  hipStream_t s = (hipStream_t)stream;
+  if (d == 0) {
+    if (ldy == n) resq::launch_zero_f32(Y, m * n, s);
+    else return fail(RESQ_ERR_UNSUPPORTED, "d = 0 needs ldy == n");
+    return check_launch("resq_linear_w16a4");
+  }
+  if (!W || (uintptr_t)W % 16 != 0 || ldw % 8 != 0 || ldw < d)
+    return fail(RESQ_ERR_ARG, "W must be non-NULL, 16-byte aligned, with ldw %% 8 == 0 and ldw >= d");
+  const size_t codes_bytes = align256((size_t)m * d / 2);
+  rc = check_ws(workspace, workspace_bytes, codes_bytes + align256(scale_bytes(format, m, d)));
+  if (rc != RESQ_OK) return rc;
+  uint8_t* codes = (uint8_t*)workspace;
+  void* scales = (char*)workspace + codes_bytes;
+  {
+    resq::ProfScope prof_(resq::kProfQuantRows, s);
+    resq::launch_quant_rows(format, X, false, m, d, ldx, codes, scales, s);
+  }
+  {
+    resq::ProfScope prof_(resq::kProfMixed, s, true);
+    resq::launch_mixed_gemm(format, true, m, n, d, W, ldw, codes, scales, Y, ldy, s);
+  }
+  return check_launch("resq_linear_w16a4");
 }
 
 int resq_diagnostics(int format, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,

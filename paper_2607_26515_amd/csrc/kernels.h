@@ -125,6 +125,14 @@ void gemm_plan_info(int fmt, int64_t M, int64_t N, int64_t K, bool may_split, in
 // scales, each 256-byte aligned) and the B buffer fit 32-bit offsets.
 bool gemm_supported(int fmt, int64_t M, int64_t N, int64_t K, int n_terms);
 
+// Mixed-precision GEMM (mixed.hip): Y[M][N] = A[M][K] B[N][K]^T in float32 on the bf16 MFMA,
+// one operand bf16 (`dense`, row-major, row stride ld) and the other FP4 (K-major codes and
+// scales of format fmt): A when a_quantized (W16A4), else B (W4A16).  dense must be 16-byte
+// aligned with ld % 8 == 0, codes 16-byte aligned, K a multiple of the format's block.
+void launch_mixed_gemm(int fmt, bool a_quantized, int64_t M, int64_t N, int64_t K, const uint16_t* dense,
+                       int64_t ld, const uint8_t* codes, const void* scales, float* Y, int64_t ldy,
+                       hipStream_t s);
+
 // p[0 .. n) = 0 (a fill kernel: callers may capture the library's launches in a graph).
 void launch_zero_f32(float* p, int64_t n, hipStream_t s);
 

@@ -47,7 +47,7 @@ void fold_locked() {
 }
 
 const char* kNames[kProfCount] = {"residual", "quant_rows", "quant_cols", "pack_hif4", "select", "gemm",
-                                  "diagnostics"};
+                                  "diagnostics", "mixed"};
 
 thread_local KernelEvents t_ev;
 thread_local bool t_ev_open = false;

@@ -8,7 +8,7 @@ namespace resq {
 
 enum ProfKernel {
   kProfResidual = 0, kProfQuantRows, kProfQuantCols, kProfPack, kProfSelect, kProfGemm, kProfDiag,
-  kProfCount
+  kProfMixed, kProfCount
 };
 
 // Returns a token for prof_end (negative when profiling is off).  With kernel_events, the

@@ -73,6 +73,7 @@ OK, ERR_ARG, ERR_SHAPE, ERR_UNSUPPORTED, ERR_HIP, ERR_WORKSPACE = 0, -1, -2, -3,
 IN_BF16, IN_F32 = 0, 1
 NOALLOC_SCRATCH_BYTES = 64 << 20  # RESQ_NOALLOC_SCRATCH_BYTES
 OP_RESIDUAL_SPARSIFY, OP_LINEAR_FWD, OP_LINEAR_BWD, OP_LINEAR_FWD_PREPARED, OP_DIAGNOSTICS = 0, 1, 2, 3, 4
+OP_LINEAR_W16A4 = 5
 DIAG_STATS = ("elements", "zeros_x", "zeros_qx", "blocks", "outlier_blocks", "energy_qx",
               "sse24_qx", "energy_qr", "sse24_qr")
 
@@ -81,7 +82,7 @@ EXPORTED = ("resq_quantize", "resq_residual_sparsify", "resq_linear_fwd", "resq_
             "resq_profile_reset", "resq_profile_read", "resq_prepared_weights_size",
             "resq_prepare_weights", "resq_linear_fwd_prepared", "resq_linear_fwd_prepared_bf16",
             "resq_diagnostics", "resq_linear_fwd_prepared_swiglu", "resq_gemm_plan",
-            "resq_linear_fwd_prepared_noalloc")
+            "resq_linear_fwd_prepared_noalloc", "resq_linear_w4a16", "resq_linear_w16a4")
 GEMM_TILES = {0: "64x64", 1: "128x256", 2: "128x192", 3: "128x192_8w"}
 
 
@@ -133,6 +134,10 @@ def load() -> ctypes.CDLL:
     lib.resq_profile_read.restype = i32
     lib.resq_linear_fwd_prepared_noalloc.argtypes = [i32, i32, vp, i64, i64, i64, vp, i64, vp, i64, vp]
     lib.resq_linear_fwd_prepared_noalloc.restype = i32
+    lib.resq_linear_w4a16.argtypes = [i32, vp, i64, i64, i64, vp, vp, i64, vp, i64, vp]
+    lib.resq_linear_w4a16.restype = i32
+    lib.resq_linear_w16a4.argtypes = [i32, vp, i64, i64, i64, vp, i64, i64, vp, i64, vp, sz, vp]
+    lib.resq_linear_w16a4.restype = i32
     lib.resq_gemm_plan.argtypes = [i32, i64, i64, i64, i32, ctypes.POINTER(ctypes.c_int32)]
     lib.resq_gemm_plan.restype = i32
     lib.resq_last_error.restype = ctypes.c_char_p
@@ -181,6 +186,15 @@ def resq_linear_fwd_prepared(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy, work
 
 def resq_linear_fwd_prepared_noalloc(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy, stream=0) -> int:
     return load().resq_linear_fwd_prepared_noalloc(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy, stream)
+
+
+def resq_linear_w4a16(fmt, X, m, d, ldx, qw_codes, qw_scales, n, Y, ldy, stream=0) -> int:
+    return load().resq_linear_w4a16(fmt, X, m, d, ldx, qw_codes, qw_scales, n, Y, ldy, stream)
+
+
+def resq_linear_w16a4(fmt, X, m, d, ldx, W, ldw, n, Y, ldy, workspace, workspace_bytes, stream=0) -> int:
+    return load().resq_linear_w16a4(fmt, X, m, d, ldx, W, ldw, n, Y, ldy, workspace, workspace_bytes,
+                                    stream)
 
 
 def resq_linear_fwd_prepared_bf16(fmt, sparsity, X, m, d, ldx, wprep, n, Y, ldy, workspace,
@@ -399,6 +413,36 @@ def linear_bwd(dy, x, w, fmt, want_dx=True, want_dw=True, ws=None, stream=None):
                          _stream(stream))
     _check(rc, "resq_linear_bwd")
     return dx, dw
+
+
+def linear_w4a16(x, qw_codes, qw_scales, fmt, y=None, stream=None):
+    """Weight-only FP4 (Table 1, W4A16): Y = X Q(W)^T, X bf16, Q(W) K-major (float32 Y)."""
+    import torch
+    m, d = x.shape
+    n = qw_codes.shape[0]
+    if y is None:
+        y = torch.empty((m, n), dtype=torch.float32, device=x.device)
+    rc = resq_linear_w4a16(_fmt(fmt), _p(x), m, d, x.stride(0), _p(qw_codes), _p(qw_scales), n,
+                           _p(y), y.stride(0), _stream(stream))
+    _check(rc, "resq_linear_w4a16")
+    return y
+
+
+def linear_w16a4(x, w, fmt, y=None, ws=None, stream=None):
+    """Activation-only FP4 (Table 1, W16A4): Y = Q(X) W^T, W bf16 (float32 Y)."""
+    import torch
+    m, d = x.shape
+    n = w.shape[0]
+    f = _fmt(fmt)
+    if y is None:
+        y = torch.empty((m, n), dtype=torch.float32, device=x.device)
+    if ws is None:
+        ws = workspace(OP_LINEAR_W16A4, f, S_NONE, m, d, n, x.device)
+    buf, nb = ws
+    rc = resq_linear_w16a4(f, _p(x), m, d, x.stride(0), _p(w), w.stride(0), n, _p(y), y.stride(0),
+                           _p(buf), nb, _stream(stream))
+    _check(rc, "resq_linear_w16a4")
+    return y
 
 
 def diagnostics(x, fmt, outlier_threshold, stream=None):

@@ -186,3 +186,19 @@ def test_noalloc_rejects_oversized_calls_on_the_host():
     assert rc == B.ERR_UNSUPPORTED and "scratch" in P.resq_last_error()
     assert P.resq_linear_fwd_prepared_noalloc(B.HIF4, 99, ptr, 4, 64, 64, ptr, n, ptr, n, 0) == B.ERR_ARG
     assert P.resq_linear_fwd_prepared_noalloc(B.HIF4, B.S_2_4, ptr, 0, 64, 64, ptr, n, ptr, n, 0) == B.OK
+
+
+def test_mixed_forms_check_arguments_on_the_host():
+    ptr = 1 << 20  # 16-byte aligned, never dereferenced
+    # misaligned X, ldx % 8 != 0, d not a multiple of the block, unknown format
+    assert P.resq_linear_w4a16(B.MXFP4, ptr + 2, 4, 64, 64, ptr, ptr, 8, ptr, 8, 0) == B.ERR_ARG
+    assert P.resq_linear_w4a16(B.MXFP4, ptr, 4, 64, 68, ptr, ptr, 8, ptr, 8, 0) == B.ERR_ARG
+    assert P.resq_linear_w4a16(B.HIF4, ptr, 4, 96, 96, ptr, ptr, 8, ptr, 8, 0) == B.ERR_SHAPE
+    assert P.resq_linear_w4a16(7, ptr, 4, 64, 64, ptr, ptr, 8, ptr, 8, 0) == B.ERR_ARG
+    # W16A4: W row stride, missing workspace
+    assert P.resq_linear_w16a4(B.MXFP4, ptr, 4, 64, 64, ptr, 60, 8, ptr, 8, ptr, 1 << 20, 0) == B.ERR_ARG
+    assert P.resq_linear_w16a4(B.MXFP4, ptr, 4, 64, 64, ptr, 64, 8, ptr, 8, 0, 0, 0) == B.ERR_WORKSPACE
+    # empty shapes are accepted without launching anything
+    assert P.resq_linear_w4a16(B.HIF4, ptr, 0, 64, 64, ptr, ptr, 8, ptr, 8, 0) == B.OK
+    # workspace: Q(X) codes and scales, each 256-byte aligned
+    assert P.resq_workspace_size(B.OP_LINEAR_W16A4, B.HIF4, 0, 100, 128, 8) == 6400 + 1024

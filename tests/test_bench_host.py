@@ -79,6 +79,8 @@ def test_extra_entries_cover_the_metric():
     for sp in ("channel50", "block32x64_50", "unstructured50"):
         assert {("qwen7b_layer_m512", f, sp) for f in ("hif4", "mxfp4")} <= names
     assert {("qwen3b_gateup_bwd_m8192", f, "none") for f in ("hif4", "mxfp4")} <= names
+    for op in ("w4a16", "w16a4"):
+        assert {("qwen3b_layer_m256", f, op) for f in ("hif4", "mxfp4")} <= names
     assert len({k for k, *_ in bench.EXTRA_ENTRIES}) == len(bench.EXTRA_ENTRIES)
 
 
