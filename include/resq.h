@@ -144,8 +144,8 @@ int resq_quantize(int format, const void* x, int in_dtype, int64_t rows, int64_t
  * rows 0..m-1 in order; a block's over its rows in order, each row adding its per-scale-block
  * partial sums (exact) in column order.
  * Alignment: codes 16 bytes, keep_mask and HiF4 scales 4 bytes (RESQ_ERR_ARG otherwise).
- * Limits (RESQ_ERR_UNSUPPORTED beyond): channel kinds d <= 24576; block kinds
- * ceil(m/32) * (d/64) <= 24576 blocks; element-wise kinds m * d <= 2^31.
+ * Limits (RESQ_ERR_UNSUPPORTED beyond): channel kinds d <= 2^31; block kinds
+ * ceil(m/32) * (d/64) <= 2^31 blocks; element-wise kinds m * d <= 2^31.
  * Workspace: resq_workspace_size(RESQ_OP_RESIDUAL_SPARSIFY, ...) bytes (0 for the local kinds).
  */
 int resq_residual_sparsify(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,

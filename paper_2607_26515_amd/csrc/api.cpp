@@ -398,7 +398,7 @@ int linear_fwd_core(int format, const Sp& sp, const uint16_t* X, int64_t m, int6
       const bool elem = sp.kind == RESQ_S_UNSTRUCT50;
       resq::launch_residual(format, resq::kResidDense, X, m, d, ldx, w.frag_x, w.fsc_x, w.qr_codes,
                             w.qr_scales, nullptr, sp.kind == RESQ_S_BLOCK32X64_50 ? w.partials : nullptr,
-                            s, true, elem ? w.sel.hist : nullptr, elem ? resq::select_hist_words() : 0,
+                            s, true, elem ? w.sel.hist : nullptr, elem ? resq::select_hist_words(m, d) : 0,
                             2, prod);
     }
     resq::ProfScope prof_(resq::kProfSelect, s);

@@ -76,22 +76,23 @@ struct SelectWs {
   uint32_t* hist;     // radix-select histograms / counters
   uint32_t* state;    // selection state (prefix, counts)
   uint8_t* group_bits;  // kept channels / blocks (bit mask)
+  uint32_t* super_counts;  // tie counts per group of workgroups (unstructured; cleared with hist)
   uint32_t* tie_counts;  // per-workgroup tie counts (unstructured)
 };
 size_t select_ws_bytes(int sparsity, int fmt, int64_t m, int64_t d);
-int64_t select_max_items();  // most channels / blocks a channel or block selection ranks
+int64_t select_max_items();  // most channels / blocks a channel or block selection ranks (2^31)
 void carve_select_ws(void* base, int sparsity, int fmt, int64_t m, int64_t d, SelectWs& ws);
 void launch_select(int fmt, int sparsity, int64_t m, int64_t d, int64_t keep, uint8_t* qr_codes,
                    const void* qr_scales, const double* partials, uint8_t* keep_mask,
                    uint8_t* group_mask, const SelectWs& ws, hipStream_t s);
 // The same selections for the forward GEMM: S(Q(dX)) is written as fragment-major operand
 // records (PackMode pack_mode) to frag / fscale; the K-major codes are left unpruned and no
-// masks are written.  For the element-wise kind the histogram (select_hist_words() words at
+// masks are written.  For the element-wise kind the histogram (select_hist_words(m, d) words at
 // ws.hist) must have been cleared beforehand (the residual pass does it).
 void launch_select_frag(int fmt, int sparsity, int64_t m, int64_t d, int64_t keep, uint8_t* qr_codes,
                         const void* qr_scales, const double* partials, const SelectWs& ws,
                         int pack_mode, uint8_t* frag, uint8_t* fscale, hipStream_t s);
-int select_hist_words();
+int select_hist_words(int64_t m, int64_t d);  // words to clear at ws.hist (histograms, group counts)
 
 // FP4 GEMM  Y[M][N] = sum_t A_t[M][K] B[N][K]^T  with A_t = Q(X) and optionally S(Q(dX)),
 // all operands fragment-major (pack.hip).  Operand A is one buffer holding the fragments and

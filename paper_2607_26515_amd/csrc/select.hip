@@ -157,7 +157,7 @@ __global__ __launch_bounds__(kThreads) void block_keys_kernel(const double* __re
   const int64_t nJ = d / 64, nI = (m + 31) / 32;
   const int64_t t = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (t >= nI * nJ) return;
-  const int64_t I = (uint32_t)t / (uint32_t)nJ, J = t - I * nJ;  // t < 2^15 (at most 24576 blocks)
+  const int64_t I = (int64_t)((uint64_t)t / (uint64_t)nJ), J = t - I * nJ;
   const int64_t r1 = (32 * I + 32 < m) ? 32 * I + 32 : m;
   const int64_t ld = d / (FMT == 0 ? 32 : 64);
   double v[32][P];
@@ -324,6 +324,79 @@ __global__ __launch_bounds__(kSelThreads) void select_top_kernel(const uint64_t*
   }
 }
 
+// ---------------------------------------------------------------------------------------
+// The same top-k for more keys than the registers hold (n > kKeysPerThread * kSelThreads):
+// each radix pass streams the keys from global memory (they stay in L2), and the threshold's
+// ties are ranked in index order chunk by chunk (1024 consecutive keys per chunk, one per
+// thread, a workgroup scan per chunk).  One workgroup, so no cross-workgroup protocol.
+// ---------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kSelThreads) void select_top_stream_kernel(const uint64_t* __restrict__ keys,
+                                                                        int64_t n, int64_t k,
+                                                                        uint8_t* __restrict__ bits,
+                                                                        uint8_t* __restrict__ bits_copy) {
+  constexpr int NW = kSelThreads / 64;
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t ch[2];
+  __shared__ uint32_t wsum[NW];
+  __shared__ uint64_t found;
+  const int tid = threadIdx.x, lane = tid & 63;
+  uint64_t prefix = 0, mask = 0;
+  uint32_t krem = (uint32_t)k;
+  for (int shift = 56; shift >= 0; shift -= 8) {
+    if (tid < 256) hist[tid] = 0;
+    __syncthreads();
+    for (int64_t base = 0; base < n; base += kSelThreads) {
+      const int64_t i = base + tid;
+      const uint64_t key = i < n ? keys[i] : 0;
+      hist_add(hist, (uint32_t)((key >> shift) & 255u), i < n && (key & mask) == prefix);
+    }
+    __syncthreads();
+    choose_digit<kSelThreads>(hist, 256, krem, wsum, ch);
+    prefix |= (uint64_t)ch[0] << shift;
+    krem = ch[1];
+    mask |= (uint64_t)255 << shift;
+    const uint32_t in_bin = hist[ch[0]];
+    __syncthreads();
+    if (in_bin == 1 && shift > 0) {
+      // a single key has this prefix: it is the threshold
+      for (int64_t base = 0; base < n; base += kSelThreads) {
+        const int64_t i = base + tid;
+        if (i < n && (keys[i] & mask) == prefix) found = keys[i];
+      }
+      __syncthreads();
+      prefix = found;
+      break;
+    }
+  }
+  const uint64_t T = prefix;
+  uint32_t seen = 0;  // ties in earlier chunks
+  for (int64_t base = 0; base < n; base += kSelThreads) {
+    const int64_t i = base + tid;
+    const bool in = i < n;
+    const uint64_t key = in ? keys[i] : 0;
+    const bool tie = in && key == T;
+    uint32_t total;
+    const uint32_t rank = seen + block_exclusive_scan<kSelThreads>(tie ? 1u : 0u, wsum, total);
+    const bool keep = in && (key > T || (tie && rank < krem));
+    const uint64_t bal = __ballot(keep);
+    if ((lane & 7) == 0 && in) {
+      const uint8_t byte = (uint8_t)(bal >> lane);
+      bits[i >> 3] = byte;
+      if (bits_copy) bits_copy[i >> 3] = byte;
+    }
+    seen += total;
+  }
+}
+
+void launch_top(const double* keys, int64_t n, int64_t k, uint8_t* bits, uint8_t* bits_copy, hipStream_t s) {
+  if (n <= (int64_t)kKeysPerThread * kSelThreads)
+    hipLaunchKernelGGL(select_top_kernel, dim3(1), dim3(kSelThreads), 0, s, (const uint64_t*)keys, n, k, bits,
+                       bits_copy);
+  else
+    hipLaunchKernelGGL(select_top_stream_kernel, dim3(1), dim3(kSelThreads), 0, s, (const uint64_t*)keys, n, k,
+                       bits, bits_copy);
+}
+
 // Apply kept channels (KIND 0) or kept blocks (KIND 1): one thread per code word; grid x
 // covers the d/8 words of a row, y the rows (grid-stride).
 template <int KIND>
@@ -362,8 +435,12 @@ constexpr int kUHist = 320;
 // workgroup's atomics.  Readers sum the copies.
 constexpr int kHistCopies = 32;
 
-__global__ void uzero_kernel(uint32_t* hist) {
-  for (int i = threadIdx.x; i < kHistCopies * kUHist; i += blockDim.x) hist[i] = 0;
+// Tie counts are summed per group of kSuper workgroups as well, so that a workgroup finds the
+// ties of all earlier workgroups in O(nwg / kSuper + kSuper) reads.
+constexpr int kSuper = 256;
+
+__global__ void uzero_kernel(uint32_t* hist, int words) {
+  for (int i = threadIdx.x; i < words; i += blockDim.x) hist[i] = 0;
 }
 
 template <int FMT>
@@ -448,6 +525,7 @@ __global__ __launch_bounds__(kThreads) void uties_kernel(const uint8_t* __restri
                                                          const void* __restrict__ scales, int64_t m,
                                                          int64_t d, uint32_t keep,
                                                          const uint32_t* __restrict__ hist,
+                                                         uint32_t* __restrict__ super_counts,
                                                          uint32_t* __restrict__ tie_counts) {
   __shared__ uint32_t lh[kUHist];
   __shared__ uint32_t ch[4];
@@ -464,7 +542,10 @@ __global__ __launch_bounds__(kThreads) void uties_kernel(const uint8_t* __restri
   }
   uint32_t total;
   block_exclusive_scan<kThreads>(ties, wsum, total);
-  if (threadIdx.x == 0) tie_counts[blockIdx.x] = total;
+  if (threadIdx.x == 0) {
+    tie_counts[blockIdx.x] = total;
+    if (total) atomicAdd(&super_counts[blockIdx.x / kSuper], total);  // integer sums: any order
+  }
 }
 
 // PMODE < 0: prune the codes in place (and write the keep mask).  PMODE >= 0: leave the codes
@@ -476,6 +557,7 @@ __global__ __launch_bounds__(kThreads) void uapply_kernel(uint8_t* __restrict__ 
                                                           const void* __restrict__ scales, int64_t m,
                                                           int64_t d, uint32_t keep,
                                                           const uint32_t* __restrict__ hist,
+                                                          const uint32_t* __restrict__ super_counts,
                                                           const uint32_t* __restrict__ tie_counts,
                                                           uint8_t* __restrict__ keep_mask,
                                                           uint8_t* __restrict__ frag,
@@ -485,9 +567,11 @@ __global__ __launch_bounds__(kThreads) void uapply_kernel(uint8_t* __restrict__ 
   __shared__ uint32_t wsum[kThreads / 64];
   load_choice(hist, lh, keep, true, wsum, ch);
   const uint32_t T = ch[2], krem = ch[3];
-  // ties kept by earlier workgroups
+  // ties of earlier workgroups: whole groups of kSuper workgroups, then this group's earlier ones
+  const uint32_t sb = blockIdx.x / kSuper;
   uint32_t before = 0;
-  for (int64_t w = threadIdx.x; w < (int64_t)blockIdx.x; w += kThreads) before += tie_counts[w];
+  for (uint32_t w = threadIdx.x; w < sb; w += kThreads) before += super_counts[w];
+  for (uint32_t w = sb * kSuper + threadIdx.x; w < blockIdx.x; w += kThreads) before += tie_counts[w];
   uint32_t tot_before;
   block_exclusive_scan<kThreads>(before, wsum, tot_before);
   const int64_t w0 = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * kWordsPerThread;
@@ -543,13 +627,18 @@ int64_t unstructured_wgs(int64_t m, int64_t d) {
   return (m * (d / 8) + per - 1) / per;
 }
 
+// words cleared before an element-wise selection: the histogram copies and the group counts
+int64_t hist_words(int64_t m, int64_t d) {
+  return (int64_t)kHistCopies * kUHist + (unstructured_wgs(m, d) + kSuper - 1) / kSuper;
+}
+
 size_t a256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 int64_t n_blocks(int64_t m, int64_t d) { return ((m + 31) / 32) * (d / 64); }
 
 }  // namespace
 
-int64_t select_max_items() { return (int64_t)kKeysPerThread * kSelThreads; }
+int64_t select_max_items() { return (int64_t)1 << 31; }
 
 size_t select_ws_bytes(int sparsity, int fmt, int64_t m, int64_t d) {
   (void)fmt;
@@ -559,7 +648,7 @@ size_t select_ws_bytes(int sparsity, int fmt, int64_t m, int64_t d) {
     case 4:  // block
       return a256((size_t)n_blocks(m, d) * 8) + a256((size_t)(n_blocks(m, d) + 31) / 32 * 4);
     case 5:  // element-wise
-      return a256(kHistCopies * kUHist * 4) + a256((size_t)unstructured_wgs(m, d) * 4);
+      return a256((size_t)hist_words(m, d) * 4) + a256((size_t)unstructured_wgs(m, d) * 4);
     default:
       return 0;
   }
@@ -575,7 +664,8 @@ void carve_select_ws(void* base, int sparsity, int fmt, int64_t m, int64_t d, Se
     ws.group_bits = (uint8_t*)(p + a256((size_t)n * 8));
   } else if (sparsity == 5) {
     ws.hist = (uint32_t*)p;
-    ws.tie_counts = (uint32_t*)(p + a256(kHistCopies * kUHist * 4));
+    ws.super_counts = ws.hist + kHistCopies * kUHist;
+    ws.tie_counts = (uint32_t*)(p + a256((size_t)hist_words(m, d) * 4));
   }
 }
 
@@ -588,8 +678,7 @@ void launch_select(int fmt, int sparsity, int64_t m, int64_t d, int64_t keep, ui
     const dim3 g((unsigned)((d + 63) / 64));
     if (fmt == 0) hipLaunchKernelGGL((channel_keys_kernel<0>), g, dim3(kChanThreads), 0, s, qr_codes, qr_scales, m, d, ws.keys);
     else hipLaunchKernelGGL((channel_keys_kernel<1>), g, dim3(kChanThreads), 0, s, qr_codes, qr_scales, m, d, ws.keys);
-    hipLaunchKernelGGL(select_top_kernel, dim3(1), dim3(kSelThreads), 0, s,
-                       (const uint64_t*)ws.keys, d, keep, ws.group_bits, group_mask);
+    launch_top(ws.keys, d, keep, ws.group_bits, group_mask, s);
     hipLaunchKernelGGL((apply_groups_kernel<0>), gw, dim3(kThreads), 0, s,
                        (uint32_t*)qr_codes, m, d, (const uint8_t*)ws.group_bits, keep_mask);
   } else if (sparsity == 4) {
@@ -597,21 +686,21 @@ void launch_select(int fmt, int sparsity, int64_t m, int64_t d, int64_t keep, ui
     const dim3 g((unsigned)((nb + kThreads - 1) / kThreads));
     if (fmt == 0) hipLaunchKernelGGL((block_keys_kernel<0>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
     else hipLaunchKernelGGL((block_keys_kernel<1>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
-    hipLaunchKernelGGL(select_top_kernel, dim3(1), dim3(kSelThreads), 0, s,
-                       (const uint64_t*)ws.keys, nb, keep, ws.group_bits, group_mask);
+    launch_top(ws.keys, nb, keep, ws.group_bits, group_mask, s);
     hipLaunchKernelGGL((apply_groups_kernel<1>), gw, dim3(kThreads), 0, s,
                        (uint32_t*)qr_codes, m, d, (const uint8_t*)ws.group_bits, keep_mask);
   } else if (sparsity == 5) {
     const unsigned nwg = (unsigned)unstructured_wgs(m, d);
-    hipLaunchKernelGGL(uzero_kernel, dim3(1), dim3(kThreads), 0, s, ws.hist);
+    hipLaunchKernelGGL(uzero_kernel, dim3(1), dim3(kThreads), 0, s, ws.hist, (int)hist_words(m, d));
     const uint32_t k = (uint32_t)keep;
 #define RESQ_U(F)                                                                                          \
     hipLaunchKernelGGL((uhist_kernel<F, 0>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k, ws.hist); \
     hipLaunchKernelGGL((uhist_kernel<F, 1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k, ws.hist); \
     hipLaunchKernelGGL((uties_kernel<F>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k,              \
-                       (const uint32_t*)ws.hist, ws.tie_counts);                                                      \
+                       (const uint32_t*)ws.hist, ws.super_counts, ws.tie_counts);                                     \
     hipLaunchKernelGGL((uapply_kernel<F, -1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k,         \
-                       (const uint32_t*)ws.hist, (const uint32_t*)ws.tie_counts, keep_mask, nullptr, nullptr);
+                       (const uint32_t*)ws.hist, (const uint32_t*)ws.super_counts, (const uint32_t*)ws.tie_counts,    \
+                       keep_mask, nullptr, nullptr);
     if (fmt == 0) { RESQ_U(0) } else { RESQ_U(1) }
 #undef RESQ_U
   }
@@ -633,24 +722,24 @@ void launch_select_frag(int fmt, int sparsity, int64_t m, int64_t d, int64_t kee
       if (fmt == 0) hipLaunchKernelGGL((block_keys_kernel<0>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
       else hipLaunchKernelGGL((block_keys_kernel<1>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
     }
-    hipLaunchKernelGGL(select_top_kernel, dim3(1), dim3(kSelThreads), 0, s, (const uint64_t*)ws.keys, n, keep,
-                       ws.group_bits, (uint8_t*)nullptr);
+    launch_top(ws.keys, n, keep, ws.group_bits, nullptr, s);
     launch_pack(pack_mode, qr_codes, qr_scales, m, d, frag, fscale, s, chan ? 1 : 2, ws.group_bits);
   } else if (sparsity == 5) {
-    const unsigned nwg = (unsigned)unstructured_wgs(m, d);  // the histogram was cleared by the residual pass
+    const unsigned nwg = (unsigned)unstructured_wgs(m, d);  // hist and group counts cleared by the residual pass
     const uint32_t k = (uint32_t)keep;
 #define RESQ_UF(F, P)                                                                                      \
     hipLaunchKernelGGL((uhist_kernel<F, 0>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k, ws.hist); \
     hipLaunchKernelGGL((uhist_kernel<F, 1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k, ws.hist); \
     hipLaunchKernelGGL((uties_kernel<F>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k,              \
-                       (const uint32_t*)ws.hist, ws.tie_counts);                                                      \
+                       (const uint32_t*)ws.hist, ws.super_counts, ws.tie_counts);                                     \
     hipLaunchKernelGGL((uapply_kernel<F, P>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k,          \
-                       (const uint32_t*)ws.hist, (const uint32_t*)ws.tie_counts, (uint8_t*)nullptr, frag, fscale);
+                       (const uint32_t*)ws.hist, (const uint32_t*)ws.super_counts, (const uint32_t*)ws.tie_counts,    \
+                       (uint8_t*)nullptr, frag, fscale);
     if (fmt == 0) { RESQ_UF(0, kPackMx) } else { RESQ_UF(1, kPackHiA) }
 #undef RESQ_UF
   }
 }
 
-int select_hist_words() { return kHistCopies * kUHist; }
+int select_hist_words(int64_t m, int64_t d) { return (int)hist_words(m, d); }
 
 }  // namespace resq
