@@ -628,8 +628,8 @@ def main() -> int:
         # same workload, the m = 512 block, prefill and the training backward
         for name, wl_name, f, sp in EXTRA_ENTRIES:
             torch.cuda.empty_cache()
-            if wl_name == args.workload and f == fmt:
-                continue
+            if wl_name == args.workload and f == fmt and sp == args.sparsity:
+                continue  # the headline itself
             if sp in ("w4a16", "w16a4"):
                 e = measure_mixed(args, P, torch, np, WORKLOADS[wl_name], f, sp, dev, sptr,
                                   args.extra_cpu_seconds)

@@ -43,6 +43,7 @@
 // every K range of fewer tiles (the ranges share no operand bytes).
 #include "kernels.h"
 #include "device_fp4.h"
+#include "gemm_geo.h"
 #include "profiler.h"
 
 
@@ -56,8 +57,6 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 constexpr int kXcds = 8;
-constexpr uint32_t kBad = 0xFFFFFFF0u;  // an offset past every operand: the load returns 0
-constexpr int kDumpBytes = 1024;         // LDS target of the padding copies (never read)
 
 struct GemmParams {
   int64_t M, N, K, nkb, mt_tiles, nt_tiles;
@@ -140,59 +139,6 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// Compile-time geometry of one configuration.
-template <int FMT, int WM, int WN, int TM, int TN, int NT, int NS, int KG>
-struct Geo {
-  static constexpr int WT = WM * WN;                  // waves per K group
-  static constexpr int W = WT * KG;                   // waves
-  static constexpr int kThreads = 64 * W;
-  static constexpr int MTW = WM * TM, NTW = WN * TN;  // row / column tiles per workgroup
-  static constexpr int FA = FMT == 0 ? 16 : 48;       // A lane record bytes (global)
-  static constexpr int FB = FMT == 0 ? 16 : 24;       // B lane record bytes (global)
-  static constexpr int PA = FA / 16;                  // A: 16-byte planes per fragment
-  static constexpr int A_FRAG = 64 * FA, B_FRAG = 64 * FB;  // bytes per fragment (global)
-  // LDS bytes per B fragment: a 12-byte copy lands each lane at a 16-byte stride
-  static constexpr int B_LDS = FMT == 0 ? 1024 : 2048;
-  static constexpr int SAJ = (MTW + 3) / 4;           // scale copies per A term (4 fragments each)
-  static constexpr int SBJ = (NTW + 3) / 4;
-  // LDS image of one K step: A [term][row tile][plane][64 x 16 B]; B [col tile] one 16-byte
-  // plane (MXFP4) or two planes of 12 bytes per lane at a 16-byte stride (HiF4); A scales
-  // [term][copy][4 x 64 B]; B scales [copy][4 x 64 B].  A stage holds KG such images (BLK
-  // bytes apart), then the padding copies' dump area.
-  static constexpr int B_OFF = NT * MTW * A_FRAG;
-  static constexpr int SA_OFF = B_OFF + NTW * B_LDS;
-  static constexpr int SB_OFF = SA_OFF + NT * SAJ * 256;
-  static constexpr int BLK = (SB_OFF + SBJ * 256 + 255) / 256 * 256;
-  static constexpr int DUMP_OFF = KG * BLK;  // padding copies
-  static constexpr int STAGE = DUMP_OFF + kDumpBytes;
-  // copy instructions per K step by class: A fragments (16 B per lane), B fragments (16 B
-  // per lane for MXFP4; two 12-byte halves for HiF4), scale bytes of A and B (4 B per lane);
-  // per stage KG times that; per wave: the class count rounded up to a multiple of W
-  static constexpr int JA1 = NT * MTW * PA, JB1 = FMT == 0 ? NTW : 2 * NTW, JS1 = NT * SAJ + SBJ;
-  static constexpr int JA = KG * JA1, JB = KG * JB1, JS = KG * JS1;
-  static constexpr int XA = (JA + W - 1) / W, XB = (JB + W - 1) / W, XS = (JS + W - 1) / W;
-  static constexpr int JW = XA + XB + XS;
-  static constexpr int SZB = FMT == 0 ? 16 : 12;
-  // the K groups' accumulators are summed through the (then idle) LDS of the stages
-  static constexpr int RED = (KG - 1) * WT * TM * TN * 16 * 64 * 4;
-  static constexpr size_t LDS = (size_t)(NS * STAGE > RED ? NS * STAGE : RED);
-  static size_t lds_bytes() { return LDS; }
-  static_assert(NS >= 2, "at least two stages");
-};
-
-// One copy instruction of a wave: this lane's source offset at K step 0 (kBad: no source,
-// the lane copies zeros) and the stage-relative LDS destination (the dump area for copies
-// that only pad the wave's count).  Each K step adds the class's step to the offset through
-// the instruction's scalar offset; a K step past the end is copied through a zero-size
-// buffer, so it reads zeros.
-struct Slot {
-  uint32_t voff, lds, kk;  // kk: the copy's K step within the stage
-};
-
-// HiF4 with more than one tile per wave keeps one register set and runs two waves per SIMD.
-template <int FMT, int TM, int TN>
-constexpr bool kSingleSet = FMT == 1 && TM * TN > 1;
-
 template <int FMT, int WM, int WN, int TM, int TN, int NT, int NS, int KG>
 __global__ __launch_bounds__(64 * WM * WN * KG)
 __attribute__((amdgpu_waves_per_eu(kSingleSet<FMT, TM, TN> ? 2 : KG)))
@@ -219,60 +165,27 @@ void gemm_kernel(GemmParams p) {
   const uint32_t kbeg = (uint32_t)(split * p.kper);                    // this split's K steps:
   const uint32_t klen = (uint32_t)min((int64_t)p.kper, p.nkb - kbeg);  // kbeg .. kbeg+klen-1
 
-  // ---- this wave's copy slots: copy jc of a class goes to wave jc % W ----
-  const uint32_t mt = (uint32_t)p.mt_tiles, nt = (uint32_t)p.nt_tiles;
+  // ---- this wave's copy slots: copy jc of a class goes to wave jc % W (gemm_geo.h) ----
+  SlotArgs sargs{};
+  for (int t = 0; t < 2; ++t) {
+    sargs.a_frag_off[t] = p.a_frag_off[t];
+    sargs.a_sc_off[t] = p.a_sc_off[t];
+  }
+  sargs.b_frag_off = p.b_frag_off;
+  sargs.b_sc_off = p.b_sc_off;
+  sargs.T0 = T0;
+  sargs.N0 = N0;
+  sargs.mt = (uint32_t)p.mt_tiles;
+  sargs.nt = (uint32_t)p.nt_tiles;
+  sargs.nkb = nkb;
   Slot sa[G::XA], sb[G::XB], ss[G::XS];
   bool ss_a[G::XS];  // scale slot reads operand A's buffer
 #pragma unroll
-  for (int x = 0; x < G::XA; ++x) {
-    const int jc = wave + G::W * x;
-    Slot c{kBad, (uint32_t)G::DUMP_OFF, 0u};
-    if (jc < G::JA) {
-      const int kk = jc / G::JA1, jl = jc % G::JA1;
-      const int t = jl / (G::MTW * G::PA), i = (jl / G::PA) % G::MTW, q = jl % G::PA;
-      c.voff = T0 + i < mt ? p.a_frag_off[t] + ((T0 + i) * nkb + kk) * G::A_FRAG + lane * G::FA + q * 16 : kBad;
-      c.lds = (uint32_t)(kk * G::BLK + (t * G::MTW + i) * G::A_FRAG + q * 1024);
-      c.kk = (uint32_t)kk;
-    }
-    sa[x] = c;
-  }
+  for (int x = 0; x < G::XA; ++x) sa[x] = slot_a<G>(wave, x, lane, sargs);
 #pragma unroll
-  for (int x = 0; x < G::XB; ++x) {
-    const int jc = wave + G::W * x;
-    Slot c{kBad, (uint32_t)G::DUMP_OFF, 0u};
-    if (jc < G::JB) {
-      const int kk = jc / G::JB1, jl = jc % G::JB1;
-      const int j = FMT == 0 ? jl : jl / 2, q = FMT == 0 ? 0 : jl % 2;
-      c.voff = N0 + j < nt ? p.b_frag_off + ((N0 + j) * nkb + kk) * G::B_FRAG + lane * G::FB + q * 12 : kBad;
-      c.lds = (uint32_t)(kk * G::BLK + G::B_OFF + j * G::B_LDS + q * 1024);
-      c.kk = (uint32_t)kk;
-    }
-    sb[x] = c;
-  }
+  for (int x = 0; x < G::XB; ++x) sb[x] = slot_b<G>(wave, x, lane, sargs);
 #pragma unroll
-  for (int x = 0; x < G::XS; ++x) {
-    const int jc = wave + G::W * x;
-    Slot c{kBad, (uint32_t)G::DUMP_OFF, 0u};
-    bool is_a = true;
-    if (jc < G::JS) {
-      const int kk = jc / G::JS1, jl = jc % G::JS1;
-      c.kk = (uint32_t)kk;
-      if (jl < NT * G::SAJ) {  // A scales: 4 fragments of one term, 16 lanes x 4 bytes each
-        const int t = jl / G::SAJ, i = 4 * (jl % G::SAJ) + lane / 16;
-        const bool ok = i < G::MTW && T0 + i < mt;
-        c.voff = ok ? p.a_sc_off[t] + ((T0 + i) * nkb + kk) * 64 + (lane % 16) * 4 : kBad;
-        c.lds = (uint32_t)(kk * G::BLK + G::SA_OFF + jl * 256);
-      } else {
-        const int q = jl - NT * G::SAJ, j = 4 * q + lane / 16;
-        const bool ok = j < G::NTW && N0 + j < nt;
-        c.voff = ok ? p.b_sc_off + ((N0 + j) * nkb + kk) * 64 + (lane % 16) * 4 : kBad;
-        c.lds = (uint32_t)(kk * G::BLK + G::SB_OFF + q * 256);
-        is_a = false;
-      }
-    }
-    ss[x] = c;
-    ss_a[x] = is_a;
-  }
+  for (int x = 0; x < G::XS; ++x) ss[x] = slot_s<G>(wave, x, lane, sargs, ss_a[x]);
 
   // Copy stage s of this split (its K steps kbeg + s*KG + kk, kk < KG) into stage buffer
   // `buf`; K steps past the split's end copy zeros (through a zero-size buffer).
@@ -668,36 +581,24 @@ Plan plan(int fmt, int64_t M, int64_t N, int64_t K, bool may_split) {
     const bool wide = M >= 512 && fmt == 0;
     pl.cfg = wide ? kWide : kMid;
     pl.tiles = wide ? wgs(4, 8) : wgs(4, 6);
+    pl.kg = 1;
+    pl.ns = fmt == 0 ? 4 : 2;  // HiF4's single register set fits two workgroups per CU at two stages
     // HiF4 grids below two workgroups per CU: eight waves per 128 x 192 tile (two per SIMD)
     if (fmt == 1 && pl.tiles < 2 * kCUs) pl.cfg = kMid8;
   }
   return pl;
 }
 
-template <int FMT>
-void launch_fmt(const GemmParams& p, int cfg, int kg, int ns, int n_terms, hipStream_t s) {
-  if (cfg == kSmall) {
-    if constexpr (FMT == 0) {
-      if (kg == 4) {
-        if (ns == 2) launch_cfg<FMT, 2, 2, 1, 1, 2, 4>(p, n_terms, s);
-        else launch_cfg<FMT, 2, 2, 1, 1, 4, 4>(p, n_terms, s);
-      } else if (kg == 1) {
-        launch_cfg<FMT, 2, 2, 1, 1, 4, 1>(p, n_terms, s);
-      } else {
-        launch_cfg<FMT, 2, 2, 1, 1, 4, 2>(p, n_terms, s);
-      }
-    } else {
-      if (kg == 1) launch_cfg<FMT, 2, 2, 1, 1, 2, 1>(p, n_terms, s);
-      else if (ns == 2) launch_cfg<FMT, 2, 2, 1, 1, 2, 2>(p, n_terms, s);
-      else launch_cfg<FMT, 2, 2, 1, 1, 4, 2>(p, n_terms, s);
-    }
-  } else if (cfg == kWide) {
-    if constexpr (FMT == 0) launch_cfg<FMT, 2, 2, 2, 4, 4>(p, n_terms, s);  // MXFP4 only
-  } else if (cfg == kMid8) {
-    if constexpr (FMT == 1) launch_cfg<FMT, 4, 2, 1, 3, 2>(p, n_terms, s);  // HiF4 only
-  } else {
-    launch_cfg<FMT, 2, 2, 2, 3, FMT == 0 ? 4 : 2>(p, n_terms, s);
+// Launches the configuration of the plan (one of RESQ_GEMM_CONFIGS); false if none matches.
+bool launch_plan(const GemmParams& p, int fmt, const Plan& pl, int n_terms, hipStream_t s) {
+#define RESQ_GEMM_LAUNCH(F, C, WM, WN, TM, TN, NS, KG)                                  \
+  if (fmt == F && pl.cfg == C && pl.ns == NS && pl.kg == KG) {                          \
+    launch_cfg<F, WM, WN, TM, TN, NS, KG>(p, n_terms, s);                               \
+    return true;                                                                          \
   }
+  RESQ_GEMM_CONFIGS(RESQ_GEMM_LAUNCH)
+#undef RESQ_GEMM_LAUNCH
+  return false;
 }
 
 }  // namespace
@@ -722,8 +623,8 @@ void gemm_plan_info(int fmt, int64_t M, int64_t N, int64_t K, bool may_split, in
   const Plan pl = plan(fmt, M, N, K, may_split);
   info[0] = pl.cfg;
   info[1] = pl.ksplit;
-  info[2] = pl.cfg == kSmall ? pl.kg : 1;
-  info[3] = pl.cfg == kSmall ? pl.ns : pl.cfg == kWide ? 4 : pl.cfg == kMid8 ? 2 : (fmt == 0 ? 4 : 2);
+  info[2] = pl.kg;
+  info[3] = pl.ns;
 }
 
 bool launch_gemm(const GemmOperands& op, hipStream_t s) {
@@ -753,9 +654,7 @@ bool launch_gemm(const GemmOperands& op, hipStream_t s) {
   }
   p.b_frag_off = (uint32_t)op.b_frag_off; p.b_sc_off = (uint32_t)op.b_sc_off;
   p.Y = op.Y; p.ldy = op.ldy; p.out_bf16 = op.out_bf16 ? 1 : 0;
-  if (op.fmt == 0) launch_fmt<0>(p, pl.cfg, pl.kg, pl.ns, op.n_terms, s);
-  else launch_fmt<1>(p, pl.cfg, pl.kg, pl.ns, op.n_terms, s);
-  return true;
+  return launch_plan(p, op.fmt, pl, op.n_terms, s);
 }
 
 }  // namespace resq

@@ -12,9 +12,18 @@
 //
 // Data movement: a workgroup of 2 x 2 waves owns a (64 TM) x (64 TN) output tile; per K
 // chunk of 64 each thread loads its share of both operands into registers (16-byte loads of
-// bf16 rows or of FP4 codes), the workgroup writes them to LDS as bf16 rows (K contiguous,
-// rows padded by 16 bytes), and each wave runs TM x TN x 4 MFMAs (K = 16 each) from LDS.  The
-// next chunk's global loads are issued before the current chunk's MFMAs.
+// bf16 rows or of FP4 codes), the workgroup writes them to one of two LDS buffers as bf16
+// rows (K contiguous, rows padded by 16 bytes; FP4 codes dequantized on the way), and each
+// wave runs TM x TN x 4 MFMAs (K = 16 each) from LDS.  Global loads run two chunks ahead of
+// the MFMAs (two register stages), so each load's latency is covered by two chunks of work;
+// one barrier per chunk.  Tall tiles (TM up to 4, i.e. every row of a 256-token decode batch)
+// spread the dequantization of a weight chunk over more output rows; small grids with long K
+// split each tile's chunks over four K groups of waves.
+//
+// Dequantization: MXFP4 pairs go through gfx950's scaled conversion to bf16
+// (v_cvt_scalef32_pk_bf16_fp4, scale 2^E, exact); a HiF4 element is the integer k (4 + m)
+// converted to float32 (exact) and scaled by 2^(e-35-b) with v_ldexp_f32 (exact), whose top
+// half is its bf16 pattern.
 //
 // MFMA operand layout (32x32x16 bf16): lane l holds row (A) / column (B) l % 32 and the 8
 // consecutive K elements 8 (l / 32) .. + 7 of the 16-wide step.  Accumulator register r of
@@ -48,29 +57,38 @@ struct MixedParams {
   int64_t ldy;
 };
 
+typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+
+// 2^E as float32 for an E8M0 code (E = code - 127; 2^-127 is a float32 subnormal).
+__device__ __forceinline__ float e8m0_f32(uint32_t code) {
+  return code ? __uint_as_float(code << 23) : __uint_as_float(0x00400000u);
+}
+
 // Eight FP4 elements (one 32-bit word of codes, element 8w+i in nibble i) dequantized to bf16
-// bits, exact.  MXFP4: magnitude in {0, .5, 1, 1.5, 2, 3, 4, 6} times 2^E; HiF4: k (4+m)
-// 2^(e-35-b) with b the level-2 + level-3 shift of each element's groups.
+// bits, exact, two per output word.  MXFP4: E2M1 magnitude times 2^E; HiF4: k (4+m)
+// 2^(e-35-b) with b the level-2 + level-3 shift of each element's groups (elem0 = the first
+// element's index inside its 64-block; pairs share their level-3 group).
 template <int FMT>
 __device__ __forceinline__ void dequant8(uint32_t w, int elem0, uint32_t scale, uint32_t out[4]) {
-  uint32_t h[8];
+  if constexpr (FMT == 0) {
+    const float sc = e8m0_f32(scale);
+    out[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 0));
+    out[1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 1));
+    out[2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 2));
+    out[3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 3));
+  } else {
+    const uint32_t f = 4u + (scale & 3u);
+    const int e = (int)((scale >> 2) & 63u) - 35;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const uint32_t c = (w >> (4 * i)) & 15u;
-    float v;
-    if constexpr (FMT == 0) {
-      v = ldexpf(e2m1_mag(c & 7u), (int)scale - 127);
-    } else {
-      const int e = (int)(scale & 0xFFu) >> 2, m = (int)(scale & 3u);
-      const int el = elem0 + i;  // element index inside the 64-block
-      const int b = (int)((scale >> (8 + el / 8)) & 1u) + (int)((scale >> (16 + el / 4)) & 1u);
-      v = ldexpf((float)((c & 7u) * (uint32_t)(4 + m)), e - 35 - b);
+    for (int i = 0; i < 4; ++i) {
+      const int el = elem0 + 2 * i;  // both elements of the pair share level-2/3 groups
+      const int sh = e - (int)((scale >> (8 + el / 8)) & 1u) - (int)((scale >> (16 + el / 4)) & 1u);
+      const uint32_t c0 = (w >> (8 * i)) & 15u, c1 = (w >> (8 * i + 4)) & 15u;
+      const uint32_t u0 = __float_as_uint(ldexpf((float)((c0 & 7u) * f), sh)) | ((c0 & 8u) << 28);
+      const uint32_t u1 = __float_as_uint(ldexpf((float)((c1 & 7u) * f), sh)) | ((c1 & 8u) << 28);
+      out[i] = (u0 >> 16) | (u1 & 0xFFFF0000u);  // exact: at most 6 significant bits
     }
-    const uint32_t u = __float_as_uint(v) | ((c & 8u) << 28);  // the code's sign, -0 kept
-    h[i] = u >> 16;  // exact: at most 6 significant bits
   }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) out[i] = h[2 * i] | (h[2 * i + 1] << 16);
 }
 
 // Per-thread staging of one operand's K chunk.  Dense: R rows x 64 bf16 = 8 R 16-byte pieces,
@@ -155,30 +173,54 @@ __device__ __forceinline__ void store_quant(const QuantStage<R>& st, uint16_t* l
   }
 }
 
-// AQ: operand A (rows of Y) is the FP4 one (W16A4); otherwise operand B is (W4A16).
-template <int FMT, bool AQ, int TM, int TN>
-__global__ __launch_bounds__(256) void mixed_gemm_kernel(MixedParams p) {
+// AQ: operand A (rows of Y) is the FP4 one (W16A4); otherwise operand B is (W4A16).  KG K
+// groups of four waves share the output tile: group g takes chunks g, g + KG, ... with its own
+// LDS buffers and register stages, and at the end groups 1.. park their accumulators in LDS
+// and group 0 adds them in group order (deterministic) and stores the tile.
+template <int FMT, bool AQ, int TM, int TN, int KG>
+__global__ __launch_bounds__(256 * KG) void mixed_gemm_kernel(MixedParams p) {
   constexpr int BM = 64 * TM, BN = 64 * TN;
-  __shared__ __attribute__((aligned(16))) uint16_t As[BM * kRowHalves];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[BN * kRowHalves];
+  constexpr int PER = TM * TN * 16 * 64;  // accumulator floats per wave
+  union Smem {
+    struct {
+      uint16_t A[KG][2][BM * kRowHalves];
+      uint16_t B[KG][2][BN * kRowHalves];
+    } t;
+    float red[KG > 1 ? (KG - 1) * 4 * PER : 1];
+  };
+  __shared__ __attribute__((aligned(16))) Smem sm;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave % 2, wn = wave / 2;
+  const int g = wave / 4, wl = wave % 4, tg = tid % 256;  // K group, wave and thread within it
+  const int wm = wl % 2, wn = wl / 2;
   const int64_t row0 = (int64_t)blockIdx.y * BM, col0 = (int64_t)blockIdx.x * BN;
   const int64_t nchunks = (p.K + kChunk - 1) / kChunk;
+  const int64_t nq = nchunks > g ? (nchunks - g + KG - 1) / KG : 0;  // this group's chunks
+  const int64_t nrounds = (nchunks + KG - 1) / KG;                   // group 0's count
+  uint16_t(*As)[BM * kRowHalves] = sm.t.A[g];
+  uint16_t(*Bs)[BN * kRowHalves] = sm.t.B[g];
 
   using AStage = typename std::conditional<AQ, QuantStage<BM>, DenseStage<BM>>::type;
   using BStage = typename std::conditional<AQ, DenseStage<BN>, QuantStage<BN>>::type;
-  AStage sa;
-  BStage sb;
-  auto load = [&](int64_t c) {
-    const int64_t k0 = c * kChunk;
+  AStage sa[2];
+  BStage sb[2];
+  auto load = [&](int64_t q, int r) {
+    const int64_t k0 = (q * KG + g) * kChunk;
     if constexpr (AQ) {
-      load_quant<FMT, BM>(sa, p.codes, p.scales, row0, p.M, k0, p.K, tid);
-      load_dense<BN>(sb, p.dense, p.ld, col0, p.N, k0, p.K, tid);
+      load_quant<FMT, BM>(sa[r], p.codes, p.scales, row0, p.M, k0, p.K, tg);
+      load_dense<BN>(sb[r], p.dense, p.ld, col0, p.N, k0, p.K, tg);
     } else {
-      load_dense<BM>(sa, p.dense, p.ld, row0, p.M, k0, p.K, tid);
-      load_quant<FMT, BN>(sb, p.codes, p.scales, col0, p.N, k0, p.K, tid);
+      load_dense<BM>(sa[r], p.dense, p.ld, row0, p.M, k0, p.K, tg);
+      load_quant<FMT, BN>(sb[r], p.codes, p.scales, col0, p.N, k0, p.K, tg);
+    }
+  };
+  auto store = [&](int r, int buf) {
+    if constexpr (AQ) {
+      store_quant<FMT, BM>(sa[r], As[buf], tg);
+      store_dense<BN>(sb[r], Bs[buf], tg);
+    } else {
+      store_dense<BM>(sa[r], As[buf], tg);
+      store_quant<FMT, BN>(sb[r], Bs[buf], tg);
     }
   };
 
@@ -190,17 +232,7 @@ __global__ __launch_bounds__(256) void mixed_gemm_kernel(MixedParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  load(0);
-  for (int64_t c = 0; c < nchunks; ++c) {
-    if constexpr (AQ) {
-      store_quant<FMT, BM>(sa, As, tid);
-      store_dense<BN>(sb, Bs, tid);
-    } else {
-      store_dense<BM>(sa, As, tid);
-      store_quant<FMT, BN>(sb, Bs, tid);
-    }
-    __syncthreads();
-    if (c + 1 < nchunks) load(c + 1);  // in flight during this chunk's MFMAs
+  auto compute = [&](int buf) {
 #pragma unroll
     for (int kk = 0; kk < kChunk / 16; ++kk) {
       const int koff = 16 * kk + 8 * (lane / 32);
@@ -208,19 +240,67 @@ __global__ __launch_bounds__(256) void mixed_gemm_kernel(MixedParams p) {
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int r = (wm * TM + i) * 32 + lane % 32;
-        a[i] = __builtin_bit_cast(v8bf, *reinterpret_cast<const v4u*>(As + r * kRowHalves + koff));
+        a[i] = __builtin_bit_cast(v8bf, *reinterpret_cast<const v4u*>(As[buf] + r * kRowHalves + koff));
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int r = (wn * TN + j) * 32 + lane % 32;
-        b[j] = __builtin_bit_cast(v8bf, *reinterpret_cast<const v4u*>(Bs + r * kRowHalves + koff));
+        b[j] = __builtin_bit_cast(v8bf, *reinterpret_cast<const v4u*>(Bs[buf] + r * kRowHalves + koff));
       }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
-    __syncthreads();  // every wave is done reading this chunk before the next one is stored
+  };
+
+  // The group's chunk q sits in register stage q % 2 from its load (two chunks ahead) until
+  // its store into LDS buffer q % 2, one chunk ahead of its MFMAs.  Each round: issue chunk
+  // q+2's loads, run chunk q's MFMAs, store chunk q+1 into the other buffer (last read during
+  // chunk q-1, which the previous barrier closed), barrier.  Every group runs group 0's round
+  // count (it has the most chunks), so all waves meet at every barrier.
+  if (nq > 0) load(0, 0);
+  if (nq > 1) load(1, 1);
+  if (nq > 0) store(0, 0);
+  __syncthreads();
+  for (int64_t q0 = 0; q0 < nrounds; q0 += 2) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int64_t q = q0 + u;
+      if (q < nrounds) {
+        if (q < nq) {
+          if (q + 2 < nq) load(q + 2, u);
+          compute(u);
+          if (q + 1 < nq) store(1 - u, 1 - u);
+        }
+        __syncthreads();
+      }
+    }
+  }
+
+  if constexpr (KG > 1) {
+    // every wave is past its last LDS read (the loop's final barrier): reuse LDS for the sums
+    if (g > 0) {
+      float* dst = sm.red + ((size_t)(g - 1) * 4 + wl) * PER;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) dst[((i * TN + j) * 16 + r) * 64 + lane] = acc[i][j][r];
+    }
+    __syncthreads();
+    if (g > 0) return;
+#pragma unroll
+    for (int gg = 1; gg < KG; ++gg) {
+      const float* src = sm.red + ((size_t)(gg - 1) * 4 + wl) * PER;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[i][j][r] += src[((i * TN + j) * 16 + r) * 64 + lane];
+    }
   }
 
   const int half = lane >> 5, l32 = lane & 31;
@@ -237,16 +317,32 @@ __global__ __launch_bounds__(256) void mixed_gemm_kernel(MixedParams p) {
     }
 }
 
+template <int FMT, bool AQ, int TM, int TN, int KG>
+void launch_tile(const MixedParams& p, hipStream_t s) {
+  const dim3 grid((unsigned)((p.N + 64 * TN - 1) / (64 * TN)), (unsigned)((p.M + 64 * TM - 1) / (64 * TM)));
+  launch_timed(mixed_gemm_kernel<FMT, AQ, TM, TN, KG>, grid, dim3(256 * KG), 0u, s, p);
+}
+
+// Tile choice: the FP4 operand's dequantization is shared by the rows (W4A16) or columns
+// (W16A4) of the tile, so the tile is as long as possible along the other operand while the
+// grid still has at least 128 workgroups; the other side stays 64 wide.  Grids of 64 x 64
+// tiles within the CUs that have at least 16 K chunks take four K groups per workgroup.
 template <int FMT, bool AQ>
 void launch_fmt(const MixedParams& p, hipStream_t s) {
-  // 128 x 128 tiles when they give at least one workgroup per CU, else 64 x 64
-  const int64_t big = ((p.M + 127) / 128) * ((p.N + 127) / 128);
-  if (big >= 256) {
-    const dim3 grid((unsigned)((p.N + 127) / 128), (unsigned)((p.M + 127) / 128));
-    launch_timed(mixed_gemm_kernel<FMT, AQ, 2, 2>, grid, dim3(256), 0u, s, p);
+  const int64_t along = AQ ? p.N : p.M, across = AQ ? p.M : p.N;
+  auto wgs = [&](int64_t t) { return ((along + 64 * t - 1) / (64 * t)) * ((across + 63) / 64); };
+  const int t = wgs(4) >= 128 ? 4 : wgs(2) >= 128 ? 2 : 1;
+  const bool kgroups = t == 1 && wgs(1) <= 256 && (p.K + kChunk - 1) / kChunk >= 16;
+  if constexpr (AQ) {
+    if (t == 4) launch_tile<FMT, AQ, 1, 4, 1>(p, s);
+    else if (t == 2) launch_tile<FMT, AQ, 1, 2, 1>(p, s);
+    else if (kgroups) launch_tile<FMT, AQ, 1, 1, 4>(p, s);
+    else launch_tile<FMT, AQ, 1, 1, 1>(p, s);
   } else {
-    const dim3 grid((unsigned)((p.N + 63) / 64), (unsigned)((p.M + 63) / 64));
-    launch_timed(mixed_gemm_kernel<FMT, AQ, 1, 1>, grid, dim3(256), 0u, s, p);
+    if (t == 4) launch_tile<FMT, AQ, 4, 1, 1>(p, s);
+    else if (t == 2) launch_tile<FMT, AQ, 2, 1, 1>(p, s);
+    else if (kgroups) launch_tile<FMT, AQ, 1, 1, 4>(p, s);
+    else launch_tile<FMT, AQ, 1, 1, 1>(p, s);
   }
 }
 
