@@ -310,7 +310,8 @@ int resq_linear_w16a4(int format, const uint16_t* X, int64_t m, int64_t d, int64
  * [2] K groups per workgroup, [3] LDS pipeline stages.  Returns RESQ_ERR_ARG for an unknown
  * format, negative sizes or a NULL info.
  */
-enum { RESQ_TILE_64x64 = 0, RESQ_TILE_128x256 = 1, RESQ_TILE_128x192 = 2, RESQ_TILE_128x192_8W = 3 };
+enum { RESQ_TILE_64x64 = 0, RESQ_TILE_128x256 = 1, RESQ_TILE_128x192 = 2, RESQ_TILE_128x192_8W = 3,
+       RESQ_TILE_64x128 = 4 };
 int resq_gemm_plan(int format, int64_t M, int64_t N, int64_t K, int split_allowed, int32_t info[4]);
 
 /* Human-readable description of the last non-OK status on this thread ("" if none). */

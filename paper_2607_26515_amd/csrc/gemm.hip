@@ -167,10 +167,10 @@ void gemm_kernel(GemmParams p) {
 
   // ---- this wave's copy slots: copy jc of a class goes to wave jc % W (gemm_geo.h) ----
   SlotArgs sargs{};
-  for (int t = 0; t < 2; ++t) {
-    sargs.a_frag_off[t] = p.a_frag_off[t];
-    sargs.a_sc_off[t] = p.a_sc_off[t];
-  }
+  sargs.a_frag0 = p.a_frag_off[0];
+  sargs.a_frag1 = p.a_frag_off[1];
+  sargs.a_sc0 = p.a_sc_off[0];
+  sargs.a_sc1 = p.a_sc_off[1];
   sargs.b_frag_off = p.b_frag_off;
   sargs.b_sc_off = p.b_sc_off;
   sargs.T0 = T0;
@@ -526,7 +526,9 @@ void launch_cfg(GemmParams p, int n_terms, hipStream_t s) {
 //    fold behind the other workgroup's MFMAs; 128 x 256 HiF4 tiles would spill.  When the
 //    HiF4 grid has fewer than two workgroups per CU (M = 256 decode), the tile runs as eight
 //    waves of 32 x 96 instead, so each SIMD still holds two waves.
-enum TileCfg { kSmall = 0, kWide = 1, kMid = 2, kMid8 = 3 };
+enum TileCfg { kSmall = 0, kWide = 1, kMid = 2, kMid8 = 3, kNarrow = 4 };
+// output tile rows and columns of each configuration
+constexpr int kTileRows[5] = {64, 128, 128, 128, 64}, kTileCols[5] = {64, 256, 192, 192, 128};
 constexpr int kCUs = 256;
 
 struct Plan {
@@ -542,20 +544,26 @@ Plan plan(int fmt, int64_t M, int64_t N, int64_t K, bool may_split) {
   Plan pl{};
   pl.ksplit = 1;
   pl.kper = nkb;
+  if (wgs(4, 4) < 240 && may_split && nkb >= 128 && kCUs / wgs(2, 4) >= 2) {
+    // small grids with long K (the down projection of a decode batch): 64 x 128 tiles with K
+    // split up to four ways; the wider tile reads each activation fragment for twice the
+    // columns (measured at m = 256, 11008 -> 2048: MXFP4 24 -> 21 us, HiF4 30 -> 27 us)
+    pl.cfg = kNarrow;
+    pl.tiles = wgs(2, 4);
+    int64_t ks = kCUs / pl.tiles;
+    ks = ks > 4 ? 4 : ks;
+    pl.ksplit = (int)ks;
+    pl.kper = (nkb + ks - 1) / ks;
+    pl.partial_bytes = (size_t)pl.tiles * pl.ksplit * (64 * 128) * sizeof(float);
+    pl.kg = fmt == 0 ? 1 : 2;
+    pl.ns = fmt == 0 ? 4 : 2;
+    return pl;
+  }
   if (wgs(4, 4) < 240) {
+    // small grids (no K split: the long-K ones that would gain from one take the 64 x 128
+    // tiles above, and the backward never splits)
     pl.cfg = kSmall;
     pl.tiles = wgs(2, 2);
-    if (may_split && pl.tiles > 0) {
-      // a split pays only for long K: its partial tiles and the reduction launch cost
-      // about as much as a short K range (measured; MXFP4 at m = 256, K = 11008: 18.8 us
-      // unsplit in four K groups, 17.4 us split in two)
-      int64_t ks = kCUs / pl.tiles;
-      ks = ks < 1 ? 1 : (ks > 2 ? 2 : ks);
-      while (ks > 1 && nkb / ks < 64) --ks;
-      pl.ksplit = (int)ks;
-      pl.kper = (nkb + ks - 1) / ks;
-      if (pl.ksplit > 1) pl.partial_bytes = (size_t)pl.tiles * pl.ksplit * (256 * 16) * sizeof(float);
-    }
     // K groups and stages (measured).  Grids within the CUs: MXFP4 takes four K groups for
     // long K ranges (>= 128 steps per workgroup) and two otherwise, HiF4 two, with four
     // stages.  Grids beyond the CUs, where workgroups share CUs: long K ranges keep their
@@ -577,6 +585,13 @@ Plan plan(int fmt, int64_t M, int64_t N, int64_t K, bool may_split) {
         if (pl.kper < 128) pl.kg = 1;
       }
     }
+  } else if (fmt == 0 && M < 512) {
+    // MXFP4 decode batches with wide N (gate_up at m = 256): 64 x 128 tiles, one K group,
+    // four stages (measured: 21.6-22.5 us as 128 x 192 tiles, 20.2-20.4 us)
+    pl.cfg = kNarrow;
+    pl.tiles = wgs(2, 4);
+    pl.kg = 1;
+    pl.ns = 4;
   } else {
     const bool wide = M >= 512 && fmt == 0;
     pl.cfg = wide ? kWide : kMid;

@@ -60,13 +60,14 @@ struct Geo {
 
 // Every configuration the GEMM instantiates, as X(format, tile configuration, WM, WN, TM, TN,
 // NS, KG); the tile configurations are 0: 64 x 64, 1: 128 x 256, 2: 128 x 192, 3: 128 x 192
-// in eight waves (the numbering of resq_gemm_plan).  Each runs with one or two activation
+// in eight waves, 4: 64 x 128 (the numbering of resq_gemm_plan).  Each runs with one or two activation
 // terms.  launch_gemm dispatches from this list, and the protocol check walks it.
 #define RESQ_GEMM_CONFIGS(X)                                                                     \
   X(0, 0, 2, 2, 1, 1, 4, 2) X(0, 0, 2, 2, 1, 1, 4, 4) X(0, 0, 2, 2, 1, 1, 2, 4)                \
-  X(0, 0, 2, 2, 1, 1, 4, 1) X(0, 1, 2, 2, 2, 4, 4, 1) X(0, 2, 2, 2, 2, 3, 4, 1)                \
+  X(0, 0, 2, 2, 1, 1, 4, 1) X(0, 1, 2, 2, 2, 4, 4, 1)                \
   X(1, 0, 2, 2, 1, 1, 4, 2) X(1, 0, 2, 2, 1, 1, 2, 2) X(1, 0, 2, 2, 1, 1, 2, 1)                \
-  X(1, 3, 4, 2, 1, 3, 2, 1) X(1, 2, 2, 2, 2, 3, 2, 1)
+  X(1, 3, 4, 2, 1, 3, 2, 1) X(1, 2, 2, 2, 2, 3, 2, 1) X(0, 4, 2, 2, 1, 2, 4, 1)                \
+  X(1, 4, 2, 2, 1, 2, 2, 2)
 
 // HiF4 with more than one tile per wave keeps one register set and runs two waves per SIMD.
 template <int FMT, int TM, int TN>
@@ -84,8 +85,12 @@ struct Slot {
 // What a wave's copies depend on besides the geometry: the operand arrays' byte offsets in
 // their buffers, the workgroup's first row / column tile, the tile counts and K steps.
 struct SlotArgs {
-  uint32_t a_frag_off[2], a_sc_off[2], b_frag_off, b_sc_off;
+  // operand A's arrays of terms 0 and 1 as separate members: an array indexed by the
+  // (run-time) term would put the struct in the kernel's private memory
+  uint32_t a_frag0, a_frag1, a_sc0, a_sc1, b_frag_off, b_sc_off;
   uint32_t T0, N0, mt, nt, nkb;
+  constexpr uint32_t frag_a(int t) const { return t == 0 ? a_frag0 : a_frag1; }
+  constexpr uint32_t scale_a(int t) const { return t == 0 ? a_sc0 : a_sc1; }
 };
 
 // Copy x of class A (fragments of operand A, 16 bytes per lane) of wave `wave`, lane `lane`:
@@ -98,7 +103,7 @@ constexpr Slot slot_a(int wave, int x, int lane, const SlotArgs& a) {
   if (jc < G::JA) {
     const int kk = jc / G::JA1, jl = jc % G::JA1;
     const int t = jl / (G::MTW * G::PA), i = (jl / G::PA) % G::MTW, q = jl % G::PA;
-    c.voff = a.T0 + i < a.mt ? a.a_frag_off[t] + ((a.T0 + i) * a.nkb + kk) * G::A_FRAG + lane * G::FA + q * 16
+    c.voff = a.T0 + i < a.mt ? a.frag_a(t) + ((a.T0 + i) * a.nkb + kk) * G::A_FRAG + lane * G::FA + q * 16
                              : kBad;
     c.lds = (uint32_t)(kk * G::BLK + (t * G::MTW + i) * G::A_FRAG + q * 1024);
     c.kk = (uint32_t)kk;
@@ -135,7 +140,7 @@ constexpr Slot slot_s(int wave, int x, int lane, const SlotArgs& a, bool& is_a) 
     if (jl < G::kNT * G::SAJ) {
       const int t = jl / G::SAJ, i = 4 * (jl % G::SAJ) + lane / 16;
       const bool ok = i < G::MTW && a.T0 + i < a.mt;
-      c.voff = ok ? a.a_sc_off[t] + ((a.T0 + i) * a.nkb + kk) * 64 + (lane % 16) * 4 : kBad;
+      c.voff = ok ? a.scale_a(t) + ((a.T0 + i) * a.nkb + kk) * 64 + (lane % 16) * 4 : kBad;
       c.lds = (uint32_t)(kk * G::BLK + G::SA_OFF + jl * 256);
     } else {
       const int q = jl - G::kNT * G::SAJ, j = 4 * q + lane / 16;

@@ -120,7 +120,7 @@ bool launch_gemm(const GemmOperands& op, hipStream_t s);
 // Scratch bytes a launch_gemm of this shape uses for its K split (0: it does not split).
 size_t gemm_split_scratch(int fmt, int64_t M, int64_t N, int64_t K);
 // The plan launch_gemm takes for these sizes: tile configuration (0: 64x64, 1: 128x256,
-// 2: 128x192, 3: 128x192 in eight waves), K split, K groups and stages.
+// 2: 128x192, 3: 128x192 in eight waves, 4: 64x128), K split, K groups and stages.
 void gemm_plan_info(int fmt, int64_t M, int64_t N, int64_t K, bool may_split, int32_t info[4]);
 // Whether launch_gemm handles these sizes: the A buffer of n_terms terms (fragments and
 // scales, each 256-byte aligned) and the B buffer fit 32-bit offsets.

@@ -83,7 +83,7 @@ EXPORTED = ("resq_quantize", "resq_residual_sparsify", "resq_linear_fwd", "resq_
             "resq_prepare_weights", "resq_linear_fwd_prepared", "resq_linear_fwd_prepared_bf16",
             "resq_diagnostics", "resq_linear_fwd_prepared_swiglu", "resq_gemm_plan",
             "resq_linear_fwd_prepared_noalloc", "resq_linear_w4a16", "resq_linear_w16a4")
-GEMM_TILES = {0: "64x64", 1: "128x256", 2: "128x192", 3: "128x192_8w"}
+GEMM_TILES = {0: "64x64", 1: "128x256", 2: "128x192", 3: "128x192_8w", 4: "64x128"}
 
 
 class ResqError(RuntimeError):

@@ -14,8 +14,12 @@ from synth import WORKLOADS, Workload, Linear, workload_tensors
 from _gpu_util import dev_bf16, log
 
 # (workload, linear, sparsity) forward cases; sizes are the benchmark workloads' own, plus
-# the 7B down projection at m = 256 (the one shape that takes four K groups with four stages)
+# the 7B down projection at m = 256
 _EXTRA = Workload("qwen7b_down_m256", 256, (Linear("down", 18944, 3584),), 0.005, 100.0)
+# backward cases: the training workload, and a narrow one whose dW GEMM (256 x 256 over
+# K = 8192, not split) takes the small tiles with four K groups and four stages (MXFP4)
+_NARROW_BWD = Workload("narrow_bwd_m8192", 8192, (Linear("proj", 256, 256),), 0.01, 50.0, backward=True)
+BWD_CASES = ["qwen3b_gateup_bwd_m8192", "narrow_bwd_m8192"]
 FWD_CASES = [
     ("qwen3b_layer_m256", "qkv", "2:4"),
     ("qwen3b_layer_m256", "qkv", "none"),
@@ -33,7 +37,7 @@ FMTS = ["mxfp4", "hif4"]
 
 
 def _workload(name):
-    return _EXTRA if name == _EXTRA.name else WORKLOADS[name]
+    return {_EXTRA.name: _EXTRA, _NARROW_BWD.name: _NARROW_BWD}.get(name) or WORKLOADS[name]
 
 
 def _plan_key(P, fmt, M, N, K, split):
@@ -44,10 +48,11 @@ def _plan_key(P, fmt, M, N, K, split):
 # every (format, tile, K groups, stages, K split) that launch_gemm can run
 INSTANTIATED = {
     ("mxfp4", "64x64", 2, 4, False), ("mxfp4", "64x64", 4, 4, False), ("mxfp4", "64x64", 4, 2, False),
-    ("mxfp4", "64x64", 1, 4, False), ("mxfp4", "64x64", 2, 4, True), ("mxfp4", "128x256", 1, 4, False),
-    ("mxfp4", "128x192", 1, 4, False),
+    ("mxfp4", "64x64", 1, 4, False), ("mxfp4", "128x256", 1, 4, False),
+    ("mxfp4", "64x128", 1, 4, True), ("mxfp4", "64x128", 1, 4, False),
     ("hif4", "64x64", 2, 4, False), ("hif4", "64x64", 2, 2, False), ("hif4", "64x64", 1, 2, False),
-    ("hif4", "64x64", 2, 4, True), ("hif4", "128x192_8w", 1, 2, False), ("hif4", "128x192", 1, 2, False),
+    ("hif4", "128x192_8w", 1, 2, False), ("hif4", "128x192", 1, 2, False),
+    ("hif4", "64x128", 2, 2, True),
 }
 
 
@@ -60,10 +65,11 @@ def test_cases_cover_every_plan():
             wl = _workload(wl_name)
             lin = next(l for l in wl.linears if l.name == lin_name)
             seen.add(_plan_key(P, fmt, wl.m, lin.n, lin.d, True))
-        wl = WORKLOADS["qwen3b_gateup_bwd_m8192"]
-        lin = wl.linears[0]
-        seen.add(_plan_key(P, fmt, wl.m, lin.d, lin.n, False))  # dX
-        seen.add(_plan_key(P, fmt, lin.n, lin.d, wl.m, False))  # dW
+        for name in BWD_CASES:
+            wl = _workload(name)
+            lin = wl.linears[0]
+            seen.add(_plan_key(P, fmt, wl.m, lin.d, lin.n, False))  # dX
+            seen.add(_plan_key(P, fmt, lin.n, lin.d, wl.m, False))  # dW
     assert seen <= INSTANTIATED, f"unexpected plans {seen - INSTANTIATED}"
     assert INSTANTIATED <= seen, f"plans not covered: {INSTANTIATED - seen}"
 
@@ -97,10 +103,11 @@ def test_forward_twice_same_bits(fmt, wl_name, lin_name, sp):
 
 @pytest.mark.gpu
 @pytest.mark.parametrize("fmt", FMTS)
-def test_backward_twice_same_bits(fmt):
+@pytest.mark.parametrize("name", BWD_CASES)
+def test_backward_twice_same_bits(fmt, name):
     import torch
     import paper_2607_26515_amd as P
-    wl = WORKLOADS["qwen3b_gateup_bwd_m8192"]
+    wl = _workload(name)
     lin = wl.linears[0]
     log(f"determinism bwd {wl.name} {fmt} m={wl.m} d={lin.d} n={lin.n}")
     xb, wb, gb = workload_tensors(wl, lin, seed=0)

@@ -196,22 +196,38 @@ def test_linear_bwd(fmt, m, d, n):
     assert_close(host(dw), o["dw64"], "dW")
 
 
+@pytest.mark.parametrize("fmt", FMTS)
+def test_linear_bwd_k_groups(fmt):
+    """The dW GEMM of m = 8384 (131 K steps), n = d = 128 runs 64 x 64 tiles unsplit with four
+    K groups (MXFP4; two for HiF4) and four stages: three K steps in the last stage."""
+    import paper_2607_26515_amd as P
+    m, d, n = 8384, 128, 128
+    log(f"linear_bwd k groups {fmt} m={m} d={d} n={n} dW plan {P.gemm_plan(fmt, n, d, m, False)}")
+    rx, rw, rg = rng_tree(m + n + d + 1, 3)
+    xb, wb, gb = activations(rx, m, d, 0.01, 50.0), weights(rw, n, d), grad_output(rg, m, n)
+    dx, dw = P.linear_bwd(dev_bf16(gb), dev_bf16(xb), dev_bf16(wb), fmt)
+    o = Q.resq_backward(fmt, bf16_bits_to_f32(gb), bf16_bits_to_f32(xb), bf16_bits_to_f32(wb))
+    assert_close(host(dx), o["dx64"], "dX")
+    assert_close(host(dw), o["dw64"], "dW")
+
+
 @pytest.mark.parametrize("sp", ["none", "2:4"])
 @pytest.mark.parametrize("fmt,m,d,n", [
     ("mxfp4", 64, 320, 128),    # 5 K steps, two K groups: the last stage is half empty
-    ("mxfp4", 64, 8384, 96),    # K split in two (66 + 65 steps), two K groups each
-    ("mxfp4", 512, 8384, 1152),  # 131 K steps, four K groups: three steps in the last stage
+    ("mxfp4", 64, 8384, 96),    # 64 x 128 tiles, K split in four (33, 33, 33, 32 steps)
+    ("mxfp4", 512, 8384, 1152),  # 64 x 128 tiles, K split in three (44, 44, 43 steps)
     ("mxfp4", 1024, 8384, 1152),  # more workgroups than CUs: four K groups, two stages
     ("hif4", 64, 320, 128),     # 5 K steps, two K groups
-    ("hif4", 32, 8384, 64),     # K split in two (66 + 65 steps), two K groups each
+    ("hif4", 32, 8384, 64),     # 64 x 128 tiles, K split in four, two K groups each
     ("hif4", 640, 320, 2048),   # more small tiles than CUs, short K: one K group, two stages
     ("hif4", 640, 8384, 2048),  # more small tiles than CUs, long K: two K groups, two stages
     ("mxfp4", 640, 320, 2048),  # more small tiles than CUs, short K: one K group, four stages
+    ("mxfp4", 256, 2048, 22016),  # 64 x 128 tiles without a split (MXFP4 decode, wide N)
 ])
 def test_linear_fwd_k_groups(fmt, sp, m, d, n):
-    """Decode-sized grids run K groups (several wave groups splitting each stage's K steps);
-    K lengths that leave the last stage partly empty, a K split with an odd half and the
-    two-stage plan must all match the oracle."""
+    """Decode-sized grids run K groups (several wave groups splitting each stage's K steps)
+    or 64 x 128 tiles with a K split; K lengths that leave the last stage partly empty, a
+    ragged K split and the two-stage plan must all match the oracle."""
     log(f"linear_fwd k groups {fmt} {sp} m={m} d={d} n={n}")
     y, o = _linear_case(fmt, sp, m, d, n, seed=m + 3 * d + n)
     assert_close(y, o["y64"], f"Y {fmt} {sp}")
