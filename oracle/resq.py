@@ -29,7 +29,7 @@ Readings of points the paper leaves open (also listed in the design notes):
   Y1  Y, dX and dW are float32: the exact float64 result rounded once.
   Y2  the optional bf16 output is that float32 result rounded again, to the nearest bf16
       (ties to even): the rounding of the float32 result, not of the float64 one.
-  M1  the mixed-precision rollout linears of Table 1 keep one operand in its 16-bit form:
+  W1  the mixed-precision rollout linears of Table 1 keep one operand in its 16-bit form:
       W4A16 is X Q(W)^T and W16A4 is Q(X) W^T, with Q along d as in Eq. 1 (the W4A8 row
       needs an 8-bit activation format that the paper does not name, and is not built).
   F1  the fused producer of the down projection's input (the SwiGLU of the gate and up
