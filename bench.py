@@ -105,14 +105,17 @@ def gemm_bytes(m, d, n, fmt, sp, y_bytes=4):
 
 def gemm_traffic(workload, fmt, sp, out="f32"):
     """HBM bytes per GEMM launch from the committed rocprofv3 counter summary, or None when
-    the summary does not cover this workload or the GEMM source changed since it was taken."""
+    the summary does not cover this workload or the GEMM source (gemm.hip and gemm_geo.h)
+    changed since it was taken."""
     import hashlib
     try:
         rec = json.load(open(os.path.join(ROOT, "profiles", "gemm_traffic.json")))
-        src = open(os.path.join(ROOT, "paper_2607_26515_amd", "csrc", "gemm.hip"), "rb").read()
+        h = hashlib.sha256()
+        for f in ("gemm.hip", "gemm_geo.h"):  # the GEMM kernel's sources
+            h.update(open(os.path.join(ROOT, "paper_2607_26515_amd", "csrc", f), "rb").read())
     except OSError:
         return None
-    if rec.get("gemm_source_sha256") != hashlib.sha256(src).hexdigest():
+    if rec.get("gemm_source_sha256") != h.hexdigest():
         return None
     key = f"{workload}/{fmt}/{sp}" + ("" if out == "f32" else f"/{out}")
     entry = rec.get("entries", {}).get(key)
