@@ -54,6 +54,7 @@ typedef int v8i __attribute__((ext_vector_type(8)));
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v3i __attribute__((ext_vector_type(3)));
 typedef float v16f __attribute__((ext_vector_type(16)));
+typedef float v4f __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 constexpr int kXcds = 8;
@@ -69,6 +70,7 @@ struct GemmParams {
   void* Y;        // float32, or bf16 bits when out_bf16
   int64_t ldy;
   int out_bf16;   // store Y as bf16 (round to nearest, ties to even) instead of float32
+  int vec_y;      // Y and ldy allow 16-byte stores of four consecutive outputs
   // grid bookkeeping (32-bit: the workgroup count is far below 2^31)
   uint32_t grid_m, grid_n, per_xcd, n_wg;
   // split-K: ksplit workgroups per tile, each over kper K steps, each writing its partial
@@ -102,6 +104,17 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) {
 __device__ __forceinline__ void store_y(void* Y, int64_t idx, float v, int out_bf16) {
   if (out_bf16) reinterpret_cast<uint16_t*>(Y)[idx] = f32_to_bf16_rne(v);
   else reinterpret_cast<float*>(Y)[idx] = v;
+}
+
+// Four consecutive outputs; Y + idx is 16-byte aligned (float32) or 8-byte aligned (bf16).
+__device__ __forceinline__ void store_y4(void* Y, int64_t idx, const v4f& v, int out_bf16) {
+  if (out_bf16) {
+    const uint32_t lo = f32_to_bf16_rne(v[0]) | ((uint32_t)f32_to_bf16_rne(v[1]) << 16);
+    const uint32_t hi = f32_to_bf16_rne(v[2]) | ((uint32_t)f32_to_bf16_rne(v[3]) << 16);
+    *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(Y) + idx) = make_uint2(lo, hi);
+  } else {
+    *reinterpret_cast<v4f*>(reinterpret_cast<float*>(Y) + idx) = v;
+  }
 }
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
@@ -452,17 +465,46 @@ void gemm_kernel(GemmParams p) {
     return;
   }
 
+  // Y through LDS, eight rows at a time: accumulator registers 4q .. 4q+3 of a tile hold its
+  // rows 8q .. 8q+7 (lanes 0-31 rows 8q .. 8q+3, lanes 32-63 rows 8q+4 .. 8q+7), so the wave
+  // writes those registers of its TN tiles into its own LDS slot as an 8 x (TN x 32) row-major
+  // block and reads it back 16 bytes per lane: each store then covers whole row segments of
+  // TN x 32 columns, not 32 columns of two rows.  The slot is this wave's alone (K groups: its
+  // reduction slot, already consumed; one group: after a barrier that ends every wave's reads
+  // of the stage buffers), and one wave's LDS accesses complete in order, so only the
+  // compiler needs to be kept from reordering them.
+  constexpr int RW = TN * 32;  // floats per staged row
+  static_assert(KG > 1 || (size_t)G::W * 8 * RW * 4 <= G::LDS, "staging slots fit the stage buffers");
+  if constexpr (KG == 1) __syncthreads();
+  float* slot = reinterpret_cast<float*>(smem) + (size_t)wt * (KG > 1 ? TM * TN * 16 * 64 : 8 * RW);
   const int half = lane >> 5, l32 = lane & 31;
+  const int64_t col0 = ((int64_t)N0 + wn * TN) * 32;
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int64_t col = ((int64_t)N0 + wn * TN + j) * 32 + l32;
+    for (int q = 0; q < 4; ++q) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t row = ((int64_t)T0 + wm * TM + i) * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        if (row < p.M && col < p.N) store_y(p.Y, row * p.ldy + col, acc[i][j][r], p.out_bf16);
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) slot[(4 * half + e) * RW + j * 32 + l32] = acc[i][j][4 * q + e];
+      asm volatile("" ::: "memory");
+      const int64_t row0 = ((int64_t)T0 + wm * TM + i) * 32 + 8 * q;
+#pragma unroll
+      for (int s = 0; s < TN; ++s) {
+        const int f = 4 * lane + 256 * s;  // flat float index in the 8 x RW block
+        const v4f v = *reinterpret_cast<const v4f*>(slot + f);
+        const int64_t row = row0 + f / RW, col = col0 + f % RW;
+        if (row < p.M) {
+          if (p.vec_y && col + 3 < p.N) {
+            store_y4(p.Y, row * p.ldy + col, v, p.out_bf16);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (col + e < p.N) store_y(p.Y, row * p.ldy + col + e, v[e], p.out_bf16);
+          }
+        }
       }
+      asm volatile("" ::: "memory");
     }
 }
 
@@ -669,6 +711,7 @@ bool launch_gemm(const GemmOperands& op, hipStream_t s) {
   }
   p.b_frag_off = (uint32_t)op.b_frag_off; p.b_sc_off = (uint32_t)op.b_sc_off;
   p.Y = op.Y; p.ldy = op.ldy; p.out_bf16 = op.out_bf16 ? 1 : 0;
+  p.vec_y = (reinterpret_cast<uintptr_t>(op.Y) % 16 == 0 && op.ldy % 4 == 0) ? 1 : 0;
   return launch_plan(p, op.fmt, pl, op.n_terms, s);
 }
 
