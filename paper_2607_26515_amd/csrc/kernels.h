@@ -76,8 +76,8 @@ struct SelectWs {
   uint32_t* hist;     // radix-select histograms / counters
   uint32_t* state;    // selection state (prefix, counts)
   uint8_t* group_bits;  // kept channels / blocks (bit mask)
-  uint32_t* super_counts;  // tie counts per group of workgroups (unstructured; cleared with hist)
-  uint32_t* tie_counts;  // per-workgroup tie counts (unstructured)
+  uint32_t* super_counts;  // [group of workgroups][64] tie counts (element-wise; cleared with hist)
+  uint32_t* tie_counts;  // [workgroup][64] tie counts (element-wise)
 };
 size_t select_ws_bytes(int sparsity, int fmt, int64_t m, int64_t d);
 int64_t select_max_items();  // most channels / blocks a channel or block selection ranks (2^31)

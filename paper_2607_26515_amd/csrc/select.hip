@@ -62,16 +62,18 @@ __device__ __forceinline__ uint32_t scale_at(const void* scales, int64_t row, in
 }
 
 // ---------------------------------------------------------------------------------------
-// Channel keys.  Workgroup = 64 channels (lane = channel) x 16 waves; wave w sums the squares
-// of a contiguous range of rows in float64 and the ranges are added in wave order.  That
-// equals the defined row-by-row sum exactly whenever no float64 addition of either order
-// rounds: every square v^2 is a multiple of 2^L, L = twice the exponent of the lowest set
-// bit of the smallest such v in the channel, so if the total is below 2^(L+53) every partial
-// sum, in any order, is a multiple of 2^L below 2^(L+53) and thus exact.  The check uses
-// 2^(L+52) to absorb any rounding of the computed total; a channel that fails it is summed
-// again row by row in the defined order.
+// Channel keys.  Workgroup = 16 channels x 64 row chunks: lane l of wave w sums the squares of
+// channel l % 16 over row chunk 4w + l / 16 in float64, and the chunk sums are added in chunk
+// (row) order.  16 channels per workgroup give d / 16 workgroups, enough to cover the CUs at
+// the layer widths of a decode batch.  The result equals the defined row-by-row sum exactly
+// whenever no float64 addition of either order rounds: every square v^2 is a multiple of 2^L,
+// L = twice the exponent of the lowest set bit of the smallest such v in the channel, so if
+// the total is below 2^(L+53) every partial sum, in any order, is a multiple of 2^L below
+// 2^(L+53) and thus exact.  The check uses 2^(L+52) to absorb any rounding of the computed
+// total; a channel that fails it is summed again row by row in the defined order.
 // ---------------------------------------------------------------------------------------
-constexpr int kChanThreads = 1024;  // channel keys: 16 waves, one row range each
+constexpr int kChanThreads = 1024;  // 16 waves
+constexpr int kChanPerWg = 16;      // channels per workgroup
 constexpr int kNoBit = 1 << 20;      // "no nonzero term yet" for the lowest-bit exponent
 
 template <int FMT>
@@ -101,13 +103,14 @@ __global__ __launch_bounds__(kChanThreads) void channel_keys_kernel(const uint8_
                                                                     const void* __restrict__ scales,
                                                                     int64_t m, int64_t d,
                                                                     double* __restrict__ keys) {
-  constexpr int NW = kChanThreads / 64, U = 8;
-  __shared__ double part[NW][64];
-  __shared__ int low[NW][64];
+  constexpr int NW = kChanThreads / 64, NC = NW * (64 / kChanPerWg), U = 8;
+  __shared__ double part[NC][kChanPerWg];
+  __shared__ int low[NC][kChanPerWg];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t j = (int64_t)blockIdx.x * 64 + lane;
-  const int64_t per = (m + NW - 1) / NW;
-  const int64_t r0 = min((int64_t)wave * per, m), r1 = min(r0 + per, m);
+  const int c = lane % kChanPerWg, chunk = wave * (64 / kChanPerWg) + lane / kChanPerWg;
+  const int64_t j = (int64_t)blockIdx.x * kChanPerWg + c;
+  const int64_t per = (m + NC - 1) / NC;
+  const int64_t r0 = min((int64_t)chunk * per, m), r1 = min(r0 + per, m);
   auto value = [&](int64_t row) {
     return decode_at<FMT>(codes[row * (d / 2) + j / 2], scale_at<FMT>(scales, row, d, j), j);
   };
@@ -125,15 +128,15 @@ __global__ __launch_bounds__(kChanThreads) void channel_keys_kernel(const uint8_
       }
     }
   }
-  part[wave][lane] = acc;
-  low[wave][lane] = lo;
+  part[chunk][c] = acc;
+  low[chunk][c] = lo;
   __syncthreads();
-  if (wave != 0 || j >= d) return;
+  if (threadIdx.x >= kChanPerWg || j >= d) return;  // thread c finishes channel c
   double sum = 0.0;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) {
-    sum += part[w][lane];
-    lo = min(lo, low[w][lane]);
+  lo = kNoBit;
+  for (int w = 0; w < NC; ++w) {
+    sum += part[w][c];
+    lo = min(lo, low[w][c]);
   }
   if (sum != 0.0 && !(sum < ldexp(1.0, lo + 52))) {
     // some addition may round: the defined order, rows 0 .. m-1
@@ -218,6 +221,35 @@ __device__ __forceinline__ void choose_digit(const uint32_t* hist, int nb, uint3
   __syncthreads();
 }
 
+// Radix digit choice by one wave over a 256-bin histogram: the digit holding the k-th
+// largest key (k >= 1; k = 0 picks the top digit), k's rank among the keys with that digit,
+// and that digit's count, to out[0..2].  Lane l holds bins 255 - 4l .. 252 - 4l.
+__device__ __forceinline__ void choose_digit_wave(const uint32_t* hist, uint32_t k, uint32_t* out) {
+  const int lane = threadIdx.x & 63;
+  uint32_t v[4], sum = 0;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    v[e] = hist[255 - 4 * lane - e];
+    sum += v[e];
+  }
+  uint32_t incl = sum;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += y;
+  }
+  uint32_t above = incl - sum;  // keys in higher bins
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    if ((above < k && k <= above + v[e]) || (k == 0 && lane == 0 && e == 0)) {
+      out[0] = (uint32_t)(255 - 4 * lane - e);
+      out[1] = k - above;
+      out[2] = v[e];
+    }
+    above += v[e];
+  }
+}
+
 // h[digit] += 1 for every active lane of the wave.  The lanes sharing the digit of the first
 // two leaders are counted with one LDS atomic each (the keys of a selection pass often share
 // a digit, and per-lane atomics on one address serialize); the rest add one by one.  Every
@@ -242,16 +274,19 @@ __device__ __forceinline__ void hist_add(uint32_t* h, uint32_t digit, bool activ
 // with coalesced loads.  The threshold's ties are ranked in index order from one table of
 // per-slot, per-wave tie counts (one barrier).
 // ---------------------------------------------------------------------------------------
-constexpr int kKeysPerThread = 24;  // n <= 24576: channels of d <= 24576, blocks of m*d <= 50M
+// KPT keys per thread (n <= 1024 KPT); launch_top takes the smallest instantiation that holds
+// the keys, so that a pass over a few thousand keys is not a walk over 24 mostly empty slots.
+constexpr int kKeysPerThread = 20;  // the largest: n <= 20480 (channels of d <= 20480)
 
+template <int KPT>
 __global__ __launch_bounds__(kSelThreads) void select_top_kernel(const uint64_t* __restrict__ keys,
                                                                  int64_t n, int64_t k,
                                                                  uint8_t* __restrict__ bits,
                                                                  uint8_t* __restrict__ bits_copy) {
+  constexpr int kKeysPerThread = KPT;
   constexpr int NW = kSelThreads / 64;
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t ch[2];
-  __shared__ uint32_t wsum[NW];
+  __shared__ uint32_t hists[2][256];  // pass p counts into hists[p & 1] while the other is cleared
+  __shared__ uint32_t ch[3];
   __shared__ uint32_t tcnt[kKeysPerThread][NW];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   uint64_t kr[kKeysPerThread];
@@ -261,36 +296,106 @@ __global__ __launch_bounds__(kSelThreads) void select_top_kernel(const uint64_t*
     kr[q] = i < n ? keys[i] : 0;
   }
   __shared__ uint64_t found;
-  uint64_t prefix = 0, mask = 0;
-  uint32_t krem = (uint32_t)k;
-  for (int shift = 56; shift >= 0; shift -= 8) {
-    if (tid < 256) hist[tid] = 0;
-    __syncthreads();
+  // Candidates: once the keys that share the threshold's digits so far fit one per thread,
+  // they are gathered into LDS (in any order: the passes only count them) and the remaining
+  // passes read one slot instead of KPT.
+  __shared__ uint64_t cand[kSelThreads];
+  __shared__ uint32_t ncand;
+  const uint64_t below = (1ull << lane) - 1ull;  // lanes before this one
+  bool compact = false;
+  uint32_t nc = 0;
+  // Bits on which all keys agree decide nothing: the OR and AND of the keys bound the digit
+  // passes to the byte-aligned span [s_bot, s_top + 8) holding every differing bit (the first
+  // pass then splits the keys instead of finding them all in one bin); above it lies the
+  // prefix of every key, below it the tail of every key.
+  __shared__ uint64_t red_or[NW], red_and[NW];
+  uint64_t kor = 0, kand = ~0ull;
 #pragma unroll
-    for (int q = 0; q < kKeysPerThread; ++q) {
-      const int64_t i = (int64_t)q * kSelThreads + tid;
-      hist_add(hist, (uint32_t)((kr[q] >> shift) & 255u), i < n && (kr[q] & mask) == prefix);
-    }
-    __syncthreads();
-    choose_digit<kSelThreads>(hist, 256, krem, wsum, ch);
-    prefix |= (uint64_t)ch[0] << shift;
-    krem = ch[1];
-    mask |= (uint64_t)255 << shift;
-    const uint32_t in_bin = hist[ch[0]];  // keys sharing the threshold's digits so far
-    __syncthreads();  // ch and hist are reused by the next pass
-    if (in_bin == 1 && shift > 0) {
-      // a single key has this prefix: it is the threshold (krem = 1), no further digit needed
+  for (int q = 0; q < kKeysPerThread; ++q) {
+    const int64_t i = (int64_t)q * kSelThreads + tid;
+    if (i < n) { kor |= kr[q]; kand &= kr[q]; }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    kor |= __shfl_xor(kor, off, 64);
+    kand &= __shfl_xor(kand, off, 64);
+  }
+  if (lane == 0) { red_or[wave] = kor; red_and[wave] = kand; }
+  __syncthreads();
+  kor = 0; kand = ~0ull;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) { kor |= red_or[w]; kand &= red_and[w]; }
+  const uint64_t diff = kor ^ kand;  // bits that differ between some two keys
+  const int s_top = diff ? (63 - __builtin_clzll(diff)) / 8 * 8 : 0;
+  const int s_bot = diff ? __builtin_ctzll(diff) / 8 * 8 : 8;  // no pass when all keys are equal
+  const uint64_t above = s_top + 8 < 64 ? ~((1ull << (s_top + 8)) - 1ull) : 0ull;
+  uint64_t prefix = kand & above, mask = above;
+  uint32_t krem = (uint32_t)k;
+  bool single = false;
+  if (tid < 512) hists[tid >> 8][tid & 255] = 0;
+  __syncthreads();
+  // Two barriers per pass: after the counts, and after the digit choice (which one wave makes
+  // with a wave scan, while other threads clear the next pass's histogram).
+  int pass = 0;
+  for (int shift = s_top; shift >= s_bot; shift -= 8, ++pass) {
+    uint32_t* hist = hists[pass & 1];
+    if (compact) {
+      const uint64_t c = tid < (int)nc ? cand[tid] : 0;
+      hist_add(hist, (uint32_t)((c >> shift) & 255u), tid < (int)nc && (c & mask) == prefix);
+    } else {
 #pragma unroll
       for (int q = 0; q < kKeysPerThread; ++q) {
         const int64_t i = (int64_t)q * kSelThreads + tid;
-        if (i < n && (kr[q] & mask) == prefix) found = kr[q];
+        hist_add(hist, (uint32_t)((kr[q] >> shift) & 255u), i < n && (kr[q] & mask) == prefix);
+      }
+    }
+    __syncthreads();
+    if (wave == 0) {
+      choose_digit_wave(hist, krem, ch);
+    } else if (tid >= 64 && tid < 64 + 256) {
+      hists[(pass + 1) & 1][tid - 64] = 0;  // read by no one since the previous pass's choice
+    }
+    __syncthreads();
+    prefix |= (uint64_t)ch[0] << shift;
+    krem = ch[1];
+    mask |= (uint64_t)255 << shift;
+    const uint32_t in_bin = ch[2];  // keys sharing the threshold's digits so far
+    if (in_bin == 1 && shift > s_bot) {
+      // a single key has this prefix: it is the threshold (krem = 1), no further digit needed
+      if (compact) {
+        if (tid < (int)nc && (cand[tid] & mask) == prefix) found = cand[tid];
+      } else {
+#pragma unroll
+        for (int q = 0; q < kKeysPerThread; ++q) {
+          const int64_t i = (int64_t)q * kSelThreads + tid;
+          if (i < n && (kr[q] & mask) == prefix) found = kr[q];
+        }
       }
       __syncthreads();
       prefix = found;
+      single = true;
       break;
     }
+    if (KPT > 1 && !compact && in_bin <= (uint32_t)kSelThreads && shift > s_bot) {
+      if (tid == 0) ncand = 0;
+      __syncthreads();
+#pragma unroll
+      for (int q = 0; q < kKeysPerThread; ++q) {
+        const int64_t i = (int64_t)q * kSelThreads + tid;
+        const bool c = i < n && (kr[q] & mask) == prefix;
+        const uint64_t b = __ballot(c);
+        uint32_t base = 0;
+        if (lane == 0 && b) base = atomicAdd(&ncand, (uint32_t)__popcll(b));
+        base = __shfl(base, 0, 64);
+        if (c) cand[base + (uint32_t)__popcll(b & below)] = kr[q];
+      }
+      __syncthreads();
+      nc = ncand;
+      compact = true;
+    }
   }
-  const uint64_t T = prefix;  // threshold key; krem of its ties are kept (in index order)
+  // threshold key (the common tail completes it); krem of its ties are kept, in index order
+  const uint64_t T = single ? prefix : (prefix | (kand & ((1ull << s_bot) - 1ull)));
   uint64_t tb[kKeysPerThread];  // tie ballots per slot
 #pragma unroll
   for (int q = 0; q < kKeysPerThread; ++q) {
@@ -299,28 +404,51 @@ __global__ __launch_bounds__(kSelThreads) void select_top_kernel(const uint64_t*
     if (lane == 0) tcnt[q][wave] = (uint32_t)__popcll(tb[q]);
   }
   __syncthreads();
-  const uint64_t below = (1ull << lane) - 1ull;  // lanes before this one
-  uint32_t seen = 0;                             // ties in earlier slots
+  // exclusive prefix of the tie counts in index order (slot-major, then wave), by wave 0
+  constexpr int NTC = kKeysPerThread * NW, PL = (NTC + 63) / 64;
+  if (wave == 0) {
+    uint32_t* flat = &tcnt[0][0];
+    uint32_t v[PL], sum = 0;
+#pragma unroll
+    for (int e = 0; e < PL; ++e) {
+      v[e] = lane * PL + e < NTC ? flat[lane * PL + e] : 0u;
+      sum += v[e];
+    }
+    uint32_t incl = sum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t y = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += y;
+    }
+    uint32_t run = incl - sum;
+#pragma unroll
+    for (int e = 0; e < PL; ++e) {
+      if (lane * PL + e < NTC) flat[lane * PL + e] = run;
+      run += v[e];
+    }
+  }
+  __syncthreads();
+  // keep bits: a wave's 64 keys are 8 whole bytes; wave-uniform stores of 8 bytes where the
+  // keys and the pointer allow it, else one byte per 8 lanes
+  const bool wide = ((uintptr_t)bits % 8 == 0) && (bits_copy == nullptr || (uintptr_t)bits_copy % 8 == 0);
 #pragma unroll
   for (int q = 0; q < kKeysPerThread; ++q) {
-    const int64_t i = (int64_t)q * kSelThreads + tid;
-    uint32_t before = 0, total = 0;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      const uint32_t c = tcnt[q][w];
-      total += c;
-      before += w < wave ? c : 0u;
-    }
+    const int64_t i0 = (int64_t)q * kSelThreads + wave * 64, i = i0 + lane;
+    if (i0 >= n) continue;  // wave-uniform
     const bool in = i < n, tie = ((tb[q] >> lane) & 1ull) != 0;
-    const uint32_t rank = seen + before + (uint32_t)__popcll(tb[q] & below);
+    const uint32_t rank = tie ? tcnt[q][wave] + (uint32_t)__popcll(tb[q] & below) : 0u;
     const bool keep = in && (kr[q] > T || (tie && rank < krem));
     const uint64_t bal = __ballot(keep);
-    if ((lane & 7) == 0 && in) {
+    if (wide && i0 + 64 <= n) {
+      if (lane == 0) {
+        *reinterpret_cast<uint64_t*>(bits + (i0 >> 3)) = bal;
+        if (bits_copy) *reinterpret_cast<uint64_t*>(bits_copy + (i0 >> 3)) = bal;
+      }
+    } else if ((lane & 7) == 0 && in) {
       const uint8_t byte = (uint8_t)(bal >> lane);
       bits[i >> 3] = byte;
       if (bits_copy) bits_copy[i >> 3] = byte;
     }
-    seen += total;
   }
 }
 
@@ -389,12 +517,24 @@ __global__ __launch_bounds__(kSelThreads) void select_top_stream_kernel(const ui
 }
 
 void launch_top(const double* keys, int64_t n, int64_t k, uint8_t* bits, uint8_t* bits_copy, hipStream_t s) {
-  if (n <= (int64_t)kKeysPerThread * kSelThreads)
-    hipLaunchKernelGGL(select_top_kernel, dim3(1), dim3(kSelThreads), 0, s, (const uint64_t*)keys, n, k, bits,
-                       bits_copy);
-  else
-    hipLaunchKernelGGL(select_top_stream_kernel, dim3(1), dim3(kSelThreads), 0, s, (const uint64_t*)keys, n, k,
-                       bits, bits_copy);
+  const uint64_t* kk = (const uint64_t*)keys;
+#define RESQ_TOP(KPT)                                                                                \
+  if (n <= (int64_t)(KPT) * kSelThreads) {                                                          \
+    hipLaunchKernelGGL(select_top_kernel<KPT>, dim3(1), dim3(kSelThreads), 0, s, kk, n, k, bits, bits_copy); \
+    return;                                                                                          \
+  }
+  RESQ_TOP(1) RESQ_TOP(2) RESQ_TOP(4) RESQ_TOP(8) RESQ_TOP(16) RESQ_TOP(kKeysPerThread)
+#undef RESQ_TOP
+  hipLaunchKernelGGL(select_top_stream_kernel, dim3(1), dim3(kSelThreads), 0, s, kk, n, k, bits, bits_copy);
+}
+
+// Channel keys of the dense Q(dX), then the top-k over them.
+void launch_channel_top(int fmt, const uint8_t* codes, const void* scales, int64_t m, int64_t d, int64_t keep,
+                        const SelectWs& ws, uint8_t* bits_copy, hipStream_t s) {
+  const dim3 g((unsigned)((d + kChanPerWg - 1) / kChanPerWg));
+  if (fmt == 0) hipLaunchKernelGGL((channel_keys_kernel<0>), g, dim3(kChanThreads), 0, s, codes, scales, m, d, ws.keys);
+  else hipLaunchKernelGGL((channel_keys_kernel<1>), g, dim3(kChanThreads), 0, s, codes, scales, m, d, ws.keys);
+  launch_top(ws.keys, d, keep, ws.group_bits, bits_copy, s);
 }
 
 // Apply kept channels (KIND 0) or kept blocks (KIND 1): one thread per code word; grid x
@@ -432,12 +572,17 @@ __global__ __launch_bounds__(kThreads) void apply_groups_kernel(uint32_t* __rest
 constexpr int kUHist = 320;
 // The global histogram is kept in kHistCopies copies; workgroup b adds into copy
 // b % kHistCopies, so the few populated bins are not one contended address for every
-// workgroup's atomics.  Readers sum the copies.
-constexpr int kHistCopies = 32;
+// workgroup's atomics.  Readers sum the copies (every workgroup of the later passes does).
+constexpr int kHistCopies = 8;
 
-// Tie counts are summed per group of kSuper workgroups as well, so that a workgroup finds the
-// ties of all earlier workgroups in O(nwg / kSuper + kSuper) reads.
+// Threshold ties.  The second pass counts, per workgroup, the keys of the chosen exponent by
+// their six mantissa bits; the threshold is one of those 64 patterns and FP4 keys have no
+// lower bits, so that table holds every workgroup's tie count for whichever threshold the
+// pass's global histogram then fixes.  The counts are also summed per group of kSuper
+// workgroups, so that a workgroup finds the ties of all earlier workgroups in
+// O(nwg / kSuper + kSuper) reads.
 constexpr int kSuper = 256;
+constexpr int kMantBins = 64;
 
 __global__ void uzero_kernel(uint32_t* hist, int words) {
   for (int i = threadIdx.x; i < words; i += blockDim.x) hist[i] = 0;
@@ -488,7 +633,9 @@ template <int FMT, int PASS>
 __global__ __launch_bounds__(kThreads) void uhist_kernel(const uint8_t* __restrict__ codes,
                                                          const void* __restrict__ scales, int64_t m,
                                                          int64_t d, uint32_t keep,
-                                                         uint32_t* __restrict__ hist) {
+                                                         uint32_t* __restrict__ hist,
+                                                         uint32_t* __restrict__ super_counts,
+                                                         uint32_t* __restrict__ tie_counts) {
   __shared__ uint32_t lh[kUHist];
   __shared__ uint32_t ch[4];
   __shared__ uint32_t wsum[kThreads / 64];
@@ -515,36 +662,13 @@ __global__ __launch_bounds__(kThreads) void uhist_kernel(const uint8_t* __restri
   }
   __syncthreads();
   constexpr int NB = PASS == 0 ? 256 : 64, OFF = PASS == 0 ? 0 : 256;
-  for (int b = tid; b < NB; b += kThreads)
-    if (lh[b]) atomicAdd(&hist[(blockIdx.x % kHistCopies) * kUHist + OFF + b], lh[b]);
-}
-
-// Threshold ties per workgroup (index order = workgroup order, then thread order).
-template <int FMT>
-__global__ __launch_bounds__(kThreads) void uties_kernel(const uint8_t* __restrict__ codes,
-                                                         const void* __restrict__ scales, int64_t m,
-                                                         int64_t d, uint32_t keep,
-                                                         const uint32_t* __restrict__ hist,
-                                                         uint32_t* __restrict__ super_counts,
-                                                         uint32_t* __restrict__ tie_counts) {
-  __shared__ uint32_t lh[kUHist];
-  __shared__ uint32_t ch[4];
-  __shared__ uint32_t wsum[kThreads / 64];
-  load_choice(hist, lh, keep, true, wsum, ch);
-  const uint32_t T = ch[2];
-  const int64_t w0 = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * kWordsPerThread;
-  uint32_t ties = 0;
-  if (w0 < m * (d / 8)) {
-    uint32_t key[32];
-    thread_keys<FMT>(codes, scales, d, w0, key);
-#pragma unroll
-    for (int e = 0; e < 32; ++e) ties += key[e] == T;
-  }
-  uint32_t total;
-  block_exclusive_scan<kThreads>(ties, wsum, total);
-  if (threadIdx.x == 0) {
-    tie_counts[blockIdx.x] = total;
-    if (total) atomicAdd(&super_counts[blockIdx.x / kSuper], total);  // integer sums: any order
+  for (int b = tid; b < NB; b += kThreads) {
+    const uint32_t c = lh[b];  // local bins 0 .. NB-1 (both passes)
+    if (c) atomicAdd(&hist[(blockIdx.x % kHistCopies) * kUHist + OFF + b], c);
+    if constexpr (PASS == 1) {
+      tie_counts[(size_t)blockIdx.x * kMantBins + b] = c;
+      if (c) atomicAdd(&super_counts[(blockIdx.x / kSuper) * kMantBins + b], c);  // integer sums: any order
+    }
   }
 }
 
@@ -567,11 +691,13 @@ __global__ __launch_bounds__(kThreads) void uapply_kernel(uint8_t* __restrict__ 
   __shared__ uint32_t wsum[kThreads / 64];
   load_choice(hist, lh, keep, true, wsum, ch);
   const uint32_t T = ch[2], krem = ch[3];
-  // ties of earlier workgroups: whole groups of kSuper workgroups, then this group's earlier ones
-  const uint32_t sb = blockIdx.x / kSuper;
+  // ties of earlier workgroups: whole groups of kSuper workgroups, then this group's earlier
+  // ones, from the second pass's counts of T's mantissa pattern
+  const uint32_t tm = (T >> 17) & 63u, sb = blockIdx.x / kSuper;
   uint32_t before = 0;
-  for (uint32_t w = threadIdx.x; w < sb; w += kThreads) before += super_counts[w];
-  for (uint32_t w = sb * kSuper + threadIdx.x; w < blockIdx.x; w += kThreads) before += tie_counts[w];
+  for (uint32_t w = threadIdx.x; w < sb; w += kThreads) before += super_counts[w * kMantBins + tm];
+  for (uint32_t w = sb * kSuper + threadIdx.x; w < blockIdx.x; w += kThreads)
+    before += tie_counts[(size_t)w * kMantBins + tm];
   uint32_t tot_before;
   block_exclusive_scan<kThreads>(before, wsum, tot_before);
   const int64_t w0 = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * kWordsPerThread;
@@ -629,7 +755,7 @@ int64_t unstructured_wgs(int64_t m, int64_t d) {
 
 // words cleared before an element-wise selection: the histogram copies and the group counts
 int64_t hist_words(int64_t m, int64_t d) {
-  return (int64_t)kHistCopies * kUHist + (unstructured_wgs(m, d) + kSuper - 1) / kSuper;
+  return (int64_t)kHistCopies * kUHist + (unstructured_wgs(m, d) + kSuper - 1) / kSuper * kMantBins;
 }
 
 size_t a256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -648,7 +774,7 @@ size_t select_ws_bytes(int sparsity, int fmt, int64_t m, int64_t d) {
     case 4:  // block
       return a256((size_t)n_blocks(m, d) * 8) + a256((size_t)(n_blocks(m, d) + 31) / 32 * 4);
     case 5:  // element-wise
-      return a256((size_t)hist_words(m, d) * 4) + a256((size_t)unstructured_wgs(m, d) * 4);
+      return a256((size_t)hist_words(m, d) * 4) + a256((size_t)unstructured_wgs(m, d) * kMantBins * 4);
     default:
       return 0;
   }
@@ -675,10 +801,7 @@ void launch_select(int fmt, int sparsity, int64_t m, int64_t d, int64_t keep, ui
   if (m == 0 || d == 0) return;
   const dim3 gw((unsigned)((d / 8 + kThreads - 1) / kThreads), (unsigned)(m < 65535 ? m : 65535));
   if (sparsity == 3) {
-    const dim3 g((unsigned)((d + 63) / 64));
-    if (fmt == 0) hipLaunchKernelGGL((channel_keys_kernel<0>), g, dim3(kChanThreads), 0, s, qr_codes, qr_scales, m, d, ws.keys);
-    else hipLaunchKernelGGL((channel_keys_kernel<1>), g, dim3(kChanThreads), 0, s, qr_codes, qr_scales, m, d, ws.keys);
-    launch_top(ws.keys, d, keep, ws.group_bits, group_mask, s);
+    launch_channel_top(fmt, qr_codes, qr_scales, m, d, keep, ws, group_mask, s);
     hipLaunchKernelGGL((apply_groups_kernel<0>), gw, dim3(kThreads), 0, s,
                        (uint32_t*)qr_codes, m, d, (const uint8_t*)ws.group_bits, keep_mask);
   } else if (sparsity == 4) {
@@ -694,10 +817,10 @@ void launch_select(int fmt, int sparsity, int64_t m, int64_t d, int64_t keep, ui
     hipLaunchKernelGGL(uzero_kernel, dim3(1), dim3(kThreads), 0, s, ws.hist, (int)hist_words(m, d));
     const uint32_t k = (uint32_t)keep;
 #define RESQ_U(F)                                                                                          \
-    hipLaunchKernelGGL((uhist_kernel<F, 0>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k, ws.hist); \
-    hipLaunchKernelGGL((uhist_kernel<F, 1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k, ws.hist); \
-    hipLaunchKernelGGL((uties_kernel<F>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k,              \
-                       (const uint32_t*)ws.hist, ws.super_counts, ws.tie_counts);                                     \
+    hipLaunchKernelGGL((uhist_kernel<F, 0>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k, ws.hist,  \
+                       ws.super_counts, ws.tie_counts);                                                               \
+    hipLaunchKernelGGL((uhist_kernel<F, 1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k, ws.hist,  \
+                       ws.super_counts, ws.tie_counts);                                                               \
     hipLaunchKernelGGL((uapply_kernel<F, -1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k,         \
                        (const uint32_t*)ws.hist, (const uint32_t*)ws.super_counts, (const uint32_t*)ws.tie_counts,    \
                        keep_mask, nullptr, nullptr);
@@ -714,24 +837,22 @@ void launch_select_frag(int fmt, int sparsity, int64_t m, int64_t d, int64_t kee
     const bool chan = sparsity == 3;
     const int64_t n = chan ? d : n_blocks(m, d);
     if (chan) {
-      const dim3 g((unsigned)((d + 63) / 64));
-      if (fmt == 0) hipLaunchKernelGGL((channel_keys_kernel<0>), g, dim3(kChanThreads), 0, s, qr_codes, qr_scales, m, d, ws.keys);
-      else hipLaunchKernelGGL((channel_keys_kernel<1>), g, dim3(kChanThreads), 0, s, qr_codes, qr_scales, m, d, ws.keys);
+      launch_channel_top(fmt, qr_codes, qr_scales, m, d, keep, ws, nullptr, s);
     } else {
       const dim3 g((unsigned)((n + kThreads - 1) / kThreads));
       if (fmt == 0) hipLaunchKernelGGL((block_keys_kernel<0>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
       else hipLaunchKernelGGL((block_keys_kernel<1>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
+      launch_top(ws.keys, n, keep, ws.group_bits, nullptr, s);
     }
-    launch_top(ws.keys, n, keep, ws.group_bits, nullptr, s);
     launch_pack(pack_mode, qr_codes, qr_scales, m, d, frag, fscale, s, chan ? 1 : 2, ws.group_bits);
   } else if (sparsity == 5) {
     const unsigned nwg = (unsigned)unstructured_wgs(m, d);  // hist and group counts cleared by the residual pass
     const uint32_t k = (uint32_t)keep;
 #define RESQ_UF(F, P)                                                                                      \
-    hipLaunchKernelGGL((uhist_kernel<F, 0>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k, ws.hist); \
-    hipLaunchKernelGGL((uhist_kernel<F, 1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k, ws.hist); \
-    hipLaunchKernelGGL((uties_kernel<F>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k,              \
-                       (const uint32_t*)ws.hist, ws.super_counts, ws.tie_counts);                                     \
+    hipLaunchKernelGGL((uhist_kernel<F, 0>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k, ws.hist,  \
+                       ws.super_counts, ws.tie_counts);                                                               \
+    hipLaunchKernelGGL((uhist_kernel<F, 1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k, ws.hist,  \
+                       ws.super_counts, ws.tie_counts);                                                               \
     hipLaunchKernelGGL((uapply_kernel<F, P>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k,          \
                        (const uint32_t*)ws.hist, (const uint32_t*)ws.super_counts, (const uint32_t*)ws.tie_counts,    \
                        (uint8_t*)nullptr, frag, fscale);
