@@ -152,29 +152,38 @@ __global__ __launch_bounds__(kChanThreads) void channel_keys_kernel(const uint8_
 // ---------------------------------------------------------------------------------------
 // Block keys: one thread per 32 x 64 block, rows in order, scale blocks in column order.
 // ---------------------------------------------------------------------------------------
+// Key of block t = (I, J): the per-scale-block sums of squares of its rows, rows in order,
+// scale blocks (P per 64 columns) in column order.
+template <int P>
+__device__ __forceinline__ double block_key(const double* __restrict__ partials, int64_t m, int64_t d, int64_t t) {
+  const int64_t nJ = d / 64;
+  const int64_t I = (int64_t)((uint64_t)t / (uint64_t)nJ), J = t - I * nJ;
+  const int64_t r1 = (32 * I + 32 < m) ? 32 * I + 32 : m;
+  const int64_t ld = d / 64 * P;  // scale blocks per row
+  double acc = 0.0;
+#pragma unroll 1
+  for (int h = 0; h < 32; h += 16) {  // 16 rows at a time: their loads issued together
+    double v[16][P];
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+#pragma unroll
+      for (int q = 0; q < P; ++q)
+        v[i][q] = 32 * I + h + i < r1 ? partials[(32 * I + h + i) * ld + J * P + q] : 0.0;
+#pragma unroll
+    for (int i = 0; i < 16; ++i)  // rows in order, scale blocks in column order
+#pragma unroll
+      for (int q = 0; q < P; ++q)
+        if (32 * I + h + i < r1) acc += v[i][q];
+  }
+  return acc;
+}
+
 template <int FMT>
 __global__ __launch_bounds__(kThreads) void block_keys_kernel(const double* __restrict__ partials,
                                                               int64_t m, int64_t d,
                                                               double* __restrict__ keys) {
-  constexpr int P = FMT == 0 ? 2 : 1;  // scale blocks per 64 columns
-  const int64_t nJ = d / 64, nI = (m + 31) / 32;
   const int64_t t = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (t >= nI * nJ) return;
-  const int64_t I = (int64_t)((uint64_t)t / (uint64_t)nJ), J = t - I * nJ;
-  const int64_t r1 = (32 * I + 32 < m) ? 32 * I + 32 : m;
-  const int64_t ld = d / (FMT == 0 ? 32 : 64);
-  double v[32][P];
-#pragma unroll
-  for (int i = 0; i < 32; ++i)  // independent loads, issued together
-#pragma unroll
-    for (int q = 0; q < P; ++q) v[i][q] = 32 * I + i < r1 ? partials[(32 * I + i) * ld + J * P + q] : 0.0;
-  double acc = 0.0;
-#pragma unroll
-  for (int i = 0; i < 32; ++i)  // rows in order, scale blocks in column order
-#pragma unroll
-    for (int q = 0; q < P; ++q)
-      if (32 * I + i < r1) acc += v[i][q];
-  keys[t] = acc;
+  if (t < ((m + 31) / 32) * (d / 64)) keys[t] = block_key<FMT == 0 ? 2 : 1>(partials, m, d, t);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -278,11 +287,15 @@ __device__ __forceinline__ void hist_add(uint32_t* h, uint32_t digit, bool activ
 // the keys, so that a pass over a few thousand keys is not a walk over 24 mostly empty slots.
 constexpr int kKeysPerThread = 20;  // the largest: n <= 20480 (channels of d <= 20480)
 
-template <int KPT>
+// BP = 0: the keys are read from `keys`; BP = 1 / 2 (one key per thread): they are the block
+// keys, summed from `partials` (BP scale blocks per 64 columns) at load.
+template <int KPT, int BP>
 __global__ __launch_bounds__(kSelThreads) void select_top_kernel(const uint64_t* __restrict__ keys,
-                                                                 int64_t n, int64_t k,
+                                                                 const double* __restrict__ partials,
+                                                                 int64_t m, int64_t d, int64_t n, int64_t k,
                                                                  uint8_t* __restrict__ bits,
                                                                  uint8_t* __restrict__ bits_copy) {
+  static_assert(BP == 0 || KPT == 1, "block keys are summed at load one per thread");
   constexpr int kKeysPerThread = KPT;
   constexpr int NW = kSelThreads / 64;
   __shared__ uint32_t hists[2][256];  // pass p counts into hists[p & 1] while the other is cleared
@@ -293,7 +306,8 @@ __global__ __launch_bounds__(kSelThreads) void select_top_kernel(const uint64_t*
 #pragma unroll
   for (int q = 0; q < kKeysPerThread; ++q) {
     const int64_t i = (int64_t)q * kSelThreads + tid;
-    kr[q] = i < n ? keys[i] : 0;
+    if constexpr (BP == 0) kr[q] = i < n ? keys[i] : 0;
+    else kr[q] = i < n ? (uint64_t)__double_as_longlong(block_key<BP>(partials, m, d, i)) : 0;
   }
   __shared__ uint64_t found;
   // Candidates: once the keys that share the threshold's digits so far fit one per thread,
@@ -520,12 +534,31 @@ void launch_top(const double* keys, int64_t n, int64_t k, uint8_t* bits, uint8_t
   const uint64_t* kk = (const uint64_t*)keys;
 #define RESQ_TOP(KPT)                                                                                \
   if (n <= (int64_t)(KPT) * kSelThreads) {                                                          \
-    hipLaunchKernelGGL(select_top_kernel<KPT>, dim3(1), dim3(kSelThreads), 0, s, kk, n, k, bits, bits_copy); \
+    hipLaunchKernelGGL((select_top_kernel<KPT, 0>), dim3(1), dim3(kSelThreads), 0, s, kk, (const double*)nullptr, \
+                       (int64_t)0, (int64_t)0, n, k, bits, bits_copy);                                \
     return;                                                                                          \
   }
   RESQ_TOP(1) RESQ_TOP(2) RESQ_TOP(4) RESQ_TOP(8) RESQ_TOP(16) RESQ_TOP(kKeysPerThread)
 #undef RESQ_TOP
   hipLaunchKernelGGL(select_top_stream_kernel, dim3(1), dim3(kSelThreads), 0, s, kk, n, k, bits, bits_copy);
+}
+
+// Block keys, then the top-k over them.  HiF4 blocks up to one per thread: the top-k sums the
+// keys itself (one launch fewer; measured at m = 512, d = 3584: 10.0 us against 4.1 + 6.6 us).
+// MXFP4 has two scale blocks per 64 columns, and one workgroup reading twice the partial sums
+// takes longer than the separate key launch (12.0 us against 4.2 + 6.2 us).
+void launch_block_top(int fmt, const double* partials, int64_t m, int64_t d, int64_t keep, const SelectWs& ws,
+                      uint8_t* bits_copy, hipStream_t s) {
+  const int64_t nb = ((m + 31) / 32) * (d / 64);
+  if (fmt == 1 && nb <= kSelThreads) {
+    hipLaunchKernelGGL((select_top_kernel<1, 1>), dim3(1), dim3(kSelThreads), 0, s, (const uint64_t*)nullptr,
+                       partials, m, d, nb, keep, ws.group_bits, bits_copy);
+    return;
+  }
+  const dim3 g((unsigned)((nb + kThreads - 1) / kThreads));
+  if (fmt == 0) hipLaunchKernelGGL((block_keys_kernel<0>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
+  else hipLaunchKernelGGL((block_keys_kernel<1>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
+  launch_top(ws.keys, nb, keep, ws.group_bits, bits_copy, s);
 }
 
 // Channel keys of the dense Q(dX), then the top-k over them.
@@ -805,11 +838,7 @@ void launch_select(int fmt, int sparsity, int64_t m, int64_t d, int64_t keep, ui
     hipLaunchKernelGGL((apply_groups_kernel<0>), gw, dim3(kThreads), 0, s,
                        (uint32_t*)qr_codes, m, d, (const uint8_t*)ws.group_bits, keep_mask);
   } else if (sparsity == 4) {
-    const int64_t nb = n_blocks(m, d);
-    const dim3 g((unsigned)((nb + kThreads - 1) / kThreads));
-    if (fmt == 0) hipLaunchKernelGGL((block_keys_kernel<0>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
-    else hipLaunchKernelGGL((block_keys_kernel<1>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
-    launch_top(ws.keys, nb, keep, ws.group_bits, group_mask, s);
+    launch_block_top(fmt, partials, m, d, keep, ws, group_mask, s);
     hipLaunchKernelGGL((apply_groups_kernel<1>), gw, dim3(kThreads), 0, s,
                        (uint32_t*)qr_codes, m, d, (const uint8_t*)ws.group_bits, keep_mask);
   } else if (sparsity == 5) {
@@ -839,10 +868,7 @@ void launch_select_frag(int fmt, int sparsity, int64_t m, int64_t d, int64_t kee
     if (chan) {
       launch_channel_top(fmt, qr_codes, qr_scales, m, d, keep, ws, nullptr, s);
     } else {
-      const dim3 g((unsigned)((n + kThreads - 1) / kThreads));
-      if (fmt == 0) hipLaunchKernelGGL((block_keys_kernel<0>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
-      else hipLaunchKernelGGL((block_keys_kernel<1>), g, dim3(kThreads), 0, s, partials, m, d, ws.keys);
-      launch_top(ws.keys, n, keep, ws.group_bits, nullptr, s);
+      launch_block_top(fmt, partials, m, d, keep, ws, nullptr, s);
     }
     launch_pack(pack_mode, qr_codes, qr_scales, m, d, frag, fscale, s, chan ? 1 : 2, ws.group_bits);
   } else if (sparsity == 5) {
