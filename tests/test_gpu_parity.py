@@ -264,3 +264,35 @@ def test_linear_fwd_prepared_bf16(fmt, sp, m, d, n):
     big = np.abs(o["y64"]) > 2.0**-4 * np.sqrt(np.mean(o["y64"] ** 2))
     assert diff[big].max(initial=0) <= 1, "bf16 outputs more than one step from the oracle's"
     assert np.mean(diff == 0) > 0.99
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("m,d,n", [(37, 512, 102), (256, 2048, 2558), (1024, 512, 4102)])
+@pytest.mark.parametrize("out", ["f32", "bf16"])
+def test_linear_fwd_output_layouts(fmt, m, d, n, out):
+    """The GEMM stores Y through LDS as row segments, 16 bytes per lane where Y and ldy allow
+    it and element by element otherwise.  A strided Y (ldy not a multiple of 4), a Y that
+    starts 4 bytes into its buffer and a width that is not a multiple of 4 must give the bits
+    of the contiguous result and leave the buffer outside Y untouched.  The shapes run the
+    small (K groups), the decode-width and the large-tile plans."""
+    import torch
+    import paper_2607_26515_amd as P
+    log(f"linear_fwd output layouts {fmt} m={m} d={d} n={n} out={out}")
+    rx, rw = rng_tree(m + 7 * n + d, 2)
+    xb, wb = activations(rx, m, d, 0.01, 50.0), weights(rw, n, d)
+    qc, qs = P.quantize(dev_bf16(wb), fmt, axis=1)
+    x = dev_bf16(xb)
+    wprep = P.prepare_weights(qc, qs, fmt)
+    ref = host(P.linear_fwd_prepared(x, wprep, n, fmt, "2:4", out=out))
+    dt = torch.float32 if out == "f32" else torch.int16
+    sentinel = -12345
+    for extra, off in ((3, 0), (6, 0), (8, 1), (6, 1)):  # scalar, vector, scalar, scalar
+        buf = torch.full((m, n + extra), sentinel, dtype=dt, device=x.device)
+        y = buf[:, off:off + n]
+        P.linear_fwd_prepared(x, wprep, n, fmt, "2:4", y=y, out=out)
+        torch.cuda.synchronize()
+        b = host(buf)
+        got = b[:, off:off + n]
+        assert np.array_equal(got.view(np.uint8), ref.view(np.uint8)), f"ldy={n + extra} offset={off}"
+        outside = np.concatenate([b[:, :off], b[:, off + n:]], axis=1)
+        assert np.all(outside == sentinel), "a store landed outside Y"
