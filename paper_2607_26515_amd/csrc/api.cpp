@@ -262,7 +262,7 @@ int run_activation_side(int format, const Sp& sp, const uint16_t* X, int64_t m, 
   {
     resq::ProfScope prof_(resq::kProfResidual, s);
     resq::launch_residual(format, resid_mode(sp), X, m, d, ldx, qx_codes, qx_scales, qr_codes,
-                          qr_scales, keep_mask, partials, s, false, nullptr, 0, sp.keep);
+                          qr_scales, keep_mask, partials, s, false, nullptr, sp.keep);
   }
   if (global_kind(sp)) {
     resq::ProfScope prof_(resq::kProfSelect, s);
@@ -396,10 +396,10 @@ int linear_fwd_core(int format, const Sp& sp, const uint16_t* X, int64_t m, int6
     {
       resq::ProfScope prof_(resq::kProfResidual, s, true);
       const bool elem = sp.kind == RESQ_S_UNSTRUCT50;
+      if (elem) resq::launch_select_clear(w.sel, m, d, s);  // the residual pass counts into it
       resq::launch_residual(format, resq::kResidDense, X, m, d, ldx, w.frag_x, w.fsc_x, w.qr_codes,
                             w.qr_scales, nullptr, sp.kind == RESQ_S_BLOCK32X64_50 ? w.partials : nullptr,
-                            s, true, elem ? w.sel.hist : nullptr, elem ? resq::select_hist_words(m, d) : 0,
-                            2, prod);
+                            s, true, elem ? w.sel.hist : nullptr, 2, prod);
     }
     resq::ProfScope prof_(resq::kProfSelect, s);
     resq::launch_select_frag(format, sp.kind, m, d, keep_count(sp, m, d), w.qr_codes, w.qr_scales,
@@ -408,7 +408,7 @@ int linear_fwd_core(int format, const Sp& sp, const uint16_t* X, int64_t m, int6
     // local kinds: the residual pass writes the MFMA fragments directly
     resq::ProfScope prof_(resq::kProfResidual, s, true);
     resq::launch_residual(format, resid_mode(sp), X, m, d, ldx, w.frag_x, w.fsc_x, w.frag_r,
-                          w.fsc_r, nullptr, nullptr, s, true, nullptr, 0, sp.keep, prod);
+                          w.fsc_r, nullptr, nullptr, s, true, nullptr, sp.keep, prod);
   }
   const uint8_t* af[2] = {w.frag_x, w.frag_r};
   const uint8_t* asc[2] = {w.fsc_x, w.fsc_r};

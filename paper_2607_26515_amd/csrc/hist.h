@@ -1,0 +1,34 @@
+// Histogram helpers shared by the selections (select.hip) and the residual pass (quant.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace resq {
+
+// The element-wise selection's global histogram: 256 exponent bins then 64 mantissa bins per
+// copy, kElemHistCopies copies; workgroup b adds into copy b % kElemHistCopies, so the few
+// populated bins are not one contended address for every workgroup's atomics.  Readers sum
+// the copies.
+constexpr int kElemHistBins = 320;
+constexpr int kElemHistCopies = 8;
+
+// h[digit] += 1 for every active lane of the wave.  The lanes sharing the digit of the first
+// two leaders are counted with one LDS atomic each (the keys of a selection pass often share
+// a digit, and per-lane atomics on one address serialize); the rest add one by one.  Every
+// lane of the wave must call this (the digit and active flag may differ per lane).
+__device__ __forceinline__ void hist_add(uint32_t* h, uint32_t digit, bool active) {
+  uint64_t pending = __ballot(active);
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    if (pending == 0) return;
+    const int leader = __ffsll((unsigned long long)pending) - 1;
+    const uint32_t dl = __shfl(digit, leader, 64);
+    const uint64_t same = __ballot(digit == dl) & pending;
+    if (__lane_id() == leader) atomicAdd(&h[dl], (uint32_t)__popcll(same));
+    pending &= ~same;
+  }
+  if ((pending >> __lane_id()) & 1ull) atomicAdd(&h[digit], 1u);
+}
+
+}  // namespace resq

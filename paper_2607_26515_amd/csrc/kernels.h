@@ -49,13 +49,13 @@ struct Producer {
 // (pack.hip layout; codes -> fragment records, scales -> per-lane scale bytes) instead of
 // K-major codes + scales: for both Q(X) and Q(dX) with the local kinds; with kResidDense
 // Q(X) as fragments and Q(dX) K-major (qr_codes, qr_scales) for the selection that follows,
-// and `zero` (zero_words 32-bit words, may be null) cleared by the same launch.  keep_mask
-// is ignored when frag is set.
+// and, with ehist (the element-wise selection's histogram, cleared beforehand by
+// launch_select_clear), the exponent histogram of |Q(dX)|.  keep_mask is ignored when frag is
+// set.
 void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
                      uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes, void* qr_scales,
                      uint8_t* keep_mask, double* partials, hipStream_t s, bool frag = false,
-                     uint32_t* zero = nullptr, int zero_words = 0, int nm_keep = 2,
-                     const Producer* prod = nullptr);
+                     uint32_t* ehist = nullptr, int nm_keep = 2, const Producer* prod = nullptr);
 
 // MFMA operand packing (pack.hip): K-major codes + scales -> fragment-major operands.
 enum PackMode { kPackMx = 0, kPackHiA = 1, kPackHiB = 2 };
@@ -88,11 +88,14 @@ void launch_select(int fmt, int sparsity, int64_t m, int64_t d, int64_t keep, ui
 // The same selections for the forward GEMM: S(Q(dX)) is written as fragment-major operand
 // records (PackMode pack_mode) to frag / fscale; the K-major codes are left unpruned and no
 // masks are written.  For the element-wise kind the histogram (select_hist_words(m, d) words at
-// ws.hist) must have been cleared beforehand (the residual pass does it).
+// ws.hist) must have been cleared (launch_select_clear) before the residual pass, which fills
+// its exponent bins.
 void launch_select_frag(int fmt, int sparsity, int64_t m, int64_t d, int64_t keep, uint8_t* qr_codes,
                         const void* qr_scales, const double* partials, const SelectWs& ws,
                         int pack_mode, uint8_t* frag, uint8_t* fscale, hipStream_t s);
 int select_hist_words(int64_t m, int64_t d);  // words to clear at ws.hist (histograms, group counts)
+// Clears the element-wise selection's histograms and group counts (ws.hist).
+void launch_select_clear(const SelectWs& ws, int64_t m, int64_t d, hipStream_t s);
 
 // FP4 GEMM  Y[M][N] = sum_t A_t[M][K] B[N][K]^T  with A_t = Q(X) and optionally S(Q(dX)),
 // all operands fragment-major (pack.hip).  Operand A is one buffer holding the fragments and

@@ -3,6 +3,7 @@
 #include "kernels.h"
 #include "profiler.h"
 #include "quant_core.h"
+#include "hist.h"
 
 namespace resq {
 namespace {
@@ -411,7 +412,7 @@ __device__ __forceinline__ void residual_frag_tile(
     const uint16_t* __restrict__ X, int64_t m, int64_t d, int64_t ldx, int64_t nkb,
     uint8_t* __restrict__ fx, uint8_t* __restrict__ fsx, uint8_t* __restrict__ fr,
     uint8_t* __restrict__ fsr, double* __restrict__ partials, int nm_keep, const Producer& prod,
-    int64_t t, int64_t kb) {
+    int64_t t, int64_t kb, uint32_t* ehist_lds) {
   const int64_t f = t * nkb + kb;  // fragment index
   const int tid = threadIdx.x;
   const int rr = tid >> 3, half = (tid >> 2) & 1, s = tid & 3;
@@ -466,6 +467,13 @@ __device__ __forceinline__ void residual_frag_tile(
     if constexpr (MODE == kResidDense) {
       store_kmajor8<FMT>(fr, fsr, partials, row < m && col0 < d, row, d, kb, half, s, code, val,
                          scale_byte, b, b2);
+      if (ehist_lds) {  // workgroup-uniform
+        // the element-wise selection's first histogram: exponent fields of |Q(dX)|, exactly
+        // the keys its passes decode from these codes (one float32 per value)
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          hist_add(ehist_lds, (__float_as_uint(val[i]) >> 23) & 255u, row < m && col0 < d);
+      }
     } else {
       store_record8<FMT>(fr, fsr, rec, s, code, scale_byte, c1, b);
     }
@@ -474,20 +482,31 @@ __device__ __forceinline__ void residual_frag_tile(
 
 // grid: x = K step, y = row tiles (grid-stride).  kResidDense (a global selection follows):
 // fr / fsr receive the K-major Q(dX) codes and scales and `partials` its per-scale-block
-// sums of squares (may be null); workgroup (0, 0) also clears zero_words words at zero (may
-// be null), the histogram the element-wise selection accumulates into.
+// sums of squares (may be null); with ehist (element-wise selection, cleared beforehand) the
+// workgroup also counts the exponent fields of |Q(dX)| and adds them into copy
+// (workgroup % kElemHistCopies) of that histogram.
 template <int FMT, int MODE, bool VEC, bool SWIGLU>
 __global__ __launch_bounds__(256) void residual_frag_kernel(
     const uint16_t* __restrict__ X, int64_t m, int64_t d, int64_t ldx, int64_t nkb,
     uint8_t* __restrict__ fx, uint8_t* __restrict__ fsx, uint8_t* __restrict__ fr,
-    uint8_t* __restrict__ fsr, double* __restrict__ partials, uint32_t* __restrict__ zero,
-    int zero_words, int nm_keep, Producer prod) {
-  if (zero != nullptr && blockIdx.x == 0 && blockIdx.y == 0)
-    for (int i = threadIdx.x; i < zero_words; i += blockDim.x) zero[i] = 0u;
+    uint8_t* __restrict__ fsr, double* __restrict__ partials, uint32_t* __restrict__ ehist,
+    int nm_keep, Producer prod) {
+  __shared__ uint32_t lh[MODE == kResidDense ? 256 : 1];
+  const bool counting = MODE == kResidDense && ehist != nullptr;
+  if (counting) {
+    lh[threadIdx.x] = 0u;  // 256 threads
+    __syncthreads();
+  }
   const int64_t mtiles = (m + 31) / 32;
   for (int64_t t = blockIdx.y; t < mtiles; t += gridDim.y)
     residual_frag_tile<FMT, MODE, VEC, SWIGLU>(X, m, d, ldx, nkb, fx, fsx, fr, fsr, partials, nm_keep,
-                                               prod, t, blockIdx.x);
+                                               prod, t, blockIdx.x, counting ? lh : nullptr);
+  if (counting) {
+    __syncthreads();
+    const uint32_t c = lh[threadIdx.x];
+    const uint32_t wg = blockIdx.y * gridDim.x + blockIdx.x;
+    if (c) atomicAdd(&ehist[(wg % kElemHistCopies) * kElemHistBins + threadIdx.x], c);
+  }
 }
 
 // ---------------------------------------------------------------------------------------
@@ -665,7 +684,7 @@ void launch_quant_cols(int fmt, const void* x, bool in_f32, int64_t rows, int64_
 void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
                      uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes, void* qr_scales,
                      uint8_t* keep_mask, double* partials, hipStream_t s, bool frag,
-                     uint32_t* zero, int zero_words, int nm_keep, const Producer* prod) {
+                     uint32_t* ehist, int nm_keep, const Producer* prod) {
   if (m == 0 || d == 0) return;
   if (frag) {
     const int64_t nkb = (d + 63) / 64;
@@ -676,7 +695,7 @@ void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d,
     const bool vec16 = prod ? ((uintptr_t)pr.g % 16 == 0 && (uintptr_t)pr.u % 16 == 0 &&
                                pr.ldg % ve == 0 && pr.ldu % ve == 0)
                             : ((uintptr_t)X % 16 == 0 && ldx % 8 == 0);
-#define RESQ_RF(F, M, V, P) launch_timed(residual_frag_kernel<F, M, V, P>, grid, dim3(256), 0u, s, X, m, d, ldx, nkb, qx_codes, (uint8_t*)qx_scales, qr_codes, (uint8_t*)qr_scales, partials, zero, zero_words, nm_keep, pr)
+#define RESQ_RF(F, M, V, P) launch_timed(residual_frag_kernel<F, M, V, P>, grid, dim3(256), 0u, s, X, m, d, ldx, nkb, qx_codes, (uint8_t*)qx_scales, qr_codes, (uint8_t*)qr_scales, partials, ehist, nm_keep, pr)
 #define RESQ_RF_MODE(F, V, P)                                        \
     switch (mode) {                                                  \
       case kResidNone: RESQ_RF(F, kResidNone, V, P); break;          \

@@ -14,6 +14,7 @@
 // equal to it are ranked by index.  Pruned codes become the +0 code in place.
 #include "kernels.h"
 #include "frag.h"
+#include "hist.h"
 
 namespace resq {
 namespace {
@@ -259,23 +260,6 @@ __device__ __forceinline__ void choose_digit_wave(const uint32_t* hist, uint32_t
   }
 }
 
-// h[digit] += 1 for every active lane of the wave.  The lanes sharing the digit of the first
-// two leaders are counted with one LDS atomic each (the keys of a selection pass often share
-// a digit, and per-lane atomics on one address serialize); the rest add one by one.  Every
-// lane of the wave must call this (the digit and active flag may differ per lane).
-__device__ __forceinline__ void hist_add(uint32_t* h, uint32_t digit, bool active) {
-  uint64_t pending = __ballot(active);
-#pragma unroll
-  for (int it = 0; it < 2; ++it) {
-    if (pending == 0) return;
-    const int leader = __ffsll((unsigned long long)pending) - 1;
-    const uint32_t dl = __shfl(digit, leader, 64);
-    const uint64_t same = __ballot(digit == dl) & pending;
-    if (__lane_id() == leader) atomicAdd(&h[dl], (uint32_t)__popcll(same));
-    pending &= ~same;
-  }
-  if ((pending >> __lane_id()) & 1ull) atomicAdd(&h[digit], 1u);
-}
 
 // ---------------------------------------------------------------------------------------
 // Single-workgroup top-k over n float64 keys -> bit mask (bit b of byte i = item 8i + b).
@@ -602,11 +586,8 @@ __global__ __launch_bounds__(kThreads) void apply_groups_kernel(uint32_t* __rest
 // hist: [0, 256) exponent counts, [256, 320) mantissa counts.  Each kernel after the first
 // recomputes the choice from the histograms, so no workgroup waits for another.
 // ---------------------------------------------------------------------------------------
-constexpr int kUHist = 320;
-// The global histogram is kept in kHistCopies copies; workgroup b adds into copy
-// b % kHistCopies, so the few populated bins are not one contended address for every
-// workgroup's atomics.  Readers sum the copies (every workgroup of the later passes does).
-constexpr int kHistCopies = 8;
+constexpr int kUHist = kElemHistBins;       // hist.h: 256 exponent bins, then 64 mantissa bins
+constexpr int kHistCopies = kElemHistCopies;  // hist.h: copies that readers sum
 
 // Threshold ties.  The second pass counts, per workgroup, the keys of the chosen exponent by
 // their six mantissa bits; the threshold is one of those 64 patterns and FP4 keys have no
@@ -872,11 +853,10 @@ void launch_select_frag(int fmt, int sparsity, int64_t m, int64_t d, int64_t kee
     }
     launch_pack(pack_mode, qr_codes, qr_scales, m, d, frag, fscale, s, chan ? 1 : 2, ws.group_bits);
   } else if (sparsity == 5) {
-    const unsigned nwg = (unsigned)unstructured_wgs(m, d);  // hist and group counts cleared by the residual pass
+    // the histograms were cleared before the residual pass, which counted the exponent bins
+    const unsigned nwg = (unsigned)unstructured_wgs(m, d);
     const uint32_t k = (uint32_t)keep;
 #define RESQ_UF(F, P)                                                                                      \
-    hipLaunchKernelGGL((uhist_kernel<F, 0>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k, ws.hist,  \
-                       ws.super_counts, ws.tie_counts);                                                               \
     hipLaunchKernelGGL((uhist_kernel<F, 1>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k, ws.hist,  \
                        ws.super_counts, ws.tie_counts);                                                               \
     hipLaunchKernelGGL((uapply_kernel<F, P>), dim3(nwg), dim3(kThreads), 0, s, qr_codes, qr_scales, m, d, k,          \
@@ -888,5 +868,10 @@ void launch_select_frag(int fmt, int sparsity, int64_t m, int64_t d, int64_t kee
 }
 
 int select_hist_words(int64_t m, int64_t d) { return (int)hist_words(m, d); }
+
+void launch_select_clear(const SelectWs& ws, int64_t m, int64_t d, hipStream_t s) {
+  if (m == 0 || d == 0) return;
+  hipLaunchKernelGGL(uzero_kernel, dim3(1), dim3(kThreads), 0, s, ws.hist, (int)hist_words(m, d));
+}
 
 }  // namespace resq
