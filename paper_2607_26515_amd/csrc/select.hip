@@ -264,11 +264,11 @@ __device__ __forceinline__ void choose_digit_wave(const uint32_t* hist, uint32_t
 // ---------------------------------------------------------------------------------------
 // Single-workgroup top-k over n float64 keys -> bit mask (bit b of byte i = item 8i + b).
 // Thread t holds keys t, t + 1024, ... in registers (KPT of them: n <= 1024 KPT), loaded once
-// with coalesced loads.  The threshold's ties are ranked in index order from one table of
-// per-slot, per-wave tie counts (one barrier).
+// with coalesced loads.  The threshold's ties are ranked in index order from a table of
+// per-slot, per-wave tie counts that one wave scans.
 // ---------------------------------------------------------------------------------------
-// KPT keys per thread (n <= 1024 KPT); launch_top takes the smallest instantiation that holds
-// the keys, so that a pass over a few thousand keys is not a walk over 24 mostly empty slots.
+// launch_top takes the smallest instantiation that holds the keys, so that a pass over a few
+// thousand keys is not a walk over many mostly empty slots.
 constexpr int kKeysPerThread = 20;  // the largest: n <= 20480 (channels of d <= 20480)
 
 // BP = 0: the keys are read from `keys`; BP = 1 / 2 (one key per thread): they are the block

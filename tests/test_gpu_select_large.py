@@ -1,4 +1,4 @@
-"""Global selections beyond the register-resident top-k (more than 24,576 channels or
+"""Global selections beyond the register-resident top-k (more than 20,480 channels or
 blocks), where each radix pass streams the keys: S^{32x64}_50% at the prefill down
 projection's size (m = 8192, d = 18944: 75,776 blocks), S_50% over 32,768 channels, and the
 element-wise kind over enough workgroups to span several tie-count groups.
@@ -70,9 +70,12 @@ def test_block_selection_prefill_down_full_size(fmt):
 
 
 @pytest.mark.parametrize("fmt", ["hif4", "mxfp4"])
-def test_channel_selection_beyond_24576_channels(fmt):
+@pytest.mark.parametrize("d", [20480, 20544, 32768])
+def test_channel_selection_at_and_beyond_the_register_limit(fmt, d):
+    """20,480 channels fill the top-k's registers (20 keys per thread); 20,544 and 32,768 take
+    the streaming top-k."""
     import paper_2607_26515_amd as P
-    m, d = 64, 32768
+    m = 64
     log(f"large channel selection {fmt} m={m} d={d}")
     xb = activations(rng_tree(21, 1)[0], m, d, 0.01, 50.0)
     out = P.residual_sparsify(dev_bf16(xb), fmt, "channel50")
