@@ -289,8 +289,8 @@ size_t resq_workspace_size(int op, int format, int sparsity, int64_t m, int64_t 
  *   resq_quantize writes them.  d must be a multiple of the format's block.  No workspace.
  * resq_linear_w16a4 - activation-only FP4: Y = Q(X) W^T with Q(X) quantized along d inside
  *   the call and W: n x d bf16, row stride ldw (ldw % 8 == 0, W 16-byte aligned).  Workspace:
- *   resq_workspace_size(RESQ_OP_LINEAR_W16A4, format, 0, m, d, n) bytes (Q(X) codes and
- *   scales), 256-byte aligned.
+ *   resq_workspace_size(RESQ_OP_LINEAR_W16A4, format, 0, m, d, n) bytes (Q(X) as its
+ *   dequantized bf16 values, m x d), 256-byte aligned.
  * Both compute in float32 on the bf16 MFMA: every FP4 value is exact in bf16, so every
  * product is exact and only the accumulation rounds.  Errors as resq_linear_fwd.
  */

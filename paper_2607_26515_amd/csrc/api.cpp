@@ -329,7 +329,7 @@ size_t resq_workspace_size(int op, int format, int sparsity, int64_t m, int64_t 
     case RESQ_OP_LINEAR_BWD: return carve_bwd(nullptr, format, m, d, n, nullptr);
     case RESQ_OP_DIAGNOSTICS: return resq::diag_ws_bytes(m, d);
     case RESQ_OP_LINEAR_W16A4:
-      return d % block_of(format) ? 0 : align256((size_t)m * d / 2) + align256(scale_bytes(format, m, d));
+      return d % block_of(format) ? 0 : align256((size_t)m * d * 2);
     default: return 0;
   }
 }
@@ -608,9 +608,11 @@ int resq_linear_w4a16(int format, const uint16_t* X, int64_t m, int64_t d, int64
   if (!qw_codes || !qw_scales || (uintptr_t)qw_codes % 16 != 0 ||
       (format == RESQ_HIF4 && (uintptr_t)qw_scales % 4 != 0))
     return fail(RESQ_ERR_ARG, "qw_codes must be 16-byte aligned (HiF4 scales 4-byte aligned)");
+  if (!resq::mixed_gemm_supported(d, ldx, 0, true))
+    return fail(RESQ_ERR_UNSUPPORTED, "d or ldx too large for 32-bit operand offsets");
   {
     resq::ProfScope prof_(resq::kProfMixed, s, true);
-    resq::launch_mixed_gemm(format, false, m, n, d, X, ldx, qw_codes, qw_scales, Y, ldy, s);
+    resq::launch_mixed_gemm(format, m, n, d, X, ldx, qw_codes, qw_scales, nullptr, 0, Y, ldy, s);
   }
   return check_launch("resq_linear_w4a16");
 }
@@ -629,18 +631,18 @@ int resq_linear_w16a4(int format, const uint16_t* X, int64_t m, int64_t d, int64
   }
   if (!W || (uintptr_t)W % 16 != 0 || ldw % 8 != 0 || ldw < d)
     return fail(RESQ_ERR_ARG, "W must be non-NULL, 16-byte aligned, with ldw %% 8 == 0 and ldw >= d");
-  const size_t codes_bytes = align256((size_t)m * d / 2);
-  rc = check_ws(workspace, workspace_bytes, codes_bytes + align256(scale_bytes(format, m, d)));
+  if (!resq::mixed_gemm_supported(d, d, ldw, false))
+    return fail(RESQ_ERR_UNSUPPORTED, "d or ldw too large for 32-bit operand offsets");
+  rc = check_ws(workspace, workspace_bytes, align256((size_t)m * d * 2));
   if (rc != RESQ_OK) return rc;
-  uint8_t* codes = (uint8_t*)workspace;
-  void* scales = (char*)workspace + codes_bytes;
+  uint16_t* qx = (uint16_t*)workspace;  // Q(X) dequantized to bf16, m x d
   {
     resq::ProfScope prof_(resq::kProfQuantRows, s);
-    resq::launch_quant_rows(format, X, false, m, d, ldx, codes, scales, s);
+    resq::launch_quant_rows_bf16(format, X, m, d, ldx, qx, d, s);
   }
   {
     resq::ProfScope prof_(resq::kProfMixed, s, true);
-    resq::launch_mixed_gemm(format, true, m, n, d, W, ldw, codes, scales, Y, ldy, s);
+    resq::launch_mixed_gemm(format, m, n, d, qx, d, nullptr, nullptr, W, ldw, Y, ldy, s);
   }
   return check_launch("resq_linear_w16a4");
 }

@@ -129,13 +129,21 @@ void gemm_plan_info(int fmt, int64_t M, int64_t N, int64_t K, bool may_split, in
 // scales, each 256-byte aligned) and the B buffer fit 32-bit offsets.
 bool gemm_supported(int fmt, int64_t M, int64_t N, int64_t K, int n_terms);
 
-// Mixed-precision GEMM (mixed.hip): Y[M][N] = A[M][K] B[N][K]^T in float32 on the bf16 MFMA,
-// one operand bf16 (`dense`, row-major, row stride ld) and the other FP4 (K-major codes and
-// scales of format fmt): A when a_quantized (W16A4), else B (W4A16).  dense must be 16-byte
-// aligned with ld % 8 == 0, codes 16-byte aligned, K a multiple of the format's block.
-void launch_mixed_gemm(int fmt, bool a_quantized, int64_t M, int64_t N, int64_t K, const uint16_t* dense,
-                       int64_t ld, const uint8_t* codes, const void* scales, float* Y, int64_t ldy,
-                       hipStream_t s);
+// Mixed-precision GEMM (mixed.hip): Y[M][N] = A[M][K] B[N][K]^T in float32 on the bf16 MFMA.
+// A is bf16 (row-major, row stride lda).  B is FP4 (K-major codes and scales of format fmt)
+// when b_codes is not null, else bf16 rows (b_dense, row stride ldb).  A, b_codes and b_dense
+// are 16-byte aligned with lda, ldb % 8 == 0, HiF4 scales 4-byte aligned, K a multiple of the
+// format's block, and mixed_gemm_supported(K, lda, ldb, b_codes != null) holds.
+void launch_mixed_gemm(int fmt, int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
+                       const uint8_t* b_codes, const void* b_scales, const uint16_t* b_dense, int64_t ldb,
+                       float* Y, int64_t ldy, hipStream_t s);
+// Whether one operand row of these strides fits the kernel's 32-bit buffer offsets (larger
+// matrices are split over several launches).
+bool mixed_gemm_supported(int64_t K, int64_t lda, int64_t ldb, bool b_quantized);
+// Q(X) along rows (blocks along cols) written as its dequantized values in bf16 (exact): out
+// is rows x cols with row stride ldo (8-byte aligned, ldo % 4 == 0).
+void launch_quant_rows_bf16(int fmt, const uint16_t* x, int64_t rows, int64_t cols, int64_t ld, uint16_t* out,
+                            int64_t ldo, hipStream_t s);
 
 // p[0 .. n) = 0 (a fill kernel: callers may capture the library's launches in a graph).
 void launch_zero_f32(float* p, int64_t n, hipStream_t s);

@@ -4,34 +4,49 @@
 //
 // Both run on gfx950's bf16 MFMA (v_mfma_f32_32x32x16_bf16, float32 accumulation).  Every
 // FP4 value is exact in bf16 (an MXFP4 value has 2 significant bits, a HiF4 value
-// k (4+m) 2^(e-35-b) at most 6), so the FP4 operand is dequantized to bf16 without rounding
-// and every product is exact in float32; only the accumulation rounds.  The FP4 operand
-// arrives K-major (codes + block scales, the ABI's exchange format) and is dequantized on
-// its way from global memory into LDS: HBM carries 4.25 (MXFP4) or 4.5 (HiF4) bits per
-// element of that operand, which is what makes W4A16 the bandwidth-saving option at decode.
+// k (4+m) 2^(e-35-b) at most 6), so an FP4 operand is dequantized to bf16 without rounding
+// and every product is exact in float32; only the accumulation rounds.
 //
-// Data movement: a workgroup of 2 x 2 waves owns a (64 TM) x (64 TN) output tile; per K
-// chunk of 64 each thread loads its share of both operands into registers (16-byte loads of
-// bf16 rows or of FP4 codes), the workgroup writes them to one of two LDS buffers as bf16
-// rows (K contiguous, rows padded by 16 bytes; FP4 codes dequantized on the way), and each
-// wave runs TM x TN x 4 MFMAs (K = 16 each) from LDS.  Global loads run two chunks ahead of
-// the MFMAs (two register stages), so each load's latency is covered by two chunks of work;
-// one barrier per chunk.  Tall tiles (TM up to 4, i.e. every row of a 256-token decode batch)
-// spread the dequantization of a weight chunk over more output rows; small grids with long K
-// split each tile's chunks over four K groups of waves.
+// Operand roles.  The row operand A (rows of Y) is always bf16: X itself (W4A16), or Q(X)
+// dequantized to bf16 by a row pass before the GEMM (W16A4: the activations are a few MB at
+// rollout batch sizes, so writing them at 2 bytes per element costs nothing next to the bf16
+// weights, and the GEMM then dequantizes nothing per output tile).  The column operand B is
+// the weight: K-major FP4 codes + block scales (W4A16), dequantized in registers right before
+// the MFMAs, so HBM carries 4.25 (MXFP4) or 4.5 (HiF4) bits per weight; or bf16 rows (W16A4).
 //
-// Dequantization: MXFP4 pairs go through gfx950's scaled conversion to bf16
-// (v_cvt_scalef32_pk_bf16_fp4, scale 2^E, exact); a HiF4 element is the integer k (4 + m)
-// converted to float32 (exact) and scaled by 2^(e-35-b) with v_ldexp_f32 (exact), whose top
-// half is its bf16 pattern.
+// Work split.  A workgroup owns a 32 TM x (32 TN WN) output tile: WN waves side by side along
+// the columns, each owning 32 TM x 32 TN of it, all of them reading the same A rows.  KG such
+// groups share the tile and split its K chunks (chunk c goes to group c mod KG); at the end
+// they add their accumulators through LDS in group order (deterministic).  Workgroups are
+// dealt to the eight XCDs in contiguous ranges, row tiles fastest, so the workgroups that read
+// one weight strip run on one XCD at about the same time and share its L2.
 //
-// MFMA operand layout (32x32x16 bf16): lane l holds row (A) / column (B) l % 32 and the 8
-// consecutive K elements 8 (l / 32) .. + 7 of the 16-wide step.  Accumulator register r of
-// lane l is row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32.
+// Data movement.  K advances in rounds of 64.  Both operands go from global memory straight
+// into LDS (buffer loads with the LDS destination, no register staging).  A copy instruction
+// moves 64 lanes x 16 bytes; it is laid out to read whole 128-byte lines (8 rows x 128 bytes
+// of A or bf16 B per round; for FP4 B, 8 columns x 128 bytes of codes, which span four
+// rounds, so FP4 codes move in super-chunks of 256 K), since copies that touch many lines
+// for few bytes each run far slower than the bytes alone would suggest.  In LDS each 128-byte
+// row keeps its 16-byte segments XOR-swizzled by the row index, so the MFMA operand reads
+// (16 bytes per lane, 32 rows) are free of bank conflicts.  A rows are copied once per group
+// (each wave 4 TM / WN of the instructions) and read by all WN waves; B is private to its
+// wave.  NS rounds are in flight; one barrier per round.  FP4 scales travel as one dword per
+// lane, tile and round (MXFP4: the aligned dword holding the lane's scale byte).
+//
+// K order inside a chunk.  The sum over K may take any order, as long as A and B pair the
+// same K.  Lane l (row or column l % 32, half h = l / 32) holds the 32 consecutive K elements
+// 32 h .. 32 h + 31 of the chunk, and the MFMA of step kk (0..3) takes elements 8 kk .. 8 kk + 7
+// of them: one 16-byte read per step for bf16, one 32-bit word of codes for FP4, whose
+// 32-element span is exactly one MXFP4 block and one half of a HiF4 block.
+//
+// MFMA layouts (32x32x16 bf16): lane l holds row (A) / column (B) l % 32 and 8 K elements of
+// the 16-wide step; accumulator register r of lane l is row 8 (r / 4) + 4 (l / 32) + r % 4,
+// column l % 32.
 #include <type_traits>
 
 #include "kernels.h"
 #include "device_fp4.h"
+#include "quant_core.h"
 #include "profiler.h"
 
 namespace resq {
@@ -40,24 +55,53 @@ namespace {
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
-constexpr int kChunk = 64;              // K elements per LDS chunk
-constexpr int kRowHalves = kChunk + 8;  // bf16 per LDS row (16 bytes of padding)
+constexpr int kXcds = 8;
+// Largest operand buffer a launch addresses (32-bit buffer offsets); kOut lies past every
+// such buffer, so a copy from it reads zeros.
+constexpr uint64_t kMaxBuffer = 0xFFFFFE00ull;
+constexpr uint32_t kOut = 0xFFFFFF00u;
 
 struct MixedParams {
   int64_t M, N, K;
-  // the bf16 operand: row-major, row stride ld (elements)
-  const uint16_t* dense;
-  int64_t ld;
-  // the FP4 operand: K-major codes [rows][K/2] and scales (MXFP4 uint8 [rows][K/32], HiF4
-  // uint32 [rows][K/64])
-  const uint8_t* codes;
-  const void* scales;
+  const void* a;        // bf16 rows, lda_b bytes apart
+  uint32_t a_bytes, lda_b;
+  const void* b;        // FP4 codes (K / 2 bytes per row) or bf16 rows, ldb_b bytes apart
+  uint32_t b_bytes, ldb_b;
+  const void* bs;       // FP4 scales: MXFP4 uint8 [N][K/32] (from byte bs_mis on), HiF4 uint32 [N][K/64]
+  uint32_t bs_bytes, bs_mis;
   float* Y;
   int64_t ldy;
+  uint32_t mt;          // row tiles
+  uint32_t n_wg, per_xcd;
 };
 
-typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+// 16 bytes per lane from buffer offset voff into LDS: lane l's bytes land at lds + 16 l.
+__device__ __forceinline__ void copy16(__amdgpu_buffer_rsrc_t r, void* lds, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)lds, 16, voff, 0, 0, 0);
+}
+
+// 4 bytes per lane from buffer offset voff (4-byte aligned) into LDS: lane l's at lds + 4 l.
+__device__ __forceinline__ void copy4(__amdgpu_buffer_rsrc_t r, void* lds, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)lds, 4, voff, 0, 0, 0);
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt field is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Barrier that also waits for this wave's LDS reads but not for its LDS-destination copies
+// (those are waited for with wait_vmcnt); the memory clobber keeps accesses on their side.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
 
 // 2^E as float32 for an E8M0 code (E = code - 127; 2^-127 is a float32 subnormal).
 __device__ __forceinline__ float e8m0_f32(uint32_t code) {
@@ -91,136 +135,127 @@ __device__ __forceinline__ void dequant8(uint32_t w, int elem0, uint32_t scale, 
   }
 }
 
-// Per-thread staging of one operand's K chunk.  Dense: R rows x 64 bf16 = 8 R 16-byte pieces,
-// spread over the 256 threads.  FP4: R rows x 2 halves of 32 codes (16 bytes each).
-template <int R>
-struct DenseStage {
-  static constexpr int kPieces = R * kChunk / 8;           // 16-byte pieces per chunk
-  static constexpr int kPer = (kPieces + 255) / 256;       // per thread
-  v4u v[kPer];
-};
-template <int R>
-struct QuantStage {
-  static constexpr int kPieces = 2 * R;                    // 16-byte code pieces per chunk
-  static constexpr int kPer = (kPieces + 255) / 256;
-  v4u c[kPer];
-  uint32_t s[kPer];
-};
-
-template <int R>
-__device__ __forceinline__ void load_dense(DenseStage<R>& st, const uint16_t* base, int64_t ld, int64_t row0,
-                                           int64_t rows, int64_t k0, int64_t K, int tid) {
-#pragma unroll
-  for (int x = 0; x < DenseStage<R>::kPer; ++x) {
-    const int piece = tid + 256 * x;
-    const int r = piece / 8, seg = piece % 8;
-    const int64_t row = row0 + r, k = k0 + 8 * seg;
-    v4u z = {0u, 0u, 0u, 0u};
-    if (piece < DenseStage<R>::kPieces && row < rows && k < K)
-      z = *reinterpret_cast<const v4u*>(base + row * ld + k);
-    st.v[x] = z;
+// Geometry of one configuration.  Per K group: a ring of NS round slots (A rows, the FP4
+// scale dwords or the bf16 B rows of one 64-K round) and, for FP4 B, a ring of RB super-chunk
+// slots (the codes of four rounds, 128 bytes per column).  Copy instructions per wave and
+// round: APW for A, TN scale dwords (FP4) or 4 TN (bf16 B); plus, in every fourth round, the
+// 4 TN copies of one FP4 super-chunk.
+template <bool BQ, int TM, int TN, int WN, int KG, int NS>
+struct MixGeo {
+  static constexpr int AI = 4 * TM;                    // A copies (1 KB, 8 rows) per round
+  static constexpr int APW = AI / WN;                  // of which each wave issues
+  static constexpr int BR = BQ ? 0 : 4 * TN;           // bf16 B copies per wave and round
+  static constexpr int SC = BQ ? TN * 256 : 0;         // FP4 scale bytes per wave and round
+  static constexpr int RSLOT = AI * 1024 + WN * (BR * 1024 + SC);  // round slot
+  static constexpr int RB = BQ ? 2 : 0;                // super-chunk slots
+  static constexpr int BSLOT = BQ ? WN * 4 * TN * 1024 : 0;        // super-chunk slot
+  static constexpr int GROUP = NS * RSLOT + RB * BSLOT;
+  static constexpr int RED = (KG - 1) * WN * TM * TN * 16 * 64 * 4;
+  static constexpr int LDS = KG * GROUP > RED ? KG * GROUP : RED;
+  // copies issued in a round of phase q (round index mod 4)
+  static constexpr int jw(int q) { return APW + BR + (BQ ? TN : 0) + (BQ && q == 0 ? 4 * TN : 0); }
+  // copies the wait at a round of phase q leaves in flight: those of the NS - 2 later rounds
+  static constexpr int inflight(int q) {
+    int n = 0;
+    for (int u = 1; u <= NS - 2; ++u) n += jw((q + u) % 4);
+    return n;
   }
-}
+  static constexpr bool ok = AI % WN == 0 && (NS == 2 || NS == 4) &&
+                             inflight(0) + jw(0) < 64 && inflight(1) + jw(1) < 64 &&
+                             inflight(2) + jw(2) < 64 && inflight(3) + jw(3) < 64 &&
+                             LDS <= 160 * 1024;
+};
 
-template <int R>
-__device__ __forceinline__ void store_dense(const DenseStage<R>& st, uint16_t* lds, int tid) {
+// A and bf16 B rows in LDS: row r (128 bytes of one 64-K round) at r * 128, its 16-byte
+// segment s at slot s ^ (r % 8), so the MFMA operand reads of eight consecutive rows hit
+// eight different bank groups.  A copy instruction moves 8 rows: lane l fills slot l % 8 of
+// row l / 8 with the segment that belongs there.  FP4 codes: column c's 128 bytes of one
+// super-chunk (256 K: segment s = round s / 2, lane half s % 2) the same way.
+__device__ __forceinline__ uint32_t swz(int row, int seg) { return (uint32_t)(row * 128 + 16 * (seg ^ (row & 7))); }
+
+template <int FMT, bool BQ, int TM, int TN, int WN, int KG, int NS>
+__global__ __launch_bounds__(64 * WN * KG) void mixed_gemm_kernel(MixedParams p) {
+  using G = MixGeo<BQ, TM, TN, WN, KG, NS>;
+  static_assert(G::ok, "configuration out of range");
+  extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
+  const uint32_t bid = blockIdx.x;
+  const uint32_t wg = (bid % kXcds) * p.per_xcd + bid / kXcds;
+  if (wg >= p.n_wg) return;
+  const uint32_t tm = wg % p.mt, tn = wg / p.mt;
+  const int lane = threadIdx.x & 63, h = lane >> 5, l32 = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = wave / WN, wn = wave % WN;
+  const int64_t row0 = (int64_t)tm * 32 * TM;
+  const int64_t colw = ((int64_t)tn * WN + wn) * 32 * TN;  // this wave's first column
+  const uint32_t nchunks = (uint32_t)((p.K + 63) / 64);
+  const uint32_t nsuper = (nchunks + 3) / 4;
+  const uint32_t nrounds = 4 * ((nsuper + KG - 1) / KG);  // per group, a multiple of 4
+  uint8_t* rring = smem + (size_t)g * G::GROUP;
+  uint8_t* bring = rring + NS * G::RSLOT;
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.a, p.a_bytes), rb = make_rsrc(p.b, p.b_bytes);
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(p.bs, p.bs_bytes);
+  // the copy lane's row within its 8-row instruction and the global segment it moves
+  const int crow = lane >> 3, cseg = (lane & 7) ^ (lane >> 3);
+
+  // Round-0 offsets of this lane's copies, and kOut masks for rows / columns outside the
+  // matrix: an offset OR-ed with kOut lies past every buffer, so its copy reads zeros.
+  uint32_t aoff[G::APW], amask[G::APW];
 #pragma unroll
-  for (int x = 0; x < DenseStage<R>::kPer; ++x) {
-    const int piece = tid + 256 * x;
-    if (piece < DenseStage<R>::kPieces) {
-      const int r = piece / 8, seg = piece % 8;
-      *reinterpret_cast<v4u*>(lds + r * kRowHalves + 8 * seg) = st.v[x];
+  for (int y = 0; y < G::APW; ++y) {
+    const int64_t row = row0 + 8 * (wn + WN * y) + crow;
+    aoff[y] = row < p.M ? (uint32_t)row * p.lda_b + 16u * cseg : 0u;
+    amask[y] = row < p.M ? 0u : kOut;
+  }
+  // B copies: bf16 rows per round (BR) or FP4 super-chunks (4 TN), 8 columns each
+  constexpr int BX = BQ ? 4 * TN : G::BR;
+  uint32_t boff[BX], bmask[BX];
+#pragma unroll
+  for (int x = 0; x < BX; ++x) {
+    const int64_t col = colw + 8 * x + crow;
+    boff[x] = col < p.N ? (uint32_t)col * p.ldb_b + 16u * cseg : 0u;
+    bmask[x] = col < p.N ? 0u : kOut;
+  }
+  uint32_t soff[TN], smask[TN];
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int64_t col = colw + 32 * j + l32;
+    smask[j] = col < p.N ? 0u : kOut;
+    if constexpr (BQ) {
+      if constexpr (FMT == 0) soff[j] = col < p.N ? (uint32_t)(col * (p.K / 32)) + h + p.bs_mis : 0u;
+      else soff[j] = col < p.N ? (uint32_t)(col * (p.K / 64)) * 4u : 0u;
     }
   }
-}
 
-template <int FMT, int R>
-__device__ __forceinline__ void load_quant(QuantStage<R>& st, const uint8_t* codes, const void* scales,
-                                           int64_t row0, int64_t rows, int64_t k0, int64_t K, int tid) {
+  // Round t of this group is chunk 4 (g + KG (t / 4)) + t % 4: each group takes whole
+  // super-chunks, so the FP4 codes of a column are read 128 contiguous bytes at a time.
+  auto chunk_of = [&](uint32_t t) { return 4u * (g + KG * (t >> 2)) + (t & 3u); };
+  auto super_copies = [&](uint32_t S) {  // FP4 super-chunk S of this group into its slot
+    const uint32_t k4 = g + KG * S;
+    uint8_t* dst = bring + (S % G::RB) * G::BSLOT + wn * 4 * TN * 1024;
+    const uint32_t kout = 256ull * k4 + 32u * cseg < (uint64_t)p.K ? 0u : kOut;
 #pragma unroll
-  for (int x = 0; x < QuantStage<R>::kPer; ++x) {
-    const int piece = tid + 256 * x;
-    const int r = piece / 2, half = piece % 2;
-    const int64_t row = row0 + r, k = k0 + 32 * half;
-    v4u z = {0u, 0u, 0u, 0u};
-    uint32_t s = 0u;
-    if (piece < QuantStage<R>::kPieces && row < rows && k < K) {
-      z = *reinterpret_cast<const v4u*>(codes + row * (K / 2) + k / 2);
-      if constexpr (FMT == 0) s = reinterpret_cast<const uint8_t*>(scales)[row * (K / 32) + k / 32];
-      else s = reinterpret_cast<const uint32_t*>(scales)[row * (K / 64) + k / 64];
-    }
-    st.c[x] = z;
-    st.s[x] = s;
-  }
-}
-
-template <int FMT, int R>
-__device__ __forceinline__ void store_quant(const QuantStage<R>& st, uint16_t* lds, int tid) {
+    for (int x = 0; x < BX; ++x) copy16(rb, dst + x * 1024, (boff[x] + 128u * k4) | bmask[x] | kout);
+  };
+  // Issue slot u: round u's A rows, scales or bf16 B rows into round slot u % NS (= rs_),
+  // and, at every fourth slot, FP4 super-chunk u / 4.
+  auto issue = [&](uint32_t u, int rs_, bool super) {
+    const uint32_t c = chunk_of(u);
+    const uint32_t kout = 64ull * c + 8u * cseg < (uint64_t)p.K ? 0u : kOut;  // this lane's 8 K
+    uint8_t* st = rring + rs_ * G::RSLOT;
 #pragma unroll
-  for (int x = 0; x < QuantStage<R>::kPer; ++x) {
-    const int piece = tid + 256 * x;
-    if (piece < QuantStage<R>::kPieces) {
-      const int r = piece / 2, half = piece % 2;
-      uint16_t* dst = lds + r * kRowHalves + 32 * half;
+    for (int y = 0; y < G::APW; ++y) copy16(ra, st + (wn + WN * y) * 1024, (aoff[y] + 128u * c) | amask[y] | kout);
+    uint8_t* sw = st + G::AI * 1024 + wn * (G::BR * 1024 + G::SC);
+    if constexpr (BQ) {
+      const uint32_t skout = 64ull * c + 32u * h < (uint64_t)p.K ? 0u : kOut;  // this lane's block
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        uint32_t o[4];
-        // element index inside the HiF4 64-block: this half's 32 elements start at 32 half
-        dequant8<FMT>(st.c[x][w], 32 * half + 8 * w, st.s[x], o);
-        *reinterpret_cast<v4u*>(dst + 8 * w) = v4u{o[0], o[1], o[2], o[3]};
+      for (int j = 0; j < TN; ++j) {
+        const uint32_t so = FMT == 0 ? (soff[j] + 2u * c) & ~3u : soff[j] + 4u * c;
+        copy4(rs, sw + j * 256, so | smask[j] | skout);
       }
-    }
-  }
-}
-
-// AQ: operand A (rows of Y) is the FP4 one (W16A4); otherwise operand B is (W4A16).  KG K
-// groups of four waves share the output tile: group g takes chunks g, g + KG, ... with its own
-// LDS buffers and register stages, and at the end groups 1.. park their accumulators in LDS
-// and group 0 adds them in group order (deterministic) and stores the tile.
-template <int FMT, bool AQ, int TM, int TN, int KG>
-__global__ __launch_bounds__(256 * KG) void mixed_gemm_kernel(MixedParams p) {
-  constexpr int BM = 64 * TM, BN = 64 * TN;
-  constexpr int PER = TM * TN * 16 * 64;  // accumulator floats per wave
-  union Smem {
-    struct {
-      uint16_t A[KG][2][BM * kRowHalves];
-      uint16_t B[KG][2][BN * kRowHalves];
-    } t;
-    float red[KG > 1 ? (KG - 1) * 4 * PER : 1];
-  };
-  __shared__ __attribute__((aligned(16))) Smem sm;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int g = wave / 4, wl = wave % 4, tg = tid % 256;  // K group, wave and thread within it
-  const int wm = wl % 2, wn = wl / 2;
-  const int64_t row0 = (int64_t)blockIdx.y * BM, col0 = (int64_t)blockIdx.x * BN;
-  const int64_t nchunks = (p.K + kChunk - 1) / kChunk;
-  const int64_t nq = nchunks > g ? (nchunks - g + KG - 1) / KG : 0;  // this group's chunks
-  const int64_t nrounds = (nchunks + KG - 1) / KG;                   // group 0's count
-  uint16_t(*As)[BM * kRowHalves] = sm.t.A[g];
-  uint16_t(*Bs)[BN * kRowHalves] = sm.t.B[g];
-
-  using AStage = typename std::conditional<AQ, QuantStage<BM>, DenseStage<BM>>::type;
-  using BStage = typename std::conditional<AQ, DenseStage<BN>, QuantStage<BN>>::type;
-  AStage sa[2];
-  BStage sb[2];
-  auto load = [&](int64_t q, int r) {
-    const int64_t k0 = (q * KG + g) * kChunk;
-    if constexpr (AQ) {
-      load_quant<FMT, BM>(sa[r], p.codes, p.scales, row0, p.M, k0, p.K, tg);
-      load_dense<BN>(sb[r], p.dense, p.ld, col0, p.N, k0, p.K, tg);
+      if (super) super_copies(u >> 2);
     } else {
-      load_dense<BM>(sa[r], p.dense, p.ld, row0, p.M, k0, p.K, tg);
-      load_quant<FMT, BN>(sb[r], p.codes, p.scales, col0, p.N, k0, p.K, tg);
-    }
-  };
-  auto store = [&](int r, int buf) {
-    if constexpr (AQ) {
-      store_quant<FMT, BM>(sa[r], As[buf], tg);
-      store_dense<BN>(sb[r], Bs[buf], tg);
-    } else {
-      store_dense<BM>(sa[r], As[buf], tg);
-      store_quant<FMT, BN>(sb[r], Bs[buf], tg);
+#pragma unroll
+      for (int x = 0; x < BX; ++x) copy16(rb, sw + x * 1024, (boff[x] + 128u * c) | bmask[x] | kout);
     }
   };
 
@@ -232,20 +267,36 @@ __global__ __launch_bounds__(256 * KG) void mixed_gemm_kernel(MixedParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  auto compute = [&](int buf) {
-#pragma unroll
-    for (int kk = 0; kk < kChunk / 16; ++kk) {
-      const int koff = 16 * kk + 8 * (lane / 32);
-      v8bf a[TM], b[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int r = (wm * TM + i) * 32 + lane % 32;
-        a[i] = __builtin_bit_cast(v8bf, *reinterpret_cast<const v4u*>(As[buf] + r * kRowHalves + koff));
-      }
+  auto compute = [&](uint32_t t, int rs_) {
+    const uint8_t* st = rring + rs_ * G::RSLOT;
+    const uint8_t* sw = st + G::AI * 1024 + wn * (G::BR * 1024 + G::SC);
+    v4u bc[TN];
+    uint32_t sc[TN];
+    if constexpr (BQ) {
+      const uint8_t* bs = bring + ((t >> 2) % G::RB) * G::BSLOT + wn * 4 * TN * 1024;
+      const uint32_t c = chunk_of(t);
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
-        const int r = (wn * TN + j) * 32 + lane % 32;
-        b[j] = __builtin_bit_cast(v8bf, *reinterpret_cast<const v4u*>(Bs[buf] + r * kRowHalves + koff));
+        bc[j] = *reinterpret_cast<const v4u*>(bs + swz(32 * j + l32, 2 * (int)(t & 3u) + h));
+        sc[j] = *reinterpret_cast<const uint32_t*>(sw + j * 256 + 4 * lane);
+        if constexpr (FMT == 0) sc[j] = (sc[j] >> (8 * ((soff[j] + 2u * c) & 3u))) & 0xFFu;
+      }
+    }
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      v8bf a[TM], b[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        a[i] = __builtin_bit_cast(v8bf, *reinterpret_cast<const v4u*>(st + swz(32 * i + l32, 4 * h + kk)));
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        if constexpr (BQ) {
+          uint32_t o[4];
+          dequant8<FMT>(bc[j][kk], 32 * h + 8 * kk, sc[j], o);
+          b[j] = __builtin_bit_cast(v8bf, v4u{o[0], o[1], o[2], o[3]});
+        } else {
+          b[j] = __builtin_bit_cast(v8bf, *reinterpret_cast<const v4u*>(sw + swz(32 * j + l32, 4 * h + kk)));
+        }
       }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
@@ -254,34 +305,37 @@ __global__ __launch_bounds__(256 * KG) void mixed_gemm_kernel(MixedParams p) {
     }
   };
 
-  // The group's chunk q sits in register stage q % 2 from its load (two chunks ahead) until
-  // its store into LDS buffer q % 2, one chunk ahead of its MFMAs.  Each round: issue chunk
-  // q+2's loads, run chunk q's MFMAs, store chunk q+1 into the other buffer (last read during
-  // chunk q-1, which the previous barrier closed), barrier.  Every group runs group 0's round
-  // count (it has the most chunks), so all waves meet at every barrier.
-  if (nq > 0) load(0, 0);
-  if (nq > 1) load(1, 1);
-  if (nq > 0) store(0, 0);
-  __syncthreads();
-  for (int64_t q0 = 0; q0 < nrounds; q0 += 2) {
+  // Round t: wait until this wave's copies of issue slots <= t have landed (those of the
+  // NS - 2 later slots stay in flight), a barrier (every wave's copies of round t have landed
+  // and every wave has finished reading round t - 1, whose round slot and, after the last
+  // round of a super-chunk, super-chunk slot are refilled next), issue slot t + NS - 1, then
+  // round t's MFMAs.  FP4 super-chunk S is issued with round 4 S, so it has landed by round
+  // 4 S; its slot (S mod 2) was last read in rounds 4 S - 8 .. 4 S - 5, before the barrier of
+  // round 4 S - NS + 1 that precedes its copies (NS <= 4).  The loop is unrolled four times,
+  // so the round slots (NS divides 4) and the wait counts are compile-time.
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int64_t q = q0 + u;
-      if (q < nrounds) {
-        if (q < nq) {
-          if (q + 2 < nq) load(q + 2, u);
-          compute(u);
-          if (q + 1 < nq) store(1 - u, 1 - u);
-        }
-        __syncthreads();
-      }
-    }
+  for (int u = 0; u < NS - 1; ++u) issue(u, u, u % 4 == 0);
+  for (uint32_t t0 = 0; t0 < nrounds; t0 += 4) {
+    auto round = [&](auto qc) {
+      constexpr int q = decltype(qc)::value;
+      wait_vmcnt<G::inflight(q)>();
+      lds_barrier();
+      issue(t0 + q + NS - 1, (q + NS - 1) % NS, (q + NS - 1) % 4 == 0);
+      compute(t0 + q, q % NS);
+    };
+    round(std::integral_constant<int, 0>{});
+    round(std::integral_constant<int, 1>{});
+    round(std::integral_constant<int, 2>{});
+    round(std::integral_constant<int, 3>{});
   }
+  wait_vmcnt<0>();  // the copies of the slots past the end have landed before LDS is reused
 
   if constexpr (KG > 1) {
-    // every wave is past its last LDS read (the loop's final barrier): reuse LDS for the sums
+    constexpr int PER = TM * TN * 16 * 64;  // accumulator floats per wave
+    float* red = reinterpret_cast<float*>(smem);
+    lds_barrier();
     if (g > 0) {
-      float* dst = sm.red + ((size_t)(g - 1) * 4 + wl) * PER;
+      float* dst = red + ((size_t)(g - 1) * WN + wn) * PER;
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -289,11 +343,11 @@ __global__ __launch_bounds__(256 * KG) void mixed_gemm_kernel(MixedParams p) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) dst[((i * TN + j) * 16 + r) * 64 + lane] = acc[i][j][r];
     }
-    __syncthreads();
+    lds_barrier();
     if (g > 0) return;
 #pragma unroll
     for (int gg = 1; gg < KG; ++gg) {
-      const float* src = sm.red + ((size_t)(gg - 1) * 4 + wl) * PER;
+      const float* src = red + ((size_t)(gg - 1) * WN + wn) * PER;
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -303,63 +357,188 @@ __global__ __launch_bounds__(256 * KG) void mixed_gemm_kernel(MixedParams p) {
     }
   }
 
-  const int half = lane >> 5, l32 = lane & 31;
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-      const int64_t col = col0 + (wn * TN + j) * 32 + l32;
+      const int64_t col = colw + 32 * j + l32;
+      if (col >= p.N) continue;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int64_t row = row0 + (wm * TM + i) * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        if (row < p.M && col < p.N) p.Y[row * p.ldy + col] = acc[i][j][r];
+        const int64_t row = row0 + 32 * i + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (row < p.M) p.Y[row * p.ldy + col] = acc[i][j][r];
       }
     }
 }
 
-template <int FMT, bool AQ, int TM, int TN, int KG>
-void launch_tile(const MixedParams& p, hipStream_t s) {
-  const dim3 grid((unsigned)((p.N + 64 * TN - 1) / (64 * TN)), (unsigned)((p.M + 64 * TM - 1) / (64 * TM)));
-  launch_timed(mixed_gemm_kernel<FMT, AQ, TM, TN, KG>, grid, dim3(256 * KG), 0u, s, p);
+// Q(X) along rows, written as the dequantized values in bf16 (exact): one lane per 4
+// elements, grid (ceil(cols / 1024), rows).  out is 8-byte aligned with ldo % 4 == 0.
+template <int FMT, bool VEC>
+__global__ __launch_bounds__(256) void quant_rows_bf16_kernel(const uint16_t* __restrict__ x, int64_t rows,
+                                                              int64_t cols, int64_t ld,
+                                                              uint16_t* __restrict__ out, int64_t ldo) {
+  const int64_t j4 = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (4 * j4 >= cols) return;  // whole blocks drop out together (cols % block == 0)
+  for (int64_t row = blockIdx.y; row < rows; row += gridDim.y) {
+    float v[4];
+    const int64_t i = row * ld + 4 * j4;
+    if constexpr (VEC) {
+      const uint2 t = *reinterpret_cast<const uint2*>(x + i);
+      v[0] = bf16_to_f32(t.x & 0xFFFFu); v[1] = bf16_to_f32(t.x >> 16);
+      v[2] = bf16_to_f32(t.y & 0xFFFFu); v[3] = bf16_to_f32(t.y >> 16);
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) v[k] = bf16_to_f32(x[i + k]);
+    }
+    const Quad q = quantize_quad<FMT>(v);
+    // the values carry at most 6 significant bits: their float32 patterns end in 16 zero bits
+    const uint32_t lo = (__float_as_uint(q.val[0]) >> 16) | (__float_as_uint(q.val[1]) & 0xFFFF0000u);
+    const uint32_t hi = (__float_as_uint(q.val[2]) >> 16) | (__float_as_uint(q.val[3]) & 0xFFFF0000u);
+    *reinterpret_cast<uint2*>(out + row * ldo + 4 * j4) = make_uint2(lo, hi);
+  }
 }
 
-// Tile choice: the FP4 operand's dequantization is shared by the rows (W4A16) or columns
-// (W16A4) of the tile, so the tile is as long as possible along the other operand while the
-// grid still has at least 128 workgroups; the other side stays 64 wide.  Grids of 64 x 64
-// tiles within the CUs that have at least 16 K chunks take four K groups per workgroup.
-template <int FMT, bool AQ>
-void launch_fmt(const MixedParams& p, hipStream_t s) {
-  const int64_t along = AQ ? p.N : p.M, across = AQ ? p.M : p.N;
-  auto wgs = [&](int64_t t) { return ((along + 64 * t - 1) / (64 * t)) * ((across + 63) / 64); };
-  const int t = wgs(4) >= 128 ? 4 : wgs(2) >= 128 ? 2 : 1;
-  const bool kgroups = t == 1 && wgs(1) <= 256 && (p.K + kChunk - 1) / kChunk >= 16;
-  if constexpr (AQ) {
-    if (t == 4) launch_tile<FMT, AQ, 1, 4, 1>(p, s);
-    else if (t == 2) launch_tile<FMT, AQ, 1, 2, 1>(p, s);
-    else if (kgroups) launch_tile<FMT, AQ, 1, 1, 4>(p, s);
-    else launch_tile<FMT, AQ, 1, 1, 1>(p, s);
+// Tile configurations (TM, TN, WN, KG, NS), instantiated for both operand kinds where they
+// fit (MixGeo::ok).
+struct MixPlan {
+  int tm, tn, wn, kg, ns;
+};
+#define RESQ_MIXED_CONFIGS(X) \
+  X(2, 1, 4, 1, 4) X(1, 1, 4, 1, 4) X(8, 1, 4, 1, 2) X(1, 1, 2, 4, 4) X(1, 1, 4, 2, 4) X(2, 1, 2, 4, 2) \
+  X(2, 2, 4, 1, 2) X(1, 2, 4, 1, 2) X(1, 1, 2, 4, 2)
+
+template <int FMT, bool BQ, int TM, int TN, int WN, int KG, int NS>
+void launch_cfg(MixedParams p, hipStream_t s) {
+  using G = MixGeo<BQ, TM, TN, WN, KG, NS>;
+  if constexpr (G::ok) {
+    p.mt = (uint32_t)((p.M + 32 * TM - 1) / (32 * TM));
+    const uint64_t nt = (uint64_t)((p.N + 32 * TN * WN - 1) / (32 * TN * WN));
+    p.n_wg = (uint32_t)(p.mt * nt);
+    p.per_xcd = (p.n_wg + kXcds - 1) / kXcds;
+    launch_timed(mixed_gemm_kernel<FMT, BQ, TM, TN, WN, KG, NS>, dim3(p.per_xcd * kXcds), dim3(64 * WN * KG),
+                 (uint32_t)G::LDS, s, p);
+  }
+}
+
+template <bool BQ>
+bool plan_fits(const MixPlan& c) {
+#define RESQ_MX_FIT(TM, TN, WN, KG, NS) \
+  if (c.tm == TM && c.tn == TN && c.wn == WN && c.kg == KG && c.ns == NS) return MixGeo<BQ, TM, TN, WN, KG, NS>::ok;
+  RESQ_MIXED_CONFIGS(RESQ_MX_FIT)
+#undef RESQ_MX_FIT
+  return false;
+}
+
+template <int FMT, bool BQ>
+void launch_plan(const MixPlan& c, const MixedParams& p, hipStream_t s) {
+#define RESQ_MX_CASE(TM, TN, WN, KG, NS) \
+  if (c.tm == TM && c.tn == TN && c.wn == WN && c.kg == KG && c.ns == NS) return launch_cfg<FMT, BQ, TM, TN, WN, KG, NS>(p, s);
+  RESQ_MIXED_CONFIGS(RESQ_MX_CASE)
+#undef RESQ_MX_CASE
+}
+
+// Plan choice (measured on MI355X at the m = 256 decode shapes).  Wide grids (many column
+// tiles): 64 x 128 tiles, one per four waves; HiF4 weights take 256-row tiles instead, so
+// each dequantized weight fragment feeds eight MFMAs (its dequantization costs some 40 VALU
+// instructions per 8 elements).  Long K with few columns: 32 x 64 tiles in four K groups.
+// Otherwise 32 x 128 tiles in two K groups (HiF4: 64 x 64 in four).  bf16 weights (W16A4):
+// 64 x 256, 64 x 64 in four K groups, or 32 x 128 in two.
+static_assert(MixGeo<true, 2, 1, 4, 1, 4>::ok && MixGeo<true, 1, 1, 4, 1, 4>::ok && MixGeo<true, 8, 1, 4, 1, 2>::ok &&
+                  MixGeo<true, 1, 1, 2, 4, 4>::ok && MixGeo<true, 2, 1, 2, 4, 2>::ok && MixGeo<true, 1, 1, 4, 2, 4>::ok &&
+                  MixGeo<false, 2, 2, 4, 1, 2>::ok && MixGeo<false, 1, 2, 4, 1, 2>::ok &&
+                  MixGeo<false, 2, 1, 2, 4, 2>::ok && MixGeo<false, 1, 1, 2, 4, 2>::ok && MixGeo<false, 1, 1, 4, 2, 4>::ok,
+              "every plan choose() returns fits");
+template <int FMT, bool BQ>
+MixPlan choose(int64_t M, int64_t N, int64_t K) {
+  const bool small = M <= 32;
+  const int64_t mt64 = (M + 63) / 64, nchunks = (K + 63) / 64;
+  MixPlan c{};
+  if constexpr (BQ) {
+    if (mt64 * ((N + 127) / 128) >= 512)
+      c = FMT == 1 && M >= 192 ? MixPlan{8, 1, 4, 1, 2} : MixPlan{small ? 1 : 2, 1, 4, 1, 4};
+    else if (nchunks >= 64)
+      c = MixPlan{1, 1, 2, 4, 4};
+    else
+      c = FMT == 1 && !small ? MixPlan{2, 1, 2, 4, 2} : MixPlan{1, 1, 4, 2, 4};
   } else {
-    if (t == 4) launch_tile<FMT, AQ, 4, 1, 1>(p, s);
-    else if (t == 2) launch_tile<FMT, AQ, 2, 1, 1>(p, s);
-    else if (kgroups) launch_tile<FMT, AQ, 1, 1, 4>(p, s);
-    else launch_tile<FMT, AQ, 1, 1, 1>(p, s);
+    if (mt64 * ((N + 255) / 256) >= 256)
+      c = MixPlan{small ? 1 : 2, 2, 4, 1, 2};
+    else if (nchunks >= 64)
+      c = MixPlan{small ? 1 : 2, 1, 2, 4, 2};
+    else
+      c = MixPlan{1, 1, 4, 2, 4};
+  }
+  return c;
+}
+
+// Rows of A (B) per launch so that every operand buffer of a launch stays within kMaxBuffer
+// bytes (mixed_gemm_supported guarantees at least one row fits).
+inline int64_t piece(int64_t row_bytes, int64_t last_bytes, int64_t per_row_extra) {
+  int64_t n = (int64_t)(kMaxBuffer - last_bytes) / row_bytes + 1;
+  if (per_row_extra > 0) n = std::min<int64_t>(n, (int64_t)kMaxBuffer / per_row_extra);
+  return n > 256 ? n / 256 * 256 : n;
+}
+
+template <int FMT, bool BQ>
+void launch_op(int64_t M, int64_t N, int64_t K, const uint16_t* a, int64_t lda, const void* b, int64_t ldb_b,
+               const void* bs, float* Y, int64_t ldy, hipStream_t s) {
+  const MixPlan c = choose<FMT, BQ>(M, N, K);
+  const int64_t a_row = lda * 2, b_last = BQ ? K / 2 : K * 2;
+  const int64_t bs_row = BQ ? (FMT == 0 ? K / 32 : K / 16) : 0;
+  const int64_t mstep = piece(a_row, K * 2, 0), nstep = piece(ldb_b, b_last, bs_row);
+  for (int64_t m0 = 0; m0 < M; m0 += mstep) {
+    const int64_t mp = std::min(mstep, M - m0);
+    for (int64_t n0 = 0; n0 < N; n0 += nstep) {
+      const int64_t np = std::min(nstep, N - n0);
+      MixedParams p{};
+      p.M = mp;
+      p.N = np;
+      p.K = K;
+      p.a = a + m0 * lda;
+      p.a_bytes = (uint32_t)((mp - 1) * a_row + K * 2);
+      p.lda_b = (uint32_t)a_row;
+      p.b = reinterpret_cast<const uint8_t*>(b) + n0 * ldb_b;
+      p.b_bytes = (uint32_t)((np - 1) * ldb_b + b_last);
+      p.ldb_b = (uint32_t)ldb_b;
+      // MXFP4 scales are read as the aligned dwords around them (base rounded down to 4
+      // bytes); an aligned dword never crosses a page, so the bytes around the scales that
+      // these dwords take along are readable
+      const uintptr_t sp = BQ ? reinterpret_cast<uintptr_t>(bs) + (uintptr_t)(n0 * bs_row) : 0u;
+      p.bs = reinterpret_cast<const void*>(sp & ~(uintptr_t)3);
+      p.bs_mis = (uint32_t)(sp & 3u);
+      p.bs_bytes = (uint32_t)((p.bs_mis + np * bs_row + 3) / 4 * 4);
+      p.Y = Y + m0 * ldy + n0;
+      p.ldy = ldy;
+      launch_plan<FMT, BQ>(c, p, s);
+    }
   }
 }
 
 }  // namespace
 
-void launch_mixed_gemm(int fmt, bool a_quantized, int64_t M, int64_t N, int64_t K, const uint16_t* dense,
-                       int64_t ld, const uint8_t* codes, const void* scales, float* Y, int64_t ldy,
-                       hipStream_t s) {
+bool mixed_gemm_supported(int64_t K, int64_t lda, int64_t ldb, bool b_quantized) {
+  const int64_t b_row = b_quantized ? K / 2 : 2 * ldb;
+  return 2 * K <= (int64_t)kMaxBuffer / 2 && 2 * lda <= (int64_t)kMaxBuffer / 2 && b_row <= (int64_t)kMaxBuffer / 2;
+}
+
+void launch_quant_rows_bf16(int fmt, const uint16_t* x, int64_t rows, int64_t cols, int64_t ld, uint16_t* out,
+                            int64_t ldo, hipStream_t s) {
+  if (rows == 0 || cols == 0) return;
+  const dim3 grid((unsigned)((cols / 4 + 255) / 256), (unsigned)(rows < 65535 ? rows : 65535));
+  const bool vec = (uintptr_t)x % 8 == 0 && ld % 4 == 0;
+#define RESQ_QRB(F, V) hipLaunchKernelGGL((quant_rows_bf16_kernel<F, V>), grid, dim3(256), 0, s, x, rows, cols, ld, out, ldo)
+  if (fmt == 0) { if (vec) RESQ_QRB(0, true); else RESQ_QRB(0, false); }
+  else { if (vec) RESQ_QRB(1, true); else RESQ_QRB(1, false); }
+#undef RESQ_QRB
+}
+
+void launch_mixed_gemm(int fmt, int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
+                       const uint8_t* b_codes, const void* b_scales, const uint16_t* b_dense, int64_t ldb,
+                       float* Y, int64_t ldy, hipStream_t s) {
   if (M == 0 || N == 0) return;
-  MixedParams p{M, N, K, dense, ld, codes, scales, Y, ldy};
-  if (fmt == 0) {
-    if (a_quantized) launch_fmt<0, true>(p, s);
-    else launch_fmt<0, false>(p, s);
-  } else {
-    if (a_quantized) launch_fmt<1, true>(p, s);
-    else launch_fmt<1, false>(p, s);
-  }
+  if (b_codes == nullptr) launch_op<0, false>(M, N, K, A, lda, b_dense, ldb * 2, nullptr, Y, ldy, s);
+  else if (fmt == 0) launch_op<0, true>(M, N, K, A, lda, b_codes, K / 2, b_scales, Y, ldy, s);
+  else launch_op<1, true>(M, N, K, A, lda, b_codes, K / 2, b_scales, Y, ldy, s);
 }
 
 }  // namespace resq

@@ -200,5 +200,8 @@ def test_mixed_forms_check_arguments_on_the_host():
     assert P.resq_linear_w16a4(B.MXFP4, ptr, 4, 64, 64, ptr, 64, 8, ptr, 8, 0, 0, 0) == B.ERR_WORKSPACE
     # empty shapes are accepted without launching anything
     assert P.resq_linear_w4a16(B.HIF4, ptr, 0, 64, 64, ptr, ptr, 8, ptr, 8, 0) == B.OK
-    # workspace: Q(X) codes and scales, each 256-byte aligned
-    assert P.resq_workspace_size(B.OP_LINEAR_W16A4, B.HIF4, 0, 100, 128, 8) == 6400 + 1024
+    # workspace: Q(X) as bf16 values, m x d (256-byte aligned)
+    assert P.resq_workspace_size(B.OP_LINEAR_W16A4, B.HIF4, 0, 100, 128, 8) == 100 * 128 * 2
+    assert P.resq_workspace_size(B.OP_LINEAR_W16A4, B.MXFP4, 0, 3, 96, 8) == 768
+    # operand rows beyond the kernel's 32-bit offsets are refused before anything is enqueued
+    assert P.resq_linear_w4a16(B.MXFP4, ptr, 4, 64, 1 << 31, ptr, ptr, 8, ptr, 8, 0) == B.ERR_UNSUPPORTED

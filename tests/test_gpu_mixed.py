@@ -2,7 +2,9 @@
 Q(X) W^T) against the oracle.
 
 - Seeded inputs at small ragged sizes (several tiles, ragged edges, a K that ends in half a
-  64-chunk for MXFP4): float32 Y within 1e-5 normwise of the oracle's float64 result.
+  64-chunk for MXFP4), and shapes that take each tile plan (few rows with very many columns,
+  few rows with long K, long K with few columns, many column tiles): float32 Y within 1e-5
+  normwise of the oracle's float64 result.
 - Identity weights, bit for bit: W4A16 with W = c I (Q(c I) = c I) must return c X (the
   activations enter unquantized); W16A4 with W = I must return Q(X), here for every finite
   bf16 value alone in its block.
@@ -28,7 +30,8 @@ def _inputs(m, d, n, seed):
 
 @pytest.mark.parametrize("fmt", FMTS)
 @pytest.mark.parametrize("m,d,n", [(37, 512, 100), (130, 2048, 700), (256, 1088, 64), (5, 64, 3),
-                                   (300, 4096, 520)])
+                                   (300, 4096, 520), (5, 64, 65600), (20, 4160, 300), (200, 4096, 96),
+                                   (256, 256, 33000), (130, 64, 22000)])
 def test_mixed_forms_match_the_oracle(fmt, m, d, n):
     import paper_2607_26515_amd as P
     if d % F.block_size(fmt):
