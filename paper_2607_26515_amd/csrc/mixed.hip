@@ -160,18 +160,22 @@ struct MixGeo {
     for (int u = 1; u <= NS - 2; ++u) n += jw((q + u) % 4);
     return n;
   }
-  static constexpr bool ok = AI % WN == 0 && (NS == 2 || NS == 4) &&
+  static constexpr bool ok = AI % WN == 0 && WN % 2 == 0 && (NS == 2 || NS == 4) &&
                              inflight(0) + jw(0) < 64 && inflight(1) + jw(1) < 64 &&
                              inflight(2) + jw(2) < 64 && inflight(3) + jw(3) < 64 &&
                              LDS <= 160 * 1024;
 };
 
-// A and bf16 B rows in LDS: row r (128 bytes of one 64-K round) at r * 128, its 16-byte
-// segment s at slot s ^ (r % 8), so the MFMA operand reads of eight consecutive rows hit
-// eight different bank groups.  A copy instruction moves 8 rows: lane l fills slot l % 8 of
-// row l / 8 with the segment that belongs there.  FP4 codes: column c's 128 bytes of one
+// A and bf16 B rows in LDS: row r (128 bytes of one 64-K round) at position
+// r ^ ((r / 8) % 2) (rows 8..15 of every 16 swap neighbours), its 16-byte segment s at slot
+// s ^ (r % 8).  The MFMA operand reads of 16 consecutive rows (one segment each) then fall
+// in 16 different 16-byte bank groups of the 256 bytes the two row parities cover.  A copy
+// instruction moves the 8 rows of 8 consecutive positions: lane l fills slot l % 8 of
+// position l / 8 with the segment that belongs there.  FP4 codes: column c's 128 bytes of one
 // super-chunk (256 K: segment s = round s / 2, lane half s % 2) the same way.
-__device__ __forceinline__ uint32_t swz(int row, int seg) { return (uint32_t)(row * 128 + 16 * (seg ^ (row & 7))); }
+__device__ __forceinline__ uint32_t swz(int row, int seg) {
+  return (uint32_t)((row ^ ((row >> 3) & 1)) * 128 + 16 * (seg ^ (row & 7)));
+}
 
 template <int FMT, bool BQ, int TM, int TN, int WN, int KG, int NS>
 __global__ __launch_bounds__(64 * WN * KG) void mixed_gemm_kernel(MixedParams p) {
@@ -194,16 +198,19 @@ __global__ __launch_bounds__(64 * WN * KG) void mixed_gemm_kernel(MixedParams p)
   uint8_t* bring = rring + NS * G::RSLOT;
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.a, p.a_bytes), rb = make_rsrc(p.b, p.b_bytes);
   const __amdgpu_buffer_rsrc_t rs = make_rsrc(p.bs, p.bs_bytes);
-  // the copy lane's row within its 8-row instruction and the global segment it moves
-  const int crow = lane >> 3, cseg = (lane & 7) ^ (lane >> 3);
+  // the copy lane's row within the 8 rows of an instruction x (x % 2 = par) and the global
+  // segment it moves
+  auto crow = [&](int par) { return (lane >> 3) ^ par; };
+  auto cseg = [&](int par) { return (lane & 7) ^ crow(par); };
+  const int apar = wn & 1;  // WN is even: every A instruction of this wave, x = wn + WN y
 
   // Round-0 offsets of this lane's copies, and kOut masks for rows / columns outside the
   // matrix: an offset OR-ed with kOut lies past every buffer, so its copy reads zeros.
   uint32_t aoff[G::APW], amask[G::APW];
 #pragma unroll
   for (int y = 0; y < G::APW; ++y) {
-    const int64_t row = row0 + 8 * (wn + WN * y) + crow;
-    aoff[y] = row < p.M ? (uint32_t)row * p.lda_b + 16u * cseg : 0u;
+    const int64_t row = row0 + 8 * (wn + WN * y) + crow(apar);
+    aoff[y] = row < p.M ? (uint32_t)row * p.lda_b + 16u * cseg(apar) : 0u;
     amask[y] = row < p.M ? 0u : kOut;
   }
   // B copies: bf16 rows per round (BR) or FP4 super-chunks (4 TN), 8 columns each
@@ -211,8 +218,8 @@ __global__ __launch_bounds__(64 * WN * KG) void mixed_gemm_kernel(MixedParams p)
   uint32_t boff[BX], bmask[BX];
 #pragma unroll
   for (int x = 0; x < BX; ++x) {
-    const int64_t col = colw + 8 * x + crow;
-    boff[x] = col < p.N ? (uint32_t)col * p.ldb_b + 16u * cseg : 0u;
+    const int64_t col = colw + 8 * x + crow(x & 1);
+    boff[x] = col < p.N ? (uint32_t)col * p.ldb_b + 16u * cseg(x & 1) : 0u;
     bmask[x] = col < p.N ? 0u : kOut;
   }
   uint32_t soff[TN], smask[TN];
@@ -232,15 +239,19 @@ __global__ __launch_bounds__(64 * WN * KG) void mixed_gemm_kernel(MixedParams p)
   auto super_copies = [&](uint32_t S) {  // FP4 super-chunk S of this group into its slot
     const uint32_t k4 = g + KG * S;
     uint8_t* dst = bring + (S % G::RB) * G::BSLOT + wn * 4 * TN * 1024;
-    const uint32_t kout = 256ull * k4 + 32u * cseg < (uint64_t)p.K ? 0u : kOut;
+    const uint32_t kout0 = 256ull * k4 + 32u * cseg(0) < (uint64_t)p.K ? 0u : kOut;
+    const uint32_t kout1 = 256ull * k4 + 32u * cseg(1) < (uint64_t)p.K ? 0u : kOut;
 #pragma unroll
-    for (int x = 0; x < BX; ++x) copy16(rb, dst + x * 1024, (boff[x] + 128u * k4) | bmask[x] | kout);
+    for (int x = 0; x < BX; ++x) copy16(rb, dst + x * 1024, (boff[x] + 128u * k4) | bmask[x] | (x & 1 ? kout1 : kout0));
   };
   // Issue slot u: round u's A rows, scales or bf16 B rows into round slot u % NS (= rs_),
   // and, at every fourth slot, FP4 super-chunk u / 4.
   auto issue = [&](uint32_t u, int rs_, bool super) {
     const uint32_t c = chunk_of(u);
-    const uint32_t kout = 64ull * c + 8u * cseg < (uint64_t)p.K ? 0u : kOut;  // this lane's 8 K
+    // kOut where the 8 K elements a copy lane moves lie past K
+    const uint32_t kout = 64ull * c + 8u * cseg(apar) < (uint64_t)p.K ? 0u : kOut;
+    const uint32_t kout0 = 64ull * c + 8u * cseg(0) < (uint64_t)p.K ? 0u : kOut;
+    const uint32_t kout1 = 64ull * c + 8u * cseg(1) < (uint64_t)p.K ? 0u : kOut;
     uint8_t* st = rring + rs_ * G::RSLOT;
 #pragma unroll
     for (int y = 0; y < G::APW; ++y) copy16(ra, st + (wn + WN * y) * 1024, (aoff[y] + 128u * c) | amask[y] | kout);
@@ -255,7 +266,7 @@ __global__ __launch_bounds__(64 * WN * KG) void mixed_gemm_kernel(MixedParams p)
       if (super) super_copies(u >> 2);
     } else {
 #pragma unroll
-      for (int x = 0; x < BX; ++x) copy16(rb, sw + x * 1024, (boff[x] + 128u * c) | bmask[x] | kout);
+      for (int x = 0; x < BX; ++x) copy16(rb, sw + x * 1024, (boff[x] + 128u * c) | bmask[x] | (x & 1 ? kout1 : kout0));
     }
   };
 
@@ -282,12 +293,22 @@ __global__ __launch_bounds__(64 * WN * KG) void mixed_gemm_kernel(MixedParams p)
         if constexpr (FMT == 0) sc[j] = (sc[j] >> (8 * ((soff[j] + 2u * c) & 3u))) & 0xFFu;
       }
     }
+    // every LDS read of the round first, so the MFMAs of the four steps issue back to back
+    v4u a[4][TM], bd[4][BQ ? 1 : TN];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+      for (int i = 0; i < TM; ++i) a[kk][i] = *reinterpret_cast<const v4u*>(st + swz(32 * i + l32, 4 * h + kk));
+    if constexpr (!BQ) {
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) bd[kk][j] = *reinterpret_cast<const v4u*>(sw + swz(32 * j + l32, 4 * h + kk));
+    }
+    __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the MFMAs
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      v8bf a[TM], b[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-        a[i] = __builtin_bit_cast(v8bf, *reinterpret_cast<const v4u*>(st + swz(32 * i + l32, 4 * h + kk)));
+      v8bf b[TN];
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         if constexpr (BQ) {
@@ -295,13 +316,14 @@ __global__ __launch_bounds__(64 * WN * KG) void mixed_gemm_kernel(MixedParams p)
           dequant8<FMT>(bc[j][kk], 32 * h + 8 * kk, sc[j], o);
           b[j] = __builtin_bit_cast(v8bf, v4u{o[0], o[1], o[2], o[3]});
         } else {
-          b[j] = __builtin_bit_cast(v8bf, *reinterpret_cast<const v4u*>(sw + swz(32 * j + l32, 4 * h + kk)));
+          b[j] = __builtin_bit_cast(v8bf, bd[kk][j]);
         }
       }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, a[kk][i]), b[j], acc[i][j], 0, 0, 0);
     }
   };
 
@@ -405,7 +427,7 @@ struct MixPlan {
 };
 #define RESQ_MIXED_CONFIGS(X) \
   X(2, 1, 4, 1, 4) X(1, 1, 4, 1, 4) X(8, 1, 4, 1, 2) X(1, 1, 2, 4, 4) X(1, 1, 4, 2, 4) X(2, 1, 2, 4, 2) \
-  X(2, 2, 4, 1, 2) X(1, 2, 4, 1, 2) X(1, 1, 2, 4, 2)
+  X(1, 1, 2, 2, 4) X(2, 2, 4, 1, 2) X(1, 2, 4, 1, 2)
 
 template <int FMT, bool BQ, int TM, int TN, int WN, int KG, int NS>
 void launch_cfg(MixedParams p, hipStream_t s) {
@@ -440,18 +462,21 @@ void launch_plan(const MixPlan& c, const MixedParams& p, hipStream_t s) {
 // Plan choice (measured on MI355X at the m = 256 decode shapes).  Wide grids (many column
 // tiles): 64 x 128 tiles, one per four waves; HiF4 weights take 256-row tiles instead, so
 // each dequantized weight fragment feeds eight MFMAs (its dequantization costs some 40 VALU
-// instructions per 8 elements).  Long K with few columns: 32 x 64 tiles in four K groups.
-// Otherwise 32 x 128 tiles in two K groups (HiF4: 64 x 64 in four).  bf16 weights (W16A4):
-// 64 x 256, 64 x 64 in four K groups, or 32 x 128 in two.
+// instructions per 8 elements).  Long K with few columns: 32 x 64 tiles in K groups.
+// Otherwise 32-row tiles in two K groups, 64 columns wide if that still fits the 256 CUs in
+// one round of workgroups, else 128 (HiF4: 64 x 64 in four K groups).  bf16 weights (W16A4):
+// 64 x 256, 32 x 64 in two K groups, or the same small tiles.
 static_assert(MixGeo<true, 2, 1, 4, 1, 4>::ok && MixGeo<true, 1, 1, 4, 1, 4>::ok && MixGeo<true, 8, 1, 4, 1, 2>::ok &&
                   MixGeo<true, 1, 1, 2, 4, 4>::ok && MixGeo<true, 2, 1, 2, 4, 2>::ok && MixGeo<true, 1, 1, 4, 2, 4>::ok &&
-                  MixGeo<false, 2, 2, 4, 1, 2>::ok && MixGeo<false, 1, 2, 4, 1, 2>::ok &&
-                  MixGeo<false, 2, 1, 2, 4, 2>::ok && MixGeo<false, 1, 1, 2, 4, 2>::ok && MixGeo<false, 1, 1, 4, 2, 4>::ok,
+                  MixGeo<true, 1, 1, 2, 2, 4>::ok && MixGeo<false, 2, 2, 4, 1, 2>::ok && MixGeo<false, 1, 2, 4, 1, 2>::ok &&
+                  MixGeo<false, 1, 1, 2, 2, 4>::ok && MixGeo<false, 1, 1, 4, 2, 4>::ok,
               "every plan choose() returns fits");
 template <int FMT, bool BQ>
 MixPlan choose(int64_t M, int64_t N, int64_t K) {
   const bool small = M <= 32;
   const int64_t mt64 = (M + 63) / 64, nchunks = (K + 63) / 64;
+  const bool one_round = ((M + 31) / 32) * ((N + 63) / 64) <= 256;  // 32 x 64 tiles fit the CUs
+  const MixPlan narrow = one_round ? MixPlan{1, 1, 2, 2, 4} : MixPlan{1, 1, 4, 2, 4};
   MixPlan c{};
   if constexpr (BQ) {
     if (mt64 * ((N + 127) / 128) >= 512)
@@ -459,14 +484,14 @@ MixPlan choose(int64_t M, int64_t N, int64_t K) {
     else if (nchunks >= 64)
       c = MixPlan{1, 1, 2, 4, 4};
     else
-      c = FMT == 1 && !small ? MixPlan{2, 1, 2, 4, 2} : MixPlan{1, 1, 4, 2, 4};
+      c = FMT == 1 && !small ? MixPlan{2, 1, 2, 4, 2} : narrow;
   } else {
     if (mt64 * ((N + 255) / 256) >= 256)
       c = MixPlan{small ? 1 : 2, 2, 4, 1, 2};
     else if (nchunks >= 64)
-      c = MixPlan{small ? 1 : 2, 1, 2, 4, 2};
+      c = MixPlan{1, 1, 2, 2, 4};
     else
-      c = MixPlan{1, 1, 4, 2, 4};
+      c = narrow;
   }
   return c;
 }

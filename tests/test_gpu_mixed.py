@@ -31,7 +31,7 @@ def _inputs(m, d, n, seed):
 @pytest.mark.parametrize("fmt", FMTS)
 @pytest.mark.parametrize("m,d,n", [(37, 512, 100), (130, 2048, 700), (256, 1088, 64), (5, 64, 3),
                                    (300, 4096, 520), (5, 64, 65600), (20, 4160, 300), (200, 4096, 96),
-                                   (256, 256, 33000), (130, 64, 22000)])
+                                   (256, 256, 33000), (130, 64, 22000), (20, 128, 20000)])
 def test_mixed_forms_match_the_oracle(fmt, m, d, n):
     import paper_2607_26515_amd as P
     if d % F.block_size(fmt):
