@@ -12,7 +12,8 @@
 // rollout batch sizes, so writing them at 2 bytes per element costs nothing next to the bf16
 // weights, and the GEMM then dequantizes nothing per output tile).  The column operand B is
 // the weight: K-major FP4 codes + block scales (W4A16), dequantized in registers right before
-// the MFMAs, so HBM carries 4.25 (MXFP4) or 4.5 (HiF4) bits per weight; or bf16 rows (W16A4).
+// the MFMAs (MXFP4 by the scaled FP4 conversion, HiF4 by a per-block byte table), so HBM
+// carries 4.25 (MXFP4) or 4.5 (HiF4) bits per weight; or bf16 rows (W16A4).
 //
 // Work split.  A workgroup owns a 32 TM x (32 TN WN) output tile: WN waves side by side along
 // the columns, each owning 32 TM x 32 TN of it, all of them reading the same A rows.  KG such
@@ -108,38 +109,77 @@ __device__ __forceinline__ float e8m0_f32(uint32_t code) {
   return code ? __uint_as_float(code << 23) : __uint_as_float(0x00400000u);
 }
 
-// Eight FP4 elements (one 32-bit word of codes, element 8w+i in nibble i) dequantized to bf16
-// bits, exact, two per output word.  MXFP4: E2M1 magnitude times 2^E; HiF4: k (4+m)
-// 2^(e-35-b) with b the level-2 + level-3 shift of each element's groups (elem0 = the first
-// element's index inside its 64-block; pairs share their level-3 group).
-template <int FMT>
-__device__ __forceinline__ void dequant8(uint32_t w, int elem0, uint32_t scale, uint32_t out[4]) {
-  if constexpr (FMT == 0) {
-    const float sc = e8m0_f32(scale);
-    out[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 0));
-    out[1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 1));
-    out[2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 2));
-    out[3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 3));
-  } else {
-    const uint32_t f = 4u + (scale & 3u);
-    const int e = (int)((scale >> 2) & 63u) - 35;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int el = elem0 + 2 * i;  // both elements of the pair share level-2/3 groups
-      const int sh = e - (int)((scale >> (8 + el / 8)) & 1u) - (int)((scale >> (16 + el / 4)) & 1u);
-      const uint32_t c0 = (w >> (8 * i)) & 15u, c1 = (w >> (8 * i + 4)) & 15u;
-      const uint32_t u0 = __float_as_uint(ldexpf((float)((c0 & 7u) * f), sh)) | ((c0 & 8u) << 28);
-      const uint32_t u1 = __float_as_uint(ldexpf((float)((c1 & 7u) * f), sh)) | ((c1 & 8u) << 28);
-      out[i] = (u0 >> 16) | (u1 & 0xFFFF0000u);  // exact: at most 6 significant bits
-    }
-  }
+// Eight MXFP4 elements (one 32-bit word of codes, element i in nibble i) dequantized to bf16
+// bits, exact, two per output word: E2M1 magnitude times 2^E through gfx950's scaled
+// conversion (v_cvt_scalef32_pk_bf16_fp4).
+__device__ __forceinline__ void mx_dequant8(uint32_t w, uint32_t scale, uint32_t out[4]) {
+  const float sc = e8m0_f32(scale);
+  out[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 0));
+  out[1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 1));
+  out[2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 2));
+  out[3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, sc, 3));
 }
 
-// Geometry of one configuration.  Per K group: a ring of NS round slots (A rows, the FP4
-// scale dwords or the bf16 B rows of one 64-K round) and, for FP4 B, a ring of RB super-chunk
-// slots (the codes of four rounds, 128 bytes per column).  Copy instructions per wave and
-// round: APW for A, TN scale dwords (FP4) or 4 TN (bf16 B); plus, in every fourth round, the
-// 4 TN copies of one FP4 super-chunk.
+// HiF4 decoding by table (the lane's 32 elements of a round lie in one 64-block).  Per round:
+// the bf16 patterns L[k] of k (4+m) 2^(e-35) for k = 0..7 (exact, L[0] = 0), split into
+// their low and high bytes, four entries per dword, and the lane's level-2 (4) and level-3
+// (8) shift bits.  Per 8 elements: the magnitudes k spread to bytes select the bytes of
+// their entries (v_perm), the signs go into the high bytes of nonzero elements, the bytes
+// pair up into bf16 values, and a saturating 16-bit subtraction of b << 7 lowers the
+// exponent by the element's shift b (nonzero values keep biased exponents far above 2, and
+// zero stays zero).
+struct Hif4Table {
+  uint32_t lo03, lo47, hi03, hi47;  // low / high bytes of L[0..3], L[4..7]
+  uint32_t l2, l3;                  // level-2 bits of the lane's 4 groups of 8, level-3 of its 8 of 4
+};
+
+__device__ __forceinline__ Hif4Table hif4_table(uint32_t scale, int h) {
+  const uint32_t f = 4u + (scale & 3u);
+  const int e = (int)((scale >> 2) & 63u) - 35;
+  uint32_t L[8];
+  L[0] = 0u;
+#pragma unroll
+  for (int k = 1; k < 8; ++k) L[k] = __float_as_uint(ldexpf((float)(k * f), e)) >> 16;  // exact
+  const uint32_t p01 = L[0] | (L[1] << 16), p23 = L[2] | (L[3] << 16);
+  const uint32_t p45 = L[4] | (L[5] << 16), p67 = L[6] | (L[7] << 16);
+  Hif4Table t;
+  t.lo03 = __builtin_amdgcn_perm(p23, p01, 0x06040200u);
+  t.hi03 = __builtin_amdgcn_perm(p23, p01, 0x07050301u);
+  t.lo47 = __builtin_amdgcn_perm(p67, p45, 0x06040200u);
+  t.hi47 = __builtin_amdgcn_perm(p67, p45, 0x07050301u);
+  t.l2 = (scale >> (8 + 4 * h)) & 0xFu;
+  t.l3 = (scale >> (16 + 8 * h)) & 0xFFu;
+  return t;
+}
+
+typedef unsigned short v2u16 __attribute__((ext_vector_type(2)));
+
+// Four elements: their nibbles in the low nibbles of the four bytes of sp; out0/out1 receive
+// elements 0,1 / 2,3 as bf16 pairs, shifted down by b.
+__device__ __forceinline__ void hif4_decode4(uint32_t sp, uint32_t b, const Hif4Table& t, uint32_t& out0,
+                                             uint32_t& out1) {
+  const uint32_t k = sp & 0x07070707u;
+  const uint32_t lo = __builtin_amdgcn_perm(t.lo47, t.lo03, k);
+  uint32_t hi = __builtin_amdgcn_perm(t.hi47, t.hi03, k);
+  hi |= (sp << 4) & (k + 0x7F7F7F7Fu) & 0x80808080u;  // the sign bit of each nonzero element
+  const v2u16 sub = __builtin_bit_cast(v2u16, b * 0x00800080u);
+  out0 = __builtin_bit_cast(uint32_t, __builtin_elementwise_sub_sat(
+                                          __builtin_bit_cast(v2u16, __builtin_amdgcn_perm(hi, lo, 0x05010400u)), sub));
+  out1 = __builtin_bit_cast(uint32_t, __builtin_elementwise_sub_sat(
+                                          __builtin_bit_cast(v2u16, __builtin_amdgcn_perm(hi, lo, 0x07030602u)), sub));
+}
+
+// Eight elements of step kk (elements 8 kk .. 8 kk + 7 of the lane's 32): one level-2 group,
+// two level-3 groups.
+template <int KK>
+__device__ __forceinline__ void hif4_decode8(uint32_t w, const Hif4Table& t, uint32_t out[4]) {
+  const uint32_t b2 = (t.l2 >> KK) & 1u;
+  const uint32_t ba = b2 + ((t.l3 >> (2 * KK)) & 1u), bb = b2 + ((t.l3 >> (2 * KK + 1)) & 1u);
+  const uint32_t ta = __builtin_amdgcn_perm(w, w, 0x0C010C00u), tb = __builtin_amdgcn_perm(w, w, 0x0C030C02u);
+  hif4_decode4(ta | (ta << 4), ba, t, out[0], out[1]);
+  hif4_decode4(tb | (tb << 4), bb, t, out[2], out[3]);
+}
+
 template <bool BQ, int TM, int TN, int WN, int KG, int NS>
 struct MixGeo {
   static constexpr int AI = 4 * TM;                    // A copies (1 KB, 8 rows) per round
@@ -283,6 +323,7 @@ __global__ __launch_bounds__(64 * WN * KG) void mixed_gemm_kernel(MixedParams p)
     const uint8_t* sw = st + G::AI * 1024 + wn * (G::BR * 1024 + G::SC);
     v4u bc[TN];
     uint32_t sc[TN];
+    [[maybe_unused]] Hif4Table tab[TN];
     if constexpr (BQ) {
       const uint8_t* bs = bring + ((t >> 2) % G::RB) * G::BSLOT + wn * 4 * TN * 1024;
       const uint32_t c = chunk_of(t);
@@ -291,6 +332,7 @@ __global__ __launch_bounds__(64 * WN * KG) void mixed_gemm_kernel(MixedParams p)
         bc[j] = *reinterpret_cast<const v4u*>(bs + swz(32 * j + l32, 2 * (int)(t & 3u) + h));
         sc[j] = *reinterpret_cast<const uint32_t*>(sw + j * 256 + 4 * lane);
         if constexpr (FMT == 0) sc[j] = (sc[j] >> (8 * ((soff[j] + 2u * c) & 3u))) & 0xFFu;
+        else tab[j] = hif4_table(sc[j], h);
       }
     }
     // every LDS read of the round first, so the MFMAs of the four steps issue back to back
@@ -306,14 +348,15 @@ __global__ __launch_bounds__(64 * WN * KG) void mixed_gemm_kernel(MixedParams p)
         for (int j = 0; j < TN; ++j) bd[kk][j] = *reinterpret_cast<const v4u*>(sw + swz(32 * j + l32, 4 * h + kk));
     }
     __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the MFMAs
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
+    auto step = [&](auto kc) {
+      constexpr int kk = decltype(kc)::value;
       v8bf b[TN];
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         if constexpr (BQ) {
           uint32_t o[4];
-          dequant8<FMT>(bc[j][kk], 32 * h + 8 * kk, sc[j], o);
+          if constexpr (FMT == 0) mx_dequant8(bc[j][kk], sc[j], o);
+          else hif4_decode8<kk>(bc[j][kk], tab[j], o);
           b[j] = __builtin_bit_cast(v8bf, v4u{o[0], o[1], o[2], o[3]});
         } else {
           b[j] = __builtin_bit_cast(v8bf, bd[kk][j]);
@@ -324,7 +367,11 @@ __global__ __launch_bounds__(64 * WN * KG) void mixed_gemm_kernel(MixedParams p)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, a[kk][i]), b[j], acc[i][j], 0, 0, 0);
-    }
+    };
+    step(std::integral_constant<int, 0>{});
+    step(std::integral_constant<int, 1>{});
+    step(std::integral_constant<int, 2>{});
+    step(std::integral_constant<int, 3>{});
   };
 
   // Round t: wait until this wave's copies of issue slots <= t have landed (those of the

@@ -85,6 +85,31 @@ def test_identity_weights_bit_exact(fmt):
     assert np.array_equal(y16.view(np.uint32), want16.view(np.uint32)), "W16A4 with W = I is not Q(X)"
 
 
+@pytest.mark.parametrize("fmt", FMTS)
+def test_identity_activations_read_out_every_weight(fmt):
+    """W4A16 with X = I returns Q(W)^T itself, so every dequantized weight the GEMM feeds to
+    the MFMA is compared bit for bit with the oracle's dequantization of the same codes and
+    scales.  Blocks span 2^-33 .. 2^27 in magnitude with elements 1 .. 2^-10 of the block
+    maximum, so every scale mantissa, most scale exponents and every level-2 / level-3 shift
+    occur."""
+    import torch
+    import paper_2607_26515_amd as P
+    log(f"mixed identity activations {fmt}")
+    d, n = 128, 8192
+    rng = np.random.default_rng(11)
+    b = F.block_size(fmt)
+    block_exp = rng.integers(-33, 28, size=(n, d // b, 1)).astype(np.float64)
+    mags = np.exp2(block_exp + rng.uniform(-10.0, 0.0, size=(n, d // b, b)))
+    w = (mags * rng.choice([-1.0, 1.0], size=mags.shape)).reshape(n, d)
+    w[rng.random(w.shape) < 0.05] = 0.0
+    wb = f32_to_bf16_bits(w.astype(np.float32))
+    qc, qs = P.quantize(dev_bf16(wb), fmt, axis=1)
+    eye = f32_to_bf16_bits(np.eye(d, dtype=np.float32))
+    y = host(P.linear_w4a16(dev_bf16(eye), qc, qs, fmt))
+    want = F.dequantize(fmt, F.unpack_nibbles(host(qc)), host(qs)).T.astype(np.float32) + np.float32(0.0)
+    assert np.array_equal((y + np.float32(0.0)).view(np.uint32), want.view(np.uint32)), "X = I does not give Q(W)^T"
+
+
 def _samples(rng, size, k):
     idx = set(rng.choice(size, size=min(k, size), replace=False).tolist()) | {0, size - 1}
     return np.array(sorted(idx))
