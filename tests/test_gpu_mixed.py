@@ -8,7 +8,9 @@ Q(X) W^T) against the oracle.
 - Identity weights, bit for bit: W4A16 with W = c I (Q(c I) = c I) must return c X (the
   activations enter unquantized); W16A4 with W = I must return Q(X), here for every finite
   bf16 value alone in its block.
-- The decode workload's linears at full size (m = 256, Qwen2.5-3B), on sampled outputs."""
+- The decode workload's linears at full size (m = 256, Qwen2.5-3B), on sampled outputs.
+- Operands whose rows lie about 2 GiB apart, which the library splits over several launches
+  (the kernel addresses operands with 32-bit offsets)."""
 import numpy as np
 import pytest
 
@@ -54,6 +56,32 @@ def test_mxfp4_half_chunk_tail():
     qc, qs = P.quantize(dev_bf16(wb), "mxfp4", axis=1)
     assert_close(host(P.linear_w4a16(dev_bf16(xb), qc, qs, "mxfp4")), Q.w4a16_forward("mxfp4", x, w)["y64"])
     assert_close(host(P.linear_w16a4(dev_bf16(xb), dev_bf16(wb), "mxfp4")), Q.w16a4_forward("mxfp4", x, w)["y64"])
+
+
+def test_operands_beyond_32_bit_offsets():
+    """Row strides of about 2 GiB: an operand of three rows then spans more than the kernel's
+    32-bit buffer offsets, so the call is split into launches over pieces of the rows of X
+    (W4A16) or of W (W16A4)."""
+    import torch
+    import paper_2607_26515_amd as P
+    ld = (1 << 30) - 128  # 2 GiB - 256 bytes per bf16 row: two rows per launch
+    m, d, n = 3, 64, 3
+    xb, wb = _inputs(m, d, n, 7)
+    x, w = bf16_bits_to_f32(xb), bf16_bits_to_f32(wb)
+    for fmt in FMTS:
+        log(f"mixed 32-bit offset pieces {fmt}")
+        big = torch.zeros((m, ld), dtype=torch.int16, device="cuda")
+        big[:, :d] = dev_bf16(xb)
+        qc, qs = P.quantize(dev_bf16(wb), fmt, axis=1)
+        y4 = host(P.linear_w4a16(big[:, :d], qc, qs, fmt))
+        del big
+        assert_close(y4, Q.w4a16_forward(fmt, x, w)["y64"], f"W4A16 {fmt}, X rows 2 GiB apart")
+        big = torch.zeros((n, ld), dtype=torch.int16, device="cuda")
+        big[:, :d] = dev_bf16(wb)
+        y16 = host(P.linear_w16a4(dev_bf16(xb), big[:, :d], fmt))
+        del big
+        torch.cuda.empty_cache()
+        assert_close(y16, Q.w16a4_forward(fmt, x, w)["y64"], f"W16A4 {fmt}, W rows 2 GiB apart")
 
 
 def _finite_bf16():
