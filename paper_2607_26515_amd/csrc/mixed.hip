@@ -17,8 +17,9 @@
 //
 // Work split.  A workgroup owns a 32 TM x (32 TN WN) output tile: WN waves side by side along
 // the columns, each owning 32 TM x 32 TN of it, all of them reading the same A rows.  KG such
-// groups share the tile and split its K chunks (chunk c goes to group c mod KG); at the end
-// they add their accumulators through LDS in group order (deterministic).  Workgroups are
+// groups share the tile and split its K range in super-chunks of four rounds (super-chunk s
+// goes to group s mod KG); at the end they add their accumulators through LDS in group order
+// (deterministic).  Workgroups are
 // dealt to the eight XCDs in contiguous ranges, row tiles fastest, so the workgroups that read
 // one weight strip run on one XCD at about the same time and share its L2.
 //
@@ -28,15 +29,16 @@
 // of A or bf16 B per round; for FP4 B, 8 columns x 128 bytes of codes, which span four
 // rounds, so FP4 codes move in super-chunks of 256 K), since copies that touch many lines
 // for few bytes each run far slower than the bytes alone would suggest.  In LDS each 128-byte
-// row keeps its 16-byte segments XOR-swizzled by the row index, so the MFMA operand reads
-// (16 bytes per lane, 32 rows) are free of bank conflicts.  A rows are copied once per group
+// row keeps its 16-byte segments XOR-swizzled by the row index and rows 8..15 of every 16
+// swap neighbours, so the MFMA operand reads (16 bytes per lane, 32 rows) are free of bank
+// conflicts.  A rows are copied once per group
 // (each wave 4 TM / WN of the instructions) and read by all WN waves; B is private to its
 // wave.  NS rounds are in flight; one barrier per round.  FP4 scales travel as one dword per
 // lane, tile and round (MXFP4: the aligned dword holding the lane's scale byte).
 //
-// K order inside a chunk.  The sum over K may take any order, as long as A and B pair the
+// K order inside a round.  The sum over K may take any order, as long as A and B pair the
 // same K.  Lane l (row or column l % 32, half h = l / 32) holds the 32 consecutive K elements
-// 32 h .. 32 h + 31 of the chunk, and the MFMA of step kk (0..3) takes elements 8 kk .. 8 kk + 7
+// 32 h .. 32 h + 31 of the round, and the MFMA of step kk (0..3) takes elements 8 kk .. 8 kk + 7
 // of them: one 16-byte read per step for bf16, one 32-bit word of codes for FP4, whose
 // 32-element span is exactly one MXFP4 block and one half of a HiF4 block.
 //
