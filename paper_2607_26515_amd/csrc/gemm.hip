@@ -561,6 +561,8 @@ void launch_cfg(GemmParams p, int n_terms, hipStream_t s) {
 //  - grids too small for 128-row tiles to fill the chip: 64 x 64 tiles in K groups (two or
 //    four groups of four waves, see plan()), and for HiF4 with long K (at least 64 steps per
 //    split) K split in two when that fills the CUs;
+//  - small grids with long K that 64 x 128 tiles already fill: the wide tiles below with the
+//    K split in up to eight;
 //  - MXFP4 with M >= 512 (7B decode and prefill): 128 x 256 tiles (fewest A re-reads per
 //    byte of B), two workgroups per CU;
 //  - otherwise: 128 x 192 tiles.  HiF4 always takes these: with one register set they fit
@@ -601,9 +603,27 @@ Plan plan(int fmt, int64_t M, int64_t N, int64_t K, bool may_split) {
     pl.ns = fmt == 0 ? 4 : 2;
     return pl;
   }
+  if (wgs(4, 4) < 240 && may_split && nkb >= 128) {
+    // small grids with long K whose 64 x 128 tiles already fill the CUs (the 7B down
+    // projection at m = 512): the wide tiles with K split, which read each activation fragment
+    // for 2-4x the columns of the 64 x 64 tiles in K groups and each weight fragment for twice
+    // the rows (measured at m = 512, 18944 -> 3584: MXFP4 54 -> 45 us as 128 x 256 in four
+    // splits; HiF4 146 -> 97 us as 128 x 192 in six splits, two workgroups per CU)
+    const bool mx = fmt == 0;
+    pl.cfg = mx ? kWide : kMid;
+    pl.tiles = mx ? wgs(4, 8) : wgs(4, 6);
+    int64_t ks = (mx ? kCUs : 2 * kCUs) / pl.tiles;
+    ks = ks < 2 ? 2 : ks > 8 ? 8 : ks;
+    pl.ksplit = (int)ks;
+    pl.kper = (nkb + ks - 1) / ks;
+    pl.partial_bytes = (size_t)pl.tiles * pl.ksplit * (kTileRows[pl.cfg] * kTileCols[pl.cfg]) * sizeof(float);
+    pl.kg = 1;
+    pl.ns = mx ? 4 : 2;
+    return pl;
+  }
   if (wgs(4, 4) < 240) {
-    // small grids (no K split: the long-K ones that would gain from one take the 64 x 128
-    // tiles above, and the backward never splits)
+    // small grids (no K split: the long-K ones that would gain from one take the tiles
+    // above, and the backward never splits)
     pl.cfg = kSmall;
     pl.tiles = wgs(2, 2);
     // K groups and stages (measured).  Grids within the CUs: MXFP4 takes four K groups for

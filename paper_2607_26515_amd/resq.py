@@ -103,6 +103,13 @@ def load() -> ctypes.CDLL:
         return _lib
     if not os.path.exists(_LIB_PATH):
         raise ResqError(f"{_LIB_PATH} is missing: build it with `python -m paper_2607_26515_amd.build`")
+    # PyTorch ships its own HIP runtime.  Loaded first, it is the one the library binds to
+    # (same soname); loaded after the library, it comes in as a second copy beside the
+    # system one, and the library's launches then find no device.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(_LIB_PATH)
     vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
     lib.resq_quantize.argtypes = [i32, vp, i32, i64, i64, i64, i32, vp, vp, vp]

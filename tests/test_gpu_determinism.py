@@ -16,10 +16,13 @@ from _gpu_util import dev_bf16, log
 # (workload, linear, sparsity) forward cases; sizes are the benchmark workloads' own, plus
 # the 7B down projection at m = 256
 _EXTRA = Workload("qwen7b_down_m256", 256, (Linear("down", 18944, 3584),), 0.005, 100.0)
-# backward cases: the training workload, and a narrow one whose dW GEMM (256 x 256 over
-# K = 8192, not split) takes the small tiles with four K groups and four stages (MXFP4)
+# backward cases: the training workload, a narrow one whose dW GEMM (256 x 256 over
+# K = 8192, not split) takes the small tiles with four K groups and four stages (MXFP4), and
+# a square one whose dW GEMM (1536 x 1536 over K = 8192, not split) fills more than the CUs
+# with them (MXFP4: four K groups, two stages; HiF4: two and two)
 _NARROW_BWD = Workload("narrow_bwd_m8192", 8192, (Linear("proj", 256, 256),), 0.01, 50.0, backward=True)
-BWD_CASES = ["qwen3b_gateup_bwd_m8192", "narrow_bwd_m8192"]
+_SQUARE_BWD = Workload("square_bwd_m8192", 8192, (Linear("proj", 1536, 1536),), 0.01, 50.0, backward=True)
+BWD_CASES = ["qwen3b_gateup_bwd_m8192", "narrow_bwd_m8192", "square_bwd_m8192"]
 FWD_CASES = [
     ("qwen3b_layer_m256", "qkv", "2:4"),
     ("qwen3b_layer_m256", "qkv", "none"),
@@ -37,7 +40,7 @@ FMTS = ["mxfp4", "hif4"]
 
 
 def _workload(name):
-    return {_EXTRA.name: _EXTRA, _NARROW_BWD.name: _NARROW_BWD}.get(name) or WORKLOADS[name]
+    return {_EXTRA.name: _EXTRA, _NARROW_BWD.name: _NARROW_BWD, _SQUARE_BWD.name: _SQUARE_BWD}.get(name) or WORKLOADS[name]
 
 
 def _plan_key(P, fmt, M, N, K, split):
@@ -48,10 +51,10 @@ def _plan_key(P, fmt, M, N, K, split):
 # every (format, tile, K groups, stages, K split) that launch_gemm can run
 INSTANTIATED = {
     ("mxfp4", "64x64", 2, 4, False), ("mxfp4", "64x64", 4, 4, False), ("mxfp4", "64x64", 4, 2, False),
-    ("mxfp4", "64x64", 1, 4, False), ("mxfp4", "128x256", 1, 4, False),
+    ("mxfp4", "64x64", 1, 4, False), ("mxfp4", "128x256", 1, 4, False), ("mxfp4", "128x256", 1, 4, True),
     ("mxfp4", "64x128", 1, 4, True), ("mxfp4", "64x128", 1, 4, False),
     ("hif4", "64x64", 2, 4, False), ("hif4", "64x64", 2, 2, False), ("hif4", "64x64", 1, 2, False),
-    ("hif4", "128x192_8w", 1, 2, False), ("hif4", "128x192", 1, 2, False),
+    ("hif4", "128x192_8w", 1, 2, False), ("hif4", "128x192", 1, 2, False), ("hif4", "128x192", 1, 2, True),
     ("hif4", "64x128", 2, 2, True),
 }
 

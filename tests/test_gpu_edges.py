@@ -101,3 +101,26 @@ def test_profiler_counts_launch_families(fmt, m, d, n):
     P.resq_profile_enable(False)
     assert g[0] == 3 and r[0] == 3
     assert 0.0 < g[1] < 3 * 10.0 and 0.0 < r[1] < 3 * 10.0  # milliseconds
+
+
+def test_library_loaded_before_torch_still_launches():
+    """A process that queries the library on the host before it imports PyTorch (here the
+    plan query) must still launch kernels afterwards: the binding loads PyTorch's HIP runtime
+    before the library, so the process holds one HIP runtime, not two.  Run in a fresh
+    process, since this one has long loaded both."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = (
+        "import paper_2607_26515_amd as P\n"
+        "P.gemm_plan('mxfp4', 256, 2560, 2048)\n"
+        "import torch\n"
+        "w = torch.zeros((64, 64), dtype=torch.int16, device='cuda')\n"
+        "c, s = P.quantize(w, 'mxfp4', axis=1)\n"
+        "torch.cuda.synchronize()\n"
+        "print('ok', int(c.sum()))\n"
+    )
+    log("library before torch, fresh process")
+    r = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0 and "ok 0" in r.stdout, r.stdout + r.stderr
