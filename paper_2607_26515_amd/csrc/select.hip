@@ -602,17 +602,31 @@ __global__ void uzero_kernel(uint32_t* hist, int words) {
   for (int i = threadIdx.x; i < words; i += blockDim.x) hist[i] = 0;
 }
 
+// A thread's 32 elements (4 words of codes from word w0, one scale block): the raw codes and
+// scale, loaded before the threshold is known so that their latency overlaps its reads, then
+// the keys.
+struct ThreadWords {
+  uint4 cw;
+  uint32_t sc;
+  int jpos;
+};
+
 template <int FMT>
-__device__ __forceinline__ void thread_keys(const uint8_t* codes, const void* scales, int64_t d,
-                                            int64_t w0, uint32_t key[32]) {
-  const uint4 cw = *reinterpret_cast<const uint4*>(codes + 4 * w0);
-  const uint32_t e0 = (uint32_t)(8 * w0), row = e0 / (uint32_t)d, j = e0 - row * (uint32_t)d;  // 32 elements, one scale block
-  const uint32_t sc = scale_at<FMT>(scales, row, d, j);
-  const int jpos = FMT == 0 ? 0 : (int)(j & 63);
-  word_keys<FMT>(cw.x, sc, jpos, key);
-  word_keys<FMT>(cw.y, sc, jpos + 8, key + 8);
-  word_keys<FMT>(cw.z, sc, jpos + 16, key + 16);
-  word_keys<FMT>(cw.w, sc, jpos + 24, key + 24);
+__device__ __forceinline__ ThreadWords thread_words(const uint8_t* codes, const void* scales, int64_t d, int64_t w0) {
+  ThreadWords t;
+  t.cw = *reinterpret_cast<const uint4*>(codes + 4 * w0);
+  const uint32_t e0 = (uint32_t)(8 * w0), row = e0 / (uint32_t)d, j = e0 - row * (uint32_t)d;
+  t.sc = scale_at<FMT>(scales, row, d, j);
+  t.jpos = FMT == 0 ? 0 : (int)(j & 63);
+  return t;
+}
+
+template <int FMT>
+__device__ __forceinline__ void thread_keys(const ThreadWords& t, uint32_t key[32]) {
+  word_keys<FMT>(t.cw.x, t.sc, t.jpos, key);
+  word_keys<FMT>(t.cw.y, t.sc, t.jpos + 8, key + 8);
+  word_keys<FMT>(t.cw.z, t.sc, t.jpos + 16, key + 16);
+  word_keys<FMT>(t.cw.w, t.sc, t.jpos + 24, key + 24);
 }
 
 // Load the histograms into LDS and resolve the threshold (all threads call this): out[0] =
@@ -654,6 +668,10 @@ __global__ __launch_bounds__(kThreads) void uhist_kernel(const uint8_t* __restri
   __shared__ uint32_t ch[4];
   __shared__ uint32_t wsum[kThreads / 64];
   const int tid = threadIdx.x;
+  const int64_t w0 = ((int64_t)blockIdx.x * kThreads + tid) * kWordsPerThread;
+  const bool in = w0 < m * (d / 8);
+  ThreadWords tw{};
+  if (in) tw = thread_words<FMT>(codes, scales, d, w0);
   uint32_t want = 0;
   if constexpr (PASS == 1) {
     load_choice(hist, lh, keep, false, wsum, ch);
@@ -662,10 +680,8 @@ __global__ __launch_bounds__(kThreads) void uhist_kernel(const uint8_t* __restri
   }
   for (int i = tid; i < kUHist; i += kThreads) lh[i] = 0;
   __syncthreads();
-  const int64_t w0 = ((int64_t)blockIdx.x * kThreads + tid) * kWordsPerThread;
-  const bool in = w0 < m * (d / 8);
   uint32_t key[32];
-  if (in) thread_keys<FMT>(codes, scales, d, w0, key);
+  if (in) thread_keys<FMT>(tw, key);
   else
 #pragma unroll
     for (int e = 0; e < 32; ++e) key[e] = 0;
@@ -703,6 +719,10 @@ __global__ __launch_bounds__(kThreads) void uapply_kernel(uint8_t* __restrict__ 
   __shared__ uint32_t lh[kUHist];
   __shared__ uint32_t ch[4];
   __shared__ uint32_t wsum[kThreads / 64];
+  const int64_t w0 = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * kWordsPerThread;
+  const bool in = w0 < m * (d / 8);
+  ThreadWords tw{};
+  if (in) tw = thread_words<FMT>(codes, scales, d, w0);
   load_choice(hist, lh, keep, true, wsum, ch);
   const uint32_t T = ch[2], krem = ch[3];
   // ties of earlier workgroups: whole groups of kSuper workgroups, then this group's earlier
@@ -714,12 +734,10 @@ __global__ __launch_bounds__(kThreads) void uapply_kernel(uint8_t* __restrict__ 
     before += tie_counts[(size_t)w * kMantBins + tm];
   uint32_t tot_before;
   block_exclusive_scan<kThreads>(before, wsum, tot_before);
-  const int64_t w0 = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * kWordsPerThread;
-  const bool in = w0 < m * (d / 8);
   uint32_t key[32];
   uint32_t ties = 0;
   if (in) {
-    thread_keys<FMT>(codes, scales, d, w0, key);
+    thread_keys<FMT>(tw, key);
 #pragma unroll
     for (int e = 0; e < 32; ++e) ties += key[e] == T;
   }
@@ -734,7 +752,7 @@ __global__ __launch_bounds__(kThreads) void uapply_kernel(uint8_t* __restrict__ 
     kept |= (uint32_t)keep << e;
   }
   uint4* cw = reinterpret_cast<uint4*>(codes + 4 * w0);
-  uint4 v = *cw;
+  uint4 v = tw.cw;
   v.x &= nibble_mask8(kept & 0xFFu);
   v.y &= nibble_mask8((kept >> 8) & 0xFFu);
   v.z &= nibble_mask8((kept >> 16) & 0xFFu);
@@ -747,7 +765,7 @@ __global__ __launch_bounds__(kThreads) void uapply_kernel(uint8_t* __restrict__ 
     const uint32_t e0 = (uint32_t)(8 * w0), row = e0 / (uint32_t)d, j = e0 - row * (uint32_t)d;
     const int64_t nkb = (d + 63) / 64, kb = j / 64;
     const int half = (int)((j / 32) & 1u);
-    const uint32_t sc = scale_at<FMT>(scales, row, d, j);
+    const uint32_t sc = tw.sc;  // the scale of this thread's block, loaded above
     const int64_t rec = ((int64_t)(row / 32) * nkb + kb) * 64 + (row & 31) + 32 * half;
     store_frag_record<PMODE>(frag, fscale, rec, v, sc, half);
     const uint4 z = make_uint4(0, 0, 0, 0);
