@@ -594,8 +594,11 @@ constexpr int kHistCopies = kElemHistCopies;  // hist.h: copies that readers sum
 // lower bits, so that table holds every workgroup's tie count for whichever threshold the
 // pass's global histogram then fixes.  The counts are also summed per group of kSuper
 // workgroups, so that a workgroup finds the ties of all earlier workgroups in
-// O(nwg / kSuper + kSuper) reads.
+// O(nwg / kSuper + kSuper) reads.  A group's sums are kSuperCopies copies (workgroup w adds
+// into copy w % kSuperCopies), so that the atomics of a group's workgroups do not all hit one
+// address; with a single group no workgroup reads them, and none are formed.
 constexpr int kSuper = 256;
+constexpr int kSuperCopies = 8;
 constexpr int kMantBins = 64;
 
 __global__ void uzero_kernel(uint32_t* hist, int words) {
@@ -697,7 +700,8 @@ __global__ __launch_bounds__(kThreads) void uhist_kernel(const uint8_t* __restri
     if (c) atomicAdd(&hist[(blockIdx.x % kHistCopies) * kUHist + OFF + b], c);
     if constexpr (PASS == 1) {
       tie_counts[(size_t)blockIdx.x * kMantBins + b] = c;
-      if (c) atomicAdd(&super_counts[(blockIdx.x / kSuper) * kMantBins + b], c);  // integer sums: any order
+      if (c && gridDim.x > kSuper)  // integer sums: any order
+        atomicAdd(&super_counts[((blockIdx.x / kSuper) * kSuperCopies + blockIdx.x % kSuperCopies) * kMantBins + b], c);
     }
   }
 }
@@ -729,7 +733,7 @@ __global__ __launch_bounds__(kThreads) void uapply_kernel(uint8_t* __restrict__ 
   // ones, from the second pass's counts of T's mantissa pattern
   const uint32_t tm = (T >> 17) & 63u, sb = blockIdx.x / kSuper;
   uint32_t before = 0;
-  for (uint32_t w = threadIdx.x; w < sb; w += kThreads) before += super_counts[w * kMantBins + tm];
+  for (uint32_t w = threadIdx.x; w < sb * kSuperCopies; w += kThreads) before += super_counts[w * kMantBins + tm];
   for (uint32_t w = sb * kSuper + threadIdx.x; w < blockIdx.x; w += kThreads)
     before += tie_counts[(size_t)w * kMantBins + tm];
   uint32_t tot_before;
@@ -787,7 +791,7 @@ int64_t unstructured_wgs(int64_t m, int64_t d) {
 
 // words cleared before an element-wise selection: the histogram copies and the group counts
 int64_t hist_words(int64_t m, int64_t d) {
-  return (int64_t)kHistCopies * kUHist + (unstructured_wgs(m, d) + kSuper - 1) / kSuper * kMantBins;
+  return (int64_t)kHistCopies * kUHist + (unstructured_wgs(m, d) + kSuper - 1) / kSuper * kSuperCopies * kMantBins;
 }
 
 size_t a256(size_t x) { return (x + 255) & ~(size_t)255; }
