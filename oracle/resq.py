@@ -36,6 +36,15 @@ Readings of points the paper leaves open (also listed in the design notes):
       projections, X = silu(G) * U, silu(g) = g / (1 + exp(-g))): X is the bf16 nearest to the
       float64 value of silu(g) * u (ties to even), rounded once, so it is the bf16 activation
       the unfused model would hand to the linear up to that single rounding.
+  N1  the fused producer of the qkv and gate/up projections' input, the RMSNorm of the
+      residual stream H (bf16, m x d) with gain gamma (bf16, d) and epsilon eps (a float32
+      >= 2^-126), as the Qwen2.5 models of Sec. 5.1 apply it before those linears (the paper
+      does not spell it out).  Every step is one IEEE float32 operation, rounded to nearest
+      even, except the sum of squares, which is exact and then rounded once:
+          s = f32(sum_j H_j^2),  mu = f32(s / d),  t = f32(mu + eps),
+          q = f32(sqrt(t)),      r = f32(1 / q),
+          X_j = bf16(f32(f32(H_j * r) * gamma_j)),
+      so X does not depend on any summation order.
 """
 from __future__ import annotations
 
@@ -311,6 +320,68 @@ def swiglu_bf16(g: np.ndarray, u: np.ndarray) -> np.ndarray:
     g = np.asarray(g, dtype=np.float64)
     u = np.asarray(u, dtype=np.float64)
     return round_f64_to_bf16(g / (1.0 + np.exp(-g)) * u)
+
+
+def _round_dyadic_to_f32(num: int, exp: int) -> np.float32:
+    """The float32 nearest to num * 2^exp (num >= 0 an integer), ties to even, with float32's
+    subnormals (spacing 2^-149) and overflow to inf."""
+    if num == 0:
+        return np.float32(0.0)
+    msb = num.bit_length() - 1 + exp            # 2^msb <= value < 2^(msb + 1)
+    unit = max(msb - 23, -149)                  # spacing of the float32 grid at the value
+    q = num
+    if unit > exp:                              # drop the bits below the grid, nearest even
+        drop = unit - exp
+        q, rem = divmod(num, 1 << drop)
+        half = 1 << (drop - 1)
+        if rem > half or (rem == half and q & 1):
+            q += 1
+    else:
+        unit = exp                              # on the grid already: num < 2^24
+    if q * 2.0**unit >= 2.0**128:
+        return np.float32(np.inf)
+    return np.float32(np.ldexp(float(q), unit))  # q <= 2^24: exact
+
+
+def exact_square_sums_f32(h: np.ndarray) -> np.ndarray:
+    """Per row of h (float32 values on the bf16 grid), the float32 nearest to the exact sum of
+    the squares (reading N1).  A bf16 value is an integer of at most 8 bits times a power of
+    two, so each square is an integer of at most 16 bits times 2^(2e); the squares of one
+    exponent are added as integers, the exponents' sums are combined exactly as one Python
+    integer, and that is rounded once."""
+    h = np.asarray(h, dtype=np.float32)
+    assert (h.view(np.uint32) & 0xFFFF == 0).all(), "H must be bf16 values"
+    frac, ex = np.frexp(h.astype(np.float64))   # h = frac * 2^ex, |frac| in [0.5, 1)
+    mant = np.abs(np.rint(frac * 256.0)).astype(np.int64)  # h = +-mant * 2^(ex - 8), exactly
+    e2 = 2 * (ex.astype(np.int64) - 8)          # h^2 = mant^2 * 2^e2
+    out = np.zeros(h.shape[0], dtype=np.float32)
+    for i in range(h.shape[0]):
+        nz = mant[i] != 0
+        if not nz.any():
+            continue
+        lo = int(e2[i][nz].min())
+        per_exp = np.zeros(int(e2[i][nz].max()) - lo + 1, dtype=np.int64)
+        np.add.at(per_exp, e2[i][nz] - lo, mant[i][nz] ** 2)   # < 2^16 each: exact in int64
+        total = sum(int(v) << k for k, v in enumerate(per_exp.tolist()) if v)
+        out[i] = _round_dyadic_to_f32(total, lo)
+    return out
+
+
+def rmsnorm_bf16(h: np.ndarray, gamma: np.ndarray, eps: float) -> np.ndarray:
+    """X = RMSNorm(H) * gamma as bf16 bit patterns (reading N1).  h: m x d float32 values on
+    the bf16 grid, gamma: d values on the bf16 grid, eps: a float32 >= 2^-126."""
+    h = np.asarray(h, dtype=np.float32)
+    gamma = np.asarray(gamma, dtype=np.float32)
+    d = h.shape[1]
+    assert d <= 2**24 and np.float32(eps) >= np.float32(2.0**-126)
+    s = exact_square_sums_f32(h)
+    mu = s / np.float32(d)
+    t = mu + np.float32(eps)
+    q = np.sqrt(t)
+    r = np.float32(1.0) / q
+    y = h * r[:, None]
+    x = y * gamma[None, :]
+    return round_to_bf16(x)
 
 
 # ----------------------------------------------------------------------------------------

@@ -450,3 +450,94 @@ def test_swiglu_matches_library_sigmoid():
     # closed forms: silu(0) = 0; u = 0 gives a zero; silu(g) -> g for large g
     z = Q.swiglu_bf16(np.array([0.0, 3.0, 80.0]), np.array([5.0, 0.0, 1.0]))
     assert bf16_bits_to_f32(z[:2]).tolist() == [0.0, 0.0] and bf16_bits_to_f32(z[2:]).tolist() == [80.0]
+
+
+# ----------------------------------------------------------------------------------------
+# Reading N1: the fused RMSNorm producer of the qkv and gate/up projections
+# ----------------------------------------------------------------------------------------
+def _nearest_f32_brute(v):
+    """The float32 nearest to the rational v >= 0, ties to the even significand: the three
+    float32 values around float(v) compared exactly as fractions."""
+    from fractions import Fraction
+    c = np.float32(float(v))
+    cands = [np.nextafter(c, np.float32(-np.inf)), c, np.nextafter(c, np.float32(np.inf))]
+    cands = [x for x in cands if np.isfinite(x) and x >= 0]
+    best = min(abs(Fraction(float(x)) - v) for x in cands)
+    near = [x for x in cands if abs(Fraction(float(x)) - v) == best]
+    return min(near, key=lambda x: int(np.array(x, np.float32).view(np.uint32)) & 1)
+
+
+def test_rmsnorm_square_sums_brute_force():
+    """The exact-then-rounded sums of squares against Fraction arithmetic and a brute-force
+    nearest float32, on rows that mix magnitudes 2^-133 (bf16 subnormals) to 2^60, zeros and
+    signs, so that the exact sums carry far more bits than float64 holds."""
+    from fractions import Fraction
+    rng = np.random.default_rng(21)
+    rows = []
+    for i in range(60):
+        d = int(rng.integers(1, 40))
+        e = rng.integers(-133 if i % 3 == 0 else -30, 61 if i % 3 == 1 else 8, d)
+        v = rng.integers(1, 256, d) * np.exp2(e.astype(np.float64) - 7) * rng.choice([-1, 1], d)
+        v[rng.random(d) < 0.2] = 0.0
+        rows.append(_bf16(v.astype(np.float32)))
+    for r in rows:
+        got = Q.exact_square_sums_f32(r[None, :])[0]
+        want = _nearest_f32_brute(sum(Fraction(float(x)) ** 2 for x in r))
+        assert got == want and np.array(got).view(np.uint32) == np.array(want).view(np.uint32), r
+
+
+def test_rmsnorm_square_sum_rounding_cases():
+    """Ties and the ends of the float32 range: 1 + 2^-24 is halfway between 1 and its successor
+    and goes to the even 1; a further 2^-120 tips it up; 3 * 2^-13 squared is 1.125 units of
+    the last place; sums below half of 2^-149 vanish, those at 2^-149 survive as subnormals;
+    2^129 overflows to inf."""
+    cases = [([1.0, 2.0**-12], 1.0), ([1.0, 2.0**-12, 2.0**-60], 1.0 + 2.0**-23),
+             ([1.0, 3 * 2.0**-13], 1.0 + 2.0**-23), ([2.0**-75, 2.0**-75], 2.0**-149),
+             ([2.0**-76, 2.0**-76, 2.0**-76], 0.0), ([2.0**-75, 2.0**-76], 2.0**-149),
+             ([2.0**64, 2.0**64], np.inf), ([0.0, -0.0], 0.0), ([-3.0, 4.0], 25.0)]
+    for row, want in cases:
+        got = Q.exact_square_sums_f32(np.array([row], np.float32))[0]
+        assert got == np.float32(want), (row, got, want)
+
+
+def test_rmsnorm_constant_rows_give_gamma():
+    """A row of one power of two +-2^k (d a power of two) has mean square 4^k; with eps far
+    below its last place t = 4^k, q = 2^k and r = 2^-k exactly, so X = +-gamma bit for bit."""
+    d = 128
+    gamma = _bf16(np.random.default_rng(5).normal(0, 1, d).astype(np.float32))
+    ks = [-40, -7, 0, 3, 40]
+    h = np.array([[(-1.0) ** i * 2.0**k] * d for i, k in enumerate(ks)], np.float32)
+    x = bf16_bits_to_f32(Q.rmsnorm_bf16(h, gamma, 2.0**-126))
+    for i in range(len(ks)):
+        assert np.array_equal(x[i], gamma * np.float32((-1.0) ** i)), ks[i]
+
+
+def test_rmsnorm_is_scale_free():
+    """Scaling H by 2^j scales s, mu and t by 4^j and r by 2^-j exactly (eps below the last
+    place of mu), so X does not change."""
+    rng = np.random.default_rng(6)
+    h = _bf16(rng.normal(0, 1, (8, 300)).astype(np.float32))
+    gamma = _bf16(rng.normal(1, 0.2, 300).astype(np.float32))
+    x0 = Q.rmsnorm_bf16(h, gamma, 2.0**-126)
+    for j in (-20, -3, 5, 30):
+        assert np.array_equal(Q.rmsnorm_bf16(h * np.float32(2.0**j), gamma, 2.0**-126), x0), j
+
+
+def test_rmsnorm_close_to_the_real_value():
+    """X against a float64 evaluation of H gamma / sqrt(mean(H^2) + eps) (math.fsum for the
+    mean): within half a bf16 place plus the float32 steps' few units of 2^-24, with eps
+    comparable to the mean square on half the rows (a dropped eps, a mean over d - 1, a
+    missing square root or a gain taken from the wrong column would all exceed it)."""
+    import math
+    rng = np.random.default_rng(7)
+    m, d = 24, 40
+    h = _bf16((rng.normal(0, 1, (m, d)) * np.exp2(rng.integers(-4, 4, (m, 1)))).astype(np.float32))
+    gamma = _bf16(rng.normal(1, 0.5, d).astype(np.float32))
+    for eps in (1e-6, 0.7):
+        x = bf16_bits_to_f32(Q.rmsnorm_bf16(h, gamma, eps)).astype(np.float64)
+        for i in range(m):
+            ms = math.fsum(float(v) ** 2 for v in h[i]) / d
+            ref = h[i].astype(np.float64) * gamma.astype(np.float64) / math.sqrt(ms + float(np.float32(eps)))
+            half_place = np.exp2(np.floor(np.log2(np.abs(ref))) - 8)  # half a bf16 place
+            tol = half_place + np.abs(ref) * 2.0**-20
+            assert (np.abs(x[i] - ref) <= tol).all(), (eps, i)
