@@ -339,6 +339,97 @@ def bench_swiglu_down(args, P, torch, np, wl, fmt, sp, dev, sptr):
     return 0
 
 
+def bench_rmsnorm_in(args, P, torch, np, wl, fmt, sp, dev, sptr):
+    """--op rmsnorm_in: the workload's qkv and gate_up projections (the linears that take an
+    RMSNorm output) with the RMSNorm of H formed inside the quantization pass
+    (resq_linear_fwd_prepared_rmsnorm: one launch for the per-row factors, then the activation
+    pass and the GEMM), against the same linears fed by a torch RMSNorm (float32 statistics)
+    that writes X (bf16) first.  A step is both linears."""
+    from synth import activations, rng_tree, workload_tensors
+    lins = [l for l in wl.linears if l.name in ("qkv", "gate_up")]
+    m = wl.m
+    f, s = P.FORMATS[fmt], P.sparsity_code(sp)
+    eps = 1e-6
+    per_copy = sum(P.resq_prepared_weights_size(f, l.n, l.d) + 2 * m * l.d for l in lins)
+    copies = int(min(32, max(2, -(-2 * LLC_BYTES // per_copy) + 1)))
+    state = []
+    for k, lin in enumerate(lins):
+        _, wb = workload_tensors(wl, lin)
+        qc, qs = P.quantize(torch.from_numpy(wb.view(np.int16)).to(dev), fmt, axis=1)
+        rh, rg = rng_tree(11 + k, 2)
+        h0 = torch.from_numpy(activations(rh, m, lin.d, 0.01, 20.0).view(np.int16)).to(dev)
+        gamma = (1.0 + 0.2 * torch.randn(lin.d, generator=torch.Generator().manual_seed(k))) \
+            .to(torch.bfloat16).view(torch.int16).to(dev)
+        ws_bytes = P.resq_workspace_size(P.OP_LINEAR_FWD_RMSNORM, f, s, m, lin.d, lin.n)
+        state.append({
+            "lin": lin, "wps": [P.prepare_weights(qc, qs, fmt) for _ in range(copies)],
+            "hs": [h0.clone() for _ in range(copies)], "gamma": gamma,
+            "y": torch.empty((m, lin.n), dtype=torch.float32, device=dev),
+            "ws": torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev), "ws_bytes": ws_bytes,
+        })
+    lib = P.load()
+
+    def fused(i):
+        c = i % copies
+        for st in state:
+            l = st["lin"]
+            rc = lib.resq_linear_fwd_prepared_rmsnorm(
+                f, s, int(st["hs"][c].data_ptr()), m, l.d, l.d, int(st["gamma"].data_ptr()), eps,
+                int(st["wps"][c].data_ptr()), l.n, int(st["y"].data_ptr()), l.n,
+                int(st["ws"].data_ptr()), st["ws_bytes"], sptr)
+            if rc != 0:
+                raise P.ResqError(f"resq_linear_fwd_prepared_rmsnorm: {P.resq_last_error()}", rc)
+
+    def unfused(i):
+        c = i % copies
+        for st in state:
+            l = st["lin"]
+            h = st["hs"][c].view(torch.bfloat16).float()
+            r = torch.rsqrt(h.pow(2).mean(-1, keepdim=True) + eps)
+            x = (h * r * st["gamma"].view(torch.bfloat16).float()).to(torch.bfloat16).view(torch.int16)
+            rc = lib.resq_linear_fwd_prepared(f, s, int(x.data_ptr()), m, l.d, l.d,
+                                              int(st["wps"][c].data_ptr()), l.n, int(st["y"].data_ptr()),
+                                              l.n, int(st["ws"].data_ptr()), st["ws_bytes"], sptr)
+            if rc != 0:
+                raise P.ResqError(f"resq_linear_fwd_prepared: {P.resq_last_error()}", rc)
+
+    def timed(fn):
+        for i in range(args.warmup):
+            fn(i)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            fn(i)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / args.steps
+
+    t_f, t_u = timed(fused), timed(unfused)
+    P.resq_profile_enable(True)
+    P.resq_profile_reset()
+    for i in range(args.steps):
+        fused(i)
+    torch.cuda.synchronize()
+    res = P.resq_profile_read("residual")
+    P.resq_profile_enable(False)
+    flops = sum(alg_flops(m, l.d, l.n, sp) for l in lins)
+    out = {
+        "metric": "ResQ qkv and gate_up projections with the RMSNorm producer fused into their "
+                  "quantization pass, TFLOP/s",
+        "value": round(flops / t_f / 1e12, 3), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(t_f * 1e3, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "fp4",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "linears": {l.name: [l.d, l.n] for l in lins}, "m": m,
+                   "format": fmt, "sparsity": sp, "op": "rmsnorm_in", "inputs": "H, gamma bf16",
+                   "eps": eps, "copies_rotated": copies},
+        "unfused_ms": round(t_u * 1e3, 5),
+        "speedup_vs_unfused": round(t_u / t_f, 3),
+        "rms_and_activation_pass_us_per_step": round(res[1] / args.steps * 1e3, 2),
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 
 
@@ -529,10 +620,13 @@ def main() -> int:
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--format", default="hif4", choices=["hif4", "mxfp4"])
     ap.add_argument("--sparsity", default="2:4")
-    ap.add_argument("--op", default="linear", choices=["linear", "diagnostics", "swiglu_down", "w4a16", "w16a4"],
+    ap.add_argument("--op", default="linear",
+                    choices=["linear", "diagnostics", "swiglu_down", "rmsnorm_in", "w4a16", "w16a4"],
                     help="linear: the ResQ layer step; diagnostics: the Figs. 2-4 statistics pass; "
-                         "swiglu_down: the down projection with its SwiGLU input fused; w4a16 / "
-                         "w16a4: the mixed-precision linears of Table 1 on every linear")
+                         "swiglu_down: the down projection with its SwiGLU input fused; "
+                         "rmsnorm_in: the qkv and gate_up projections with their RMSNorm input "
+                         "fused; w4a16 / w16a4: the mixed-precision linears of Table 1 on every "
+                         "linear")
     ap.add_argument("--outlier-threshold", type=float, default=10.0,
                     help="--op diagnostics: |x| above which a block counts as holding an outlier")
     ap.add_argument("--out", default="f32", choices=["f32", "bf16"],
@@ -597,6 +691,12 @@ def main() -> int:
             print("bench.py: --op swiglu_down needs a forward workload with a down projection", file=sys.stderr)
             return 2
         return bench_swiglu_down(args, P, torch, np, wl, args.format, args.sparsity, dev, sptr)
+    if args.op == "rmsnorm_in":
+        if wl.backward or not any(l.name in ("qkv", "gate_up") for l in wl.linears):
+            print("bench.py: --op rmsnorm_in needs a forward workload with a qkv or gate_up "
+                  "projection", file=sys.stderr)
+            return 2
+        return bench_rmsnorm_in(args, P, torch, np, wl, args.format, args.sparsity, dev, sptr)
     if args.op in ("w4a16", "w16a4"):
         if wl.backward:
             print(f"bench.py: --op {args.op} needs a forward workload", file=sys.stderr)

@@ -104,7 +104,8 @@ typedef enum {
   RESQ_OP_LINEAR_BWD = 2,
   RESQ_OP_LINEAR_FWD_PREPARED = 3,
   RESQ_OP_DIAGNOSTICS = 4,
-  RESQ_OP_LINEAR_W16A4 = 5
+  RESQ_OP_LINEAR_W16A4 = 5,
+  RESQ_OP_LINEAR_FWD_RMSNORM = 6
 } resq_op;
 
 /*
@@ -236,6 +237,28 @@ int resq_linear_fwd_prepared_swiglu(int format, int sparsity, const void* G, con
                                     int in_dtype, int64_t m, int64_t d, int64_t ldg, int64_t ldu,
                                     const void* wprep, int64_t n, float* Y, int64_t ldy,
                                     void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * resq_linear_fwd_prepared_rmsnorm - resq_linear_fwd_prepared for a projection that takes an
+ * RMSNorm output (the qkv and gate/up projections of the Qwen2.5 models of Sec. 5.1), with the
+ * normalization formed inside the quantization pass instead of being read:
+ *     X = RMSNorm(H) * gamma,   per row: s = f32(sum_j H_j^2) (the exact sum, rounded once),
+ *     r = f32(1 / f32(sqrt(f32(f32(s / d) + eps)))),   X_j = bf16(f32(f32(H_j r) gamma_j)),
+ * every float32 step rounded to nearest even.  The exact sum makes X independent of summation
+ * order: it is bit for bit the X of that definition.  A first launch computes r per row
+ * (into the workspace); the activation pass reads H and gamma, forms X, then computes Q(X),
+ * dX, Q(dX) and S as the other forward entry points do (Eq. 4).  X is never written.
+ * H      : m x d bf16 (bit patterns), row stride ldh >= d, 2-byte aligned (16-byte aligned
+ *          with ldh % 8 == 0 for 16-byte loads).  d <= 2^18 (else RESQ_ERR_UNSUPPORTED).
+ * gamma  : d bf16 values.
+ * eps    : finite, >= 2^-126 (else RESQ_ERR_ARG).
+ * wprep, n, Y (float32), ldy and errors: as resq_linear_fwd_prepared.  Workspace:
+ * resq_workspace_size(RESQ_OP_LINEAR_FWD_RMSNORM, format, sparsity, m, d, n) bytes.
+ */
+int resq_linear_fwd_prepared_rmsnorm(int format, int sparsity, const uint16_t* H, int64_t m,
+                                     int64_t d, int64_t ldh, const uint16_t* gamma, float eps,
+                                     const void* wprep, int64_t n, float* Y, int64_t ldy,
+                                     void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * resq_linear_bwd - the FP4 training-policy backward GEMMs of the linear Y = X W^T:

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <algorithm>
 #include <cstdio>
+#include <cmath>
 #include <mutex>
 #include <string>
 
@@ -120,6 +121,7 @@ struct ActWs {
   uint8_t* frag_r;
   uint8_t* fsc_r;
   float* gemm_partial;       // split-K partial tiles
+  float* rinv;               // the RMSNorm producer's per-row factors
   resq::SelectWs sel;
 };
 
@@ -179,7 +181,8 @@ void carve_prepared(const void* base, int fmt, int64_t n, int64_t d, const uint8
   *fsc = b + align256(resq::frag_bytes(b_pack_mode(fmt), n, d));
 }
 
-size_t carve_fwd(void* base, int fmt, const Sp& sp, int64_t m, int64_t d, int64_t n, ActWs* w) {
+size_t carve_fwd(void* base, int fmt, const Sp& sp, int64_t m, int64_t d, int64_t n, ActWs* w,
+                 bool rms = false) {
   Carver c(base);
   ActWs t{};
   if (global_kind(sp)) {  // the dense K-major Q(dX) the selection ranks
@@ -195,6 +198,7 @@ size_t carve_fwd(void* base, int fmt, const Sp& sp, int64_t m, int64_t d, int64_
   }
   const size_t pb = resq::gemm_split_scratch(fmt, m, n, d);
   if (pb > 0) t.gemm_partial = (float*)c.take(pb);
+  if (rms) t.rinv = (float*)c.take((size_t)m * sizeof(float));
   if (w) *w = t;
   return c.off;
 }
@@ -326,6 +330,7 @@ size_t resq_workspace_size(int op, int format, int sparsity, int64_t m, int64_t 
     case RESQ_OP_LINEAR_FWD:
       return carve_fwd(nullptr, format, sp, m, d, n, nullptr) + prepared_bytes(format, n, d);
     case RESQ_OP_LINEAR_FWD_PREPARED: return carve_fwd(nullptr, format, sp, m, d, n, nullptr);
+    case RESQ_OP_LINEAR_FWD_RMSNORM: return carve_fwd(nullptr, format, sp, m, d, n, nullptr, true);
     case RESQ_OP_LINEAR_BWD: return carve_bwd(nullptr, format, m, d, n, nullptr);
     case RESQ_OP_DIAGNOSTICS: return resq::diag_ws_bytes(m, d);
     case RESQ_OP_LINEAR_W16A4:
@@ -543,9 +548,40 @@ int resq_linear_fwd_prepared_swiglu(int format, int sparsity, const void* G, con
   const size_t need = carve_fwd(workspace, format, sp, m, d, n, &w);
   rc = check_ws(workspace, workspace_bytes, need);
   if (rc != RESQ_OK) return rc;
-  const resq::Producer prod{G, U, ldg, ldu, in_dtype == RESQ_IN_F32};
+  const resq::Producer prod{G, U, ldg, ldu, in_dtype == RESQ_IN_F32, resq::kProdSwiglu, nullptr};
   return linear_fwd_core(format, sp, nullptr, m, d, 0, wprep, n, Y, ldy, false, w,
                          (hipStream_t)stream, &prod);
+}
+
+int resq_linear_fwd_prepared_rmsnorm(int format, int sparsity, const uint16_t* H, int64_t m,
+                                     int64_t d, int64_t ldh, const uint16_t* gamma, float eps,
+                                     const void* wprep, int64_t n, float* Y, int64_t ldy,
+                                     void* workspace, size_t workspace_bytes, void* stream) {
+  const Sp sp = decode_sparsity(sparsity);
+  int rc = check_fwd_args(format, sparsity, sp, H, m, d, ldh, n, Y, ldy);
+  if (rc != RESQ_OK) return rc;
+  if (!std::isfinite(eps) || !(eps >= 0x1p-126f))
+    return fail(RESQ_ERR_ARG, "eps (%g) must be finite and at least 2^-126", (double)eps);
+  if (d > resq::kRmsMaxD)
+    return fail(RESQ_ERR_UNSUPPORTED, "the RMSNorm producer supports d <= %lld (d=%lld)",
+                (long long)resq::kRmsMaxD, (long long)d);
+  if (m > 0 && d > 0 && !gamma) return fail(RESQ_ERR_ARG, "gamma is NULL");
+  if (m == 0 || n == 0) return ok();
+  if (d > 0 && !wprep) return fail(RESQ_ERR_ARG, "wprep is NULL");
+  if ((uintptr_t)wprep % 256 != 0) return fail(RESQ_ERR_ARG, "wprep must be 256-byte aligned");
+  if ((uintptr_t)H % 2 != 0 || (uintptr_t)gamma % 2 != 0)
+    return fail(RESQ_ERR_ARG, "H and gamma must be 2-byte aligned");
+  ActWs w{};
+  const size_t need = carve_fwd(workspace, format, sp, m, d, n, &w, true);
+  rc = check_ws(workspace, workspace_bytes, need);
+  if (rc != RESQ_OK) return rc;
+  const hipStream_t s = (hipStream_t)stream;
+  {
+    resq::ProfScope prof_(resq::kProfResidual, s, true);
+    resq::launch_rms_rows(H, m, d, ldh, eps, w.rinv, s);
+  }
+  const resq::Producer prod{H, gamma, ldh, 0, false, resq::kProdRmsnorm, w.rinv};
+  return linear_fwd_core(format, sp, nullptr, m, d, 0, wprep, n, Y, ldy, false, w, s, &prod);
 }
 
 int resq_linear_fwd(int format, int sparsity, const uint16_t* X, int64_t m, int64_t d,

@@ -34,14 +34,28 @@ void launch_quant_cols(int fmt, const void* x, bool in_f32, int64_t rows, int64_
                        int64_t ld, uint8_t* codes, void* scales, hipStream_t s);
 
 // A producer fused into the forward's activation pass: instead of reading X, the pass forms
-// X = silu(G) * U (the SwiGLU feeding a down projection) from G and U (m x d, row strides ldg
-// and ldu, bf16 or float32), each element the bf16 nearest to its float64 value.
+// X from the producer's inputs.  kProdSwiglu: X = silu(G) * U (the SwiGLU feeding a down
+// projection) from G = g and U = u (m x d, row strides ldg and ldu, bf16 or float32), each
+// element the bf16 nearest to its float64 value.  kProdRmsnorm: X = RMSNorm(H) * gamma from
+// H = g (bf16, row stride ldg), gamma = u (d bf16 values) and rinv (m float32 factors
+// 1 / sqrt(mean(H^2) + eps), written by launch_rms_rows), each element
+// bf16(f32(f32(H r) gamma)).
+enum ProducerKind { kProdSwiglu = 1, kProdRmsnorm = 2 };
 struct Producer {
   const void* g;
   const void* u;
   int64_t ldg, ldu;
   bool f32;
+  int kind;
+  const float* rinv;
 };
+
+// The RMSNorm producer's per-row factors: rinv[i] = f32(1 / f32(sqrt(f32(f32(s_i / d) + eps))))
+// with s_i the float32 nearest to the exact sum of the squares of row i of H (bf16, m x d, row
+// stride ldh), every float32 step rounded to nearest even.  d <= 2^18; eps >= 2^-126, finite.
+constexpr int64_t kRmsMaxD = (int64_t)1 << 18;
+void launch_rms_rows(const uint16_t* H, int64_t m, int64_t d, int64_t ldh, float eps, float* rinv,
+                     hipStream_t s);
 
 // Q(X), dX = X - Q(X), Q(dX), and S_k:4 / S_k:8 (k = nm_keep) / identity / none.  keep_mask
 // and partials may be null.  prod (frag = true only): X comes from that producer.  partials (double [m][d/B]) receives the exact per-scale-block sums of squares of

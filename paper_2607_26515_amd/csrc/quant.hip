@@ -405,9 +405,159 @@ __device__ __forceinline__ void swiglu8(const Producer& p, int64_t row, int64_t 
   }
 }
 
-// Row tile t, K step kb of the fused residual pass (one workgroup of 256 threads).  SWIGLU:
-// X comes from the producer `prod` instead of from X.
-template <int FMT, int MODE, bool VEC, bool SWIGLU>
+// ---------------------------------------------------------------------------------------
+// RMSNorm producer.  Float32 steps rounded to nearest even, each checked exactly: a float64
+// result rounded to float32 is within one place of the right answer, and the exact comparison
+// with the midpoints next to it (products of at most 25 x 25 bits, exact in float64) fixes
+// the last place.  Neither a quotient of float32 values nor a square root of one can fall on
+// a midpoint, so there are no ties.
+// ---------------------------------------------------------------------------------------
+__device__ __forceinline__ float f32_up(float x) { return __uint_as_float(__float_as_uint(x) + 1u); }
+__device__ __forceinline__ float f32_down(float x) { return __uint_as_float(__float_as_uint(x) - 1u); }
+
+// a / b to nearest, for a >= 0 and b > 0 (inf allowed in one of them)
+__device__ float div_rn_f32(float a, float b) {
+  float z = (float)((double)a / (double)b);
+  if (!isfinite(z) || !isfinite(b)) return z;
+  if (0.5 * ((double)z + (double)f32_up(z)) * (double)b < (double)a) return f32_up(z);
+  if (z > 0.f && 0.5 * ((double)z + (double)f32_down(z)) * (double)b > (double)a) return f32_down(z);
+  return z;
+}
+
+// sqrt(t) to nearest, for t >= 0 (inf allowed)
+__device__ float sqrt_rn_f32(float t) {
+  float z = (float)sqrt((double)t);
+  if (!isfinite(z)) return z;
+  const double hi = 0.5 * ((double)z + (double)f32_up(z));
+  if (hi * hi < (double)t) return f32_up(z);
+  const double lo = 0.5 * ((double)z + (double)f32_down(z));
+  if (z > 0.f && lo * lo > (double)t) return f32_down(z);
+  return z;
+}
+
+// A bf16 value is M * 2^(E - 134) with M < 2^8 (E = the exponent field, 1 for subnormals), so
+// its square is M^2 * 2^(2E - 268).  One row's squares are added as integers per exponent
+// field (per-wave LDS histograms, at most 2^16 * (d / 4 + 512) < 2^32 per wave and bin for
+// d <= 2^18), the 255 bin totals are added into an integer of kRmsLimbs 32-bit limbs in
+// units of 2^-268 (bin E at bit 2E, below 2^(2 * 255 + 34) < 2^(32 * kRmsLimbs)), and that
+// exact sum is rounded once: to 53 bits by truncation with the sticky lowest bit (round to
+// odd), then to float32 to nearest even, which gives the float32 nearest to the exact sum
+// (53 >= 24 + 2 bits).
+constexpr int kRmsLimbs = 18;
+
+__device__ float rms_row_factor(const unsigned long long* limb, int64_t d, float eps) {
+  uint32_t n[kRmsLimbs];
+  unsigned long long carry = 0;
+#pragma unroll
+  for (int l = 0; l < kRmsLimbs; ++l) {
+    const unsigned long long v = limb[l] + carry;
+    n[l] = (uint32_t)v;
+    carry = v >> 32;
+  }
+  int top = kRmsLimbs - 1;
+  while (top >= 0 && n[top] == 0u) --top;
+  float s = 0.f;
+  if (top >= 0) {
+    const int lz = __clz(n[top]);
+    const int msb = 32 * top + 31 - lz;  // the sum lies in [2^(msb - 268), 2^(msb - 267))
+    const uint32_t x1 = top >= 1 ? n[top - 1] : 0u, x0 = top >= 2 ? n[top - 2] : 0u;
+    unsigned long long w = ((((unsigned long long)n[top]) << 32) | x1) << lz;  // msb at bit 63
+    bool sticky;
+    if (lz > 0) {
+      w |= x0 >> (32 - lz);
+      sticky = (x0 << lz) != 0u;
+    } else {
+      sticky = x0 != 0u;
+    }
+    for (int l = 0; l < top - 2; ++l) sticky |= n[l] != 0u;
+    unsigned long long sig = w >> 11;
+    sticky |= (w & 0x7FFull) != 0ull;
+    if (sticky) sig |= 1ull;
+    s = (float)ldexp((double)sig, msb - 52 - 268);  // exact in float64, then one rounding
+  }
+  const float mu = div_rn_f32(s, (float)d);
+  const float t = mu + eps;
+  return div_rn_f32(1.f, sqrt_rn_f32(t));
+}
+
+// grid-stride over rows, one workgroup of 256 threads per row at a time
+template <bool VEC>
+__global__ __launch_bounds__(256) void rms_rows_kernel(const uint16_t* __restrict__ H, int64_t m,
+                                                        int64_t d, int64_t ldh, float eps,
+                                                        float* __restrict__ rinv) {
+  __shared__ uint32_t wh[4][256];
+  __shared__ unsigned long long limb[kRmsLimbs];
+  const int tid = threadIdx.x, wave = tid >> 6;
+  for (int64_t row = blockIdx.x; row < m; row += gridDim.x) {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) wh[w][tid] = 0u;
+    if (tid < kRmsLimbs) limb[tid] = 0ull;
+    __syncthreads();
+    const uint16_t* src = H + row * ldh;
+    for (int64_t c = (int64_t)tid * 8; c < d; c += 256 * 8) {  // d % 8 == 0
+      uint32_t b[8];
+      if constexpr (VEC) {
+        const uint4 u = *reinterpret_cast<const uint4*>(src + c);
+        const uint32_t v[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) { b[2 * e] = v[e] & 0xFFFFu; b[2 * e + 1] = v[e] >> 16; }
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) b[i] = src[c + i];
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const uint32_t e = (b[i] >> 7) & 0xFFu;
+        const uint32_t mant = (b[i] & 0x7Fu) | (e ? 0x80u : 0u);
+        if (mant) atomicAdd(&wh[wave][e ? e : 1u], mant * mant);
+      }
+    }
+    __syncthreads();
+    // bin tid (0 .. 255) at bit 2 * tid: three 32-bit pieces into three limbs
+    const unsigned long long T = (unsigned long long)wh[0][tid] + wh[1][tid] + wh[2][tid] + wh[3][tid];
+    if (T) {
+      const int off = 2 * tid, L = off >> 5, sh = off & 31;
+      const unsigned long long lo = (T & 0xFFFFFFFFull) << sh, hi = (T >> 32) << sh;
+      atomicAdd(&limb[L], lo & 0xFFFFFFFFull);
+      atomicAdd(&limb[L + 1], (lo >> 32) + (hi & 0xFFFFFFFFull));
+      if (hi >> 32) atomicAdd(&limb[L + 2], hi >> 32);
+    }
+    __syncthreads();
+    if (tid == 0) rinv[row] = rms_row_factor(limb, d, eps);
+    __syncthreads();  // the next row clears the histograms and limbs
+  }
+}
+
+// X = RMSNorm(H) * gamma for 8 consecutive elements of one row
+template <bool VEC>
+__device__ __forceinline__ void rmsnorm8(const Producer& p, int64_t row, int64_t col0, float x[8]) {
+  const uint16_t* hs = reinterpret_cast<const uint16_t*>(p.g) + row * p.ldg + col0;
+  const uint16_t* gs = reinterpret_cast<const uint16_t*>(p.u) + col0;
+  const float r = p.rinv[row];
+  float h[8], g[8];
+  if constexpr (VEC) {
+    const uint4 hw = *reinterpret_cast<const uint4*>(hs), gw = *reinterpret_cast<const uint4*>(gs);
+    const uint32_t hv[4] = {hw.x, hw.y, hw.z, hw.w}, gv[4] = {gw.x, gw.y, gw.z, gw.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      h[2 * e] = bf16_to_f32(hv[e] & 0xFFFFu); h[2 * e + 1] = bf16_to_f32(hv[e] >> 16);
+      g[2 * e] = bf16_to_f32(gv[e] & 0xFFFFu); g[2 * e + 1] = bf16_to_f32(gv[e] >> 16);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) { h[i] = bf16_to_f32(hs[i]); g[i] = bf16_to_f32(gs[i]); }
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float y = h[i] * r;   // two separate float32 products, each rounded
+    const uint32_t u = __float_as_uint(y * g[i]);
+    x[i] = __uint_as_float(((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16) << 16);
+  }
+}
+
+// Row tile t, K step kb of the fused residual pass (one workgroup of 256 threads).  PROD
+// (a ProducerKind, or 0): X comes from the producer `prod` instead of from X.
+template <int FMT, int MODE, bool VEC, int PROD>
 __device__ __forceinline__ void residual_frag_tile(
     const uint16_t* __restrict__ X, int64_t m, int64_t d, int64_t ldx, int64_t nkb,
     uint8_t* __restrict__ fx, uint8_t* __restrict__ fsx, uint8_t* __restrict__ fr,
@@ -419,8 +569,10 @@ __device__ __forceinline__ void residual_frag_tile(
   const int64_t row = t * 32 + rr;
   const int64_t col0 = kb * 64 + 32 * half + 8 * s;
   float x[8];
-  if (SWIGLU && row < m && col0 < d) {
+  if (PROD == kProdSwiglu && row < m && col0 < d) {
     swiglu8<VEC>(prod, row, col0, x);
+  } else if (PROD == kProdRmsnorm && row < m && col0 < d) {
+    rmsnorm8<VEC>(prod, row, col0, x);
   } else if (row < m && col0 < d) {
     const uint16_t* src = X + row * ldx + col0;
     if constexpr (VEC) {
@@ -485,7 +637,7 @@ __device__ __forceinline__ void residual_frag_tile(
 // sums of squares (may be null); with ehist (element-wise selection, cleared beforehand) the
 // workgroup also counts the exponent fields of |Q(dX)| and adds them into copy
 // (workgroup % kElemHistCopies) of that histogram.
-template <int FMT, int MODE, bool VEC, bool SWIGLU>
+template <int FMT, int MODE, bool VEC, int PROD>
 __global__ __launch_bounds__(256) void residual_frag_kernel(
     const uint16_t* __restrict__ X, int64_t m, int64_t d, int64_t ldx, int64_t nkb,
     uint8_t* __restrict__ fx, uint8_t* __restrict__ fsx, uint8_t* __restrict__ fr,
@@ -499,7 +651,7 @@ __global__ __launch_bounds__(256) void residual_frag_kernel(
   }
   const int64_t mtiles = (m + 31) / 32;
   for (int64_t t = blockIdx.y; t < mtiles; t += gridDim.y)
-    residual_frag_tile<FMT, MODE, VEC, SWIGLU>(X, m, d, ldx, nkb, fx, fsx, fr, fsr, partials, nm_keep,
+    residual_frag_tile<FMT, MODE, VEC, PROD>(X, m, d, ldx, nkb, fx, fsx, fr, fsr, partials, nm_keep,
                                                prod, t, blockIdx.x, counting ? lh : nullptr);
   if (counting) {
     __syncthreads();
@@ -681,6 +833,16 @@ void launch_quant_cols(int fmt, const void* x, bool in_f32, int64_t rows, int64_
 #undef RESQ_QC
 }
 
+void launch_rms_rows(const uint16_t* H, int64_t m, int64_t d, int64_t ldh, float eps, float* rinv,
+                     hipStream_t s) {
+  if (m == 0) return;
+  const unsigned grid = (unsigned)(m < 8192 ? m : 8192);
+  if ((uintptr_t)H % 16 == 0 && ldh % 8 == 0)
+    launch_timed(rms_rows_kernel<true>, dim3(grid), dim3(256), 0u, s, H, m, d, ldh, eps, rinv);
+  else
+    launch_timed(rms_rows_kernel<false>, dim3(grid), dim3(256), 0u, s, H, m, d, ldh, eps, rinv);
+}
+
 void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
                      uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes, void* qr_scales,
                      uint8_t* keep_mask, double* partials, hipStream_t s, bool frag,
@@ -689,8 +851,8 @@ void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d,
   if (frag) {
     const int64_t nkb = (d + 63) / 64;
     const dim3 grid((unsigned)nkb, grid_rows((m + 31) / 32));
-    const Producer pr = prod ? *prod : Producer{nullptr, nullptr, 0, 0, false};
-    // 16-byte loads: 8 bf16 of X (or of G and U), or 2 x 4 floats of G and U
+    const Producer pr = prod ? *prod : Producer{nullptr, nullptr, 0, 0, false, 0, nullptr};
+    // 16-byte loads: 8 bf16 of X (or of G and U, or of H and gamma), or 2 x 4 floats of G and U
     const int64_t ve = prod ? (prod->f32 ? 4 : 8) : 8;
     const bool vec16 = prod ? ((uintptr_t)pr.g % 16 == 0 && (uintptr_t)pr.u % 16 == 0 &&
                                pr.ldg % ve == 0 && pr.ldu % ve == 0)
@@ -706,10 +868,12 @@ void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d,
       default: RESQ_RF(F, kResid24, V, P); break;                    \
     }
 #define RESQ_RF_VEC(F, P) if (vec16) { RESQ_RF_MODE(F, true, P) } else { RESQ_RF_MODE(F, false, P) }
-    if (prod) {
-      if (fmt == kMX) { RESQ_RF_VEC(kMX, true) } else { RESQ_RF_VEC(kHI, true) }
+    if (prod && prod->kind == kProdRmsnorm) {
+      if (fmt == kMX) { RESQ_RF_VEC(kMX, kProdRmsnorm) } else { RESQ_RF_VEC(kHI, kProdRmsnorm) }
+    } else if (prod) {
+      if (fmt == kMX) { RESQ_RF_VEC(kMX, kProdSwiglu) } else { RESQ_RF_VEC(kHI, kProdSwiglu) }
     } else {
-      if (fmt == kMX) { RESQ_RF_VEC(kMX, false) } else { RESQ_RF_VEC(kHI, false) }
+      if (fmt == kMX) { RESQ_RF_VEC(kMX, 0) } else { RESQ_RF_VEC(kHI, 0) }
     }
 #undef RESQ_RF_VEC
 #undef RESQ_RF_MODE

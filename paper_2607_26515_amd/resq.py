@@ -74,6 +74,7 @@ IN_BF16, IN_F32 = 0, 1
 NOALLOC_SCRATCH_BYTES = 64 << 20  # RESQ_NOALLOC_SCRATCH_BYTES
 OP_RESIDUAL_SPARSIFY, OP_LINEAR_FWD, OP_LINEAR_BWD, OP_LINEAR_FWD_PREPARED, OP_DIAGNOSTICS = 0, 1, 2, 3, 4
 OP_LINEAR_W16A4 = 5
+OP_LINEAR_FWD_RMSNORM = 6
 DIAG_STATS = ("elements", "zeros_x", "zeros_qx", "blocks", "outlier_blocks", "energy_qx",
               "sse24_qx", "energy_qr", "sse24_qr")
 
@@ -82,7 +83,8 @@ EXPORTED = ("resq_quantize", "resq_residual_sparsify", "resq_linear_fwd", "resq_
             "resq_profile_reset", "resq_profile_read", "resq_prepared_weights_size",
             "resq_prepare_weights", "resq_linear_fwd_prepared", "resq_linear_fwd_prepared_bf16",
             "resq_diagnostics", "resq_linear_fwd_prepared_swiglu", "resq_gemm_plan",
-            "resq_linear_fwd_prepared_noalloc", "resq_linear_w4a16", "resq_linear_w16a4")
+            "resq_linear_fwd_prepared_noalloc", "resq_linear_w4a16", "resq_linear_w16a4",
+            "resq_linear_fwd_prepared_rmsnorm")
 GEMM_TILES = {0: "64x64", 1: "128x256", 2: "128x192", 3: "128x192_8w", 4: "64x128"}
 
 
@@ -130,6 +132,9 @@ def load() -> ctypes.CDLL:
     lib.resq_linear_fwd_prepared_swiglu.argtypes = [i32, i32, vp, vp, i32, i64, i64, i64, i64, vp, i64,
                                                     vp, i64, vp, sz, vp]
     lib.resq_linear_fwd_prepared_swiglu.restype = i32
+    lib.resq_linear_fwd_prepared_rmsnorm.argtypes = [i32, i32, vp, i64, i64, i64, vp, ctypes.c_float,
+                                                     vp, i64, vp, i64, vp, sz, vp]
+    lib.resq_linear_fwd_prepared_rmsnorm.restype = i32
     for f in ("resq_quantize", "resq_residual_sparsify", "resq_linear_fwd", "resq_linear_bwd"):
         getattr(lib, f).restype = i32
     lib.resq_workspace_size.restype = sz
@@ -214,6 +219,12 @@ def resq_linear_fwd_prepared_swiglu(fmt, sparsity, G, U, in_dtype, m, d, ldg, ld
                                     workspace, workspace_bytes, stream=0) -> int:
     return load().resq_linear_fwd_prepared_swiglu(fmt, sparsity, G, U, in_dtype, m, d, ldg, ldu,
                                                   wprep, n, Y, ldy, workspace, workspace_bytes, stream)
+
+
+def resq_linear_fwd_prepared_rmsnorm(fmt, sparsity, H, m, d, ldh, gamma, eps, wprep, n, Y, ldy,
+                                     workspace, workspace_bytes, stream=0) -> int:
+    return load().resq_linear_fwd_prepared_rmsnorm(fmt, sparsity, H, m, d, ldh, gamma, eps, wprep,
+                                                   n, Y, ldy, workspace, workspace_bytes, stream)
 
 
 def resq_diagnostics(fmt, X, m, d, ldx, outlier_threshold, stats, workspace, workspace_bytes,
@@ -449,6 +460,27 @@ def linear_w16a4(x, w, fmt, y=None, ws=None, stream=None):
     rc = resq_linear_w16a4(f, _p(x), m, d, x.stride(0), _p(w), w.stride(0), n, _p(y), y.stride(0),
                            _p(buf), nb, _stream(stream))
     _check(rc, "resq_linear_w16a4")
+    return y
+
+
+def linear_fwd_rmsnorm(h, gamma, eps, wprep, n, fmt, sparsity, y=None, ws=None, stream=None):
+    """Y = ResQ linear of X = RMSNorm(H) * gamma (formed inside the quantization pass); H is an
+    m x d bf16 view (int16 bit patterns or bfloat16) with unit column stride, gamma d bf16
+    values, eps a float32 >= 2^-126."""
+    import torch
+    m, d = h.shape
+    f, sp = _fmt(fmt), _sp(sparsity)
+    if gamma.numel() != d or not gamma.is_contiguous():
+        raise ValueError("gamma must hold d contiguous values")
+    if y is None:
+        y = torch.empty((m, n), dtype=torch.float32, device=h.device)
+    if ws is None:
+        ws = workspace(OP_LINEAR_FWD_RMSNORM, f, sp, m, d, n, h.device)
+    buf, nb = ws
+    rc = resq_linear_fwd_prepared_rmsnorm(f, sp, _p(h), m, d, h.stride(0), _p(gamma), float(eps),
+                                          _p(wprep), n, _p(y), y.stride(0), _p(buf), nb,
+                                          _stream(stream))
+    _check(rc, "resq_linear_fwd_prepared_rmsnorm")
     return y
 
 

@@ -154,6 +154,30 @@ def test_swiglu_forward_rejects_bad_arguments():
     assert call(B.MXFP4, B.S_2_4, 0, 0, B.IN_BF16, 0, 64, 64, 64, 0, 8, 0, 8, 0, 0, 0) == B.OK
 
 
+def test_rmsnorm_forward_rejects_bad_arguments():
+    ptr = 1 << 20  # never dereferenced
+    call = P.resq_linear_fwd_prepared_rmsnorm
+    m, d, n = 4, 64, 8
+    ws = P.resq_workspace_size(B.OP_LINEAR_FWD_RMSNORM, B.MXFP4, B.S_2_4, m, d, n)
+    base = P.resq_workspace_size(B.OP_LINEAR_FWD_PREPARED, B.MXFP4, B.S_2_4, m, d, n)
+    assert base + 4 * m <= ws < base + 4 * m + 512  # plus the per-row factors
+    big = P.resq_workspace_size(B.OP_LINEAR_FWD_RMSNORM, B.HIF4, B.S_2_4, 5000, 2048, 2560)
+    assert big >= P.resq_workspace_size(B.OP_LINEAR_FWD_PREPARED, B.HIF4, B.S_2_4, 5000, 2048, 2560) + 20000
+    # eps: zero, below 2^-126, NaN, inf
+    for eps in (0.0, 2.0**-127, float("nan"), float("inf"), -1e-6):
+        assert call(B.MXFP4, B.S_2_4, ptr, m, d, d, ptr, eps, ptr, n, ptr, n, ptr, ws, 0) == B.ERR_ARG, eps
+    # d beyond 2^18, NULL gamma, odd H address, ld < d, block size, missing workspace
+    assert call(B.MXFP4, B.S_2_4, ptr, m, 2**18 + 32, 2**18 + 32, ptr, 1e-6, ptr, n, ptr, n, ptr, ws, 0) \
+        == B.ERR_UNSUPPORTED
+    assert call(B.MXFP4, B.S_2_4, ptr, m, d, d, 0, 1e-6, ptr, n, ptr, n, ptr, ws, 0) == B.ERR_ARG
+    assert call(B.MXFP4, B.S_2_4, ptr + 1, m, d, d, ptr, 1e-6, ptr, n, ptr, n, ptr, ws, 0) == B.ERR_ARG
+    assert call(B.MXFP4, B.S_2_4, ptr, m, d, d - 1, ptr, 1e-6, ptr, n, ptr, n, ptr, ws, 0) == B.ERR_ARG
+    assert call(B.HIF4, B.S_2_4, ptr, m, 96, 96, ptr, 1e-6, ptr, n, ptr, n, ptr, ws, 0) == B.ERR_SHAPE
+    assert call(B.MXFP4, B.S_2_4, ptr, m, d, d, ptr, 1e-6, ptr, n, ptr, n, 0, 0, 0) == B.ERR_WORKSPACE
+    # nothing to do: m = 0
+    assert call(B.MXFP4, B.S_2_4, 0, 0, d, d, 0, 1e-6, 0, n, 0, n, 0, 0, 0) == B.OK
+
+
 def test_profiler_names_and_reset():
     import ctypes
     n, ms = ctypes.c_int64(-1), ctypes.c_double(-1.0)
