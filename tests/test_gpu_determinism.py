@@ -120,3 +120,39 @@ def test_backward_twice_same_bits(fmt, name):
     torch.cuda.synchronize()
     assert _same_bits(dx1, dx2), "dX differs between two identical calls"
     assert _same_bits(dw1, dw2), "dW differs between two identical calls"
+
+
+_SPLIT_CASES = [("qwen3b_layer_m256", "down", "2:4"), ("qwen7b_down_m256", "down", "2:4"),
+                ("qwen7b_layer_m512", "down", "block32x64_50"), ("qwen7b_layer_m512", "down", "unstructured50")]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("wl_name,lin_name,sp", _SPLIT_CASES)
+def test_split_k_from_any_workspace(fmt, wl_name, lin_name, sp):
+    """A K-split GEMM keeps its partial tiles in the workspace, and every partial is written
+    before the reduction reads it: a workspace full of 0xFF bytes, the same workspace used
+    again, and a zeroed one give the same bits."""
+    import torch
+    import paper_2607_26515_amd as P
+    wl = _workload(wl_name)
+    lin = next(l for l in wl.linears if l.name == lin_name)
+    plan = P.gemm_plan(fmt, wl.m, lin.n, lin.d, True)
+    log(f"split-K workspace {wl_name}/{lin_name} {fmt} {sp} plan={plan}")
+    assert plan["ksplit"] > 1, "the case must split K"
+    xb, wb = workload_tensors(wl, lin, seed=1)
+    x = dev_bf16(xb)
+    qc, qs = P.quantize(dev_bf16(wb), fmt, axis=1)
+    wprep = P.prepare_weights(qc, qs, fmt)
+    del qc, qs
+    code = P.sparsity_code(sp)
+    dirty = P.workspace(P.OP_LINEAR_FWD_PREPARED, fmt, code, wl.m, lin.d, lin.n, x.device)
+    dirty[0].fill_(255)
+    clean = P.workspace(P.OP_LINEAR_FWD_PREPARED, fmt, code, wl.m, lin.d, lin.n, x.device)
+    clean[0].zero_()
+    y1 = P.linear_fwd_prepared(x, wprep, lin.n, fmt, sp, ws=dirty)
+    y2 = P.linear_fwd_prepared(x, wprep, lin.n, fmt, sp, ws=dirty)
+    y3 = P.linear_fwd_prepared(x, wprep, lin.n, fmt, sp, ws=clean)
+    torch.cuda.synchronize()
+    assert _same_bits(y1, y3), f"dirty workspace: {int((y1 != y3).sum())} outputs differ"
+    assert _same_bits(y2, y3), f"reused workspace: {int((y2 != y3).sum())} outputs differ"
