@@ -117,3 +117,25 @@ def test_rmsnorm_identity_weights_read_out_x():
         # a sum over K starting from +0: a -0 product gives +0, as the oracle's matmul does
         want = (qx * qi[None, :]).astype(np.float32) + np.float32(0.0)
         assert np.array_equal(y.view(np.uint32), want.view(np.uint32)), fmt
+
+
+def test_rmsnorm_largest_d():
+    """d = 2^18, the largest the producer takes: a row of one value with the largest bf16
+    significand (255 / 128 * 2^e) fills each per-wave bin of the square-sum histogram to
+    65536 * 255^2, 99.2% of its 32-bit range; a second row mixes magnitudes, a third is
+    zero.  The GEMM over K = 2^18 splits K."""
+    import paper_2607_26515_amd as P
+    log("rmsnorm d = 2^18")
+    m, d, n = 3, 1 << 18, 32
+    rng = np.random.default_rng(29)
+    rows = np.zeros((m, d), np.float32)
+    rows[0] = 255.0 / 128.0 * 2.0**-3
+    rows[1] = rng.standard_t(3, d) * np.exp2(rng.integers(-20, 20, d))
+    h = f32_to_bf16_bits(rows)
+    assert (h[0] & 0x7F == 0x7F).all()
+    gamma = _gamma(d, 31)
+    wb = weights(rng_tree(6, 1)[0], n, d)
+    assert P.gemm_plan("hif4", m, n, d, True)["ksplit"] > 1
+    for fmt in FMTS:
+        y, y_ref, _ = _run(h, gamma, 1e-6, fmt, "2:4", n, wb)
+        assert np.array_equal(y.view(np.uint32), y_ref.view(np.uint32)), fmt
