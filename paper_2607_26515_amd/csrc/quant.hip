@@ -624,7 +624,7 @@ __device__ __forceinline__ void residual_frag_tile(
         // the keys its passes decode from these codes (one float32 per value)
 #pragma unroll
         for (int i = 0; i < 8; ++i)
-          hist_add(ehist_lds, (__float_as_uint(val[i]) >> 23) & 255u, row < m && col0 < d);
+          hist_add_copies(ehist_lds, 256, (__float_as_uint(val[i]) >> 23) & 255u, row < m && col0 < d);
       }
     } else {
       store_record8<FMT>(fr, fsr, rec, s, code, scale_byte, c1, b);
@@ -643,10 +643,10 @@ __global__ __launch_bounds__(256) void residual_frag_kernel(
     uint8_t* __restrict__ fx, uint8_t* __restrict__ fsx, uint8_t* __restrict__ fr,
     uint8_t* __restrict__ fsr, double* __restrict__ partials, uint32_t* __restrict__ ehist,
     int nm_keep, Producer prod) {
-  __shared__ uint32_t lh[MODE == kResidDense ? 256 : 1];
+  __shared__ uint32_t lh[MODE == kResidDense ? kLdsCopies * 257 : 1];  // hist.h copies of 256 bins
   const bool counting = MODE == kResidDense && ehist != nullptr;
   if (counting) {
-    lh[threadIdx.x] = 0u;  // 256 threads
+    for (int i = threadIdx.x; i < kLdsCopies * 257; i += 256) lh[i] = 0u;
     __syncthreads();
   }
   const int64_t mtiles = (m + 31) / 32;
@@ -655,7 +655,7 @@ __global__ __launch_bounds__(256) void residual_frag_kernel(
                                                prod, t, blockIdx.x, counting ? lh : nullptr);
   if (counting) {
     __syncthreads();
-    const uint32_t c = lh[threadIdx.x];
+    const uint32_t c = hist_sum_copies(lh, 256, threadIdx.x);
     const uint32_t wg = blockIdx.y * gridDim.x + blockIdx.x;
     if (c) atomicAdd(&ehist[(wg % kElemHistCopies) * kElemHistBins + threadIdx.x], c);
   }

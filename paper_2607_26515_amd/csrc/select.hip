@@ -667,7 +667,9 @@ __global__ __launch_bounds__(kThreads) void uhist_kernel(const uint8_t* __restri
                                                          uint32_t* __restrict__ hist,
                                                          uint32_t* __restrict__ super_counts,
                                                          uint32_t* __restrict__ tie_counts) {
+  constexpr int NB = PASS == 0 ? 256 : 64, OFF = PASS == 0 ? 0 : 256;
   __shared__ uint32_t lh[kUHist];
+  __shared__ uint32_t lc[kLdsCopies * (NB + 1)];  // this workgroup's counts (hist.h copies)
   __shared__ uint32_t ch[4];
   __shared__ uint32_t wsum[kThreads / 64];
   const int tid = threadIdx.x;
@@ -679,9 +681,8 @@ __global__ __launch_bounds__(kThreads) void uhist_kernel(const uint8_t* __restri
   if constexpr (PASS == 1) {
     load_choice(hist, lh, keep, false, wsum, ch);
     want = ch[0];
-    __syncthreads();  // lh is cleared below
   }
-  for (int i = tid; i < kUHist; i += kThreads) lh[i] = 0;
+  for (int i = tid; i < kLdsCopies * (NB + 1); i += kThreads) lc[i] = 0;
   __syncthreads();
   uint32_t key[32];
   if (in) thread_keys<FMT>(tw, key);
@@ -690,13 +691,12 @@ __global__ __launch_bounds__(kThreads) void uhist_kernel(const uint8_t* __restri
     for (int e = 0; e < 32; ++e) key[e] = 0;
 #pragma unroll
   for (int e = 0; e < 32; ++e) {
-    if constexpr (PASS == 0) hist_add(lh, key[e] >> 23, in);
-    else hist_add(lh, (key[e] >> 17) & 63u, in && (key[e] >> 23) == want);
+    if constexpr (PASS == 0) hist_add_copies(lc, NB, key[e] >> 23, in);
+    else hist_add_copies(lc, NB, (key[e] >> 17) & 63u, in && (key[e] >> 23) == want);
   }
   __syncthreads();
-  constexpr int NB = PASS == 0 ? 256 : 64, OFF = PASS == 0 ? 0 : 256;
   for (int b = tid; b < NB; b += kThreads) {
-    const uint32_t c = lh[b];  // local bins 0 .. NB-1 (both passes)
+    const uint32_t c = hist_sum_copies(lc, NB, b);  // local bins 0 .. NB-1 (both passes)
     if (c) atomicAdd(&hist[(blockIdx.x % kHistCopies) * kUHist + OFF + b], c);
     if constexpr (PASS == 1) {
       tie_counts[(size_t)blockIdx.x * kMantBins + b] = c;
