@@ -231,15 +231,16 @@ __device__ __forceinline__ void choose_digit(const uint32_t* hist, int nb, uint3
   __syncthreads();
 }
 
-// Radix digit choice by one wave over a 256-bin histogram: the digit holding the k-th
-// largest key (k >= 1; k = 0 picks the top digit), k's rank among the keys with that digit,
-// and that digit's count, to out[0..2].  Lane l holds bins 255 - 4l .. 252 - 4l.
+// Radix digit choice by one wave over a 256-bin histogram (hist.h copies, summed here): the
+// digit holding the k-th largest key (k >= 1; k = 0 picks the top digit), k's rank among the
+// keys with that digit, and that digit's count, to out[0..2].  Lane l holds bins 255 - 4l ..
+// 252 - 4l.
 __device__ __forceinline__ void choose_digit_wave(const uint32_t* hist, uint32_t k, uint32_t* out) {
   const int lane = threadIdx.x & 63;
   uint32_t v[4], sum = 0;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    v[e] = hist[255 - 4 * lane - e];
+    v[e] = hist_sum_copies(hist, 256, 255 - 4 * lane - e);
     sum += v[e];
   }
   uint32_t incl = sum;
@@ -282,7 +283,8 @@ __global__ __launch_bounds__(kSelThreads) void select_top_kernel(const uint64_t*
   static_assert(BP == 0 || KPT == 1, "block keys are summed at load one per thread");
   constexpr int kKeysPerThread = KPT;
   constexpr int NW = kSelThreads / 64;
-  __shared__ uint32_t hists[2][256];  // pass p counts into hists[p & 1] while the other is cleared
+  constexpr int HW = kLdsCopies * 257;  // one pass's histogram: hist.h copies of 256 bins
+  __shared__ uint32_t hists[2][HW];  // pass p counts into hists[p & 1] while the other is cleared
   __shared__ uint32_t ch[3];
   __shared__ uint32_t tcnt[kKeysPerThread][NW];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -330,7 +332,7 @@ __global__ __launch_bounds__(kSelThreads) void select_top_kernel(const uint64_t*
   uint64_t prefix = kand & above, mask = above;
   uint32_t krem = (uint32_t)k;
   bool single = false;
-  if (tid < 512) hists[tid >> 8][tid & 255] = 0;
+  for (int i = tid; i < 2 * HW; i += kSelThreads) hists[i / HW][i % HW] = 0;
   __syncthreads();
   // Two barriers per pass: after the counts, and after the digit choice (which one wave makes
   // with a wave scan, while other threads clear the next pass's histogram).
@@ -339,19 +341,20 @@ __global__ __launch_bounds__(kSelThreads) void select_top_kernel(const uint64_t*
     uint32_t* hist = hists[pass & 1];
     if (compact) {
       const uint64_t c = tid < (int)nc ? cand[tid] : 0;
-      hist_add(hist, (uint32_t)((c >> shift) & 255u), tid < (int)nc && (c & mask) == prefix);
+      hist_add_copies(hist, 256, (uint32_t)((c >> shift) & 255u), tid < (int)nc && (c & mask) == prefix);
     } else {
 #pragma unroll
       for (int q = 0; q < kKeysPerThread; ++q) {
         const int64_t i = (int64_t)q * kSelThreads + tid;
-        hist_add(hist, (uint32_t)((kr[q] >> shift) & 255u), i < n && (kr[q] & mask) == prefix);
+        hist_add_copies(hist, 256, (uint32_t)((kr[q] >> shift) & 255u), i < n && (kr[q] & mask) == prefix);
       }
     }
     __syncthreads();
     if (wave == 0) {
       choose_digit_wave(hist, krem, ch);
-    } else if (tid >= 64 && tid < 64 + 256) {
-      hists[(pass + 1) & 1][tid - 64] = 0;  // read by no one since the previous pass's choice
+    } else {
+      for (int i = tid - 64; i < HW; i += kSelThreads - 64)
+        hists[(pass + 1) & 1][i] = 0;  // read by no one since the previous pass's choice
     }
     __syncthreads();
     prefix |= (uint64_t)ch[0] << shift;
