@@ -17,8 +17,9 @@ constexpr int kElemHistCopies = 8;
 // copy c at c * (nb + 1) (so that the copies of one bin lie in different banks), lane l adding
 // into copy l % kLdsCopies with one plain LDS atomic per element.  A counting pass's keys
 // fall into a few bins; on one address the atomics of a wave serialize, and the copies cut
-// that chain eight-fold (measured: the mantissa pass at m = 512, d = 3584 took 11.2 us with
-// the leader-based hist_add below and 5.8 us this way).  Readers sum the copies.
+// that chain eight-fold (measured: the mantissa pass at m = 512, d = 3584 took 11.2 us with a
+// wave-level add that counted the lanes sharing a leader's digit with one atomic, 5.8 us this
+// way).  Readers sum the copies.
 constexpr int kLdsCopies = 8;
 __device__ __forceinline__ void hist_add_copies(uint32_t* h, int nb, uint32_t digit, bool active) {
   if (active) atomicAdd(&h[(threadIdx.x % kLdsCopies) * (nb + 1) + digit], 1u);
@@ -28,24 +29,6 @@ __device__ __forceinline__ uint32_t hist_sum_copies(const uint32_t* h, int nb, i
 #pragma unroll
   for (int c = 0; c < kLdsCopies; ++c) v += h[c * (nb + 1) + bin];
   return v;
-}
-
-// h[digit] += 1 for every active lane of the wave.  The lanes sharing the digit of the first
-// two leaders are counted with one LDS atomic each (the keys of a selection pass often share
-// a digit, and per-lane atomics on one address serialize); the rest add one by one.  Every
-// lane of the wave must call this (the digit and active flag may differ per lane).
-__device__ __forceinline__ void hist_add(uint32_t* h, uint32_t digit, bool active) {
-  uint64_t pending = __ballot(active);
-#pragma unroll
-  for (int it = 0; it < 2; ++it) {
-    if (pending == 0) return;
-    const int leader = __ffsll((unsigned long long)pending) - 1;
-    const uint32_t dl = __shfl(digit, leader, 64);
-    const uint64_t same = __ballot(digit == dl) & pending;
-    if (__lane_id() == leader) atomicAdd(&h[dl], (uint32_t)__popcll(same));
-    pending &= ~same;
-  }
-  if ((pending >> __lane_id()) & 1ull) atomicAdd(&h[digit], 1u);
 }
 
 }  // namespace resq

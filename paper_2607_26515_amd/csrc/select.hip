@@ -464,7 +464,8 @@ __global__ __launch_bounds__(kSelThreads) void select_top_stream_kernel(const ui
                                                                         uint8_t* __restrict__ bits,
                                                                         uint8_t* __restrict__ bits_copy) {
   constexpr int NW = kSelThreads / 64;
-  __shared__ uint32_t hist[256];
+  __shared__ uint32_t hc[kLdsCopies * 257];  // hist.h copies of the pass's 256 bins
+  __shared__ uint32_t hist[256];             // their sums
   __shared__ uint32_t ch[2];
   __shared__ uint32_t wsum[NW];
   __shared__ uint64_t found;
@@ -472,13 +473,15 @@ __global__ __launch_bounds__(kSelThreads) void select_top_stream_kernel(const ui
   uint64_t prefix = 0, mask = 0;
   uint32_t krem = (uint32_t)k;
   for (int shift = 56; shift >= 0; shift -= 8) {
-    if (tid < 256) hist[tid] = 0;
+    for (int i = tid; i < kLdsCopies * 257; i += kSelThreads) hc[i] = 0;
     __syncthreads();
     for (int64_t base = 0; base < n; base += kSelThreads) {
       const int64_t i = base + tid;
       const uint64_t key = i < n ? keys[i] : 0;
-      hist_add(hist, (uint32_t)((key >> shift) & 255u), i < n && (key & mask) == prefix);
+      hist_add_copies(hc, 256, (uint32_t)((key >> shift) & 255u), i < n && (key & mask) == prefix);
     }
+    __syncthreads();
+    if (tid < 256) hist[tid] = hist_sum_copies(hc, 256, tid);
     __syncthreads();
     choose_digit<kSelThreads>(hist, 256, krem, wsum, ch);
     prefix |= (uint64_t)ch[0] << shift;
