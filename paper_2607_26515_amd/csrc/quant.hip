@@ -437,8 +437,9 @@ __device__ float sqrt_rn_f32(float t) {
 
 // A bf16 value is M * 2^(E - 134) with M < 2^8 (E = the exponent field, 1 for subnormals), so
 // its square is M^2 * 2^(2E - 268).  One row's squares are added as integers per exponent
-// field (per-wave LDS histograms, at most 2^16 * (d / 4 + 512) < 2^32 per wave and bin for
-// d <= 2^18), the 255 bin totals are added into an integer of kRmsLimbs 32-bit limbs in
+// field (LDS histograms in kLdsCopies per-lane copies, hist.h; a copy's bin gets at most
+// d / 8 squares below 2^16, under 2^32 for d <= 2^18), the 255 bin totals are added into an
+// integer of kRmsLimbs 32-bit limbs in
 // units of 2^-268 (bin E at bit 2E, below 2^(2 * 255 + 34) < 2^(32 * kRmsLimbs)), and that
 // exact sum is rounded once: to 53 bits by truncation with the sticky lowest bit (round to
 // odd), then to float32 to nearest even, which gives the float32 nearest to the exact sum
@@ -485,12 +486,12 @@ template <bool VEC>
 __global__ __launch_bounds__(256) void rms_rows_kernel(const uint16_t* __restrict__ H, int64_t m,
                                                         int64_t d, int64_t ldh, float eps,
                                                         float* __restrict__ rinv) {
-  __shared__ uint32_t wh[4][256];
+  __shared__ uint32_t wh[kLdsCopies * 257];
   __shared__ unsigned long long limb[kRmsLimbs];
-  const int tid = threadIdx.x, wave = tid >> 6;
+  const int tid = threadIdx.x;
+  uint32_t* hc = wh + (tid % kLdsCopies) * 257;  // this lane's copy
   for (int64_t row = blockIdx.x; row < m; row += gridDim.x) {
-#pragma unroll
-    for (int w = 0; w < 4; ++w) wh[w][tid] = 0u;
+    for (int i = tid; i < kLdsCopies * 257; i += 256) wh[i] = 0u;
     if (tid < kRmsLimbs) limb[tid] = 0ull;
     __syncthreads();
     const uint16_t* src = H + row * ldh;
@@ -509,12 +510,14 @@ __global__ __launch_bounds__(256) void rms_rows_kernel(const uint16_t* __restric
       for (int i = 0; i < 8; ++i) {
         const uint32_t e = (b[i] >> 7) & 0xFFu;
         const uint32_t mant = (b[i] & 0x7Fu) | (e ? 0x80u : 0u);
-        if (mant) atomicAdd(&wh[wave][e ? e : 1u], mant * mant);
+        if (mant) atomicAdd(&hc[e ? e : 1u], mant * mant);
       }
     }
     __syncthreads();
     // bin tid (0 .. 255) at bit 2 * tid: three 32-bit pieces into three limbs
-    const unsigned long long T = (unsigned long long)wh[0][tid] + wh[1][tid] + wh[2][tid] + wh[3][tid];
+    unsigned long long T = 0;  // up to 2^18 squares below 2^16: 64-bit
+#pragma unroll
+    for (int c = 0; c < kLdsCopies; ++c) T += wh[c * 257 + tid];
     if (T) {
       const int off = 2 * tid, L = off >> 5, sh = off & 31;
       const unsigned long long lo = (T & 0xFFFFFFFFull) << sh, hi = (T >> 32) << sh;
