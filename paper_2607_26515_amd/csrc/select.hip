@@ -638,32 +638,68 @@ __device__ __forceinline__ void thread_keys(const ThreadWords& t, uint32_t key[3
   word_keys<FMT>(t.cw.w, t.sc, t.jpos + 24, key + 24);
 }
 
-// Load the histograms into LDS and resolve the threshold (all threads call this): out[0] =
-// exponent digit, out[1] = rank within it; with full, out[2] = threshold key T and out[3] =
-// the number of keys equal to T that are kept.
-__device__ __forceinline__ void load_choice(const uint32_t* hist, uint32_t* lh, uint32_t k, bool full,
-                                            uint32_t* wsum, uint32_t* out) {
-  for (int i = threadIdx.x; i < kUHist; i += blockDim.x) {
-    uint32_t v = 0;
-#pragma unroll 8
-    for (int c = 0; c < kHistCopies; ++c) v += hist[c * kUHist + i];
-    lh[i] = v;
-  }
-  __syncthreads();
-  choose_digit<kThreads>(lh, 256, k, wsum, out);
-  if (full) {
-    const uint32_t de = out[0], ke = out[1];
-    __syncthreads();
-    choose_digit<kThreads>(lh + 256, 64, ke, wsum, out + 2);
-    const uint32_t dm = out[2];
-    __syncthreads();
-    if (threadIdx.x == 0) {
+// Resolve the threshold from the global histogram (all threads call this; wave 0 reads the
+// histogram, summing its copies, and scans it, one barrier for the rest): out[0] = exponent
+// digit, out[1] = rank within it; with full, out[2] = threshold key T and out[3] = the number
+// of keys equal to T that are kept.  Lane l holds exponent bins 255 - 4l .. 252 - 4l and
+// mantissa bin 63 - l, each digit chosen as by a scan from the top bin down.
+__device__ __forceinline__ void load_choice(const uint32_t* hist, uint32_t k, bool full, uint32_t* out) {
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    uint32_t v[4] = {0u, 0u, 0u, 0u}, mv = 0u;
+#pragma unroll
+    for (int c = 0; c < kHistCopies; ++c) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] += hist[c * kUHist + 255 - 4 * lane - e];
+      if (full) mv += hist[c * kUHist + 256 + 63 - lane];
+    }
+    // exponent digit: the bin holding the k-th largest key (k = 0: the top bin)
+    const uint32_t sum = v[0] + v[1] + v[2] + v[3];
+    uint32_t incl = sum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t y = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += y;
+    }
+    uint32_t above = incl - sum, de = 0, ke = 0;
+    bool found = false;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if ((above < k && k <= above + v[e]) || (k == 0 && lane == 0 && e == 0)) {
+        de = (uint32_t)(255 - 4 * lane - e);
+        ke = k - above;
+        found = true;
+      }
+      above += v[e];
+    }
+    uint64_t who = __ballot(found);
+    int src = who ? __ffsll((unsigned long long)who) - 1 : 0;
+    de = __shfl(de, src, 64);
+    ke = __shfl(ke, src, 64);
+    if (full) {
+      // mantissa digit among the keys of exponent de, for rank ke
+      uint32_t mincl = mv;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_up(mincl, o, 64);
+        if (lane >= o) mincl += y;
+      }
+      const uint32_t mabove = mincl - mv;
+      const bool hit = (mabove < ke && ke <= mabove + mv) || (ke == 0 && lane == 0);
+      who = __ballot(hit);
+      src = who ? __ffsll((unsigned long long)who) - 1 : 0;
+      const uint32_t dm = (uint32_t)(63 - src), krem = __shfl(ke - mabove, src, 64);
+      if (lane == 0) {
+        out[2] = (de << 23) | (dm << 17);
+        out[3] = krem;
+      }
+    }
+    if (lane == 0) {
       out[0] = de;
       out[1] = ke;
-      out[2] = (de << 23) | (dm << 17);
     }
-    __syncthreads();
   }
+  __syncthreads();
 }
 
 template <int FMT, int PASS>
@@ -674,10 +710,8 @@ __global__ __launch_bounds__(kThreads) void uhist_kernel(const uint8_t* __restri
                                                          uint32_t* __restrict__ super_counts,
                                                          uint32_t* __restrict__ tie_counts) {
   constexpr int NB = PASS == 0 ? 256 : 64, OFF = PASS == 0 ? 0 : 256;
-  __shared__ uint32_t lh[kUHist];
   __shared__ uint32_t lc[kLdsCopies * (NB + 1)];  // this workgroup's counts (hist.h copies)
   __shared__ uint32_t ch[4];
-  __shared__ uint32_t wsum[kThreads / 64];
   const int tid = threadIdx.x;
   const int64_t w0 = ((int64_t)blockIdx.x * kThreads + tid) * kWordsPerThread;
   const bool in = w0 < m * (d / 8);
@@ -685,7 +719,7 @@ __global__ __launch_bounds__(kThreads) void uhist_kernel(const uint8_t* __restri
   if (in) tw = thread_words<FMT>(codes, scales, d, w0);
   uint32_t want = 0;
   if constexpr (PASS == 1) {
-    load_choice(hist, lh, keep, false, wsum, ch);
+    load_choice(hist, keep, false, ch);
     want = ch[0];
   }
   for (int i = tid; i < kLdsCopies * (NB + 1); i += kThreads) lc[i] = 0;
@@ -726,14 +760,13 @@ __global__ __launch_bounds__(kThreads) void uapply_kernel(uint8_t* __restrict__ 
                                                           uint8_t* __restrict__ keep_mask,
                                                           uint8_t* __restrict__ frag,
                                                           uint8_t* __restrict__ fscale) {
-  __shared__ uint32_t lh[kUHist];
   __shared__ uint32_t ch[4];
   __shared__ uint32_t wsum[kThreads / 64];
   const int64_t w0 = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * kWordsPerThread;
   const bool in = w0 < m * (d / 8);
   ThreadWords tw{};
   if (in) tw = thread_words<FMT>(codes, scales, d, w0);
-  load_choice(hist, lh, keep, true, wsum, ch);
+  load_choice(hist, keep, true, ch);
   const uint32_t T = ch[2], krem = ch[3];
   // ties of earlier workgroups: whole groups of kSuper workgroups, then this group's earlier
   // ones, from the second pass's counts of T's mantissa pattern
