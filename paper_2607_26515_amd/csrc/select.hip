@@ -190,21 +190,21 @@ __global__ __launch_bounds__(kThreads) void block_keys_kernel(const double* __re
 // ---------------------------------------------------------------------------------------
 // Workgroup-wide exclusive scan of one uint32 per thread (any multiple of 64 threads).
 // ---------------------------------------------------------------------------------------
-template <int NT>
-__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* wsum, uint32_t& total) {
+template <int NT, typename T = uint32_t>
+__device__ __forceinline__ T block_exclusive_scan(T v, T* wsum, T& total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  uint32_t x = v;
+  T x = v;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t y = __shfl_up(x, o, 64);
+    const T y = __shfl_up(x, o, 64);
     if (lane >= o) x += y;
   }
   if (lane == 63) wsum[wave] = x;
   __syncthreads();
-  uint32_t before = 0, all = 0;
+  T before = 0, all = 0;
 #pragma unroll
   for (int w = 0; w < NT / 64; ++w) {
-    const uint32_t s = wsum[w];
+    const T s = wsum[w];
     if (w < wave) before += s;
     all += s;
   }
@@ -717,13 +717,14 @@ __global__ __launch_bounds__(kThreads) void uhist_kernel(const uint8_t* __restri
   const bool in = w0 < m * (d / 8);
   ThreadWords tw{};
   if (in) tw = thread_words<FMT>(codes, scales, d, w0);
+  for (int i = tid; i < kLdsCopies * (NB + 1); i += kThreads) lc[i] = 0;
   uint32_t want = 0;
   if constexpr (PASS == 1) {
-    load_choice(hist, keep, false, ch);
+    load_choice(hist, keep, false, ch);  // its barrier also ends the clearing
     want = ch[0];
+  } else {
+    __syncthreads();
   }
-  for (int i = tid; i < kLdsCopies * (NB + 1); i += kThreads) lc[i] = 0;
-  __syncthreads();
   uint32_t key[32];
   if (in) thread_keys<FMT>(tw, key);
   else
@@ -761,7 +762,7 @@ __global__ __launch_bounds__(kThreads) void uapply_kernel(uint8_t* __restrict__ 
                                                           uint8_t* __restrict__ frag,
                                                           uint8_t* __restrict__ fscale) {
   __shared__ uint32_t ch[4];
-  __shared__ uint32_t wsum[kThreads / 64];
+  __shared__ uint64_t wsum[kThreads / 64];
   const int64_t w0 = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * kWordsPerThread;
   const bool in = w0 < m * (d / 8);
   ThreadWords tw{};
@@ -775,8 +776,6 @@ __global__ __launch_bounds__(kThreads) void uapply_kernel(uint8_t* __restrict__ 
   for (uint32_t w = threadIdx.x; w < sb * kSuperCopies; w += kThreads) before += super_counts[w * kMantBins + tm];
   for (uint32_t w = sb * kSuper + threadIdx.x; w < blockIdx.x; w += kThreads)
     before += tie_counts[(size_t)w * kMantBins + tm];
-  uint32_t tot_before;
-  block_exclusive_scan<kThreads>(before, wsum, tot_before);
   uint32_t key[32];
   uint32_t ties = 0;
   if (in) {
@@ -784,8 +783,12 @@ __global__ __launch_bounds__(kThreads) void uapply_kernel(uint8_t* __restrict__ 
 #pragma unroll
     for (int e = 0; e < 32; ++e) ties += key[e] == T;
   }
-  uint32_t total;
-  uint32_t rank = tot_before + block_exclusive_scan<kThreads>(ties, wsum, total);
+  // one scan for both: this workgroup's ties in the low half (their exclusive prefix ranks
+  // this thread's ties; at most 8192, no carry), the earlier workgroups' in the high half
+  // (only their total is needed; at most m d <= 2^31)
+  uint64_t total;
+  const uint64_t pre = block_exclusive_scan<kThreads, uint64_t>(((uint64_t)before << 32) | ties, wsum, total);
+  uint32_t rank = (uint32_t)(total >> 32) + (uint32_t)pre;
   if (!in) return;
   uint32_t kept = 0;  // 32 keep bits
 #pragma unroll
