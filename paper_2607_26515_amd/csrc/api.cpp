@@ -402,13 +402,15 @@ int linear_fwd_core(int format, const Sp& sp, const uint16_t* X, int64_t m, int6
       resq::ProfScope prof_(resq::kProfResidual, s, true);
       const bool elem = sp.kind == RESQ_S_UNSTRUCT50;
       if (elem) resq::launch_select_clear(w.sel, m, d, s);  // the residual pass counts into it
+      // the block kind: the pass writes the block keys, which the top-k then ranks directly
+      const bool block = sp.kind == RESQ_S_BLOCK32X64_50;
       resq::launch_residual(format, resq::kResidDense, X, m, d, ldx, w.frag_x, w.fsc_x, w.qr_codes,
-                            w.qr_scales, nullptr, sp.kind == RESQ_S_BLOCK32X64_50 ? w.partials : nullptr,
-                            s, true, elem ? w.sel.hist : nullptr, 2, prod);
+                            w.qr_scales, nullptr, nullptr, s, true, elem ? w.sel.hist : nullptr, 2, prod,
+                            block ? w.sel.keys : nullptr);
     }
     resq::ProfScope prof_(resq::kProfSelect, s);
     resq::launch_select_frag(format, sp.kind, m, d, keep_count(sp, m, d), w.qr_codes, w.qr_scales,
-                             w.partials, w.sel, a_pack_mode(format), w.frag_r, w.fsc_r, s);
+                             nullptr, w.sel, a_pack_mode(format), w.frag_r, w.fsc_r, s);
   } else {
     // local kinds: the residual pass writes the MFMA fragments directly
     resq::ProfScope prof_(resq::kProfResidual, s, true);

@@ -64,12 +64,15 @@ void launch_rms_rows(const uint16_t* H, int64_t m, int64_t d, int64_t ldh, float
 // K-major codes + scales: for both Q(X) and Q(dX) with the local kinds; with kResidDense
 // Q(X) as fragments and Q(dX) K-major (qr_codes, qr_scales) for the selection that follows,
 // and, with ehist (the element-wise selection's histogram, cleared beforehand by
-// launch_select_clear), the exponent histogram of |Q(dX)|.  keep_mask is ignored when frag is
-// set.
+// launch_select_clear), the exponent histogram of |Q(dX)|; with bkeys (frag and kResidDense,
+// d % 64 == 0) the keys of the 32 x 64 blocks, summed as the block selection defines them
+// (ceil(m / 32) x d / 64 doubles, block (I, J) at I * d / 64 + J).  keep_mask is ignored when
+// frag is set.
 void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
                      uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes, void* qr_scales,
                      uint8_t* keep_mask, double* partials, hipStream_t s, bool frag = false,
-                     uint32_t* ehist = nullptr, int nm_keep = 2, const Producer* prod = nullptr);
+                     uint32_t* ehist = nullptr, int nm_keep = 2, const Producer* prod = nullptr,
+                     double* bkeys = nullptr);
 
 // MFMA operand packing (pack.hip): K-major codes + scales -> fragment-major operands.
 enum PackMode { kPackMx = 0, kPackHiA = 1, kPackHiB = 2 };
@@ -101,7 +104,8 @@ void launch_select(int fmt, int sparsity, int64_t m, int64_t d, int64_t keep, ui
                    uint8_t* group_mask, const SelectWs& ws, hipStream_t s);
 // The same selections for the forward GEMM: S(Q(dX)) is written as fragment-major operand
 // records (PackMode pack_mode) to frag / fscale; the K-major codes are left unpruned and no
-// masks are written.  For the element-wise kind the histogram (select_hist_words(m, d) words at
+// masks are written.  Block kind with partials = null: the residual pass has written the
+// block keys to ws.keys.  For the element-wise kind the histogram (select_hist_words(m, d) words at
 // ws.hist) must have been cleared (launch_select_clear) before the residual pass, which fills
 // its exponent bins.
 void launch_select_frag(int fmt, int sparsity, int64_t m, int64_t d, int64_t keep, uint8_t* qr_codes,

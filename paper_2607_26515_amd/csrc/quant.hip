@@ -292,7 +292,8 @@ __device__ __forceinline__ void store_kmajor8(uint8_t* __restrict__ codes, uint8
                                               double* __restrict__ partials, bool in, int64_t row,
                                               int64_t d, int64_t kb, int half, int s,
                                               const uint32_t code[8], const float val[8],
-                                              uint32_t scale_byte, const int b[2], int b2) {
+                                              uint32_t scale_byte, const int b[2], int b2,
+                                              double* __restrict__ rowsq = nullptr) {
   const int64_t col0 = kb * 64 + 32 * half + 8 * s;
   uint32_t w = 0;
 #pragma unroll
@@ -307,6 +308,7 @@ __device__ __forceinline__ void store_kmajor8(uint8_t* __restrict__ codes, uint8
       scales[row * (d / 32) + kb * 2 + half] = (uint8_t)scale_byte;
       if (partials) partials[row * (d / 32) + kb * 2 + half] = sq;
     }
+    if (rowsq && s == 0) rowsq[half] = in ? sq : 0.0;  // this row's sum of scale block `half`
   } else {
     const int base = __lane_id() & ~7;  // the row's 8 lanes
     const uint32_t bits2 = (uint32_t)(__ballot(b2 != 0) >> base) & 0xFFu;
@@ -318,6 +320,7 @@ __device__ __forceinline__ void store_kmajor8(uint8_t* __restrict__ codes, uint8
       reinterpret_cast<uint32_t*>(scales)[row * (d / 64) + kb] = meta;
       if (partials) partials[row * (d / 64) + kb] = sq;
     }
+    if (rowsq && half == 0 && s == 0) rowsq[0] = in ? sq : 0.0;  // this row's sum of the 64-block
   }
 }
 
@@ -565,7 +568,7 @@ __device__ __forceinline__ void residual_frag_tile(
     const uint16_t* __restrict__ X, int64_t m, int64_t d, int64_t ldx, int64_t nkb,
     uint8_t* __restrict__ fx, uint8_t* __restrict__ fsx, uint8_t* __restrict__ fr,
     uint8_t* __restrict__ fsr, double* __restrict__ partials, int nm_keep, const Producer& prod,
-    int64_t t, int64_t kb, uint32_t* ehist_lds) {
+    int64_t t, int64_t kb, uint32_t* ehist_lds, double* rowsq_lds, double* __restrict__ bkeys) {
   const int64_t f = t * nkb + kb;  // fragment index
   const int tid = threadIdx.x;
   const int rr = tid >> 3, half = (tid >> 2) & 1, s = tid & 3;
@@ -621,7 +624,21 @@ __device__ __forceinline__ void residual_frag_tile(
     }
     if constexpr (MODE == kResidDense) {
       store_kmajor8<FMT>(fr, fsr, partials, row < m && col0 < d, row, d, kb, half, s, code, val,
-                         scale_byte, b, b2);
+                         scale_byte, b, b2, bkeys ? rowsq_lds + 2 * rr : nullptr);
+      if (bkeys) {  // workgroup-uniform
+        // the key of 32 x 64 block (t, kb): its rows' scale-block sums, rows in order, scale
+        // blocks in column order (the order the selection defines)
+        __syncthreads();
+        if (threadIdx.x == 0) {
+          double acc = 0.0;
+          for (int i = 0; i < 32; ++i)
+            if (t * 32 + i < m)
+#pragma unroll
+              for (int q = 0; q < (FMT == kMX ? 2 : 1); ++q) acc += rowsq_lds[2 * i + q];
+          bkeys[t * (d / 64) + kb] = acc;
+        }
+        __syncthreads();  // the row sums are overwritten by the next row tile
+      }
       if (ehist_lds) {  // workgroup-uniform
         // the element-wise selection's first histogram: exponent fields of |Q(dX)|, exactly
         // the keys its passes decode from these codes (one float32 per value)
@@ -639,14 +656,16 @@ __device__ __forceinline__ void residual_frag_tile(
 // fr / fsr receive the K-major Q(dX) codes and scales and `partials` its per-scale-block
 // sums of squares (may be null); with ehist (element-wise selection, cleared beforehand) the
 // workgroup also counts the exponent fields of |Q(dX)| and adds them into copy
-// (workgroup % kElemHistCopies) of that histogram.
+// (workgroup % kElemHistCopies) of that histogram; with bkeys (block selection) it writes the
+// key of each 32 x 64 block it covers (d % 64 == 0).
 template <int FMT, int MODE, bool VEC, int PROD>
 __global__ __launch_bounds__(256) void residual_frag_kernel(
     const uint16_t* __restrict__ X, int64_t m, int64_t d, int64_t ldx, int64_t nkb,
     uint8_t* __restrict__ fx, uint8_t* __restrict__ fsx, uint8_t* __restrict__ fr,
     uint8_t* __restrict__ fsr, double* __restrict__ partials, uint32_t* __restrict__ ehist,
-    int nm_keep, Producer prod) {
+    int nm_keep, Producer prod, double* __restrict__ bkeys) {
   __shared__ uint32_t lh[MODE == kResidDense ? kLdsCopies * 257 : 1];  // hist.h copies of 256 bins
+  __shared__ double rowsq[MODE == kResidDense ? 64 : 1];  // block keys: the tile's row sums
   const bool counting = MODE == kResidDense && ehist != nullptr;
   if (counting) {
     for (int i = threadIdx.x; i < kLdsCopies * 257; i += 256) lh[i] = 0u;
@@ -655,7 +674,8 @@ __global__ __launch_bounds__(256) void residual_frag_kernel(
   const int64_t mtiles = (m + 31) / 32;
   for (int64_t t = blockIdx.y; t < mtiles; t += gridDim.y)
     residual_frag_tile<FMT, MODE, VEC, PROD>(X, m, d, ldx, nkb, fx, fsx, fr, fsr, partials, nm_keep,
-                                               prod, t, blockIdx.x, counting ? lh : nullptr);
+                                               prod, t, blockIdx.x, counting ? lh : nullptr, rowsq,
+                                               MODE == kResidDense ? bkeys : nullptr);
   if (counting) {
     __syncthreads();
     const uint32_t c = hist_sum_copies(lh, 256, threadIdx.x);
@@ -849,7 +869,7 @@ void launch_rms_rows(const uint16_t* H, int64_t m, int64_t d, int64_t ldh, float
 void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d, int64_t ldx,
                      uint8_t* qx_codes, void* qx_scales, uint8_t* qr_codes, void* qr_scales,
                      uint8_t* keep_mask, double* partials, hipStream_t s, bool frag,
-                     uint32_t* ehist, int nm_keep, const Producer* prod) {
+                     uint32_t* ehist, int nm_keep, const Producer* prod, double* bkeys) {
   if (m == 0 || d == 0) return;
   if (frag) {
     const int64_t nkb = (d + 63) / 64;
@@ -860,7 +880,7 @@ void launch_residual(int fmt, int mode, const uint16_t* X, int64_t m, int64_t d,
     const bool vec16 = prod ? ((uintptr_t)pr.g % 16 == 0 && (uintptr_t)pr.u % 16 == 0 &&
                                pr.ldg % ve == 0 && pr.ldu % ve == 0)
                             : ((uintptr_t)X % 16 == 0 && ldx % 8 == 0);
-#define RESQ_RF(F, M, V, P) launch_timed(residual_frag_kernel<F, M, V, P>, grid, dim3(256), 0u, s, X, m, d, ldx, nkb, qx_codes, (uint8_t*)qx_scales, qr_codes, (uint8_t*)qr_scales, partials, ehist, nm_keep, pr)
+#define RESQ_RF(F, M, V, P) launch_timed(residual_frag_kernel<F, M, V, P>, grid, dim3(256), 0u, s, X, m, d, ldx, nkb, qx_codes, (uint8_t*)qx_scales, qr_codes, (uint8_t*)qr_scales, partials, ehist, nm_keep, pr, bkeys)
 #define RESQ_RF_MODE(F, V, P)                                        \
     switch (mode) {                                                  \
       case kResidNone: RESQ_RF(F, kResidNone, V, P); break;          \

@@ -913,7 +913,8 @@ void launch_select_frag(int fmt, int sparsity, int64_t m, int64_t d, int64_t kee
     if (chan) {
       launch_channel_top(fmt, qr_codes, qr_scales, m, d, keep, ws, nullptr, s);
     } else {
-      launch_block_top(fmt, partials, m, d, keep, ws, nullptr, s);
+      if (partials) launch_block_top(fmt, partials, m, d, keep, ws, nullptr, s);
+      else launch_top(ws.keys, n, keep, ws.group_bits, nullptr, s);  // keys from the residual pass
     }
     launch_pack(pack_mode, qr_codes, qr_scales, m, d, frag, fscale, s, chan ? 1 : 2, ws.group_bits);
   } else if (sparsity == 5) {
