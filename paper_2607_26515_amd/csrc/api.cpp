@@ -115,7 +115,6 @@ struct Carver {
 struct ActWs {
   uint8_t* qr_codes;  // dense K-major Q(dX) (global selections only)
   void* qr_scales;
-  double* partials;
   uint8_t* frag_x;
   uint8_t* fsc_x;
   uint8_t* frag_r;
@@ -155,10 +154,13 @@ resq::GemmOperands gemm_operands(int fmt, int64_t M, int64_t N, int64_t K, int n
   return op;
 }
 
+// partials: the block kind's per-row scale-block sums (resq_residual_sparsify; the forward's
+// residual pass writes the block keys instead and passes null).
 size_t carve_select(Carver& c, int fmt, const Sp& sp, int64_t m, int64_t d, double** partials,
                     resq::SelectWs* sel) {
   const size_t start = c.off;
-  void* part = (sp.kind == RESQ_S_BLOCK32X64_50) ? c.take((size_t)m * (d / block_of(fmt)) * 8) : nullptr;
+  void* part = (partials && sp.kind == RESQ_S_BLOCK32X64_50) ? c.take((size_t)m * (d / block_of(fmt)) * 8)
+                                                             : nullptr;
   if (partials) *partials = (double*)part;
   const size_t sb = global_kind(sp) ? resq::select_ws_bytes(sp.kind, fmt, m, d) : 0;
   void* sw = sb ? c.take(sb) : nullptr;
@@ -189,7 +191,7 @@ size_t carve_fwd(void* base, int fmt, const Sp& sp, int64_t m, int64_t d, int64_
     t.qr_codes = (uint8_t*)c.take((size_t)m * d / 2);
     t.qr_scales = c.take(scale_bytes(fmt, m, d));
   }
-  carve_select(c, fmt, sp, m, d, &t.partials, &t.sel);
+  carve_select(c, fmt, sp, m, d, nullptr, &t.sel);
   t.frag_x = (uint8_t*)c.take(resq::frag_bytes(a_pack_mode(fmt), m, d));
   t.fsc_x = (uint8_t*)c.take(resq::frag_scale_bytes(m, d));
   if (sp.kind != RESQ_S_NONE) {
@@ -324,7 +326,8 @@ size_t resq_workspace_size(int op, int format, int sparsity, int64_t m, int64_t 
   switch (op) {
     case RESQ_OP_RESIDUAL_SPARSIFY: {
       Carver c(nullptr);
-      carve_select(c, format, sp, m, d, nullptr, nullptr);
+      double* partials = nullptr;  // counted: this entry point writes the block partials
+      carve_select(c, format, sp, m, d, &partials, nullptr);
       return c.off;
     }
     case RESQ_OP_LINEAR_FWD:

@@ -229,3 +229,13 @@ def test_mixed_forms_check_arguments_on_the_host():
     assert P.resq_workspace_size(B.OP_LINEAR_W16A4, B.MXFP4, 0, 3, 96, 8) == 768
     # operand rows beyond the kernel's 32-bit offsets are refused before anything is enqueued
     assert P.resq_linear_w4a16(B.MXFP4, ptr, 4, 64, 1 << 31, ptr, ptr, 8, ptr, 8, 0) == B.ERR_UNSUPPORTED
+
+
+def test_residual_sparsify_workspace_holds_block_partials():
+    """The block kind's resq_residual_sparsify writes per-row scale-block sums (m x d / B
+    doubles) into its workspace besides the keys; the size query counts them."""
+    for fmt, blk in ((B.MXFP4, 32), (B.HIF4, 64)):
+        for m, d in ((1, 64), (100, 2048), (512, 18944)):
+            need = P.resq_workspace_size(B.OP_RESIDUAL_SPARSIFY, fmt, B.S_BLOCK32X64_50, m, d, 0)
+            nblocks = -(-m // 32) * (d // 64)
+            assert need >= m * (d // blk) * 8 + nblocks * 8, (fmt, m, d, need)
