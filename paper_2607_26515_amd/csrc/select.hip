@@ -23,35 +23,17 @@ constexpr int kThreads = 256;
 constexpr int kSelThreads = 1024;   // single-workgroup select (channel and block keys)
 constexpr int kWordsPerThread = 4;  // element-wise passes: 4 code words = 32 elements
 
-// |value| of the 8 elements of one 32-bit code word, as float32 bit patterns (all values of
-// both formats are exact in float32, denormals included).  jpos = position of the word's first
-// element inside its scale block.
-template <int FMT>
-__device__ __forceinline__ void word_keys(uint32_t cw, uint32_t scale, int jpos, uint32_t key[8]) {
-  if constexpr (FMT == 0) {
-    const uint32_t mag = cw & 0x77777777u;  // magnitudes only
-    const float sc = mx_scale_f32((int)scale - 127);
+// MXFP4: |value| of the 8 elements of one 32-bit code word, as float32 bit patterns (exact,
+// denormals included), two per hardware conversion.
+__device__ __forceinline__ void mx_word_keys(uint32_t cw, uint32_t scale, uint32_t key[8]) {
+  const uint32_t mag = cw & 0x77777777u;  // magnitudes only
+  const float sc = mx_scale_f32((int)scale - 127);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      float v0, v1;
-      mx_value2((mag >> (8 * q)) & 0xFFu, sc, v0, v1);
-      key[2 * q] = __float_as_uint(v0);
-      key[2 * q + 1] = __float_as_uint(v1);
-    }
-    return;
-  }
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const uint32_t c = (cw >> (4 * e)) & 7u;  // magnitude only
-    float v;
-    if constexpr (FMT == 0) {
-      v = mx_value(c, (int)scale - 127);
-    } else {
-      const int p = jpos + e;
-      const int b = (int)((scale >> (8 + p / 8)) & 1u) + (int)((scale >> (16 + p / 4)) & 1u);
-      v = hif4_value(c, (int)(scale & 0xFFu), b);
-    }
-    key[e] = __float_as_uint(v);
+  for (int q = 0; q < 4; ++q) {
+    float v0, v1;
+    mx_value2((mag >> (8 * q)) & 0xFFu, sc, v0, v1);
+    key[2 * q] = __float_as_uint(v0);
+    key[2 * q + 1] = __float_as_uint(v1);
   }
 }
 
@@ -630,12 +612,47 @@ __device__ __forceinline__ ThreadWords thread_words(const uint8_t* codes, const 
   return t;
 }
 
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+// HiF4 keys of word Q of a thread's four (its elements 8Q .. 8Q + 7, one level-2 group and two
+// level-3 groups): value k (4 + m) 2^(e - 35 - b).  The eight magnitudes k spread to the bytes
+// of two dwords, one 16-bit-lane multiply by 4 + m forms four products k (4 + m) <= 49 at once
+// (no carry crosses a byte), each byte converts to float32 exactly, and ldexp applies the
+// group's 2^(e - 35 - b) (exact: the smallest nonzero value, 4 * 2^-37, is normal).  f2 holds
+// 4 + m in both 16-bit lanes, e35 = e - 35; l2 and l3 are the thread's level-2 and level-3
+// shift bits, from its first group on.
+template <int Q>
+__device__ __forceinline__ void hif4_word_keys(uint32_t cw, uint32_t f2, int e35, uint32_t l2, uint32_t l3,
+                                               uint32_t key[8]) {
+  const uint32_t ta = __builtin_amdgcn_perm(cw, cw, 0x0C010C00u), tb = __builtin_amdgcn_perm(cw, cw, 0x0C030C02u);
+  const uint32_t ka = (ta | (ta << 4)) & 0x07070707u, kb = (tb | (tb << 4)) & 0x07070707u;
+  const uint32_t pa = __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, ka) * __builtin_bit_cast(u16x2, f2));
+  const uint32_t pb = __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, kb) * __builtin_bit_cast(u16x2, f2));
+  const int b2 = (int)((l2 >> Q) & 1u);
+  const int ea = e35 - b2 - (int)((l3 >> (2 * Q)) & 1u), eb = e35 - b2 - (int)((l3 >> (2 * Q + 1)) & 1u);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    key[i] = __float_as_uint(ldexpf((float)((pa >> (8 * i)) & 0xFFu), ea));
+    key[4 + i] = __float_as_uint(ldexpf((float)((pb >> (8 * i)) & 0xFFu), eb));
+  }
+}
+
 template <int FMT>
 __device__ __forceinline__ void thread_keys(const ThreadWords& t, uint32_t key[32]) {
-  word_keys<FMT>(t.cw.x, t.sc, t.jpos, key);
-  word_keys<FMT>(t.cw.y, t.sc, t.jpos + 8, key + 8);
-  word_keys<FMT>(t.cw.z, t.sc, t.jpos + 16, key + 16);
-  word_keys<FMT>(t.cw.w, t.sc, t.jpos + 24, key + 24);
+  if constexpr (FMT == 1) {
+    const uint32_t f2 = (4u + (t.sc & 3u)) * 0x00010001u;
+    const int e35 = (int)((t.sc >> 2) & 63u) - 35;
+    const uint32_t l2 = t.sc >> (8 + t.jpos / 8), l3 = t.sc >> (16 + t.jpos / 4);
+    hif4_word_keys<0>(t.cw.x, f2, e35, l2, l3, key);
+    hif4_word_keys<1>(t.cw.y, f2, e35, l2, l3, key + 8);
+    hif4_word_keys<2>(t.cw.z, f2, e35, l2, l3, key + 16);
+    hif4_word_keys<3>(t.cw.w, f2, e35, l2, l3, key + 24);
+  } else {
+    mx_word_keys(t.cw.x, t.sc, key);
+    mx_word_keys(t.cw.y, t.sc, key + 8);
+    mx_word_keys(t.cw.z, t.sc, key + 16);
+    mx_word_keys(t.cw.w, t.sc, key + 24);
+  }
 }
 
 // Resolve the threshold from the global histogram (all threads call this; wave 0 reads the
