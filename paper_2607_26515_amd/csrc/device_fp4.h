@@ -168,6 +168,17 @@ __device__ __forceinline__ float hif4_value(uint32_t code, int c1, int b) {
   return (code & 8) ? -v : v;
 }
 
+// The grid step of level-1 code c1 and shift b, (4+m) 2^(e-35-b) (exact and normal: at least
+// 4 * 2^-37), and the element value k * step carrying the sign of x, which is the code's sign
+// (k = 0 included: a signed zero); k * step <= 7 * 7 * 2^28 is exact.  The quantizers use this
+// form: one conversion, one multiply and one sign insertion per element.
+__device__ __forceinline__ float hif4_step(int c1, int b) {
+  return ldexpf((float)(4 + (c1 & 3)), (c1 >> 2) - 35 - b);
+}
+__device__ __forceinline__ float hif4_signed_value(uint32_t k, float step, float x) {
+  return copysignf((float)k * step, x);
+}
+
 // Compress the even bits of a 16-bit value into 8 bits.
 __device__ __forceinline__ uint32_t even_bits16(uint32_t x) {
   x &= 0x5555u;

@@ -217,11 +217,12 @@ __device__ __forceinline__ void quantize8(const float x[8], uint32_t code[8], fl
       b[hh] = b2 + (a4 <= (b2 ? fit1 : fit0) ? 1 : 0);
     }
     const Hif4Mid mid = hif4_mid(c1);
+    const float step[2] = {hif4_step(c1, b[0]), hif4_step(c1, b[1])};
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const uint32_t k = hif4_k(x[i], c1, b[i / 4], mid);
       code[i] = ((__float_as_uint(x[i]) >> 28) & 8u) | k;
-      val[i] = hif4_value(code[i], c1, b[i / 4]);
+      val[i] = hif4_signed_value(k, step[i / 4], x[i]);
     }
   }
 }

@@ -54,11 +54,12 @@ __device__ __forceinline__ Quad quantize_quad(const float x[4]) {
     const uint32_t bits2 = even_bits16((uint32_t)(m2 >> base) & 0xFFFFu);
     q.scale = (uint32_t)q.c1 | (bits2 << 8) | (bits3 << 16);
     const Hif4Mid mid = hif4_mid(q.c1);
+    const float step = hif4_step(q.c1, q.b);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const uint32_t k = hif4_k(x[i], q.c1, q.b, mid);
       q.code[i] = ((__float_as_uint(x[i]) >> 28) & 8u) | k;
-      q.val[i] = hif4_value(q.code[i], q.c1, q.b);
+      q.val[i] = hif4_signed_value(k, step, x[i]);
     }
   }
   return q;
