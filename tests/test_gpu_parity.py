@@ -185,11 +185,14 @@ def test_linear_fwd_is_deterministic(fmt):
 def test_linear_bwd(fmt, m, d, n):
     import paper_2607_26515_amd as P
     b = F.block_size(fmt)
-    if m % b or n % b:
-        pytest.skip("m and n must be multiples of the block size")
     log(f"linear_bwd {fmt} m={m} d={d} n={n}")
     rx, rw, rg = rng_tree(m + n + d, 3)
     xb, wb, gb = activations(rx, m, d, 0.01, 50.0), weights(rw, n, d), grad_output(rg, m, n)
+    if m % b or n % b:
+        # both GEMMs contract over a blocked axis (n for dX, m for dW): refused before any launch
+        with pytest.raises(P.ResqError, match="needs"):
+            P.linear_bwd(dev_bf16(gb), dev_bf16(xb), dev_bf16(wb), fmt)
+        return
     dx, dw = P.linear_bwd(dev_bf16(gb), dev_bf16(xb), dev_bf16(wb), fmt)
     o = Q.resq_backward(fmt, bf16_bits_to_f32(gb), bf16_bits_to_f32(xb), bf16_bits_to_f32(wb))
     assert_close(host(dx), o["dx64"], "dX")
