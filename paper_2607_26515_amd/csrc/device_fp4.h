@@ -192,14 +192,25 @@ __device__ __forceinline__ uint32_t even_bits16(uint32_t x) {
 // MFMA operand encodings for HiF4 (f8f6f4 MFMA, formats: 2 = FP6 E2M3, 3 = BF6 E3M2)
 // ------------------------------------------------------------------------------------------
 // Activation side: V = k (4+m) 2^(2-b) <= 196 (value = V 2^(e-37)) is split V = 16 hi + lo;
-// hi, lo <= 15 are E2M3 codes of hi/8, lo/8 (E2M3 code t has value t/8 for t <= 15).
-// Scales: hi term 2^(e-30) -> E8M0 e + 97, lo term 2^(e-34) -> E8M0 e + 93.
-__device__ __forceinline__ void hif4_split_e2m3(uint32_t code, int c1, int b, uint32_t& hi,
-                                                uint32_t& lo) {
-  const uint32_t V = ((code & 7) * (4 + (c1 & 3))) << (2 - b);
-  const uint32_t s = (code & 8) << 2;  // sign -> bit 5
-  hi = s | (V >> 4);
-  lo = s | (V & 15);
+// hi, lo <= 15 are E2M3 codes of hi/8, lo/8 (E2M3 code t has value t/8 for t <= 15), each
+// with the element's sign in bit 5.  Scales: hi term 2^(e-30) -> E8M0 e + 97, lo term
+// 2^(e-34) -> E8M0 e + 93.
+// hif4_split4 splits the four elements of one level-3 group (shift b) at once: their codes in
+// the low nibbles of the bytes of nb (high nibbles ignored), q2 = 4+m in both 16-bit lanes.
+// One 16-bit-lane multiply forms the four products k (4+m) <= 49 (no carry crosses a byte)
+// and one shift applies 2 - b (V <= 196 stays in its byte); the four 6-bit hi and lo fields
+// then close up into 24 bits each, field j at bit 6j.
+__device__ __forceinline__ uint32_t close_up6x4(uint32_t x) {  // bytes f0..f3 (< 64) -> 24 bits
+  const uint32_t t = (x & 0x003F003Fu) | ((x >> 2) & 0x0FC00FC0u);
+  return (t & 0xFFFu) | ((t >> 4) & 0xFFF000u);
+}
+__device__ __forceinline__ void hif4_split4(uint32_t nb, uint32_t q2, uint32_t b, uint32_t& hi24, uint32_t& lo24) {
+  typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+  const uint32_t k = nb & 0x07070707u, sg = (nb & 0x08080808u) << 2;
+  const uint32_t kq = __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, k) * __builtin_bit_cast(u16x2, q2));
+  const uint32_t V = kq << (2u - b);
+  hi24 = close_up6x4(sg | ((V >> 4) & 0x0F0F0F0Fu));
+  lo24 = close_up6x4(sg | (V & 0x0F0F0F0Fu));
 }
 
 // Weight side: k 2^-b as a BF6 E3M2 code (value exact), sign in bit 5; the remaining

@@ -16,6 +16,31 @@ __device__ __forceinline__ void put6(uint32_t* out, int i, uint32_t f) {
   if ((bit & 31) > 26) out[(bit >> 5) + 1] |= f >> (32 - (bit & 31));
 }
 
+// The HiF4 activation split (hif4_split4) of a 32-element lane record: field i of the record
+// at bit 6i of hi (a) and lo (b).
+__device__ __forceinline__ void hif4_split_record(const uint32_t words[4], uint32_t scale, int half,
+                                                  uint32_t a[6], uint32_t b[6]) {
+  const uint32_t q2 = (4u + (scale & 3u)) * 0x00010001u;
+  const uint32_t l2 = scale >> (8 + 4 * half), l3 = scale >> (16 + 8 * half);
+  uint32_t ch[8], cl[8];
+#pragma unroll
+  for (int g = 0; g < 8; ++g) {
+    const uint32_t w = words[g >> 1];
+    const uint32_t t = __builtin_amdgcn_perm(w, w, (g & 1) ? 0x0C030C02u : 0x0C010C00u);
+    // nibble 4(g&1)+j of w in the low nibble of byte j (the high nibbles are ignored)
+    hif4_split4(t | (t << 4), q2, ((l2 >> (g >> 1)) & 1u) + ((l3 >> g) & 1u), ch[g], cl[g]);
+  }
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    a[3 * h] = ch[4 * h] | (ch[4 * h + 1] << 24);
+    a[3 * h + 1] = (ch[4 * h + 1] >> 8) | (ch[4 * h + 2] << 16);
+    a[3 * h + 2] = (ch[4 * h + 2] >> 16) | (ch[4 * h + 3] << 8);
+    b[3 * h] = cl[4 * h] | (cl[4 * h + 1] << 24);
+    b[3 * h + 1] = (cl[4 * h + 1] >> 8) | (cl[4 * h + 2] << 16);
+    b[3 * h + 2] = (cl[4 * h + 2] >> 16) | (cl[4 * h + 3] << 8);
+  }
+}
+
 // Nibble mask keeping the elements whose bit is set in `keep` (bit e = element e of a word).
 __device__ __forceinline__ uint32_t nibble_mask8(uint32_t keep) {
   uint32_t m = 0;
@@ -35,17 +60,14 @@ __device__ __forceinline__ void store_frag_record(uint8_t* __restrict__ frag, ui
     const uint32_t c1 = scale & 0xFFu;
     const uint32_t words[4] = {cw.x, cw.y, cw.z, cw.w};
     uint32_t a[6] = {0, 0, 0, 0, 0, 0}, b[6] = {0, 0, 0, 0, 0, 0};
+    if constexpr (MODE == kPackHiA) {
+      hif4_split_record(words, scale, half, a, b);
+    } else {
 #pragma unroll
-    for (int i = 0; i < 32; ++i) {
-      const uint32_t code = (words[i >> 3] >> (4 * (i & 7))) & 15u;
-      const int h = half * 8 + (i >> 2);
-      const int sh = (int)((scale >> (8 + (h >> 1))) & 1u) + (int)((scale >> (16 + h)) & 1u);
-      if constexpr (MODE == kPackHiA) {
-        uint32_t hi, lo;
-        hif4_split_e2m3(code, (int)c1, sh, hi, lo);
-        put6(a, i, hi);
-        put6(b, i, lo);
-      } else {
+      for (int i = 0; i < 32; ++i) {
+        const uint32_t code = (words[i >> 3] >> (4 * (i & 7))) & 15u;
+        const int h = half * 8 + (i >> 2);
+        const int sh = (int)((scale >> (8 + (h >> 1))) & 1u) + (int)((scale >> (16 + h)) & 1u);
         put6(a, i, hif4_e3m2(code, sh));
       }
     }

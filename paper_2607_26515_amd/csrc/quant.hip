@@ -242,16 +242,11 @@ __device__ __forceinline__ void store_record8(uint8_t* __restrict__ frag, uint8_
     // 48-bit run is built as two 24-bit runs of 4 fields (one level-3 shift each) in 32-bit
     // words.
     uint32_t rh[2], rl[2];
+    const uint32_t q2 = (4u + ((uint32_t)c1 & 3u)) * 0x00010001u;
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
-      rh[hh] = rl[hh] = 0u;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        uint32_t hi, lo;
-        hif4_split_e2m3(code[4 * hh + e], c1, b[hh], hi, lo);
-        rh[hh] |= hi << (6 * e);
-        rl[hh] |= lo << (6 * e);
-      }
+      const uint32_t nb = code[4 * hh] | (code[4 * hh + 1] << 8) | (code[4 * hh + 2] << 16) | (code[4 * hh + 3] << 24);
+      hif4_split4(nb, q2, (uint32_t)b[hh], rh[hh], rl[hh]);
     }
     const uint64_t h = rh[0] | ((uint64_t)rh[1] << 24), l = rl[0] | ((uint64_t)rl[1] << 24);
     // thread s writes record dwords 3s .. 3s+2: hi of slices 0,1 / hi of 2,3 / lo of 0,1 /
