@@ -214,13 +214,22 @@ __device__ __forceinline__ void hif4_split4(uint32_t nb, uint32_t q2, uint32_t b
 }
 
 // Weight side: k 2^-b as a BF6 E3M2 code (value exact), sign in bit 5; the remaining
-// factor (4+m) 2^(e-35) is the E8M0 scale e + 92 times the per-column factor (4+m).
-__device__ __forceinline__ uint32_t hif4_e3m2(uint32_t code, int b) {
-  const uint32_t k = code & 7;
-  // E3M2 (bias 3) of k: 0, 1.0 (e3,m0), 2.0 (e4), 3.0 (e4,m2), 4.0 (e5), 5, 6, 7
-  const uint32_t lut = (k == 0) ? 0u : (k == 1) ? 12u : (k == 2) ? 16u : (k == 3) ? 18u : 16u + k;
-  const uint32_t mag = k ? lut - ((uint32_t)b << 2) : 0u;
-  return ((code & 8) << 2) | mag;
+// factor (4+m) 2^(e-35) is the E8M0 scale e + 92 times the per-column factor (4+m).  The
+// E3M2 code (bias 3) of k = 0..7 is 0, 12 (1.0), 16 (2.0), 18 (3.0), 20, 21, 22, 23, and the
+// shift b lowers the exponent field of a nonzero one by b.
+// hif4_e3m2x4 encodes the four elements of one level-3 group (shift b) at once, their codes
+// in the low nibbles of the bytes of nb (high nibbles ignored): the codes of k come from a
+// byte table by v_perm, nonzero ones lowered by b << 2 (at least 12 - 8, so no borrow crosses
+// a byte), the sign goes to bit 5, and the four 6-bit fields close up into 24 bits, field j
+// at bit 6j.
+__device__ __forceinline__ uint32_t hif4_e3m2x4(uint32_t nb, uint32_t b) {
+  typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+  const uint32_t k = nb & 0x07070707u;
+  const uint32_t e = __builtin_amdgcn_perm(0x17161514u, 0x12100C00u, k);  // 0 12 16 18 20 21 22 23
+  const uint32_t nz = ((k + 0x7F7F7F7Fu) & 0x80808080u) >> 7;              // 1 in each nonzero byte
+  const uint32_t sub = __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, nz) *
+                                                        __builtin_bit_cast(u16x2, (4u * b) * 0x00010001u));
+  return close_up6x4(((nb & 0x08080808u) << 2) | (e - sub));
 }
 
 }  // namespace resq

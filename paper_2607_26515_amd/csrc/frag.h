@@ -9,13 +9,6 @@
 
 namespace resq {
 
-// OR a 6-bit field into bit position 6i of a little-endian bit string.
-__device__ __forceinline__ void put6(uint32_t* out, int i, uint32_t f) {
-  const int bit = 6 * i;
-  out[bit >> 5] |= f << (bit & 31);
-  if ((bit & 31) > 26) out[(bit >> 5) + 1] |= f >> (32 - (bit & 31));
-}
-
 // The HiF4 activation split (hif4_split4) of a 32-element lane record: field i of the record
 // at bit 6i of hi (a) and lo (b).
 __device__ __forceinline__ void hif4_split_record(const uint32_t words[4], uint32_t scale, int half,
@@ -63,13 +56,20 @@ __device__ __forceinline__ void store_frag_record(uint8_t* __restrict__ frag, ui
     if constexpr (MODE == kPackHiA) {
       hif4_split_record(words, scale, half, a, b);
     } else {
+      const uint32_t l2 = scale >> (8 + 4 * half), l3 = scale >> (16 + 8 * half);
+      uint32_t c[8];
 #pragma unroll
-      for (int i = 0; i < 32; ++i) {
-        const uint32_t code = (words[i >> 3] >> (4 * (i & 7))) & 15u;
-        const int h = half * 8 + (i >> 2);
-        const int sh = (int)((scale >> (8 + (h >> 1))) & 1u) + (int)((scale >> (16 + h)) & 1u);
-        put6(a, i, hif4_e3m2(code, sh));
+      for (int g = 0; g < 8; ++g) {
+        const uint32_t w = words[g >> 1];
+        const uint32_t t = __builtin_amdgcn_perm(w, w, (g & 1) ? 0x0C030C02u : 0x0C010C00u);
+        c[g] = hif4_e3m2x4(t | (t << 4), ((l2 >> (g >> 1)) & 1u) + ((l3 >> g) & 1u));
       }
+      a[0] = c[0] | (c[1] << 24);
+      a[1] = (c[1] >> 8) | (c[2] << 16);
+      a[2] = (c[2] >> 16) | (c[3] << 8);
+      a[3] = c[4] | (c[5] << 24);
+      a[4] = (c[5] >> 8) | (c[6] << 16);
+      a[5] = (c[6] >> 16) | (c[7] << 8);
     }
     if constexpr (MODE == kPackHiA) {
       uint4* p = reinterpret_cast<uint4*>(frag + gid * 48);

@@ -695,9 +695,11 @@ __global__ __launch_bounds__(256) void residual_frag_kernel(
 __device__ __forceinline__ void store_record8_e3m2(uint8_t* __restrict__ frag, uint8_t* __restrict__ fsc,
                                                    int64_t rec, int s, const uint32_t code[8],
                                                    uint32_t scale_byte, const int b[2]) {
-  uint32_t r[2] = {0u, 0u};  // two 24-bit runs of 4 fields
+  uint32_t r[2];  // two 24-bit runs of 4 fields
 #pragma unroll
-  for (int i = 0; i < 8; ++i) r[i / 4] |= hif4_e3m2(code[i], b[i / 4]) << (6 * (i % 4));
+  for (int hh = 0; hh < 2; ++hh)
+    r[hh] = hif4_e3m2x4(code[4 * hh] | (code[4 * hh + 1] << 8) | (code[4 * hh + 2] << 16) | (code[4 * hh + 3] << 24),
+                        (uint32_t)b[hh]);
   const uint64_t h = r[0] | ((uint64_t)r[1] << 24);
   const uint32_t plo = __shfl_xor((uint32_t)h, 1, 64), phi = __shfl_xor((uint32_t)(h >> 32), 1, 64);
   if ((s & 1) == 0) {
